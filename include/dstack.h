@@ -1,0 +1,293 @@
+/*
+ * dstack.h -- C ABI of an MI355X-native implementation of the D-STACK hot
+ * path (Dhakal, Kulkarni, Ramakrishnan, "D-STACK: High Throughput DNN
+ * Inference by Effective Multiplexing and Spatio-Temporal Scheduling of
+ * GPUs", arxiv 2304.13541).
+ *
+ * The paper's problem (Sec. 1, Sec. 5, Sec. 6): give each DNN only the GPU
+ * share beyond which its latency stops improving (its "Knee"), choose the
+ * batch that maximises efficacy under its SLO, and run several models at
+ * once without over-subscribing the GPU.  Here a GPU share is a CU-masked
+ * HIP stream ("partition") whose CUs are counted in slots: slot j is the
+ * j-th CU of every one of the 8 XCDs, so a partition of s slots owns 8*s of
+ * the 256 CUs, spread evenly over the XCDs.
+ *
+ * Conventions
+ *  - Every call returns dstack_status; results go through out-parameters.
+ *    No C++ exception crosses this boundary.
+ *  - DSTACK_E_INVALID: a NULL pointer, a fraction <= 0, > 1 or NaN, a batch
+ *    < 1 or above the model's maximum, a slot range outside 0..32, a size
+ *    that does not match.  DSTACK_E_UNSUPPORTED: unknown architecture or a
+ *    shape a kernel does not handle.  DSTACK_E_HIP: a HIP runtime error
+ *    (its text is in dstack_last_error()).  DSTACK_E_STATE: a second
+ *    concurrent call on the same (model, partition) pair.
+ *  - Handles are created and destroyed by the caller.  The library owns
+ *    weights, workspaces and the masked streams.  Device pointers passed in
+ *    (inputs, outputs) stay owned by the caller.
+ *  - dstack_last_error() is thread-local text for the last non-OK status.
+ */
+#ifndef DSTACK_H
+#define DSTACK_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  DSTACK_OK = 0,
+  DSTACK_E_INVALID = -1,
+  DSTACK_E_UNSUPPORTED = -2,
+  DSTACK_E_HIP = -3,
+  DSTACK_E_OOM = -4,
+  DSTACK_E_INFEASIBLE = -5,
+  DSTACK_E_STATE = -6
+} dstack_status;
+
+#define DSTACK_TOTAL_SLOTS 32
+#define DSTACK_CUS_PER_SLOT 8
+#define DSTACK_MAX_SWEEP 32
+#define DSTACK_MAX_BATCHES 8
+#define DSTACK_MAX_MODELS 16
+#define DSTACK_MAX_JOBS 512
+
+typedef struct dstack_partition_s* dstack_partition;
+typedef struct dstack_model_s* dstack_model;
+
+/* Text of the last non-OK status on the calling thread ("" if none). */
+const char* dstack_last_error(void);
+
+/* ------------------------------------------------------------------ */
+/* Partitions (CU-masked streams)                                      */
+/* ------------------------------------------------------------------ */
+/* The paper confines each model to a share of the SMs with MPS
+ * (Sec. 3, Sec. 3.2); here the share is a CU mask on a HIP stream.
+ *
+ * dstack_fraction_to_slots: slots = clamp(floor(32*f + 1/2), 1, 32).
+ *   Host only.  E_INVALID for f <= 0, f > 1 or NaN.
+ * dstack_partition_create: a partition of that many slots starting at slot 0.
+ * dstack_partition_create_at: slots [slot_offset, slot_offset + n_slots).
+ * dstack_partition_create_mask: any non-empty set of slots (bit j = slot j),
+ *   as produced by dstack_schedule's per-job slot masks.
+ * The partition owns one new HIP stream (default priority) whose CU mask
+ * has bits 8j..8j+7 set for every slot j (mask bit i selects CU i/8 of XCD
+ * i%8).  Several partitions may overlap; keeping concurrent ones disjoint
+ * is the scheduler's job.
+ * dstack_partition_query: n_cu, the 8 CU-mask words and the hipStream_t (as
+ *   void*, usable with torch.cuda.ExternalStream).  Any out pointer may be
+ *   NULL. */
+dstack_status dstack_fraction_to_slots(double cu_fraction, int* slots);
+dstack_status dstack_partition_create(double cu_fraction, dstack_partition* out);
+dstack_status dstack_partition_create_at(int slot_offset, int n_slots, dstack_partition* out);
+dstack_status dstack_partition_create_mask(uint32_t slot_mask, dstack_partition* out);
+dstack_status dstack_partition_query(dstack_partition p, int* n_cu, uint32_t mask_words[8], void** hip_stream);
+dstack_status dstack_synchronize(dstack_partition p);
+void dstack_partition_destroy(dstack_partition p);
+
+/* Probe (verification of the slot -> CU mapping): launches n_blocks
+ * one-wave workgroups on the partition's stream; each records its hardware
+ * XCC id and HW_ID register into host_out[2*i], host_out[2*i+1].  Blocks
+ * until done.  n_blocks in 1..65536; host_out holds 2*n_blocks words. */
+dstack_status dstack_probe_cu_ids(dstack_partition p, int n_blocks, uint32_t* host_out);
+
+/* ------------------------------------------------------------------ */
+/* Models                                                              */
+/* ------------------------------------------------------------------ */
+/* arch: "tinycnn", "resnet50", "mobilenetv2", "vgg19", "lstm2".
+ * Weights are drawn from `seed` (Sec. 3.1 uses trained models; here
+ * random-weight models of the same architecture):
+ *   tensor t uses the splitmix64 stream whose state starts at
+ *   seed ^ (0x9E3779B97F4A7C15 * (t + 1)); u = (next >> 11) * 2^-53, with
+ *   u = 0 replaced by 1; conv/FC weights are He-normal (std sqrt(2/fan_in),
+ *   Box-Muller pairs in order, 2*pi as its fp64 value); LSTM tensors are
+ *   (2u - 1)/32; conv/FC biases are 0; every value is rounded to bf16 RNE
+ *   from fp64.  Tensor order is layer order, weight before bias
+ *   (ResNet block: conv1, conv2, conv3, downsample).  Logical layouts:
+ *   conv [K][R][S][C], depthwise [C][3][3], FC [out][in], LSTM [4H][in]
+ *   with gate order i, f, g, o.  BN layers have gamma 1, beta 0, mean 0,
+ *   var 1, eps 1e-5 (folded into per-channel fp32 scale/shift). */
+typedef struct {
+  char arch[16];
+  int is_lstm;              /* 0: image classifier, 1: sequence model */
+  int max_batch;            /* largest batch dstack_infer accepts */
+  int in_h, in_w, in_c;     /* CNN: per-item input [H][W][C] bf16 NHWC */
+  int seq_len, in_features; /* LSTM: input [T][batch][in_features] bf16 */
+  int out_features;         /* CNN: classes (fp32 logits); LSTM: hidden (fp32 h) */
+  int num_tensors;
+  int64_t num_params;
+  int num_kernels;          /* kernel launches per forward */
+  double flops_per_item;    /* algorithmic FLOPs (2 per MAC) per inference */
+  double mfma_flops_per_item; /* of which in MFMA convolution/GEMM kernels */
+  double weight_bytes;      /* bf16 weights read per forward */
+} dstack_model_info;
+
+dstack_status dstack_model_load(const char* arch, uint64_t seed, dstack_model* out);
+dstack_status dstack_model_query(dstack_model m, dstack_model_info* out);
+/* Copy tensor `tensor_index` (bf16 bits, logical layout) to host memory;
+ * `bytes` must equal 2 * numel. */
+dstack_status dstack_model_export_params(dstack_model m, int tensor_index, void* host_dst, size_t bytes);
+void dstack_model_destroy(dstack_model m);
+
+/* Host-only generation of one tensor of an architecture (same bits as
+ * dstack_model_load), without a device.  With host_dst == NULL only
+ * *numel is filled. */
+dstack_status dstack_generate_params(const char* arch, uint64_t seed, int tensor_index, void* host_dst,
+                                     size_t bytes, int64_t* numel);
+
+/* ------------------------------------------------------------------ */
+/* Inference                                                           */
+/* ------------------------------------------------------------------ */
+/* Batched forward pass, asynchronous on the partition's stream.
+ *   CNN:  d_in = [batch][H][W][3] bf16 NHWC, d_out = [batch][classes] fp32.
+ *   LSTM: d_in = [50][batch][512] bf16,       d_out = [50][batch][1024] fp32
+ *         (the second layer's h for every step).
+ * Activations between layers are bf16 (fp32 accumulation; LSTM cell state
+ * and h in fp32).  Workspace is per (model, partition) and is allocated on
+ * the first call for that pair. */
+dstack_status dstack_infer(dstack_model m, int batch, const void* d_in, void* d_out, dstack_partition p);
+
+/* Per-kernel timing of one forward: fills up to max_layers entries with
+ * the elapsed device time (ms, HIP events around each kernel on the
+ * partition's stream), the kernel class (0 MFMA conv/GEMM, 1 depthwise,
+ * 2 FC, 3 LSTM step, 4 pool/glue) and its algorithmic FLOPs and bytes.
+ * Synchronises the partition. */
+typedef struct {
+  int kind;
+  float ms;
+  double flops;
+  double bytes;
+} dstack_layer_time;
+dstack_status dstack_profile_layers(dstack_model m, int batch, const void* d_in, void* d_out, dstack_partition p,
+                                    dstack_layer_time* out, int max_layers, int* n_layers);
+
+/* ------------------------------------------------------------------ */
+/* Knee sweep (Sec. 3.1 measurement; Sec. 4.3 Eq. first_order_derivative;  */
+/* Sec. 5 Eq. efficiencySquareLatency)                                 */
+/* ------------------------------------------------------------------ */
+/* For each fraction: a partition of dstack_fraction_to_slots(f) slots,
+ * `warmup` untimed forwards, then `reps` forwards each timed with HIP
+ * events; latency = median, rounded half-up to whole microseconds.
+ * Efficacy eta = batch / (L^2 * slots); knee = argmax eta (exact integer
+ * comparison, ties to fewer slots); deployed = min(32, knee + 2 slots),
+ * the paper's 5-10% over-provisioning.  reps >= 1, n in 1..32. */
+typedef struct {
+  int n;
+  int batch;
+  int slots[DSTACK_MAX_SWEEP];
+  int n_cu[DSTACK_MAX_SWEEP];
+  int64_t latency_us[DSTACK_MAX_SWEEP];  /* median, whole us */
+  double latency_us_exact[DSTACK_MAX_SWEEP];
+  double p99_us[DSTACK_MAX_SWEEP];
+  int knee_index;
+  int knee_slots;
+  int deployed_slots;
+} dstack_knee_result;
+
+dstack_status dstack_knee_sweep(dstack_model m, int batch, const double* fractions, int n, int warmup, int reps,
+                                dstack_knee_result* out);
+
+/* ------------------------------------------------------------------ */
+/* Scheduling (pure host, deterministic, integer microseconds)          */
+/* ------------------------------------------------------------------ */
+/* Per model (Sec. 5.1, Eqs. max_batch_size, meet_slo, meet_half_slo):
+ * choose (b, s) on the measured grid maximising eta = b/(L^2 s) subject to
+ * b <= max_batch, L + C(b) <= SLO, L <= floor(SLO/2), where C(b) =
+ * ceil(b*1e6/rate) if rate > 0 else 482*b us; ties: higher eta, fewer
+ * slots, larger b.  None feasible: b = 1 (else the smallest batch), its
+ * lowest-latency s (ties fewer), feasible = 0.  Deployed slots =
+ * min(total, s + overprov).
+ * Session plan (Sec. 6.1, 6.1.1): model i has jobs k = 0..ceil(T/SLO)-1 in
+ * windows [k*SLO, min((k+1)*SLO, T)); EDF order (deadline, SLO, model, k);
+ * even k earliest feasible start, odd k latest; candidate starts are the
+ * window ends and every placed job's end and start - L; a start is
+ * feasible if the slots of all overlapping jobs plus its own never exceed
+ * the total; otherwise retry at the knee, then each smaller swept slot
+ * count ("below the knee"); otherwise missed = 1 (slots 0, duration 0,
+ * start = release).  Latency at an unswept slot count = that of the
+ * largest swept count below it.  Slot ids: jobs in (start, placement
+ * order) take the lowest free ids.  utilisation_ppm =
+ * floor(1e6 * sum(s*L) / (total*T)).
+ * Returns DSTACK_E_INFEASIBLE (with the full best-effort plan filled) if
+ * any model had no feasible (b, s) or any job was missed. */
+typedef struct {
+  int64_t slo_us;
+  int max_batch;
+  int rate_per_s;                       /* 0: no rate, C(b) = 482*b */
+  int n_batches;                        /* rows of the timing table */
+  int batches[DSTACK_MAX_BATCHES];
+  int n_slots;                          /* columns (ascending slot counts) */
+  int slots[DSTACK_MAX_SWEEP];
+  int64_t latency_us[DSTACK_MAX_BATCHES][DSTACK_MAX_SWEEP]; /* <= 0: not measured */
+} dstack_sched_model;
+
+typedef struct {
+  int64_t period_us;
+  int total_slots;      /* 1..64; 32 = the whole MI355X */
+  int overprov_slots;   /* 2 by default */
+} dstack_sched_params;
+
+typedef struct {
+  int model, k;
+  int64_t release_us, deadline_us, start_us, duration_us;
+  int slots;
+  int missed;
+  uint64_t slot_mask;
+} dstack_job;
+
+typedef struct {
+  int n_models;
+  int batch[DSTACK_MAX_MODELS];
+  int knee_slots[DSTACK_MAX_MODELS];
+  int deployed_slots[DSTACK_MAX_MODELS];
+  int64_t latency_us[DSTACK_MAX_MODELS];
+  int feasible[DSTACK_MAX_MODELS];
+  int n_jobs;                           /* in placement (EDF) order */
+  dstack_job jobs[DSTACK_MAX_JOBS];
+  int64_t utilisation_ppm;
+} dstack_schedule_out;
+
+dstack_status dstack_schedule(const dstack_sched_model* models, int n_models, const dstack_sched_params* params,
+                              dstack_schedule_out* out);
+
+/* ------------------------------------------------------------------ */
+/* Kernel-level entry points (the layers of Sec. 4.1's A.int table)     */
+/* ------------------------------------------------------------------ */
+/* All pointers are device pointers; `stream` is a hipStream_t (NULL = the
+ * null stream).  Asynchronous.  Layouts are NHWC / KRSC bf16 with fp32
+ * per-channel scale and shift; act: 0 none, 1 ReLU, 2 ReLU6.
+ *
+ * conv2d: y = act(scale[k] * sum_{r,s,c} x[n, ho*st-pad+r, wo*st-pad+s, c]
+ *   * w[k,r,s,c] + shift[k] (+ res[n,ho,wo,k])), zero outside the image;
+ *   C % 8 == 0 and K % 4 == 0 (else E_UNSUPPORTED); res may be NULL;
+ *   out_fp32 selects an fp32 instead of bf16 output.
+ * dwconv3x3: per-channel 3x3, pad 1, stride 1 or 2, w [3][3][C] (device
+ *   layout), then scale/shift and act; C % 8 == 0.
+ * fc: y[b][o] = act(sum_i x[b][i] * w[o][i] + bias[o]); batch 1..32,
+ *   I % 8 == 0; out_fp32 selects fp32 output.
+ * maxpool: k x k window, stride, pad (padding never wins); C % 8 == 0.
+ * avgpool: global mean over H x W, fp32 accumulate, bf16 out; C % 8 == 0.
+ * lstm_layer: one LSTM layer over T steps (gate order i, f, g, o; h0 = c0
+ *   = 0); x [T][B][I] bf16; w_ih [4H][I], w_hh [4H][H] bf16; bias [4H]
+ *   fp32 (= b_ih + b_hh); h_bf16 [T][B][H] receives h rounded to bf16;
+ *   h_f32 [T][B][H] (may be NULL) receives h in fp32; B in 1..32,
+ *   H % 16 == 0, I % 8 == 0; workspace needs lstm_workspace_bytes. */
+dstack_status dstack_op_conv2d(const void* x, int N, int H, int W, int C, const void* w, int K, int R, int S,
+                               int stride, int pad, const float* scale, const float* shift, const void* res, int act,
+                               void* y, int out_fp32, void* stream);
+dstack_status dstack_op_dwconv3x3(const void* x, int N, int H, int W, int C, const void* w, int stride,
+                                  const float* scale, const float* shift, int act, void* y, void* stream);
+dstack_status dstack_op_fc(const void* x, int B, int I, const void* w, const float* bias, int O, int act, void* y,
+                           int out_fp32, void* stream);
+dstack_status dstack_op_maxpool(const void* x, int N, int H, int W, int C, int k, int stride, int pad, void* y,
+                                void* stream);
+dstack_status dstack_op_avgpool(const void* x, int N, int H, int W, int C, void* y, void* stream);
+size_t dstack_lstm_workspace_bytes(int T, int B, int H);
+dstack_status dstack_op_lstm_layer(const void* x, int T, int B, int I, int H, const void* w_ih, const void* w_hh,
+                                   const float* bias, void* h_bf16, float* h_f32, void* workspace, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* DSTACK_H */

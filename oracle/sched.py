@@ -233,3 +233,16 @@ def temporal_utilisation(slos_and_shares):
     num = sum(slo * share for slo, share in slos_and_shares)
     den = sum(slo for slo, _ in slos_and_shares)
     return num / den
+
+
+def schedule(models, period, total=TOTAL_SLOTS, overprov=OVERPROVISION_SLOTS):
+    """Per-model optimisation followed by the session plan.
+
+    models: list of dicts {slo_us, max_batch, rate_per_s, table: {b: {s: L}}}.
+    Returns (choices, jobs, utilisation_ppm, feasible_all)."""
+    choices = [optimize(m["table"], m["slo_us"], m["max_batch"], m.get("rate_per_s", 0)) for m in models]
+    pms = [PlanModel(slo=m["slo_us"], knee=c.slots, slots=deployed_slots(c.slots, overprov, total),
+                     row=m["table"][c.batch], batch=c.batch) for m, c in zip(models, choices)]
+    jobs = plan(pms, period, total)
+    ok = all(c.feasible for c in choices) and not any(j.missed for j in jobs)
+    return choices, jobs, utilisation_ppm(jobs, period, total), ok

@@ -1,0 +1,337 @@
+"""Python binding of libdstack (argument marshalling only).
+
+Every computation runs in the HIP library behind the C ABI declared in
+``include/dstack.h``; this module only converts arguments, checks status
+codes and wraps PyTorch device tensors and streams.  It raises if the
+compiled library is missing: there is no fallback path.
+"""
+import ctypes
+import os
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libdstack.so")
+
+OK, E_INVALID, E_UNSUPPORTED, E_HIP, E_OOM, E_INFEASIBLE, E_STATE = 0, -1, -2, -3, -4, -5, -6
+TOTAL_SLOTS = 32
+CUS_PER_SLOT = 8
+MAX_SWEEP, MAX_BATCHES, MAX_MODELS, MAX_JOBS = 32, 8, 16, 512
+ARCHS = ("tinycnn", "resnet50", "mobilenetv2", "vgg19", "lstm2")
+KIND_NAMES = {0: "mfma", 1: "depthwise", 2: "fc", 3: "lstm_step", 4: "glue"}
+
+
+class DStackError(RuntimeError):
+    def __init__(self, status, msg):
+        super().__init__("dstack status %d: %s" % (status, msg))
+        self.status = status
+
+
+class ModelInfo(ctypes.Structure):
+    _fields_ = [("arch", ctypes.c_char * 16), ("is_lstm", ctypes.c_int), ("max_batch", ctypes.c_int),
+                ("in_h", ctypes.c_int), ("in_w", ctypes.c_int), ("in_c", ctypes.c_int),
+                ("seq_len", ctypes.c_int), ("in_features", ctypes.c_int), ("out_features", ctypes.c_int),
+                ("num_tensors", ctypes.c_int), ("num_params", ctypes.c_int64), ("num_kernels", ctypes.c_int),
+                ("flops_per_item", ctypes.c_double), ("mfma_flops_per_item", ctypes.c_double),
+                ("weight_bytes", ctypes.c_double)]
+
+
+class LayerTime(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int), ("ms", ctypes.c_float), ("flops", ctypes.c_double), ("bytes", ctypes.c_double)]
+
+
+class KneeResult(ctypes.Structure):
+    _fields_ = [("n", ctypes.c_int), ("batch", ctypes.c_int), ("slots", ctypes.c_int * MAX_SWEEP),
+                ("n_cu", ctypes.c_int * MAX_SWEEP), ("latency_us", ctypes.c_int64 * MAX_SWEEP),
+                ("latency_us_exact", ctypes.c_double * MAX_SWEEP), ("p99_us", ctypes.c_double * MAX_SWEEP),
+                ("knee_index", ctypes.c_int), ("knee_slots", ctypes.c_int), ("deployed_slots", ctypes.c_int)]
+
+
+class SchedModel(ctypes.Structure):
+    _fields_ = [("slo_us", ctypes.c_int64), ("max_batch", ctypes.c_int), ("rate_per_s", ctypes.c_int),
+                ("n_batches", ctypes.c_int), ("batches", ctypes.c_int * MAX_BATCHES), ("n_slots", ctypes.c_int),
+                ("slots", ctypes.c_int * MAX_SWEEP), ("latency_us", (ctypes.c_int64 * MAX_SWEEP) * MAX_BATCHES)]
+
+
+class SchedParams(ctypes.Structure):
+    _fields_ = [("period_us", ctypes.c_int64), ("total_slots", ctypes.c_int), ("overprov_slots", ctypes.c_int)]
+
+
+class Job(ctypes.Structure):
+    _fields_ = [("model", ctypes.c_int), ("k", ctypes.c_int), ("release_us", ctypes.c_int64),
+                ("deadline_us", ctypes.c_int64), ("start_us", ctypes.c_int64), ("duration_us", ctypes.c_int64),
+                ("slots", ctypes.c_int), ("missed", ctypes.c_int), ("slot_mask", ctypes.c_uint64)]
+
+
+class ScheduleOut(ctypes.Structure):
+    _fields_ = [("n_models", ctypes.c_int), ("batch", ctypes.c_int * MAX_MODELS),
+                ("knee_slots", ctypes.c_int * MAX_MODELS), ("deployed_slots", ctypes.c_int * MAX_MODELS),
+                ("latency_us", ctypes.c_int64 * MAX_MODELS), ("feasible", ctypes.c_int * MAX_MODELS),
+                ("n_jobs", ctypes.c_int), ("jobs", Job * MAX_JOBS), ("utilisation_ppm", ctypes.c_int64)]
+
+
+_lib = None
+_vp, _i, _d, _u64, _sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_double, ctypes.c_uint64, ctypes.c_size_t
+_fp = ctypes.POINTER(ctypes.c_float)
+
+_SIGS = {
+    "dstack_last_error": ([], ctypes.c_char_p),
+    "dstack_fraction_to_slots": ([_d, ctypes.POINTER(_i)], _i),
+    "dstack_partition_create": ([_d, ctypes.POINTER(_vp)], _i),
+    "dstack_partition_create_at": ([_i, _i, ctypes.POINTER(_vp)], _i),
+    "dstack_partition_create_mask": ([ctypes.c_uint32, ctypes.POINTER(_vp)], _i),
+    "dstack_partition_query": ([_vp, ctypes.POINTER(_i), ctypes.POINTER(ctypes.c_uint32), ctypes.POINTER(_vp)], _i),
+    "dstack_synchronize": ([_vp], _i),
+    "dstack_partition_destroy": ([_vp], None),
+    "dstack_probe_cu_ids": ([_vp, _i, ctypes.POINTER(ctypes.c_uint32)], _i),
+    "dstack_model_load": ([ctypes.c_char_p, _u64, ctypes.POINTER(_vp)], _i),
+    "dstack_model_query": ([_vp, ctypes.POINTER(ModelInfo)], _i),
+    "dstack_model_export_params": ([_vp, _i, _vp, _sz], _i),
+    "dstack_model_destroy": ([_vp], None),
+    "dstack_generate_params": ([ctypes.c_char_p, _u64, _i, _vp, _sz, ctypes.POINTER(ctypes.c_int64)], _i),
+    "dstack_infer": ([_vp, _i, _vp, _vp, _vp], _i),
+    "dstack_profile_layers": ([_vp, _i, _vp, _vp, _vp, ctypes.POINTER(LayerTime), _i, ctypes.POINTER(_i)], _i),
+    "dstack_knee_sweep": ([_vp, _i, ctypes.POINTER(_d), _i, _i, _i, ctypes.POINTER(KneeResult)], _i),
+    "dstack_schedule": ([ctypes.POINTER(SchedModel), _i, ctypes.POINTER(SchedParams), ctypes.POINTER(ScheduleOut)], _i),
+    "dstack_op_conv2d": ([_vp, _i, _i, _i, _i, _vp, _i, _i, _i, _i, _i, _vp, _vp, _vp, _i, _vp, _i, _vp], _i),
+    "dstack_op_dwconv3x3": ([_vp, _i, _i, _i, _i, _vp, _i, _vp, _vp, _i, _vp, _vp], _i),
+    "dstack_op_fc": ([_vp, _i, _i, _vp, _vp, _i, _i, _vp, _i, _vp], _i),
+    "dstack_op_maxpool": ([_vp, _i, _i, _i, _i, _i, _i, _i, _vp, _vp], _i),
+    "dstack_op_avgpool": ([_vp, _i, _i, _i, _i, _vp, _vp], _i),
+    "dstack_lstm_workspace_bytes": ([_i, _i, _i], _sz),
+    "dstack_op_lstm_layer": ([_vp, _i, _i, _i, _i, _vp, _vp, _vp, _vp, _vp, _vp, _vp], _i),
+}
+
+
+def lib():
+    """Load libdstack.so (built in-tree by paper_2304_13541_amd/build.py)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError("libdstack.so is not built (run __graft_entry__.build()); there is no fallback path")
+        try:  # PyTorch bundles a HIP runtime with the same soname: load it first so one runtime serves both
+            import torch  # noqa: F401
+        except ImportError:
+            pass
+        L = ctypes.CDLL(LIB_PATH)
+        for name, (args, res) in _SIGS.items():
+            f = getattr(L, name)
+            f.argtypes = args
+            f.restype = res
+        _lib = L
+    return _lib
+
+
+def _check(st):
+    if st != OK:
+        raise DStackError(st, lib().dstack_last_error().decode())
+    return st
+
+
+def _ptr(t):
+    """Device pointer of a torch tensor (or None)."""
+    if t is None:
+        return None
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def fraction_to_slots(f):
+    s = ctypes.c_int()
+    _check(lib().dstack_fraction_to_slots(float(f), ctypes.byref(s)))
+    return s.value
+
+
+class Partition:
+    """A CU-masked HIP stream owning 8 CUs (one per XCD) per slot."""
+
+    def __init__(self, fraction=None, slot_offset=None, n_slots=None, slot_mask=None):
+        h = ctypes.c_void_p()
+        if slot_mask is not None:
+            _check(lib().dstack_partition_create_mask(ctypes.c_uint32(slot_mask), ctypes.byref(h)))
+        elif slot_offset is not None:
+            _check(lib().dstack_partition_create_at(slot_offset, n_slots, ctypes.byref(h)))
+        else:
+            _check(lib().dstack_partition_create(float(fraction), ctypes.byref(h)))
+        self.h = h
+        n = ctypes.c_int()
+        words = (ctypes.c_uint32 * 8)()
+        st = ctypes.c_void_p()
+        _check(lib().dstack_partition_query(h, ctypes.byref(n), words, ctypes.byref(st)))
+        self.n_cu = n.value
+        self.mask_words = list(words)
+        self.stream_ptr = st.value or 0
+
+    def torch_stream(self, device="cuda:0"):
+        import torch
+        return torch.cuda.ExternalStream(self.stream_ptr, device=device)
+
+    def synchronize(self):
+        _check(lib().dstack_synchronize(self.h))
+
+    def probe_cu_ids(self, n_blocks=4096):
+        out = (ctypes.c_uint32 * (2 * n_blocks))()
+        _check(lib().dstack_probe_cu_ids(self.h, n_blocks, out))
+        return np.frombuffer(out, dtype=np.uint32).reshape(n_blocks, 2).copy()
+
+    def destroy(self):
+        if self.h:
+            lib().dstack_partition_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.destroy()
+        except Exception:
+            pass
+
+
+class Model:
+    """A random-weight model of one architecture, weights resident in HBM."""
+
+    def __init__(self, arch, seed):
+        h = ctypes.c_void_p()
+        _check(lib().dstack_model_load(arch.encode(), ctypes.c_uint64(seed), ctypes.byref(h)))
+        self.h = h
+        self.arch = arch
+        self.seed = seed
+        info = ModelInfo()
+        _check(lib().dstack_model_query(h, ctypes.byref(info)))
+        self.info = info
+
+    def destroy(self):
+        if self.h:
+            lib().dstack_model_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.destroy()
+        except Exception:
+            pass
+
+    def input_shape(self, batch):
+        i = self.info
+        return (i.seq_len, batch, i.in_features) if i.is_lstm else (batch, i.in_h, i.in_w, i.in_c)
+
+    def output_shape(self, batch):
+        i = self.info
+        return (i.seq_len, batch, i.out_features) if i.is_lstm else (batch, i.out_features)
+
+    def export_params(self, idx):
+        n = ctypes.c_int64()
+        _check(lib().dstack_generate_params(self.arch.encode(), ctypes.c_uint64(self.seed), idx, None, 0,
+                                            ctypes.byref(n)))
+        out = np.empty(n.value, dtype=np.uint16)
+        _check(lib().dstack_model_export_params(self.h, idx, out.ctypes.data, out.nbytes))
+        return out
+
+    def infer(self, batch, x, y, partition):
+        """x: bf16 device tensor, y: fp32 device tensor; async on the partition's stream."""
+        _check(lib().dstack_infer(self.h, batch, _ptr(x), _ptr(y), partition.h))
+
+    def profile_layers(self, batch, x, y, partition, max_layers=512):
+        arr = (LayerTime * max_layers)()
+        n = ctypes.c_int()
+        _check(lib().dstack_profile_layers(self.h, batch, _ptr(x), _ptr(y), partition.h, arr, max_layers,
+                                           ctypes.byref(n)))
+        return [dict(kind=arr[i].kind, ms=arr[i].ms, flops=arr[i].flops, bytes=arr[i].bytes) for i in range(n.value)]
+
+    def knee_sweep(self, batch, fractions, warmup=5, reps=20):
+        fr = (ctypes.c_double * len(fractions))(*fractions)
+        r = KneeResult()
+        _check(lib().dstack_knee_sweep(self.h, batch, fr, len(fractions), warmup, reps, ctypes.byref(r)))
+        n = r.n
+        return dict(batch=r.batch, slots=list(r.slots[:n]), n_cu=list(r.n_cu[:n]),
+                    latency_us=list(r.latency_us[:n]), latency_us_exact=list(r.latency_us_exact[:n]),
+                    p99_us=list(r.p99_us[:n]), knee_index=r.knee_index, knee_slots=r.knee_slots,
+                    deployed_slots=r.deployed_slots)
+
+
+def generate_params(arch, seed, idx):
+    """Host-only generation of one weight tensor (bf16 bits, logical layout)."""
+    n = ctypes.c_int64()
+    _check(lib().dstack_generate_params(arch.encode(), ctypes.c_uint64(seed), idx, None, 0, ctypes.byref(n)))
+    out = np.empty(n.value, dtype=np.uint16)
+    _check(lib().dstack_generate_params(arch.encode(), ctypes.c_uint64(seed), idx, out.ctypes.data, out.nbytes,
+                                        ctypes.byref(n)))
+    return out
+
+
+def schedule(models, period_us, total_slots=TOTAL_SLOTS, overprov_slots=2):
+    """models: list of dicts {slo_us, max_batch, rate_per_s, table: {batch: {slots: latency_us}}}.
+    Returns (status, result dict); status is OK or E_INFEASIBLE (plan still filled)."""
+    arr = (SchedModel * len(models))()
+    for i, m in enumerate(models):
+        e = arr[i]
+        e.slo_us = m["slo_us"]
+        e.max_batch = m["max_batch"]
+        e.rate_per_s = m.get("rate_per_s", 0)
+        batches = sorted(m["table"])
+        slots = sorted({s for b in batches for s in m["table"][b]})
+        e.n_batches = len(batches)
+        e.n_slots = len(slots)
+        for q, b in enumerate(batches):
+            e.batches[q] = b
+            for r, s in enumerate(slots):
+                e.latency_us[q][r] = m["table"][b].get(s, 0)
+        for r, s in enumerate(slots):
+            e.slots[r] = s
+    prm = SchedParams(period_us, total_slots, overprov_slots)
+    out = ScheduleOut()
+    st = lib().dstack_schedule(arr, len(models), ctypes.byref(prm), ctypes.byref(out))
+    if st not in (OK, E_INFEASIBLE):
+        _check(st)
+    n = out.n_models
+    jobs = [dict(model=j.model, k=j.k, release=j.release_us, deadline=j.deadline_us, start=j.start_us,
+                 duration=j.duration_us, slots=j.slots, missed=j.missed, slot_mask=j.slot_mask)
+            for j in out.jobs[:out.n_jobs]]
+    return st, dict(batch=list(out.batch[:n]), knee_slots=list(out.knee_slots[:n]),
+                    deployed_slots=list(out.deployed_slots[:n]), latency_us=list(out.latency_us[:n]),
+                    feasible=list(out.feasible[:n]), jobs=jobs, utilisation_ppm=out.utilisation_ppm)
+
+
+# ---------------------------------------------------------- kernel ops ----
+
+def _stream(stream):
+    if stream is None:
+        return None
+    return ctypes.c_void_p(stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
+
+
+def conv2d(x, w, K, R, S, stride, pad, scale, shift, res, act, y, out_fp32=False, stream=None):
+    N, H, W, C = x.shape
+    _check(lib().dstack_op_conv2d(_ptr(x), N, H, W, C, _ptr(w), K, R, S, stride, pad, _ptr(scale), _ptr(shift),
+                                  _ptr(res), act, _ptr(y), int(out_fp32), _stream(stream)))
+
+
+def dwconv3x3(x, w_rsc, stride, scale, shift, act, y, stream=None):
+    N, H, W, C = x.shape
+    _check(lib().dstack_op_dwconv3x3(_ptr(x), N, H, W, C, _ptr(w_rsc), stride, _ptr(scale), _ptr(shift), act,
+                                     _ptr(y), _stream(stream)))
+
+
+def fc(x, w, bias, act, y, out_fp32=False, stream=None):
+    B, I = x.shape
+    O = w.shape[0]
+    _check(lib().dstack_op_fc(_ptr(x), B, I, _ptr(w), _ptr(bias), O, act, _ptr(y), int(out_fp32), _stream(stream)))
+
+
+def maxpool(x, k, stride, pad, y, stream=None):
+    N, H, W, C = x.shape
+    _check(lib().dstack_op_maxpool(_ptr(x), N, H, W, C, k, stride, pad, _ptr(y), _stream(stream)))
+
+
+def avgpool(x, y, stream=None):
+    N, H, W, C = x.shape
+    _check(lib().dstack_op_avgpool(_ptr(x), N, H, W, C, _ptr(y), _stream(stream)))
+
+
+def lstm_workspace_bytes(T, B, H):
+    return lib().dstack_lstm_workspace_bytes(T, B, H)
+
+
+def lstm_layer(x, w_ih, w_hh, bias, h_bf16, h_f32, workspace, stream=None):
+    T, B, I = x.shape
+    H = w_hh.shape[1]
+    _check(lib().dstack_op_lstm_layer(_ptr(x), T, B, I, H, _ptr(w_ih), _ptr(w_hh), _ptr(bias), _ptr(h_bf16),
+                                      _ptr(h_f32), _ptr(workspace), _stream(stream)))

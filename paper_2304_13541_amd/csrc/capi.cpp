@@ -1,0 +1,477 @@
+// C ABI of the library: partitions (CU-masked streams), models, inference,
+// knee sweep, scheduling and kernel-level entry points.  Every function
+// catches C++ exceptions and converts them to a status.
+#include <hip/hip_ext.h>
+
+#include <algorithm>
+#include <atomic>
+#include <cmath>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "model.hpp"
+#include "sched.hpp"
+
+using namespace dstack;
+
+namespace dstack {
+
+static thread_local std::string t_err;
+void set_error(const std::string& msg) { t_err = msg; }
+void clear_error() { t_err.clear(); }
+
+}  // namespace dstack
+
+struct dstack_partition_s {
+  int id;
+  uint32_t slot_mask;
+  int n_slots;
+  int n_cu;
+  uint32_t words[8];
+  hipStream_t stream;
+};
+
+struct dstack_model_s {
+  Model m;
+};
+
+namespace {
+
+std::atomic<int> g_next_partition_id{1};
+
+template <typename F>
+dstack_status guarded(F&& f) {
+  try {
+    clear_error();
+    return f();
+  } catch (const std::bad_alloc&) {
+    return fail(DSTACK_E_OOM, "host allocation failed");
+  } catch (const std::exception& e) {
+    return fail(DSTACK_E_STATE, std::string("internal error: ") + e.what());
+  } catch (...) {
+    return fail(DSTACK_E_STATE, "internal error");
+  }
+}
+
+dstack_status make_partition(uint32_t slot_mask, dstack_partition* out) {
+  DS_CHECK(out, DSTACK_E_INVALID, "partition: null out pointer");
+  DS_CHECK(slot_mask != 0, DSTACK_E_INVALID, "partition: empty slot set");
+  auto* p = new dstack_partition_s();
+  p->id = g_next_partition_id++;
+  p->slot_mask = slot_mask;
+  p->n_slots = __builtin_popcount(slot_mask);
+  p->n_cu = p->n_slots * DSTACK_CUS_PER_SLOT;
+  std::memset(p->words, 0, sizeof(p->words));
+  // slot j = mask bits 8j..8j+7 = CU j of each of the 8 XCDs (bit i -> XCD i % 8)
+  for (int j = 0; j < DSTACK_TOTAL_SLOTS; ++j)
+    if ((slot_mask >> j) & 1) p->words[j / 4] |= 0xFFu << (8 * (j % 4));
+  hipError_t e = hipExtStreamCreateWithCUMask(&p->stream, 8, p->words);
+  if (e != hipSuccess) {
+    delete p;
+    return hip_fail(e, "hipExtStreamCreateWithCUMask");
+  }
+  *out = p;
+  return DSTACK_OK;
+}
+
+dstack_status slots_from_fraction(double f, int* slots) {
+  DS_CHECK(slots, DSTACK_E_INVALID, "fraction: null out pointer");
+  DS_CHECK(std::isfinite(f) && f > 0.0 && f <= 1.0, DSTACK_E_INVALID, "fraction must be in (0, 1]");
+  int s = (int)std::floor(32.0 * f + 0.5);
+  *slots = std::min(32, std::max(1, s));
+  return DSTACK_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* dstack_last_error(void) { return t_err.c_str(); }
+
+dstack_status dstack_fraction_to_slots(double f, int* slots) {
+  return guarded([&] { return slots_from_fraction(f, slots); });
+}
+
+dstack_status dstack_partition_create(double f, dstack_partition* out) {
+  return guarded([&] {
+    int s;
+    dstack_status st = slots_from_fraction(f, &s);
+    if (st != DSTACK_OK) return st;
+    return make_partition(s == 32 ? 0xFFFFFFFFu : ((1u << s) - 1), out);
+  });
+}
+
+dstack_status dstack_partition_create_at(int off, int n, dstack_partition* out) {
+  return guarded([&] {
+    DS_CHECK(off >= 0 && n >= 1 && off + n <= DSTACK_TOTAL_SLOTS, DSTACK_E_INVALID, "slot range outside 0..32");
+    uint32_t m = (n == 32) ? 0xFFFFFFFFu : (((1u << n) - 1) << off);
+    return make_partition(m, out);
+  });
+}
+
+dstack_status dstack_partition_create_mask(uint32_t slot_mask, dstack_partition* out) {
+  return guarded([&] { return make_partition(slot_mask, out); });
+}
+
+dstack_status dstack_partition_query(dstack_partition p, int* n_cu, uint32_t mask_words[8], void** hip_stream) {
+  return guarded([&] {
+    DS_CHECK(p, DSTACK_E_INVALID, "null partition");
+    if (n_cu) *n_cu = p->n_cu;
+    if (mask_words) std::memcpy(mask_words, p->words, sizeof(p->words));
+    if (hip_stream) *hip_stream = (void*)p->stream;
+    return DSTACK_OK;
+  });
+}
+
+dstack_status dstack_synchronize(dstack_partition p) {
+  return guarded([&] {
+    DS_CHECK(p, DSTACK_E_INVALID, "null partition");
+    DS_HIP(hipStreamSynchronize(p->stream));
+    return DSTACK_OK;
+  });
+}
+
+void dstack_partition_destroy(dstack_partition p) {
+  if (!p) return;
+  (void)hipStreamSynchronize(p->stream);
+  (void)hipStreamDestroy(p->stream);
+  delete p;
+}
+
+dstack_status dstack_probe_cu_ids(dstack_partition p, int n_blocks, uint32_t* host_out) {
+  return guarded([&] {
+    DS_CHECK(p && host_out, DSTACK_E_INVALID, "probe: null pointer");
+    DS_CHECK(n_blocks >= 1 && n_blocks <= 65536, DSTACK_E_INVALID, "probe: n_blocks in 1..65536");
+    uint32_t* d = nullptr;
+    DS_HIP(hipMalloc(&d, (size_t)n_blocks * 8));
+    dstack_status s = launch_probe(d, n_blocks, p->stream);
+    hipError_t e = hipSuccess;
+    if (s == DSTACK_OK) e = hipStreamSynchronize(p->stream);
+    if (s == DSTACK_OK && e == hipSuccess) e = hipMemcpy(host_out, d, (size_t)n_blocks * 8, hipMemcpyDeviceToHost);
+    (void)hipFree(d);
+    if (s != DSTACK_OK) return s;
+    if (e != hipSuccess) return hip_fail(e, "probe");
+    return DSTACK_OK;
+  });
+}
+
+dstack_status dstack_model_load(const char* arch, uint64_t seed, dstack_model* out) {
+  return guarded([&] {
+    DS_CHECK(arch && out, DSTACK_E_INVALID, "model_load: null pointer");
+    auto* h = new dstack_model_s();
+    h->m.seed = seed;
+    dstack_status s = build_arch(arch, h->m);
+    if (s == DSTACK_OK) s = upload_weights(h->m);
+    if (s != DSTACK_OK) {
+      std::string msg = t_err;
+      delete h;
+      set_error(msg);
+      return s;
+    }
+    *out = h;
+    return DSTACK_OK;
+  });
+}
+
+dstack_status dstack_model_query(dstack_model h, dstack_model_info* out) {
+  return guarded([&] {
+    DS_CHECK(h && out, DSTACK_E_INVALID, "model_query: null pointer");
+    const Model& m = h->m;
+    std::memset(out, 0, sizeof(*out));
+    std::strncpy(out->arch, m.arch.c_str(), sizeof(out->arch) - 1);
+    out->is_lstm = m.is_lstm;
+    out->max_batch = m.max_batch;
+    out->in_h = m.in_h;
+    out->in_w = m.in_w;
+    out->in_c = m.in_c;
+    out->seq_len = m.seq_len;
+    out->in_features = m.in_features;
+    out->out_features = m.out_features;
+    out->num_tensors = (int)m.tensors.size();
+    int64_t np = 0;
+    for (const auto& t : m.tensors) np += t.numel;
+    out->num_params = np;
+    double f, mf, wb;
+    int nk;
+    model_cost(m, 1, &f, &mf, &wb, &nk);
+    out->flops_per_item = f;
+    out->mfma_flops_per_item = mf;
+    out->weight_bytes = wb;
+    out->num_kernels = nk;
+    return DSTACK_OK;
+  });
+}
+
+static void unlayout(const TensorSpec& t, const uint16_t* dev, uint16_t* logical) {
+  if (t.layout == 0) {
+    std::memcpy(logical, dev, (size_t)t.numel * 2);
+  } else if (t.layout == 1) {
+    int64_t krs = (int64_t)t.d0 * t.d1 * t.d2;
+    for (int64_t q = 0; q < krs; ++q)
+      for (int c = 0; c < t.d3; ++c) logical[q * t.d3 + c] = dev[q * 8 + c];
+  } else {
+    int C = t.d0;
+    for (int c = 0; c < C; ++c)
+      for (int rs = 0; rs < 9; ++rs) logical[(size_t)c * 9 + rs] = dev[(size_t)rs * C + c];
+  }
+}
+
+dstack_status dstack_model_export_params(dstack_model h, int idx, void* dst, size_t bytes) {
+  return guarded([&] {
+    DS_CHECK(h && dst, DSTACK_E_INVALID, "export: null pointer");
+    const Model& m = h->m;
+    DS_CHECK(idx >= 0 && idx < (int)m.tensors.size(), DSTACK_E_INVALID, "export: tensor index out of range");
+    const TensorSpec& t = m.tensors[idx];
+    DS_CHECK(bytes == (size_t)t.numel * 2, DSTACK_E_INVALID, "export: byte count must be 2 * numel");
+    int64_t dev_numel = t.layout == 1 ? (int64_t)t.d0 * t.d1 * t.d2 * 8 : t.numel;
+    std::vector<uint16_t> tmp((size_t)dev_numel);
+    DS_HIP(hipMemcpy(tmp.data(), m.d_w + t.dev_off, (size_t)dev_numel * 2, hipMemcpyDeviceToHost));
+    unlayout(t, tmp.data(), (uint16_t*)dst);
+    return DSTACK_OK;
+  });
+}
+
+void dstack_model_destroy(dstack_model h) {
+  if (!h) return;
+  (void)hipDeviceSynchronize();
+  delete h;
+}
+
+dstack_status dstack_generate_params(const char* arch, uint64_t seed, int idx, void* dst, size_t bytes,
+                                     int64_t* numel) {
+  return guarded([&] {
+    DS_CHECK(arch, DSTACK_E_INVALID, "generate: null arch");
+    Model m;
+    m.seed = seed;
+    dstack_status s = build_arch(arch, m);
+    if (s != DSTACK_OK) return s;
+    DS_CHECK(idx >= 0 && idx < (int)m.tensors.size(), DSTACK_E_INVALID, "generate: tensor index out of range");
+    const TensorSpec& t = m.tensors[idx];
+    if (numel) *numel = t.numel;
+    if (!dst) return DSTACK_OK;
+    DS_CHECK(bytes == (size_t)t.numel * 2, DSTACK_E_INVALID, "generate: byte count must be 2 * numel");
+    generate_tensor(seed, idx, t, (uint16_t*)dst);
+    return DSTACK_OK;
+  });
+}
+
+// ---------------------------------------------------------------- infer ----
+
+namespace {
+
+struct BusyGuard {
+  std::atomic<bool>& f;
+  bool ok;
+  explicit BusyGuard(std::atomic<bool>& flag) : f(flag) {
+    bool expected = false;
+    ok = f.compare_exchange_strong(expected, true);
+  }
+  ~BusyGuard() {
+    if (ok) f.store(false);
+  }
+};
+
+dstack_status check_batch(const Model& m, int batch) {
+  DS_CHECK(batch >= 1 && batch <= m.max_batch, DSTACK_E_INVALID,
+           "batch must be in 1.." + std::to_string(m.max_batch));
+  return DSTACK_OK;
+}
+
+// Workspace id 0 is reserved for knee sweeps, which run one partition at a
+// time and reuse a single workspace across fractions.
+constexpr int SWEEP_WS_ID = 0;
+
+dstack_status infer_impl(Model& m, int batch, const void* d_in, void* d_out, dstack_partition p, KernelTimer* timer,
+                         int ws_id = -1) {
+  DS_CHECK(d_in && d_out && p, DSTACK_E_INVALID, "infer: null pointer");
+  dstack_status s = check_batch(m, batch);
+  if (s != DSTACK_OK) return s;
+  Workspace* ws;
+  s = get_workspace(m, ws_id >= 0 ? ws_id : p->id, p->n_cu, &ws);
+  if (s != DSTACK_OK) return s;
+  BusyGuard g(ws->busy);
+  DS_CHECK(g.ok, DSTACK_E_STATE, "infer: another call on this (model, partition) is in progress");
+  return forward(m, batch, d_in, d_out, *ws, p->n_cu, p->stream, timer);
+}
+
+}  // namespace
+
+dstack_status dstack_infer(dstack_model h, int batch, const void* d_in, void* d_out, dstack_partition p) {
+  return guarded([&] {
+    DS_CHECK(h, DSTACK_E_INVALID, "infer: null model");
+    return infer_impl(h->m, batch, d_in, d_out, p, nullptr);
+  });
+}
+
+dstack_status dstack_profile_layers(dstack_model h, int batch, const void* d_in, void* d_out, dstack_partition p,
+                                    dstack_layer_time* out, int max_layers, int* n_layers) {
+  return guarded([&] {
+    DS_CHECK(h && out && n_layers && p, DSTACK_E_INVALID, "profile: null pointer");
+    KernelTimer timer;
+    timer.st = p->stream;
+    dstack_status s = infer_impl(h->m, batch, d_in, d_out, p, &timer);
+    if (s != DSTACK_OK) return s;
+    DS_HIP(hipStreamSynchronize(p->stream));
+    int n = 0;
+    for (auto& r : timer.recs) {
+      if (n >= max_layers) break;
+      float ms = 0.f;
+      DS_HIP(hipEventElapsedTime(&ms, r.a, r.b));
+      out[n++] = dstack_layer_time{r.kind, ms, r.flops, r.bytes};
+    }
+    *n_layers = n;
+    return DSTACK_OK;
+  });
+}
+
+// ----------------------------------------------------------- knee sweep ----
+
+dstack_status dstack_knee_sweep(dstack_model h, int batch, const double* fractions, int n, int warmup, int reps,
+                                dstack_knee_result* out) {
+  return guarded([&] {
+    DS_CHECK(h && fractions && out, DSTACK_E_INVALID, "knee_sweep: null pointer");
+    DS_CHECK(n >= 1 && n <= DSTACK_MAX_SWEEP && warmup >= 0 && reps >= 1, DSTACK_E_INVALID,
+             "knee_sweep: n in 1..32, warmup >= 0, reps >= 1");
+    Model& m = h->m;
+    dstack_status s = check_batch(m, batch);
+    if (s != DSTACK_OK) return s;
+    std::memset(out, 0, sizeof(*out));
+    out->n = n;
+    out->batch = batch;
+    // scratch input/output at the model's maximum batch (contents: a fixed pattern)
+    size_t in_bytes = m.is_lstm ? (size_t)m.seq_len * m.max_batch * m.in_features * 2
+                                : (size_t)m.max_batch * m.in_h * m.in_w * m.in_c * 2;
+    size_t out_bytes = m.is_lstm ? (size_t)m.seq_len * m.max_batch * m.out_features * 4
+                                 : (size_t)m.max_batch * m.out_features * 4;
+    if (!m.sweep_in) {
+      DS_HIP(hipMalloc(&m.sweep_in, in_bytes));
+      DS_HIP(hipMalloc(&m.sweep_out, out_bytes));
+      std::vector<uint16_t> pat(in_bytes / 2);
+      uint64_t z = 0x2545F4914F6CDD1DULL;
+      for (auto& v : pat) {  // xorshift values in about [-1, 1), as bf16
+        z ^= z << 13; z ^= z >> 7; z ^= z << 17;
+        v = bf16_from_double(((double)(z >> 11) * (1.0 / 9007199254740992.0)) * 2.0 - 1.0);
+      }
+      DS_HIP(hipMemcpy(m.sweep_in, pat.data(), in_bytes, hipMemcpyHostToDevice));
+    }
+    for (int i = 0; i < n; ++i) {
+      int slots;
+      s = slots_from_fraction(fractions[i], &slots);
+      if (s != DSTACK_OK) return s;
+      dstack_partition p;
+      s = make_partition(slots == 32 ? 0xFFFFFFFFu : ((1u << slots) - 1), &p);
+      if (s != DSTACK_OK) return s;
+      std::vector<float> ms(reps);
+      std::vector<hipEvent_t> ev(2 * reps);
+      for (auto& e : ev) {
+        if (hipEventCreate(&e) != hipSuccess) e = nullptr;
+      }
+      for (int w = 0; w < warmup && s == DSTACK_OK; ++w)
+        s = infer_impl(m, batch, m.sweep_in, m.sweep_out, p, nullptr, SWEEP_WS_ID);
+      for (int r = 0; r < reps && s == DSTACK_OK; ++r) {
+        (void)hipEventRecord(ev[2 * r], p->stream);
+        s = infer_impl(m, batch, m.sweep_in, m.sweep_out, p, nullptr, SWEEP_WS_ID);
+        (void)hipEventRecord(ev[2 * r + 1], p->stream);
+      }
+      hipError_t e = hipStreamSynchronize(p->stream);
+      for (int r = 0; r < reps && e == hipSuccess; ++r) e = hipEventElapsedTime(&ms[r], ev[2 * r], ev[2 * r + 1]);
+      for (auto& x : ev)
+        if (x) (void)hipEventDestroy(x);
+      dstack_partition_destroy(p);
+      if (s != DSTACK_OK) return s;
+      if (e != hipSuccess) return hip_fail(e, "knee_sweep timing");
+      std::vector<double> us(reps);
+      for (int r = 0; r < reps; ++r) us[r] = 1000.0 * ms[r];
+      std::sort(us.begin(), us.end());
+      double med = (reps % 2) ? us[reps / 2] : 0.5 * (us[reps / 2 - 1] + us[reps / 2]);
+      out->slots[i] = slots;
+      out->n_cu[i] = slots * DSTACK_CUS_PER_SLOT;
+      out->latency_us_exact[i] = med;
+      out->latency_us[i] = std::max<int64_t>(1, (int64_t)std::floor(med + 0.5));
+      out->p99_us[i] = us[std::min(reps - 1, (int)std::ceil(0.99 * reps) - 1)];
+    }
+    int k = knee_index(batch, out->latency_us, out->slots, n);
+    out->knee_index = k;
+    out->knee_slots = out->slots[k];
+    out->deployed_slots = std::min(DSTACK_TOTAL_SLOTS, out->knee_slots + 2);
+    return DSTACK_OK;
+  });
+}
+
+dstack_status dstack_schedule(const dstack_sched_model* models, int n, const dstack_sched_params* prm,
+                              dstack_schedule_out* out) {
+  return guarded([&] { return schedule(models, n, prm, out); });
+}
+
+// ----------------------------------------------------- kernel-level ops ----
+
+dstack_status dstack_op_conv2d(const void* x, int N, int H, int W, int C, const void* w, int K, int R, int S,
+                               int stride, int pad, const float* scale, const float* shift, const void* res, int act,
+                               void* y, int out_fp32, void* stream) {
+  return guarded([&] {
+    DS_CHECK(x && w && y, DSTACK_E_INVALID, "conv2d: null pointer");
+    DS_CHECK(act >= 0 && act <= 2, DSTACK_E_INVALID, "conv2d: act must be 0, 1 or 2");
+    return launch_conv2d(static_cast<const bf16*>(x), N, H, W, C, static_cast<const bf16*>(w), K, R, S, stride, pad,
+                         scale, shift, static_cast<const bf16*>(res), act, y, out_fp32 != 0, 256, (hipStream_t)stream);
+  });
+}
+
+dstack_status dstack_op_dwconv3x3(const void* x, int N, int H, int W, int C, const void* w, int stride,
+                                  const float* scale, const float* shift, int act, void* y, void* stream) {
+  return guarded([&] {
+    DS_CHECK(x && w && y && scale && shift, DSTACK_E_INVALID, "dwconv3x3: null pointer");
+    DS_CHECK(act >= 0 && act <= 2, DSTACK_E_INVALID, "dwconv3x3: act must be 0, 1 or 2");
+    return launch_dwconv3x3(static_cast<const bf16*>(x), N, H, W, C, static_cast<const bf16*>(w), stride, scale,
+                            shift, act, static_cast<bf16*>(y), (hipStream_t)stream);
+  });
+}
+
+dstack_status dstack_op_fc(const void* x, int B, int I, const void* w, const float* bias, int O, int act, void* y,
+                           int out_fp32, void* stream) {
+  return guarded([&] {
+    DS_CHECK(x && w && y, DSTACK_E_INVALID, "fc: null pointer");
+    DS_CHECK(act >= 0 && act <= 2, DSTACK_E_INVALID, "fc: act must be 0, 1 or 2");
+    return launch_fc(static_cast<const bf16*>(x), B, I, static_cast<const bf16*>(w), bias, O, act, y, out_fp32 != 0,
+                     (hipStream_t)stream);
+  });
+}
+
+dstack_status dstack_op_maxpool(const void* x, int N, int H, int W, int C, int k, int stride, int pad, void* y,
+                                void* stream) {
+  return guarded([&] {
+    DS_CHECK(x && y, DSTACK_E_INVALID, "maxpool: null pointer");
+    return launch_maxpool(static_cast<const bf16*>(x), N, H, W, C, k, stride, pad, static_cast<bf16*>(y),
+                          (hipStream_t)stream);
+  });
+}
+
+dstack_status dstack_op_avgpool(const void* x, int N, int H, int W, int C, void* y, void* stream) {
+  return guarded([&] {
+    DS_CHECK(x && y, DSTACK_E_INVALID, "avgpool: null pointer");
+    return launch_avgpool(static_cast<const bf16*>(x), N, H, W, C, static_cast<bf16*>(y), (hipStream_t)stream);
+  });
+}
+
+size_t dstack_lstm_workspace_bytes(int T, int B, int H) {
+  if (T <= 0 || B <= 0 || H <= 0) return 0;
+  return ((size_t)T * B * 4 * H * 4 + 255) / 256 * 256 + (size_t)B * H * 4;
+}
+
+dstack_status dstack_op_lstm_layer(const void* x, int T, int B, int I, int H, const void* w_ih, const void* w_hh,
+                                   const float* bias, void* h_bf16, float* h_f32, void* workspace, void* stream) {
+  return guarded([&] {
+    DS_CHECK(x && w_ih && w_hh && bias && h_bf16 && workspace, DSTACK_E_INVALID, "lstm_layer: null pointer");
+    DS_CHECK(T >= 1 && I % 8 == 0 && I > 0, DSTACK_E_UNSUPPORTED, "lstm_layer: T >= 1, I % 8 == 0");
+    DS_CHECK(B >= 1 && B <= 32, DSTACK_E_UNSUPPORTED, "lstm_layer: batch must be 1..32");
+    DS_CHECK(H >= 32 && H % 32 == 0, DSTACK_E_UNSUPPORTED, "lstm_layer: H must be a multiple of 32");
+    float* gx = static_cast<float*>(workspace);
+    float* c = reinterpret_cast<float*>(static_cast<char*>(workspace) + ((size_t)T * B * 4 * H * 4 + 255) / 256 * 256);
+    return lstm_layer_run(static_cast<const bf16*>(x), T, B, I, H, static_cast<const bf16*>(w_ih),
+                          static_cast<const bf16*>(w_hh), bias, static_cast<bf16*>(h_bf16), h_f32, gx, c, 256,
+                          (hipStream_t)stream, nullptr);
+  });
+}
+
+}  // extern "C"

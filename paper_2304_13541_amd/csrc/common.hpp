@@ -1,0 +1,71 @@
+// Shared definitions of the HIP library: bf16 vector types, status and
+// error-text plumbing, launch helpers.
+#pragma once
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <cstdio>
+#include <string>
+
+#include "../../include/dstack.h"
+
+namespace dstack {
+
+typedef __bf16 bf16;
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
+typedef __attribute__((__vector_size__(4 * sizeof(__bf16)))) __bf16 bf16x4;
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
+typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16;
+
+enum Act { ACT_NONE = 0, ACT_RELU = 1, ACT_RELU6 = 2 };
+
+// Thread-local error text behind dstack_last_error().
+void set_error(const std::string& msg);
+void clear_error();
+
+inline dstack_status fail(dstack_status st, const std::string& msg) {
+  set_error(msg);
+  return st;
+}
+
+inline dstack_status hip_fail(hipError_t e, const char* what) {
+  return fail(DSTACK_E_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+#define DS_HIP(call)                                        \
+  do {                                                      \
+    hipError_t e_ = (call);                                 \
+    if (e_ != hipSuccess) return ::dstack::hip_fail(e_, #call); \
+  } while (0)
+
+#define DS_CHECK(cond, st, msg)                      \
+  do {                                               \
+    if (!(cond)) return ::dstack::fail((st), (msg)); \
+  } while (0)
+
+inline int ceil_div(int a, int b) { return (a + b - 1) / b; }
+inline int out_dim(int in, int k, int stride, int pad) { return (in + 2 * pad - k) / stride + 1; }
+
+__device__ __forceinline__ float apply_act(float v, int act) {
+  if (act == ACT_RELU) return fmaxf(v, 0.0f);
+  if (act == ACT_RELU6) return fminf(fmaxf(v, 0.0f), 6.0f);
+  return v;
+}
+
+// ---- kernel launchers (defined in the .hip files) ----
+dstack_status launch_conv2d(const bf16* x, int N, int H, int W, int C, const bf16* w, int K, int R, int S,
+                            int stride, int pad, const float* scale, const float* shift, const bf16* res, int act,
+                            void* y, bool out_fp32, int n_cu, hipStream_t st);
+dstack_status launch_dwconv3x3(const bf16* x, int N, int H, int W, int C, const bf16* w_rsc, int stride,
+                               const float* scale, const float* shift, int act, bf16* y, hipStream_t st);
+dstack_status launch_fc(const bf16* x, int B, int I, const bf16* w, const float* bias, int O, int act, void* y,
+                        bool out_fp32, hipStream_t st);
+dstack_status launch_maxpool(const bf16* x, int N, int H, int W, int C, int k, int stride, int pad, bf16* y,
+                             hipStream_t st);
+dstack_status launch_avgpool(const bf16* x, int N, int H, int W, int C, bf16* y, hipStream_t st);
+dstack_status launch_pack_c8(const bf16* x, int npix, int C, bf16* y, hipStream_t st);
+dstack_status launch_lstm_step(const float* gx_t, const bf16* w_hh, const bf16* h_prev, float* c, bf16* h_next,
+                               float* h_f32, int B, int H, bool first, hipStream_t st);
+dstack_status launch_probe(uint32_t* d_out, int n_blocks, hipStream_t st);
+
+}  // namespace dstack

@@ -1,0 +1,131 @@
+// Model builder and executor: the five architectures as flat lists of
+// kernel launches over NHWC bf16 activations, with per-(model, partition)
+// workspaces.
+#pragma once
+#include <atomic>
+#include <map>
+#include <memory>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "common.hpp"
+
+namespace dstack {
+
+enum Dist { DIST_HE = 0, DIST_ZERO = 1, DIST_LSTM = 2 };
+
+struct TensorSpec {
+  int64_t numel = 0;
+  int dist = DIST_HE;
+  int fan_in = 0;
+  // device placement
+  int64_t dev_off = 0;   // bf16 elements into the weight arena
+  int layout = 0;        // 0 same as logical, 1 conv stem padded C->8, 2 depthwise [C][3][3] -> [3][3][C]
+  int d0 = 0, d1 = 0, d2 = 0, d3 = 0;  // logical dims for re-layout
+};
+
+uint16_t bf16_from_double(double x);
+void generate_tensor(uint64_t seed, int index, const TensorSpec& t, uint16_t* out);
+
+enum OpKind { OP_PACK, OP_CONV, OP_DW, OP_MAXPOOL, OP_AVGPOOL, OP_FC, OP_LSTM };
+enum KernelClass { KC_MFMA = 0, KC_DW = 1, KC_FC = 2, KC_LSTM = 3, KC_GLUE = 4 };
+
+constexpr int BUF_IN = -1;
+constexpr int BUF_OUT = -2;
+constexpr int BUF_NONE = -3;
+
+struct Op {
+  OpKind kind;
+  int in = BUF_NONE, out = BUF_NONE, res = BUF_NONE;
+  int H = 0, W = 0, C = 0, K = 0, R = 1, S = 1, stride = 1, pad = 0, act = 0, Ho = 0, Wo = 0;
+  int C_true = 0;           // channels before padding (FLOP accounting)
+  int64_t w_off = 0;        // bf16 elements into the weight arena
+  int64_t scale_off = -1;   // fp32 elements into the fp32 arena (-1: none)
+  int64_t shift_off = -1;
+  int out_f32 = 0;
+  // LSTM layer
+  int T = 0, I = 0, Hd = 0;
+  int64_t wih_off = 0, whh_off = 0, bias_off = 0;
+  // tensor indices used when folding biases / BN at upload (-1: none)
+  int w_t = -1, bias_t = -1, bn = 0;
+  int wih_t = -1, whh_t = -1, bih_t = -1, bhh_t = -1;
+};
+
+struct KernelTimer;  // optional per-kernel event recorder
+
+struct Workspace {
+  void* base = nullptr;
+  size_t bytes = 0;
+  std::vector<char*> bufs;
+  float* splitk = nullptr;
+  size_t splitk_bytes = 0;
+  float* lstm_gx = nullptr;
+  float* lstm_c = nullptr;
+  bf16* lstm_h[2] = {nullptr, nullptr};
+  std::atomic<bool> busy{false};
+};
+
+struct Model {
+  std::string arch;
+  uint64_t seed = 0;
+  int is_lstm = 0;
+  int max_batch = 32;
+  int in_h = 0, in_w = 0, in_c = 0;
+  int seq_len = 0, in_features = 0, out_features = 0;
+  std::vector<TensorSpec> tensors;
+  std::vector<Op> ops;
+  std::vector<int64_t> buf_elems;   // per-item bf16 elements of each buffer id
+  int64_t n_weights = 0;            // bf16 arena size
+  int64_t n_fp32 = 0;               // fp32 arena size
+  std::vector<float> fp32_host;     // scale/shift/bias values
+  bf16* d_w = nullptr;
+  float* d_f32 = nullptr;
+  int lstm_T = 0, lstm_B_max = 32, lstm_H = 0;
+  std::mutex ws_mu;
+  std::map<int, std::unique_ptr<Workspace>> ws;  // by partition id
+  // scratch for knee sweeps
+  void* sweep_in = nullptr;
+  void* sweep_out = nullptr;
+
+  ~Model();
+};
+
+// Architecture description (host only; no device memory touched).
+dstack_status build_arch(const std::string& arch, Model& m);
+// Device upload of the generated weights and folded BN parameters.
+dstack_status upload_weights(Model& m);
+// Workspace for batch <= max_batch, on demand.
+dstack_status get_workspace(Model& m, int partition_id, int n_cu, Workspace** out);
+
+// Enqueue one forward pass on `st`.  `timer` may be null.
+dstack_status forward(Model& m, int batch, const void* d_in, void* d_out, Workspace& ws, int n_cu, hipStream_t st,
+                      KernelTimer* timer);
+
+// Algorithmic cost of the ops at a batch size.
+void model_cost(const Model& m, int batch, double* flops, double* mfma_flops, double* weight_bytes, int* n_kernels);
+
+struct KernelTimer {
+  struct Rec {
+    int kind;
+    double flops, bytes;
+    hipEvent_t a, b;
+  };
+  hipStream_t st;
+  std::vector<Rec> recs;
+  hipEvent_t pending = nullptr;
+  void before();
+  void after(int kind, double flops, double bytes);
+  ~KernelTimer();
+};
+
+size_t conv_splitk_workspace_bytes(int M, int K, int Kg, int n_cu);
+dstack_status launch_conv2d_ws(const bf16* x, int N, int H, int W, int C, const bf16* w, int K, int R, int S,
+                               int stride, int pad, const float* scale, const float* shift, const bf16* res,
+                               int act, void* y, bool out_fp32, int n_cu, float* splitk_ws, size_t splitk_bytes,
+                               hipStream_t st);
+dstack_status lstm_layer_run(const bf16* x, int T, int B, int I, int H, const bf16* w_ih, const bf16* w_hh,
+                             const float* bias, bf16* h_bf16, float* h_f32, float* gx, float* c, int n_cu,
+                             hipStream_t st, KernelTimer* timer);
+
+}  // namespace dstack

@@ -1,0 +1,149 @@
+"""Kernel-level parity on the GPU: each HIP kernel, called through the C ABI,
+against the fp64 oracle on the same seeded bf16 inputs.  Shapes span several
+tiles with ragged tails in every GEMM dimension, odd spatial sizes with
+stride 2, K not a multiple of the tile, and every epilogue variant.
+
+Bar: infinity-norm relative error <= 2e-2 (bf16 inputs, fp32 accumulation,
+bf16 or fp32 output)."""
+import numpy as np
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+TOL = 2e-2
+
+
+@pytest.fixture(scope="module")
+def env(oracle_mod):
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2304_13541_amd as ds
+    from tests import gpu_util as gu
+    from tests import inputs
+    return ds, gu, inputs, oracle_mod, torch
+
+
+CONV_CASES = [
+    # N, H, W, C, K, R, stride, pad, act, residual, out_fp32
+    (2, 9, 7, 16, 36, 3, 1, 1, 1, False, False),
+    (1, 15, 15, 24, 20, 3, 2, 1, 2, False, False),
+    (3, 5, 5, 64, 132, 1, 1, 0, 0, True, False),
+    (2, 23, 23, 8, 64, 7, 2, 3, 1, False, False),
+    (2, 28, 28, 64, 192, 3, 1, 1, 1, True, False),
+    (1, 14, 14, 256, 1028, 1, 2, 0, 0, False, True),
+    (4, 7, 7, 512, 512, 3, 1, 1, 1, False, False),
+    (1, 1, 1, 520, 4, 1, 1, 0, 0, False, True),
+]
+
+
+@pytest.mark.parametrize("case", CONV_CASES)
+def test_conv2d(env, case):
+    ds, gu, inputs, oracle, torch = env
+    N, H, W, C, K, R, st, pad, act, use_res, f32 = case
+    print("conv2d case", case, flush=True)
+    xb = inputs.normal_bf16(1, (N, H, W, C))
+    wb = inputs.normal_bf16(2, (K, R, R, C), scale=(2.0 / (R * R * C)) ** 0.5)
+    rng = np.random.default_rng(3)
+    scale = rng.uniform(0.5, 1.5, K).astype(np.float32)
+    shift = rng.uniform(-0.2, 0.2, K).astype(np.float32)
+    Ho, Wo = (H + 2 * pad - R) // st + 1, (W + 2 * pad - R) // st + 1
+    resb = inputs.normal_bf16(4, (N, Ho, Wo, K)) if use_res else None
+    y = gu.empty_f32((N, Ho, Wo, K)) if f32 else gu.empty_bf16((N, Ho, Wo, K))
+    ds.conv2d(gu.dev_bf16(xb), gu.dev_bf16(wb), K, R, R, st, pad, gu.dev_f32(scale), gu.dev_f32(shift),
+              gu.dev_bf16(resb) if use_res else None, act, y, out_fp32=f32)
+    torch.cuda.synchronize()
+    x = oracle.bf16_bits_to_f64(xb)
+    w = oracle.bf16_bits_to_f64(wb)
+    ref = oracle.conv2d(x, w, st, pad) * scale.astype(np.float64) + shift.astype(np.float64)
+    if use_res:
+        ref = ref + oracle.bf16_bits_to_f64(resb)
+    ref = np.maximum(ref, 0) if act == 1 else (np.clip(ref, 0, 6) if act == 2 else ref)
+    err = oracle.rel_err(gu.host(y), ref)
+    print("rel_err", err)
+    assert err <= TOL
+
+
+@pytest.mark.parametrize("case", [(2, 11, 9, 32, 1), (1, 12, 12, 96, 2), (3, 7, 7, 960, 1), (2, 15, 13, 144, 2)])
+def test_dwconv3x3(env, case):
+    ds, gu, inputs, oracle, torch = env
+    N, H, W, C, st = case
+    xb = inputs.normal_bf16(5, (N, H, W, C))
+    wb = inputs.normal_bf16(6, (C, 3, 3), scale=0.47)
+    rng = np.random.default_rng(7)
+    scale = rng.uniform(0.5, 1.5, C).astype(np.float32)
+    shift = rng.uniform(-0.2, 0.2, C).astype(np.float32)
+    Ho, Wo = (H + 2 - 3) // st + 1, (W + 2 - 3) // st + 1
+    y = gu.empty_bf16((N, Ho, Wo, C))
+    w_rsc = np.ascontiguousarray(wb.reshape(C, 9).T.reshape(3, 3, C))  # device layout [3][3][C]
+    ds.dwconv3x3(gu.dev_bf16(xb), gu.dev_bf16(w_rsc), st, gu.dev_f32(scale), gu.dev_f32(shift), 2, y)
+    torch.cuda.synchronize()
+    ref = oracle.dwconv(oracle.bf16_bits_to_f64(xb), oracle.bf16_bits_to_f64(wb), st, 1)
+    ref = np.clip(ref * scale + shift, 0, 6)
+    assert oracle.rel_err(gu.host(y), ref) <= TOL
+
+
+@pytest.mark.parametrize("case", [(1, 64, 10, 0, True), (8, 25088, 40, 1, False), (16, 2048, 1000, 0, True),
+                                  (32, 1280, 37, 1, False), (5, 520, 9, 2, True)])
+def test_fc(env, case):
+    ds, gu, inputs, oracle, torch = env
+    B, I, O, act, f32 = case
+    xb = inputs.normal_bf16(8, (B, I))
+    wb = inputs.normal_bf16(9, (O, I), scale=(2.0 / I) ** 0.5)
+    bias = np.random.default_rng(10).uniform(-0.5, 0.5, O).astype(np.float32)
+    y = gu.empty_f32((B, O)) if f32 else gu.empty_bf16((B, O))
+    ds.fc(gu.dev_bf16(xb), gu.dev_bf16(wb), gu.dev_f32(bias), act, y, out_fp32=f32)
+    torch.cuda.synchronize()
+    ref = oracle.fc(oracle.bf16_bits_to_f64(xb), oracle.bf16_bits_to_f64(wb), bias)
+    ref = np.maximum(ref, 0) if act == 1 else (np.clip(ref, 0, 6) if act == 2 else ref)
+    assert oracle.rel_err(gu.host(y), ref) <= TOL
+
+
+@pytest.mark.parametrize("case", [(2, 8, 8, 16, 2, 2, 0), (1, 112, 112, 64, 3, 2, 1), (3, 7, 9, 8, 3, 2, 1)])
+def test_pools(env, case):
+    ds, gu, inputs, oracle, torch = env
+    N, H, W, C, k, st, pad = case
+    xb = inputs.normal_bf16(11, (N, H, W, C))
+    Ho, Wo = (H + 2 * pad - k) // st + 1, (W + 2 * pad - k) // st + 1
+    y = gu.empty_bf16((N, Ho, Wo, C))
+    ds.maxpool(gu.dev_bf16(xb), k, st, pad, y)
+    g = gu.empty_bf16((N, C))
+    ds.avgpool(gu.dev_bf16(xb), g)
+    torch.cuda.synchronize()
+    x = oracle.bf16_bits_to_f64(xb)
+    assert np.array_equal(gu.host(y), oracle.maxpool(x, k, st, pad))  # a max of bf16 values is exact
+    assert oracle.rel_err(gu.host(g), oracle.avgpool(x)) <= TOL
+
+
+@pytest.mark.parametrize("case", [(5, 3, 64, 64), (50, 32, 512, 1024), (7, 17, 40, 96)])
+def test_lstm_layer(env, case):
+    ds, gu, inputs, oracle, torch = env
+    T, B, I, H = case
+    xb = inputs.normal_bf16(12, (T, B, I))
+    a = 1.0 / np.sqrt(H)
+    wih = inputs.uniform_bf16(13, (4 * H, I), -a, a)
+    whh = inputs.uniform_bf16(14, (4 * H, H), -a, a)
+    bias = np.random.default_rng(15).uniform(-2 * a, 2 * a, 4 * H).astype(np.float32)
+    hb = gu.empty_bf16((T, B, H))
+    hf = gu.empty_f32((T, B, H))
+    ws = torch.empty(ds.lstm_workspace_bytes(T, B, H), dtype=torch.uint8, device="cuda:0")
+    ds.lstm_layer(gu.dev_bf16(xb), gu.dev_bf16(wih), gu.dev_bf16(whh), gu.dev_f32(bias), hb, hf, ws)
+    torch.cuda.synchronize()
+    h_ref, _ = oracle.lstm_layer(oracle.bf16_bits_to_f64(xb), oracle.bf16_bits_to_f64(wih),
+                                 oracle.bf16_bits_to_f64(whh), bias.astype(np.float64), np.zeros(4 * H), round_h=True)
+    assert oracle.rel_err(gu.host(hf), h_ref) <= TOL
+    assert oracle.rel_err(gu.host(hb), h_ref) <= TOL
+
+
+def test_kernel_argument_errors(env):
+    ds, gu, inputs, oracle, torch = env
+    x = gu.empty_bf16((1, 4, 4, 12))
+    w = gu.empty_bf16((8, 3, 3, 12))
+    y = gu.empty_bf16((1, 4, 4, 8))
+    with pytest.raises(ds.DStackError) as e:  # C % 8 != 0
+        ds.conv2d(x, w, 8, 3, 3, 1, 1, None, None, None, 0, y)
+    assert e.value.status == ds.E_UNSUPPORTED
+    xb = gu.empty_bf16((33, 64))
+    with pytest.raises(ds.DStackError) as e:  # batch > 32
+        ds.fc(xb, gu.empty_bf16((10, 64)), None, 0, gu.empty_f32((33, 10)), out_fp32=True)
+    assert e.value.status == ds.E_UNSUPPORTED

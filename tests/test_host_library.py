@@ -1,0 +1,139 @@
+"""Host-side checks of the HIP library (no GPU needed): it loads, exports every
+entry point its header declares, generates weights bit-identical to the
+oracle's independent generator, and makes scheduling decisions identical to
+the scheduler oracle's."""
+import math
+import os
+import random
+import re
+
+import numpy as np
+import pytest
+
+import paper_2304_13541_amd as ds
+from oracle import sched
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    text = open(os.path.join(ROOT, "include", "dstack.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(dstack_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    L = ds.lib()
+    names = declared_functions()
+    assert len(names) >= 20
+    for n in names:
+        assert hasattr(L, n), n
+    assert set(names) == set(ds._SIGS)
+
+
+def test_fraction_to_slots():
+    table = {0.1: 3, 0.2: 6, 0.25: 8, 0.3: 10, 0.4: 13, 0.5: 16, 0.6: 19, 0.7: 22, 0.8: 26, 0.9: 29, 1.0: 32,
+             0.001: 1}
+    for f, s in table.items():
+        assert ds.fraction_to_slots(f) == s == min(32, max(1, math.floor(32 * f + 0.5)))
+    for bad in (0.0, -0.1, 1.0001, float("nan"), float("inf")):
+        with pytest.raises(ds.DStackError) as e:
+            ds.fraction_to_slots(bad)
+        assert e.value.status == ds.E_INVALID
+
+
+@pytest.mark.parametrize("arch", ["tinycnn", "resnet50", "mobilenetv2", "lstm2", "vgg19"])
+def test_weights_bit_identical_to_oracle(oracle_mod, arch):
+    m = oracle_mod.Model(arch, 1234)
+    n = m.num_tensors()
+    idxs = range(n) if arch != "vgg19" else [0, 1, 2, 5, 17, 30, 33, 35, 37]
+    for i in idxs:
+        lib_bits = ds.generate_params(arch, 1234, i)
+        assert np.array_equal(lib_bits, m.tensor_bf16(i)), (arch, i)
+
+
+def test_generate_params_errors():
+    with pytest.raises(ds.DStackError) as e:
+        ds.generate_params("alexnet", 1, 0)
+    assert e.value.status == ds.E_UNSUPPORTED
+    with pytest.raises(ds.DStackError) as e:
+        ds.generate_params("tinycnn", 1, 99)
+    assert e.value.status == ds.E_INVALID
+
+
+def _lib_vs_oracle(models, period, total=32, overprov=2):
+    st, got = ds.schedule(models, period, total, overprov)
+    choices, jobs, util, ok = sched.schedule(models, period, total, overprov)
+    assert (st == ds.OK) == ok
+    assert got["batch"] == [c.batch for c in choices]
+    assert got["knee_slots"] == [c.slots for c in choices]
+    assert got["latency_us"] == [c.latency for c in choices]
+    assert got["feasible"] == [int(c.feasible) for c in choices]
+    assert got["deployed_slots"] == [min(total, c.slots + overprov) for c in choices]
+    assert got["utilisation_ppm"] == util
+    assert len(got["jobs"]) == len(jobs)
+    for a, b in zip(got["jobs"], jobs):
+        assert (a["model"], a["k"], a["release"], a["deadline"], a["start"], a["duration"], a["slots"], a["missed"],
+                a["slot_mask"]) == (b.model, b.k, b.release, b.deadline, b.start, b.duration, b.slots,
+                                    int(b.missed), b.slot_mask)
+    return got
+
+
+def _amdahl_table(a_us, c_us, batches, slots):
+    return {b: {s: int(a_us * (1 + 0.1 * b) + c_us * b / s) for s in slots} for b in batches}
+
+
+SWEEP_SLOTS = [3, 6, 10, 13, 16, 19, 22, 26, 29, 32]
+
+
+def test_schedule_parity_config_shaped_tables():
+    # two-model mix (ResNet-50-like SLO 25 ms, MobileNetV2-like 15 ms) and the four-model mix
+    r50 = dict(slo_us=25000, max_batch=16, rate_per_s=0, table=_amdahl_table(400, 9000, [1, 2, 4, 8, 16], SWEEP_SLOTS))
+    mb = dict(slo_us=15000, max_batch=32, rate_per_s=0, table=_amdahl_table(300, 2500, [1, 2, 4, 8, 16, 32], SWEEP_SLOTS))
+    _lib_vs_oracle([r50, mb], 100000)
+    vgg = dict(slo_us=50000, max_batch=32, rate_per_s=150, table=_amdahl_table(800, 30000, [1, 2, 4, 8], SWEEP_SLOTS))
+    lstm = dict(slo_us=30000, max_batch=32, rate_per_s=300, table=_amdahl_table(3000, 2000, [1, 2, 4, 8], SWEEP_SLOTS))
+    r50r = dict(r50, rate_per_s=400)
+    mbr = dict(mb, rate_per_s=800)
+    _lib_vs_oracle([r50r, mbr, vgg, lstm], 100000)
+
+
+def test_schedule_parity_paper_table():
+    models = [dict(slo_us=25000, max_batch=16, table={16: {3: 8000}}),
+              dict(slo_us=50000, max_batch=16, table={16: {4: 28000}}),
+              dict(slo_us=100000, max_batch=16, table={16: {5: 55000}})]
+    got = _lib_vs_oracle(models, 100000, total=10, overprov=0)
+    assert got["utilisation_ppm"] == 595000
+
+
+def test_schedule_parity_random():
+    rnd = random.Random(2026)
+    for trial in range(300):
+        models = []
+        total = rnd.choice([8, 16, 32])
+        for _ in range(rnd.randint(1, 6)):
+            batches = sorted(rnd.sample([1, 2, 4, 8, 16, 32], rnd.randint(1, 6)))
+            slots = sorted(rnd.sample(range(1, total + 1), rnd.randint(1, min(10, total))))
+            table = {}
+            for b in batches:
+                row = {}
+                for s in slots:
+                    if rnd.random() < 0.9:
+                        row[s] = rnd.randint(100, 60000)
+                if row:
+                    table[b] = row
+            if not table:
+                continue
+            models.append(dict(slo_us=rnd.choice([10000, 15000, 25000, 30000, 50000, 100000]),
+                               max_batch=rnd.choice([1, 4, 8, 16, 32]), rate_per_s=rnd.choice([0, 0, 150, 400, 800]),
+                               table=table))
+        if not models:
+            continue
+        _lib_vs_oracle(models, rnd.choice([50000, 100000]), total=total, overprov=rnd.choice([0, 2]))
+
+
+def test_schedule_rejects_bad_arguments():
+    with pytest.raises(ds.DStackError):
+        ds.schedule([dict(slo_us=0, max_batch=1, table={1: {4: 10}})], 100000)
+    with pytest.raises(ds.DStackError):
+        ds.schedule([dict(slo_us=1000, max_batch=1, table={1: {40: 10}})], 100000)
