@@ -158,6 +158,7 @@ typedef struct {
   float ms;
   double flops;
   double bytes;
+  int gemm_m, gemm_n, gemm_k;  /* GEMM view of MFMA kernels (pixels, out channels, depth); else 0 */
 } dstack_layer_time;
 dstack_status dstack_profile_layers(dstack_model m, int batch, const void* d_in, void* d_out, dstack_partition p,
                                     dstack_layer_time* out, int max_layers, int* n_layers);

@@ -37,7 +37,8 @@ class ModelInfo(ctypes.Structure):
 
 
 class LayerTime(ctypes.Structure):
-    _fields_ = [("kind", ctypes.c_int), ("ms", ctypes.c_float), ("flops", ctypes.c_double), ("bytes", ctypes.c_double)]
+    _fields_ = [("kind", ctypes.c_int), ("ms", ctypes.c_float), ("flops", ctypes.c_double), ("bytes", ctypes.c_double),
+                ("gemm_m", ctypes.c_int), ("gemm_n", ctypes.c_int), ("gemm_k", ctypes.c_int)]
 
 
 class KneeResult(ctypes.Structure):
@@ -234,7 +235,8 @@ class Model:
         n = ctypes.c_int()
         _check(lib().dstack_profile_layers(self.h, batch, _ptr(x), _ptr(y), partition.h, arr, max_layers,
                                            ctypes.byref(n)))
-        return [dict(kind=arr[i].kind, ms=arr[i].ms, flops=arr[i].flops, bytes=arr[i].bytes) for i in range(n.value)]
+        return [dict(kind=arr[i].kind, ms=arr[i].ms, flops=arr[i].flops, bytes=arr[i].bytes,
+                     gemm=(arr[i].gemm_m, arr[i].gemm_n, arr[i].gemm_k)) for i in range(n.value)]
 
     def knee_sweep(self, batch, fractions, warmup=5, reps=20):
         fr = (ctypes.c_double * len(fractions))(*fractions)

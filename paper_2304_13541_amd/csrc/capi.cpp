@@ -319,7 +319,7 @@ dstack_status dstack_profile_layers(dstack_model h, int batch, const void* d_in,
       if (n >= max_layers) break;
       float ms = 0.f;
       DS_HIP(hipEventElapsedTime(&ms, r.a, r.b));
-      out[n++] = dstack_layer_time{r.kind, ms, r.flops, r.bytes};
+      out[n++] = dstack_layer_time{r.kind, ms, r.flops, r.bytes, r.m, r.n, r.k};
     }
     *n_layers = n;
     return DSTACK_OK;

@@ -10,14 +10,24 @@
 // a pixel is gathered on the fly, 8 channels (16 bytes) at a time, which
 // needs C % 8 == 0 (3-channel stems are zero-padded to 8 before the call).
 //
-// Block: 256 threads = 4 waves in a 2x2 grid over the (BN x BM) tile; each
-// wave owns (BN/2 x BM/2) and issues v_mfma_f32_16x16x32_bf16 on it.  Tiles
-// of BK = 64 depth are staged global -> registers -> LDS with a two-stage
-// LDS ring, so the next tile's global loads are in flight during the current
-// tile's MFMAs.  Operand layouts of the 16x16x32 bf16 MFMA (checked on the
-// device): lane l holds A[l%16][8*(l/16) .. +8) and B[8*(l/16) .. +8)[l%16];
-// the result holds C[4*(l/16)+i][l%16], i = 0..3, so each lane ends with 4
-// consecutive output channels of one pixel: one 8-byte bf16 store.
+// Data movement.  Each depth tile (BK = 64) of both operands is copied from
+// global memory straight into LDS with buffer_load_dwordx4 ... lds: a wave's
+// load moves 64 lanes x 16 bytes into one contiguous 1 KB LDS block (8 tile
+// rows of 128 bytes).  An out-of-range buffer offset deposits zeros, which
+// implements the convolution's zero padding, the pixel tail and the depth
+// tail without branches on the data path.  A ring of STAGES such tiles keeps
+// STAGES-1 tiles in flight while the matrix cores work on the current one;
+// the wait is a vmcnt count (loads retire in order) followed by one barrier.
+// Rows are stored unpadded with their eight 16-byte chunks XOR-swizzled by
+// (row/2) % 8, so the 16 rows an MFMA fragment read touches fall on 16
+// distinct 4-bank groups.
+//
+// Compute.  256 threads = 4 waves in a WN x WM grid over the (BN x BM) tile;
+// each wave issues v_mfma_f32_16x16x32_bf16 on its (BN/WN x BM/WM) sub-tile.
+// Operand layouts (checked on the device): lane l holds A[l%16][8*(l/16)..+8)
+// and B[8*(l/16)..+8)[l%16]; the result holds C[4*(l/16)+i][l%16], i = 0..3,
+// so each lane ends with 4 consecutive output channels of one pixel and the
+// epilogue (scale, shift, residual, activation) is one 8-byte store.
 //
 // Split-K: with gridDim.z = splits > 1 each z-slice accumulates a range of
 // depth tiles and writes raw fp32 partial sums to a workspace; a second
@@ -25,6 +35,25 @@
 #include "common.hpp"
 
 namespace dstack {
+
+// Division by a runtime constant d >= 1 for 0 <= n < 2^31 with a multiply-high:
+// l = ceil(log2 d), m = floor(2^32 (2^l - d) / d) + 1, n / d = (mulhi(m, n) + n) >> l
+// (Granlund & Montgomery, "Division by invariant integers using
+// multiplication", PLDI 1994).
+struct FastDiv {
+  unsigned m;
+  int l;
+  int d;
+  static FastDiv make(int d) {
+    FastDiv f;
+    f.d = d;
+    f.l = 0;
+    while ((1LL << f.l) < d) ++f.l;
+    f.m = (unsigned)((((1ULL << 32) * ((1ULL << f.l) - (unsigned long long)d)) / (unsigned long long)d) + 1);
+    return f;
+  }
+  __device__ __forceinline__ int div(int n) const { return (int)((__umulhi(m, (unsigned)n) + (unsigned)n) >> l); }
+};
 
 struct ConvArgs {
   const bf16* x;
@@ -38,12 +67,19 @@ struct ConvArgs {
   int M, Kg;
   int act;
   int kt_per_split;
+  int tiles_n;         // output-channel tiles (fastest-varying in the tile order)
+  int tiles;           // tiles per split slice
+  FastDiv div_wo, div_ho, div_c, div_s, div_tn;
 };
 
-constexpr int BK = 64;
-constexpr int LDK = BK + 8;   // LDS row pitch (bf16): 144 B, spreads 16 rows over all banks
-constexpr int CPR = BK / 8;   // 16-byte chunks per tile row
-constexpr int RSTEP = 256 / CPR;
+constexpr int BK = 64;          // depth per LDS stage (bf16 elements)
+constexpr int ROW_BYTES = 128;  // one tile row = BK bf16
+constexpr unsigned OOB = 0x80000000u;  // buffer offset past any tensor (< 2 GB): loads zeros
+
+// Addressing of the activation operand: 1x1 stride 1 (the pixel row is the
+// input row), 1x1 strided, C % 64 == 0 (a depth tile lies in one (r, s)), or
+// the general per-chunk (r, s, c) decomposition.
+enum ConvMode { MODE_1X1 = 0, MODE_TILED = 1, MODE_GENERIC = 2, MODE_1X1S1 = 3 };
 
 __device__ __forceinline__ void store_out4(void* y, bool f32, long idx, const float v[4]) {
   if (f32) {
@@ -71,39 +107,123 @@ __device__ __forceinline__ void epilogue4(const ConvArgs& a, bool f32, int px, i
   store_out4(a.y, f32, idx, v);
 }
 
-template <int BN, int BM, bool OUT_F32, bool SPLIT>
-__global__ __launch_bounds__(256) void conv_igemm_kernel(ConvArgs a) {
-  constexpr int NW = BN * CPR / 256;  // weight chunks per thread
-  constexpr int NX = BM * CPR / 256;  // activation chunks per thread
-  constexpr int TN = BN / 32;         // 16-row MFMA tiles per wave (channels)
-  constexpr int TM = BM / 32;         // 16-col MFMA tiles per wave (pixels)
-  static_assert(NW >= 1 && NX >= 1, "tile too small for 256 threads");
+// vmcnt wait with an immediate count (gfx9 encoding: vmcnt[3:0] | vmcnt[5:4] << 14,
+// expcnt and lgkmcnt left at "no wait").
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt is 6 bits");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
 
-  __shared__ __attribute__((aligned(16))) bf16 lds[2][(BN + BM) * LDK];
+typedef __attribute__((__vector_size__(4 * sizeof(int)))) int i32x4;
+
+// Raw buffer descriptor: base, no stride, num_records = byte size (offsets at
+// or past it read as zero), gfx9 data-format word.
+__device__ __forceinline__ i32x4 make_rsrc(const void* base, unsigned bytes) {
+  const unsigned long long p = (unsigned long long)base;
+  i32x4 r;
+  r[0] = (int)(unsigned)(p & 0xffffffffu);
+  r[1] = (int)(unsigned)((p >> 32) & 0xffffu);
+  r[2] = (int)bytes;
+  r[3] = 0x00020000;
+  return r;
+}
+
+// 32-bit LDS byte address of a pointer into a __shared__ array.
+__device__ __forceinline__ unsigned lds_address(const void* p) {
+  return (unsigned)(unsigned long long)(const __attribute__((address_space(3))) void*)p;
+}
+
+// 16 bytes per lane from buffer offset `voff` into LDS at lds_base + 16 * lane.
+// Issued as inline asm so that the compiler does not treat every later LDS
+// read as dependent on it (it would wait for all loads in flight); the
+// kernel's own vmcnt waits order these loads against the LDS reads.
+// M0 (the LDS destination) is saved and restored around the load.
+__device__ __forceinline__ void load_to_lds16(i32x4 rsrc, unsigned voff, unsigned lds_base) {
+  unsigned saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %1\n\t"
+      "s_nop 0\n\t"
+      "buffer_load_dwordx4 %2, %3, 0 offen lds\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "s"(lds_base), "v"(voff), "s"(rsrc)
+      : "memory");
+}
+
+template <int BN, int BM, int WN, int WM, int STAGES, int MODE, bool OUT_F32, bool SPLIT>
+__global__ __launch_bounds__(256) void conv_igemm_kernel(ConvArgs a) {
+  constexpr int ROWS = BN + BM;
+  constexpr int STAGE_BYTES = ROWS * ROW_BYTES;
+  constexpr int LOADS = ROWS / 8;       // wave-loads (8 rows each) per stage
+  constexpr int LPW = LOADS / 4;        // per wave
+  constexpr int TN = BN / WN / 16;      // MFMA tiles per wave along channels
+  constexpr int TM = BM / WM / 16;      // ... along pixels
+  static_assert(LOADS % 4 == 0 && WN * WM == 4 && TN >= 1 && TM >= 1, "tile shape");
+  static_assert(STAGES >= 2 && STAGES <= 4, "2..4 stages");
+
+  __shared__ __attribute__((aligned(1024))) unsigned char lds[STAGES * STAGE_BYTES];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
-  const int wn = wave & 1, wm = wave >> 1;
-  const int n0 = blockIdx.y * BN;  // first output channel of the tile
-  const int m0 = blockIdx.x * BM;  // first output pixel of the tile
-  const int kc = tid % CPR;
+  const int wn = wave % WN, wm = wave / WN;
+  // XCD-aware tile order: consecutive workgroups go round-robin to the 8 XCDs,
+  // so XCD x is given the contiguous tile range [x*q + min(x, r), ...) of the
+  // (pixel tile, channel tile) order with channel tiles fastest; the blocks
+  // that share an activation tile then share that XCD's L2.
+  int tile;
+  {
+    const int L = blockIdx.x;
+    const int q = a.tiles >> 3, r = a.tiles & 7;
+    const int x = L & 7, i = L >> 3;
+    tile = x * q + min(x, r) + i;
+  }
+  const int tm_idx = a.div_tn.div(tile);
+  const int n0 = (tile - tm_idx * a.tiles_n) * BN;
+  const int m0 = tm_idx * BM;
 
-  // per-row im2col bookkeeping for this thread's activation chunks
-  int xbase[NX], hi0[NX], wi0[NX];
-  bool xvalid[NX];
+  const i32x4 wrs = make_rsrc(a.w, (unsigned)((long)a.K * a.Kg * 2));
+  const i32x4 xrs = make_rsrc(a.x, (unsigned)((long)a.N * a.H * a.W * a.C * 2));
+  const int wave_u = __builtin_amdgcn_readfirstlane(wave);  // wave-uniform copy: scalar branches
+  const unsigned lds0 = __builtin_amdgcn_readfirstlane(lds_address(lds));
+
+  // ---- per-load addressing (each lane: one 16-byte chunk of one tile row) ----
+  const int rin = lane >> 3;           // row within the 8-row group
+  unsigned base[LPW];                  // byte offset at depth tile 0 (OOB if the row is outside the tensor)
+  int hi0[LPW], wi0[LPW];              // TILED / GENERIC: top-left input coordinate of the pixel
+  int chunk[LPW];                      // logical 16-byte chunk of the row this lane moves
 #pragma unroll
-  for (int i = 0; i < NX; ++i) {
-    int m = m0 + tid / CPR + RSTEP * i;
-    xvalid[i] = m < a.M;
-    int mm = xvalid[i] ? m : 0;
-    int wo = mm % a.Wo;
-    int t = mm / a.Wo;
-    int ho = t % a.Ho;
-    int n = t / a.Ho;
-    xbase[i] = n * a.H * a.W * a.C;
-    hi0[i] = ho * a.stride - a.pad;
-    wi0[i] = wo * a.stride - a.pad;
+  for (int i = 0; i < LPW; ++i) {
+    const int r = 8 * (wave * LPW + i) + rin;
+    const int c = (lane & 7) ^ ((r >> 1) & 7);
+    chunk[i] = c;
+    hi0[i] = 0;
+    wi0[i] = 0;
+    if (r < BN) {
+      const int n = n0 + r;
+      base[i] = n < a.K ? (unsigned)(((long)n * a.Kg + c * 8) * 2) : OOB;
+    } else {
+      const int m = m0 + r - BN;
+      if (m < a.M) {
+        const int t = a.div_wo.div(m);
+        const int wo = m - t * a.Wo;
+        const int nn = a.div_ho.div(t);
+        const int ho = t - nn * a.Ho;
+        if (MODE == MODE_1X1S1) {  // the output pixel is the input pixel
+          base[i] = (unsigned)(((long)m * a.C + c * 8) * 2);
+        } else if (MODE == MODE_1X1) {
+          base[i] = (unsigned)(((((long)nn * a.H + ho * a.stride) * a.W + wo * a.stride) * a.C + c * 8) * 2);
+        } else {
+          base[i] = (unsigned)((long)nn * a.H * a.W);  // image's first pixel
+          hi0[i] = ho * a.stride - a.pad;
+          wi0[i] = wo * a.stride - a.pad;
+        }
+      } else {
+        base[i] = OOB;
+      }
+    }
   }
 
   const int nkt_total = (a.Kg + BK - 1) / BK;
@@ -113,35 +233,46 @@ __global__ __launch_bounds__(256) void conv_igemm_kernel(ConvArgs a) {
     kt1 = min(nkt_total, kt0 + a.kt_per_split);
   }
 
-  bf16x8 wr[NW], xr[NX];
-  const bf16x8 zero8 = {};
-
-  auto load_tiles = [&](int kt) {
-    const int k = kt * BK + kc * 8;
-    const bool kin = k < a.Kg;
-#pragma unroll
-    for (int i = 0; i < NW; ++i) {
-      int n = n0 + tid / CPR + RSTEP * i;
-      wr[i] = (kin && n < a.K) ? *reinterpret_cast<const bf16x8*>(a.w + (long)n * a.Kg + k) : zero8;
+  // issue the direct-to-LDS loads of depth tile kt into stage `st`
+  auto issue = [&](int kt, int st) {
+    const int k0 = kt * BK;
+    int tr = 0, ts = 0, tc = 0;
+    if (MODE == MODE_TILED) {  // C % 64 == 0: the whole tile is inside one (r, s)
+      const int rs = a.div_c.div(k0);
+      tc = k0 - rs * a.C;
+      tr = a.div_s.div(rs);
+      ts = rs - tr * a.S;
     }
-    int rs = kin ? k / a.C : 0;
-    int c = k - rs * a.C;
-    int r = rs / a.S;
-    int s = rs - r * a.S;
+    const unsigned sb = lds0 + st * STAGE_BYTES;
 #pragma unroll
-    for (int i = 0; i < NX; ++i) {
-      int hi = hi0[i] + r, wi = wi0[i] + s;
-      bool ok = kin && xvalid[i] && (unsigned)hi < (unsigned)a.H && (unsigned)wi < (unsigned)a.W;
-      xr[i] = ok ? *reinterpret_cast<const bf16x8*>(a.x + xbase[i] + (hi * a.W + wi) * a.C + c) : zero8;
+    for (int i = 0; i < LPW; ++i) {
+      const int g = wave_u * LPW + i;  // wave-load index: rows 8g..8g+7 of the stage
+      const int k = k0 + chunk[i] * 8;
+      const bool kin = k < a.Kg;
+      if (g < BN / 8) {  // weight rows (scalar branch)
+        const unsigned off = (base[i] != OOB && kin) ? base[i] + (unsigned)(k0 * 2) : OOB;
+        load_to_lds16(wrs, off, sb + g * 1024);
+      } else {           // activation rows
+        unsigned off;
+        if (MODE == MODE_1X1 || MODE == MODE_1X1S1) {
+          off = (base[i] != OOB && kin) ? base[i] + (unsigned)(k0 * 2) : OOB;
+        } else {
+          int r, s, c;
+          if (MODE == MODE_TILED) {
+            r = tr; s = ts; c = tc + chunk[i] * 8;
+          } else {
+            const int rs = a.div_c.div(k);
+            c = k - rs * a.C;
+            r = a.div_s.div(rs);
+            s = rs - r * a.S;
+          }
+          const int hi = hi0[i] + r, wi = wi0[i] + s;
+          const bool ok = base[i] != OOB && kin && (unsigned)hi < (unsigned)a.H && (unsigned)wi < (unsigned)a.W;
+          off = ok ? (unsigned)(((base[i] + hi * a.W + wi) * a.C + c) * 2) : OOB;
+        }
+        load_to_lds16(xrs, off, sb + g * 1024);
+      }
     }
-  };
-  auto store_tiles = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < NW; ++i)
-      *reinterpret_cast<bf16x8*>(&lds[buf][(tid / CPR + RSTEP * i) * LDK + kc * 8]) = wr[i];
-#pragma unroll
-    for (int i = 0; i < NX; ++i)
-      *reinterpret_cast<bf16x8*>(&lds[buf][(BN + tid / CPR + RSTEP * i) * LDK + kc * 8]) = xr[i];
   };
 
   f32x4 acc[TN][TM];
@@ -150,55 +281,105 @@ __global__ __launch_bounds__(256) void conv_igemm_kernel(ConvArgs a) {
 #pragma unroll
     for (int j = 0; j < TM; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  if (kt0 < kt1) {
-    load_tiles(kt0);
-    store_tiles(0);
-  }
-  __syncthreads();
+  // fragment read addresses (bytes within a stage) for logical chunk `c` of row `r`
+  auto frag = [&](const unsigned char* sb, int r, int c) -> bf16x8 {
+    return *reinterpret_cast<const bf16x8*>(sb + r * ROW_BYTES + ((c ^ ((r >> 1) & 7)) << 4));
+  };
+  const int arow = wn * (BN / WN) + (lane & 15);
+  const int brow = BN + wm * (BM / WM) + (lane & 15);
+  const int cq = lane >> 4;
 
-  const int arow = wn * (BN / 2) + (lane & 15);
-  const int brow = BN + wm * (BM / 2) + (lane & 15);
-  const int koff = (lane >> 4) * 8;
+  // prologue: STAGES-1 tiles in flight
+#pragma unroll
+  for (int s = 0; s < STAGES - 1; ++s)
+    if (kt0 + s < kt1) issue(kt0 + s, s);
 
   for (int kt = kt0; kt < kt1; ++kt) {
-    const int buf = (kt - kt0) & 1;
-    const bool more = kt + 1 < kt1;
-    if (more) load_tiles(kt + 1);
+    const int st = (kt - kt0) % STAGES;
+    // tiles issued after kt that may stay in flight
+    const int after = min(STAGES - 2, kt1 - 1 - kt);
+    if (after >= 2)
+      wait_vmcnt<2 * LPW>();
+    else if (after == 1)
+      wait_vmcnt<LPW>();
+    else
+      wait_vmcnt<0>();
+    __syncthreads();  // every wave's part of tile kt is in LDS; every wave is done with tile kt-1
+    if (kt + STAGES - 1 < kt1) issue(kt + STAGES - 1, (kt - kt0 + STAGES - 1) % STAGES);
+    const unsigned char* sb = lds + st * STAGE_BYTES;
 #pragma unroll
-    for (int ks = 0; ks < BK; ks += 32) {
+    for (int ks = 0; ks < BK / 8; ks += 4) {
       bf16x8 af[TN], bfr[TM];
 #pragma unroll
-      for (int i = 0; i < TN; ++i)
-        af[i] = *reinterpret_cast<const bf16x8*>(&lds[buf][(arow + i * 16) * LDK + ks + koff]);
+      for (int i = 0; i < TN; ++i) af[i] = frag(sb, arow + i * 16, ks + cq);
 #pragma unroll
-      for (int j = 0; j < TM; ++j)
-        bfr[j] = *reinterpret_cast<const bf16x8*>(&lds[buf][(brow + j * 16) * LDK + ks + koff]);
+      for (int j = 0; j < TM; ++j) bfr[j] = frag(sb, brow + j * 16, ks + cq);
 #pragma unroll
       for (int i = 0; i < TN; ++i)
 #pragma unroll
         for (int j = 0; j < TM; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
     }
-    if (more) store_tiles(buf ^ 1);
-    __syncthreads();
   }
 
-  // epilogue: lane holds channels ch0..ch0+3 of pixel px for each (i, j) tile
+  // Epilogue through LDS: each lane holds channels ch..ch+3 of one pixel per
+  // MFMA tile, i.e. 8-byte pieces of 16 different pixel rows.  The fp32 tile
+  // is first written to LDS as [pixel][channel] (unpadded rows of BN floats,
+  // 16-byte units XOR-swizzled by pixel % 8), then consecutive threads take
+  // consecutive 4-channel groups of a pixel row, so residual reads and output
+  // writes cover whole row segments.
+  static_assert(BM * BN * 4 <= STAGES * STAGE_BYTES, "epilogue tile must fit in the stage ring");
+  static_assert(BN / 4 >= 8, "swizzle needs 8 units per row");
+  __syncthreads();  // all waves are done reading the last stage
+  float* ct = reinterpret_cast<float*>(lds);
+  auto cidx = [](int pl, int cl) { return pl * BN + ((((cl >> 2) ^ (pl & 7))) << 2); };
 #pragma unroll
   for (int i = 0; i < TN; ++i) {
-    const int ch0 = n0 + wn * (BN / 2) + i * 16 + (lane >> 4) * 4;
+    const int cl = wn * (BN / WN) + i * 16 + (lane >> 4) * 4;
 #pragma unroll
     for (int j = 0; j < TM; ++j) {
-      const int px = m0 + wm * (BM / 2) + j * 16 + (lane & 15);
-      if (px >= a.M || ch0 >= a.K) continue;
-      float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
-      if (SPLIT) {
-        float* p = a.partial + ((long)blockIdx.z * a.M + px) * a.K + ch0;
-        *reinterpret_cast<f32x4*>(p) = f32x4{v[0], v[1], v[2], v[3]};
-      } else {
-        epilogue4(a, OUT_F32, px, ch0, v);
-      }
+      const int pl = wm * (BM / WM) + j * 16 + (lane & 15);
+      *reinterpret_cast<f32x4*>(ct + cidx(pl, cl)) = acc[i][j];
     }
+  }
+  __syncthreads();
+  // thread -> fixed 4-channel group (256 is a multiple of the groups per row),
+  // ROWS_PT pixel rows; all residual loads are issued before any store
+  constexpr int G = BN / 4;
+  constexpr int RSTEP = 256 / G;
+  constexpr int ROWS_PT = BM / RSTEP;
+  static_assert(256 % G == 0 && BM % RSTEP == 0, "epilogue thread mapping");
+  const int cl = (tid % G) * 4;
+  const int ch0 = n0 + cl;
+  if (ch0 >= a.K) return;
+  const int pl0 = tid / G;
+  if (SPLIT) {
+#pragma unroll
+    for (int k = 0; k < ROWS_PT; ++k) {
+      const int pl = pl0 + k * RSTEP, px = m0 + pl;
+      if (px < a.M)
+        *reinterpret_cast<f32x4*>(a.partial + ((long)blockIdx.z * a.M + px) * a.K + ch0) =
+            *reinterpret_cast<const f32x4*>(ct + cidx(pl, cl));
+    }
+    return;
+  }
+  const f32x4 sc = a.scale ? *reinterpret_cast<const f32x4*>(a.scale + ch0) : f32x4{1.f, 1.f, 1.f, 1.f};
+  const f32x4 sh = a.shift ? *reinterpret_cast<const f32x4*>(a.shift + ch0) : f32x4{0.f, 0.f, 0.f, 0.f};
+  bf16x4 rv[ROWS_PT];
+#pragma unroll
+  for (int k = 0; k < ROWS_PT; ++k) {
+    const int px = m0 + pl0 + k * RSTEP;
+    rv[k] = (a.res && px < a.M) ? *reinterpret_cast<const bf16x4*>(a.res + (long)px * a.K + ch0) : bf16x4{};
+  }
+#pragma unroll
+  for (int k = 0; k < ROWS_PT; ++k) {
+    const int pl = pl0 + k * RSTEP, px = m0 + pl;
+    if (px >= a.M) continue;
+    const f32x4 t = *reinterpret_cast<const f32x4*>(ct + cidx(pl, cl));
+    float v[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) v[e] = apply_act(t[e] * sc[e] + sh[e] + (float)rv[k][e], a.act);
+    store_out4(a.y, OUT_F32, (long)px * a.K + ch0, v);
   }
 }
 
@@ -218,43 +399,65 @@ __global__ void splitk_reduce_kernel(ConvArgs a, int splits, int out_f32) {
   epilogue4(a, out_f32 != 0, px, ch0, v);
 }
 
-template <int BN, int BM>
-static void launch_cfg(const ConvArgs& a, bool f32, int splits, hipStream_t st) {
-  dim3 grid(ceil_div(a.M, BM), ceil_div(a.K, BN), splits);
-  if (splits > 1)
-    hipLaunchKernelGGL((conv_igemm_kernel<BN, BM, false, true>), grid, dim3(256), 0, st, a);
-  else if (f32)
-    hipLaunchKernelGGL((conv_igemm_kernel<BN, BM, true, false>), grid, dim3(256), 0, st, a);
-  else
-    hipLaunchKernelGGL((conv_igemm_kernel<BN, BM, false, false>), grid, dim3(256), 0, st, a);
-}
-
-// Split-K workspace: a grow-only device buffer per stream would be needed for
-// concurrent splits; the caller passes it through ConvArgs.partial instead.
 struct ConvPlan {
   int bn, bm, splits;
 };
 
 // Tile and split choice from the GEMM shape and the CUs of the partition.
+// With two LDS stages a 128x128 block takes 64 KB, so two or three blocks
+// share a CU and cover each other's load latency; the plan therefore aims at
+// two or more blocks per CU: smaller pixel tiles first, then split-K when the
+// reduction is deep enough (>= 4 depth tiles per slice).
 static ConvPlan choose_plan(int M, int K, int Kg, int n_cu) {
   ConvPlan p;
-  p.bn = K >= 128 ? 128 : (K >= 64 ? 64 : 32);
-  p.bm = (p.bn == 32) ? 256 : 128;
+  const long target = 2L * n_cu;
+  p.bn = K <= 32 ? 32 : (K <= 64 ? 64 : 128);
+  p.bm = 128;
   long tiles = (long)ceil_div(M, p.bm) * ceil_div(K, p.bn);
-  if (tiles < n_cu && p.bn == 128 && M <= 64 * n_cu) {
+  if (tiles < target && p.bn >= 64) {
     p.bm = 64;
     tiles = (long)ceil_div(M, p.bm) * ceil_div(K, p.bn);
   }
   p.splits = 1;
-  int nkt = ceil_div(Kg, BK);
-  // too few tiles to cover the partition and a deep reduction: split the depth
-  while (tiles * p.splits * 2 <= n_cu && nkt / (p.splits * 2) >= 4 && p.splits < 16) p.splits *= 2;
+  const int nkt = ceil_div(Kg, BK);
+  while (tiles * p.splits < target && nkt / (p.splits * 2) >= 4 && p.splits < 16) p.splits *= 2;
   return p;
 }
 
 size_t conv_splitk_workspace_bytes(int M, int K, int Kg, int n_cu) {
   ConvPlan p = choose_plan(M, K, Kg, n_cu);
   return p.splits > 1 ? (size_t)p.splits * M * K * sizeof(float) : 0;
+}
+
+#ifndef DS_CONV_STAGES
+#define DS_CONV_STAGES 2
+#endif
+
+template <int BN, int BM, int WN, int WM, int MODE>
+static void launch_mode(ConvArgs a, bool f32, int splits, hipStream_t st) {
+  constexpr int STAGES = DS_CONV_STAGES;
+  a.tiles_n = ceil_div(a.K, BN);
+  a.tiles = ceil_div(a.M, BM) * a.tiles_n;
+  a.div_tn = FastDiv::make(a.tiles_n);
+  dim3 grid(a.tiles, 1, splits);
+  if (splits > 1)
+    hipLaunchKernelGGL((conv_igemm_kernel<BN, BM, WN, WM, STAGES, MODE, false, true>), grid, dim3(256), 0, st, a);
+  else if (f32)
+    hipLaunchKernelGGL((conv_igemm_kernel<BN, BM, WN, WM, STAGES, MODE, true, false>), grid, dim3(256), 0, st, a);
+  else
+    hipLaunchKernelGGL((conv_igemm_kernel<BN, BM, WN, WM, STAGES, MODE, false, false>), grid, dim3(256), 0, st, a);
+}
+
+template <int BN, int BM, int WN, int WM>
+static void launch_cfg(const ConvArgs& a, int mode, bool f32, int splits, hipStream_t st) {
+  if (mode == MODE_1X1S1)
+    launch_mode<BN, BM, WN, WM, MODE_1X1S1>(a, f32, splits, st);
+  else if (mode == MODE_1X1)
+    launch_mode<BN, BM, WN, WM, MODE_1X1>(a, f32, splits, st);
+  else if (mode == MODE_TILED)
+    launch_mode<BN, BM, WN, WM, MODE_TILED>(a, f32, splits, st);
+  else
+    launch_mode<BN, BM, WN, WM, MODE_GENERIC>(a, f32, splits, st);
 }
 
 dstack_status launch_conv2d_ws(const bf16* x, int N, int H, int W, int C, const bf16* w, int K, int R, int S,
@@ -271,11 +474,19 @@ dstack_status launch_conv2d_ws(const bf16* x, int N, int H, int W, int C, const 
   a.Ho = out_dim(H, R, stride, pad);
   a.Wo = out_dim(W, S, stride, pad);
   DS_CHECK(a.Ho > 0 && a.Wo > 0, DSTACK_E_INVALID, "conv2d: empty output");
-  DS_CHECK((long)N * H * W * C < (1L << 31) && (long)N * a.Ho * a.Wo * K < (1L << 31) && (long)K * R * S * C < (1L << 31),
-           DSTACK_E_UNSUPPORTED, "conv2d: tensor too large for 32-bit indexing");
+  // buffer offsets are 32-bit with bit 31 reserved as the out-of-range marker
+  DS_CHECK((long)N * H * W * C * 2 < (1L << 31) && (long)N * a.Ho * a.Wo * K < (1L << 31) &&
+               (long)K * R * S * C * 2 < (1L << 31),
+           DSTACK_E_UNSUPPORTED, "conv2d: tensor too large for 31-bit byte offsets");
   a.M = N * a.Ho * a.Wo;
   a.Kg = R * S * C;
   a.act = act;
+  a.div_wo = FastDiv::make(a.Wo);
+  a.div_ho = FastDiv::make(a.Ho);
+  a.div_c = FastDiv::make(C);
+  a.div_s = FastDiv::make(S);
+  const bool one = R == 1 && S == 1 && pad == 0;
+  const int mode = one ? (stride == 1 ? MODE_1X1S1 : MODE_1X1) : (C % BK == 0 ? MODE_TILED : MODE_GENERIC);
   ConvPlan p = choose_plan(a.M, K, a.Kg, n_cu);
   if (p.splits > 1 && (splitk_ws == nullptr || splitk_bytes < (size_t)p.splits * a.M * K * sizeof(float)))
     p.splits = 1;
@@ -283,13 +494,16 @@ dstack_status launch_conv2d_ws(const bf16* x, int N, int H, int W, int C, const 
   a.kt_per_split = ceil_div(nkt, p.splits);
   p.splits = ceil_div(nkt, a.kt_per_split);  // no empty slices
   if (p.splits > 1) a.partial = splitk_ws;
-#define DS_CONV_CASE(BN_, BM_) \
-  if (p.bn == BN_ && p.bm == BM_) launch_cfg<BN_, BM_>(a, out_fp32, p.splits, st);
-  DS_CONV_CASE(128, 128)
-  else DS_CONV_CASE(128, 64)
-  else DS_CONV_CASE(64, 128)
-  else DS_CONV_CASE(32, 256)
-#undef DS_CONV_CASE
+  if (p.bn == 128 && p.bm == 128)
+    launch_cfg<128, 128, 2, 2>(a, mode, out_fp32, p.splits, st);
+  else if (p.bn == 128 && p.bm == 64)
+    launch_cfg<128, 64, 2, 2>(a, mode, out_fp32, p.splits, st);
+  else if (p.bn == 64 && p.bm == 128)
+    launch_cfg<64, 128, 2, 2>(a, mode, out_fp32, p.splits, st);
+  else if (p.bn == 64 && p.bm == 64)
+    launch_cfg<64, 64, 2, 2>(a, mode, out_fp32, p.splits, st);
+  else
+    launch_cfg<32, 128, 1, 4>(a, mode, out_fp32, p.splits, st);
   if (p.splits > 1) {
     long nq = (long)a.M * (K / 4);
     hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)((nq + 255) / 256)), dim3(256), 0, st, a, p.splits,

@@ -26,7 +26,7 @@ namespace dstack {
 namespace {
 
 constexpr double BN_EPS = 1e-5;
-constexpr size_t SPLITK_WS_BYTES = (size_t)128 * 128 * 128 * 4;
+constexpr size_t SPLITK_WS_BYTES = (size_t)32 << 20;
 
 struct Builder {
   Model& m;
@@ -479,8 +479,9 @@ dstack_status get_workspace(Model& m, int pid, int n_cu, Workspace** out) {
     offs.push_back(total);
     total += align256((size_t)e * m.max_batch * 2);
   }
-  // split-K partial sums: splits * tiles <= n_cu / 2 bounds a request by
-  // 128 CUs * one 128x128 fp32 tile; a shape asking for more runs unsplit
+  // split-K partial sums: a split plan stops doubling once splits * tiles
+  // reaches 2 * n_cu (so stays below 4 * 256 tiles of at most 128 x 64 fp32
+  // values = 32 MB); a shape asking for more runs unsplit
   size_t sk = 0;
   for (const Op& op : m.ops)
     if (op.kind == OP_CONV) sk = SPLITK_WS_BYTES;
@@ -524,11 +525,11 @@ void KernelTimer::before() {
   }
 }
 
-void KernelTimer::after(int kind, double flops, double bytes) {
+void KernelTimer::after(int kind, double flops, double bytes, int m, int n, int k) {
   hipEvent_t e;
   (void)hipEventCreate(&e);
   (void)hipEventRecord(e, st);
-  recs.push_back(Rec{kind, flops, bytes, pending, e});
+  recs.push_back(Rec{kind, flops, bytes, pending, e, m, n, k});
   pending = nullptr;
 }
 
@@ -560,7 +561,7 @@ dstack_status lstm_layer_run(const bf16* x, int T, int B, int I, int H, const bf
   if (s != DSTACK_OK) return s;
   if (timer)
     timer->after(KC_MFMA, 2.0 * T * B * I * 4.0 * H,
-                 (double)T * B * I * 2 + 4.0 * H * I * 2 + (double)T * B * 4 * H * 4);
+                 (double)T * B * I * 2 + 4.0 * H * I * 2 + (double)T * B * 4 * H * 4, T * B, 4 * H, I);
   for (int t = 0; t < T; ++t) {
     if (timer) timer->before();
     s = launch_lstm_step(gx + (size_t)t * B * 4 * H, w_hh, t ? h_bf16 + (size_t)(t - 1) * B * H : nullptr, c,
@@ -569,7 +570,8 @@ dstack_status lstm_layer_run(const bf16* x, int T, int B, int I, int H, const bf
     if (timer)
       timer->after(KC_LSTM, 2.0 * B * H * 4.0 * H,
                    4.0 * H * H * 2 + (double)B * H * 2 + (double)B * 4 * H * 4 + 2.0 * B * H * 4 + (double)B * H * 2 +
-                       (h_f32 ? (double)B * H * 4 : 0.0));
+                       (h_f32 ? (double)B * H * 4 : 0.0),
+                   B, 4 * H, H);
   }
   return DSTACK_OK;
 }
@@ -600,6 +602,7 @@ dstack_status forward(Model& m, int batch, const void* d_in, void* d_out, Worksp
     if (timer) timer->before();
     int kind = KC_GLUE;
     double fl = 0, by = 0;
+    int gm = 0, gn = 0, gk = 0;
     switch (op.kind) {
       case OP_PACK:
         s = launch_pack_c8(src, batch * op.H * op.W, op.C, (bf16*)dst, st);
@@ -614,6 +617,9 @@ dstack_status forward(Model& m, int batch, const void* d_in, void* d_out, Worksp
         kind = KC_MFMA;
         fl = conv_flops(op, batch);
         by = conv_bytes(op, batch);
+        gm = batch * op.Ho * op.Wo;
+        gn = op.K;
+        gk = op.R * op.S * op.C;
         break;
       case OP_DW:
         s = launch_dwconv3x3(src, batch, op.H, op.W, op.C, m.d_w + op.w_off, op.stride, f32 + op.scale_off,
@@ -640,7 +646,7 @@ dstack_status forward(Model& m, int batch, const void* d_in, void* d_out, Worksp
         break;
     }
     if (s != DSTACK_OK) return s;
-    if (timer) timer->after(kind, fl, by);
+    if (timer) timer->after(kind, fl, by, gm, gn, gk);
   }
   return DSTACK_OK;
 }

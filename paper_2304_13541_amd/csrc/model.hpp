@@ -110,12 +110,13 @@ struct KernelTimer {
     int kind;
     double flops, bytes;
     hipEvent_t a, b;
+    int m, n, k;
   };
   hipStream_t st;
   std::vector<Rec> recs;
   hipEvent_t pending = nullptr;
   void before();
-  void after(int kind, double flops, double bytes);
+  void after(int kind, double flops, double bytes, int m = 0, int n = 0, int k = 0);
   ~KernelTimer();
 };
 
