@@ -88,9 +88,11 @@ void dstack_partition_destroy(dstack_partition p);
 
 /* Probe (verification of the slot -> CU mapping): launches n_blocks
  * one-wave workgroups on the partition's stream; each records its hardware
- * XCC id and HW_ID register into host_out[2*i], host_out[2*i+1].  Blocks
+ * XCC id and HW_ID register into host_out[2*i], host_out[2*i+1].  With
+ * via_graph != 0 the launch is captured into a HIP graph and the graph is
+ * launched on the partition's stream (forward passes run that way).  Blocks
  * until done.  n_blocks in 1..65536; host_out holds 2*n_blocks words. */
-dstack_status dstack_probe_cu_ids(dstack_partition p, int n_blocks, uint32_t* host_out);
+dstack_status dstack_probe_cu_ids(dstack_partition p, int n_blocks, int via_graph, uint32_t* host_out);
 
 /* ------------------------------------------------------------------ */
 /* Models                                                              */

@@ -84,7 +84,7 @@ _SIGS = {
     "dstack_partition_query": ([_vp, ctypes.POINTER(_i), ctypes.POINTER(ctypes.c_uint32), ctypes.POINTER(_vp)], _i),
     "dstack_synchronize": ([_vp], _i),
     "dstack_partition_destroy": ([_vp], None),
-    "dstack_probe_cu_ids": ([_vp, _i, ctypes.POINTER(ctypes.c_uint32)], _i),
+    "dstack_probe_cu_ids": ([_vp, _i, _i, ctypes.POINTER(ctypes.c_uint32)], _i),
     "dstack_model_load": ([ctypes.c_char_p, _u64, ctypes.POINTER(_vp)], _i),
     "dstack_model_query": ([_vp, ctypes.POINTER(ModelInfo)], _i),
     "dstack_model_export_params": ([_vp, _i, _vp, _sz], _i),
@@ -169,9 +169,9 @@ class Partition:
     def synchronize(self):
         _check(lib().dstack_synchronize(self.h))
 
-    def probe_cu_ids(self, n_blocks=4096):
+    def probe_cu_ids(self, n_blocks=4096, via_graph=False):
         out = (ctypes.c_uint32 * (2 * n_blocks))()
-        _check(lib().dstack_probe_cu_ids(self.h, n_blocks, out))
+        _check(lib().dstack_probe_cu_ids(self.h, n_blocks, int(via_graph), out))
         return np.frombuffer(out, dtype=np.uint32).reshape(n_blocks, 2).copy()
 
     def destroy(self):

@@ -6,6 +6,7 @@
 #include <algorithm>
 #include <atomic>
 #include <cmath>
+#include <cstdlib>
 #include <cstring>
 #include <new>
 #include <string>
@@ -140,15 +141,31 @@ void dstack_partition_destroy(dstack_partition p) {
   delete p;
 }
 
-dstack_status dstack_probe_cu_ids(dstack_partition p, int n_blocks, uint32_t* host_out) {
+dstack_status dstack_probe_cu_ids(dstack_partition p, int n_blocks, int via_graph, uint32_t* host_out) {
   return guarded([&] {
     DS_CHECK(p && host_out, DSTACK_E_INVALID, "probe: null pointer");
     DS_CHECK(n_blocks >= 1 && n_blocks <= 65536, DSTACK_E_INVALID, "probe: n_blocks in 1..65536");
     uint32_t* d = nullptr;
     DS_HIP(hipMalloc(&d, (size_t)n_blocks * 8));
-    dstack_status s = launch_probe(d, n_blocks, p->stream);
+    dstack_status s = DSTACK_OK;
     hipError_t e = hipSuccess;
-    if (s == DSTACK_OK) e = hipStreamSynchronize(p->stream);
+    if (via_graph) {
+      hipGraph_t g = nullptr;
+      hipGraphExec_t ex = nullptr;
+      e = hipStreamBeginCapture(p->stream, hipStreamCaptureModeThreadLocal);
+      if (e == hipSuccess) {
+        s = launch_probe(d, n_blocks, p->stream);
+        e = hipStreamEndCapture(p->stream, &g);
+      }
+      if (s == DSTACK_OK && e == hipSuccess) e = hipGraphInstantiate(&ex, g, nullptr, nullptr, 0);
+      if (s == DSTACK_OK && e == hipSuccess) e = hipGraphLaunch(ex, p->stream);
+      if (e == hipSuccess && s == DSTACK_OK) e = hipStreamSynchronize(p->stream);
+      if (ex) (void)hipGraphExecDestroy(ex);
+      if (g) (void)hipGraphDestroy(g);
+    } else {
+      s = launch_probe(d, n_blocks, p->stream);
+    }
+    if (s == DSTACK_OK && e == hipSuccess) e = hipStreamSynchronize(p->stream);
     if (s == DSTACK_OK && e == hipSuccess) e = hipMemcpy(host_out, d, (size_t)n_blocks * 8, hipMemcpyDeviceToHost);
     (void)hipFree(d);
     if (s != DSTACK_OK) return s;
@@ -282,6 +299,16 @@ dstack_status check_batch(const Model& m, int batch) {
 // Workspace id 0 is reserved for knee sweeps, which run one partition at a
 // time and reuse a single workspace across fractions.
 constexpr int SWEEP_WS_ID = 0;
+constexpr size_t kMaxGraphsPerWorkspace = 32;
+
+// Forward passes are replayed as HIP graphs unless DSTACK_GRAPH=0.
+bool graphs_enabled() {
+  static const bool on = [] {
+    const char* v = std::getenv("DSTACK_GRAPH");
+    return !(v && v[0] == '0');
+  }();
+  return on;
+}
 
 dstack_status infer_impl(Model& m, int batch, const void* d_in, void* d_out, dstack_partition p, KernelTimer* timer,
                          int ws_id = -1) {
@@ -293,7 +320,35 @@ dstack_status infer_impl(Model& m, int batch, const void* d_in, void* d_out, dst
   if (s != DSTACK_OK) return s;
   BusyGuard g(ws->busy);
   DS_CHECK(g.ok, DSTACK_E_STATE, "infer: another call on this (model, partition) is in progress");
-  return forward(m, batch, d_in, d_out, *ws, p->n_cu, p->stream, timer);
+  if (timer || !graphs_enabled()) return forward(m, batch, d_in, d_out, *ws, p->n_cu, p->stream, timer);
+  // one forward = one graph launch: captured on first use of this key
+  const Workspace::GraphKey key{batch, d_in, d_out, p->n_cu};
+  auto it = ws->graphs.find(key);
+  if (it == ws->graphs.end()) {
+    DS_HIP(hipStreamBeginCapture(p->stream, hipStreamCaptureModeThreadLocal));
+    s = forward(m, batch, d_in, d_out, *ws, p->n_cu, p->stream, nullptr);
+    hipGraph_t graph = nullptr;
+    hipError_t e = hipStreamEndCapture(p->stream, &graph);
+    if (s != DSTACK_OK) {
+      if (graph) (void)hipGraphDestroy(graph);
+      return s;
+    }
+    if (e != hipSuccess) return hip_fail(e, "hipStreamEndCapture");
+    hipGraphExec_t exec = nullptr;
+    e = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
+    (void)hipGraphDestroy(graph);
+    if (e != hipSuccess) return hip_fail(e, "hipGraphInstantiate");
+    if (ws->graph_order.size() >= kMaxGraphsPerWorkspace) {  // evict the oldest capture
+      auto old = ws->graphs.find(ws->graph_order.front());
+      (void)hipGraphExecDestroy(old->second);
+      ws->graphs.erase(old);
+      ws->graph_order.erase(ws->graph_order.begin());
+    }
+    it = ws->graphs.emplace(key, exec).first;
+    ws->graph_order.push_back(key);
+  }
+  DS_HIP(hipGraphLaunch(it->second, p->stream));
+  return DSTACK_OK;
 }
 
 }  // namespace

@@ -454,6 +454,10 @@ dstack_status upload_weights(Model& m) {
   return DSTACK_OK;
 }
 
+Workspace::~Workspace() {
+  for (auto& kv : graphs) (void)hipGraphExecDestroy(kv.second);
+}
+
 Model::~Model() {
   for (auto& kv : ws)
     if (kv.second->base) (void)hipFree(kv.second->base);

@@ -64,6 +64,23 @@ struct Workspace {
   float* lstm_c = nullptr;
   bf16* lstm_h[2] = {nullptr, nullptr};
   std::atomic<bool> busy{false};
+  // captured forward passes, keyed by (batch, input, output, CUs of the
+  // partition); replayed with one hipGraphLaunch
+  struct GraphKey {
+    int batch;
+    const void* in;
+    void* out;
+    int n_cu;
+    bool operator<(const GraphKey& o) const {
+      if (batch != o.batch) return batch < o.batch;
+      if (in != o.in) return in < o.in;
+      if (out != o.out) return out < o.out;
+      return n_cu < o.n_cu;
+    }
+  };
+  std::map<GraphKey, hipGraphExec_t> graphs;
+  std::vector<GraphKey> graph_order;  // insertion order, for eviction
+  ~Workspace();
 };
 
 struct Model {

@@ -122,12 +122,13 @@ def test_model_info(env):
     assert m.info.max_batch == 32
 
 
-def test_partition_cu_mask_confines_kernels(env):
+@pytest.mark.parametrize("via_graph", [False, True])
+def test_partition_cu_mask_confines_kernels(env, via_graph):
     ds, gu, inputs, oracle, torch = env
     for off, n in [(0, 1), (5, 3), (0, 13), (0, 32), (20, 12)]:
         p = ds.Partition(slot_offset=off, n_slots=n)
         assert p.n_cu == 8 * n
-        ids = p.probe_cu_ids(4096)
+        ids = p.probe_cu_ids(4096, via_graph=via_graph)
         xcc = ids[:, 0] & 0xF
         hw = ids[:, 1]
         cus = {(int(a), int((h >> 13) & 7), int((h >> 12) & 1), int((h >> 8) & 15)) for a, h in zip(xcc, hw)}
@@ -160,6 +161,30 @@ def test_disjoint_partitions_concurrent_equal_sequential(env):
     pa.synchronize()
     pb.synchronize()
     assert torch.equal(ya1, ya2) and torch.equal(yb1, yb2)
+
+
+@pytest.mark.parametrize("arch,batch,fraction", [("mobilenetv2", 4, 0.25), ("resnet50", 2, 0.5), ("lstm2", 3, 0.3)])
+def test_graph_replays_equal_eager(env, arch, batch, fraction):
+    """dstack_infer replays a captured graph; dstack_profile_layers runs the
+    same kernels eagerly.  Every replay, with eager work and synchronisation
+    in between, must equal the eager result bit for bit."""
+    ds, gu, inputs, oracle, torch = env
+    m = ds.Model(arch, 21)
+    p = ds.Partition(fraction)
+    xb = inputs.sequence_batch(5, batch) if arch == "lstm2" else inputs.image_batch(5, batch)
+    x = gu.dev_bf16(xb)
+    y_eager = gu.empty_f32(m.output_shape(batch))
+    m.profile_layers(batch, x, y_eager, p)
+    ref = y_eager.clone()
+    y = gu.empty_f32(m.output_shape(batch))
+    for rep in range(4):
+        y.fill_(float("nan"))
+        torch.cuda.synchronize()
+        m.infer(batch, x, y, p)
+        p.synchronize()
+        assert torch.equal(y, ref), (arch, rep)
+        m.profile_layers(batch, x, y_eager, p)  # eager work between replays
+        assert torch.equal(y_eager, ref)
 
 
 def test_knee_sweep_tiny(env):
