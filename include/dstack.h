@@ -255,6 +255,54 @@ dstack_status dstack_schedule(const dstack_sched_model* models, int n_models, co
                               dstack_schedule_out* out);
 
 /* ------------------------------------------------------------------ */
+/* Launcher simulation (Sec. 6.1.2: fair, opportunistic, dynamic fill)  */
+/* ------------------------------------------------------------------ */
+/* Runs the dstack_schedule plan every period for duration_us against a
+ * virtual integer-us clock whose job durations come from the timing table,
+ * with per-model request queues fed by the arrival traces.
+ *  - A planned job takes up to the model's batch of the oldest queued
+ *    requests (none queued: it does not run) and lasts its planned time.
+ *  - With fod != 0, every arrival and every completion triggers one FOD
+ *    pass: candidates are models with no running job and a non-empty queue,
+ *    ordered by runs in the last sessions_window sessions (session = t /
+ *    period), then cumulative busy us, then index; the first that fits
+ *    starts on the lowest-numbered free slots (its deployed count) with the
+ *    largest batch of {1,2,4,8,16,32} that is <= max_batch, <= queued and
+ *    whose latency ends before the next planned start (at or after now) that
+ *    touches those slots or its own next planned start.  At most one FOD
+ *    start per pass.
+ *  - Same-instant events: completions, then planned starts, then arrivals
+ *    (each by model index, then issue order).
+ *  - No job starts at or after duration_us.  Served requests with
+ *    completion - arrival > SLO and requests still queued when the last
+ *    started job ends both count as violations.
+ * arrivals_us[i] must be sorted and inside [0, duration_us).  job_hash is
+ * FNV-1a (64-bit) over (start, model, batch, slot mask, duration, kind) of
+ * every started job, kind 0 planned / 1 FOD, each as 8 little-endian bytes. */
+typedef struct {
+  int64_t duration_us;
+  int fod;
+  int sessions_window;                          /* 10 */
+  const int64_t* arrivals_us[DSTACK_MAX_MODELS];
+  int n_arrivals[DSTACK_MAX_MODELS];
+} dstack_sim_params;
+
+typedef struct {
+  int64_t served, violations, unserved, planned_runs, fod_runs, busy_us, p50_us, p99_us;
+} dstack_model_stats;
+
+typedef struct {
+  int n_models;
+  dstack_model_stats models[DSTACK_MAX_MODELS];
+  int64_t utilisation_ppm;                      /* floor(1e6 * slot-us inside [0, duration) / (total * duration)) */
+  uint64_t job_hash;
+  int64_t last_end_us;
+} dstack_run_out;
+
+dstack_status dstack_simulate(const dstack_sched_model* models, int n_models, const dstack_sched_params* params,
+                              const dstack_sim_params* sim, dstack_run_out* out);
+
+/* ------------------------------------------------------------------ */
 /* Kernel-level entry points (the layers of Sec. 4.1's A.int table)     */
 /* ------------------------------------------------------------------ */
 /* All pointers are device pointers; `stream` is a hipStream_t (NULL = the

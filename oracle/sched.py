@@ -246,3 +246,180 @@ def schedule(models, period, total=TOTAL_SLOTS, overprov=OVERPROVISION_SLOTS):
     jobs = plan(pms, period, total)
     ok = all(c.feasible for c in choices) and not any(j.missed for j in jobs)
     return choices, jobs, utilisation_ppm(jobs, period, total), ok
+
+
+# ---------------------------------------------------------------------------
+# Launcher simulation: the session plan repeated every period, plus the fair,
+# opportunistic, dynamic (FOD) fill of Sec. 6.1.2, on a virtual integer-us
+# clock driven by the timing table (a TimingTable-driven stand-in for the GPU).
+#
+# Readings (restated in the design notes):
+# * planned job (model i, start p*T + st): takes up to b_i of the oldest
+#   queued requests; with none queued it does not run; it runs for the
+#   planned duration;
+# * FOD is triggered by every request arrival and every job completion; the
+#   candidates are models with no running job and >= 1 queued request,
+#   ordered by (runs in the current and previous 9 sessions, cumulative busy
+#   us, model index) -- "fewest runs" (Sec. 6.1.2) then "least time" (Sec. 6.3);
+#   the first candidate that fits is launched (at most one per trigger):
+#   it takes the lowest-numbered s_i slots free now (s_i = its deployed
+#   slots); its gap ends at the first planned start at or after now whose
+#   slots meet them, or at its own model's next planned start (a planned job
+#   at this very instant may not have been processed yet); its batch is the largest
+#   b in {1,2,4,8,16,32} with b <= max_batch, b <= queued and L(b, s_i) <= gap;
+# * events at one instant: completions, then planned starts, then arrivals
+#   (each group by model, then by issue order); FOD runs after each
+#   completion and each arrival;
+# * a served request violates its SLO if completion - arrival > SLO; no job
+#   starts at or after the end of the trace, and requests still queued when
+#   the last started job ends are unserved (also violations); utilisation
+#   counts slot-time inside [0, duration);
+# * runs/busy time are charged at job start; the session of time t is t // T.
+# ---------------------------------------------------------------------------
+
+FNV_OFFSET = 0xcbf29ce484222325
+FNV_PRIME = 0x100000001b3
+
+
+def _fnv(h, v):
+    v &= (1 << 64) - 1
+    for i in range(8):
+        h ^= (v >> (8 * i)) & 0xff
+        h = (h * FNV_PRIME) & ((1 << 64) - 1)
+    return h
+
+
+def _nearest_rank(sorted_vals, pct):
+    if not sorted_vals:
+        return 0
+    k = max(1, -(-pct * len(sorted_vals) // 100))
+    return sorted_vals[k - 1]
+
+
+def simulate(models, period, duration, arrivals, total=TOTAL_SLOTS, overprov=OVERPROVISION_SLOTS, fod=True,
+             sessions_window=10):
+    """models: as for schedule(); arrivals: per model sorted list of integer us in [0, duration).
+    Returns dict with per-model counters, utilisation_ppm and a hash of the job log."""
+    import collections
+    import heapq
+    choices, jobs, _, _ = schedule(models, period, total, overprov)
+    n = len(models)
+    dep = [deployed_slots(c.slots, overprov, total) for c in choices]
+    planned = [j for j in jobs if not j.missed]
+    # next planned start of each model after time t (over all periods)
+    n_periods = ceil_div(duration, period)
+
+    def lat(i, b, s):
+        row = models[i]["table"].get(b)
+        return latency_at(row, s) if row else None
+
+    # events: (time, kind, model, seq, payload); kind 0 completion, 1 planned start, 2 arrival
+    ev = []
+    seq = 0
+    for p in range(n_periods):
+        for j in planned:
+            t = p * period + j.start
+            if t < duration:
+                heapq.heappush(ev, (t, 1, j.model, seq, (j.slot_mask, j.duration)))
+                seq += 1
+    for i in range(n):
+        for a in arrivals[i]:
+            heapq.heappush(ev, (a, 2, i, seq, None))
+            seq += 1
+    planned_starts = sorted((p * period + j.start, j.model, j.slot_mask) for p in range(n_periods)
+                            for j in planned if p * period + j.start < duration)
+
+    queue = [collections.deque() for _ in range(n)]
+    running = {}  # model -> (end, mask)
+    used = 0
+    runs = [collections.Counter() for _ in range(n)]
+    busy = [0] * n
+    served = [0] * n
+    late = [0] * n
+    lats = [[] for _ in range(n)]
+    planned_runs = [0] * n
+    fod_runs = [0] * n
+    slot_us = 0
+    h = FNV_OFFSET
+    last_end = 0
+    log = []
+
+    def start_job(t, i, mask, dur, b, kind):
+        nonlocal used, seq, slot_us, h, last_end
+        reqs = [queue[i].popleft() for _ in range(b)]
+        running[i] = (t + dur, mask)
+        used |= mask
+        heapq.heappush(ev, (t + dur, 0, i, seq, reqs))
+        seq += 1
+        runs[i][t // period] += 1
+        busy[i] += dur
+        slot_us += bin(mask).count("1") * (min(t + dur, duration) - t)
+        last_end = max(last_end, t + dur)
+        for v in (t, i, b, mask, dur, kind):
+            h = _fnv(h, v)
+        log.append((t, t + dur, i, mask, kind, b))
+        if kind == 0:
+            planned_runs[i] += 1
+        else:
+            fod_runs[i] += 1
+
+    def fod_pass(t):
+        if t >= duration:  # nothing starts once the trace has ended
+            return
+        cands = [i for i in range(n) if i not in running and queue[i]]
+        cur = t // period
+        cands.sort(key=lambda i: (sum(runs[i][s] for s in range(cur - sessions_window + 1, cur + 1)), busy[i], i))
+        for i in cands:
+            s = dep[i]
+            free = [sid for sid in range(total) if not (used >> sid) & 1]
+            if len(free) < s:
+                continue
+            mask = 0
+            for sid in free[:s]:
+                mask |= 1 << sid
+            gap = None
+            for (ps, pm, pmask) in planned_starts:
+                if ps >= t and ((pmask & mask) or pm == i):
+                    gap = ps - t
+                    break
+            best = None
+            for b in BATCH_GRID:
+                if b > models[i]["max_batch"] or b > len(queue[i]):
+                    continue
+                L = lat(i, b, s)
+                if L is None or (gap is not None and L > gap):
+                    continue
+                best = (b, L)
+            if best is None:
+                continue
+            start_job(t, i, mask, best[1], best[0], 1)
+            return
+
+    while ev:
+        t, kind, i, _, payload = heapq.heappop(ev)
+        if kind == 0:
+            end, mask = running.pop(i)
+            used &= ~mask
+            for a in payload:
+                served[i] += 1
+                lats[i].append(t - a)
+                if t - a > models[i]["slo_us"]:
+                    late[i] += 1
+            if fod:
+                fod_pass(t)
+        elif kind == 1:
+            mask, dur = payload
+            if queue[i] and i not in running:
+                start_job(t, i, mask, dur, min(choices[i].batch, len(queue[i])), 0)
+        else:
+            queue[i].append(t)
+            if fod:
+                fod_pass(t)
+    out = []
+    for i in range(n):
+        L = sorted(lats[i])
+        out.append(dict(served=served[i], violations=late[i] + len(queue[i]), unserved=len(queue[i]),
+                        planned_runs=planned_runs[i], fod_runs=fod_runs[i], busy_us=busy[i],
+                        p50_us=_nearest_rank(L, 50), p99_us=_nearest_rank(L, 99)))
+    return dict(models=out, utilisation_ppm=slot_us * 1000000 // (total * max(duration, 1)), job_hash=h,
+                last_end_us=last_end, log=log)

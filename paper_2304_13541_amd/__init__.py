@@ -71,6 +71,21 @@ class ScheduleOut(ctypes.Structure):
                 ("n_jobs", ctypes.c_int), ("jobs", Job * MAX_JOBS), ("utilisation_ppm", ctypes.c_int64)]
 
 
+class SimParams(ctypes.Structure):
+    _fields_ = [("duration_us", ctypes.c_int64), ("fod", ctypes.c_int), ("sessions_window", ctypes.c_int),
+                ("arrivals_us", ctypes.POINTER(ctypes.c_int64) * MAX_MODELS), ("n_arrivals", ctypes.c_int * MAX_MODELS)]
+
+
+class ModelStats(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int64) for n in ("served", "violations", "unserved", "planned_runs", "fod_runs",
+                                               "busy_us", "p50_us", "p99_us")]
+
+
+class RunOut(ctypes.Structure):
+    _fields_ = [("n_models", ctypes.c_int), ("models", ModelStats * MAX_MODELS), ("utilisation_ppm", ctypes.c_int64),
+                ("job_hash", ctypes.c_uint64), ("last_end_us", ctypes.c_int64)]
+
+
 _lib = None
 _vp, _i, _d, _u64, _sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_double, ctypes.c_uint64, ctypes.c_size_t
 _fp = ctypes.POINTER(ctypes.c_float)
@@ -94,6 +109,8 @@ _SIGS = {
     "dstack_profile_layers": ([_vp, _i, _vp, _vp, _vp, ctypes.POINTER(LayerTime), _i, ctypes.POINTER(_i)], _i),
     "dstack_knee_sweep": ([_vp, _i, ctypes.POINTER(_d), _i, _i, _i, ctypes.POINTER(KneeResult)], _i),
     "dstack_schedule": ([ctypes.POINTER(SchedModel), _i, ctypes.POINTER(SchedParams), ctypes.POINTER(ScheduleOut)], _i),
+    "dstack_simulate": ([ctypes.POINTER(SchedModel), _i, ctypes.POINTER(SchedParams), ctypes.POINTER(SimParams),
+                         ctypes.POINTER(RunOut)], _i),
     "dstack_op_conv2d": ([_vp, _i, _i, _i, _i, _vp, _i, _i, _i, _i, _i, _vp, _vp, _vp, _i, _vp, _i, _vp], _i),
     "dstack_op_dwconv3x3": ([_vp, _i, _i, _i, _i, _vp, _i, _vp, _vp, _i, _vp, _vp], _i),
     "dstack_op_fc": ([_vp, _i, _i, _vp, _vp, _i, _i, _vp, _i, _vp], _i),
@@ -257,6 +274,52 @@ def generate_params(arch, seed, idx):
     _check(lib().dstack_generate_params(arch.encode(), ctypes.c_uint64(seed), idx, out.ctypes.data, out.nbytes,
                                         ctypes.byref(n)))
     return out
+
+
+def _sched_models(models):
+    arr = (SchedModel * len(models))()
+    for i, m in enumerate(models):
+        e = arr[i]
+        e.slo_us = m["slo_us"]
+        e.max_batch = m["max_batch"]
+        e.rate_per_s = m.get("rate_per_s", 0)
+        batches = sorted(m["table"])
+        slots = sorted({s for b in batches for s in m["table"][b]})
+        e.n_batches = len(batches)
+        e.n_slots = len(slots)
+        for q, b in enumerate(batches):
+            e.batches[q] = b
+            for r, s in enumerate(slots):
+                e.latency_us[q][r] = m["table"][b].get(s, 0)
+        for r, s in enumerate(slots):
+            e.slots[r] = s
+    return arr
+
+
+def _stats(out):
+    return [dict((f, getattr(out.models[i], f)) for f, _ in ModelStats._fields_) for i in range(out.n_models)]
+
+
+def simulate(models, period_us, duration_us, arrivals, total_slots=TOTAL_SLOTS, overprov_slots=2, fod=True,
+             sessions_window=10):
+    """Launcher simulation on the timing table (see dstack_simulate).
+    arrivals: per model sorted integer-us arrival times.  Returns a dict."""
+    arr = _sched_models(models)
+    sp = SimParams()
+    sp.duration_us = duration_us
+    sp.fod = int(fod)
+    sp.sessions_window = sessions_window
+    keep = []
+    for i, a in enumerate(arrivals):
+        buf = (ctypes.c_int64 * max(1, len(a)))(*a)
+        keep.append(buf)
+        sp.arrivals_us[i] = ctypes.cast(buf, ctypes.POINTER(ctypes.c_int64))
+        sp.n_arrivals[i] = len(a)
+    out = RunOut()
+    _check(lib().dstack_simulate(arr, len(models), ctypes.byref(SchedParams(period_us, total_slots, overprov_slots)),
+                                 ctypes.byref(sp), ctypes.byref(out)))
+    return dict(models=_stats(out), utilisation_ppm=out.utilisation_ppm, job_hash=out.job_hash,
+                last_end_us=out.last_end_us)
 
 
 def schedule(models, period_us, total_slots=TOTAL_SLOTS, overprov_slots=2):

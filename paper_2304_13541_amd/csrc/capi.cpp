@@ -460,6 +460,11 @@ dstack_status dstack_schedule(const dstack_sched_model* models, int n, const dst
   return guarded([&] { return schedule(models, n, prm, out); });
 }
 
+dstack_status dstack_simulate(const dstack_sched_model* models, int n, const dstack_sched_params* prm,
+                              const dstack_sim_params* sim, dstack_run_out* out) {
+  return guarded([&] { return simulate(models, n, prm, sim, out); });
+}
+
 // ----------------------------------------------------- kernel-level ops ----
 
 dstack_status dstack_op_conv2d(const void* x, int N, int H, int W, int C, const void* w, int K, int R, int S,

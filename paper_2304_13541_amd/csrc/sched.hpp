@@ -10,5 +10,7 @@ bool eta_greater(int64_t b1, int64_t L1, int64_t s1, int64_t b2, int64_t L2, int
 int knee_index(int b, const int64_t* lat, const int* slots, int n);
 dstack_status schedule(const dstack_sched_model* models, int n, const dstack_sched_params* prm,
                        dstack_schedule_out* out);
+dstack_status simulate(const dstack_sched_model* models, int n, const dstack_sched_params* prm,
+                       const dstack_sim_params* sim, dstack_run_out* out);
 
 }  // namespace dstack

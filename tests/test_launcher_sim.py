@@ -1,0 +1,118 @@
+"""Launcher simulation (Sec. 6.1.2 FOD fill on the session plan): the library's
+dstack_simulate against the scheduler oracle's simulate(), bit-exact, on
+random timing tables and Poisson traces and on the four-model workload shape
+(ResNet-50, MobileNetV2, VGG-19, LSTM at 400/800/150/300 req/s, SLOs
+25/15/50/30 ms, 100 ms sessions, 10 s)."""
+import random
+
+import pytest
+
+import paper_2304_13541_amd as ds
+from oracle import sched
+from tests.inputs import poisson_arrivals
+
+SWEEP = [3, 6, 10, 13, 16, 19, 22, 26, 29, 32]
+
+
+def amdahl(a, c, batches, slots=SWEEP):
+    return {b: {s: int(a * (1 + 0.05 * b) + c * b / s) for s in slots} for b in batches}
+
+
+def compare(models, period, duration, arrivals, total=32, overprov=2, fod=True):
+    got = ds.simulate(models, period, duration, arrivals, total, overprov, fod)
+    ref = sched.simulate(models, period, duration, arrivals, total, overprov, fod)
+    assert got["models"] == ref["models"]
+    assert got["utilisation_ppm"] == ref["utilisation_ppm"]
+    assert got["last_end_us"] == ref["last_end_us"]
+    assert got["job_hash"] == ref["job_hash"]
+    for i, m in enumerate(got["models"]):
+        assert m["served"] + m["unserved"] == len(arrivals[i])
+        assert m["violations"] >= m["unserved"]
+    return got
+
+
+def four_model_mix(scale=1):
+    rates = [400 * scale, 800 * scale, 150 * scale, 300 * scale]
+    slos = [25000, 15000, 50000, 30000]
+    tables = [amdahl(300, 9000, [1, 2, 4, 8, 16]), amdahl(250, 3000, [1, 2, 4, 8, 16, 32]),
+              amdahl(600, 40000, [1, 2, 4, 8]), amdahl(2500, 1500, [1, 2, 4, 8, 16, 32])]
+    bmax = [16, 32, 8, 32]
+    models = [dict(slo_us=s, max_batch=b, rate_per_s=r, table=t) for s, b, r, t in zip(slos, bmax, rates, tables)]
+    arrivals = [poisson_arrivals(2026 + i, r, 10_000_000) for i, r in enumerate(rates)]
+    return models, arrivals
+
+
+@pytest.mark.parametrize("fod", [True, False])
+def test_four_model_mix_parity(fod):
+    models, arrivals = four_model_mix()
+    got = compare(models, 100000, 10_000_000, arrivals, fod=fod)
+    if fod:
+        assert sum(m["fod_runs"] for m in got["models"]) > 0
+
+
+def test_four_model_mix_heavy_load_parity():
+    models, arrivals = four_model_mix(scale=8)
+    compare(models, 100000, 10_000_000, arrivals)
+
+
+def test_random_parity():
+    rnd = random.Random(7)
+    for trial in range(60):
+        n = rnd.randint(1, 4)
+        models, arrivals = [], []
+        for i in range(n):
+            batches = sorted(rnd.sample([1, 2, 4, 8, 16, 32], rnd.randint(1, 4)))
+            tab = amdahl(rnd.randint(100, 3000), rnd.randint(500, 40000), batches,
+                         sorted(rnd.sample(range(1, 33), rnd.randint(2, 8))))
+            models.append(dict(slo_us=rnd.choice([10000, 15000, 25000, 30000, 50000]), max_batch=rnd.choice([4, 16, 32]),
+                               rate_per_s=rnd.choice([0, 200, 800]), table=tab))
+            arrivals.append(poisson_arrivals(trial * 10 + i, rnd.choice([50, 300, 1500]), 1_000_000))
+        compare(models, rnd.choice([50000, 100000]), 1_000_000, arrivals, overprov=rnd.choice([0, 2]),
+                fod=rnd.random() < 0.8)
+
+
+def test_fod_raises_utilisation_paper_models():
+    """Sec. 6.1.2: opportunistic fill raises utilisation over the ST-only plan
+    (the paper's example goes from 60% to 74%).  Paper table (10% slot units),
+    requests always waiting."""
+    models = [dict(slo_us=25000, max_batch=16, table={16: {3: 8000}}),
+              dict(slo_us=50000, max_batch=16, table={16: {4: 28000}}),
+              dict(slo_us=100000, max_batch=16, table={16: {5: 55000}})]
+    dense = [list(range(0, 1_000_000, 200)) for _ in range(3)]
+    st_only = sched.simulate(models, 100000, 1_000_000, dense, total=10, overprov=0, fod=False)
+    with_fod = compare(models, 100000, 1_000_000, dense, total=10, overprov=0, fod=True)
+    # the ST-only plan (59.5%) every period, except that the two jobs planned at
+    # t = 0 (Alexnet 3 x 8 ms, ResNet-50 4 x 28 ms) find an empty queue
+    lost = (3 * 8000 + 4 * 28000) * 1_000_000 // (10 * 1_000_000)
+    assert st_only["utilisation_ppm"] == 595000 - lost
+    assert with_fod["utilisation_ppm"] > st_only["utilisation_ppm"]
+    print("utilisation ST-only %.1f%%, with FOD %.1f%%" % (st_only["utilisation_ppm"] / 1e4,
+                                                          with_fod["utilisation_ppm"] / 1e4))
+
+
+def test_simulate_rejects_bad_traces():
+    models = [dict(slo_us=25000, max_batch=16, table={1: {4: 1000}})]
+    with pytest.raises(ds.DStackError):
+        ds.simulate(models, 100000, 1_000_000, [[5, 3]])
+    with pytest.raises(ds.DStackError):
+        ds.simulate(models, 100000, 1_000_000, [[1_000_000]])
+
+
+def test_simulation_invariants():
+    """No instant has two running jobs on one slot or more slots than exist;
+    nothing starts after the trace; each model runs one job at a time."""
+    for scale in (1, 8):
+        models, arrivals = four_model_mix(scale)
+        r = sched.simulate(models, 100000, 10_000_000, arrivals)
+        log = sorted(r["log"])
+        for t0, t1, i, mask, kind, b in log:
+            assert t0 < 10_000_000 and t1 > t0 and 1 <= b <= models[i]["max_batch"]
+            assert mask and mask < (1 << 32)
+        points = sorted({j[0] for j in log})
+        for t in points:
+            act = [j for j in log if j[0] <= t < j[1]]
+            acc = 0
+            for j in act:
+                assert acc & j[3] == 0
+                acc |= j[3]
+            assert len({j[2] for j in act}) == len(act)
