@@ -316,21 +316,26 @@ dstack_status dstack_simulate(const dstack_sched_model* models, int n_models, co
  * dwconv3x3: per-channel 3x3, pad 1, stride 1 or 2, w [3][3][C] (device
  *   layout), then scale/shift and act; C % 8 == 0.
  * fc: y[b][o] = act(sum_i x[b][i] * w[o][i] + bias[o]); batch 1..32,
- *   I % 8 == 0; out_fp32 selects fp32 output.
+ *   I % 8 == 0; out_fp32 selects fp32 output.  workspace (device, may be
+ *   NULL) holds fp32 partial sums when the depth I is split over several
+ *   blocks: fc_workspace_bytes(B, I, O) bytes give the split chosen for the
+ *   whole GPU; NULL or fewer bytes run fewer splits (same result up to fp32
+ *   summation order).
  * maxpool: k x k window, stride, pad (padding never wins); C % 8 == 0.
  * avgpool: global mean over H x W, fp32 accumulate, bf16 out; C % 8 == 0.
  * lstm_layer: one LSTM layer over T steps (gate order i, f, g, o; h0 = c0
  *   = 0); x [T][B][I] bf16; w_ih [4H][I], w_hh [4H][H] bf16; bias [4H]
  *   fp32 (= b_ih + b_hh); h_bf16 [T][B][H] receives h rounded to bf16;
  *   h_f32 [T][B][H] (may be NULL) receives h in fp32; B in 1..32,
- *   H % 16 == 0, I % 8 == 0; workspace needs lstm_workspace_bytes. */
+ *   H % 32 == 0 and H <= 2048, I % 8 == 0; workspace needs lstm_workspace_bytes. */
 dstack_status dstack_op_conv2d(const void* x, int N, int H, int W, int C, const void* w, int K, int R, int S,
                                int stride, int pad, const float* scale, const float* shift, const void* res, int act,
                                void* y, int out_fp32, void* stream);
 dstack_status dstack_op_dwconv3x3(const void* x, int N, int H, int W, int C, const void* w, int stride,
                                   const float* scale, const float* shift, int act, void* y, void* stream);
+size_t dstack_fc_workspace_bytes(int B, int I, int O);
 dstack_status dstack_op_fc(const void* x, int B, int I, const void* w, const float* bias, int O, int act, void* y,
-                           int out_fp32, void* stream);
+                           int out_fp32, void* workspace, size_t workspace_bytes, void* stream);
 dstack_status dstack_op_maxpool(const void* x, int N, int H, int W, int C, int k, int stride, int pad, void* y,
                                 void* stream);
 dstack_status dstack_op_avgpool(const void* x, int N, int H, int W, int C, void* y, void* stream);

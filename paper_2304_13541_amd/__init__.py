@@ -113,7 +113,8 @@ _SIGS = {
                          ctypes.POINTER(RunOut)], _i),
     "dstack_op_conv2d": ([_vp, _i, _i, _i, _i, _vp, _i, _i, _i, _i, _i, _vp, _vp, _vp, _i, _vp, _i, _vp], _i),
     "dstack_op_dwconv3x3": ([_vp, _i, _i, _i, _i, _vp, _i, _vp, _vp, _i, _vp, _vp], _i),
-    "dstack_op_fc": ([_vp, _i, _i, _vp, _vp, _i, _i, _vp, _i, _vp], _i),
+    "dstack_fc_workspace_bytes": ([_i, _i, _i], _sz),
+    "dstack_op_fc": ([_vp, _i, _i, _vp, _vp, _i, _i, _vp, _i, _vp, _sz, _vp], _i),
     "dstack_op_maxpool": ([_vp, _i, _i, _i, _i, _i, _i, _i, _vp, _vp], _i),
     "dstack_op_avgpool": ([_vp, _i, _i, _i, _i, _vp, _vp], _i),
     "dstack_lstm_workspace_bytes": ([_i, _i, _i], _sz),
@@ -375,10 +376,17 @@ def dwconv3x3(x, w_rsc, stride, scale, shift, act, y, stream=None):
                                      _ptr(y), _stream(stream)))
 
 
-def fc(x, w, bias, act, y, out_fp32=False, stream=None):
+def fc_workspace_bytes(B, I, O):
+    return lib().dstack_fc_workspace_bytes(B, I, O)
+
+
+def fc(x, w, bias, act, y, out_fp32=False, workspace=None, stream=None):
+    """workspace: optional device buffer for the depth split's partial sums."""
     B, I = x.shape
     O = w.shape[0]
-    _check(lib().dstack_op_fc(_ptr(x), B, I, _ptr(w), _ptr(bias), O, act, _ptr(y), int(out_fp32), _stream(stream)))
+    wsb = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    _check(lib().dstack_op_fc(_ptr(x), B, I, _ptr(w), _ptr(bias), O, act, _ptr(y), int(out_fp32), _ptr(workspace),
+                              wsb, _stream(stream)))
 
 
 def maxpool(x, k, stride, pad, y, stream=None):

@@ -488,13 +488,18 @@ dstack_status dstack_op_dwconv3x3(const void* x, int N, int H, int W, int C, con
   });
 }
 
+size_t dstack_fc_workspace_bytes(int B, int I, int O) {
+  if (B < 1 || I < 1 || O < 1) return 0;
+  return fc_workspace_bytes(B, I, O, 256);
+}
+
 dstack_status dstack_op_fc(const void* x, int B, int I, const void* w, const float* bias, int O, int act, void* y,
-                           int out_fp32, void* stream) {
+                           int out_fp32, void* workspace, size_t workspace_bytes, void* stream) {
   return guarded([&] {
     DS_CHECK(x && w && y, DSTACK_E_INVALID, "fc: null pointer");
     DS_CHECK(act >= 0 && act <= 2, DSTACK_E_INVALID, "fc: act must be 0, 1 or 2");
     return launch_fc(static_cast<const bf16*>(x), B, I, static_cast<const bf16*>(w), bias, O, act, y, out_fp32 != 0,
-                     (hipStream_t)stream);
+                     256, static_cast<float*>(workspace), workspace ? workspace_bytes : 0, (hipStream_t)stream);
   });
 }
 
@@ -525,7 +530,7 @@ dstack_status dstack_op_lstm_layer(const void* x, int T, int B, int I, int H, co
     DS_CHECK(x && w_ih && w_hh && bias && h_bf16 && workspace, DSTACK_E_INVALID, "lstm_layer: null pointer");
     DS_CHECK(T >= 1 && I % 8 == 0 && I > 0, DSTACK_E_UNSUPPORTED, "lstm_layer: T >= 1, I % 8 == 0");
     DS_CHECK(B >= 1 && B <= 32, DSTACK_E_UNSUPPORTED, "lstm_layer: batch must be 1..32");
-    DS_CHECK(H >= 32 && H % 32 == 0, DSTACK_E_UNSUPPORTED, "lstm_layer: H must be a multiple of 32");
+    DS_CHECK(H >= 32 && H % 32 == 0 && H <= 2048, DSTACK_E_UNSUPPORTED, "lstm_layer: H must be a multiple of 32, <= 2048");
     float* gx = static_cast<float*>(workspace);
     float* c = reinterpret_cast<float*>(static_cast<char*>(workspace) + ((size_t)T * B * 4 * H * 4 + 255) / 256 * 256);
     return lstm_layer_run(static_cast<const bf16*>(x), T, B, I, H, static_cast<const bf16*>(w_ih),

@@ -483,12 +483,13 @@ dstack_status get_workspace(Model& m, int pid, int n_cu, Workspace** out) {
     offs.push_back(total);
     total += align256((size_t)e * m.max_batch * 2);
   }
-  // split-K partial sums: a split plan stops doubling once splits * tiles
-  // reaches 2 * n_cu (so stays below 4 * 256 tiles of at most 128 x 64 fp32
-  // values = 32 MB); a shape asking for more runs unsplit
+  // split-K partial sums: a conv split plan stops doubling once splits *
+  // tiles reaches 2 * n_cu (so stays below 4 * 256 tiles of at most 128 x 64
+  // fp32 values = 32 MB), an FC split needs at most 16 * 32 * O fp32 values;
+  // a shape asking for more runs with fewer splits
   size_t sk = 0;
   for (const Op& op : m.ops)
-    if (op.kind == OP_CONV) sk = SPLITK_WS_BYTES;
+    if (op.kind == OP_CONV || op.kind == OP_FC) sk = SPLITK_WS_BYTES;
   size_t sk_off = total;
   total += align256(sk);
   size_t gx_off = 0, c_off = 0, h0_off = 0, h1_off = 0;
@@ -641,7 +642,8 @@ dstack_status forward(Model& m, int batch, const void* d_in, void* d_out, Worksp
         by = (double)batch * (op.H * op.W + 1) * op.C * 2;
         break;
       case OP_FC:
-        s = launch_fc(src, batch, op.C, m.d_w + op.w_off, f32 + op.shift_off, op.K, op.act, dst, op.out_f32 != 0, st);
+        s = launch_fc(src, batch, op.C, m.d_w + op.w_off, f32 + op.shift_off, op.K, op.act, dst, op.out_f32 != 0, n_cu,
+                      ws.splitk, ws.splitk_bytes, st);
         kind = KC_FC;
         fl = 2.0 * batch * op.C * (double)op.K;
         by = (double)op.K * op.C * 2 + (double)batch * op.C * 2 + (double)batch * op.K * (op.out_f32 ? 4 : 2);

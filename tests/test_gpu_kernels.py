@@ -83,16 +83,24 @@ def test_dwconv3x3(env, case):
     assert oracle.rel_err(gu.host(y), ref) <= TOL
 
 
+@pytest.mark.parametrize("split", [False, True])
 @pytest.mark.parametrize("case", [(1, 64, 10, 0, True), (8, 25088, 40, 1, False), (16, 2048, 1000, 0, True),
-                                  (32, 1280, 37, 1, False), (5, 520, 9, 2, True)])
-def test_fc(env, case):
+                                  (32, 1280, 37, 1, False), (5, 520, 9, 2, True), (8, 4096, 1000, 0, True),
+                                  (3, 72, 50, 1, False), (17, 9216, 33, 0, True), (32, 4096, 4096, 1, False)])
+def test_fc(env, case, split):
+    """Depth tails (I % 32 != 0), o-tile and batch-tile tails, and with a
+    workspace the depth-split path (partial sums + reduce)."""
     ds, gu, inputs, oracle, torch = env
     B, I, O, act, f32 = case
     xb = inputs.normal_bf16(8, (B, I))
     wb = inputs.normal_bf16(9, (O, I), scale=(2.0 / I) ** 0.5)
     bias = np.random.default_rng(10).uniform(-0.5, 0.5, O).astype(np.float32)
     y = gu.empty_f32((B, O)) if f32 else gu.empty_bf16((B, O))
-    ds.fc(gu.dev_bf16(xb), gu.dev_bf16(wb), gu.dev_f32(bias), act, y, out_fp32=f32)
+    ws = None
+    if split:
+        nbytes = ds.fc_workspace_bytes(B, I, O)
+        ws = gu.empty_f32((max(nbytes // 4, 1),))
+    ds.fc(gu.dev_bf16(xb), gu.dev_bf16(wb), gu.dev_f32(bias), act, y, out_fp32=f32, workspace=ws)
     torch.cuda.synchronize()
     ref = oracle.fc(oracle.bf16_bits_to_f64(xb), oracle.bf16_bits_to_f64(wb), bias)
     ref = np.maximum(ref, 0) if act == 1 else (np.clip(ref, 0, 6) if act == 2 else ref)

@@ -137,3 +137,15 @@ def test_schedule_rejects_bad_arguments():
         ds.schedule([dict(slo_us=0, max_batch=1, table={1: {4: 10}})], 100000)
     with pytest.raises(ds.DStackError):
         ds.schedule([dict(slo_us=1000, max_batch=1, table={1: {40: 10}})], 100000)
+
+
+def test_fc_workspace_bytes():
+    """Depth-split plan of the FC kernel on 256 CUs: splits double while the
+    grid (16-row tiles x splits) stays below 512 blocks and each split keeps
+    16 or more 32-deep steps; the workspace holds splits x B x O fp32 sums."""
+    import paper_2304_13541_amd as ds
+    assert ds.fc_workspace_bytes(8, 4096, 1000) == 8 * 8 * 1000 * 4      # 63 tiles, 128 steps -> 8 splits
+    assert ds.fc_workspace_bytes(8, 25088, 4096) == 2 * 8 * 4096 * 4     # 256 tiles -> 2 splits
+    assert ds.fc_workspace_bytes(16, 1280, 1000) == 2 * 16 * 1000 * 4    # 40 steps -> 2 splits
+    assert ds.fc_workspace_bytes(1, 64, 10) == 0                         # 2 steps: unsplit
+    assert ds.fc_workspace_bytes(0, 64, 10) == 0
