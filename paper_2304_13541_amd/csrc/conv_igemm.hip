@@ -134,12 +134,17 @@ __device__ __forceinline__ unsigned lds_address(const void* p) {
   return (unsigned)(unsigned long long)(const __attribute__((address_space(3))) void*)p;
 }
 
-// 16 bytes per lane from buffer offset `voff` into LDS at lds_base + 16 * lane.
-// Issued as inline asm so that the compiler does not treat every later LDS
-// read as dependent on it (it would wait for all loads in flight); the
-// kernel's own vmcnt waits order these loads against the LDS reads.
-// M0 (the LDS destination) is saved and restored around the load.
-__device__ __forceinline__ void load_to_lds16(i32x4 rsrc, unsigned voff, unsigned lds_base) {
+// NL wave-loads of 16 bytes per lane: load j moves buffer offsets off[j]
+// into LDS at lds_base + 1024 * j + 16 * lane.  Issued as inline asm so that
+// the compiler does not treat every later LDS read as dependent on it (it
+// would wait for all loads in flight); the kernel's own vmcnt waits order
+// these loads against the LDS reads.  M0 (the LDS destination) is saved once,
+// stepped by 1 KB between loads (one wait state after each write), restored.
+template <int NL>
+__device__ __forceinline__ void load_group(i32x4 rsrc, const unsigned (&off)[NL], unsigned lds_base);
+
+template <>
+__device__ __forceinline__ void load_group<1>(i32x4 rsrc, const unsigned (&off)[1], unsigned lds_base) {
   unsigned saved;
   asm volatile(
       "s_mov_b32 %0, m0\n\t"
@@ -148,19 +153,58 @@ __device__ __forceinline__ void load_to_lds16(i32x4 rsrc, unsigned voff, unsigne
       "buffer_load_dwordx4 %2, %3, 0 offen lds\n\t"
       "s_mov_b32 m0, %0"
       : "=&s"(saved)
-      : "s"(lds_base), "v"(voff), "s"(rsrc)
+      : "s"(lds_base), "v"(off[0]), "s"(rsrc)
       : "memory");
+}
+
+template <>
+__device__ __forceinline__ void load_group<2>(i32x4 rsrc, const unsigned (&off)[2], unsigned lds_base) {
+  unsigned saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %1\n\t"
+      "s_nop 0\n\t"
+      "buffer_load_dwordx4 %2, %4, 0 offen lds\n\t"
+      "s_add_u32 m0, m0, 0x400\n\t"
+      "s_nop 0\n\t"
+      "buffer_load_dwordx4 %3, %4, 0 offen lds\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "s"(lds_base), "v"(off[0]), "v"(off[1]), "s"(rsrc)
+      : "memory", "scc");
+}
+
+template <>
+__device__ __forceinline__ void load_group<4>(i32x4 rsrc, const unsigned (&off)[4], unsigned lds_base) {
+  unsigned saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %1\n\t"
+      "s_nop 0\n\t"
+      "buffer_load_dwordx4 %2, %6, 0 offen lds\n\t"
+      "s_add_u32 m0, m0, 0x400\n\t"
+      "s_nop 0\n\t"
+      "buffer_load_dwordx4 %3, %6, 0 offen lds\n\t"
+      "s_add_u32 m0, m0, 0x400\n\t"
+      "s_nop 0\n\t"
+      "buffer_load_dwordx4 %4, %6, 0 offen lds\n\t"
+      "s_add_u32 m0, m0, 0x400\n\t"
+      "s_nop 0\n\t"
+      "buffer_load_dwordx4 %5, %6, 0 offen lds\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "s"(lds_base), "v"(off[0]), "v"(off[1]), "v"(off[2]), "v"(off[3]), "s"(rsrc)
+      : "memory", "scc");
 }
 
 template <int BN, int BM, int WN, int WM, int STAGES, int MODE, bool OUT_F32, bool SPLIT>
 __global__ __launch_bounds__(256) void conv_igemm_kernel(ConvArgs a) {
   constexpr int ROWS = BN + BM;
   constexpr int STAGE_BYTES = ROWS * ROW_BYTES;
-  constexpr int LOADS = ROWS / 8;       // wave-loads (8 rows each) per stage
-  constexpr int LPW = LOADS / 4;        // per wave
+  constexpr int LPW = ROWS / 32;        // wave-loads (8 rows each) per wave per stage
   constexpr int TN = BN / WN / 16;      // MFMA tiles per wave along channels
   constexpr int TM = BM / WM / 16;      // ... along pixels
-  static_assert(LOADS % 4 == 0 && WN * WM == 4 && TN >= 1 && TM >= 1, "tile shape");
+  static_assert(BN % 32 == 0 && BM % 32 == 0 && WN * WM == 4 && TN >= 1 && TM >= 1, "tile shape");
   static_assert(STAGES >= 2 && STAGES <= 4, "2..4 stages");
 
   __shared__ __attribute__((aligned(1024))) unsigned char lds[STAGES * STAGE_BYTES];
@@ -189,39 +233,62 @@ __global__ __launch_bounds__(256) void conv_igemm_kernel(ConvArgs a) {
   const int wave_u = __builtin_amdgcn_readfirstlane(wave);  // wave-uniform copy: scalar branches
   const unsigned lds0 = __builtin_amdgcn_readfirstlane(lds_address(lds));
 
-  // ---- per-load addressing (each lane: one 16-byte chunk of one tile row) ----
-  const int rin = lane >> 3;           // row within the 8-row group
-  unsigned base[LPW];                  // byte offset at depth tile 0 (OOB if the row is outside the tensor)
-  int hi0[LPW], wi0[LPW];              // TILED / GENERIC: top-left input coordinate of the pixel
-  int chunk[LPW];                      // logical 16-byte chunk of the row this lane moves
+  // ---- per-lane addressing ----
+  // Every wave moves WPW 8-row groups of weight rows and APW 8-row groups of
+  // pixel rows per stage; lane l moves 16-byte chunk (l % 8) of row l / 8 of
+  // each group, stored at its swizzled position.
+  constexpr int WPW = BN / 32, APW = BM / 32;
+  const int rin = lane >> 3;
+  unsigned woff[WPW];  // byte offset of the lane's chunk at depth 0; OOB past K (stays >= 2^31 after adding depth)
 #pragma unroll
-  for (int i = 0; i < LPW; ++i) {
-    const int r = 8 * (wave * LPW + i) + rin;
+  for (int j = 0; j < WPW; ++j) {
+    const int r = 8 * (wave * WPW + j) + rin;
     const int c = (lane & 7) ^ ((r >> 1) & 7);
-    chunk[i] = c;
-    hi0[i] = 0;
-    wi0[i] = 0;
-    if (r < BN) {
-      const int n = n0 + r;
-      base[i] = n < a.K ? (unsigned)(((long)n * a.Kg + c * 8) * 2) : OOB;
-    } else {
-      const int m = m0 + r - BN;
-      if (m < a.M) {
-        const int t = a.div_wo.div(m);
-        const int wo = m - t * a.Wo;
-        const int nn = a.div_ho.div(t);
-        const int ho = t - nn * a.Ho;
-        if (MODE == MODE_1X1S1) {  // the output pixel is the input pixel
-          base[i] = (unsigned)(((long)m * a.C + c * 8) * 2);
-        } else if (MODE == MODE_1X1) {
-          base[i] = (unsigned)(((((long)nn * a.H + ho * a.stride) * a.W + wo * a.stride) * a.C + c * 8) * 2);
-        } else {
-          base[i] = (unsigned)((long)nn * a.H * a.W);  // image's first pixel
-          hi0[i] = ho * a.stride - a.pad;
-          wi0[i] = wo * a.stride - a.pad;
-        }
+    const int n = n0 + r;
+    woff[j] = n < a.K ? (unsigned)(((long)n * a.Kg + c * 8) * 2) : OOB;
+  }
+  // pixel rows: 1x1 modes keep the chunk's byte offset at depth 0 (OOB past
+  // M); TILED keeps the byte offset of the chunk at (r, s) = (0, 0) relative
+  // to the (possibly padded-out) top-left input pixel, plus a bit mask of the
+  // (r, s) window positions that fall inside the image; GENERIC keeps the
+  // image's first pixel and the top-left coordinate.
+  int aoff[APW];
+  unsigned vmask[APW];
+  int hi0[APW], wi0[APW], chunk[APW];
+#pragma unroll
+  for (int j = 0; j < APW; ++j) {
+    const int rl = 8 * (wave * APW + j) + rin;
+    const int r = BN + rl;
+    const int c = (lane & 7) ^ ((r >> 1) & 7);
+    chunk[j] = c;
+    const int m = m0 + rl;
+    aoff[j] = (int)OOB;
+    vmask[j] = 0;
+    hi0[j] = 0;
+    wi0[j] = 0;
+    if (m < a.M) {
+      const int t = a.div_wo.div(m);
+      const int wo = m - t * a.Wo;
+      const int nn = a.div_ho.div(t);
+      const int ho = t - nn * a.Ho;
+      if (MODE == MODE_1X1S1) {  // the output pixel is the input pixel
+        aoff[j] = (int)(((long)m * a.C + c * 8) * 2);
+      } else if (MODE == MODE_1X1) {
+        aoff[j] = (int)(((((long)nn * a.H + ho * a.stride) * a.W + wo * a.stride) * a.C + c * 8) * 2);
       } else {
-        base[i] = OOB;
+        const int h0 = ho * a.stride - a.pad, w0 = wo * a.stride - a.pad;
+        if (MODE == MODE_TILED) {
+          aoff[j] = ((((nn * a.H + h0) * a.W + w0) * a.C) + c * 8) * 2;
+          for (int rr = 0; rr < a.R; ++rr)
+            for (int ss = 0; ss < a.S; ++ss)
+              if ((unsigned)(h0 + rr) < (unsigned)a.H && (unsigned)(w0 + ss) < (unsigned)a.W)
+                vmask[j] |= 1u << (rr * a.S + ss);
+        } else {
+          aoff[j] = nn * a.H * a.W;  // image's first pixel
+          vmask[j] = 1;
+          hi0[j] = h0;
+          wi0[j] = w0;
+        }
       }
     }
   }
@@ -232,47 +299,47 @@ __global__ __launch_bounds__(256) void conv_igemm_kernel(ConvArgs a) {
     kt0 = blockIdx.z * a.kt_per_split;
     kt1 = min(nkt_total, kt0 + a.kt_per_split);
   }
+  const bool kfull = (a.Kg % BK) == 0;  // no depth tail
 
-  // issue the direct-to-LDS loads of depth tile kt into stage `st`
+  // issue the direct-to-LDS loads of depth tile kt into stage `st`.  Weight
+  // chunks past the depth Kg read the next row (finite values) or zeros; the
+  // pixel chunks there are forced to zero, so they add nothing.
   auto issue = [&](int kt, int st) {
     const int k0 = kt * BK;
-    int tr = 0, ts = 0, tc = 0;
-    if (MODE == MODE_TILED) {  // C % 64 == 0: the whole tile is inside one (r, s)
-      const int rs = a.div_c.div(k0);
-      tc = k0 - rs * a.C;
-      tr = a.div_s.div(rs);
-      ts = rs - tr * a.S;
-    }
     const unsigned sb = lds0 + st * STAGE_BYTES;
+    unsigned wv[WPW];
 #pragma unroll
-    for (int i = 0; i < LPW; ++i) {
-      const int g = wave_u * LPW + i;  // wave-load index: rows 8g..8g+7 of the stage
-      const int k = k0 + chunk[i] * 8;
-      const bool kin = k < a.Kg;
-      if (g < BN / 8) {  // weight rows (scalar branch)
-        const unsigned off = (base[i] != OOB && kin) ? base[i] + (unsigned)(k0 * 2) : OOB;
-        load_to_lds16(wrs, off, sb + g * 1024);
-      } else {           // activation rows
-        unsigned off;
-        if (MODE == MODE_1X1 || MODE == MODE_1X1S1) {
-          off = (base[i] != OOB && kin) ? base[i] + (unsigned)(k0 * 2) : OOB;
-        } else {
-          int r, s, c;
-          if (MODE == MODE_TILED) {
-            r = tr; s = ts; c = tc + chunk[i] * 8;
-          } else {
-            const int rs = a.div_c.div(k);
-            c = k - rs * a.C;
-            r = a.div_s.div(rs);
-            s = rs - r * a.S;
-          }
-          const int hi = hi0[i] + r, wi = wi0[i] + s;
-          const bool ok = base[i] != OOB && kin && (unsigned)hi < (unsigned)a.H && (unsigned)wi < (unsigned)a.W;
-          off = ok ? (unsigned)(((base[i] + hi * a.W + wi) * a.C + c) * 2) : OOB;
-        }
-        load_to_lds16(xrs, off, sb + g * 1024);
+    for (int j = 0; j < WPW; ++j) wv[j] = woff[j] + (unsigned)(k0 * 2);
+    load_group<WPW>(wrs, wv, sb + wave_u * WPW * 1024);
+    unsigned av[APW];
+    if (MODE == MODE_1X1 || MODE == MODE_1X1S1) {
+#pragma unroll
+      for (int j = 0; j < APW; ++j) {
+        const bool kin = kfull || k0 + chunk[j] * 8 < a.Kg;
+        av[j] = kin ? (unsigned)aoff[j] + (unsigned)(k0 * 2) : OOB;
+      }
+    } else if (MODE == MODE_TILED) {  // C % 64 == 0: the whole tile is inside one (r, s)
+      const int rs = a.div_c.div(k0);
+      const int tc = k0 - rs * a.C;
+      const int tr = a.div_s.div(rs);
+      const int ts = rs - tr * a.S;
+      const int delta = ((tr * a.W + ts) * a.C + tc) * 2;  // wave-uniform
+#pragma unroll
+      for (int j = 0; j < APW; ++j) av[j] = ((vmask[j] >> rs) & 1) ? (unsigned)(aoff[j] + delta) : OOB;
+    } else {
+#pragma unroll
+      for (int j = 0; j < APW; ++j) {
+        const int k = k0 + chunk[j] * 8;
+        const int rs = a.div_c.div(k);
+        const int c = k - rs * a.C;
+        const int r = a.div_s.div(rs);
+        const int s = rs - r * a.S;
+        const int hi = hi0[j] + r, wi = wi0[j] + s;
+        const bool ok = vmask[j] && k < a.Kg && (unsigned)hi < (unsigned)a.H && (unsigned)wi < (unsigned)a.W;
+        av[j] = ok ? (unsigned)(((aoff[j] + hi * a.W + wi) * a.C + c) * 2) : OOB;
       }
     }
+    load_group<APW>(xrs, av, sb + (BN / 8 + wave_u * APW) * 1024);
   };
 
   f32x4 acc[TN][TM];
@@ -429,13 +496,22 @@ size_t conv_splitk_workspace_bytes(int M, int K, int Kg, int n_cu) {
   return p.splits > 1 ? (size_t)p.splits * M * K * sizeof(float) : 0;
 }
 
-#ifndef DS_CONV_STAGES
-#define DS_CONV_STAGES 2
-#endif
+// Ring depth per tile shape: the deepest ring (at most 4) with which two
+// blocks still share a CU's 160 KB of LDS, so that two blocks and STAGES-1
+// tiles each keep loads in flight.
+constexpr int conv_stages(int bn, int bm) {
+  const int stage = (bn + bm) * ROW_BYTES;
+  const int s = (80 * 1024) / stage;
+  return s < 2 ? 2 : (s > 4 ? 4 : s);
+}
 
 template <int BN, int BM, int WN, int WM, int MODE>
 static void launch_mode(ConvArgs a, bool f32, int splits, hipStream_t st) {
+#ifdef DS_CONV_STAGES
   constexpr int STAGES = DS_CONV_STAGES;
+#else
+  constexpr int STAGES = conv_stages(BN, BM);
+#endif
   a.tiles_n = ceil_div(a.K, BN);
   a.tiles = ceil_div(a.M, BM) * a.tiles_n;
   a.div_tn = FastDiv::make(a.tiles_n);
@@ -486,7 +562,8 @@ dstack_status launch_conv2d_ws(const bf16* x, int N, int H, int W, int C, const 
   a.div_c = FastDiv::make(C);
   a.div_s = FastDiv::make(S);
   const bool one = R == 1 && S == 1 && pad == 0;
-  const int mode = one ? (stride == 1 ? MODE_1X1S1 : MODE_1X1) : (C % BK == 0 ? MODE_TILED : MODE_GENERIC);
+  const int mode = one ? (stride == 1 ? MODE_1X1S1 : MODE_1X1)
+                       : (C % BK == 0 && R * S <= 32 ? MODE_TILED : MODE_GENERIC);
   ConvPlan p = choose_plan(a.M, K, a.Kg, n_cu);
   if (p.splits > 1 && (splitk_ws == nullptr || splitk_bytes < (size_t)p.splits * a.M * K * sizeof(float)))
     p.splits = 1;
