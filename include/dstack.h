@@ -229,6 +229,14 @@ typedef struct {
   int64_t period_us;
   int total_slots;      /* 1..64; 32 = the whole MI355X */
   int overprov_slots;   /* 2 by default */
+  int placement;        /* 0: each job takes the lowest free slot ids;
+                           1: home ranges -- each model owns one contiguous
+                           range of its deployed size (models by decreasing
+                           size, then index, take the offset of least summed
+                           overlap with the ranges placed before, lowest on
+                           ties); a job uses its whole home range (no
+                           below-knee fallback) and starts only when no
+                           overlapping job uses a slot of it */
 } dstack_sched_params;
 
 typedef struct {
@@ -249,6 +257,7 @@ typedef struct {
   int n_jobs;                           /* in placement (EDF) order */
   dstack_job jobs[DSTACK_MAX_JOBS];
   int64_t utilisation_ppm;
+  int home_offset[DSTACK_MAX_MODELS];   /* placement 1: first slot of each home range */
 } dstack_schedule_out;
 
 dstack_status dstack_schedule(const dstack_sched_model* models, int n_models, const dstack_sched_params* params,

@@ -35,7 +35,15 @@ notes):
   lowest-numbered slots free at their start; an interval set whose load
   never exceeds the total can always be coloured this way;
 * utilisation = sum over placed jobs of s * L / (total * T) (the paper's
-  knee% x busy-time accounting, Sec. 6.1).
+  knee% x busy-time accounting, Sec. 6.1);
+* home placement (an alternative to lowest free ids, for a launcher that
+  gives every model one fixed set of CUs, as a GPU% fixed per model
+  process does in Sec. 6): every model owns one contiguous slot range of
+  its deployed size; models in order of decreasing size (then index) take
+  the offset in [0, total - size] whose summed overlap with the ranges
+  already placed is least, lowest offset on ties; a job runs on its whole
+  home range only (no smaller fallback) and may start when no overlapping
+  placed job's range meets its own.
 """
 from dataclasses import dataclass, field
 from typing import Dict, List, Optional
@@ -73,6 +81,25 @@ def knee(row: Dict[int, int], b: int) -> int:
 
 def deployed_slots(knee_s: int, overprov=OVERPROVISION_SLOTS, total=TOTAL_SLOTS) -> int:
     return min(total, knee_s + overprov)
+
+
+def home_offsets(sizes: List[int], total: int = TOTAL_SLOTS) -> List[int]:
+    """Offset of each model's fixed slot range (home placement)."""
+    offs = [0] * len(sizes)
+    placed = []
+    for i in sorted(range(len(sizes)), key=lambda i: (-sizes[i], i)):
+        best = None
+        for o in range(total - sizes[i] + 1):
+            overlap = sum(max(0, min(o + sizes[i], po + ps) - max(o, po)) for po, ps in placed)
+            if best is None or overlap < best[0]:
+                best = (overlap, o)
+        offs[i] = best[1]
+        placed.append((offs[i], sizes[i]))
+    return offs
+
+
+def range_mask(offset: int, size: int) -> int:
+    return ((1 << size) - 1) << offset
 
 
 def assembly_us(b: int, rate: int) -> int:
@@ -155,7 +182,12 @@ def _max_load(placed: List[Job], t0: int, t1: int) -> int:
     return best
 
 
-def _find_start(placed, ws, we, L, s, latest, total):
+def _conflicts(placed: List[Job], t0: int, t1: int, mask: int) -> bool:
+    """Does a placed job overlapping [t0, t1) in time use a slot of mask?"""
+    return any(p.start < t1 and t0 < p.end and (p.slot_mask & mask) for p in placed)
+
+
+def _find_start(placed, ws, we, L, s, latest, total, home_mask=None):
     if L > we - ws:
         return None
     cands = {ws, we - L}
@@ -166,13 +198,17 @@ def _find_start(placed, ws, we, L, s, latest, total):
     if latest:
         cands.reverse()
     for t in cands:
-        if _max_load(placed, t, t + L) + s <= total:
+        if home_mask is None:
+            if _max_load(placed, t, t + L) + s <= total:
+                return t
+        elif not _conflicts(placed, t, t + L, home_mask):
             return t
     return None
 
 
-def plan(models: List[PlanModel], period: int, total: int = TOTAL_SLOTS) -> List[Job]:
-    """Spatio-temporal session plan; returns jobs in placement (EDF) order."""
+def plan(models: List[PlanModel], period: int, total: int = TOTAL_SLOTS, homes: Optional[List[int]] = None) -> List[Job]:
+    """Spatio-temporal session plan; returns jobs in placement (EDF) order.
+    homes: per-model range offsets for home placement (None: lowest free ids)."""
     jobs = []
     for i, m in enumerate(models):
         r = ceil_div(period, m.slo)
@@ -186,20 +222,26 @@ def plan(models: List[PlanModel], period: int, total: int = TOTAL_SLOTS) -> List
         j.order = order
         m = models[j.model]
         options = [m.slots]
-        if m.knee != m.slots:
-            options.append(m.knee)
-        options += [s for s in sorted(m.row, reverse=True) if s < m.knee]
+        if homes is None:
+            if m.knee != m.slots:
+                options.append(m.knee)
+            options += [s for s in sorted(m.row, reverse=True) if s < m.knee]
+        hm = None if homes is None else range_mask(homes[j.model], m.slots)
         for s in options:
             L = latency_at(m.row, s)
             if L is None:
                 continue
-            t = _find_start(placed, j.release, j.deadline, L, s, j.k % 2 == 1, total)
+            t = _find_start(placed, j.release, j.deadline, L, s, j.k % 2 == 1, total, hm)
             if t is not None:
                 j.start, j.duration, j.slots = t, L, s
+                if hm is not None:
+                    j.slot_mask = hm
                 placed.append(j)
                 break
         else:
             j.start, j.duration, j.slots, j.missed = j.release, 0, 0, True
+    if homes is not None:
+        return jobs
     # slot ids: lowest free ids at each start, in (start, placement order)
     busy = []  # (end, mask)
     for j in sorted(placed, key=lambda p: (p.start, p.order)):
@@ -235,15 +277,17 @@ def temporal_utilisation(slos_and_shares):
     return num / den
 
 
-def schedule(models, period, total=TOTAL_SLOTS, overprov=OVERPROVISION_SLOTS):
+def schedule(models, period, total=TOTAL_SLOTS, overprov=OVERPROVISION_SLOTS, placement="lowest"):
     """Per-model optimisation followed by the session plan.
 
-    models: list of dicts {slo_us, max_batch, rate_per_s, table: {b: {s: L}}}.
+    models: list of dicts {slo_us, max_batch, rate_per_s, table: {b: {s: L}}};
+    placement: "lowest" (lowest free slot ids) or "home" (fixed ranges).
     Returns (choices, jobs, utilisation_ppm, feasible_all)."""
     choices = [optimize(m["table"], m["slo_us"], m["max_batch"], m.get("rate_per_s", 0)) for m in models]
     pms = [PlanModel(slo=m["slo_us"], knee=c.slots, slots=deployed_slots(c.slots, overprov, total),
                      row=m["table"][c.batch], batch=c.batch) for m, c in zip(models, choices)]
-    jobs = plan(pms, period, total)
+    homes = home_offsets([pm.slots for pm in pms], total) if placement == "home" else None
+    jobs = plan(pms, period, total, homes)
     ok = all(c.feasible for c in choices) and not any(j.missed for j in jobs)
     return choices, jobs, utilisation_ppm(jobs, period, total), ok
 
@@ -263,7 +307,8 @@ def schedule(models, period, total=TOTAL_SLOTS, overprov=OVERPROVISION_SLOTS):
 #   us, model index) -- "fewest runs" (Sec. 6.1.2) then "least time" (Sec. 6.3);
 #   the first candidate that fits is launched (at most one per trigger):
 #   it takes the lowest-numbered s_i slots free now (s_i = its deployed
-#   slots); its gap ends at the first planned start at or after now whose
+#   slots) -- with home placement, its own range, which must be all free;
+#   its gap ends at the first planned start at or after now whose
 #   slots meet them, or at its own model's next planned start (a planned job
 #   at this very instant may not have been processed yet); its batch is the largest
 #   b in {1,2,4,8,16,32} with b <= max_batch, b <= queued and L(b, s_i) <= gap;
@@ -297,14 +342,15 @@ def _nearest_rank(sorted_vals, pct):
 
 
 def simulate(models, period, duration, arrivals, total=TOTAL_SLOTS, overprov=OVERPROVISION_SLOTS, fod=True,
-             sessions_window=10):
+             sessions_window=10, placement="lowest"):
     """models: as for schedule(); arrivals: per model sorted list of integer us in [0, duration).
     Returns dict with per-model counters, utilisation_ppm and a hash of the job log."""
     import collections
     import heapq
-    choices, jobs, _, _ = schedule(models, period, total, overprov)
+    choices, jobs, _, _ = schedule(models, period, total, overprov, placement)
     n = len(models)
     dep = [deployed_slots(c.slots, overprov, total) for c in choices]
+    homes = home_offsets(dep, total) if placement == "home" else None
     planned = [j for j in jobs if not j.missed]
     # next planned start of each model after time t (over all periods)
     n_periods = ceil_div(duration, period)
@@ -371,12 +417,17 @@ def simulate(models, period, duration, arrivals, total=TOTAL_SLOTS, overprov=OVE
         cands.sort(key=lambda i: (sum(runs[i][s] for s in range(cur - sessions_window + 1, cur + 1)), busy[i], i))
         for i in cands:
             s = dep[i]
-            free = [sid for sid in range(total) if not (used >> sid) & 1]
-            if len(free) < s:
-                continue
-            mask = 0
-            for sid in free[:s]:
-                mask |= 1 << sid
+            if homes is not None:  # its own range, all of it free
+                mask = range_mask(homes[i], s)
+                if used & mask:
+                    continue
+            else:  # the lowest-numbered free slots
+                free = [sid for sid in range(total) if not (used >> sid) & 1]
+                if len(free) < s:
+                    continue
+                mask = 0
+                for sid in free[:s]:
+                    mask |= 1 << sid
             gap = None
             for (ps, pm, pmask) in planned_starts:
                 if ps >= t and ((pmask & mask) or pm == i):

@@ -55,7 +55,8 @@ class SchedModel(ctypes.Structure):
 
 
 class SchedParams(ctypes.Structure):
-    _fields_ = [("period_us", ctypes.c_int64), ("total_slots", ctypes.c_int), ("overprov_slots", ctypes.c_int)]
+    _fields_ = [("period_us", ctypes.c_int64), ("total_slots", ctypes.c_int), ("overprov_slots", ctypes.c_int),
+                ("placement", ctypes.c_int)]
 
 
 class Job(ctypes.Structure):
@@ -68,7 +69,8 @@ class ScheduleOut(ctypes.Structure):
     _fields_ = [("n_models", ctypes.c_int), ("batch", ctypes.c_int * MAX_MODELS),
                 ("knee_slots", ctypes.c_int * MAX_MODELS), ("deployed_slots", ctypes.c_int * MAX_MODELS),
                 ("latency_us", ctypes.c_int64 * MAX_MODELS), ("feasible", ctypes.c_int * MAX_MODELS),
-                ("n_jobs", ctypes.c_int), ("jobs", Job * MAX_JOBS), ("utilisation_ppm", ctypes.c_int64)]
+                ("n_jobs", ctypes.c_int), ("jobs", Job * MAX_JOBS), ("utilisation_ppm", ctypes.c_int64),
+                ("home_offset", ctypes.c_int * MAX_MODELS)]
 
 
 class SimParams(ctypes.Structure):
@@ -301,8 +303,11 @@ def _stats(out):
     return [dict((f, getattr(out.models[i], f)) for f, _ in ModelStats._fields_) for i in range(out.n_models)]
 
 
+PLACEMENTS = {"lowest": 0, "home": 1}
+
+
 def simulate(models, period_us, duration_us, arrivals, total_slots=TOTAL_SLOTS, overprov_slots=2, fod=True,
-             sessions_window=10):
+             sessions_window=10, placement="lowest"):
     """Launcher simulation on the timing table (see dstack_simulate).
     arrivals: per model sorted integer-us arrival times.  Returns a dict."""
     arr = _sched_models(models)
@@ -317,13 +322,13 @@ def simulate(models, period_us, duration_us, arrivals, total_slots=TOTAL_SLOTS, 
         sp.arrivals_us[i] = ctypes.cast(buf, ctypes.POINTER(ctypes.c_int64))
         sp.n_arrivals[i] = len(a)
     out = RunOut()
-    _check(lib().dstack_simulate(arr, len(models), ctypes.byref(SchedParams(period_us, total_slots, overprov_slots)),
-                                 ctypes.byref(sp), ctypes.byref(out)))
+    prm = SchedParams(period_us, total_slots, overprov_slots, PLACEMENTS[placement])
+    _check(lib().dstack_simulate(arr, len(models), ctypes.byref(prm), ctypes.byref(sp), ctypes.byref(out)))
     return dict(models=_stats(out), utilisation_ppm=out.utilisation_ppm, job_hash=out.job_hash,
                 last_end_us=out.last_end_us)
 
 
-def schedule(models, period_us, total_slots=TOTAL_SLOTS, overprov_slots=2):
+def schedule(models, period_us, total_slots=TOTAL_SLOTS, overprov_slots=2, placement="lowest"):
     """models: list of dicts {slo_us, max_batch, rate_per_s, table: {batch: {slots: latency_us}}}.
     Returns (status, result dict); status is OK or E_INFEASIBLE (plan still filled)."""
     arr = (SchedModel * len(models))()
@@ -342,7 +347,7 @@ def schedule(models, period_us, total_slots=TOTAL_SLOTS, overprov_slots=2):
                 e.latency_us[q][r] = m["table"][b].get(s, 0)
         for r, s in enumerate(slots):
             e.slots[r] = s
-    prm = SchedParams(period_us, total_slots, overprov_slots)
+    prm = SchedParams(period_us, total_slots, overprov_slots, PLACEMENTS[placement])
     out = ScheduleOut()
     st = lib().dstack_schedule(arr, len(models), ctypes.byref(prm), ctypes.byref(out))
     if st not in (OK, E_INFEASIBLE):
@@ -353,7 +358,8 @@ def schedule(models, period_us, total_slots=TOTAL_SLOTS, overprov_slots=2):
             for j in out.jobs[:out.n_jobs]]
     return st, dict(batch=list(out.batch[:n]), knee_slots=list(out.knee_slots[:n]),
                     deployed_slots=list(out.deployed_slots[:n]), latency_us=list(out.latency_us[:n]),
-                    feasible=list(out.feasible[:n]), jobs=jobs, utilisation_ppm=out.utilisation_ppm)
+                    feasible=list(out.feasible[:n]), jobs=jobs, utilisation_ppm=out.utilisation_ppm,
+                    home_offset=list(out.home_offset[:n]) if placement == "home" else None)
 
 
 # ---------------------------------------------------------- kernel ops ----

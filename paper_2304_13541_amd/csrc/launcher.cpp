@@ -11,7 +11,8 @@
 //    last `sessions_window` sessions, then cumulative busy time, then index
 //    ("fewest runs", "least time in the GPU"); the first candidate that fits
 //    starts (one per trigger) on the lowest-numbered free slots, as many as
-//    its deployed share, with the largest grid batch that is queued and whose
+//    its deployed share (home placement: on its home range, all of it free),
+//    with the largest grid batch that is queued and whose
 //    latency fits before the next planned start (at or after now) touching
 //    those slots or its own next planned start;
 //  - same-instant events: completions, planned starts, arrivals, each by
@@ -177,13 +178,18 @@ dstack_status simulate(const dstack_sched_model* models, int n, const dstack_sch
     for (int i : cands) {
       const int s = plan->deployed_slots[i];
       uint64_t mask = 0;
-      int got = 0;
-      for (int sid = 0; sid < total && got < s; ++sid)
-        if (!((used >> sid) & 1)) {
-          mask |= 1ULL << sid;
-          ++got;
-        }
-      if (got < s) continue;
+      if (prm->placement == 1) {
+        mask = range_mask(plan->home_offset[i], s);
+        if (used & mask) continue;
+      } else {
+        int got = 0;
+        for (int sid = 0; sid < total && got < s; ++sid)
+          if (!((used >> sid) & 1)) {
+            mask |= 1ULL << sid;
+            ++got;
+          }
+        if (got < s) continue;
+      }
       // -1: no planned start constrains it; a planned start at this very
       // instant counts (same-instant planned starts are processed after
       // completions)

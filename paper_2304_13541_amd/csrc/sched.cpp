@@ -11,6 +11,9 @@
 //  * Session plan (Sec. 6.1, 6.1.1): EDF over per-SLO windows, consecutive
 //    runs pushed apart (even runs early, odd runs late), no over-subscription,
 //    below-knee fallback, no preemption.
+//  * Placement: lowest free slot ids per job, or fixed home ranges (one
+//    contiguous range of the deployed size per model, the launcher's one
+//    CU-masked stream per model); a home job needs its whole range free.
 #include <algorithm>
 #include <cstring>
 #include <vector>
@@ -65,6 +68,7 @@ struct Placed {
   int64_t start, end;
   int slots;
   int job;
+  uint64_t mask;  // home placement: the range it occupies
 };
 
 // Largest total slots of placed jobs at any instant in [t0, t1).  The load is
@@ -84,8 +88,17 @@ int peak_load(const std::vector<Placed>& placed, int64_t t0, int64_t t1) {
   return peak;
 }
 
+// home placement: does a placed job overlapping [t0, t1) use a slot of mask?
+bool conflicts(const std::vector<Placed>& placed, int64_t t0, int64_t t1, uint64_t mask) {
+  for (const Placed& p : placed)
+    if (p.start < t1 && t0 < p.end && (p.mask & mask)) return true;
+  return false;
+}
+
+// home_mask == 0: feasible when the summed slots stay within the total;
+// otherwise when no overlapping job meets the home range
 bool find_start(const std::vector<Placed>& placed, int64_t ws, int64_t we, int64_t L, int s, bool latest, int total,
-                int64_t* out) {
+                uint64_t home_mask, int64_t* out) {
   if (L > we - ws) return false;
   std::vector<int64_t> cand;
   cand.push_back(ws);
@@ -101,7 +114,8 @@ bool find_start(const std::vector<Placed>& placed, int64_t ws, int64_t we, int64
   ok.erase(std::unique(ok.begin(), ok.end()), ok.end());
   if (latest) std::reverse(ok.begin(), ok.end());
   for (int64_t t : ok) {
-    if (peak_load(placed, t, t + L) + s <= total) {
+    const bool fits = home_mask ? !conflicts(placed, t, t + L, home_mask) : peak_load(placed, t, t + L) + s <= total;
+    if (fits) {
       *out = t;
       return true;
     }
@@ -111,11 +125,36 @@ bool find_start(const std::vector<Placed>& placed, int64_t ws, int64_t we, int64
 
 }  // namespace
 
+void home_offsets(const int* sizes, int n, int total, int* offs) {
+  std::vector<int> order(n);
+  for (int i = 0; i < n; ++i) order[i] = i;
+  std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return sizes[a] > sizes[b]; });
+  std::vector<std::pair<int, int>> placed;  // (offset, size)
+  for (int i : order) {
+    int best = -1, best_ov = 0;
+    for (int o = 0; o + sizes[i] <= total; ++o) {
+      int ov = 0;
+      for (auto& p : placed) ov += std::max(0, std::min(o + sizes[i], p.first + p.second) - std::max(o, p.first));
+      if (best < 0 || ov < best_ov) {
+        best = o;
+        best_ov = ov;
+      }
+    }
+    offs[i] = best;
+    placed.push_back({best, sizes[i]});
+  }
+}
+
+uint64_t range_mask(int offset, int size) {
+  return (size >= 64 ? ~0ULL : ((1ULL << size) - 1)) << offset;
+}
+
 dstack_status schedule(const dstack_sched_model* models, int n, const dstack_sched_params* prm,
                        dstack_schedule_out* out) {
   DS_CHECK(models && prm && out, DSTACK_E_INVALID, "schedule: null pointer");
   DS_CHECK(n >= 1 && n <= DSTACK_MAX_MODELS, DSTACK_E_INVALID, "schedule: 1..16 models");
-  DS_CHECK(prm->period_us > 0 && prm->total_slots >= 1 && prm->total_slots <= 64 && prm->overprov_slots >= 0,
+  DS_CHECK(prm->period_us > 0 && prm->total_slots >= 1 && prm->total_slots <= 64 && prm->overprov_slots >= 0 &&
+               (prm->placement == 0 || prm->placement == 1),
            DSTACK_E_INVALID, "schedule: bad params");
   std::memset(out, 0, sizeof(*out));
   out->n_models = n;
@@ -200,6 +239,13 @@ dstack_status schedule(const dstack_sched_model* models, int n, const dstack_sch
     out->latency_us[i] = bL;
   }
 
+  const bool home = prm->placement == 1;
+  std::vector<uint64_t> hmask(n, 0);
+  if (home) {
+    home_offsets(deployed.data(), n, total, out->home_offset);
+    for (int i = 0; i < n; ++i) hmask[i] = range_mask(out->home_offset[i], deployed[i]);
+  }
+
   // jobs in EDF order (deadline, SLO, model, k)
   struct J {
     int model, k;
@@ -228,22 +274,26 @@ dstack_status schedule(const dstack_sched_model* models, int n, const dstack_sch
     dj.k = j.k;
     dj.release_us = j.ws;
     dj.deadline_us = j.we;
-    // deployed slots, then the knee, then every smaller swept count
+    // deployed slots, then the knee, then every smaller swept count (home
+    // placement: the home range only)
     std::vector<int> opts{deployed[j.model]};
-    if (knee[j.model] != deployed[j.model]) opts.push_back(knee[j.model]);
     const Row& row = rows[j.model];
-    for (int q = (int)row.s.size() - 1; q >= 0; --q)
-      if (row.s[q] < knee[j.model]) opts.push_back(row.s[q]);
+    if (!home) {
+      if (knee[j.model] != deployed[j.model]) opts.push_back(knee[j.model]);
+      for (int q = (int)row.s.size() - 1; q >= 0; --q)
+        if (row.s[q] < knee[j.model]) opts.push_back(row.s[q]);
+    }
     bool done = false;
     for (int s : opts) {
       int64_t L = row.at(s);
       if (L <= 0) continue;
       int64_t t;
-      if (find_start(placed, j.ws, j.we, L, s, (j.k & 1) != 0, total, &t)) {
+      if (find_start(placed, j.ws, j.we, L, s, (j.k & 1) != 0, total, hmask[j.model], &t)) {
         dj.start_us = t;
         dj.duration_us = L;
         dj.slots = s;
-        placed.push_back(Placed{t, t + L, s, (int)o});
+        dj.slot_mask = hmask[j.model];
+        placed.push_back(Placed{t, t + L, s, (int)o, hmask[j.model]});
         done = true;
         break;
       }
@@ -258,7 +308,7 @@ dstack_status schedule(const dstack_sched_model* models, int n, const dstack_sch
   }
 
   // slot ids: in (start, placement order), lowest free ids at the start
-  std::vector<Placed> order = placed;
+  std::vector<Placed> order = home ? std::vector<Placed>() : placed;
   std::stable_sort(order.begin(), order.end(), [](const Placed& a, const Placed& b) {
     if (a.start != b.start) return a.start < b.start;
     return a.job < b.job;

@@ -61,9 +61,9 @@ def test_generate_params_errors():
     assert e.value.status == ds.E_INVALID
 
 
-def _lib_vs_oracle(models, period, total=32, overprov=2):
-    st, got = ds.schedule(models, period, total, overprov)
-    choices, jobs, util, ok = sched.schedule(models, period, total, overprov)
+def _lib_vs_oracle(models, period, total=32, overprov=2, placement="lowest"):
+    st, got = ds.schedule(models, period, total, overprov, placement)
+    choices, jobs, util, ok = sched.schedule(models, period, total, overprov, placement)
     assert (st == ds.OK) == ok
     assert got["batch"] == [c.batch for c in choices]
     assert got["knee_slots"] == [c.slots for c in choices]
@@ -96,6 +96,9 @@ def test_schedule_parity_config_shaped_tables():
     r50r = dict(r50, rate_per_s=400)
     mbr = dict(mb, rate_per_s=800)
     _lib_vs_oracle([r50r, mbr, vgg, lstm], 100000)
+    for ms in ([r50, mb], [r50r, mbr, vgg, lstm]):
+        got = _lib_vs_oracle(ms, 100000, placement="home")
+        assert got["home_offset"] == sched.home_offsets(got["deployed_slots"], 32)
 
 
 def test_schedule_parity_paper_table():
@@ -129,7 +132,8 @@ def test_schedule_parity_random():
                                table=table))
         if not models:
             continue
-        _lib_vs_oracle(models, rnd.choice([50000, 100000]), total=total, overprov=rnd.choice([0, 2]))
+        _lib_vs_oracle(models, rnd.choice([50000, 100000]), total=total, overprov=rnd.choice([0, 2]),
+                       placement=rnd.choice(["lowest", "home"]))
 
 
 def test_schedule_rejects_bad_arguments():

@@ -18,9 +18,9 @@ def amdahl(a, c, batches, slots=SWEEP):
     return {b: {s: int(a * (1 + 0.05 * b) + c * b / s) for s in slots} for b in batches}
 
 
-def compare(models, period, duration, arrivals, total=32, overprov=2, fod=True):
-    got = ds.simulate(models, period, duration, arrivals, total, overprov, fod)
-    ref = sched.simulate(models, period, duration, arrivals, total, overprov, fod)
+def compare(models, period, duration, arrivals, total=32, overprov=2, fod=True, placement="lowest"):
+    got = ds.simulate(models, period, duration, arrivals, total, overprov, fod, placement=placement)
+    ref = sched.simulate(models, period, duration, arrivals, total, overprov, fod, placement=placement)
     assert got["models"] == ref["models"]
     assert got["utilisation_ppm"] == ref["utilisation_ppm"]
     assert got["last_end_us"] == ref["last_end_us"]
@@ -42,10 +42,11 @@ def four_model_mix(scale=1):
     return models, arrivals
 
 
+@pytest.mark.parametrize("placement", ["lowest", "home"])
 @pytest.mark.parametrize("fod", [True, False])
-def test_four_model_mix_parity(fod):
+def test_four_model_mix_parity(fod, placement):
     models, arrivals = four_model_mix()
-    got = compare(models, 100000, 10_000_000, arrivals, fod=fod)
+    got = compare(models, 100000, 10_000_000, arrivals, fod=fod, placement=placement)
     if fod:
         assert sum(m["fod_runs"] for m in got["models"]) > 0
 
@@ -68,7 +69,7 @@ def test_random_parity():
                                rate_per_s=rnd.choice([0, 200, 800]), table=tab))
             arrivals.append(poisson_arrivals(trial * 10 + i, rnd.choice([50, 300, 1500]), 1_000_000))
         compare(models, rnd.choice([50000, 100000]), 1_000_000, arrivals, overprov=rnd.choice([0, 2]),
-                fod=rnd.random() < 0.8)
+                fod=rnd.random() < 0.8, placement=rnd.choice(["lowest", "home"]))
 
 
 def test_fod_raises_utilisation_paper_models():
@@ -101,9 +102,9 @@ def test_simulate_rejects_bad_traces():
 def test_simulation_invariants():
     """No instant has two running jobs on one slot or more slots than exist;
     nothing starts after the trace; each model runs one job at a time."""
-    for scale in (1, 8):
+    for scale, placement in ((1, "lowest"), (8, "lowest"), (8, "home")):
         models, arrivals = four_model_mix(scale)
-        r = sched.simulate(models, 100000, 10_000_000, arrivals)
+        r = sched.simulate(models, 100000, 10_000_000, arrivals, placement=placement)
         log = sorted(r["log"])
         for t0, t1, i, mask, kind, b in log:
             assert t0 < 10_000_000 and t1 > t0 and 1 <= b <= models[i]["max_batch"]

@@ -189,3 +189,70 @@ def test_plan_brute_force_small():
         if sum(m.slots * m.row[m.slots] * sched.ceil_div(10000, m.slo) for m in models) <= 4 * 10000 // 4:
             # load at most a quarter of capacity and each job fits its window alone
             assert not any(j.missed for j in jobs)
+
+
+# ---- home placement (one fixed slot range per model) ----
+
+def test_home_offsets_hand_cases():
+    # disjoint when they fit: largest first at 0, then the first zero-overlap offsets
+    assert sched.home_offsets([6, 10, 8], 32) == [18, 0, 10]
+    # 20 + 20 > 32: the second range goes where it overlaps the first least (offset 12, 8 slots)
+    assert sched.home_offsets([20, 20], 32) == [0, 12]
+    # equal sizes keep index order; a full-width range overlaps everything equally -> offset 0
+    assert sched.home_offsets([32, 4], 32) == [0, 0]
+    assert sched.home_offsets([5, 5, 5], 10) == [0, 5, 0]
+    assert sched.range_mask(3, 4) == 0b1111000
+
+
+def test_home_plan_disjoint_homes_closed_form():
+    """With disjoint homes nothing conflicts, so every job starts at its window
+    edge: even k at the window start, odd k at the window end minus L."""
+    models = [sched.PlanModel(slo=25000, knee=8, slots=10, row={10: 4000, 8: 5000}),
+              sched.PlanModel(slo=15000, knee=6, slots=8, row={8: 3000}),
+              sched.PlanModel(slo=50000, knee=10, slots=12, row={12: 20000})]
+    homes = sched.home_offsets([m.slots for m in models], 32)
+    assert homes == [12, 22, 0]
+    jobs = sched.plan(models, 100000, 32, homes)
+    for j in jobs:
+        m = models[j.model]
+        L = m.row[m.slots]
+        assert not j.missed and j.slots == m.slots and j.duration == L
+        assert j.slot_mask == sched.range_mask(homes[j.model], m.slots)
+        assert j.start == (j.release if j.k % 2 == 0 else j.deadline - L)
+
+
+def test_home_plan_overlapping_homes_serialise():
+    """Two models whose homes overlap never run at the same time; jobs keep
+    their windows, and the plan matches a hand-worked case."""
+    models = [sched.PlanModel(slo=50000, knee=18, slots=20, row={20: 30000}),
+              sched.PlanModel(slo=50000, knee=18, slots=20, row={20: 15000})]
+    homes = sched.home_offsets([20, 20], 32)
+    jobs = sched.plan(models, 100000, 32, homes)
+    # EDF order: (deadline 50000: m0 k0, m1 k0), (100000: m0 k1, m1 k1).
+    # m0 k0 at 0; m1 k0 earliest start clear of [0, 30000) is 30000; m0 k1
+    # (odd: latest) at 100000 - 30000; m1 k1 (odd: latest) cannot overlap
+    # [70000, 100000), so it ends there: 70000 - 15000.
+    got = [(j.model, j.k, j.start, j.missed) for j in jobs]
+    assert got == [(0, 0, 0, False), (1, 0, 30000, False), (0, 1, 70000, False), (1, 1, 55000, False)]
+
+
+def test_home_plan_invariants_random():
+    rnd = random.Random(17)
+    for _ in range(200):
+        models = []
+        for _ in range(rnd.randint(1, 5)):
+            grid = sorted(rnd.sample(range(1, 33), rnd.randint(2, 8)))
+            row, L = {}, rnd.randint(5000, 40000)
+            for s in grid:
+                L = max(500, int(L * rnd.uniform(0.5, 1.0)))
+                row[s] = L
+            kn = sched.knee(row, 8)
+            models.append(sched.PlanModel(slo=rnd.choice([15000, 25000, 30000, 50000, 100000]), knee=kn,
+                                          slots=sched.deployed_slots(kn), row=row))
+        homes = sched.home_offsets([m.slots for m in models], 32)
+        jobs = sched.plan(models, 100000, 32, homes)
+        _check_valid(models, jobs, 100000, sched.TOTAL_SLOTS)
+        for j in jobs:
+            if not j.missed:
+                assert j.slots == models[j.model].slots
+                assert j.slot_mask == sched.range_mask(homes[j.model], j.slots)
