@@ -298,6 +298,8 @@ typedef struct {
 
 typedef struct {
   int64_t served, violations, unserved, planned_runs, fod_runs, busy_us, p50_us, p99_us;
+  int64_t plan_skips;   /* planned starts that did not run (empty queue, model still running,
+                           or -- live launcher only -- its slots still held by an overrunning job) */
 } dstack_model_stats;
 
 typedef struct {
@@ -310,6 +312,46 @@ typedef struct {
 
 dstack_status dstack_simulate(const dstack_sched_model* models, int n_models, const dstack_sched_params* params,
                               const dstack_sim_params* sim, dstack_run_out* out);
+
+/* ------------------------------------------------------------------ */
+/* Live launcher (Sec. 6.1.2 on the GPU)                                */
+/* ------------------------------------------------------------------ */
+/* Runs the same plan and the same FOD decisions as dstack_simulate, on the
+ * host's monotonic clock (us since the call's start, after a warm-up) with
+ * real batches: model i owns one partition on its home range (placement
+ * must be 1) and every job of model i is dstack_infer(models[i], b, d_in[i],
+ * d_out[i], that partition).  Requests arrive when the clock passes their
+ * trace time; a job's requests complete when its end event is seen by the
+ * polling host thread (latency = that time - arrival).  Decisions use the
+ * timing table only (busy time is charged with the table latency); a planned
+ * start finds its home range still held by an overrunning job, or the model
+ * still running, and is skipped (plan_skips).  busy_us, the percentiles and
+ * utilisation_ppm use measured GPU time (device events around each job).
+ * Not reproducible run to run: job_hash covers the decisions taken.
+ *  - n_models in 1..4 (one CU-masked stream per model);
+ *  - d_in[i], d_out[i]: caller-owned device buffers sized for the model's
+ *    max batch (input and output shapes of dstack_model_query); every job
+ *    reads the first b rows of d_in[i] and writes those of d_out[i];
+ *  - tables[i]: the timing table of models[i] (max_batch <= the model's);
+ *  - the call blocks for about duration_us plus the last job, then waits for
+ *    the device; log (may be NULL) receives up to log_capacity job records,
+ *    *n_log the number of jobs started.
+ * Errors: E_INVALID (bad arguments, placement != 1), E_UNSUPPORTED (more
+ * than 4 models), E_HIP; the plan's E_INFEASIBLE is not an error here (the
+ * filled plan runs, as in dstack_simulate). */
+typedef struct {
+  int64_t start_us;     /* host clock at launch */
+  int64_t end_us;       /* host clock when completion was seen */
+  int64_t gpu_us;       /* device time between the job's start and end events */
+  int64_t table_us;     /* latency the decision assumed */
+  int model, batch, kind;  /* kind 0 planned, 1 FOD */
+  uint64_t slot_mask;
+} dstack_job_record;
+
+dstack_status dstack_serve(const dstack_model* models, int n_models, const void* const* d_in, void* const* d_out,
+                           const dstack_sched_model* tables, const dstack_sched_params* params,
+                           const dstack_sim_params* sim, dstack_run_out* out, dstack_job_record* log,
+                           int log_capacity, int* n_log);
 
 /* ------------------------------------------------------------------ */
 /* Kernel-level entry points (the layers of Sec. 4.1's A.int table)     */

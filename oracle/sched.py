@@ -319,7 +319,9 @@ def schedule(models, period, total=TOTAL_SLOTS, overprov=OVERPROVISION_SLOTS, pl
 #   starts at or after the end of the trace, and requests still queued when
 #   the last started job ends are unserved (also violations); utilisation
 #   counts slot-time inside [0, duration);
-# * runs/busy time are charged at job start; the session of time t is t // T.
+# * runs/busy time are charged at job start; the session of time t is t // T;
+# * a planned start that finds an empty queue or its model running is skipped
+#   (counted per model).
 # ---------------------------------------------------------------------------
 
 FNV_OFFSET = 0xcbf29ce484222325
@@ -385,6 +387,7 @@ def simulate(models, period, duration, arrivals, total=TOTAL_SLOTS, overprov=OVE
     lats = [[] for _ in range(n)]
     planned_runs = [0] * n
     fod_runs = [0] * n
+    plan_skips = [0] * n
     slot_us = 0
     h = FNV_OFFSET
     last_end = 0
@@ -462,6 +465,8 @@ def simulate(models, period, duration, arrivals, total=TOTAL_SLOTS, overprov=OVE
             mask, dur = payload
             if queue[i] and i not in running:
                 start_job(t, i, mask, dur, min(choices[i].batch, len(queue[i])), 0)
+            else:
+                plan_skips[i] += 1
         else:
             queue[i].append(t)
             if fod:
@@ -471,6 +476,6 @@ def simulate(models, period, duration, arrivals, total=TOTAL_SLOTS, overprov=OVE
         L = sorted(lats[i])
         out.append(dict(served=served[i], violations=late[i] + len(queue[i]), unserved=len(queue[i]),
                         planned_runs=planned_runs[i], fod_runs=fod_runs[i], busy_us=busy[i],
-                        p50_us=_nearest_rank(L, 50), p99_us=_nearest_rank(L, 99)))
+                        p50_us=_nearest_rank(L, 50), p99_us=_nearest_rank(L, 99), plan_skips=plan_skips[i]))
     return dict(models=out, utilisation_ppm=slot_us * 1000000 // (total * max(duration, 1)), job_hash=h,
                 last_end_us=last_end, log=log)

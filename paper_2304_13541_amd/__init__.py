@@ -80,7 +80,13 @@ class SimParams(ctypes.Structure):
 
 class ModelStats(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int64) for n in ("served", "violations", "unserved", "planned_runs", "fod_runs",
-                                               "busy_us", "p50_us", "p99_us")]
+                                               "busy_us", "p50_us", "p99_us", "plan_skips")]
+
+
+class JobRecord(ctypes.Structure):
+    _fields_ = [("start_us", ctypes.c_int64), ("end_us", ctypes.c_int64), ("gpu_us", ctypes.c_int64),
+                ("table_us", ctypes.c_int64), ("model", ctypes.c_int), ("batch", ctypes.c_int),
+                ("kind", ctypes.c_int), ("slot_mask", ctypes.c_uint64)]
 
 
 class RunOut(ctypes.Structure):
@@ -113,6 +119,9 @@ _SIGS = {
     "dstack_schedule": ([ctypes.POINTER(SchedModel), _i, ctypes.POINTER(SchedParams), ctypes.POINTER(ScheduleOut)], _i),
     "dstack_simulate": ([ctypes.POINTER(SchedModel), _i, ctypes.POINTER(SchedParams), ctypes.POINTER(SimParams),
                          ctypes.POINTER(RunOut)], _i),
+    "dstack_serve": ([ctypes.POINTER(_vp), _i, ctypes.POINTER(_vp), ctypes.POINTER(_vp), ctypes.POINTER(SchedModel),
+                      ctypes.POINTER(SchedParams), ctypes.POINTER(SimParams), ctypes.POINTER(RunOut),
+                      ctypes.POINTER(JobRecord), _i, ctypes.POINTER(_i)], _i),
     "dstack_op_conv2d": ([_vp, _i, _i, _i, _i, _vp, _i, _i, _i, _i, _i, _vp, _vp, _vp, _i, _vp, _i, _vp], _i),
     "dstack_op_dwconv3x3": ([_vp, _i, _i, _i, _i, _vp, _i, _vp, _vp, _i, _vp, _vp], _i),
     "dstack_fc_workspace_bytes": ([_i, _i, _i], _sz),
@@ -306,11 +315,8 @@ def _stats(out):
 PLACEMENTS = {"lowest": 0, "home": 1}
 
 
-def simulate(models, period_us, duration_us, arrivals, total_slots=TOTAL_SLOTS, overprov_slots=2, fod=True,
-             sessions_window=10, placement="lowest"):
-    """Launcher simulation on the timing table (see dstack_simulate).
-    arrivals: per model sorted integer-us arrival times.  Returns a dict."""
-    arr = _sched_models(models)
+def _sim_params(duration_us, arrivals, fod, sessions_window):
+    """SimParams plus the arrival buffers it points into (keep them alive)."""
     sp = SimParams()
     sp.duration_us = duration_us
     sp.fod = int(fod)
@@ -321,11 +327,42 @@ def simulate(models, period_us, duration_us, arrivals, total_slots=TOTAL_SLOTS, 
         keep.append(buf)
         sp.arrivals_us[i] = ctypes.cast(buf, ctypes.POINTER(ctypes.c_int64))
         sp.n_arrivals[i] = len(a)
+    return sp, keep
+
+
+def simulate(models, period_us, duration_us, arrivals, total_slots=TOTAL_SLOTS, overprov_slots=2, fod=True,
+             sessions_window=10, placement="lowest"):
+    """Launcher simulation on the timing table (see dstack_simulate).
+    arrivals: per model sorted integer-us arrival times.  Returns a dict."""
+    arr = _sched_models(models)
+    sp, keep = _sim_params(duration_us, arrivals, fod, sessions_window)
     out = RunOut()
     prm = SchedParams(period_us, total_slots, overprov_slots, PLACEMENTS[placement])
     _check(lib().dstack_simulate(arr, len(models), ctypes.byref(prm), ctypes.byref(sp), ctypes.byref(out)))
     return dict(models=_stats(out), utilisation_ppm=out.utilisation_ppm, job_hash=out.job_hash,
                 last_end_us=out.last_end_us)
+
+
+def serve(handles, tables, inputs, outputs, period_us, duration_us, arrivals, total_slots=TOTAL_SLOTS,
+          overprov_slots=2, fod=True, sessions_window=10, log_capacity=1 << 16):
+    """Live launcher (see dstack_serve): handles are Model objects, tables the
+    timing tables in the form simulate() takes, inputs/outputs device tensors
+    sized for each model's max batch.  Blocks for about duration_us."""
+    n = len(handles)
+    arr = _sched_models(tables)
+    sp, keep = _sim_params(duration_us, arrivals, fod, sessions_window)
+    hv = (_vp * n)(*[m.h.value for m in handles])
+    iv = (_vp * n)(*[t.data_ptr() for t in inputs])
+    ov = (_vp * n)(*[t.data_ptr() for t in outputs])
+    prm = SchedParams(period_us, total_slots, overprov_slots, PLACEMENTS["home"])
+    out = RunOut()
+    log = (JobRecord * max(1, log_capacity))()
+    n_log = ctypes.c_int(0)
+    _check(lib().dstack_serve(hv, n, iv, ov, arr, ctypes.byref(prm), ctypes.byref(sp), ctypes.byref(out), log,
+                              log_capacity, ctypes.byref(n_log)))
+    jobs = [dict((f, getattr(r, f)) for f, _ in JobRecord._fields_) for r in log[:min(n_log.value, log_capacity)]]
+    return dict(models=_stats(out), utilisation_ppm=out.utilisation_ppm, job_hash=out.job_hash,
+                last_end_us=out.last_end_us, n_jobs=n_log.value, log=jobs)
 
 
 def schedule(models, period_us, total_slots=TOTAL_SLOTS, overprov_slots=2, placement="lowest"):

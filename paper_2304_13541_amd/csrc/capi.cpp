@@ -12,6 +12,7 @@
 #include <string>
 #include <vector>
 
+#include "launcher.hpp"
 #include "model.hpp"
 #include "sched.hpp"
 
@@ -463,6 +464,13 @@ dstack_status dstack_schedule(const dstack_sched_model* models, int n, const dst
 dstack_status dstack_simulate(const dstack_sched_model* models, int n, const dstack_sched_params* prm,
                               const dstack_sim_params* sim, dstack_run_out* out) {
   return guarded([&] { return simulate(models, n, prm, sim, out); });
+}
+
+dstack_status dstack_serve(const dstack_model* models, int n, const void* const* d_in, void* const* d_out,
+                           const dstack_sched_model* tables, const dstack_sched_params* prm,
+                           const dstack_sim_params* sim, dstack_run_out* out, dstack_job_record* log,
+                           int log_capacity, int* n_log) {
+  return guarded([&] { return serve(models, n, d_in, d_out, tables, prm, sim, out, log, log_capacity, n_log); });
 }
 
 // ----------------------------------------------------- kernel-level ops ----

@@ -1,0 +1,79 @@
+// Decision state of the launcher, shared by the virtual-clock simulation
+// and the live launcher: per-model request queues, the slots in use, the
+// per-session run counts and busy time that rank the fair, opportunistic,
+// dynamic (FOD) fill of Sec. 6.1.2, and the planned starts of the session
+// plan repeated every period.  All times are integer microseconds from the
+// start of the run; busy time is charged at start with the timing-table
+// latency, so that the decisions depend on the table and the arrivals only.
+#pragma once
+#include <deque>
+#include <map>
+#include <vector>
+
+#include "sched.hpp"
+
+namespace dstack {
+
+struct PlannedStart {
+  int64_t t;
+  int model;
+  uint64_t mask;
+  int64_t dur;
+};
+
+class LaunchState {
+ public:
+  // plan: the dstack_schedule result for the same models and params
+  LaunchState(const dstack_sched_model* models, int n, const dstack_sched_params* prm, const dstack_sim_params* sim,
+              const dstack_schedule_out* plan);
+
+  const std::vector<PlannedStart>& planned() const { return pstarts_; }
+  int n() const { return n_; }
+  bool running(int i) const { return running_[i] != 0; }
+  bool free(uint64_t mask) const { return (used_ & mask) == 0; }
+  size_t queued(int i) const { return queue_[i].size(); }
+  void arrive(int i, int64_t t) { queue_[i].push_back(t); }
+  int plan_batch(int i) const { return plan_->batch[i]; }
+
+  struct Pick {
+    int model;
+    uint64_t mask;
+    int batch;
+    int64_t latency;
+  };
+  // the FOD choice at time t (false: nothing fits)
+  bool fod_pick(int64_t t, Pick* out) const;
+  // a job starts: pops b requests (returned, oldest first), charges the run
+  // and `charged_us` of busy time, marks its slots used
+  std::vector<int64_t> start(int64_t t, int i, uint64_t mask, int64_t charged_us, int b);
+  // the job of model i ended: frees its slots
+  void finish(int i);
+  // latency of batch b at `slots` from the table (largest swept count <= slots), -1 if none
+  int64_t table_latency(int i, int b, int slots) const;
+
+ private:
+  const dstack_sched_model* models_;
+  int n_;
+  const dstack_sched_params* prm_;
+  const dstack_sim_params* sim_;
+  const dstack_schedule_out* plan_;
+  int64_t T_, D_;
+  std::vector<PlannedStart> pstarts_;  // by time, then plan order
+  std::vector<std::deque<int64_t>> queue_;
+  std::vector<char> running_;
+  std::vector<uint64_t> run_mask_;
+  uint64_t used_ = 0;
+  std::vector<std::map<int64_t, int64_t>> runs_;  // session -> runs started
+  std::vector<int64_t> busy_;
+};
+
+// nearest-rank percentile (sorts v)
+int64_t nearest_rank(std::vector<int64_t>& v, int pct);
+// duration > 0, window >= 1, each model's arrivals sorted inside [0, duration)
+bool check_trace(int n, const dstack_sim_params* sim);
+
+dstack_status serve(const dstack_model* models, int n, const void* const* d_in, void* const* d_out,
+                    const dstack_sched_model* tables, const dstack_sched_params* prm, const dstack_sim_params* sim,
+                    dstack_run_out* out, dstack_job_record* log, int log_capacity, int* n_log);
+
+}  // namespace dstack

@@ -1,0 +1,250 @@
+// Live launcher: the session plan and the FOD fill of Sec. 6.1.2 driving
+// real batches on CU-masked streams.  Model i owns one partition on its home
+// range (the plan's home placement), so at most four masked streams exist at
+// once; the host thread follows the request trace on its monotonic clock,
+// launches planned and FOD jobs through dstack_infer, and polls each job's
+// end event.  The decisions are those of the virtual-clock simulation (the
+// same LaunchState, fed with table latencies); only the completion times and
+// GPU durations are measured.
+#include <hip/hip_runtime.h>
+
+#include <chrono>
+#include <cmath>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "launcher.hpp"
+
+namespace dstack {
+
+namespace {
+
+int64_t host_us() {
+  return std::chrono::duration_cast<std::chrono::microseconds>(std::chrono::steady_clock::now().time_since_epoch())
+      .count();
+}
+
+constexpr int kMaxServeModels = 4;
+constexpr int64_t kDrainLimitUs = 60LL * 1000 * 1000;  // a job still running this long after the trace: error
+const int kGrid[] = {1, 2, 4, 8, 16, 32};
+
+struct Running {
+  bool on = false;
+  int64_t start = 0, table_us = 0;
+  uint64_t mask = 0;
+  int batch = 0, kind = 0;
+  std::vector<int64_t> reqs;
+};
+
+struct Resources {
+  std::vector<dstack_partition> part;
+  std::vector<hipEvent_t> ev0, ev1;
+  bool drained = true;  // false: a job may still run, keep the partitions
+  ~Resources() {
+    for (hipEvent_t e : ev0)
+      if (e) (void)hipEventDestroy(e);
+    for (hipEvent_t e : ev1)
+      if (e) (void)hipEventDestroy(e);
+    if (drained)
+      for (dstack_partition p : part)
+        if (p) dstack_partition_destroy(p);
+  }
+};
+
+}  // namespace
+
+dstack_status serve(const dstack_model* models, int n, const void* const* d_in, void* const* d_out,
+                    const dstack_sched_model* tables, const dstack_sched_params* prm, const dstack_sim_params* sim,
+                    dstack_run_out* out, dstack_job_record* log, int log_capacity, int* n_log) {
+  DS_CHECK(models && d_in && d_out && tables && prm && sim && out, DSTACK_E_INVALID, "serve: null pointer");
+  DS_CHECK(n >= 1 && n <= DSTACK_MAX_MODELS, DSTACK_E_INVALID, "serve: bad model count");
+  DS_CHECK(n <= kMaxServeModels, DSTACK_E_UNSUPPORTED, "serve: at most 4 models (one CU-masked stream each)");
+  DS_CHECK(prm->placement == 1, DSTACK_E_INVALID, "serve: placement must be 1 (home ranges)");
+  DS_CHECK(log_capacity >= 0 && (log || log_capacity == 0), DSTACK_E_INVALID, "serve: bad log buffer");
+  DS_CHECK(check_trace(n, sim), DSTACK_E_INVALID, "serve: bad trace (see dstack_simulate)");
+  for (int i = 0; i < n; ++i) {
+    DS_CHECK(models[i] && d_in[i] && d_out[i], DSTACK_E_INVALID, "serve: null model or buffer");
+    dstack_model_info q;
+    dstack_status s = dstack_model_query(models[i], &q);
+    if (s != DSTACK_OK) return s;
+    DS_CHECK(tables[i].max_batch >= 1 && tables[i].max_batch <= q.max_batch, DSTACK_E_INVALID,
+             "serve: table max_batch above the model's");
+  }
+  std::vector<dstack_schedule_out> plan_box(1);
+  dstack_schedule_out* plan = &plan_box[0];
+  dstack_status st = schedule(tables, n, prm, plan);
+  if (st != DSTACK_OK && st != DSTACK_E_INFEASIBLE) return st;
+
+  Resources res;
+  res.part.assign(n, nullptr);
+  res.ev0.assign(n, nullptr);
+  res.ev1.assign(n, nullptr);
+  std::vector<hipStream_t> stream(n);
+  for (int i = 0; i < n; ++i) {
+    st = dstack_partition_create_at(plan->home_offset[i], plan->deployed_slots[i], &res.part[i]);
+    if (st != DSTACK_OK) return st;
+    void* sp = nullptr;
+    st = dstack_partition_query(res.part[i], nullptr, nullptr, &sp);
+    if (st != DSTACK_OK) return st;
+    stream[i] = (hipStream_t)sp;
+    DS_HIP(hipEventCreate(&res.ev0[i]));
+    DS_HIP(hipEventCreate(&res.ev1[i]));
+  }
+  LaunchState ls(tables, n, prm, sim, plan);
+
+  // warm-up: every batch a job of this run can take (captures its graph)
+  for (int i = 0; i < n; ++i) {
+    const int dep = plan->deployed_slots[i];
+    for (int b : kGrid) {
+      if (b > tables[i].max_batch) continue;
+      if (b != plan->batch[i] && ls.table_latency(i, b, dep) <= 0) continue;
+      for (int r = 0; r < 2; ++r) {
+        st = dstack_infer(models[i], b, d_in[i], d_out[i], res.part[i]);
+        if (st != DSTACK_OK) return st;
+      }
+    }
+  }
+  for (int i = 0; i < n; ++i) {
+    st = dstack_synchronize(res.part[i]);
+    if (st != DSTACK_OK) return st;
+  }
+
+  const int64_t D = sim->duration_us;
+  const int total = prm->total_slots;
+  std::vector<Running> run(n);
+  std::vector<int64_t> served(n, 0), late(n, 0), pruns(n, 0), fruns(n, 0), skips(n, 0), busy(n, 0);
+  std::vector<std::vector<int64_t>> lats(n);
+  std::vector<int> next_arr(n, 0);
+  size_t next_plan = 0;
+  int64_t slot_us = 0, last_end = 0;
+  uint64_t h = 0xcbf29ce484222325ULL;
+  int jobs = 0;
+  const std::vector<PlannedStart>& P = ls.planned();
+  const int64_t t0 = host_us();
+  auto clock = [&] { return host_us() - t0; };
+
+  auto launch = [&](int64_t t, int i, uint64_t mask, int64_t table_us, int b, int kind) -> dstack_status {
+    Running& r = run[i];
+    r.reqs = ls.start(t, i, mask, table_us, b);
+    r.on = true;
+    r.start = t;
+    r.table_us = table_us;
+    r.mask = mask;
+    r.batch = b;
+    r.kind = kind;
+    DS_HIP(hipEventRecord(res.ev0[i], stream[i]));
+    dstack_status s = dstack_infer(models[i], b, d_in[i], d_out[i], res.part[i]);
+    if (s != DSTACK_OK) return s;
+    DS_HIP(hipEventRecord(res.ev1[i], stream[i]));
+    for (int64_t v : {t, (int64_t)i, (int64_t)b, (int64_t)mask, table_us, (int64_t)kind})
+      for (int k = 0; k < 8; ++k) {
+        h ^= ((uint64_t)v >> (8 * k)) & 0xff;
+        h *= 0x100000001b3ULL;
+      }
+    (kind == 0 ? pruns : fruns)[i] += 1;
+    return DSTACK_OK;
+  };
+  auto fod_pass = [&](int64_t t) -> dstack_status {
+    LaunchState::Pick pk;
+    if (sim->fod && ls.fod_pick(t, &pk)) return launch(t, pk.model, pk.mask, pk.latency, pk.batch, 1);
+    return DSTACK_OK;
+  };
+
+  // every decision and launch reads the clock when it is taken, so that a
+  // job's start is never before the completion that freed its slots
+  for (;;) {
+    const int64_t t = clock();
+    bool busy_now = false;
+    // completions
+    for (int i = 0; i < n; ++i) {
+      if (!run[i].on) continue;
+      const hipError_t q = hipEventQuery(res.ev1[i]);
+      if (q == hipErrorNotReady) {
+        busy_now = true;
+        continue;
+      }
+      if (q != hipSuccess) {
+        res.drained = false;
+        return fail(DSTACK_E_HIP, std::string("serve: ") + hipGetErrorString(q));
+      }
+      float ms = 0.f;
+      DS_HIP(hipEventElapsedTime(&ms, res.ev0[i], res.ev1[i]));
+      const int64_t gpu_us = (int64_t)llround((double)ms * 1000.0);
+      const int64_t te = clock();
+      Running& r = run[i];
+      r.on = false;
+      ls.finish(i);
+      for (int64_t a : r.reqs) {
+        served[i] += 1;
+        lats[i].push_back(te - a);
+        if (te - a > tables[i].slo_us) late[i] += 1;
+      }
+      busy[i] += gpu_us;
+      slot_us += (int64_t)__builtin_popcountll(r.mask) * std::max<int64_t>(0, std::min(r.start + gpu_us, D) - r.start);
+      last_end = std::max(last_end, te);
+      if (jobs < log_capacity)
+        log[jobs] = dstack_job_record{r.start, te, gpu_us, r.table_us, i, r.batch, r.kind, r.mask};
+      ++jobs;
+      st = fod_pass(te);
+      if (st != DSTACK_OK) return st;
+    }
+    // planned starts that are due
+    while (next_plan < P.size() && P[next_plan].t <= t) {
+      const PlannedStart& ps = P[next_plan++];
+      const int i = ps.model;
+      if (ls.queued(i) && !ls.running(i) && ls.free(ps.mask)) {
+        st = launch(clock(), i, ps.mask, ps.dur, std::min<int>(ls.plan_batch(i), (int)ls.queued(i)), 0);
+        if (st != DSTACK_OK) return st;
+        busy_now = true;
+      } else {
+        skips[i] += 1;
+      }
+    }
+    // arrivals that are due, in time order
+    for (;;) {
+      int j = -1;
+      for (int i = 0; i < n; ++i)
+        if (next_arr[i] < sim->n_arrivals[i] && sim->arrivals_us[i][next_arr[i]] <= t &&
+            (j < 0 || sim->arrivals_us[i][next_arr[i]] < sim->arrivals_us[j][next_arr[j]]))
+          j = i;
+      if (j < 0) break;
+      ls.arrive(j, sim->arrivals_us[j][next_arr[j]]);
+      next_arr[j] += 1;
+      st = fod_pass(clock());
+      if (st != DSTACK_OK) return st;
+    }
+    for (int i = 0; i < n; ++i) busy_now = busy_now || run[i].on;
+    if (t >= D && !busy_now) break;
+    if (t > D + kDrainLimitUs) {
+      res.drained = false;
+      return fail(DSTACK_E_HIP, "serve: a job did not complete within 60 s after the trace");
+    }
+  }
+  for (int i = 0; i < n; ++i) {
+    st = dstack_synchronize(res.part[i]);
+    if (st != DSTACK_OK) return st;
+  }
+
+  std::memset(out, 0, sizeof(*out));
+  out->n_models = n;
+  for (int i = 0; i < n; ++i) {
+    dstack_model_stats& s = out->models[i];
+    s.served = served[i];
+    s.unserved = (int64_t)ls.queued(i);
+    s.violations = late[i] + s.unserved;
+    s.planned_runs = pruns[i];
+    s.fod_runs = fruns[i];
+    s.busy_us = busy[i];
+    s.p50_us = nearest_rank(lats[i], 50);
+    s.p99_us = nearest_rank(lats[i], 99);
+    s.plan_skips = skips[i];
+  }
+  out->utilisation_ppm = (int64_t)((unsigned __int128)slot_us * 1000000 / ((unsigned __int128)total * (uint64_t)D));
+  out->job_hash = h;
+  out->last_end_us = last_end;
+  if (n_log) *n_log = jobs;
+  return DSTACK_OK;
+}
+
+}  // namespace dstack
