@@ -1,26 +1,33 @@
 """Benchmark: multi-DNN spatial multiplexing on one MI355X.
 
-Workload (one GPU): ResNet-50 v1.5 at batch 16 (SLO 25 ms) and MobileNetV2
-1.0 at batch 32 (SLO 15 ms), synthetic N(0,1) 224x224x3 bf16 images standing
-in for ImageNet, random-weight bf16 models.
+Headline workload (one GPU): ResNet-50 v1.5 at batch 16 (SLO 25 ms) and
+MobileNetV2 1.0 at batch 32 (SLO 15 ms), synthetic N(0,1) 224x224x3 bf16
+images standing in for ImageNet, random-weight bf16 models.
 
 Setup (untimed): load both models and sweep each over batches {1,2,4,8,16[,32]}
 x CU fractions 10%..100% (knee sweep: median latency of 20 timed forwards per
 point).  At the workload's batch each model's knee is the efficacy optimum
 b/(L^2 s) over the swept slot counts; it is deployed with 2 slots of
-over-provisioning.  The CU-masked partitions (disjoint slot ranges) are packed
-over the 32 slots round-robin over the models -- instances of one model share
-its weights -- up to 4 partitions (more concurrently active masked queues are
-avoided on this part).  The SLO-constrained (batch, slots) choice of
-dstack_schedule over the whole table is reported alongside.
+over-provisioning (shrunk proportionally when the models do not fit together).
+The CU-masked partitions (disjoint slot ranges) are packed over the 32 slots
+round-robin over the models, up to 4 partitions (more concurrently active
+masked queues are avoided on this part).  The SLO-constrained (batch, slots)
+choice of dstack_schedule over the whole table is reported alongside.
 
-One step = one 100 ms session: each partition runs r = ceil(100 ms / SLO)
-batches of its model back to back, all partitions concurrently.  Value =
-aggregate inferences/s over K steps.  The time-sliced full-GPU baseline runs
-the same per-model batch counts one batch at a time on an unmasked
-partition.  Per-kernel HIP-event timing on each partition's stream gives the
-conv MFMA TFLOP/s at the knee and the roofline fraction of the dominant
-kernel (the implicit-GEMM convolution).
+One step = ceil(100 ms / SLO) batches of each partition's model, back to back,
+all partitions concurrently (closed loop).  Value = aggregate inferences/s
+over K steps.  The time-sliced full-GPU baseline runs the same per-model batch
+counts one batch at a time on an unmasked partition.  Per-kernel HIP-event
+timing on each partition's stream gives the conv MFMA TFLOP/s at the knee and
+the roofline fraction of the dominant kernel (the implicit-GEMM convolution);
+each partition's batch time alone vs in the mix gives the interference.
+
+Also reported (not the headline): the VGG-19 batch 8 + LSTM batch 32 pair in
+the same closed-loop form ("config4"), and the four-model Poisson mix
+(ResNet-50, MobileNetV2, VGG-19, LSTM at 400/800/150/300 req/s, SLOs
+25/15/50/30 ms, 100 ms sessions) through the live launcher dstack_serve for
+10 s at the stated rates plus a capacity sweep of 2 s runs at k x the rates
+("config5"); --headline-only skips both.
 """
 import argparse
 import hashlib
@@ -53,7 +60,7 @@ CONV_SRC = os.path.join(ROOT, "paper_2304_13541_amd", "csrc", "conv_igemm.hip")
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=20)
+    p.add_argument("--steps", type=int, default=200)
     p.add_argument("--warmup", type=int, default=3)
     p.add_argument("--sweep-warmup", type=int, default=5)
     p.add_argument("--sweep-reps", type=int, default=20)
@@ -61,6 +68,10 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--table", default=None, help="load a timing table JSON instead of sweeping")
     p.add_argument("--save-table", default=None)
+    p.add_argument("--steps4", type=int, default=40, help="steps of the VGG-19 + LSTM pair")
+    p.add_argument("--serve-seconds", type=float, default=10.0, help="four-model mix at the stated rates")
+    p.add_argument("--capacity-seconds", type=float, default=2.0, help="each point of the capacity sweep")
+    p.add_argument("--headline-only", action="store_true", help="skip the VGG-19 + LSTM pair and the four-model mix")
     return p.parse_args()
 
 
@@ -124,6 +135,210 @@ def knee_at(row, b):
     return best
 
 
+def fit_slots(dep, total):
+    """Deployed slot counts that fit together: shrink proportionally (round
+    half-up), then take slots from the largest until the sum fits."""
+    if sum(dep) <= total:
+        return list(dep)
+    tot = sum(dep)
+    out = [max(1, int(math.floor(s * total / tot + 0.5))) for s in dep]
+    while sum(out) > total:
+        out[out.index(max(out))] -= 1
+    return out
+
+
+def pack_lanes(dep, total, max_parts):
+    """Disjoint (model, slot offset, slots) partitions, round-robin over the
+    models while they fit, at most max_parts of them."""
+    lanes, off, i, misses, n = [], 0, 0, 0, len(dep)
+    while misses < n and len(lanes) < max_parts:
+        mi = i % n
+        if off + dep[mi] <= total:
+            lanes.append((mi, off, dep[mi]))
+            off += dep[mi]
+            misses = 0
+        else:
+            misses += 1
+        i += 1
+    return lanes
+
+
+class Mix:
+    """Closed-loop concurrent run of several models on disjoint CU-masked
+    partitions, and the time-sliced full-GPU run of the same work."""
+
+    def __init__(self, ds, torch, models, batch, xs, out_shapes, lanes, reps):
+        from tests import gpu_util as gu
+        self.ds, self.torch, self.models, self.batch, self.xs = ds, torch, models, batch, xs
+        self.lanes, self.reps = lanes, reps
+        self.parts = [ds.Partition(slot_offset=o, n_slots=s) for _, o, s in lanes]
+        self.ys = [gu.empty_f32(out_shapes[mi]) for mi, _, _ in lanes]
+        self.lane_count = [sum(1 for l in lanes if l[0] == mi) for mi in range(len(models))]
+        self.items_per_step = sum(reps[mi] * batch[mi] for mi, _, _ in lanes)
+
+    def _sync(self, parts):
+        for p in parts:
+            p.synchronize()
+        self.torch.cuda.synchronize()
+
+    def run(self, steps, lanes=None):
+        lanes = range(len(self.lanes)) if lanes is None else lanes
+        for _ in range(steps):
+            for li in lanes:
+                mi = self.lanes[li][0]
+                for _r in range(self.reps[mi]):
+                    self.models[mi].infer(self.batch[mi], self.xs[mi], self.ys[li], self.parts[li])
+
+    def timed(self, steps, warmup, lanes=None):
+        self.run(warmup, lanes)
+        self._sync(self.parts)
+        t0 = time.perf_counter()
+        self.run(steps, lanes)
+        self._sync(self.parts)
+        return time.perf_counter() - t0
+
+    def timesliced(self, steps, warmup, out_shapes):
+        from tests import gpu_util as gu
+        full = self.ds.Partition(1.0)
+        yf = [gu.empty_f32(sh) for sh in out_shapes]
+
+        def go(k):
+            for _ in range(k):
+                for mi, m in enumerate(self.models):
+                    for _r in range(self.lane_count[mi] * self.reps[mi]):
+                        m.infer(self.batch[mi], self.xs[mi], yf[mi], full)
+        go(warmup)
+        full.synchronize()
+        t0 = time.perf_counter()
+        go(steps)
+        full.synchronize()
+        dt = time.perf_counter() - t0
+        full.destroy()
+        return dt
+
+    def interference(self, steps, warmup, t_mix, mix_steps):
+        """Per lane: time per batch alone on its partition (steps steps) vs in
+        the mix (t_mix over mix_steps steps)."""
+        out = []
+        for li, (mi, o, s) in enumerate(self.lanes):
+            alone = self.timed(steps, warmup, [li]) / (steps * self.reps[mi])
+            mixed = t_mix / (mix_steps * self.reps[mi])
+            out.append(dict(lane=li, model=mi, slot_offset=o, slots=s, alone_us=1e6 * alone, mixed_us=1e6 * mixed,
+                            slowdown=mixed / alone))
+        return out
+
+    def destroy(self):
+        for p in self.parts:
+            p.destroy()
+
+
+def layer_stats(ds, m, batch, x, y, part):
+    """Per-kind kernel totals of three profiled forwards (HIP events on the partition's stream)."""
+    recs = m.profile_layers(batch, x, y, part)
+    for _ in range(2):
+        for r, r2 in zip(recs, m.profile_layers(batch, x, y, part)):
+            r["ms"] += r2["ms"]
+    for r in recs:
+        r["ms"] /= 3.0
+    by_kind = {}
+    for r in recs:
+        d = by_kind.setdefault(ds.KIND_NAMES[r["kind"]], dict(n=0, ms=0.0, flops=0.0, bytes=0.0))
+        d["n"] += 1
+        d["ms"] += r["ms"]
+        d["flops"] += r["flops"]
+        d["bytes"] += r["bytes"]
+    return recs, by_kind
+
+
+def config4(ds, torch, args):
+    """VGG-19 batch 8 + 2-layer LSTM batch 32, closed loop on deployed-knee
+    partitions (shrunk proportionally to fit), vs time-sliced full GPU."""
+    from tests import inputs
+    specs = [("vgg19", 1040, 8, [8]), ("lstm2", 1041, 32, [32])]
+    models = [ds.Model(a, s) for a, s, _, _ in specs]
+    batch = [b for _, _, b, _ in specs]
+    rows = []
+    for (arch, seed, b, _), m in zip(specs, models):
+        r = m.knee_sweep(b, FRACTIONS, warmup=args.sweep_warmup, reps=args.sweep_reps)
+        rows.append(dict(zip(r["slots"], r["latency_us"])))
+    knee = [knee_at(r, b) for r, b in zip(rows, batch)]
+    dep = fit_slots([min(32, k + OVERPROV) for k in knee], 32)
+    lanes = [(0, 0, dep[0]), (1, dep[0], dep[1])]
+    lat = [rows[i][max(s for s in rows[i] if s <= dep[i])] for i in range(2)]
+    reps = [max(1, int(round(20000 / L))) for L in lat]  # each lane busy about 20 ms per step
+    xs = [gu_dev(inputs.image_batch(1041, 8)), gu_dev(inputs.sequence_batch(1042, 32))]
+    shapes = [m.output_shape(b) for m, b in zip(models, batch)]
+    mix = Mix(ds, torch, models, batch, xs, shapes, lanes, reps)
+    steps = args.steps4
+    t_mix = mix.timed(steps, 2)
+    t_seq = mix.timesliced(steps, 2, shapes)
+    inter = mix.interference(max(2, steps // 4), 1, t_mix, steps)
+    res = dict(workload="VGG-19 batch 8 + 2-layer LSTM (512->1024, T=50) batch 32, closed loop on deployed-knee "
+                        "partitions; inferences = images + sequences",
+               knee_slots=knee, deployed_slots=dep, reps_per_step=reps, steps=steps,
+               value=mix.items_per_step * steps / t_mix, timesliced=mix.items_per_step * steps / t_seq,
+               speedup_vs_timesliced=t_seq / t_mix, interference=inter,
+               per_model_inf_s=[reps[i] * batch[i] * steps / t_mix for i in range(2)],
+               latency_rows={specs[i][0]: rows[i] for i in range(2)})
+    mix.destroy()
+    for m in models:
+        m.destroy()
+    return res
+
+
+def gu_dev(a):
+    from tests import gpu_util as gu
+    return gu.dev_bf16(a)
+
+
+def config5(ds, torch, models4, tables4, args):
+    """Four-model Poisson mix through the live launcher (plan + FOD on home
+    ranges): stated rates for args.serve_seconds, then a capacity sweep."""
+    from tests import inputs
+    rates = [400, 800, 150, 300]
+    slos = [25000, 15000, 50000, 30000]
+    bmax = [16, 32, 8, 32]
+    xs, ys = [], []
+    for m, b in zip(models4, bmax):
+        shp = m.input_shape(b)
+        if len(shp) == 3:
+            xs.append(gu_dev(inputs.sequence_batch(1051, shp[1], shp[0], shp[2])))
+        else:
+            xs.append(gu_dev(inputs.image_batch(1050, b)))
+        ys.append(torch.empty(m.output_shape(b), device="cuda", dtype=torch.float32))
+
+    def one(k, dur_us):
+        tabs = [dict(slo_us=slo, max_batch=b, rate_per_s=r * k, table=t)
+                for slo, b, r, t in zip(slos, bmax, rates, tables4)]
+        arr = [inputs.poisson_arrivals(2026 + i, r * k, dur_us) for i, r in enumerate(rates)]
+        r = ds.serve(models4, tabs, xs, ys, PERIOD_US, dur_us, arr, log_capacity=0)
+        n_req = sum(len(a) for a in arr)
+        viol = sum(s["violations"] for s in r["models"])
+        st, plan = ds.schedule(tabs, PERIOD_US, placement="home")
+        return dict(k=k, offered_req_s=n_req / (dur_us * 1e-6), served_req_s=sum(s["served"] for s in r["models"]) /
+                    (dur_us * 1e-6), violations_per_s=viol / (dur_us * 1e-6), violation_frac=viol / max(1, n_req),
+                    utilisation_ppm=r["utilisation_ppm"], n_jobs=r["n_jobs"],
+                    plan=dict(batch=plan["batch"], deployed_slots=plan["deployed_slots"],
+                              home_offset=plan["home_offset"], utilisation_ppm=plan["utilisation_ppm"],
+                              status="ok" if st == ds.OK else "infeasible"),
+                    per_model=[dict(arch=m.arch, **s) for m, s in zip(models4, r["models"])])
+    stated = one(1, int(args.serve_seconds * 1e6))
+    sweep, capacity = [], None
+    for k in (2, 4, 8, 16):
+        r = one(k, int(args.capacity_seconds * 1e6))
+        sweep.append({kk: r[kk] for kk in ("k", "offered_req_s", "served_req_s", "violation_frac", "utilisation_ppm")})
+        if r["violation_frac"] <= 0.01:
+            capacity = r["offered_req_s"]
+        else:
+            break
+    if capacity is None and stated["violation_frac"] <= 0.01:
+        capacity = stated["offered_req_s"]
+    return dict(workload="four-model Poisson mix (ResNet-50, MobileNetV2, VGG-19, LSTM at 400/800/150/300 req/s, "
+                         "SLOs 25/15/50/30 ms, 100 ms sessions) through dstack_serve on home CU ranges",
+                stated_rates=stated, capacity_sweep=sweep, capacity_req_s_at_1pct=capacity,
+                capacity_seconds=args.capacity_seconds)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -156,24 +371,9 @@ def main():
 
     batch = [b for _, _, _, b, _ in MODELS]
     knee = [knee_at(t["table"][b], b) for t, b in zip(tables, batch)]
-    dep = [min(ds.TOTAL_SLOTS, k + OVERPROV) for k in knee]
+    dep = fit_slots([min(ds.TOTAL_SLOTS, k + OVERPROV) for k in knee], ds.TOTAL_SLOTS)
     reps = [math.ceil(PERIOD_US / slo) for _, _, slo, _, _ in MODELS]
-    lanes, off = [], 0  # (model, slot offset, slots)
-    if sum(dep) > ds.TOTAL_SLOTS:  # shrink proportionally: one partition per model
-        tot = sum(dep)
-        dep = [max(1, math.floor(s * ds.TOTAL_SLOTS / tot)) for s in dep]
-    i, misses = 0, 0
-    while misses < n_models and len(lanes) < MAX_PARTITIONS:
-        mi = i % n_models
-        if off + dep[mi] <= ds.TOTAL_SLOTS:
-            lanes.append((mi, off, dep[mi]))
-            off += dep[mi]
-            misses = 0
-        else:
-            misses += 1
-        i += 1
-    parts = [ds.Partition(slot_offset=o, n_slots=s) for _, o, s in lanes]
-    lane_count = [sum(1 for l in lanes if l[0] == mi) for mi in range(n_models)]
+    lanes = pack_lanes(dep, ds.TOTAL_SLOTS, MAX_PARTITIONS)
 
     # the SLO-constrained choice over the whole table (reported; Sec. 5.1)
     sched_in = [dict(slo_us=slo, max_batch=b, rate_per_s=0, table=t["table"])
@@ -181,57 +381,20 @@ def main():
     sched_st, plan = ds.schedule(sched_in, PERIOD_US)
 
     xs = [gu.dev_bf16(inputs.image_batch(seed + 1, b)) for (a, seed, *_), b in zip(MODELS, batch)]
-    ys = [gu.empty_f32((batch[mi], 1000)) for mi, _, _ in lanes]
-
-    def run_mix(k):
-        for _ in range(k):
-            for li, (mi, _, _) in enumerate(lanes):
-                for _r in range(reps[mi]):
-                    models[mi].infer(batch[mi], xs[mi], ys[li], parts[li])
-
-    def sync_all():
-        for p in parts:
-            p.synchronize()
-        torch.cuda.synchronize()
-
-    run_mix(args.warmup)
-    sync_all()
-    t0 = time.perf_counter()
-    run_mix(args.steps)
-    sync_all()
-    t_mix = time.perf_counter() - t0
-    items_per_step = sum(reps[mi] * batch[mi] for mi, _, _ in lanes)
-    value = items_per_step * args.steps / t_mix
-
-    # ---- time-sliced baseline: same batches and per-model counts, one at a time, whole GPU ----
-    full = ds.Partition(1.0)
-    yf = [gu.empty_f32((b, 1000)) for b in batch]
-
-    def run_seq(k):
-        for _ in range(k):
-            for mi, m in enumerate(models):
-                for _r in range(lane_count[mi] * reps[mi]):
-                    m.infer(batch[mi], xs[mi], yf[mi], full)
-    run_seq(args.warmup)
-    full.synchronize()
-    t0 = time.perf_counter()
-    run_seq(args.steps)
-    full.synchronize()
-    t_seq = time.perf_counter() - t0
-    seq_value = items_per_step * args.steps / t_seq
-    full.destroy()
+    shapes = [(b, 1000) for b in batch]
+    mix = Mix(ds, torch, models, batch, xs, shapes, lanes, reps)
+    t_mix = mix.timed(args.steps, args.warmup)
+    value = mix.items_per_step * args.steps / t_mix
+    t_seq = mix.timesliced(args.steps, args.warmup, shapes)
+    seq_value = mix.items_per_step * args.steps / t_seq
+    inter = mix.interference(max(5, args.steps // 4), args.warmup, t_mix, args.steps)
 
     # ---- per-kernel timing at the deployed partitions (HIP events on each partition's stream) ----
     per_model = []
     conv_fl, conv_ms, conv_n, conv_by = 0.0, 0.0, 0, 0.0
     for i, m in enumerate(models):
         li = next(k for k, l in enumerate(lanes) if l[0] == i)
-        recs = m.profile_layers(batch[i], xs[i], ys[li], parts[li])
-        for _ in range(2):  # average of three profiled forwards
-            for r, r2 in zip(recs, m.profile_layers(batch[i], xs[i], ys[li], parts[li])):
-                r["ms"] += r2["ms"]
-        for r in recs:
-            r["ms"] /= 3.0
+        recs, by_kind = layer_stats(ds, m, batch[i], xs[i], mix.ys[li], mix.parts[li])
         mf = [r for r in recs if r["kind"] == 0]
         fl = sum(r["flops"] for r in mf)
         ms = sum(r["ms"] for r in mf)
@@ -239,27 +402,39 @@ def main():
         conv_ms += ms
         conv_n += len(mf)
         conv_by += sum(r["bytes"] for r in mf)
-        by_kind = {}
-        for r in recs:
-            d = by_kind.setdefault(ds.KIND_NAMES[r["kind"]], dict(n=0, ms=0.0, flops=0.0, bytes=0.0))
-            d["n"] += 1
-            d["ms"] += r["ms"]
-            d["flops"] += r["flops"]
-            d["bytes"] += r["bytes"]
-        n_cu = parts[li].n_cu
+        n_cu = mix.parts[li].n_cu
         tf = fl / (ms * 1e-3) / 1e12 if ms > 0 else None
         per_model.append(dict(
             arch=MODELS[i][0], batch=batch[i], knee_slots=knee[i], slots=dep[i], n_cu=n_cu,
-            partitions=lane_count[i], jobs_per_step=reps[i], latency_us_at_knee=tables[i]["table"][batch[i]][knee[i]],
+            partitions=mix.lane_count[i], jobs_per_step=reps[i],
+            latency_us_at_knee=tables[i]["table"][batch[i]][knee[i]],
             conv_mfma_tflops=tf, conv_frac_of_partition_peak=tf / (PEAK_BF16_TFLOPS * n_cu / 256) if tf else None,
             slo_optimal=dict(batch=plan["batch"][i], knee_slots=plan["knee_slots"][i],
                              deployed_slots=plan["deployed_slots"][i], latency_us=plan["latency_us"][i],
                              feasible=plan["feasible"][i]),
             kernels=by_kind))
+    mix.destroy()
     avg_ms = conv_ms / max(conv_n, 1)
     achieved = (conv_fl / max(conv_n, 1)) / (avg_ms * 1e-3) / 1e12
     knee_cu = sum(p["n_cu"] * p["kernels"]["mfma"]["ms"] for p in per_model) / max(
         sum(p["kernels"]["mfma"]["ms"] for p in per_model), 1e-9)
+
+    # ---- the other workloads: VGG-19 + LSTM pair, four-model Poisson mix through the live launcher ----
+    c4 = c5 = None
+    if not args.headline_only:
+        c4 = config4(ds, torch, args)
+        extra = [("vgg19", 1052, [1, 2, 4, 8]), ("lstm2", 1053, [1, 2, 4, 8, 16, 32])]
+        m4 = [ds.Model(a, s) for a, s, _ in extra]
+        t4 = [t["table"] for t in tables]
+        for (a, s, bs), m in zip(extra, m4):
+            tab = {}
+            for b in bs:
+                r = m.knee_sweep(b, FRACTIONS, warmup=args.sweep_warmup, reps=args.sweep_reps)
+                tab[b] = dict(zip(r["slots"], r["latency_us"]))
+            t4.append(tab)
+        c5 = config5(ds, torch, models + m4, t4, args)
+        for m in m4:
+            m.destroy()
 
     # calibration copy for the HBM byte counters (a plain 256 MiB device copy)
     a = torch.empty(64 * 1024 * 1024, dtype=torch.float32, device="cuda:0")
@@ -285,16 +460,17 @@ def main():
         "config": {
             "workload": "two-model mix: ResNet-50 v1.5 batch 16 (SLO 25 ms) + MobileNetV2 1.0 batch 32 "
                         "(SLO 15 ms), 224x224x3, each on CU-masked partitions of its knee + 2 slots packed "
-                        "over the 32 slots; one step = one 100 ms session per partition",
+                        "over the 32 slots; one step = ceil(100 ms / SLO) batches per partition, closed loop",
             "batch": batch, "knee_slots": knee, "deployed_slots": dep,
             "partitions": [(MODELS[mi][0], o, s) for mi, o, s in lanes],
-            "jobs_per_step": reps, "items_per_step": items_per_step, "seeds": [s for _, s, *_ in MODELS],
+            "jobs_per_step": reps, "items_per_step": mix.items_per_step, "seeds": [s for _, s, *_ in MODELS],
             "parallelism": "spatial (CU masks), 1 GPU",
         },
         "conv_mfma_tflops_at_knee": conv_fl / (conv_ms * 1e-3) / 1e12,
         "conv_knee_cu": knee_cu,
         "timesliced_inferences_per_s": seq_value,
         "speedup_vs_timesliced": value / seq_value,
+        "interference": inter,
         "roofline": {
             "bound": "mfma", "kernel": "conv_igemm (all launches of both models at their partitions)",
             "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS,
@@ -307,6 +483,8 @@ def main():
         "cpu_baseline": cpu,
         "schedule_status": "ok" if sched_st == ds.OK else "infeasible",
         "per_model": per_model,
+        "config4": c4,
+        "config5": c5,
         "timing_tables": {t["arch"]: {str(b): row for b, row in t["table"].items()} for t in tables},
         "sweep_seconds": sweep_s,
     }

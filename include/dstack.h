@@ -329,9 +329,11 @@ dstack_status dstack_simulate(const dstack_sched_model* models, int n_models, co
  * utilisation_ppm use measured GPU time (device events around each job).
  * Not reproducible run to run: job_hash covers the decisions taken.
  *  - n_models in 1..4 (one CU-masked stream per model);
- *  - d_in[i], d_out[i]: caller-owned device buffers sized for the model's
- *    max batch (input and output shapes of dstack_model_query); every job
- *    reads the first b rows of d_in[i] and writes those of d_out[i];
+ *  - d_in[i], d_out[i]: caller-owned device buffers holding the model's
+ *    input and output at tables[i].max_batch (shapes of dstack_model_query);
+ *    a job of batch b reads its input from the start of d_in[i] and writes
+ *    its output to the start of d_out[i], in the layouts of dstack_infer at
+ *    batch b (the trace's requests carry no data of their own);
  *  - tables[i]: the timing table of models[i] (max_batch <= the model's);
  *  - the call blocks for about duration_us plus the last job, then waits for
  *    the device; log (may be NULL) receives up to log_capacity job records,
