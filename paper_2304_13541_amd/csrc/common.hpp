@@ -23,6 +23,15 @@ enum Act { ACT_NONE = 0, ACT_RELU = 1, ACT_RELU6 = 2 };
 void set_error(const std::string& msg);
 void clear_error();
 
+// Optional events that a launcher attaches to its kernels' own dispatch
+// packets (hipExtLaunchKernelGGL): `start` takes the begin timestamp of the
+// first kernel of the operation, `stop` the end timestamp of the last one.
+// Set by the per-kernel profiler for one launch at a time; null otherwise.
+struct DispatchEvents {
+  hipEvent_t start = nullptr, stop = nullptr;
+};
+DispatchEvents& dispatch_events();
+
 inline dstack_status fail(dstack_status st, const std::string& msg) {
   set_error(msg);
   return st;

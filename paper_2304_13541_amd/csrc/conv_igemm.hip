@@ -32,6 +32,8 @@
 // Split-K: with gridDim.z = splits > 1 each z-slice accumulates a range of
 // depth tiles and writes raw fp32 partial sums to a workspace; a second
 // kernel sums the slices and applies the epilogue.
+#include <hip/hip_ext.h>
+
 #include "common.hpp"
 
 namespace dstack {
@@ -496,6 +498,15 @@ size_t conv_splitk_workspace_bytes(int M, int K, int Kg, int n_cu) {
   return p.splits > 1 ? (size_t)p.splits * M * K * sizeof(float) : 0;
 }
 
+// 256-thread launch; through hipExtLaunchKernelGGL when dispatch events are armed
+template <typename K>
+static void launch_k(K kernel, dim3 grid, hipStream_t st, hipEvent_t e0, hipEvent_t e1, const ConvArgs& a) {
+  if (e0 || e1)
+    hipExtLaunchKernelGGL(kernel, grid, dim3(256), 0, st, e0, e1, 0, a);
+  else
+    hipLaunchKernelGGL(kernel, grid, dim3(256), 0, st, a);
+}
+
 // Ring depth per tile shape: the deepest ring (at most 4) with which two
 // blocks still share a CU's 160 KB of LDS, so that two blocks and STAGES-1
 // tiles each keep loads in flight.
@@ -516,12 +527,16 @@ static void launch_mode(ConvArgs a, bool f32, int splits, hipStream_t st) {
   a.tiles = ceil_div(a.M, BM) * a.tiles_n;
   a.div_tn = FastDiv::make(a.tiles_n);
   dim3 grid(a.tiles, 1, splits);
+  // with dispatch events armed: start on this kernel, stop on it too unless
+  // a split-K reduce follows (that kernel takes the stop)
+  const DispatchEvents& de = dispatch_events();
+  hipEvent_t e0 = de.start, e1 = splits > 1 ? nullptr : de.stop;
   if (splits > 1)
-    hipLaunchKernelGGL((conv_igemm_kernel<BN, BM, WN, WM, STAGES, MODE, false, true>), grid, dim3(256), 0, st, a);
+    launch_k(conv_igemm_kernel<BN, BM, WN, WM, STAGES, MODE, false, true>, grid, st, e0, e1, a);
   else if (f32)
-    hipLaunchKernelGGL((conv_igemm_kernel<BN, BM, WN, WM, STAGES, MODE, true, false>), grid, dim3(256), 0, st, a);
+    launch_k(conv_igemm_kernel<BN, BM, WN, WM, STAGES, MODE, true, false>, grid, st, e0, e1, a);
   else
-    hipLaunchKernelGGL((conv_igemm_kernel<BN, BM, WN, WM, STAGES, MODE, false, false>), grid, dim3(256), 0, st, a);
+    launch_k(conv_igemm_kernel<BN, BM, WN, WM, STAGES, MODE, false, false>, grid, st, e0, e1, a);
 }
 
 template <int BN, int BM, int WN, int WM>
@@ -583,8 +598,12 @@ dstack_status launch_conv2d_ws(const bf16* x, int N, int H, int W, int C, const 
     launch_cfg<32, 128, 1, 4>(a, mode, out_fp32, p.splits, st);
   if (p.splits > 1) {
     long nq = (long)a.M * (K / 4);
-    hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)((nq + 255) / 256)), dim3(256), 0, st, a, p.splits,
-                       out_fp32 ? 1 : 0);
+    const dim3 rg((unsigned)((nq + 255) / 256));
+    hipEvent_t e1 = dispatch_events().stop;
+    if (e1)
+      hipExtLaunchKernelGGL(splitk_reduce_kernel, rg, dim3(256), 0, st, nullptr, e1, 0, a, p.splits, out_fp32 ? 1 : 0);
+    else
+      hipLaunchKernelGGL(splitk_reduce_kernel, rg, dim3(256), 0, st, a, p.splits, out_fp32 ? 1 : 0);
   }
   DS_HIP(hipGetLastError());
   return DSTACK_OK;

@@ -530,7 +530,24 @@ void KernelTimer::before() {
   }
 }
 
+DispatchEvents& dispatch_events() {
+  static thread_local DispatchEvents ev;
+  return ev;
+}
+
+void KernelTimer::before_dispatch() {
+  (void)hipEventCreate(&ds_start);
+  (void)hipEventCreate(&ds_stop);
+  dispatch_events() = DispatchEvents{ds_start, ds_stop};
+}
+
 void KernelTimer::after(int kind, double flops, double bytes, int m, int n, int k) {
+  if (ds_start) {  // timed by the kernels' own dispatch packets
+    recs.push_back(Rec{kind, flops, bytes, ds_start, ds_stop, m, n, k});
+    ds_start = ds_stop = nullptr;
+    dispatch_events() = DispatchEvents{};
+    return;
+  }
   hipEvent_t e;
   (void)hipEventCreate(&e);
   (void)hipEventRecord(e, st);
@@ -544,6 +561,9 @@ KernelTimer::~KernelTimer() {
     (void)hipEventDestroy(r.b);
   }
   if (pending) (void)hipEventDestroy(pending);
+  if (ds_start) (void)hipEventDestroy(ds_start);
+  if (ds_stop) (void)hipEventDestroy(ds_stop);
+  dispatch_events() = DispatchEvents{};
 }
 
 static double conv_flops(const Op& op, int b) {
@@ -604,7 +624,12 @@ dstack_status forward(Model& m, int batch, const void* d_in, void* d_out, Worksp
       if (s != DSTACK_OK) return s;
       continue;
     }
-    if (timer) timer->before();
+    if (timer) {  // convolutions: timestamps of their own dispatches; others: events around them
+      if (op.kind == OP_CONV)
+        timer->before_dispatch();
+      else
+        timer->before();
+    }
     int kind = KC_GLUE;
     double fl = 0, by = 0;
     int gm = 0, gn = 0, gk = 0;

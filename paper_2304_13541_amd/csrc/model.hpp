@@ -132,7 +132,9 @@ struct KernelTimer {
   hipStream_t st;
   std::vector<Rec> recs;
   hipEvent_t pending = nullptr;
+  hipEvent_t ds_start = nullptr, ds_stop = nullptr;  // armed dispatch events (before_dispatch)
   void before();
+  void before_dispatch();
   void after(int kind, double flops, double bytes, int m = 0, int n = 0, int k = 0);
   ~KernelTimer();
 };
