@@ -34,6 +34,8 @@
 // kernel sums the slices and applies the epilogue.
 #include <hip/hip_ext.h>
 
+#include <type_traits>
+
 #include "common.hpp"
 
 namespace dstack {
@@ -281,10 +283,12 @@ __global__ __launch_bounds__(256) void conv_igemm_kernel(ConvArgs a) {
         const int h0 = ho * a.stride - a.pad, w0 = wo * a.stride - a.pad;
         if (MODE == MODE_TILED) {
           aoff[j] = ((((nn * a.H + h0) * a.W + w0) * a.C) + c * 8) * 2;
+          // window rows [rlo, rhi) and columns [slo, shi) fall inside the image
+          const int rlo = max(0, -h0), rhi = min(a.R, a.H - h0);
+          const int slo = max(0, -w0), shi = min(a.S, a.W - w0);
+          const unsigned cols = shi > slo ? (unsigned)((1ull << shi) - (1ull << slo)) : 0u;  // S <= 32
           for (int rr = 0; rr < a.R; ++rr)
-            for (int ss = 0; ss < a.S; ++ss)
-              if ((unsigned)(h0 + rr) < (unsigned)a.H && (unsigned)(w0 + ss) < (unsigned)a.W)
-                vmask[j] |= 1u << (rr * a.S + ss);
+            if (rr >= rlo && rr < rhi) vmask[j] |= cols << (rr * a.S);
         } else {
           aoff[j] = nn * a.H * a.W;  // image's first pixel
           vmask[j] = 1;
@@ -434,22 +438,37 @@ __global__ __launch_bounds__(256) void conv_igemm_kernel(ConvArgs a) {
   }
   const f32x4 sc = a.scale ? *reinterpret_cast<const f32x4*>(a.scale + ch0) : f32x4{1.f, 1.f, 1.f, 1.f};
   const f32x4 sh = a.shift ? *reinterpret_cast<const f32x4*>(a.shift + ch0) : f32x4{0.f, 0.f, 0.f, 0.f};
+  // element index of the thread's first row; rows step by RSTEP pixels
+  // (M * K < 2^31 is checked at launch)
+  const int idx0 = (m0 + pl0) * a.K + ch0;
+  const int dstep = RSTEP * a.K;
   bf16x4 rv[ROWS_PT];
 #pragma unroll
   for (int k = 0; k < ROWS_PT; ++k) {
     const int px = m0 + pl0 + k * RSTEP;
-    rv[k] = (a.res && px < a.M) ? *reinterpret_cast<const bf16x4*>(a.res + (long)px * a.K + ch0) : bf16x4{};
+    rv[k] = (a.res && px < a.M) ? *reinterpret_cast<const bf16x4*>(a.res + idx0 + k * dstep) : bf16x4{};
   }
+  // the activation is chosen once: none, or a clamp to [0, hi] (ReLU: hi = inf)
+  const float hi = a.act == ACT_RELU6 ? 6.0f : INFINITY;
+  auto rows = [&](auto clamp) {
 #pragma unroll
-  for (int k = 0; k < ROWS_PT; ++k) {
-    const int pl = pl0 + k * RSTEP, px = m0 + pl;
-    if (px >= a.M) continue;
-    const f32x4 t = *reinterpret_cast<const f32x4*>(ct + cidx(pl, cl));
-    float v[4];
+    for (int k = 0; k < ROWS_PT; ++k) {
+      const int pl = pl0 + k * RSTEP;
+      if (m0 + pl >= a.M) continue;
+      const f32x4 t = *reinterpret_cast<const f32x4*>(ct + cidx(pl, cl));
+      float v[4];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) v[e] = apply_act(t[e] * sc[e] + sh[e] + (float)rv[k][e], a.act);
-    store_out4(a.y, OUT_F32, (long)px * a.K + ch0, v);
-  }
+      for (int e = 0; e < 4; ++e) {
+        v[e] = t[e] * sc[e] + sh[e] + (float)rv[k][e];
+        if (decltype(clamp)::value) v[e] = fminf(fmaxf(v[e], 0.0f), hi);
+      }
+      store_out4(a.y, OUT_F32, idx0 + k * dstep, v);
+    }
+  };
+  if (a.act == ACT_NONE)
+    rows(std::false_type{});
+  else
+    rows(std::true_type{});
 }
 
 // Sum split-K partial slices and apply the epilogue; one thread per 4 channels.
