@@ -471,6 +471,182 @@ __global__ __launch_bounds__(256) void conv_igemm_kernel(ConvArgs a) {
     rows(std::true_type{});
 }
 
+// 256-thread launch; through hipExtLaunchKernelGGL when dispatch events are armed
+template <typename K, typename... Args>
+static void launch_k(K kernel, dim3 grid, hipStream_t st, hipEvent_t e0, hipEvent_t e1, Args... args) {
+  if (e0 || e1)
+    hipExtLaunchKernelGGL(kernel, grid, dim3(256), 0, st, e0, e1, 0, args...);
+  else
+    hipLaunchKernelGGL(kernel, grid, dim3(256), 0, st, args...);
+}
+
+// 1x1, stride-1 convolution of small depth (C <= 32): a streaming GEMM that
+// stages nothing of its inputs in LDS.  The output (M x K) is many times the
+// input (M x C) and the weights (K x C) are tiny, so the layer is bound by
+// writing its output.  Each wave keeps NB channel blocks (16 channels each)
+// of weight fragments in registers (A operand; depth in KS steps of 32, zero
+// past C) and walks pixel groups of 16: the group's B fragment is read
+// straight from the input rows (lane l: pixel l % 16, depth 8 * (l / 16) ..
+// + 8), and NB x KS MFMAs give each lane 4 consecutive channels of one pixel
+// per block.  Scale and shift are applied there; with more than one block
+// the fp32 tile then goes through the wave's own LDS region (rows padded by
+// 16 bytes) so that each lane finishes 8 consecutive channels of one pixel:
+// residual reads and output stores are 16-byte pieces of whole pixel rows.  The next group's
+// fragment is loaded before the current one is multiplied.  Grid: x strides
+// over pixel groups (4 waves per block), y over channel chunks of 16 * NB.
+template <int NB, int KS, bool OUT_F32>
+__global__ __launch_bounds__(256) void conv_igemm_1x1s_kernel(ConvArgs a, int groups) {
+  constexpr int RS = 16 * NB + 4;  // staged row stride in floats
+  __shared__ __attribute__((aligned(16))) float stage[4][16 * RS];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int row = lane & 15, kq = (lane >> 4) * 8;
+  const int cb0 = blockIdx.y * NB;  // first 16-channel block of this chunk
+  float* my = stage[wave];
+  bf16x8 wa[NB][KS];
+#pragma unroll
+  for (int b = 0; b < NB; ++b) {
+    const int ch = (cb0 + b) * 16 + row;
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      const int k = s * 32 + kq;
+      wa[b][s] = (ch < a.K && k < a.C) ? *reinterpret_cast<const bf16x8*>(a.w + (long)ch * a.C + k) : bf16x8{};
+    }
+  }
+  // per-lane scale and shift of its 4 channels in every block, kept across groups
+  f32x4 sc[NB], sh[NB];
+#pragma unroll
+  for (int b = 0; b < NB; ++b) {
+    const int ch0 = (cb0 + b) * 16 + 4 * (lane >> 4);
+    const bool in = ch0 < a.K;
+    sc[b] = (in && a.scale) ? *reinterpret_cast<const f32x4*>(a.scale + ch0) : f32x4{1.f, 1.f, 1.f, 1.f};
+    sh[b] = (in && a.shift) ? *reinterpret_cast<const f32x4*>(a.shift + ch0) : f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  const bool clamp = a.act != ACT_NONE;
+  const float hi = a.act == ACT_RELU6 ? 6.0f : INFINITY;
+  auto load_px = [&](int g, bf16x8 (&bx)[KS]) {
+    const int px = g * 16 + row;
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      const int k = s * 32 + kq;
+      bx[s] = (g < groups && px < a.M && k < a.C) ? *reinterpret_cast<const bf16x8*>(a.x + (long)px * a.C + k)
+                                                  : bf16x8{};
+    }
+  };
+  const int stride = gridDim.x * 4;
+  int g = blockIdx.x * 4 + wave;
+  bf16x8 cur[KS], nxt[KS];
+  load_px(g, cur);
+  for (; g < groups; g += stride) {
+    load_px(g + stride, nxt);
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s = 0; s < KS; ++s) acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wa[b][s], cur[s], acc, 0, 0, 0);
+      // C layout: lane holds channels 4 * (lane / 16) + i of block b, pixel lane % 16
+      f32x4 t;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) t[i] = acc[i] * sc[b][i] + sh[b][i];
+      if (NB == 1) {  // 16-channel rows: the 64 lanes' 8-byte pieces already tile whole rows
+        const int px = g * 16 + row, ch0 = cb0 * 16 + 4 * (lane >> 4);
+        if (px < a.M && ch0 < a.K) {
+          const int idx = px * a.K + ch0;
+          const bf16x4 r4 = a.res ? *reinterpret_cast<const bf16x4*>(a.res + idx) : bf16x4{};
+          float v[4];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const float u = t[i] + (float)r4[i];
+            v[i] = clamp ? fminf(fmaxf(u, 0.0f), hi) : u;
+          }
+          store_out4(a.y, OUT_F32, idx, v);
+        }
+      } else {
+        *reinterpret_cast<f32x4*>(my + row * RS + 16 * b + 4 * (lane >> 4)) = t;
+      }
+    }
+    if (NB == 1) {
+#pragma unroll
+      for (int s = 0; s < KS; ++s) cur[s] = nxt[s];
+      continue;
+    }
+    // the wave reads back what its own lanes wrote (LDS keeps a wave's order)
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    // 16 pixels x 2*NB pieces of 8 channels
+#pragma unroll
+    for (int p = 0; p < (32 * NB + 63) / 64; ++p) {
+      const int e = p * 64 + lane;
+      if (e >= 32 * NB) break;
+      const int pl = e / (2 * NB), c8 = e - pl * (2 * NB);
+      const int px = g * 16 + pl, ch = cb0 * 16 + 8 * c8;
+      if (px >= a.M || ch >= a.K) continue;
+      const f32x4 t0 = *reinterpret_cast<const f32x4*>(my + pl * RS + 8 * c8);
+      const f32x4 t1 = *reinterpret_cast<const f32x4*>(my + pl * RS + 8 * c8 + 4);
+      const int idx = px * a.K + ch;
+      const bf16x8 r8 = a.res ? *reinterpret_cast<const bf16x8*>(a.res + idx) : bf16x8{};
+      float v[8];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        v[i] = t0[i] + (float)r8[i];
+        v[i + 4] = t1[i] + (float)r8[i + 4];
+      }
+#pragma unroll
+      for (int i = 0; i < 8; ++i) v[i] = clamp ? fminf(fmaxf(v[i], 0.0f), hi) : v[i];
+      if (OUT_F32) {
+        float* yo = reinterpret_cast<float*>(a.y) + idx;
+        *reinterpret_cast<f32x4*>(yo) = f32x4{v[0], v[1], v[2], v[3]};
+        *reinterpret_cast<f32x4*>(yo + 4) = f32x4{v[4], v[5], v[6], v[7]};
+      } else {
+        bf16x8 o;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) o[i] = (bf16)v[i];
+        *reinterpret_cast<bf16x8*>(reinterpret_cast<bf16*>(a.y) + idx) = o;
+      }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+    for (int s = 0; s < KS; ++s) cur[s] = nxt[s];
+  }
+}
+
+template <int NB, int KS>
+static void launch_1x1s_nb(const ConvArgs& a, bool f32, int n_cu, hipStream_t st) {
+  const int groups = ceil_div(a.M, 16);
+  const int chunks = ceil_div(a.K, 16 * NB);
+  // about 32 waves per CU over all chunks (their loads in flight hide the
+  // latency of the next group); every wave walks >= 1 group
+  const int bx = max(1, min(ceil_div(groups, 4), ceil_div(n_cu * 8, chunks)));
+  const dim3 grid(bx, chunks);
+  const DispatchEvents& de = dispatch_events();
+  if (f32)
+    launch_k(conv_igemm_1x1s_kernel<NB, KS, true>, grid, st, de.start, de.stop, a, groups);
+  else
+    launch_k(conv_igemm_1x1s_kernel<NB, KS, false>, grid, st, de.start, de.stop, a, groups);
+}
+
+// channel blocks per wave: the largest divisor of K / 16 that is at most 8
+static void launch_1x1s(const ConvArgs& a, bool f32, int n_cu, hipStream_t st) {
+  const int blocks = a.K / 16;
+  int nb = 8;
+  while (blocks % nb) --nb;
+#define DS_NB_CASE(N)                   \
+  case N:                               \
+    launch_1x1s_nb<N, 1>(a, f32, n_cu, st); \
+    break;
+  switch (nb) {
+    DS_NB_CASE(1)
+    DS_NB_CASE(2)
+    DS_NB_CASE(3)
+    DS_NB_CASE(4)
+    DS_NB_CASE(5)
+    DS_NB_CASE(6)
+    DS_NB_CASE(7)
+    DS_NB_CASE(8)
+  }
+#undef DS_NB_CASE
+}
+
 // Sum split-K partial slices and apply the epilogue; one thread per 4 channels.
 __global__ void splitk_reduce_kernel(ConvArgs a, int splits, int out_f32) {
   long q = (long)blockIdx.x * blockDim.x + threadIdx.x;
@@ -515,15 +691,6 @@ static ConvPlan choose_plan(int M, int K, int Kg, int n_cu) {
 size_t conv_splitk_workspace_bytes(int M, int K, int Kg, int n_cu) {
   ConvPlan p = choose_plan(M, K, Kg, n_cu);
   return p.splits > 1 ? (size_t)p.splits * M * K * sizeof(float) : 0;
-}
-
-// 256-thread launch; through hipExtLaunchKernelGGL when dispatch events are armed
-template <typename K>
-static void launch_k(K kernel, dim3 grid, hipStream_t st, hipEvent_t e0, hipEvent_t e1, const ConvArgs& a) {
-  if (e0 || e1)
-    hipExtLaunchKernelGGL(kernel, grid, dim3(256), 0, st, e0, e1, 0, a);
-  else
-    hipLaunchKernelGGL(kernel, grid, dim3(256), 0, st, a);
 }
 
 // Ring depth per tile shape: the deepest ring (at most 4) with which two
@@ -596,6 +763,11 @@ dstack_status launch_conv2d_ws(const bf16* x, int N, int H, int W, int C, const 
   a.div_c = FastDiv::make(C);
   a.div_s = FastDiv::make(S);
   const bool one = R == 1 && S == 1 && pad == 0;
+  if (one && stride == 1 && C <= 32 && K % 16 == 0) {  // small depth: the streaming kernel
+    launch_1x1s(a, out_fp32, n_cu > 0 ? n_cu : 256, st);
+    DS_HIP(hipGetLastError());
+    return DSTACK_OK;
+  }
   const int mode = one ? (stride == 1 ? MODE_1X1S1 : MODE_1X1)
                        : (C % BK == 0 && R * S <= 32 ? MODE_TILED : MODE_GENERIC);
   ConvPlan p = choose_plan(a.M, K, a.Kg, n_cu);

@@ -34,6 +34,15 @@ CONV_CASES = [
     (1, 14, 14, 256, 1028, 1, 2, 0, 0, False, True),
     (4, 7, 7, 512, 512, 3, 1, 1, 1, False, False),
     (1, 1, 1, 520, 4, 1, 1, 0, 0, False, True),
+    # 1x1 stride 1 with C <= 32 and K % 16 == 0: the streaming small-depth kernel
+    # (ragged pixel counts, depth tails inside a 32-deep step, 1..8 channel blocks per wave);
+    # C = 64 and 40 take the tiled kernel
+    (2, 9, 7, 16, 96, 1, 1, 0, 2, False, False),
+    (1, 11, 11, 24, 144, 1, 1, 0, 2, False, False),
+    (3, 5, 7, 32, 16, 1, 1, 0, 0, False, True),
+    (2, 6, 6, 64, 256, 1, 1, 0, 1, True, False),
+    (1, 3, 3, 8, 48, 1, 1, 0, 1, False, False),
+    (1, 4, 5, 40, 80, 1, 1, 0, 2, True, True),
 ]
 
 
