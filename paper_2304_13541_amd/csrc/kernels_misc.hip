@@ -11,47 +11,85 @@ __device__ __forceinline__ bf16x8 ld8(const bf16* p) { return *reinterpret_cast<
 __device__ __forceinline__ void st8(bf16* p, bf16x8 v) { *reinterpret_cast<bf16x8*>(p) = v; }
 
 // ------------------------------------------------------------ depthwise ----
-// One thread per (output pixel, 8-channel group).  Weights in [3][3][C].
-template <int STRIDE>
+// Thread = 8 channels (one 16-byte vector) x V consecutive output pixels of
+// one output row.  The 9 weight vectors stay in registers; the input rows are
+// walked once each: row r contributes input columns wo0*STRIDE-1 ..
+// (wo0+V-1)*STRIDE+1, every column loaded once and used by the (up to 3)
+// outputs whose window covers it.  Loads per V outputs: 3 * ((V-1)*STRIDE+3)
+// vectors instead of 9 * V.  Consecutive threads take consecutive channel
+// vectors of the same pixels (coalesced 16-byte accesses); padding reads zero.
+// Weights in [3][3][C].
+template <int STRIDE, int V>
 __global__ __launch_bounds__(256) void dwconv3x3_kernel(const bf16* __restrict__ x, int N, int H, int W, int C,
                                                         const bf16* __restrict__ w, const float* __restrict__ scale,
                                                         const float* __restrict__ shift, int act,
                                                         bf16* __restrict__ y, int Ho, int Wo) {
+  constexpr int COLS = (V - 1) * STRIDE + 3;  // input columns a row of the window spans
   const int CV = C >> 3;
-  long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
-  long total = (long)N * Ho * Wo * CV;
+  const int segs = (Wo + V - 1) / V;
+  const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  const long total = (long)N * Ho * segs * CV;
   if (idx >= total) return;
-  int cv = (int)(idx % CV);
-  long pix = idx / CV;
-  int wo = (int)(pix % Wo);
-  long t = pix / Wo;
-  int ho = (int)(t % Ho);
-  int n = (int)(t / Ho);
-  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  const int cv = (int)(idx % CV);
+  long t = idx / CV;
+  const int seg = (int)(t % segs);
+  t /= segs;
+  const int ho = (int)(t % Ho);
+  const int n = (int)(t / Ho);
+  const int wo0 = seg * V;
+  const int wi0 = wo0 * STRIDE - 1;
+
+  bf16x8 wv[9];
+#pragma unroll
+  for (int k = 0; k < 9; ++k) wv[k] = ld8(w + k * C + cv * 8);
+  float acc[V][8];
+#pragma unroll
+  for (int v = 0; v < V; ++v)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[v][e] = 0.f;
+
 #pragma unroll
   for (int r = 0; r < 3; ++r) {
-    int hi = ho * STRIDE - 1 + r;
+    const int hi = ho * STRIDE - 1 + r;
     if ((unsigned)hi >= (unsigned)H) continue;
+    const bf16* xrow = x + (((long)n * H + hi) * W) * C + cv * 8;
 #pragma unroll
-    for (int s = 0; s < 3; ++s) {
-      int wi = wo * STRIDE - 1 + s;
-      if ((unsigned)wi >= (unsigned)W) continue;
-      bf16x8 xv = ld8(x + (((long)n * H + hi) * W + wi) * C + cv * 8);
-      bf16x8 wv = ld8(w + (r * 3 + s) * C + cv * 8);
+    for (int c = 0; c < COLS; ++c) {
+      const int wi = wi0 + c;
+      const bf16x8 xv = (unsigned)wi < (unsigned)W ? ld8(xrow + (long)wi * C) : bf16x8{};
+      // outputs v whose window column s = c - v*STRIDE lies in 0..2
 #pragma unroll
-      for (int e = 0; e < 8; ++e) acc[e] += (float)xv[e] * (float)wv[e];
+      for (int v = 0; v < V; ++v) {
+        const int s = c - v * STRIDE;
+        if (s < 0 || s > 2) continue;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[v][e] += (float)xv[e] * (float)wv[r * 3 + s][e];
+      }
     }
   }
   const f32x4* sc = reinterpret_cast<const f32x4*>(scale + cv * 8);
   const f32x4* sh = reinterpret_cast<const f32x4*>(shift + cv * 8);
-  f32x4 s0 = sc[0], s1 = sc[1], h0 = sh[0], h1 = sh[1];
-  bf16x8 o;
+  const f32x4 s0 = sc[0], s1 = sc[1], h0 = sh[0], h1 = sh[1];
+  bf16* yrow = y + (((long)n * Ho + ho) * Wo) * C + cv * 8;
 #pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    o[e] = (bf16)apply_act(acc[e] * s0[e] + h0[e], act);
-    o[e + 4] = (bf16)apply_act(acc[e + 4] * s1[e] + h1[e], act);
+  for (int v = 0; v < V; ++v) {
+    if (wo0 + v >= Wo) break;
+    bf16x8 o;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      o[e] = (bf16)apply_act(acc[v][e] * s0[e] + h0[e], act);
+      o[e + 4] = (bf16)apply_act(acc[v][e + 4] * s1[e] + h1[e], act);
+    }
+    st8(yrow + (long)(wo0 + v) * C, o);
   }
-  st8(y + pix * C + cv * 8, o);
+}
+
+template <int STRIDE, int V>
+static void dw_launch(const bf16* x, int N, int H, int W, int C, const bf16* w, const float* scale,
+                      const float* shift, int act, bf16* y, int Ho, int Wo, hipStream_t st) {
+  const long total = (long)N * Ho * ((Wo + V - 1) / V) * (C / 8);
+  hipLaunchKernelGGL((dwconv3x3_kernel<STRIDE, V>), dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st, x, N, H,
+                     W, C, w, scale, shift, act, y, Ho, Wo);
 }
 
 dstack_status launch_dwconv3x3(const bf16* x, int N, int H, int W, int C, const bf16* w_rsc, int stride,
@@ -59,13 +97,17 @@ dstack_status launch_dwconv3x3(const bf16* x, int N, int H, int W, int C, const 
   DS_CHECK(C % 8 == 0, DSTACK_E_UNSUPPORTED, "dwconv3x3: C must be a multiple of 8");
   DS_CHECK(stride == 1 || stride == 2, DSTACK_E_UNSUPPORTED, "dwconv3x3: stride must be 1 or 2");
   DS_CHECK(N > 0 && H > 0 && W > 0, DSTACK_E_INVALID, "dwconv3x3: bad shape");
-  int Ho = out_dim(H, 3, stride, 1), Wo = out_dim(W, 3, stride, 1);
-  long total = (long)N * Ho * Wo * (C / 8);
-  dim3 grid((unsigned)((total + 255) / 256));
-  if (stride == 1)
-    hipLaunchKernelGGL(dwconv3x3_kernel<1>, grid, dim3(256), 0, st, x, N, H, W, C, w_rsc, scale, shift, act, y, Ho, Wo);
-  else
-    hipLaunchKernelGGL(dwconv3x3_kernel<2>, grid, dim3(256), 0, st, x, N, H, W, C, w_rsc, scale, shift, act, y, Ho, Wo);
+  DS_CHECK(scale && shift, DSTACK_E_INVALID, "dwconv3x3: scale and shift are required");
+  const int Ho = out_dim(H, 3, stride, 1), Wo = out_dim(W, 3, stride, 1);
+  // outputs per thread along W: 8 on stride-1 rows at least 28 wide, else 4
+  if (stride == 1) {
+    if (Wo >= 28)
+      dw_launch<1, 8>(x, N, H, W, C, w_rsc, scale, shift, act, y, Ho, Wo, st);
+    else
+      dw_launch<1, 4>(x, N, H, W, C, w_rsc, scale, shift, act, y, Ho, Wo, st);
+  } else {
+    dw_launch<2, 4>(x, N, H, W, C, w_rsc, scale, shift, act, y, Ho, Wo, st);
+  }
   DS_HIP(hipGetLastError());
   return DSTACK_OK;
 }
