@@ -159,32 +159,46 @@ dstack_status launch_maxpool(const bf16* x, int N, int H, int W, int C, int k, i
   return DSTACK_OK;
 }
 
-// Global average pool: one thread per (image, 8-channel group), fp32 sum.
+// Global average pool.  Block = 32 channel vectors (8 channels each) x 8
+// position groups of one image: thread (g, v) sums positions g, g+8, ... of
+// vector v (its loads independent and in flight together), fp32 partial sums
+// are combined in LDS and thread g = 0 writes the mean.
 __global__ __launch_bounds__(256) void avgpool_kernel(const bf16* __restrict__ x, int N, int HW, int C,
                                                       bf16* __restrict__ y) {
+  __shared__ float part[8][32][9];  // [group][vector][8 sums + pad]
   const int CV = C >> 3;
-  int idx = blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= N * CV) return;
-  int cv = idx % CV, n = idx / CV;
+  const int v = threadIdx.x & 31, g = threadIdx.x >> 5;
+  const int cv = blockIdx.x * 32 + v, n = blockIdx.y;
   float s[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-  const bf16* p = x + (long)n * HW * C + cv * 8;
-  for (int i = 0; i < HW; ++i) {
-    bf16x8 v = ld8(p + (long)i * C);
+  if (cv < CV) {
+    const bf16* p = x + (long)n * HW * C + cv * 8;
+#pragma unroll 4
+    for (int i = g; i < HW; i += 8) {
+      const bf16x8 t = ld8(p + (long)i * C);
 #pragma unroll
-    for (int e = 0; e < 8; ++e) s[e] += (float)v[e];
+      for (int e = 0; e < 8; ++e) s[e] += (float)t[e];
+    }
   }
-  float inv = 1.0f / (float)HW;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) part[g][v][e] = s[e];
+  __syncthreads();
+  if (g != 0 || cv >= CV) return;
+  const float inv = 1.0f / (float)HW;
   bf16x8 o;
 #pragma unroll
-  for (int e = 0; e < 8; ++e) o[e] = (bf16)(s[e] * inv);
+  for (int e = 0; e < 8; ++e) {
+    float t = 0.f;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) t += part[k][v][e];
+    o[e] = (bf16)(t * inv);
+  }
   st8(y + (long)n * C + cv * 8, o);
 }
 
 dstack_status launch_avgpool(const bf16* x, int N, int H, int W, int C, bf16* y, hipStream_t st) {
   DS_CHECK(C % 8 == 0, DSTACK_E_UNSUPPORTED, "avgpool: C must be a multiple of 8");
-  DS_CHECK(N > 0 && H > 0 && W > 0, DSTACK_E_INVALID, "avgpool: bad shape");
-  int total = N * (C / 8);
-  hipLaunchKernelGGL(avgpool_kernel, dim3(ceil_div(total, 256)), dim3(256), 0, st, x, N, H * W, C, y);
+  DS_CHECK(N > 0 && H > 0 && W > 0 && N <= 65535, DSTACK_E_INVALID, "avgpool: bad shape");
+  hipLaunchKernelGGL(avgpool_kernel, dim3(ceil_div(C / 8, 32), N), dim3(256), 0, st, x, N, H * W, C, y);
   DS_HIP(hipGetLastError());
   return DSTACK_OK;
 }
@@ -199,9 +213,50 @@ __global__ __launch_bounds__(256) void pack_c8_kernel(const bf16* __restrict__ x
   st8(y + p * 8, o);
 }
 
+// 3-channel images (the common case): block = 2048 pixels.  Threads load
+// the block's 12 KB of input as 16-byte vectors (thread t: vectors t, t + 256,
+// t + 512), stage it in LDS, then each store instruction writes 64
+// consecutive output pixels (lane l: pixel 64 k + l of the wave's range).
+// npix is a multiple of 8; pixels past it (the last block) are not stored.
+__global__ __launch_bounds__(256) void pack_c3_kernel(const bf16* __restrict__ x, long npix, bf16* __restrict__ y) {
+  __shared__ bf16x8 in[768];  // 2048 pixels x 3 channels
+  const long p0 = (long)blockIdx.x * 2048;
+  const long nvec = npix * 3 / 8;  // npix is a multiple of 8: whole input vectors
+  const long v0 = p0 * 3 / 8;
+#pragma unroll
+  for (int k = 0; k < 3; ++k) {
+    const int i = threadIdx.x + 256 * k;
+    in[i] = v0 + i < nvec ? reinterpret_cast<const bf16x8*>(x)[v0 + i] : bf16x8{};
+  }
+  __syncthreads();
+  const bf16* e = reinterpret_cast<const bf16*>(in);
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    const int pl = wave * 512 + k * 64 + lane;  // pixel within the block
+    const long p = p0 + pl;
+    if (p >= npix) break;
+    bf16x8 o = {};
+    o[0] = e[3 * pl];
+    o[1] = e[3 * pl + 1];
+    o[2] = e[3 * pl + 2];
+    st8(y + p * 8, o);
+  }
+}
+
 dstack_status launch_pack_c8(const bf16* x, int npix, int C, bf16* y, hipStream_t st) {
   DS_CHECK(C >= 1 && C <= 8 && npix > 0, DSTACK_E_INVALID, "pack: bad shape");
-  hipLaunchKernelGGL(pack_c8_kernel, dim3(ceil_div(npix, 256)), dim3(256), 0, st, x, (long)npix, C, y);
+  long done = 0;
+  if (C == 3 && ((uintptr_t)x & 15) == 0) {
+    // the fast path takes a multiple of 8 pixels (whole 16-byte input vectors)
+    const long npix3 = (long)npix / 8 * 8;
+    if (npix3 > 0)
+      hipLaunchKernelGGL(pack_c3_kernel, dim3((unsigned)((npix3 + 2047) / 2048)), dim3(256), 0, st, x, npix3, y);
+    done = npix3;
+  }
+  if (done < npix)
+    hipLaunchKernelGGL(pack_c8_kernel, dim3((unsigned)((npix - done + 255) / 256)), dim3(256), 0, st, x + done * C,
+                       (long)(npix - done), C, y + done * 8);
   DS_HIP(hipGetLastError());
   return DSTACK_OK;
 }

@@ -119,7 +119,8 @@ def test_fc(env, case, split):
     assert oracle.rel_err(gu.host(y), ref) <= TOL
 
 
-@pytest.mark.parametrize("case", [(2, 8, 8, 16, 2, 2, 0), (1, 112, 112, 64, 3, 2, 1), (3, 7, 9, 8, 3, 2, 1)])
+@pytest.mark.parametrize("case", [(2, 8, 8, 16, 2, 2, 0), (1, 112, 112, 64, 3, 2, 1), (3, 7, 9, 8, 3, 2, 1),
+                                  (2, 7, 7, 2048, 3, 2, 1), (1, 7, 7, 1288, 2, 2, 0)])
 def test_pools(env, case):
     ds, gu, inputs, oracle, torch = env
     N, H, W, C, k, st, pad = case
