@@ -63,7 +63,7 @@ const char* dstack_last_error(void);
 /* Partitions (CU-masked streams)                                      */
 /* ------------------------------------------------------------------ */
 /* The paper confines each model to a share of the SMs with MPS
- * (Sec. 3, Sec. 3.2); here the share is a CU mask on a HIP stream.
+ * (Sec. 3.1); here the share is a CU mask on a HIP stream.
  *
  * dstack_fraction_to_slots: slots = clamp(floor(32*f + 1/2), 1, 32).
  *   Host only.  E_INVALID for f <= 0, f > 1 or NaN.
@@ -98,7 +98,7 @@ dstack_status dstack_probe_cu_ids(dstack_partition p, int n_blocks, int via_grap
 /* Models                                                              */
 /* ------------------------------------------------------------------ */
 /* arch: "tinycnn", "resnet50", "mobilenetv2", "vgg19", "lstm2".
- * Weights are drawn from `seed` (Sec. 3.1 uses trained models; here
+ * Weights are drawn from `seed` (Sec. 3 uses trained models; here
  * random-weight models of the same architecture):
  *   tensor t uses the splitmix64 stream whose state starts at
  *   seed ^ (0x9E3779B97F4A7C15 * (t + 1)); u = (next >> 11) * 2^-53, with
@@ -166,7 +166,7 @@ dstack_status dstack_profile_layers(dstack_model m, int batch, const void* d_in,
                                     dstack_layer_time* out, int max_layers, int* n_layers);
 
 /* ------------------------------------------------------------------ */
-/* Knee sweep (Sec. 3.1 measurement; Sec. 4.3 Eq. first_order_derivative;  */
+/* Knee sweep (Sec. 3.2 measurement; Sec. 4.3 Eq. first_order_derivative;  */
 /* Sec. 5 Eq. efficiencySquareLatency)                                 */
 /* ------------------------------------------------------------------ */
 /* For each fraction: a partition of dstack_fraction_to_slots(f) slots,

@@ -1,6 +1,6 @@
 // Architectures and their executor.
 //
-// The paper's workloads (Sec. 3.1, Sec. 6.3, Table model_characteristics)
+// The paper's workloads (Sec. 3, Sec. 6.3, Table model_characteristics)
 // are stock image classifiers and a recurrent model.  Each architecture here
 // is a flat list of kernel launches over NHWC bf16 activation buffers:
 //   tinycnn      4 x (conv3x3 + BN + ReLU), 2x2 max pools after convs 2 and 4,

@@ -1,5 +1,5 @@
 // Seeded weight generation for random-weight models (the paper evaluates
-// trained torchvision models, Sec. 3.1; here the same architectures carry
+// trained torchvision models, Sec. 3; here the same architectures carry
 // synthetic weights drawn from a seed).
 //
 // splitmix64 (Steele, Lea, Flood, OOPSLA 2014): state += 0x9E3779B97F4A7C15,
