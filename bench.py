@@ -22,7 +22,10 @@ timing on each partition's stream gives the conv MFMA TFLOP/s at the knee and
 the roofline fraction of the dominant kernel (the implicit-GEMM convolution);
 each partition's batch time alone vs in the mix gives the interference.
 
-Also reported (not the headline): the VGG-19 batch 8 + LSTM batch 32 pair in
+Also reported (not the headline): for each headline model the knee found by
+a binary search from 30% against the sweep's knee, and the cost of a GPU%
+change, cold and active-standby ("reconfiguration"); the VGG-19 batch 8 +
+LSTM batch 32 pair in
 the same closed-loop form ("config4"), and the four-model Poisson mix
 (ResNet-50, MobileNetV2, VGG-19, LSTM at 400/800/150/300 req/s, SLOs
 25/15/50/30 ms, 100 ms sessions) through the live launcher dstack_serve for
@@ -419,6 +422,15 @@ def main():
     knee_cu = sum(p["n_cu"] * p["kernels"]["mfma"]["ms"] for p in per_model) / max(
         sum(p["kernels"]["mfma"]["ms"] for p in per_model), 1e-9)
 
+    # ---- GPU% reconfiguration (Sec. 3.5, 3.6): knee search from 30% vs the sweep, cost of a change ----
+    reconf = []
+    for i, m in enumerate(models):
+        ks = m.knee_search(batch[i], FRACTIONS, 10, args.sweep_warmup, args.sweep_reps)
+        sw = m.switch_probe(batch[i], 10, dep[i], reps=10)
+        reconf.append(dict(arch=MODELS[i][0], batch=batch[i], search_knee_slots=ks["knee_slots"],
+                           sweep_knee_slots=knee[i], search_probes=ks["probes"], search_seconds=ks["seconds"],
+                           switch_from_slots=10, switch_to_slots=dep[i], **sw))
+
     # ---- the other workloads: VGG-19 + LSTM pair, four-model Poisson mix through the live launcher ----
     c4 = c5 = None
     if not args.headline_only:
@@ -483,6 +495,7 @@ def main():
         "cpu_baseline": cpu,
         "schedule_status": "ok" if sched_st == ds.OK else "infeasible",
         "per_model": per_model,
+        "reconfiguration": reconf,
         "config4": c4,
         "config5": c5,
         "timing_tables": {t["arch"]: {str(b): row for b, row in t["table"].items()} for t in tables},

@@ -191,6 +191,61 @@ typedef struct {
 dstack_status dstack_knee_sweep(dstack_model m, int batch, const double* fractions, int n, int warmup, int reps,
                                 dstack_knee_result* out);
 
+/* Knee search for a model without a profile (Sec. 3.6: it starts at a
+ * nominal 30% and the knee is found from its latency by a binary search).
+ * Reading: the search runs over the same ascending GPU% grid as the sweep
+ * (candidate slot counts c[0..n)), with eta(s) = b / (L(s)^2 s) taken as
+ * unimodal over it (at single-slot steps latency falls in steps and eta has
+ * local maxima).  It keeps an index interval [lo, hi] = [0, n - 1], probes
+ * c[mid] and c[mid + 1] (mid = the last candidate <= start_slots first, then
+ * (lo + hi) / 2, clamped into [lo, hi - 1]) and moves lo = mid + 1 when
+ * eta(c[mid + 1]) > eta(c[mid]) (exact 128-bit compare), else hi = mid,
+ * until lo == hi; c[lo] is the knee.  Each candidate is measured at most
+ * once; probe_slots/probe_latency_us list the measurements in order.
+ *  - _table: latency_us[i] (> 0) stands in for the measurement at slots[i]
+ *    (ascending, in 1..total); pure host; deployed = min(total, knee +
+ *    overprov_slots).
+ *  - live: candidates from `fractions` (ascending) as dstack_knee_sweep;
+ *    each probe measures the median latency (integer us, rounded half up)
+ *    of `reps` forwards after `warmup` on a fresh partition of the first s
+ *    slots; total 32, over-provision 2; seconds = wall time of the search.
+ *    start_slots 10 = 30%. */
+#define DSTACK_MAX_PROBES 64
+typedef struct {
+  int batch;
+  int knee_slots;
+  int deployed_slots;
+  int n_probes;
+  int probe_slots[DSTACK_MAX_PROBES];
+  int64_t probe_latency_us[DSTACK_MAX_PROBES];
+  double seconds;
+} dstack_knee_search_result;
+
+dstack_status dstack_knee_search_table(int batch, const int* slots, const int64_t* latency_us, int n,
+                                       int start_slots, int total, int overprov_slots,
+                                       dstack_knee_search_result* out);
+dstack_status dstack_knee_search(dstack_model m, int batch, const double* fractions, int n, int start_slots,
+                                 int warmup, int reps, dstack_knee_search_result* out);
+
+/* GPU% change of a running model (Sec. 3.5).  A GPU% is a CU-masked stream
+ * here, so a change creates a stream (no model reload: weights are shared).
+ * The model runs at batch on the first from_slots slots (warmed up); then
+ *  - cold: a partition of the first to_slots slots is created and its first
+ *    forward (workspace allocation, graph capture) is run: create_us is the
+ *    stream creation, cold_us creation through the first result (host clock);
+ *  - active-standby: with that partition ready, `reps` times the active
+ *    runs a batch and the host, on its completion, hands the next batch to
+ *    the standby; standby_gap_us is the median (max: _max_us) device-clock
+ *    time between the active's end and the standby's start;
+ *  - from/to_latency_us: median of 5 forwards on each size.
+ * Uses profiling buffers of the model (fixed input pattern). */
+typedef struct {
+  double create_us, cold_us, standby_gap_us, standby_gap_max_us, from_latency_us, to_latency_us;
+} dstack_switch_result;
+
+dstack_status dstack_switch_probe(dstack_model m, int batch, int from_slots, int to_slots, int reps,
+                                  dstack_switch_result* out);
+
 /* ------------------------------------------------------------------ */
 /* Scheduling (pure host, deterministic, integer microseconds)          */
 /* ------------------------------------------------------------------ */

@@ -79,6 +79,38 @@ def knee(row: Dict[int, int], b: int) -> int:
     return best
 
 
+def knee_search(latency, b: int, candidates, start: int):
+    """Knee of a model without a profile (Sec. 3.6: start at a nominal 30%,
+    binary search on the latency).  Reading: over the ascending GPU% grid
+    `candidates` (slot counts) eta(s) = b / (L(s)^2 s) is taken as unimodal;
+    keep the index interval [lo, hi] = [0, n - 1], probe candidates mid and
+    mid + 1 (mid = the last candidate <= start first, then the midpoint,
+    clamped into [lo, hi - 1]); if eta rises from mid to mid + 1 the knee is
+    above mid, else at or below it.  latency(s) is called once per slot
+    count.  Returns (knee slots, probes)."""
+    c = list(candidates)
+    seen = {}
+    probes = []
+
+    def L(i):
+        if i not in seen:
+            seen[i] = latency(c[i])
+            probes.append((c[i], seen[i]))
+        return seen[i]
+
+    lo, hi = 0, len(c) - 1
+    mid = max([i for i in range(len(c)) if c[i] <= start], default=0)
+    while lo < hi:
+        mid = min(max(mid, lo), hi - 1)
+        a, d = L(mid), L(mid + 1)
+        if eta_gt(b, d, c[mid + 1], b, a, c[mid]):
+            lo = mid + 1
+        else:
+            hi = mid
+        mid = (lo + hi) // 2
+    return c[lo], probes
+
+
 def deployed_slots(knee_s: int, overprov=OVERPROVISION_SLOTS, total=TOTAL_SLOTS) -> int:
     return min(total, knee_s + overprov)
 

@@ -48,6 +48,20 @@ class KneeResult(ctypes.Structure):
                 ("knee_index", ctypes.c_int), ("knee_slots", ctypes.c_int), ("deployed_slots", ctypes.c_int)]
 
 
+MAX_PROBES = 64
+
+
+class KneeSearchResult(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int), ("knee_slots", ctypes.c_int), ("deployed_slots", ctypes.c_int),
+                ("n_probes", ctypes.c_int), ("probe_slots", ctypes.c_int * MAX_PROBES),
+                ("probe_latency_us", ctypes.c_int64 * MAX_PROBES), ("seconds", ctypes.c_double)]
+
+
+class SwitchResult(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_double) for n in ("create_us", "cold_us", "standby_gap_us", "standby_gap_max_us",
+                                               "from_latency_us", "to_latency_us")]
+
+
 class SchedModel(ctypes.Structure):
     _fields_ = [("slo_us", ctypes.c_int64), ("max_batch", ctypes.c_int), ("rate_per_s", ctypes.c_int),
                 ("n_batches", ctypes.c_int), ("batches", ctypes.c_int * MAX_BATCHES), ("n_slots", ctypes.c_int),
@@ -119,6 +133,10 @@ _SIGS = {
     "dstack_schedule": ([ctypes.POINTER(SchedModel), _i, ctypes.POINTER(SchedParams), ctypes.POINTER(ScheduleOut)], _i),
     "dstack_simulate": ([ctypes.POINTER(SchedModel), _i, ctypes.POINTER(SchedParams), ctypes.POINTER(SimParams),
                          ctypes.POINTER(RunOut)], _i),
+    "dstack_knee_search_table": ([_i, ctypes.POINTER(_i), ctypes.POINTER(ctypes.c_int64), _i, _i, _i, _i,
+                                  ctypes.POINTER(KneeSearchResult)], _i),
+    "dstack_knee_search": ([_vp, _i, ctypes.POINTER(_d), _i, _i, _i, _i, ctypes.POINTER(KneeSearchResult)], _i),
+    "dstack_switch_probe": ([_vp, _i, _i, _i, _i, ctypes.POINTER(SwitchResult)], _i),
     "dstack_serve": ([ctypes.POINTER(_vp), _i, ctypes.POINTER(_vp), ctypes.POINTER(_vp), ctypes.POINTER(SchedModel),
                       ctypes.POINTER(SchedParams), ctypes.POINTER(SimParams), ctypes.POINTER(RunOut),
                       ctypes.POINTER(JobRecord), _i, ctypes.POINTER(_i)], _i),
@@ -267,6 +285,20 @@ class Model:
         return [dict(kind=arr[i].kind, ms=arr[i].ms, flops=arr[i].flops, bytes=arr[i].bytes,
                      gemm=(arr[i].gemm_m, arr[i].gemm_n, arr[i].gemm_k)) for i in range(n.value)]
 
+    def knee_search(self, batch, fractions=None, start_slots=10, warmup=5, reps=20):
+        """Binary-search the knee from live latency over the GPU% grid (see dstack_knee_search)."""
+        fractions = fractions or [0.1 * i for i in range(1, 11)]
+        fr = (_d * len(fractions))(*fractions)
+        r = KneeSearchResult()
+        _check(lib().dstack_knee_search(self.h, batch, fr, len(fractions), start_slots, warmup, reps, ctypes.byref(r)))
+        return _search_dict(r)
+
+    def switch_probe(self, batch, from_slots, to_slots, reps=10):
+        """Cost of a GPU% change, cold and active-standby (see dstack_switch_probe)."""
+        r = SwitchResult()
+        _check(lib().dstack_switch_probe(self.h, batch, from_slots, to_slots, reps, ctypes.byref(r)))
+        return dict((f, getattr(r, f)) for f, _ in SwitchResult._fields_)
+
     def knee_sweep(self, batch, fractions, warmup=5, reps=20):
         fr = (ctypes.c_double * len(fractions))(*fractions)
         r = KneeResult()
@@ -276,6 +308,23 @@ class Model:
                     latency_us=list(r.latency_us[:n]), latency_us_exact=list(r.latency_us_exact[:n]),
                     p99_us=list(r.p99_us[:n]), knee_index=r.knee_index, knee_slots=r.knee_slots,
                     deployed_slots=r.deployed_slots)
+
+
+def _search_dict(r):
+    n = min(r.n_probes, MAX_PROBES)
+    return dict(batch=r.batch, knee_slots=r.knee_slots, deployed_slots=r.deployed_slots, n_probes=r.n_probes,
+                probes=[(r.probe_slots[i], r.probe_latency_us[i]) for i in range(n)], seconds=r.seconds)
+
+
+def knee_search_table(batch, table, total=TOTAL_SLOTS, start_slots=10, overprov_slots=2):
+    """Knee search over the slot counts of a {slots: latency_us} table (host only)."""
+    cand = sorted(table)
+    sl = (_i * len(cand))(*cand)
+    lat = (ctypes.c_int64 * len(cand))(*[table[s] for s in cand])
+    r = KneeSearchResult()
+    _check(lib().dstack_knee_search_table(batch, sl, lat, len(cand), start_slots, total, overprov_slots,
+                                          ctypes.byref(r)))
+    return _search_dict(r)
 
 
 def generate_params(arch, seed, idx):

@@ -4,6 +4,7 @@
 #include <hip/hip_ext.h>
 
 #include <algorithm>
+#include <chrono>
 #include <atomic>
 #include <cmath>
 #include <cstdlib>
@@ -384,6 +385,69 @@ dstack_status dstack_profile_layers(dstack_model h, int batch, const void* d_in,
 
 // ----------------------------------------------------------- knee sweep ----
 
+namespace {
+
+// Scratch input/output of the model at its maximum batch for profiling runs
+// (contents: a fixed xorshift pattern of values in about [-1, 1)).
+dstack_status ensure_sweep_buffers(Model& m) {
+  if (m.sweep_in) return DSTACK_OK;
+  size_t in_bytes = m.is_lstm ? (size_t)m.seq_len * m.max_batch * m.in_features * 2
+                              : (size_t)m.max_batch * m.in_h * m.in_w * m.in_c * 2;
+  size_t out_bytes = m.is_lstm ? (size_t)m.seq_len * m.max_batch * m.out_features * 4
+                               : (size_t)m.max_batch * m.out_features * 4;
+  DS_HIP(hipMalloc(&m.sweep_in, in_bytes));
+  DS_HIP(hipMalloc(&m.sweep_out, out_bytes));
+  std::vector<uint16_t> pat(in_bytes / 2);
+  uint64_t z = 0x2545F4914F6CDD1DULL;
+  for (auto& v : pat) {
+    z ^= z << 13; z ^= z >> 7; z ^= z << 17;
+    v = bf16_from_double(((double)(z >> 11) * (1.0 / 9007199254740992.0)) * 2.0 - 1.0);
+  }
+  DS_HIP(hipMemcpy(m.sweep_in, pat.data(), in_bytes, hipMemcpyHostToDevice));
+  return DSTACK_OK;
+}
+
+uint32_t first_slots_mask(int slots) { return slots >= 32 ? 0xFFFFFFFFu : ((1u << slots) - 1); }
+
+// Median and p99 latency (us) of `reps` event-timed forwards after `warmup`
+// on a fresh partition of the first `slots` slots.
+dstack_status measure_latency(Model& m, int batch, int slots, int warmup, int reps, double* med, double* p99) {
+  dstack_status s = ensure_sweep_buffers(m);
+  if (s != DSTACK_OK) return s;
+  dstack_partition p;
+  s = make_partition(first_slots_mask(slots), &p);
+  if (s != DSTACK_OK) return s;
+  std::vector<float> ms(reps);
+  std::vector<hipEvent_t> ev(2 * reps);
+  for (auto& e : ev) {
+    if (hipEventCreate(&e) != hipSuccess) e = nullptr;
+  }
+  for (int w = 0; w < warmup && s == DSTACK_OK; ++w)
+    s = infer_impl(m, batch, m.sweep_in, m.sweep_out, p, nullptr, SWEEP_WS_ID);
+  for (int r = 0; r < reps && s == DSTACK_OK; ++r) {
+    (void)hipEventRecord(ev[2 * r], p->stream);
+    s = infer_impl(m, batch, m.sweep_in, m.sweep_out, p, nullptr, SWEEP_WS_ID);
+    (void)hipEventRecord(ev[2 * r + 1], p->stream);
+  }
+  hipError_t e = hipStreamSynchronize(p->stream);
+  for (int r = 0; r < reps && e == hipSuccess; ++r) e = hipEventElapsedTime(&ms[r], ev[2 * r], ev[2 * r + 1]);
+  for (auto& x : ev)
+    if (x) (void)hipEventDestroy(x);
+  dstack_partition_destroy(p);
+  if (s != DSTACK_OK) return s;
+  if (e != hipSuccess) return hip_fail(e, "latency timing");
+  std::vector<double> us(reps);
+  for (int r = 0; r < reps; ++r) us[r] = 1000.0 * ms[r];
+  std::sort(us.begin(), us.end());
+  *med = (reps % 2) ? us[reps / 2] : 0.5 * (us[reps / 2 - 1] + us[reps / 2]);
+  *p99 = us[std::min(reps - 1, (int)std::ceil(0.99 * reps) - 1)];
+  return DSTACK_OK;
+}
+
+int64_t round_us(double us) { return std::max<int64_t>(1, (int64_t)std::floor(us + 0.5)); }
+
+}  // namespace
+
 dstack_status dstack_knee_sweep(dstack_model h, int batch, const double* fractions, int n, int warmup, int reps,
                                 dstack_knee_result* out) {
   return guarded([&] {
@@ -396,62 +460,175 @@ dstack_status dstack_knee_sweep(dstack_model h, int batch, const double* fractio
     std::memset(out, 0, sizeof(*out));
     out->n = n;
     out->batch = batch;
-    // scratch input/output at the model's maximum batch (contents: a fixed pattern)
-    size_t in_bytes = m.is_lstm ? (size_t)m.seq_len * m.max_batch * m.in_features * 2
-                                : (size_t)m.max_batch * m.in_h * m.in_w * m.in_c * 2;
-    size_t out_bytes = m.is_lstm ? (size_t)m.seq_len * m.max_batch * m.out_features * 4
-                                 : (size_t)m.max_batch * m.out_features * 4;
-    if (!m.sweep_in) {
-      DS_HIP(hipMalloc(&m.sweep_in, in_bytes));
-      DS_HIP(hipMalloc(&m.sweep_out, out_bytes));
-      std::vector<uint16_t> pat(in_bytes / 2);
-      uint64_t z = 0x2545F4914F6CDD1DULL;
-      for (auto& v : pat) {  // xorshift values in about [-1, 1), as bf16
-        z ^= z << 13; z ^= z >> 7; z ^= z << 17;
-        v = bf16_from_double(((double)(z >> 11) * (1.0 / 9007199254740992.0)) * 2.0 - 1.0);
-      }
-      DS_HIP(hipMemcpy(m.sweep_in, pat.data(), in_bytes, hipMemcpyHostToDevice));
-    }
     for (int i = 0; i < n; ++i) {
       int slots;
       s = slots_from_fraction(fractions[i], &slots);
       if (s != DSTACK_OK) return s;
-      dstack_partition p;
-      s = make_partition(slots == 32 ? 0xFFFFFFFFu : ((1u << slots) - 1), &p);
+      double med, p99;
+      s = measure_latency(m, batch, slots, warmup, reps, &med, &p99);
       if (s != DSTACK_OK) return s;
-      std::vector<float> ms(reps);
-      std::vector<hipEvent_t> ev(2 * reps);
-      for (auto& e : ev) {
-        if (hipEventCreate(&e) != hipSuccess) e = nullptr;
-      }
-      for (int w = 0; w < warmup && s == DSTACK_OK; ++w)
-        s = infer_impl(m, batch, m.sweep_in, m.sweep_out, p, nullptr, SWEEP_WS_ID);
-      for (int r = 0; r < reps && s == DSTACK_OK; ++r) {
-        (void)hipEventRecord(ev[2 * r], p->stream);
-        s = infer_impl(m, batch, m.sweep_in, m.sweep_out, p, nullptr, SWEEP_WS_ID);
-        (void)hipEventRecord(ev[2 * r + 1], p->stream);
-      }
-      hipError_t e = hipStreamSynchronize(p->stream);
-      for (int r = 0; r < reps && e == hipSuccess; ++r) e = hipEventElapsedTime(&ms[r], ev[2 * r], ev[2 * r + 1]);
-      for (auto& x : ev)
-        if (x) (void)hipEventDestroy(x);
-      dstack_partition_destroy(p);
-      if (s != DSTACK_OK) return s;
-      if (e != hipSuccess) return hip_fail(e, "knee_sweep timing");
-      std::vector<double> us(reps);
-      for (int r = 0; r < reps; ++r) us[r] = 1000.0 * ms[r];
-      std::sort(us.begin(), us.end());
-      double med = (reps % 2) ? us[reps / 2] : 0.5 * (us[reps / 2 - 1] + us[reps / 2]);
       out->slots[i] = slots;
       out->n_cu[i] = slots * DSTACK_CUS_PER_SLOT;
       out->latency_us_exact[i] = med;
-      out->latency_us[i] = std::max<int64_t>(1, (int64_t)std::floor(med + 0.5));
-      out->p99_us[i] = us[std::min(reps - 1, (int)std::ceil(0.99 * reps) - 1)];
+      out->latency_us[i] = round_us(med);
+      out->p99_us[i] = p99;
     }
     int k = knee_index(batch, out->latency_us, out->slots, n);
     out->knee_index = k;
     out->knee_slots = out->slots[k];
     out->deployed_slots = std::min(DSTACK_TOTAL_SLOTS, out->knee_slots + 2);
+    return DSTACK_OK;
+  });
+}
+
+namespace {
+
+void fill_search(int batch, int total, int overprov, int knee, const std::vector<std::pair<int, int64_t>>& probes,
+                 dstack_knee_search_result* out) {
+  out->batch = batch;
+  out->knee_slots = knee;
+  out->deployed_slots = std::min(total, knee + overprov);
+  out->n_probes = (int)probes.size();
+  for (size_t i = 0; i < probes.size() && i < DSTACK_MAX_PROBES; ++i) {
+    out->probe_slots[i] = probes[i].first;
+    out->probe_latency_us[i] = probes[i].second;
+  }
+}
+
+}  // namespace
+
+dstack_status dstack_knee_search_table(int batch, const int* slots, const int64_t* latency_us, int n,
+                                       int start_slots, int total, int overprov_slots,
+                                       dstack_knee_search_result* out) {
+  return guarded([&] {
+    DS_CHECK(slots && latency_us && out, DSTACK_E_INVALID, "knee_search: null pointer");
+    DS_CHECK(batch >= 1 && n >= 1 && n <= DSTACK_MAX_SWEEP && total >= 1 && total <= 64 && overprov_slots >= 0,
+             DSTACK_E_INVALID, "knee_search: bad arguments");
+    std::vector<int> cand(slots, slots + n);
+    for (int i = 0; i < n; ++i) {
+      DS_CHECK(latency_us[i] > 0 && cand[i] >= 1 && cand[i] <= total && (i == 0 || cand[i] > cand[i - 1]),
+               DSTACK_E_INVALID, "knee_search: ascending slot counts in 1..total, latencies > 0");
+    }
+    std::memset(out, 0, sizeof(*out));
+    std::vector<std::pair<int, int64_t>> probes;
+    const int k = knee_search(batch, cand, start_slots, [&](int s) {
+      return latency_us[std::lower_bound(cand.begin(), cand.end(), s) - cand.begin()];
+    }, &probes);
+    fill_search(batch, total, overprov_slots, cand[k], probes, out);
+    return DSTACK_OK;
+  });
+}
+
+dstack_status dstack_knee_search(dstack_model h, int batch, const double* fractions, int n, int start_slots, int warmup,
+                                 int reps, dstack_knee_search_result* out) {
+  return guarded([&] {
+    DS_CHECK(h && fractions && out, DSTACK_E_INVALID, "knee_search: null pointer");
+    DS_CHECK(n >= 1 && n <= DSTACK_MAX_SWEEP && warmup >= 0 && reps >= 1, DSTACK_E_INVALID,
+             "knee_search: n in 1..32, warmup >= 0, reps >= 1");
+    Model& m = h->m;
+    dstack_status s = check_batch(m, batch);
+    if (s != DSTACK_OK) return s;
+    std::vector<int> cand;
+    for (int i = 0; i < n; ++i) {
+      int slots;
+      s = slots_from_fraction(fractions[i], &slots);
+      if (s != DSTACK_OK) return s;
+      DS_CHECK(cand.empty() || slots > cand.back(), DSTACK_E_INVALID, "knee_search: fractions must ascend");
+      cand.push_back(slots);
+    }
+    std::memset(out, 0, sizeof(*out));
+    std::vector<std::pair<int, int64_t>> probes;
+    dstack_status err = DSTACK_OK;
+    const auto t0 = std::chrono::steady_clock::now();
+    const int k = knee_search(batch, cand, start_slots, [&](int slots) -> int64_t {
+      if (err != DSTACK_OK) return 1;
+      double med, p99;
+      err = measure_latency(m, batch, slots, warmup, reps, &med, &p99);
+      return err == DSTACK_OK ? round_us(med) : 1;
+    }, &probes);
+    if (err != DSTACK_OK) return err;
+    out->seconds = std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count();
+    fill_search(batch, DSTACK_TOTAL_SLOTS, 2, cand[k], probes, out);
+    return DSTACK_OK;
+  });
+}
+
+dstack_status dstack_switch_probe(dstack_model h, int batch, int from_slots, int to_slots, int reps,
+                                  dstack_switch_result* out) {
+  return guarded([&] {
+    DS_CHECK(h && out, DSTACK_E_INVALID, "switch_probe: null pointer");
+    DS_CHECK(from_slots >= 1 && from_slots <= DSTACK_TOTAL_SLOTS && to_slots >= 1 && to_slots <= DSTACK_TOTAL_SLOTS &&
+                 reps >= 1 && reps <= 1000,
+             DSTACK_E_INVALID, "switch_probe: slots in 1..32, reps in 1..1000");
+    Model& m = h->m;
+    dstack_status s = check_batch(m, batch);
+    if (s != DSTACK_OK) return s;
+    s = ensure_sweep_buffers(m);
+    if (s != DSTACK_OK) return s;
+    std::memset(out, 0, sizeof(*out));
+    using clk = std::chrono::steady_clock;
+    auto us_since = [](clk::time_point t) { return std::chrono::duration<double, std::micro>(clk::now() - t).count(); };
+    // the active partition, warmed up; its own workspace id keeps the two apart
+    constexpr int ACTIVE_WS = 1, STANDBY_WS = 2;
+    dstack_partition a = nullptr, b = nullptr;
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    auto cleanup = [&] {
+      if (e0) (void)hipEventDestroy(e0);
+      if (e1) (void)hipEventDestroy(e1);
+      if (a) dstack_partition_destroy(a);
+      if (b) dstack_partition_destroy(b);
+    };
+    auto run = [&](dstack_partition p, int ws) { return infer_impl(m, batch, m.sweep_in, m.sweep_out, p, nullptr, ws); };
+    s = make_partition(first_slots_mask(from_slots), &a);
+    for (int r = 0; r < 3 && s == DSTACK_OK; ++r) s = run(a, ACTIVE_WS);
+    if (s == DSTACK_OK && hipStreamSynchronize(a->stream) != hipSuccess) s = fail(DSTACK_E_HIP, "switch_probe: sync");
+    if (s != DSTACK_OK) {
+      cleanup();
+      return s;
+    }
+    // cold change: a new partition is created and its first forward captured and run
+    auto t0 = clk::now();
+    s = make_partition(first_slots_mask(to_slots), &b);
+    out->create_us = us_since(t0);
+    if (s == DSTACK_OK) s = run(b, STANDBY_WS);
+    if (s == DSTACK_OK && hipStreamSynchronize(b->stream) != hipSuccess) s = fail(DSTACK_E_HIP, "switch_probe: sync");
+    out->cold_us = us_since(t0);
+    // active-standby: the standby is ready; after the active's batch ends the
+    // host hands the next batch to the standby; gap = standby start - active end (device clock)
+    if (s == DSTACK_OK && (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess))
+      s = fail(DSTACK_E_HIP, "switch_probe: events");
+    std::vector<double> gaps;
+    for (int r = 0; r < reps && s == DSTACK_OK; ++r) {
+      s = run(a, ACTIVE_WS);
+      if (s != DSTACK_OK) break;
+      (void)hipEventRecord(e0, a->stream);
+      if (hipEventSynchronize(e0) != hipSuccess) {
+        s = fail(DSTACK_E_HIP, "switch_probe: wait");
+        break;
+      }
+      (void)hipEventRecord(e1, b->stream);
+      s = run(b, STANDBY_WS);
+      if (s != DSTACK_OK) break;
+      if (hipStreamSynchronize(b->stream) != hipSuccess) {
+        s = fail(DSTACK_E_HIP, "switch_probe: sync");
+        break;
+      }
+      float ms = 0.f;
+      (void)hipEventElapsedTime(&ms, e0, e1);
+      gaps.push_back(1000.0 * ms);
+    }
+    if (s == DSTACK_OK) {
+      double med, p99;
+      s = measure_latency(m, batch, from_slots, 2, 5, &med, &p99);
+      out->from_latency_us = med;
+      if (s == DSTACK_OK) s = measure_latency(m, batch, to_slots, 2, 5, &med, &p99);
+      out->to_latency_us = med;
+    }
+    cleanup();
+    if (s != DSTACK_OK) return s;
+    std::sort(gaps.begin(), gaps.end());
+    out->standby_gap_us = gaps[gaps.size() / 2];
+    out->standby_gap_max_us = gaps.back();
     return DSTACK_OK;
   });
 }

@@ -44,6 +44,32 @@ int knee_index(int b, const int64_t* lat, const int* slots, int n) {
   return best;
 }
 
+int knee_search(int b, const std::vector<int>& cand, int start, const std::function<int64_t(int)>& latency,
+                std::vector<std::pair<int, int64_t>>* probes) {
+  const int n = (int)cand.size();
+  std::vector<int64_t> seen(n, 0);
+  auto L = [&](int i) {
+    if (!seen[i]) {
+      seen[i] = latency(cand[i]);
+      probes->push_back({cand[i], seen[i]});
+    }
+    return seen[i];
+  };
+  int lo = 0, hi = n - 1, mid = 0;
+  for (int i = 0; i < n; ++i)
+    if (cand[i] <= start) mid = i;
+  while (lo < hi) {
+    mid = std::min(std::max(mid, lo), hi - 1);
+    const int64_t a = L(mid), c = L(mid + 1);
+    if (eta_greater(b, c, cand[mid + 1], b, a, cand[mid]))
+      lo = mid + 1;  // the next candidate still raises the efficacy
+    else
+      hi = mid;
+    mid = lo + (hi - lo) / 2;
+  }
+  return lo;
+}
+
 namespace {
 
 const int kBatchGrid[] = {1, 2, 4, 8, 16, 32};

@@ -153,3 +153,25 @@ def test_fc_workspace_bytes():
     assert ds.fc_workspace_bytes(16, 1280, 1000) == 2 * 16 * 1000 * 4    # 40 steps -> 2 splits
     assert ds.fc_workspace_bytes(1, 64, 10) == 0                         # 2 steps: unsplit
     assert ds.fc_workspace_bytes(0, 64, 10) == 0
+
+
+def test_knee_search_table_parity():
+    """dstack_knee_search_table takes the oracle's probes in the oracle's
+    order and ends on its knee, on random (not necessarily unimodal) tables
+    over random ascending candidate sets."""
+    import paper_2304_13541_amd as ds
+    rnd = random.Random(31)
+    for trial in range(300):
+        total = rnd.choice([1, 2, 5, 16, 32])
+        cand = sorted(rnd.sample(range(1, total + 1), rnd.randint(1, min(total, 12))))
+        table = {s: rnd.randint(50, 40000) for s in cand}
+        b, start = rnd.choice([1, 4, 16, 32]), rnd.randint(0, total)
+        got = ds.knee_search_table(b, table, total, start, overprov_slots=2)
+        k, probes = sched.knee_search(lambda s: table[s], b, cand, start)
+        assert got["knee_slots"] == k
+        assert got["probes"] == probes and got["n_probes"] == len(probes)
+        assert got["deployed_slots"] == min(total, k + 2)
+    with pytest.raises(ds.DStackError):  # a latency of 0
+        ds.knee_search_table(1, {3: 0, 6: 10})
+    with pytest.raises(ds.DStackError):  # a slot count above the total
+        ds.knee_search_table(1, {3: 5, 40: 10})

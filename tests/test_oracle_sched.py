@@ -256,3 +256,58 @@ def test_home_plan_invariants_random():
             if not j.missed:
                 assert j.slots == models[j.model].slots
                 assert j.slot_mask == sched.range_mask(homes[j.model], j.slots)
+
+
+# ---- knee search without a profile (binary search from 30%) ----
+
+GRID = [3, 6, 10, 13, 16, 19, 22, 26, 29, 32]  # the sweep's 10%..100% slot counts
+
+
+def _eta_argmax(table, b):
+    """Brute force: argmax of b / (L^2 s), ties to fewer slots."""
+    best = None
+    for s in sorted(table):
+        if best is None or sched.eta_gt(b, table[s], s, b, table[best], best):
+            best = s
+    return best
+
+
+def test_knee_search_unimodal_equals_brute_force():
+    """Where the efficacy over the candidates rises then falls, the search
+    ends on the same slot count as scanning them all, with few probes."""
+    rnd = random.Random(5)
+    checked = 0
+    for trial in range(600):
+        cand = GRID if trial % 2 else list(range(1, 33))
+        a, c, d = rnd.uniform(100, 3000), rnd.uniform(500, 60000), rnd.uniform(0, 30)
+        table = {s: max(1, int(a + c / s + d * s)) for s in cand}  # Amdahl plus a per-slot cost
+        b = rnd.choice([1, 2, 4, 8, 16, 32])
+        etas = [b / (table[s] ** 2 * s) for s in cand]
+        peak = max(range(len(cand)), key=lambda i: etas[i])
+        if any(etas[i] >= etas[i + 1] for i in range(peak)) or any(etas[i] <= etas[i + 1] for i in range(peak, len(cand) - 1)):
+            continue  # not strictly unimodal after integer rounding
+        k, probes = sched.knee_search(lambda s: table[s], b, cand, 10)
+        assert k == _eta_argmax(table, b)
+        assert len(probes) <= (8 if cand is GRID else 12)
+        assert len({s for s, _ in probes}) == len(probes)
+        checked += 1
+    assert checked >= 200
+
+
+def test_knee_search_hand_cases():
+    # efficacy strictly falling: the knee is the smallest candidate; first probes at 10 and 13
+    k, probes = sched.knee_search(lambda s: 1000, 4, GRID, 10)
+    assert k == 3 and [s for s, _ in probes][:2] == [10, 13]
+    # latency exactly c / s: eta = b s / c^2 rises with s -> the whole GPU
+    k, _ = sched.knee_search(lambda s: 64000 // s, 8, GRID, 10)
+    assert k == 32
+    # a single candidate needs no probe
+    assert sched.knee_search(lambda s: 5, 1, [7], 10) == (7, [])
+    # Amdahl a + c/s on every slot count: eta = b s / (a s + c)^2 peaks at s = c / a (here 8)
+    amd = {s: 1000 + 8000 // s for s in range(1, 33)}
+    k, probes = sched.knee_search(lambda s: amd[s], 16, range(1, 33), 10)
+    assert k == _eta_argmax(amd, 16) == 8
+    assert [s for s, _ in probes][:2] == [10, 11]
+    # a start below every candidate begins at the first
+    k, probes = sched.knee_search(lambda s: 1000, 1, GRID, 1)
+    assert probes[0][0] == 3 and k == 3
