@@ -25,12 +25,11 @@ each partition's batch time alone vs in the mix gives the interference.
 Also reported (not the headline): for each headline model the knee found by
 a binary search from 30% against the sweep's knee, and the cost of a GPU%
 change, cold and active-standby ("reconfiguration"); the VGG-19 batch 8 +
-LSTM batch 32 pair in
-the same closed-loop form ("config4"), and the four-model Poisson mix
-(ResNet-50, MobileNetV2, VGG-19, LSTM at 400/800/150/300 req/s, SLOs
-25/15/50/30 ms, 100 ms sessions) through the live launcher dstack_serve for
-10 s at the stated rates plus a capacity sweep of 2 s runs at k x the rates
-("config5"); --headline-only skips both.
+LSTM batch 32 pair in the same closed-loop form ("config4"), and the
+four-model Poisson mix (ResNet-50, MobileNetV2, VGG-19, LSTM at
+400/800/150/300 req/s, SLOs 25/15/50/30 ms, 100 ms sessions) through the live
+launcher dstack_serve for 10 s at the stated rates plus a capacity sweep of
+2 s runs at k x the rates ("config5"); --headline-only skips all three.
 """
 import argparse
 import hashlib
@@ -74,7 +73,7 @@ def parse():
     p.add_argument("--steps4", type=int, default=40, help="steps of the VGG-19 + LSTM pair")
     p.add_argument("--serve-seconds", type=float, default=10.0, help="four-model mix at the stated rates")
     p.add_argument("--capacity-seconds", type=float, default=2.0, help="each point of the capacity sweep")
-    p.add_argument("--headline-only", action="store_true", help="skip the VGG-19 + LSTM pair and the four-model mix")
+    p.add_argument("--headline-only", action="store_true", help="skip the GPU%% reconfiguration probes, the VGG-19 + LSTM pair and the four-model mix")
     return p.parse_args()
 
 
@@ -424,7 +423,7 @@ def main():
 
     # ---- GPU% reconfiguration (Sec. 3.5, 3.6): knee search from 30% vs the sweep, cost of a change ----
     reconf = []
-    for i, m in enumerate(models):
+    for i, m in enumerate(models if not args.headline_only else []):
         ks = m.knee_search(batch[i], FRACTIONS, 10, args.sweep_warmup, args.sweep_reps)
         sw = m.switch_probe(batch[i], 10, dep[i], reps=10)
         reconf.append(dict(arch=MODELS[i][0], batch=batch[i], search_knee_slots=ks["knee_slots"],

@@ -362,23 +362,72 @@ __global__ __launch_bounds__(256) void conv_igemm_kernel(ConvArgs a) {
   const int brow = BN + wm * (BM / WM) + (lane & 15);
   const int cq = lane >> 4;
 
+  // Epilogue mapping: thread -> fixed 4-channel group (256 is a multiple of
+  // the groups per row) and ROWS_PT pixel rows RSTEP apart.  Its per-channel
+  // scale and shift are fetched now and its residual rows right after the
+  // last depth tile's loads, so that neither round trip follows the loop.
+  constexpr int G = BN / 4;
+  constexpr int RSTEP = 256 / G;
+  constexpr int ROWS_PT = BM / RSTEP;
+  static_assert(256 % G == 0 && BM % RSTEP == 0, "epilogue thread mapping");
+  static_assert(2 * LPW + ROWS_PT < 64, "vmcnt range");
+  const int cl = (tid % G) * 4;
+  const int ch0 = n0 + cl;
+  const int pl0 = tid / G;
+  const int chc = min(ch0, a.K - 4);  // in-range channel for the prefetches (K % 4 == 0)
+  f32x4 sc = f32x4{1.f, 1.f, 1.f, 1.f}, sh = f32x4{0.f, 0.f, 0.f, 0.f};
+  if (!SPLIT) {
+    if (a.scale) sc = *reinterpret_cast<const f32x4*>(a.scale + chc);
+    if (a.shift) sh = *reinterpret_cast<const f32x4*>(a.shift + chc);
+  }
+  // residual rows: exactly ROWS_PT buffer loads per lane (rows past M read
+  // row M-1 and are not stored), so the stage waits can count them
+  const bool has_res = !SPLIT && a.res != nullptr;
+  bf16x4 rv[ROWS_PT];
+  auto load_res = [&]() __attribute__((always_inline)) {
+    const __amdgpu_buffer_rsrc_t rr =
+        __builtin_amdgcn_make_buffer_rsrc((void*)a.res, (short)0, (int)(unsigned)((long)a.M * a.K * 2), 0x00020000);
+#pragma unroll
+    for (int k = 0; k < ROWS_PT; ++k) {
+      const int px = min(m0 + pl0 + k * RSTEP, a.M - 1);
+      const auto v = __builtin_amdgcn_raw_buffer_load_b64(rr, (int)(((unsigned)px * (unsigned)a.K + (unsigned)chc) * 2u), 0, 0);
+      rv[k] = __builtin_bit_cast(bf16x4, v);
+    }
+  };
+#pragma unroll
+  for (int k = 0; k < ROWS_PT; ++k) rv[k] = bf16x4{};
+
   // prologue: STAGES-1 tiles in flight
 #pragma unroll
   for (int s = 0; s < STAGES - 1; ++s)
     if (kt0 + s < kt1) issue(kt0 + s, s);
+  if (has_res && kt1 - kt0 <= STAGES - 1) load_res();
 
   for (int kt = kt0; kt < kt1; ++kt) {
     const int st = (kt - kt0) % STAGES;
     // tiles issued after kt that may stay in flight
+    // (the residual rows, once issued, are the youngest loads)
     const int after = min(STAGES - 2, kt1 - 1 - kt);
-    if (after >= 2)
-      wait_vmcnt<2 * LPW>();
-    else if (after == 1)
-      wait_vmcnt<LPW>();
-    else
-      wait_vmcnt<0>();
+    if (has_res && kt1 - 1 - kt <= STAGES - 2) {
+      if (after >= 2)
+        wait_vmcnt<2 * LPW + ROWS_PT>();
+      else if (after == 1)
+        wait_vmcnt<LPW + ROWS_PT>();
+      else
+        wait_vmcnt<ROWS_PT>();
+    } else {
+      if (after >= 2)
+        wait_vmcnt<2 * LPW>();
+      else if (after == 1)
+        wait_vmcnt<LPW>();
+      else
+        wait_vmcnt<0>();
+    }
     __syncthreads();  // every wave's part of tile kt is in LDS; every wave is done with tile kt-1
-    if (kt + STAGES - 1 < kt1) issue(kt + STAGES - 1, (kt - kt0 + STAGES - 1) % STAGES);
+    if (kt + STAGES - 1 < kt1) {
+      issue(kt + STAGES - 1, (kt - kt0 + STAGES - 1) % STAGES);
+      if (has_res && kt + STAGES - 1 == kt1 - 1) load_res();
+    }
     const unsigned char* sb = lds + st * STAGE_BYTES;
 #pragma unroll
     for (int ks = 0; ks < BK / 8; ks += 4) {
@@ -403,6 +452,7 @@ __global__ __launch_bounds__(256) void conv_igemm_kernel(ConvArgs a) {
   // writes cover whole row segments.
   static_assert(BM * BN * 4 <= STAGES * STAGE_BYTES, "epilogue tile must fit in the stage ring");
   static_assert(BN / 4 >= 8, "swizzle needs 8 units per row");
+  wait_vmcnt<0>();  // scale, shift and residual rows are in registers: no waits between the row stores
   __syncthreads();  // all waves are done reading the last stage
   float* ct = reinterpret_cast<float*>(lds);
   auto cidx = [](int pl, int cl) { return pl * BN + ((((cl >> 2) ^ (pl & 7))) << 2); };
@@ -416,50 +466,33 @@ __global__ __launch_bounds__(256) void conv_igemm_kernel(ConvArgs a) {
     }
   }
   __syncthreads();
-  // thread -> fixed 4-channel group (256 is a multiple of the groups per row),
-  // ROWS_PT pixel rows; all residual loads are issued before any store
-  constexpr int G = BN / 4;
-  constexpr int RSTEP = 256 / G;
-  constexpr int ROWS_PT = BM / RSTEP;
-  static_assert(256 % G == 0 && BM % RSTEP == 0, "epilogue thread mapping");
-  const int cl = (tid % G) * 4;
-  const int ch0 = n0 + cl;
   if (ch0 >= a.K) return;
-  const int pl0 = tid / G;
+  // all of the thread's rows are read from LDS before the first store
+  f32x4 t[ROWS_PT];
+#pragma unroll
+  for (int k = 0; k < ROWS_PT; ++k) t[k] = *reinterpret_cast<const f32x4*>(ct + cidx(pl0 + k * RSTEP, cl));
   if (SPLIT) {
 #pragma unroll
     for (int k = 0; k < ROWS_PT; ++k) {
-      const int pl = pl0 + k * RSTEP, px = m0 + pl;
-      if (px < a.M)
-        *reinterpret_cast<f32x4*>(a.partial + ((long)blockIdx.z * a.M + px) * a.K + ch0) =
-            *reinterpret_cast<const f32x4*>(ct + cidx(pl, cl));
+      const int px = m0 + pl0 + k * RSTEP;
+      if (px < a.M) *reinterpret_cast<f32x4*>(a.partial + ((long)blockIdx.z * a.M + px) * a.K + ch0) = t[k];
     }
     return;
   }
-  const f32x4 sc = a.scale ? *reinterpret_cast<const f32x4*>(a.scale + ch0) : f32x4{1.f, 1.f, 1.f, 1.f};
-  const f32x4 sh = a.shift ? *reinterpret_cast<const f32x4*>(a.shift + ch0) : f32x4{0.f, 0.f, 0.f, 0.f};
   // element index of the thread's first row; rows step by RSTEP pixels
   // (M * K < 2^31 is checked at launch)
   const int idx0 = (m0 + pl0) * a.K + ch0;
   const int dstep = RSTEP * a.K;
-  bf16x4 rv[ROWS_PT];
-#pragma unroll
-  for (int k = 0; k < ROWS_PT; ++k) {
-    const int px = m0 + pl0 + k * RSTEP;
-    rv[k] = (a.res && px < a.M) ? *reinterpret_cast<const bf16x4*>(a.res + idx0 + k * dstep) : bf16x4{};
-  }
   // the activation is chosen once: none, or a clamp to [0, hi] (ReLU: hi = inf)
   const float hi = a.act == ACT_RELU6 ? 6.0f : INFINITY;
   auto rows = [&](auto clamp) {
 #pragma unroll
     for (int k = 0; k < ROWS_PT; ++k) {
-      const int pl = pl0 + k * RSTEP;
-      if (m0 + pl >= a.M) continue;
-      const f32x4 t = *reinterpret_cast<const f32x4*>(ct + cidx(pl, cl));
+      if (m0 + pl0 + k * RSTEP >= a.M) continue;
       float v[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        v[e] = t[e] * sc[e] + sh[e] + (float)rv[k][e];
+        v[e] = t[k][e] * sc[e] + sh[e] + (float)rv[k][e];
         if (decltype(clamp)::value) v[e] = fminf(fmaxf(v[e], 0.0f), hi);
       }
       store_out4(a.y, OUT_F32, idx0 + k * dstep, v);
