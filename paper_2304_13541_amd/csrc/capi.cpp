@@ -318,7 +318,7 @@ dstack_status infer_impl(Model& m, int batch, const void* d_in, void* d_out, dst
   dstack_status s = check_batch(m, batch);
   if (s != DSTACK_OK) return s;
   Workspace* ws;
-  s = get_workspace(m, ws_id >= 0 ? ws_id : p->id, p->n_cu, &ws);
+  s = get_workspace(m, ws_id >= 0 ? ws_id : p->id, p->n_cu, p->stream, &ws);
   if (s != DSTACK_OK) return s;
   BusyGuard g(ws->busy);
   DS_CHECK(g.ok, DSTACK_E_STATE, "infer: another call on this (model, partition) is in progress");

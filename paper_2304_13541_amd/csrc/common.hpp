@@ -61,6 +61,9 @@ __device__ __forceinline__ float apply_act(float v, int act) {
   return v;
 }
 
+// split-K arrival counters per model workspace (conv tiles of one launch)
+constexpr int SPLITK_TILE_COUNTERS = 4096;
+
 // ---- kernel launchers (defined in the .hip files) ----
 dstack_status launch_conv2d(const bf16* x, int N, int H, int W, int C, const bf16* w, int K, int R, int S,
                             int stride, int pad, const float* scale, const float* shift, const bf16* res, int act,

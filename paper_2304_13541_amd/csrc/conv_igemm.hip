@@ -30,8 +30,9 @@
 // epilogue (scale, shift, residual, activation) is one 8-byte store.
 //
 // Split-K: with gridDim.z = splits > 1 each z-slice accumulates a range of
-// depth tiles and writes raw fp32 partial sums to a workspace; a second
-// kernel sums the slices and applies the epilogue.
+// depth tiles and writes raw fp32 partial sums to a workspace; the last block
+// of each tile to finish (a per-tile arrival counter) sums the slices and
+// applies the epilogue, so no second kernel is launched.
 #include <hip/hip_ext.h>
 
 #include <type_traits>
@@ -67,6 +68,7 @@ struct ConvArgs {
   const bf16* res;     // nullptr: no residual
   void* y;
   float* partial;      // split-K workspace [splits][M][K]
+  unsigned* counters;  // split-K: per-tile arrival counters (zero between launches)
   int N, H, W, C, K, R, S, stride, pad, Ho, Wo;
   int M, Kg;
   int act;
@@ -79,6 +81,7 @@ struct ConvArgs {
 constexpr int BK = 64;          // depth per LDS stage (bf16 elements)
 constexpr int ROW_BYTES = 128;  // one tile row = BK bf16
 constexpr unsigned OOB = 0x80000000u;  // buffer offset past any tensor (< 2 GB): loads zeros
+constexpr int CPOL_SC1 = 16;           // buffer cache-policy bit: device scope (past the per-XCD L2)
 
 // Addressing of the activation operand: 1x1 stride 1 (the pixel row is the
 // input row), 1x1 strided, C % 64 == 0 (a depth tile lies in one (r, s)), or
@@ -93,22 +96,6 @@ __device__ __forceinline__ void store_out4(void* y, bool f32, long idx, const fl
     bf16x4 o = {(bf16)v[0], (bf16)v[1], (bf16)v[2], (bf16)v[3]};
     *reinterpret_cast<bf16x4*>(reinterpret_cast<bf16*>(y) + idx) = o;
   }
-}
-
-__device__ __forceinline__ void epilogue4(const ConvArgs& a, bool f32, int px, int ch0, const float acc[4]) {
-  float v[4];
-  f32x4 sc = a.scale ? *reinterpret_cast<const f32x4*>(a.scale + ch0) : f32x4{1.f, 1.f, 1.f, 1.f};
-  f32x4 sh = a.shift ? *reinterpret_cast<const f32x4*>(a.shift + ch0) : f32x4{0.f, 0.f, 0.f, 0.f};
-  long idx = (long)px * a.K + ch0;
-  bf16x4 r4 = {};
-  if (a.res) r4 = *reinterpret_cast<const bf16x4*>(a.res + idx);
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    float t = acc[i] * sc[i] + sh[i];
-    if (a.res) t += (float)r4[i];
-    v[i] = apply_act(t, a.act);
-  }
-  store_out4(a.y, f32, idx, v);
 }
 
 // vmcnt wait with an immediate count (gfx9 encoding: vmcnt[3:0] | vmcnt[5:4] << 14,
@@ -376,7 +363,7 @@ __global__ __launch_bounds__(256) void conv_igemm_kernel(ConvArgs a) {
   const int pl0 = tid / G;
   const int chc = min(ch0, a.K - 4);  // in-range channel for the prefetches (K % 4 == 0)
   f32x4 sc = f32x4{1.f, 1.f, 1.f, 1.f}, sh = f32x4{0.f, 0.f, 0.f, 0.f};
-  if (!SPLIT) {
+  if (!SPLIT || a.counters) {
     if (a.scale) sc = *reinterpret_cast<const f32x4*>(a.scale + chc);
     if (a.shift) sh = *reinterpret_cast<const f32x4*>(a.shift + chc);
   }
@@ -466,19 +453,63 @@ __global__ __launch_bounds__(256) void conv_igemm_kernel(ConvArgs a) {
     }
   }
   __syncthreads();
-  if (ch0 >= a.K) return;
   // all of the thread's rows are read from LDS before the first store
   f32x4 t[ROWS_PT];
 #pragma unroll
   for (int k = 0; k < ROWS_PT; ++k) t[k] = *reinterpret_cast<const f32x4*>(ct + cidx(pl0 + k * RSTEP, cl));
   if (SPLIT) {
+    // Fused reduction: every block writes its slice with device-scope stores
+    // (they pass the per-XCD L2s) and bumps the tile's counter once they have
+    // all completed; the block that brings it to gridDim.z reads the slices
+    // back in slice order (the sum does not depend on which block is last),
+    // runs the epilogue and puts the counter back to 0 for the next launch.
+    const unsigned slice_bytes = (unsigned)a.M * (unsigned)a.K * 4u;  // split workspaces are < 4 GB
+    const __amdgpu_buffer_rsrc_t pa =
+        __builtin_amdgcn_make_buffer_rsrc(a.partial, (short)0, (int)(slice_bytes * gridDim.z), 0x00020000);
+    if (ch0 < a.K) {
 #pragma unroll
-    for (int k = 0; k < ROWS_PT; ++k) {
-      const int px = m0 + pl0 + k * RSTEP;
-      if (px < a.M) *reinterpret_cast<f32x4*>(a.partial + ((long)blockIdx.z * a.M + px) * a.K + ch0) = t[k];
+      for (int k = 0; k < ROWS_PT; ++k) {
+        const int px = m0 + pl0 + k * RSTEP;
+        if (px < a.M)
+          __builtin_amdgcn_raw_buffer_store_b128(
+              t[k], pa, (int)(blockIdx.z * slice_bytes + ((unsigned)px * a.K + ch0) * 4u), 0, CPOL_SC1);
+      }
     }
-    return;
+    wait_vmcnt<0>();
+    __syncthreads();  // the whole slice is written; every thread is done reading the staged tile
+    int* flag = reinterpret_cast<int*>(lds);
+    if (tid == 0)
+      *flag = (int)__hip_atomic_fetch_add(a.counters + tile, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __syncthreads();
+    if (*flag != (int)gridDim.z - 1) return;
+    if (tid == 0) __hip_atomic_store(a.counters + tile, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (ch0 >= a.K) return;
+    if (a.res && ROWS_PT < 16) load_res();  // in flight with the slices (128-pixel tiles: after them)
+    const int S = gridDim.z;
+    // ZC slices per round, all of their loads in flight together (64 VGPRs)
+    constexpr int ZC = ROWS_PT >= 16 ? 1 : 16 / ROWS_PT;
+    for (int z0 = 0; z0 < S; z0 += ZC) {
+      f32x4 q[ZC][ROWS_PT];
+#pragma unroll
+      for (int c = 0; c < ZC; ++c) {
+        const unsigned z = (unsigned)min(z0 + c, S - 1);
+#pragma unroll
+        for (int k = 0; k < ROWS_PT; ++k) {
+          const int px = min(m0 + pl0 + k * RSTEP, a.M - 1);
+          q[c][k] = __builtin_amdgcn_raw_buffer_load_b128(pa, (int)(z * slice_bytes + ((unsigned)px * a.K + ch0) * 4u),
+                                                          0, CPOL_SC1);
+        }
+      }
+#pragma unroll
+      for (int c = 0; c < ZC; ++c)
+        if (z0 + c < S)
+#pragma unroll
+          for (int k = 0; k < ROWS_PT; ++k) t[k] = z0 + c == 0 ? q[c][k] : t[k] + q[c][k];
+    }
+    if (a.res && ROWS_PT >= 16) load_res();
+    wait_vmcnt<0>();  // residual rows
   }
+  if (ch0 >= a.K) return;
   // element index of the thread's first row; rows step by RSTEP pixels
   // (M * K < 2^31 is checked at launch)
   const int idx0 = (m0 + pl0) * a.K + ch0;
@@ -680,49 +711,61 @@ static void launch_1x1s(const ConvArgs& a, bool f32, int n_cu, hipStream_t st) {
 #undef DS_NB_CASE
 }
 
-// Sum split-K partial slices and apply the epilogue; one thread per 4 channels.
-__global__ void splitk_reduce_kernel(ConvArgs a, int splits, int out_f32) {
-  long q = (long)blockIdx.x * blockDim.x + threadIdx.x;
-  long nq = (long)a.M * (a.K / 4);
-  if (q >= nq) return;
-  int px = (int)(q / (a.K / 4));
-  int ch0 = (int)(q % (a.K / 4)) * 4;
-  float v[4] = {0.f, 0.f, 0.f, 0.f};
-  for (int s = 0; s < splits; ++s) {
-    f32x4 p = *reinterpret_cast<const f32x4*>(a.partial + ((long)s * a.M + px) * a.K + ch0);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) v[i] += p[i];
-  }
-  epilogue4(a, out_f32 != 0, px, ch0, v);
-}
-
 struct ConvPlan {
   int bn, bm, splits;
 };
 
-// Tile and split choice from the GEMM shape and the CUs of the partition.
-// With two LDS stages a 128x128 block takes 64 KB, so two or three blocks
-// share a CU and cover each other's load latency; the plan therefore aims at
-// two or more blocks per CU: smaller pixel tiles first, then split-K when the
-// reduction is deep enough (>= 4 depth tiles per slice).
-static ConvPlan choose_plan(int M, int K, int Kg, int n_cu) {
-  ConvPlan p;
-  const long target = 2L * n_cu;
-  p.bn = K <= 32 ? 32 : (K <= 64 ? 64 : 128);
-  p.bm = 128;
-  long tiles = (long)ceil_div(M, p.bm) * ceil_div(K, p.bn);
-  if (tiles < target && p.bn >= 64) {
-    p.bm = 64;
-    tiles = (long)ceil_div(M, p.bm) * ceil_div(K, p.bn);
-  }
-  p.splits = 1;
+// Tile and split choice from the GEMM shape and the CUs of the partition, by
+// an estimate of the launch's duration.  Two blocks share a CU (the LDS ring
+// is sized for it), so a launch runs in ceil(blocks / (2 * CUs)) rounds and
+// blocks of one round start and end together; a block costs a ramp until its
+// first depth tile lands, a per-step time that depends on the tile shape, and
+// an epilogue (plus, with a fused split-K, the wait for its slice to reach
+// device scope and the last block's read-back of all slices).  The constants
+// are per-block phase times measured on MI355X with two blocks per CU.  Split
+// plans are considered only when the caller gives a workspace and counters.
+struct TileCost {
+  int bn, bm;
+  double step_us;  // one 64-deep step
+};
+static constexpr TileCost kTiles[] = {
+    {128, 128, 0.70}, {128, 64, 0.47}, {64, 128, 0.47}, {64, 64, 0.34}, {32, 128, 0.25}};
+constexpr double kRampUs = 1.4;
+constexpr double kSliceWriteUs = 2.6;   // device-scope slice stores until acknowledged
+constexpr double kSliceReadUs = 0.35;   // per slice, the last block's read-back
+
+static double plan_cost(const TileCost& t, int M, int K, int nkt, int splits, int n_cu) {
+  const int per = ceil_div(nkt, splits);
+  const int s = ceil_div(nkt, per);
+  const long blocks = (long)ceil_div(M, t.bm) * ceil_div(K, t.bn) * s;
+  const long rounds = (blocks + 2L * n_cu - 1) / (2L * n_cu);
+  double blk = kRampUs + per * t.step_us + 0.6 + 1.5 * (t.bn * t.bm) / 16384.0;
+  if (s > 1) blk += kSliceWriteUs + kSliceReadUs * s;
+  return (double)rounds * blk;
+}
+
+static ConvPlan choose_plan(int M, int K, int Kg, int n_cu, bool can_split, size_t split_bytes) {
+  const int bn = K <= 32 ? 32 : (K <= 64 ? 64 : 128);
   const int nkt = ceil_div(Kg, BK);
-  while (tiles * p.splits < target && nkt / (p.splits * 2) >= 4 && p.splits < 16) p.splits *= 2;
-  return p;
+  ConvPlan best{bn, 128, 1};
+  double best_t = 1e30;
+  for (const TileCost& t : kTiles) {
+    if (t.bn != bn) continue;
+    for (int sp = 1; sp <= 16; sp *= 2) {
+      if (sp > 1 && (!can_split || nkt / sp < 2 || (size_t)sp * M * K * sizeof(float) > split_bytes)) break;
+      if (sp > 1 && (long)ceil_div(M, t.bm) * ceil_div(K, t.bn) > SPLITK_TILE_COUNTERS) break;
+      const double c = plan_cost(t, M, K, nkt, sp, n_cu);
+      if (c < best_t * 0.97) {  // a split or a smaller tile must win by more than 3%
+        best_t = c;
+        best = ConvPlan{t.bn, t.bm, sp};
+      }
+    }
+  }
+  return best;
 }
 
 size_t conv_splitk_workspace_bytes(int M, int K, int Kg, int n_cu) {
-  ConvPlan p = choose_plan(M, K, Kg, n_cu);
+  ConvPlan p = choose_plan(M, K, Kg, n_cu, true, (size_t)1 << 40);
   return p.splits > 1 ? (size_t)p.splits * M * K * sizeof(float) : 0;
 }
 
@@ -746,10 +789,9 @@ static void launch_mode(ConvArgs a, bool f32, int splits, hipStream_t st) {
   a.tiles = ceil_div(a.M, BM) * a.tiles_n;
   a.div_tn = FastDiv::make(a.tiles_n);
   dim3 grid(a.tiles, 1, splits);
-  // with dispatch events armed: start on this kernel, stop on it too unless
-  // a split-K reduce follows (that kernel takes the stop)
+  // with dispatch events armed: both on this kernel (the split-K reduction is in it)
   const DispatchEvents& de = dispatch_events();
-  hipEvent_t e0 = de.start, e1 = splits > 1 ? nullptr : de.stop;
+  hipEvent_t e0 = de.start, e1 = de.stop;
   if (splits > 1)
     launch_k(conv_igemm_kernel<BN, BM, WN, WM, STAGES, MODE, false, true>, grid, st, e0, e1, a);
   else if (f32)
@@ -773,7 +815,7 @@ static void launch_cfg(const ConvArgs& a, int mode, bool f32, int splits, hipStr
 dstack_status launch_conv2d_ws(const bf16* x, int N, int H, int W, int C, const bf16* w, int K, int R, int S,
                                int stride, int pad, const float* scale, const float* shift, const bf16* res,
                                int act, void* y, bool out_fp32, int n_cu, float* splitk_ws, size_t splitk_bytes,
-                               hipStream_t st) {
+                               unsigned* tile_counters, hipStream_t st) {
   DS_CHECK(C % 8 == 0, DSTACK_E_UNSUPPORTED, "conv2d: C must be a multiple of 8");
   DS_CHECK(K % 4 == 0, DSTACK_E_UNSUPPORTED, "conv2d: K must be a multiple of 4");
   DS_CHECK(N > 0 && H > 0 && W > 0 && K > 0 && R > 0 && S > 0 && stride > 0 && pad >= 0, DSTACK_E_INVALID,
@@ -803,13 +845,16 @@ dstack_status launch_conv2d_ws(const bf16* x, int N, int H, int W, int C, const 
   }
   const int mode = one ? (stride == 1 ? MODE_1X1S1 : MODE_1X1)
                        : (C % BK == 0 && R * S <= 32 ? MODE_TILED : MODE_GENERIC);
-  ConvPlan p = choose_plan(a.M, K, a.Kg, n_cu);
-  if (p.splits > 1 && (splitk_ws == nullptr || splitk_bytes < (size_t)p.splits * a.M * K * sizeof(float)))
-    p.splits = 1;
+  // split-K only with a workspace and the counters of the fused reduction
+  ConvPlan p = choose_plan(a.M, K, a.Kg, n_cu, splitk_ws != nullptr && tile_counters != nullptr, splitk_bytes);
   int nkt = ceil_div(a.Kg, BK);
   a.kt_per_split = ceil_div(nkt, p.splits);
   p.splits = ceil_div(nkt, a.kt_per_split);  // no empty slices
-  if (p.splits > 1) a.partial = splitk_ws;
+  a.counters = nullptr;
+  if (p.splits > 1) {
+    a.partial = splitk_ws;
+    a.counters = tile_counters;
+  }
   if (p.bn == 128 && p.bm == 128)
     launch_cfg<128, 128, 2, 2>(a, mode, out_fp32, p.splits, st);
   else if (p.bn == 128 && p.bm == 64)
@@ -820,15 +865,6 @@ dstack_status launch_conv2d_ws(const bf16* x, int N, int H, int W, int C, const 
     launch_cfg<64, 64, 2, 2>(a, mode, out_fp32, p.splits, st);
   else
     launch_cfg<32, 128, 1, 4>(a, mode, out_fp32, p.splits, st);
-  if (p.splits > 1) {
-    long nq = (long)a.M * (K / 4);
-    const dim3 rg((unsigned)((nq + 255) / 256));
-    hipEvent_t e1 = dispatch_events().stop;
-    if (e1)
-      hipExtLaunchKernelGGL(splitk_reduce_kernel, rg, dim3(256), 0, st, nullptr, e1, 0, a, p.splits, out_fp32 ? 1 : 0);
-    else
-      hipLaunchKernelGGL(splitk_reduce_kernel, rg, dim3(256), 0, st, a, p.splits, out_fp32 ? 1 : 0);
-  }
   DS_HIP(hipGetLastError());
   return DSTACK_OK;
 }
@@ -837,7 +873,7 @@ dstack_status launch_conv2d(const bf16* x, int N, int H, int W, int C, const bf1
                             int stride, int pad, const float* scale, const float* shift, const bf16* res, int act,
                             void* y, bool out_fp32, int n_cu, hipStream_t st) {
   return launch_conv2d_ws(x, N, H, W, C, w, K, R, S, stride, pad, scale, shift, res, act, y, out_fp32, n_cu,
-                          nullptr, 0, st);
+                          nullptr, 0, nullptr, st);
 }
 
 }  // namespace dstack

@@ -469,7 +469,7 @@ Model::~Model() {
 
 static size_t align256(size_t b) { return (b + 255) / 256 * 256; }
 
-dstack_status get_workspace(Model& m, int pid, int n_cu, Workspace** out) {
+dstack_status get_workspace(Model& m, int pid, int n_cu, hipStream_t st, Workspace** out) {
   std::lock_guard<std::mutex> g(m.ws_mu);
   auto it = m.ws.find(pid);
   if (it != m.ws.end()) {
@@ -492,6 +492,8 @@ dstack_status get_workspace(Model& m, int pid, int n_cu, Workspace** out) {
     if (op.kind == OP_CONV || op.kind == OP_FC) sk = SPLITK_WS_BYTES;
   size_t sk_off = total;
   total += align256(sk);
+  const size_t cnt_off = total;
+  if (sk) total += align256(SPLITK_TILE_COUNTERS * sizeof(unsigned));
   size_t gx_off = 0, c_off = 0, h0_off = 0, h1_off = 0;
   if (m.is_lstm) {
     gx_off = total;
@@ -510,6 +512,16 @@ dstack_status get_workspace(Model& m, int pid, int n_cu, Workspace** out) {
   if (sk) {
     w->splitk = (float*)(base + sk_off);
     w->splitk_bytes = sk;
+    // the counters start at zero; each fused split-K launch leaves them so
+    w->tile_counters = (unsigned*)(base + cnt_off);
+    dstack_status zs = DSTACK_OK;
+    if (hipMemsetAsync(w->tile_counters, 0, SPLITK_TILE_COUNTERS * sizeof(unsigned), st) != hipSuccess ||
+        hipStreamSynchronize(st) != hipSuccess)
+      zs = fail(DSTACK_E_HIP, "workspace: clearing the split-K counters failed");
+    if (zs != DSTACK_OK) {
+      (void)hipFree(w->base);
+      return zs;
+    }
   }
   if (m.is_lstm) {
     w->lstm_gx = (float*)(base + gx_off);
@@ -582,7 +594,7 @@ dstack_status lstm_layer_run(const bf16* x, int T, int B, int I, int H, const bf
   // input projection of all steps at once: gx[t*B + b][:] = W_ih x + b_ih + b_hh (fp32)
   if (timer) timer->before();
   dstack_status s = launch_conv2d_ws(x, T * B, 1, 1, I, w_ih, 4 * H, 1, 1, 1, 0, nullptr, bias, nullptr, ACT_NONE,
-                                     gx, true, n_cu, nullptr, 0, st);
+                                     gx, true, n_cu, nullptr, 0, nullptr, st);
   if (s != DSTACK_OK) return s;
   if (timer)
     timer->after(KC_MFMA, 2.0 * T * B * I * 4.0 * H,
@@ -643,7 +655,7 @@ dstack_status forward(Model& m, int batch, const void* d_in, void* d_out, Worksp
                              op.scale_off >= 0 ? f32 + op.scale_off : nullptr,
                              op.shift_off >= 0 ? f32 + op.shift_off : nullptr,
                              (const bf16*)bufp(op.res, d_in, d_out), op.act, dst, false, n_cu, ws.splitk,
-                             ws.splitk_bytes, st);
+                             ws.splitk_bytes, ws.tile_counters, st);
         kind = KC_MFMA;
         fl = conv_flops(op, batch);
         by = conv_bytes(op, batch);

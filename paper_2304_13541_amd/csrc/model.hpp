@@ -60,6 +60,7 @@ struct Workspace {
   std::vector<char*> bufs;
   float* splitk = nullptr;
   size_t splitk_bytes = 0;
+  unsigned* tile_counters = nullptr;  // SPLITK_TILE_COUNTERS split-K arrival counters, zero between launches
   float* lstm_gx = nullptr;
   float* lstm_c = nullptr;
   bf16* lstm_h[2] = {nullptr, nullptr};
@@ -113,7 +114,7 @@ dstack_status build_arch(const std::string& arch, Model& m);
 // Device upload of the generated weights and folded BN parameters.
 dstack_status upload_weights(Model& m);
 // Workspace for batch <= max_batch, on demand.
-dstack_status get_workspace(Model& m, int partition_id, int n_cu, Workspace** out);
+dstack_status get_workspace(Model& m, int partition_id, int n_cu, hipStream_t st, Workspace** out);
 
 // Enqueue one forward pass on `st`.  `timer` may be null.
 dstack_status forward(Model& m, int batch, const void* d_in, void* d_out, Workspace& ws, int n_cu, hipStream_t st,
@@ -143,7 +144,7 @@ size_t conv_splitk_workspace_bytes(int M, int K, int Kg, int n_cu);
 dstack_status launch_conv2d_ws(const bf16* x, int N, int H, int W, int C, const bf16* w, int K, int R, int S,
                                int stride, int pad, const float* scale, const float* shift, const bf16* res,
                                int act, void* y, bool out_fp32, int n_cu, float* splitk_ws, size_t splitk_bytes,
-                               hipStream_t st);
+                               unsigned* tile_counters, hipStream_t st);
 dstack_status lstm_layer_run(const bf16* x, int T, int B, int I, int H, const bf16* w_ih, const bf16* w_hh,
                              const float* bias, bf16* h_bf16, float* h_f32, float* gx, float* c, int n_cu,
                              hipStream_t st, KernelTimer* timer);
