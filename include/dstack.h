@@ -153,7 +153,8 @@ dstack_status dstack_infer(dstack_model m, int batch, const void* d_in, void* d_
 /* Per-kernel timing of one forward: fills up to max_layers entries with
  * the elapsed device time (ms, HIP events around each kernel on the
  * partition's stream), the kernel class (0 MFMA conv/GEMM, 1 depthwise,
- * 2 FC, 3 LSTM step, 4 pool/glue) and its algorithmic FLOPs and bytes.
+ * 2 FC, 3 LSTM step, 4 pool/glue, 5 direct RGB stem conv) and its
+ * algorithmic FLOPs and bytes.
  * Synchronises the partition. */
 typedef struct {
   int kind;
@@ -439,6 +440,16 @@ dstack_status dstack_serve(const dstack_model* models, int n_models, const void*
 dstack_status dstack_op_conv2d(const void* x, int N, int H, int W, int C, const void* w, int K, int R, int S,
                                int stride, int pad, const float* scale, const float* shift, const void* res, int act,
                                void* y, int out_fp32, void* stream);
+/* conv2d_rgb: the conv2d above for a 3-channel image x [N][H][W][3] read as
+ *   it is (the stems of Sec. 3's CNNs; no packing to 8 channels), with
+ *   weights w4 [K][R][R][4] bf16 (channel 3 zero: the stem layout the
+ *   models store), no residual and bf16 output.  (R, K) one of (3, 16),
+ *   (3, 32), (3, 64), (7, 64) (else E_UNSUPPORTED); stride >= 1,
+ *   0 <= pad < R; scale and shift are required; image rows too wide for a
+ *   64 KB LDS tile of the input rows that 256 output pixels touch give
+ *   E_UNSUPPORTED. */
+dstack_status dstack_op_conv2d_rgb(const void* x, int N, int H, int W, const void* w4, int K, int R, int stride,
+                                   int pad, const float* scale, const float* shift, int act, void* y, void* stream);
 dstack_status dstack_op_dwconv3x3(const void* x, int N, int H, int W, int C, const void* w, int stride,
                                   const float* scale, const float* shift, int act, void* y, void* stream);
 size_t dstack_fc_workspace_bytes(int B, int I, int O);

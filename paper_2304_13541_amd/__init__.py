@@ -18,7 +18,7 @@ TOTAL_SLOTS = 32
 CUS_PER_SLOT = 8
 MAX_SWEEP, MAX_BATCHES, MAX_MODELS, MAX_JOBS = 32, 8, 16, 512
 ARCHS = ("tinycnn", "resnet50", "mobilenetv2", "vgg19", "lstm2")
-KIND_NAMES = {0: "mfma", 1: "depthwise", 2: "fc", 3: "lstm_step", 4: "glue"}
+KIND_NAMES = {0: "mfma", 1: "depthwise", 2: "fc", 3: "lstm_step", 4: "glue", 5: "direct_conv"}
 
 
 class DStackError(RuntimeError):
@@ -141,6 +141,7 @@ _SIGS = {
                       ctypes.POINTER(SchedParams), ctypes.POINTER(SimParams), ctypes.POINTER(RunOut),
                       ctypes.POINTER(JobRecord), _i, ctypes.POINTER(_i)], _i),
     "dstack_op_conv2d": ([_vp, _i, _i, _i, _i, _vp, _i, _i, _i, _i, _i, _vp, _vp, _vp, _i, _vp, _i, _vp], _i),
+    "dstack_op_conv2d_rgb": ([_vp, _i, _i, _i, _vp, _i, _i, _i, _i, _vp, _vp, _i, _vp, _vp], _i),
     "dstack_op_dwconv3x3": ([_vp, _i, _i, _i, _i, _vp, _i, _vp, _vp, _i, _vp, _vp], _i),
     "dstack_fc_workspace_bytes": ([_i, _i, _i], _sz),
     "dstack_op_fc": ([_vp, _i, _i, _vp, _vp, _i, _i, _vp, _i, _vp, _sz, _vp], _i),
@@ -460,6 +461,14 @@ def conv2d(x, w, K, R, S, stride, pad, scale, shift, res, act, y, out_fp32=False
     N, H, W, C = x.shape
     _check(lib().dstack_op_conv2d(_ptr(x), N, H, W, C, _ptr(w), K, R, S, stride, pad, _ptr(scale), _ptr(shift),
                                   _ptr(res), act, _ptr(y), int(out_fp32), _stream(stream)))
+
+
+def conv2d_rgb(x, w4, K, R, stride, pad, scale, shift, act, y, stream=None):
+    """x [N,H,W,3] bf16, w4 [K,R,R,4] bf16 (channel 3 zero) -> y [N,Ho,Wo,K] bf16."""
+    N, H, W, C = x.shape
+    assert C == 3
+    _check(lib().dstack_op_conv2d_rgb(_ptr(x), N, H, W, _ptr(w4), K, R, stride, pad, _ptr(scale), _ptr(shift), act,
+                                      _ptr(y), _stream(stream)))
 
 
 def dwconv3x3(x, w_rsc, stride, scale, shift, act, y, stream=None):

@@ -230,6 +230,10 @@ static void unlayout(const TensorSpec& t, const uint16_t* dev, uint16_t* logical
     int64_t krs = (int64_t)t.d0 * t.d1 * t.d2;
     for (int64_t q = 0; q < krs; ++q)
       for (int c = 0; c < t.d3; ++c) logical[q * t.d3 + c] = dev[q * 8 + c];
+  } else if (t.layout == 3) {
+    int64_t krs = (int64_t)t.d0 * t.d1 * t.d2;
+    for (int64_t q = 0; q < krs; ++q)
+      for (int c = 0; c < t.d3; ++c) logical[q * t.d3 + c] = dev[q * 4 + c];
   } else {
     int C = t.d0;
     for (int c = 0; c < C; ++c)
@@ -244,9 +248,9 @@ dstack_status dstack_model_export_params(dstack_model h, int idx, void* dst, siz
     DS_CHECK(idx >= 0 && idx < (int)m.tensors.size(), DSTACK_E_INVALID, "export: tensor index out of range");
     const TensorSpec& t = m.tensors[idx];
     DS_CHECK(bytes == (size_t)t.numel * 2, DSTACK_E_INVALID, "export: byte count must be 2 * numel");
-    int64_t dev_numel = t.layout == 1 ? (int64_t)t.d0 * t.d1 * t.d2 * 8 : t.numel;
-    std::vector<uint16_t> tmp((size_t)dev_numel);
-    DS_HIP(hipMemcpy(tmp.data(), m.d_w + t.dev_off, (size_t)dev_numel * 2, hipMemcpyDeviceToHost));
+    const int64_t n_dev = dev_numel(t);
+    std::vector<uint16_t> tmp((size_t)n_dev);
+    DS_HIP(hipMemcpy(tmp.data(), m.d_w + t.dev_off, (size_t)n_dev * 2, hipMemcpyDeviceToHost));
     unlayout(t, tmp.data(), (uint16_t*)dst);
     return DSTACK_OK;
   });
@@ -660,6 +664,16 @@ dstack_status dstack_op_conv2d(const void* x, int N, int H, int W, int C, const 
     DS_CHECK(act >= 0 && act <= 2, DSTACK_E_INVALID, "conv2d: act must be 0, 1 or 2");
     return launch_conv2d(static_cast<const bf16*>(x), N, H, W, C, static_cast<const bf16*>(w), K, R, S, stride, pad,
                          scale, shift, static_cast<const bf16*>(res), act, y, out_fp32 != 0, 256, (hipStream_t)stream);
+  });
+}
+
+dstack_status dstack_op_conv2d_rgb(const void* x, int N, int H, int W, const void* w4, int K, int R, int stride,
+                                   int pad, const float* scale, const float* shift, int act, void* y, void* stream) {
+  return guarded([&] {
+    DS_CHECK(x && w4 && y, DSTACK_E_INVALID, "conv2d_rgb: null pointer");
+    DS_CHECK(act >= 0 && act <= 2, DSTACK_E_INVALID, "conv2d_rgb: act must be 0, 1 or 2");
+    return launch_conv2d_rgb(static_cast<const bf16*>(x), N, H, W, static_cast<const bf16*>(w4), K, R, stride, pad,
+                             scale, shift, act, static_cast<bf16*>(y), (hipStream_t)stream);
   });
 }
 

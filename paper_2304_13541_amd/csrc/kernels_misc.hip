@@ -1,5 +1,5 @@
-// Memory-bound kernels of the hot path: depthwise 3x3 convolution, pooling
-// and input packing.  In the paper's terms (Sec. 4.1) these are the low
+// Memory-bound kernels of the hot path: depthwise 3x3 convolution and
+// pooling.  In the paper's terms (Sec. 4.1) these are the low
 // arithmetic-intensity kernels: they are written for coalesced 16-byte
 // accesses along the channel (NHWC) axis, not for matrix cores.
 
@@ -199,64 +199,6 @@ dstack_status launch_avgpool(const bf16* x, int N, int H, int W, int C, bf16* y,
   DS_CHECK(C % 8 == 0, DSTACK_E_UNSUPPORTED, "avgpool: C must be a multiple of 8");
   DS_CHECK(N > 0 && H > 0 && W > 0 && N <= 65535, DSTACK_E_INVALID, "avgpool: bad shape");
   hipLaunchKernelGGL(avgpool_kernel, dim3(ceil_div(C / 8, 32), N), dim3(256), 0, st, x, N, H * W, C, y);
-  DS_HIP(hipGetLastError());
-  return DSTACK_OK;
-}
-
-// Input packing: [npix][C] -> [npix][8] with zero channels C..7 (C <= 8).
-__global__ __launch_bounds__(256) void pack_c8_kernel(const bf16* __restrict__ x, long npix, int C,
-                                                      bf16* __restrict__ y) {
-  long p = (long)blockIdx.x * blockDim.x + threadIdx.x;
-  if (p >= npix) return;
-  bf16x8 o = {};
-  for (int c = 0; c < C; ++c) o[c] = x[p * C + c];
-  st8(y + p * 8, o);
-}
-
-// 3-channel images (the common case): block = 2048 pixels.  Threads load
-// the block's 12 KB of input as 16-byte vectors (thread t: vectors t, t + 256,
-// t + 512), stage it in LDS, then each store instruction writes 64
-// consecutive output pixels (lane l: pixel 64 k + l of the wave's range).
-// npix is a multiple of 8; pixels past it (the last block) are not stored.
-__global__ __launch_bounds__(256) void pack_c3_kernel(const bf16* __restrict__ x, long npix, bf16* __restrict__ y) {
-  __shared__ bf16x8 in[768];  // 2048 pixels x 3 channels
-  const long p0 = (long)blockIdx.x * 2048;
-  const long nvec = npix * 3 / 8;  // npix is a multiple of 8: whole input vectors
-  const long v0 = p0 * 3 / 8;
-#pragma unroll
-  for (int k = 0; k < 3; ++k) {
-    const int i = threadIdx.x + 256 * k;
-    in[i] = v0 + i < nvec ? reinterpret_cast<const bf16x8*>(x)[v0 + i] : bf16x8{};
-  }
-  __syncthreads();
-  const bf16* e = reinterpret_cast<const bf16*>(in);
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-#pragma unroll
-  for (int k = 0; k < 8; ++k) {
-    const int pl = wave * 512 + k * 64 + lane;  // pixel within the block
-    const long p = p0 + pl;
-    if (p >= npix) break;
-    bf16x8 o = {};
-    o[0] = e[3 * pl];
-    o[1] = e[3 * pl + 1];
-    o[2] = e[3 * pl + 2];
-    st8(y + p * 8, o);
-  }
-}
-
-dstack_status launch_pack_c8(const bf16* x, int npix, int C, bf16* y, hipStream_t st) {
-  DS_CHECK(C >= 1 && C <= 8 && npix > 0, DSTACK_E_INVALID, "pack: bad shape");
-  long done = 0;
-  if (C == 3 && ((uintptr_t)x & 15) == 0) {
-    // the fast path takes a multiple of 8 pixels (whole 16-byte input vectors)
-    const long npix3 = (long)npix / 8 * 8;
-    if (npix3 > 0)
-      hipLaunchKernelGGL(pack_c3_kernel, dim3((unsigned)((npix3 + 2047) / 2048)), dim3(256), 0, st, x, npix3, y);
-    done = npix3;
-  }
-  if (done < npix)
-    hipLaunchKernelGGL(pack_c8_kernel, dim3((unsigned)((npix - done + 255) / 256)), dim3(256), 0, st, x + done * C,
-                       (long)(npix - done), C, y + done * 8);
   DS_HIP(hipGetLastError());
   return DSTACK_OK;
 }

@@ -41,9 +41,8 @@ struct Builder {
     t.fan_in = fan_in;
     t.layout = layout;
     t.d0 = d0; t.d1 = d1; t.d2 = d2; t.d3 = d3;
-    int64_t dev_numel = (layout == 1) ? (int64_t)d0 * d1 * d2 * 8 : numel;
     t.dev_off = m.n_weights;
-    m.n_weights += (dev_numel + 127) / 128 * 128;  // 256-byte aligned tensors
+    m.n_weights += (dev_numel(t) + 127) / 128 * 128;  // 256-byte aligned tensors
     m.tensors.push_back(t);
     return (int)m.tensors.size() - 1;
   }
@@ -95,6 +94,26 @@ class ArchBuilder {
     if (bn) op.scale_off = b.f32(K);
     if (bn || bias_t >= 0) op.shift_off = b.f32(K);
     op.out = (out_buf == -100) ? b.alloc((int64_t)op.Ho * op.Wo * K) : out_buf;
+    op.w_t = wt;
+    op.bias_t = bias_t;
+    op.bn = bn ? 1 : 0;
+    push(op);
+    return Shape{op.out, op.Ho, op.Wo, K};
+  }
+  // stem conv straight from the 3-channel input image (weights [K][R][R][4])
+  Shape conv_rgb(int H, int W, int wt, int K, int R, int stride, int pad, bool bn, int bias_t, int act) {
+    Op op;
+    op.kind = OP_CONV_RGB;
+    op.in = BUF_IN;
+    op.H = H; op.W = W; op.C = 3; op.K = K; op.R = R; op.S = R; op.stride = stride; op.pad = pad;
+    op.act = act;
+    op.Ho = out_dim(H, R, stride, pad);
+    op.Wo = out_dim(W, R, stride, pad);
+    op.C_true = 3;
+    op.w_off = m.tensors[wt].dev_off;
+    op.scale_off = b.f32(K);  // 1 without BN
+    op.shift_off = b.f32(K);
+    op.out = b.alloc((int64_t)op.Ho * op.Wo * K);
     op.w_t = wt;
     op.bias_t = bias_t;
     op.bn = bn ? 1 : 0;
@@ -156,15 +175,6 @@ class ArchBuilder {
     push(op);
     return Shape{op.out, 1, 1, O};
   }
-  Shape pack(int H, int W) {
-    Op op;
-    op.kind = OP_PACK;
-    op.in = BUF_IN;
-    op.H = H; op.W = W; op.C = 3; op.K = 8;
-    op.out = b.alloc((int64_t)H * W * 8);
-    push(op);
-    return Shape{op.out, H, W, 8};
-  }
   void done(const Shape& s, const Shape& keep) {
     if (s.buf != keep.buf) b.release(s.buf);
   }
@@ -178,11 +188,11 @@ void build_tiny(ArchBuilder& A) {
   const int ch[5] = {3, 16, 32, 32, 64};
   int wt[4];
   for (int l = 0; l < 4; ++l)
-    wt[l] = A.b.tensor((int64_t)ch[l + 1] * 9 * ch[l], DIST_HE, 9 * ch[l], l == 0 ? 1 : 0, ch[l + 1], 3, 3, ch[l]);
+    wt[l] = A.b.tensor((int64_t)ch[l + 1] * 9 * ch[l], DIST_HE, 9 * ch[l], l == 0 ? 3 : 0, ch[l + 1], 3, 3, ch[l]);
   int fw = A.b.tensor(640, DIST_HE, 64);
   int fb = A.b.tensor(10, DIST_ZERO, 0);
-  Shape x = A.pack(32, 32);
-  for (int l = 0; l < 4; ++l) {
+  Shape x = A.conv_rgb(32, 32, wt[0], ch[1], 3, 1, 1, true, -1, ACT_RELU);
+  for (int l = 1; l < 4; ++l) {
     Shape y = A.conv(x, wt[l], ch[l + 1], 3, 1, 1, true, -1, ACT_RELU, BUF_NONE, ch[l]);
     A.b.release(x.buf);
     x = y;
@@ -203,7 +213,7 @@ void build_r50(ArchBuilder& A) {
   m.in_c = 3;
   m.out_features = 1000;
   static const int stages[4][3] = {{3, 64, 1}, {4, 128, 2}, {6, 256, 2}, {3, 512, 2}};
-  int stem = A.b.tensor(64L * 49 * 3, DIST_HE, 147, 1, 64, 7, 7, 3);
+  int stem = A.b.tensor(64L * 49 * 3, DIST_HE, 147, 3, 64, 7, 7, 3);
   struct Blk {
     int w1, w2, w3, wd, planes, stride, cin;
   };
@@ -227,9 +237,7 @@ void build_r50(ArchBuilder& A) {
   int fw = A.b.tensor(1000L * 2048, DIST_HE, 2048);
   int fb = A.b.tensor(1000, DIST_ZERO, 0);
 
-  Shape x = A.pack(224, 224);
-  Shape s = A.conv(x, stem, 64, 7, 2, 3, true, -1, ACT_RELU, BUF_NONE, 3);
-  A.b.release(x.buf);
+  Shape s = A.conv_rgb(224, 224, stem, 64, 7, 2, 3, true, -1, ACT_RELU);
   Shape cur = A.maxpool(s, 3, 2, 1);
   A.b.release(s.buf);
   for (const Blk& k : blks) {
@@ -256,7 +264,7 @@ void build_mbv2(ArchBuilder& A) {
   m.out_features = 1000;
   static const int cfg[7][4] = {{1, 16, 1, 1}, {6, 24, 2, 2}, {6, 32, 3, 2}, {6, 64, 4, 2},
                                 {6, 96, 3, 1}, {6, 160, 3, 2}, {6, 320, 1, 1}};
-  int stem = A.b.tensor(32L * 9 * 3, DIST_HE, 27, 1, 32, 3, 3, 3);
+  int stem = A.b.tensor(32L * 9 * 3, DIST_HE, 27, 3, 32, 3, 3, 3);
   struct Blk {
     int we, wd, wp, cin, hid, cout, stride;
   };
@@ -281,9 +289,7 @@ void build_mbv2(ArchBuilder& A) {
   int fw = A.b.tensor(1000L * 1280, DIST_HE, 1280);
   int fb = A.b.tensor(1000, DIST_ZERO, 0);
 
-  Shape x = A.pack(224, 224);
-  Shape cur = A.conv(x, stem, 32, 3, 2, 1, true, -1, ACT_RELU6, BUF_NONE, 3);
-  A.b.release(x.buf);
+  Shape cur = A.conv_rgb(224, 224, stem, 32, 3, 2, 1, true, -1, ACT_RELU6);
   for (const Blk& k : blks) {
     Shape e = cur;
     if (k.we >= 0) e = A.conv(cur, k.we, k.hid, 1, 1, 0, true, -1, ACT_RELU6, BUF_NONE, k.cin);
@@ -314,7 +320,7 @@ void build_vgg(ArchBuilder& A) {
   for (int st = 0; st < 5; ++st)
     for (int i = 0; i < nconv[st]; ++i) {
       int cout = chs[st];
-      wts.push_back(A.b.tensor((int64_t)cout * 9 * cin, DIST_HE, 9 * cin, cin == 3 ? 1 : 0, cout, 3, 3, cin));
+      wts.push_back(A.b.tensor((int64_t)cout * 9 * cin, DIST_HE, 9 * cin, cin == 3 ? 3 : 0, cout, 3, 3, cin));
       bts.push_back(A.b.tensor(cout, DIST_ZERO, 0));
       couts.push_back(cout);
       cins.push_back(cin);
@@ -324,10 +330,10 @@ void build_vgg(ArchBuilder& A) {
   int f2 = A.b.tensor(4096L * 4096, DIST_HE, 4096), b2 = A.b.tensor(4096, DIST_ZERO, 0);
   int f3 = A.b.tensor(1000L * 4096, DIST_HE, 4096), b3 = A.b.tensor(1000, DIST_ZERO, 0);
 
-  Shape cur = A.pack(224, 224);
-  size_t li = 0;
+  Shape cur = A.conv_rgb(224, 224, wts[0], couts[0], 3, 1, 1, false, bts[0], ACT_RELU);
+  size_t li = 1;
   for (int st = 0; st < 5; ++st) {
-    for (int i = 0; i < nconv[st]; ++i, ++li) {
+    for (int i = st == 0 ? 1 : 0; i < nconv[st]; ++i, ++li) {
       Shape y = A.conv(cur, wts[li], couts[li], 3, 1, 1, false, bts[li], ACT_RELU, BUF_NONE, cins[li]);
       A.b.release(cur.buf);
       cur = y;
@@ -416,6 +422,10 @@ dstack_status upload_weights(Model& m) {
       int64_t krs = (int64_t)t.d0 * t.d1 * t.d2;
       for (int64_t q = 0; q < krs; ++q)
         for (int c = 0; c < t.d3; ++c) dst[q * 8 + c] = v[(size_t)(q * t.d3 + c)];
+    } else if (t.layout == 3) {  // RGB stem [K][R][S][3] -> [K][R][S][4]
+      int64_t krs = (int64_t)t.d0 * t.d1 * t.d2;
+      for (int64_t q = 0; q < krs; ++q)
+        for (int c = 0; c < t.d3; ++c) dst[q * 4 + c] = v[(size_t)(q * t.d3 + c)];
     } else {  // depthwise [C][3][3] -> [3][3][C]
       int C = t.d0;
       for (int c = 0; c < C; ++c)
@@ -646,9 +656,12 @@ dstack_status forward(Model& m, int batch, const void* d_in, void* d_out, Worksp
     double fl = 0, by = 0;
     int gm = 0, gn = 0, gk = 0;
     switch (op.kind) {
-      case OP_PACK:
-        s = launch_pack_c8(src, batch * op.H * op.W, op.C, (bf16*)dst, st);
-        by = (double)batch * op.H * op.W * (3 + 8) * 2;
+      case OP_CONV_RGB:
+        s = launch_conv2d_rgb(src, batch, op.H, op.W, m.d_w + op.w_off, op.K, op.R, op.stride, op.pad,
+                              f32 + op.scale_off, f32 + op.shift_off, op.act, (bf16*)dst, st);
+        kind = KC_DIRECT;
+        fl = conv_flops(op, batch);
+        by = conv_bytes(op, batch);
         break;
       case OP_CONV:
         s = launch_conv2d_ws(src, batch, op.H, op.W, op.C, m.d_w + op.w_off, op.K, op.R, op.S, op.stride, op.pad,
@@ -702,6 +715,10 @@ void model_cost(const Model& m, int b, double* flops, double* mfma, double* wbyt
       case OP_CONV:
         f += conv_flops(op, b);
         mf += conv_flops(op, b);
+        ++n;
+        break;
+      case OP_CONV_RGB:
+        f += conv_flops(op, b);
         ++n;
         break;
       case OP_DW:

@@ -21,15 +21,23 @@ struct TensorSpec {
   int fan_in = 0;
   // device placement
   int64_t dev_off = 0;   // bf16 elements into the weight arena
-  int layout = 0;        // 0 same as logical, 1 conv stem padded C->8, 2 depthwise [C][3][3] -> [3][3][C]
+  int layout = 0;        // 0 same as logical, 1 conv stem padded C->8, 2 depthwise [C][3][3] -> [3][3][C],
+                         // 3 RGB stem padded C->4
   int d0 = 0, d1 = 0, d2 = 0, d3 = 0;  // logical dims for re-layout
 };
+// elements of a tensor's device layout
+inline int64_t dev_numel(const TensorSpec& t) {
+  if (t.layout == 1) return (int64_t)t.d0 * t.d1 * t.d2 * 8;
+  if (t.layout == 3) return (int64_t)t.d0 * t.d1 * t.d2 * 4;
+  return t.numel;
+}
+
 
 uint16_t bf16_from_double(double x);
 void generate_tensor(uint64_t seed, int index, const TensorSpec& t, uint16_t* out);
 
-enum OpKind { OP_PACK, OP_CONV, OP_DW, OP_MAXPOOL, OP_AVGPOOL, OP_FC, OP_LSTM };
-enum KernelClass { KC_MFMA = 0, KC_DW = 1, KC_FC = 2, KC_LSTM = 3, KC_GLUE = 4 };
+enum OpKind { OP_CONV, OP_DW, OP_MAXPOOL, OP_AVGPOOL, OP_FC, OP_LSTM, OP_CONV_RGB };
+enum KernelClass { KC_MFMA = 0, KC_DW = 1, KC_FC = 2, KC_LSTM = 3, KC_GLUE = 4, KC_DIRECT = 5 };
 
 constexpr int BUF_IN = -1;
 constexpr int BUF_OUT = -2;

@@ -73,6 +73,45 @@ def test_conv2d(env, case):
     assert err <= TOL
 
 
+RGB_CASES = [
+    # N, H, W, K, R, stride, pad, act
+    (2, 17, 16, 32, 3, 2, 1, 2),    # MobileNetV2-like stem, ragged last tile; W % 8 == 0 (vector row copy)
+    (1, 32, 32, 16, 3, 1, 1, 1),    # the tiny CNN's stem
+    (3, 9, 13, 32, 3, 2, 1, 0),     # W % 8 != 0 (element row copy), odd sizes, no activation
+    (1, 5, 300, 16, 3, 1, 0, 1),    # output rows wider than a 256-pixel tile, pad 0
+    (2, 11, 21, 64, 3, 1, 1, 1),    # VGG-19-like stem (3 x 3, 64 channels)
+    (2, 23, 24, 64, 7, 2, 3, 1),    # ResNet-50-like stem (7 x 7 / 2, 64 channels)
+    (1, 224, 224, 32, 3, 2, 1, 2),  # the full 224 x 224 MobileNetV2 stem
+    (1, 224, 224, 64, 7, 2, 3, 1),  # the full 224 x 224 ResNet-50 stem
+]
+
+
+@pytest.mark.parametrize("case", RGB_CASES)
+def test_conv2d_rgb(env, case):
+    """Direct 3-channel stem conv on the matrix cores (weights [K][R][R][4],
+    channel 3 zero) against the oracle's conv2d on the unpadded tensors."""
+    ds, gu, inputs, oracle, torch = env
+    N, H, W, K, R, st, pad, act = case
+    print("conv2d_rgb case", case, flush=True)
+    xb = inputs.normal_bf16(11, (N, H, W, 3))
+    wb = inputs.normal_bf16(12, (K, R, R, 3), scale=(2.0 / (3 * R * R)) ** 0.5)
+    w4 = np.zeros((K, R, R, 4), dtype=wb.dtype)
+    w4[..., :3] = wb
+    rng = np.random.default_rng(13)
+    scale = rng.uniform(0.5, 1.5, K).astype(np.float32)
+    shift = rng.uniform(-0.2, 0.2, K).astype(np.float32)
+    Ho, Wo = (H + 2 * pad - R) // st + 1, (W + 2 * pad - R) // st + 1
+    y = gu.empty_bf16((N, Ho, Wo, K))
+    ds.conv2d_rgb(gu.dev_bf16(xb), gu.dev_bf16(w4), K, R, st, pad, gu.dev_f32(scale), gu.dev_f32(shift), act, y)
+    torch.cuda.synchronize()
+    ref = oracle.conv2d(oracle.bf16_bits_to_f64(xb), oracle.bf16_bits_to_f64(wb), st, pad)
+    ref = ref * scale.astype(np.float64) + shift.astype(np.float64)
+    ref = np.maximum(ref, 0) if act == 1 else (np.clip(ref, 0, 6) if act == 2 else ref)
+    err = oracle.rel_err(gu.host(y), ref)
+    print("rel_err", err)
+    assert err <= TOL
+
+
 @pytest.mark.parametrize("case", [(2, 11, 9, 32, 1), (1, 12, 12, 96, 2), (3, 7, 7, 960, 1), (2, 15, 13, 144, 2),
                                   (1, 30, 30, 16, 1), (2, 7, 33, 24, 1), (1, 29, 29, 40, 2), (1, 5, 61, 8, 2)])
 def test_dwconv3x3(env, case):
@@ -163,6 +202,14 @@ def test_kernel_argument_errors(env):
     y = gu.empty_bf16((1, 4, 4, 8))
     with pytest.raises(ds.DStackError) as e:  # C % 8 != 0
         ds.conv2d(x, w, 8, 3, 3, 1, 1, None, None, None, 0, y)
+    assert e.value.status == ds.E_UNSUPPORTED
+    x3 = gu.empty_bf16((1, 8, 8, 3))
+    sc = gu.dev_f32(np.ones(128, np.float32))
+    with pytest.raises(ds.DStackError) as e:  # RGB stem with K = 128
+        ds.conv2d_rgb(x3, gu.empty_bf16((128, 3, 3, 4)), 128, 3, 1, 1, sc, sc, 0, gu.empty_bf16((1, 8, 8, 128)))
+    assert e.value.status == ds.E_UNSUPPORTED
+    with pytest.raises(ds.DStackError) as e:  # RGB stem with a 5 x 5 filter
+        ds.conv2d_rgb(x3, gu.empty_bf16((16, 5, 5, 4)), 16, 5, 1, 2, sc, sc, 0, gu.empty_bf16((1, 8, 8, 16)))
     assert e.value.status == ds.E_UNSUPPORTED
     xb = gu.empty_bf16((33, 64))
     with pytest.raises(ds.DStackError) as e:  # batch > 32
