@@ -21,15 +21,21 @@ counts one batch at a time on an unmasked partition.  Per-kernel HIP-event
 timing on each partition's stream gives the conv MFMA TFLOP/s at the knee and
 the roofline fraction of the dominant kernel (the implicit-GEMM convolution);
 each partition's batch time alone vs in the mix gives the interference.
+Rooflines per model use P(n) = 2516.6 TFLOP/s * n/256 and BW(n) measured by a
+device copy on the partition's stream ("per_model[].roofline"); "mix" holds
+the same-work makespan ratio, the FLOP-weighted work rate, the CU-weighted
+roofline busy fraction and the same models on unmasked concurrent streams.
 
-Also reported (not the headline): for each headline model the knee found by
-a binary search from 30% against the sweep's knee, and the cost of a GPU%
-change, cold and active-standby ("reconfiguration"); the VGG-19 batch 8 +
-LSTM batch 32 pair in the same closed-loop form ("config4"), and the
-four-model Poisson mix (ResNet-50, MobileNetV2, VGG-19, LSTM at
-400/800/150/300 req/s, SLOs 25/15/50/30 ms, 100 ms sessions) through the live
-launcher dstack_serve for 10 s at the stated rates plus a capacity sweep of
-2 s runs at k x the rates ("config5"); --headline-only skips all three.
+Also reported (not the headline): the tiny CNN at 100/50/25% ("config1");
+ResNet-50 at batch 1/8/32 over the 10 fractions ("config2"); for each
+headline model the knee found by a binary search from 30% against the sweep's
+knee, and the cost of a GPU% change, cold and active-standby
+("reconfiguration"); the VGG-19 batch 8 + LSTM batch 32 pair in the same
+closed-loop form ("config4"), and the four-model Poisson mix (ResNet-50,
+MobileNetV2, VGG-19, LSTM at 400/800/150/300 req/s, SLOs 25/15/50/30 ms,
+100 ms sessions) through the live launcher dstack_serve for 10 s at the
+stated rates plus a capacity sweep of 2 s runs at k x the rates ("config5");
+--headline-only skips these.
 """
 import argparse
 import hashlib
@@ -105,11 +111,16 @@ def measured_traffic():
     return float(vals["traffic_bytes_per_launch"])
 
 
-def cpu_baseline(budget_s):
+def cpu_baseline(budget_s, sched_in):
     """The oracle, as it stands, on the host cores: sampled items of the same
-    workload (batch items are independent), parity mode."""
+    workload (batch items are independent), parity mode; and the scheduler
+    oracle's time for the same scheduling decision as the library's."""
     import oracle
+    from oracle import sched as osched
     from tests import inputs
+    t_s = time.perf_counter()
+    osched.schedule(sched_in, PERIOD_US)
+    sched_s = time.perf_counter() - t_s
     done, t0 = 0, time.perf_counter()
     models = {a: oracle.Model(a, s) for a, s, *_ in MODELS}
     i = 0
@@ -124,7 +135,7 @@ def cpu_baseline(budget_s):
     threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
     return dict(value=done / el, unit="inferences/s", cores=threads, kind="oracle",
                 sample="%d single 224x224 images alternating ResNet-50 / MobileNetV2 (fp64 oracle, parity mode), "
-                       "%.1f s" % (done, el))
+                       "%.1f s" % (done, el), scheduler_oracle_seconds=sched_s)
 
 
 def knee_at(row, b):
@@ -135,6 +146,59 @@ def knee_at(row, b):
         if best is None or b * row[best] ** 2 * best > b * L * L * s:
             best = s
     return best
+
+
+def bw_probe(torch, part, mib=512, reps=5):
+    """HBM bandwidth available to a partition: a plain device copy on its
+    stream (bytes read + written per second, GB/s).  BW(n) of the roofline."""
+    st = part.torch_stream()
+    n = mib * 1024 * 1024 // 4
+    with torch.cuda.stream(st):
+        a = torch.zeros(n, dtype=torch.float32, device="cuda")
+        b = torch.empty_like(a)
+        b.copy_(a)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(st)
+        for _ in range(reps):
+            b.copy_(a)
+        e1.record(st)
+    torch.cuda.synchronize()
+    gbs = 2.0 * n * 4 * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    del a, b
+    return gbs
+
+
+def model_roofline(ds, recs, n_cu, bw_gbs, latency_us):
+    """Roofline of one model's forward on a partition of n_cu CUs: MFMA peak
+    P(n) = 2516.6 TFLOP/s * n/256, HBM BW(n) measured; per layer the bound is
+    max(FLOP/P, bytes/BW); conv layers at or above the ridge P/BW are judged
+    against MFMA, the rest and the memory-bound kernels against BW."""
+    P = PEAK_BF16_TFLOPS * 1e12 * n_cu / 256
+    BW = bw_gbs * 1e9
+    ridge = P / BW
+    t_roof = sum(max(r["flops"] / P, r["bytes"] / BW) for r in recs)
+    t_kern = sum(r["ms"] for r in recs) * 1e-3
+    mfma_bound = [r for r in recs if r["kind"] == 0 and r["bytes"] > 0 and r["flops"] / r["bytes"] >= ridge]
+    mb_ms = sum(r["ms"] for r in mfma_bound)
+    conv_mfma_frac = sum(r["flops"] for r in mfma_bound) / (mb_ms * 1e-3) / P if mb_ms > 0 else None
+    hbm = {}
+    for r in recs:
+        if r in mfma_bound:
+            continue
+        name = "conv_below_ridge" if r["kind"] == 0 else ds.KIND_NAMES[r["kind"]]
+        d = hbm.setdefault(name, dict(n=0, ms=0.0, bytes=0.0))
+        d["n"] += 1
+        d["ms"] += r["ms"]
+        d["bytes"] += r["bytes"]
+    for d in hbm.values():
+        d["achieved_gbs"] = d["bytes"] / (d["ms"] * 1e-3) / 1e9 if d["ms"] > 0 else None
+        d["hbm_frac"] = d["achieved_gbs"] / bw_gbs if d["achieved_gbs"] else None
+    return dict(n_cu=n_cu, hbm_gbs_measured=bw_gbs, mfma_peak_tflops=P / 1e12, ridge_flop_per_byte=ridge,
+                t_roof_us=1e6 * t_roof, kernel_sum_us=1e6 * t_kern, latency_us=latency_us,
+                model_roofline_frac=1e6 * t_roof / latency_us if latency_us else None,
+                kernel_roofline_frac=t_roof / t_kern if t_kern > 0 else None,
+                conv_mfma_frac=conv_mfma_frac, conv_mfma_frac_target=0.6, mfma_bound_conv_layers=len(mfma_bound),
+                hbm_bound=hbm)
 
 
 def fit_slots(dep, total):
@@ -250,6 +314,31 @@ def layer_stats(ds, m, batch, x, y, part):
         d["flops"] += r["flops"]
         d["bytes"] += r["bytes"]
     return recs, by_kind
+
+
+def config1(ds):
+    """Tiny CNN batch 4 (32x32x3) at 100/50/25% of the GPU: 1000 timed forwards each."""
+    m = ds.Model("tinycnn", 1010)
+    fr = [1.0, 0.5, 0.25]
+    r = m.knee_sweep(4, fr, warmup=50, reps=1000)
+    m.destroy()
+    return dict(workload="tiny CNN batch 4, 32x32x3, seed 1010", fractions=fr, n_cu=r["n_cu"],
+                latency_us=r["latency_us"], p99_us=r["p99_us"], inferences_per_s=[4e6 / L for L in r["latency_us"]])
+
+
+def config2(ds, args):
+    """ResNet-50 at batch 1, 8 and 32 over the 10 fractions: latency, inf/s,
+    efficacy b / (L^2 * CUs) and the knee (Sec. 3.2)."""
+    m = ds.Model("resnet50", 1020)
+    rows = []
+    for b in (1, 8, 32):
+        r = m.knee_sweep(b, FRACTIONS, warmup=args.sweep_warmup, reps=args.sweep_reps)
+        rows.append(dict(batch=b, n_cu=r["n_cu"], latency_us=r["latency_us"], p99_us=r["p99_us"],
+                         inferences_per_s=[b * 1e6 / L for L in r["latency_us"]],
+                         eta=[b / (L * L * c) for L, c in zip(r["latency_us"], r["n_cu"])],
+                         knee_slots=r["knee_slots"], deployed_slots=r["deployed_slots"]))
+    m.destroy()
+    return dict(workload="ResNet-50 v1.5, 224x224x3, seed 1020", fractions=FRACTIONS, rows=rows)
 
 
 def config4(ds, torch, args):
@@ -390,6 +479,18 @@ def main():
     t_seq = mix.timesliced(args.steps, args.warmup, shapes)
     seq_value = mix.items_per_step * args.steps / t_seq
     inter = mix.interference(max(5, args.steps // 4), args.warmup, t_mix, args.steps)
+    # the same models concurrently on unmasked streams (each stream may use every CU): the
+    # MPS-default analogue, a second, non-target baseline
+    full_lanes = [(mi, 0, ds.TOTAL_SLOTS) for mi, _, _ in lanes]
+    umix = Mix(ds, torch, models, batch, xs, shapes, full_lanes, reps)
+    t_umix = umix.timed(args.steps, args.warmup)
+    umix.destroy()
+    unmasked_value = mix.items_per_step * args.steps / t_umix
+    # HBM bandwidth each deployed partition (and the whole GPU) can draw: BW(n) of the rooflines
+    bw_lane = [bw_probe(torch, p) for p in mix.parts]
+    pfull = ds.Partition(1.0)
+    bw_full = bw_probe(torch, pfull)
+    pfull.destroy()
 
     # ---- per-kernel timing at the deployed partitions (HIP events on each partition's stream) ----
     per_model = []
@@ -414,8 +515,23 @@ def main():
             slo_optimal=dict(batch=plan["batch"][i], knee_slots=plan["knee_slots"][i],
                              deployed_slots=plan["deployed_slots"][i], latency_us=plan["latency_us"][i],
                              feasible=plan["feasible"][i]),
-            kernels=by_kind))
+            kernels=by_kind,
+            inferences_per_s_in_mix=mix.lane_count[i] * reps[i] * batch[i] * args.steps / t_mix,
+            roofline=model_roofline(ds, recs, n_cu, bw_lane[li],
+                                    next(x["alone_us"] for x in inter if x["lane"] == li))))
     mix.destroy()
+    # mix-level: same-work makespan ratio (one step's jobs run one by one on the whole GPU, from the
+    # timing table, over the measured step), FLOP-weighted work rate, CU-weighted roofline busy time
+    full_us = sum(mix.lane_count[i] * reps[i] * tables[i]["table"][batch[i]][ds.TOTAL_SLOTS] for i in range(n_models))
+    step_us = 1e6 * t_mix / args.steps
+    flops_item = [m.info.flops_per_item for m in models]
+    mix_metrics = dict(
+        same_work_makespan_ratio=full_us / step_us,
+        flop_weighted_tflops=sum(p["inferences_per_s_in_mix"] * f for p, f in zip(per_model, flops_item)) / 1e12,
+        mix_roofline_frac=sum(mix.lane_count[i] * reps[i] * per_model[i]["roofline"]["t_roof_us"] *
+                              per_model[i]["n_cu"] / 256 for i in range(n_models)) / step_us,
+        unmasked_concurrent_inferences_per_s=unmasked_value,
+        hbm_gbs_full_gpu=bw_full)
     avg_ms = conv_ms / max(conv_n, 1)
     achieved = (conv_fl / max(conv_n, 1)) / (avg_ms * 1e-3) / 1e12
     knee_cu = sum(p["n_cu"] * p["kernels"]["mfma"]["ms"] for p in per_model) / max(
@@ -431,8 +547,10 @@ def main():
                            switch_from_slots=10, switch_to_slots=dep[i], **sw))
 
     # ---- the other workloads: VGG-19 + LSTM pair, four-model Poisson mix through the live launcher ----
-    c4 = c5 = None
+    c1 = c2 = c4 = c5 = None
     if not args.headline_only:
+        c1 = config1(ds)
+        c2 = config2(ds, args)
         c4 = config4(ds, torch, args)
         extra = [("vgg19", 1052, [1, 2, 4, 8]), ("lstm2", 1053, [1, 2, 4, 8, 16, 32])]
         m4 = [ds.Model(a, s) for a, s, _ in extra]
@@ -453,7 +571,7 @@ def main():
     b.copy_(a)
     torch.cuda.synchronize()
 
-    cpu = None if args.no_cpu_baseline else cpu_baseline(args.cpu_seconds)
+    cpu = None if args.no_cpu_baseline else cpu_baseline(args.cpu_seconds, sched_in)
 
     out = {
         "metric": METRIC,
@@ -482,6 +600,7 @@ def main():
         "timesliced_inferences_per_s": seq_value,
         "speedup_vs_timesliced": value / seq_value,
         "interference": inter,
+        "mix": mix_metrics,
         "roofline": {
             "bound": "mfma", "kernel": "conv_igemm (all launches of both models at their partitions)",
             "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS,
@@ -495,6 +614,8 @@ def main():
         "schedule_status": "ok" if sched_st == ds.OK else "infeasible",
         "per_model": per_model,
         "reconfiguration": reconf,
+        "config1": c1,
+        "config2": c2,
         "config4": c4,
         "config5": c5,
         "timing_tables": {t["arch"]: {str(b): row for b, row in t["table"].items()} for t in tables},
