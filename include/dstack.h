@@ -153,8 +153,8 @@ dstack_status dstack_infer(dstack_model m, int batch, const void* d_in, void* d_
 /* Per-kernel timing of one forward: fills up to max_layers entries with
  * the elapsed device time (ms, HIP events around each kernel on the
  * partition's stream), the kernel class (0 MFMA conv/GEMM, 1 depthwise,
- * 2 FC, 3 LSTM step, 4 pool/glue, 5 direct RGB stem conv) and its
- * algorithmic FLOPs and bytes.
+ * 2 FC, 3 LSTM step, 4 pool/glue, 5 direct RGB stem conv, 6 fused expand
+ * + depthwise) and its algorithmic FLOPs and bytes.
  * Synchronises the partition. */
 typedef struct {
   int kind;
@@ -450,6 +450,16 @@ dstack_status dstack_op_conv2d(const void* x, int N, int H, int W, int C, const 
  *   E_UNSUPPORTED. */
 dstack_status dstack_op_conv2d_rgb(const void* x, int N, int H, int W, const void* w4, int K, int R, int stride,
                                    int pad, const float* scale, const float* shift, int act, void* y, void* stream);
+/* expand_dw: the expand half of an inverted residual block (Sec. 3's
+ *   MobileNet) in one kernel: e = act_e(se[c] * sum_i x[n,h,w,i] * we[c,i]
+ *   + he[c]) rounded to bf16, then y = act_d(sd[c] * dwconv3x3(e) + hd[c])
+ *   with pad 1 and stride 1 or 2 (zero e outside the image); x [N][H][W][Cin],
+ *   we [Ce][Cin], wd [3][3][Ce] (device layout), y [N][Ho][Wo][Ce] bf16; the
+ *   expanded tensor e is never written to memory.  Cin % 8 == 0 and <= 160,
+ *   Ce % 48 == 0 (else E_UNSUPPORTED); all pointers required. */
+dstack_status dstack_op_expand_dw(const void* x, int N, int H, int W, int Cin, const void* we, int Ce,
+                                  const float* se, const float* he, int act_e, const void* wd, int stride,
+                                  const float* sd, const float* hd, int act_d, void* y, void* stream);
 dstack_status dstack_op_dwconv3x3(const void* x, int N, int H, int W, int C, const void* w, int stride,
                                   const float* scale, const float* shift, int act, void* y, void* stream);
 size_t dstack_fc_workspace_bytes(int B, int I, int O);

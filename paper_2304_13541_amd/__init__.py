@@ -18,7 +18,7 @@ TOTAL_SLOTS = 32
 CUS_PER_SLOT = 8
 MAX_SWEEP, MAX_BATCHES, MAX_MODELS, MAX_JOBS = 32, 8, 16, 512
 ARCHS = ("tinycnn", "resnet50", "mobilenetv2", "vgg19", "lstm2")
-KIND_NAMES = {0: "mfma", 1: "depthwise", 2: "fc", 3: "lstm_step", 4: "glue", 5: "direct_conv"}
+KIND_NAMES = {0: "mfma", 1: "depthwise", 2: "fc", 3: "lstm_step", 4: "glue", 5: "direct_conv", 6: "expand_dw"}
 
 
 class DStackError(RuntimeError):
@@ -143,6 +143,7 @@ _SIGS = {
     "dstack_op_conv2d": ([_vp, _i, _i, _i, _i, _vp, _i, _i, _i, _i, _i, _vp, _vp, _vp, _i, _vp, _i, _vp], _i),
     "dstack_op_conv2d_rgb": ([_vp, _i, _i, _i, _vp, _i, _i, _i, _i, _vp, _vp, _i, _vp, _vp], _i),
     "dstack_op_dwconv3x3": ([_vp, _i, _i, _i, _i, _vp, _i, _vp, _vp, _i, _vp, _vp], _i),
+    "dstack_op_expand_dw": ([_vp, _i, _i, _i, _i, _vp, _i, _vp, _vp, _i, _vp, _i, _vp, _vp, _i, _vp, _vp], _i),
     "dstack_fc_workspace_bytes": ([_i, _i, _i], _sz),
     "dstack_op_fc": ([_vp, _i, _i, _vp, _vp, _i, _i, _vp, _i, _vp, _sz, _vp], _i),
     "dstack_op_maxpool": ([_vp, _i, _i, _i, _i, _i, _i, _i, _vp, _vp], _i),
@@ -469,6 +470,13 @@ def conv2d_rgb(x, w4, K, R, stride, pad, scale, shift, act, y, stream=None):
     assert C == 3
     _check(lib().dstack_op_conv2d_rgb(_ptr(x), N, H, W, _ptr(w4), K, R, stride, pad, _ptr(scale), _ptr(shift), act,
                                       _ptr(y), _stream(stream)))
+
+
+def expand_dw(x, we, Ce, se, he, act_e, wd_rsc, stride, sd, hd, act_d, y, stream=None):
+    """x [N,H,W,Cin] -> act_d(sd * dw3x3(act_e(se * (x @ we^T) + he)) + hd) -> y [N,Ho,Wo,Ce] (bf16)."""
+    N, H, W, Cin = x.shape
+    _check(lib().dstack_op_expand_dw(_ptr(x), N, H, W, Cin, _ptr(we), Ce, _ptr(se), _ptr(he), act_e, _ptr(wd_rsc),
+                                     stride, _ptr(sd), _ptr(hd), act_d, _ptr(y), _stream(stream)))
 
 
 def dwconv3x3(x, w_rsc, stride, scale, shift, act, y, stream=None):

@@ -677,6 +677,16 @@ dstack_status dstack_op_conv2d_rgb(const void* x, int N, int H, int W, const voi
   });
 }
 
+dstack_status dstack_op_expand_dw(const void* x, int N, int H, int W, int Cin, const void* we, int Ce,
+                                  const float* se, const float* he, int act_e, const void* wd, int stride,
+                                  const float* sd, const float* hd, int act_d, void* y, void* stream) {
+  return guarded([&] {
+    return launch_expand_dw(static_cast<const bf16*>(x), N, H, W, Cin, static_cast<const bf16*>(we), Ce, se, he,
+                            act_e, static_cast<const bf16*>(wd), stride, sd, hd, act_d, static_cast<bf16*>(y),
+                            (hipStream_t)stream);
+  });
+}
+
 dstack_status dstack_op_dwconv3x3(const void* x, int N, int H, int W, int C, const void* w, int stride,
                                   const float* scale, const float* shift, int act, void* y, void* stream) {
   return guarded([&] {

@@ -78,6 +78,9 @@ dstack_status launch_fc(const bf16* x, int B, int I, const bf16* w, const float*
 dstack_status launch_maxpool(const bf16* x, int N, int H, int W, int C, int k, int stride, int pad, bf16* y,
                              hipStream_t st);
 dstack_status launch_avgpool(const bf16* x, int N, int H, int W, int C, bf16* y, hipStream_t st);
+dstack_status launch_expand_dw(const bf16* x, int N, int H, int W, int Cin, const bf16* we, int Ce, const float* se,
+                               const float* he, int act_e, const bf16* wd, int stride, const float* sd,
+                               const float* hd, int act_d, bf16* y, hipStream_t st);
 dstack_status launch_conv2d_rgb(const bf16* x, int N, int H, int W, const bf16* w4, int K, int R, int stride, int pad,
                                 const float* scale, const float* shift, int act, bf16* y, hipStream_t st);
 dstack_status launch_lstm_step(const float* gx_t, const bf16* w_hh, const bf16* h_prev, float* c, bf16* h_next,

@@ -120,6 +120,29 @@ class ArchBuilder {
     push(op);
     return Shape{op.out, op.Ho, op.Wo, K};
   }
+  // expand 1x1 conv + BN + ReLU6 and depthwise 3x3 + BN + ReLU6 in one kernel
+  Shape expand_dw(const Shape& s, int we, int Ce, int wd, int stride) {
+    Op op;
+    op.kind = OP_EXPAND_DW;
+    op.in = s.buf;
+    op.H = s.H; op.W = s.W; op.C = s.C; op.K = Ce; op.R = 3; op.S = 3; op.stride = stride; op.pad = 1;
+    op.act = ACT_RELU6;
+    op.act2 = ACT_RELU6;
+    op.Ho = out_dim(s.H, 3, stride, 1);
+    op.Wo = out_dim(s.W, 3, stride, 1);
+    op.C_true = s.C;
+    op.w_off = m.tensors[we].dev_off;
+    op.w2_off = m.tensors[wd].dev_off;
+    op.scale_off = b.f32(Ce);
+    op.shift_off = b.f32(Ce);
+    op.scale2_off = b.f32(Ce);
+    op.shift2_off = b.f32(Ce);
+    op.out = b.alloc((int64_t)op.Ho * op.Wo * Ce);
+    op.w_t = we;
+    op.bn = 1;
+    push(op);
+    return Shape{op.out, op.Ho, op.Wo, Ce};
+  }
   Shape dw(const Shape& s, int wt, int stride) {
     Op op;
     op.kind = OP_DW;
@@ -291,10 +314,15 @@ void build_mbv2(ArchBuilder& A) {
 
   Shape cur = A.conv_rgb(224, 224, stem, 32, 3, 2, 1, true, -1, ACT_RELU6);
   for (const Blk& k : blks) {
-    Shape e = cur;
-    if (k.we >= 0) e = A.conv(cur, k.we, k.hid, 1, 1, 0, true, -1, ACT_RELU6, BUF_NONE, k.cin);
-    Shape d = A.dw(e, k.wd, k.stride);
-    if (e.buf != cur.buf) A.b.release(e.buf);
+    Shape d;
+    if (k.we >= 0 && k.cin % 8 == 0 && k.cin <= 160 && k.hid % 48 == 0) {
+      d = A.expand_dw(cur, k.we, k.hid, k.wd, k.stride);
+    } else {
+      Shape e = cur;
+      if (k.we >= 0) e = A.conv(cur, k.we, k.hid, 1, 1, 0, true, -1, ACT_RELU6, BUF_NONE, k.cin);
+      d = A.dw(e, k.wd, k.stride);
+      if (e.buf != cur.buf) A.b.release(e.buf);
+    }
     bool res = k.stride == 1 && k.cin == k.cout;
     Shape p = A.conv(d, k.wp, k.cout, 1, 1, 0, true, -1, ACT_NONE, res ? cur.buf : BUF_NONE, k.hid);
     A.b.release(d.buf);
@@ -453,6 +481,9 @@ dstack_status upload_weights(Model& m) {
       // BN(y + bias) = sc * y + (bias * sc + beta - mean * sc), beta = mean = 0
       if (op.scale_off >= 0) m.fp32_host[op.scale_off + k] = (float)sc;
       if (op.shift_off >= 0) m.fp32_host[op.shift_off + k] = (float)(bias * sc);
+      // the fused depthwise stage: BN, no bias
+      if (op.scale2_off >= 0) m.fp32_host[op.scale2_off + k] = (float)bn_scale;
+      if (op.shift2_off >= 0) m.fp32_host[op.shift2_off + k] = 0.0f;
     }
   }
   DS_HIP(hipMalloc(&m.d_w, (size_t)m.n_weights * 2));
@@ -656,6 +687,15 @@ dstack_status forward(Model& m, int batch, const void* d_in, void* d_out, Worksp
     double fl = 0, by = 0;
     int gm = 0, gn = 0, gk = 0;
     switch (op.kind) {
+      case OP_EXPAND_DW:
+        s = launch_expand_dw(src, batch, op.H, op.W, op.C, m.d_w + op.w_off, op.K, f32 + op.scale_off,
+                             f32 + op.shift_off, op.act, m.d_w + op.w2_off, op.stride, f32 + op.scale2_off,
+                             f32 + op.shift2_off, op.act2, (bf16*)dst, st);
+        kind = KC_EXPAND_DW;
+        fl = 2.0 * batch * op.H * op.W * (double)op.C * op.K + 2.0 * batch * op.Ho * op.Wo * op.K * 9;
+        by = (double)batch * op.H * op.W * op.C * 2 + (double)op.K * op.C * 2 + 9.0 * op.K * 2 +
+             (double)batch * op.Ho * op.Wo * op.K * 2;
+        break;
       case OP_CONV_RGB:
         s = launch_conv2d_rgb(src, batch, op.H, op.W, m.d_w + op.w_off, op.K, op.R, op.stride, op.pad,
                               f32 + op.scale_off, f32 + op.shift_off, op.act, (bf16*)dst, st);
@@ -719,6 +759,11 @@ void model_cost(const Model& m, int b, double* flops, double* mfma, double* wbyt
         break;
       case OP_CONV_RGB:
         f += conv_flops(op, b);
+        ++n;
+        break;
+      case OP_EXPAND_DW:
+        f += 2.0 * b * op.H * op.W * (double)op.C * op.K + 2.0 * b * op.Ho * op.Wo * op.K * 9;
+        mf += 2.0 * b * op.H * op.W * (double)op.C * op.K;
         ++n;
         break;
       case OP_DW:

@@ -36,8 +36,8 @@ inline int64_t dev_numel(const TensorSpec& t) {
 uint16_t bf16_from_double(double x);
 void generate_tensor(uint64_t seed, int index, const TensorSpec& t, uint16_t* out);
 
-enum OpKind { OP_CONV, OP_DW, OP_MAXPOOL, OP_AVGPOOL, OP_FC, OP_LSTM, OP_CONV_RGB };
-enum KernelClass { KC_MFMA = 0, KC_DW = 1, KC_FC = 2, KC_LSTM = 3, KC_GLUE = 4, KC_DIRECT = 5 };
+enum OpKind { OP_CONV, OP_DW, OP_MAXPOOL, OP_AVGPOOL, OP_FC, OP_LSTM, OP_CONV_RGB, OP_EXPAND_DW };
+enum KernelClass { KC_MFMA = 0, KC_DW = 1, KC_FC = 2, KC_LSTM = 3, KC_GLUE = 4, KC_DIRECT = 5, KC_EXPAND_DW = 6 };
 
 constexpr int BUF_IN = -1;
 constexpr int BUF_OUT = -2;
@@ -52,6 +52,9 @@ struct Op {
   int64_t scale_off = -1;   // fp32 elements into the fp32 arena (-1: none)
   int64_t shift_off = -1;
   int out_f32 = 0;
+  // fused expand + depthwise: the depthwise weights, BN and activation
+  int64_t w2_off = 0, scale2_off = -1, shift2_off = -1;
+  int act2 = 0;
   // LSTM layer
   int T = 0, I = 0, Hd = 0;
   int64_t wih_off = 0, whh_off = 0, bias_off = 0;

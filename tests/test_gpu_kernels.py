@@ -134,6 +134,50 @@ def test_dwconv3x3(env, case):
     assert oracle.rel_err(gu.host(y), ref) <= TOL
 
 
+EXPAND_DW_CASES = [
+    # N, H, W, Cin, Ce, stride, act_e, act_d
+    (2, 14, 14, 64, 384, 1, 2, 2),    # MobileNetV2 stage 4 (one 14 x 14 tile per chunk)
+    (1, 15, 13, 24, 144, 2, 2, 2),    # odd sizes, stride 2
+    (3, 7, 7, 160, 960, 1, 2, 2),     # depth 160 = 5 MFMA steps, 20 channel chunks
+    (1, 9, 31, 16, 96, 2, 1, 0),      # depth 16 < 32 (zero tail), other activations
+    (2, 56, 56, 24, 144, 1, 2, 2),    # several tiles per image with halos
+    (1, 28, 28, 32, 192, 2, 2, 2),
+    (1, 5, 6, 8, 48, 1, 0, 1),        # one partial tile, depth 8
+]
+
+
+@pytest.mark.parametrize("case", EXPAND_DW_CASES)
+def test_expand_dw(env, case):
+    """Fused expand 1x1 + BN + act, bf16 rounding of the expanded tensor,
+    depthwise 3x3 + BN + act, against the oracle's conv2d and dwconv."""
+    ds, gu, inputs, oracle, torch = env
+    N, H, W, Cin, Ce, st, act_e, act_d = case
+    print("expand_dw case", case, flush=True)
+    xb = inputs.normal_bf16(21, (N, H, W, Cin))
+    web = inputs.normal_bf16(22, (Ce, Cin), scale=(2.0 / Cin) ** 0.5)
+    wdb = inputs.normal_bf16(23, (Ce, 3, 3), scale=0.47)
+    rng = np.random.default_rng(24)
+    se, sd = rng.uniform(0.5, 1.5, Ce).astype(np.float32), rng.uniform(0.5, 1.5, Ce).astype(np.float32)
+    he, hd = rng.uniform(-0.2, 0.2, Ce).astype(np.float32), rng.uniform(-0.2, 0.2, Ce).astype(np.float32)
+    Ho, Wo = (H + 2 - 3) // st + 1, (W + 2 - 3) // st + 1
+    y = gu.empty_bf16((N, Ho, Wo, Ce))
+    wd_rsc = np.ascontiguousarray(wdb.reshape(Ce, 9).T.reshape(3, 3, Ce))
+    ds.expand_dw(gu.dev_bf16(xb), gu.dev_bf16(web), Ce, gu.dev_f32(se), gu.dev_f32(he), act_e, gu.dev_bf16(wd_rsc), st,
+                 gu.dev_f32(sd), gu.dev_f32(hd), act_d, y)
+    torch.cuda.synchronize()
+
+    def act(v, a):
+        return np.maximum(v, 0) if a == 1 else (np.clip(v, 0, 6) if a == 2 else v)
+    w1 = oracle.bf16_bits_to_f64(web).reshape(Ce, 1, 1, Cin)
+    e = act(oracle.conv2d(oracle.bf16_bits_to_f64(xb), w1, 1, 0) * se.astype(np.float64) + he.astype(np.float64), act_e)
+    e = oracle.bf16_round(e)  # the expanded tensor is stored as bf16 (in LDS), as between two layers
+    ref = act(oracle.dwconv(e, oracle.bf16_bits_to_f64(wdb), st, 1) * sd.astype(np.float64) + hd.astype(np.float64),
+              act_d)
+    err = oracle.rel_err(gu.host(y), ref)
+    print("rel_err", err)
+    assert err <= TOL
+
+
 @pytest.mark.parametrize("split", [False, True])
 @pytest.mark.parametrize("case", [(1, 64, 10, 0, True), (8, 25088, 40, 1, False), (16, 2048, 1000, 0, True),
                                   (32, 1280, 37, 1, False), (5, 520, 9, 2, True), (8, 4096, 1000, 0, True),
@@ -210,6 +254,10 @@ def test_kernel_argument_errors(env):
     assert e.value.status == ds.E_UNSUPPORTED
     with pytest.raises(ds.DStackError) as e:  # RGB stem with a 5 x 5 filter
         ds.conv2d_rgb(x3, gu.empty_bf16((16, 5, 5, 4)), 16, 5, 1, 2, sc, sc, 0, gu.empty_bf16((1, 8, 8, 16)))
+    assert e.value.status == ds.E_UNSUPPORTED
+    with pytest.raises(ds.DStackError) as e:  # expanded channels not a multiple of 48
+        ds.expand_dw(gu.empty_bf16((1, 4, 4, 16)), gu.empty_bf16((64, 16)), 64, sc, sc, 2, gu.empty_bf16((3, 3, 64)), 1,
+                     sc, sc, 2, gu.empty_bf16((1, 4, 4, 64)))
     assert e.value.status == ds.E_UNSUPPORTED
     xb = gu.empty_bf16((33, 64))
     with pytest.raises(ds.DStackError) as e:  # batch > 32
