@@ -48,7 +48,11 @@ __global__ __launch_bounds__(256) void expand_dw_kernel(ExpandDwArgs a) {
   constexpr int RB = CB / 16;       // MFMA row blocks of expanded channels
   constexpr int PS = CB * 2 + 16;   // LDS bytes per E pixel (padded)
   constexpr int CV = CB / 8;        // 8-channel vectors per pixel
+  constexpr int WROW = DS * 64 + 16;  // LDS bytes per expand-weight row (depth padded to DS*32, + 16 against conflicts)
   __shared__ __attribute__((aligned(16))) unsigned char et[ED_MAX_EM * PS];
+  __shared__ __attribute__((aligned(16))) unsigned char wel[CB * WROW];  // expand weights of the chunk
+  __shared__ __attribute__((aligned(16))) bf16 wdl[9 * CB];              // depthwise weights of the chunk
+  __shared__ __attribute__((aligned(16))) float bnl[4 * CB];             // se, he, sd, hd of the chunk
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, quad = lane >> 4;
   // XCD-aware order: consecutive logical blocks (the channel chunks of one
@@ -68,39 +72,27 @@ __global__ __launch_bounds__(256) void expand_dw_kernel(ExpandDwArgs a) {
   const int ho0 = th * a.TR, wo0 = tw * a.TW;
   const int er0 = ho0 * a.stride - 1, ec0 = wo0 * a.stride - 1;
 
-  // expand weights for this chunk: row c0 + rb*16 + lane%16, depth ds*32 + quad*8 .. +8
-  bf16x8 wa[RB][DS];
-#pragma unroll
-  for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-    for (int ds = 0; ds < DS; ++ds) {
-      const int c = ds * 32 + quad * 8;
-      wa[rb][ds] = c < a.Cin ? *reinterpret_cast<const bf16x8*>(a.we + (long)(c0 + rb * 16 + (lane & 15)) * a.Cin + c)
-                             : bf16x8{};
+  // stage the chunk's weights and BN in LDS (each is read by many lanes):
+  // expand rows c0.. as 16-byte vectors (zero past Cin), depthwise [9][CB], BN
+  {
+    const int vpr = DS * 4;  // 16-byte vectors per padded row
+    for (int v = tid; v < CB * vpr; v += 256) {
+      const int row = v / vpr, col = (v - row * vpr) * 8;
+      const uint4 w = col < a.Cin ? *reinterpret_cast<const uint4*>(a.we + (long)(c0 + row) * a.Cin + col) : uint4{};
+      *reinterpret_cast<uint4*>(wel + row * WROW + col * 2) = w;
     }
-
-  // ---- depthwise 3x3 from the E tile: thread = fixed 8-channel vector cv,
-  // pixels tid / CV, + PT, ...; its 9 weight vectors and BN stay in registers ----
-  constexpr int PT = 256 / CV;  // pixels in flight per pass
-  const int cv = tid % CV;  // threads >= PT * CV take no part in the depthwise pass
-  const int ch = c0 + cv * 8;
-  bf16x8 wv[9];
-#pragma unroll
-  for (int k = 0; k < 9; ++k) wv[k] = *reinterpret_cast<const bf16x8*>(a.wd + k * a.Ce + ch);
-  const f32x4 s0 = *reinterpret_cast<const f32x4*>(a.sd + ch), s1 = *reinterpret_cast<const f32x4*>(a.sd + ch + 4);
-  const f32x4 h0 = *reinterpret_cast<const f32x4*>(a.hd + ch), h1 = *reinterpret_cast<const f32x4*>(a.hd + ch + 4);
-  // BN of the expand for this lane's channels c0 + rb*16 + 4*quad + i
-  f32x4 sce[RB], she[RB];
-#pragma unroll
-  for (int rb = 0; rb < RB; ++rb) {
-    sce[rb] = *reinterpret_cast<const f32x4*>(a.se + c0 + rb * 16 + 4 * quad);
-    she[rb] = *reinterpret_cast<const f32x4*>(a.he + c0 + rb * 16 + 4 * quad);
+    for (int v = tid; v < 9 * CB / 8; v += 256) {
+      const int k = v / (CB / 8), cvv = v - k * (CB / 8);
+      *reinterpret_cast<uint4*>(wdl + k * CB + cvv * 8) = *reinterpret_cast<const uint4*>(a.wd + k * a.Ce + c0 + cvv * 8);
+    }
+    for (int v = tid; v < CB; v += 256) {
+      bnl[v] = a.se[c0 + v];
+      bnl[CB + v] = a.he[c0 + v];
+      bnl[2 * CB + v] = a.sd[c0 + v];
+      bnl[3 * CB + v] = a.hd[c0 + v];
+    }
   }
-
-  const float2 be = act_bounds(a.act_e), bd = act_bounds(a.act_d);
-
-  // ---- expand: E tile pixels in groups of 16; wave w takes groups w, w+4, w+8, w+12
-  // (EM <= 256), all of its input fragments loaded before the first MFMA ----
+  // the E tile's input fragments: wave w takes pixel groups w, w+4, w+8, w+12 (EM <= 256)
   const int groups = (a.EM + 15) / 16;
   bf16x8 b[4][DS];
   bool inside[4];
@@ -120,6 +112,25 @@ __global__ __launch_bounds__(256) void expand_dw_kernel(ExpandDwArgs a) {
       b[u][ds] = inside[u] && c < a.Cin ? *reinterpret_cast<const bf16x8*>(xp + c) : bf16x8{};
     }
   }
+  __syncthreads();  // weights and BN staged
+
+  // expand weights: row rb*16 + lane%16 of the chunk, depth ds*32 + quad*8 .. +8
+  bf16x8 wa[RB][DS];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+    for (int ds = 0; ds < DS; ++ds)
+      wa[rb][ds] = *reinterpret_cast<const bf16x8*>(wel + (rb * 16 + (lane & 15)) * WROW + (ds * 32 + quad * 8) * 2);
+  // expand BN for this lane's channels rb*16 + 4*quad + i
+  f32x4 sce[RB], she[RB];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    sce[rb] = *reinterpret_cast<const f32x4*>(bnl + rb * 16 + 4 * quad);
+    she[rb] = *reinterpret_cast<const f32x4*>(bnl + CB + rb * 16 + 4 * quad);
+  }
+  const float2 be = act_bounds(a.act_e), bd = act_bounds(a.act_d);
+
+  // ---- expand on the matrix cores, BN + activation, bf16 E tile in LDS ----
 #pragma unroll
   for (int u = 0; u < 4; ++u) {
     if (wave + 4 * u >= groups) break;  // wave-uniform
@@ -136,7 +147,19 @@ __global__ __launch_bounds__(256) void expand_dw_kernel(ExpandDwArgs a) {
     }
   }
   __syncthreads();
+  // ---- depthwise 3x3 from the E tile: thread = fixed 8-channel vector cv,
+  // pixels tid / CV, + PT, ...; its 9 weight vectors and BN in registers ----
+  constexpr int PT = 256 / CV;  // pixels in flight per pass
   if (tid >= PT * CV) return;
+  const int cv = tid % CV;
+  const int ch = c0 + cv * 8;
+  bf16x8 wv[9];
+#pragma unroll
+  for (int k = 0; k < 9; ++k) wv[k] = *reinterpret_cast<const bf16x8*>(wdl + k * CB + cv * 8);
+  const f32x4 s0 = *reinterpret_cast<const f32x4*>(bnl + 2 * CB + cv * 8);
+  const f32x4 s1 = *reinterpret_cast<const f32x4*>(bnl + 2 * CB + cv * 8 + 4);
+  const f32x4 h0 = *reinterpret_cast<const f32x4*>(bnl + 3 * CB + cv * 8);
+  const f32x4 h1 = *reinterpret_cast<const f32x4*>(bnl + 3 * CB + cv * 8 + 4);
 
   const int npix = a.TR * a.TW;
   for (int pix = tid / CV; pix < npix; pix += PT) {
