@@ -729,10 +729,10 @@ struct TileCost {
   double step_us;  // one 64-deep step
 };
 static constexpr TileCost kTiles[] = {
-    {128, 128, 0.70}, {128, 64, 0.47}, {64, 128, 0.47}, {64, 64, 0.34}, {32, 128, 0.25}};
+    {128, 128, 0.65}, {128, 64, 0.485}, {64, 128, 0.50}, {64, 64, 0.42}, {32, 128, 0.25}};
 constexpr double kRampUs = 1.4;
 constexpr double kSliceWriteUs = 2.6;   // device-scope slice stores until acknowledged
-constexpr double kSliceReadUs = 0.35;   // per slice, the last block's read-back
+constexpr double kSliceReadUs = 0.75;   // per slice of 8192 fp32 values, the last block's read-back
 
 static double plan_cost(const TileCost& t, int M, int K, int nkt, int splits, int n_cu) {
   const int per = ceil_div(nkt, splits);
@@ -740,17 +740,18 @@ static double plan_cost(const TileCost& t, int M, int K, int nkt, int splits, in
   const long blocks = (long)ceil_div(M, t.bm) * ceil_div(K, t.bn) * s;
   const long rounds = (blocks + 2L * n_cu - 1) / (2L * n_cu);
   double blk = kRampUs + per * t.step_us + 0.6 + 1.5 * (t.bn * t.bm) / 16384.0;
-  if (s > 1) blk += kSliceWriteUs + kSliceReadUs * s;
+  if (s > 1) blk += kSliceWriteUs + kSliceReadUs * s * (t.bn * t.bm) / 8192.0;
   return (double)rounds * blk;
 }
 
 static ConvPlan choose_plan(int M, int K, int Kg, int n_cu, bool can_split, size_t split_bytes) {
-  const int bn = K <= 32 ? 32 : (K <= 64 ? 64 : 128);
+  // channel tiles: 32 for K <= 32, 64 for K <= 64, else 64 or 128
+  const int bn_min = K <= 32 ? 32 : 64, bn_max = K <= 32 ? 32 : (K <= 64 ? 64 : 128);
   const int nkt = ceil_div(Kg, BK);
-  ConvPlan best{bn, 128, 1};
+  ConvPlan best{bn_max, 128, 1};
   double best_t = 1e30;
   for (const TileCost& t : kTiles) {
-    if (t.bn != bn) continue;
+    if (t.bn < bn_min || t.bn > bn_max) continue;
     for (int sp = 1; sp <= 16; sp *= 2) {
       if (sp > 1 && (!can_split || nkt / sp < 2 || (size_t)sp * M * K * sizeof(float) > split_bytes)) break;
       if (sp > 1 && (long)ceil_div(M, t.bm) * ceil_div(K, t.bn) > SPLITK_TILE_COUNTERS) break;
