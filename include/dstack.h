@@ -456,7 +456,7 @@ dstack_status dstack_op_conv2d_rgb(const void* x, int N, int H, int W, const voi
  *   with pad 1 and stride 1 or 2 (zero e outside the image); x [N][H][W][Cin],
  *   we [Ce][Cin], wd [3][3][Ce] (device layout), y [N][Ho][Wo][Ce] bf16; the
  *   expanded tensor e is never written to memory.  Cin % 8 == 0 and <= 160,
- *   Ce % 48 == 0 (else E_UNSUPPORTED); all pointers required. */
+ *   Ce a multiple of 48 or 64 (else E_UNSUPPORTED); all pointers required. */
 dstack_status dstack_op_expand_dw(const void* x, int N, int H, int W, int Cin, const void* we, int Ce,
                                   const float* se, const float* he, int act_e, const void* wd, int stride,
                                   const float* sd, const float* hd, int act_d, void* y, void* stream);

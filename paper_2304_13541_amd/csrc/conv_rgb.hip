@@ -32,6 +32,7 @@ __global__ __launch_bounds__(256) void conv_rgb_kernel(const uint16_t* __restric
   constexpr int KB = K / 16;        // 16-channel MFMA row blocks
   constexpr int ROW = K * 2 + 16;   // staged output row (one pixel), padded against bank conflicts
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  __shared__ __attribute__((aligned(16))) float bnl[2 * K];  // scale, shift
   uint2* patch = reinterpret_cast<uint2*>(smem);                // [rows][W] pixels, 4 bf16 each
   uint2* wl = reinterpret_cast<uint2*>(smem + patch_bytes);     // [K][RR] weight pixels, 4 bf16 each
   unsigned char* ot = smem + patch_bytes;  // after the weights are in registers: the output tile
@@ -51,6 +52,10 @@ __global__ __launch_bounds__(256) void conv_rgb_kernel(const uint16_t* __restric
   {
     const uint2* wsrc = reinterpret_cast<const uint2*>(w4);
     for (int i = tid; i < K * RR; i += 256) wl[i] = wsrc[i];
+    if (tid < K) {
+      bnl[tid] = scale[tid];
+      bnl[K + tid] = shift[tid];
+    }
   }
   if (vec16) {  // W % 8 == 0, 16-byte aligned image: 8 pixels = 3 16-byte loads -> 4 16-byte LDS writes
     const uint4* src = reinterpret_cast<const uint4*>(x + base);
@@ -126,13 +131,19 @@ __global__ __launch_bounds__(256) void conv_rgb_kernel(const uint16_t* __restric
       }
       b[dc] = __builtin_bit_cast(bf16x8, uint4{v[0].x, v[0].y, v[1].x, v[1].y});
     }
+    // depth outer, channel blocks inner: KB independent accumulation chains in flight
+    f32x4 accs[KB];
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) accs[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int dc = 0; dc < DC; ++dc)
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) accs[kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[kb][dc], b[dc], accs[kb], 0, 0, 0);
 #pragma unroll
     for (int kb = 0; kb < KB; ++kb) {
-      f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int dc = 0; dc < DC; ++dc) acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[kb][dc], b[dc], acc, 0, 0, 0);
-      const f32x4 sc = *reinterpret_cast<const f32x4*>(scale + kb * 16 + 4 * quad);
-      const f32x4 sh = *reinterpret_cast<const f32x4*>(shift + kb * 16 + 4 * quad);
+      const f32x4 acc = accs[kb];
+      const f32x4 sc = *reinterpret_cast<const f32x4*>(bnl + kb * 16 + 4 * quad);
+      const f32x4 sh = *reinterpret_cast<const f32x4*>(bnl + K + kb * 16 + 4 * quad);
       bf16x4 o;  // this lane's channels kb*16 + 4*quad.. of its pixel
 #pragma unroll
       for (int i = 0; i < 4; ++i) {

@@ -227,7 +227,7 @@ dstack_status launch_expand_dw(const bf16* x, int N, int H, int W, int Cin, cons
   DS_CHECK(x && we && se && he && wd && sd && hd && y, DSTACK_E_INVALID, "expand_dw: null pointer");
   DS_CHECK(N > 0 && H > 0 && W > 0 && (stride == 1 || stride == 2), DSTACK_E_INVALID, "expand_dw: bad shape");
   DS_CHECK(Cin % 8 == 0 && Cin <= 160, DSTACK_E_UNSUPPORTED, "expand_dw: Cin must be a multiple of 8, at most 160");
-  DS_CHECK(Ce % 48 == 0, DSTACK_E_UNSUPPORTED, "expand_dw: Ce must be a multiple of 48");
+  DS_CHECK(Ce % 48 == 0 || Ce % 64 == 0, DSTACK_E_UNSUPPORTED, "expand_dw: Ce must be a multiple of 48 or 64");
   DS_CHECK(act_e >= 0 && act_e <= 2 && act_d >= 0 && act_d <= 2, DSTACK_E_INVALID, "expand_dw: act must be 0, 1 or 2");
   ExpandDwArgs a;
   a.x = x; a.we = we; a.se = se; a.he = he; a.wd = wd; a.sd = sd; a.hd = hd; a.y = y;
@@ -242,11 +242,18 @@ dstack_status launch_expand_dw(const bf16* x, int N, int H, int W, int Cin, cons
   a.EM = a.ER * a.EC;
   a.tiles_h = ceil_div(a.Ho, a.TR);
   a.tiles_w = ceil_div(a.Wo, a.TW);
-  a.chunks = Ce / 48;
-  const long blocks = (long)N * a.tiles_h * a.tiles_w * a.chunks;
+  // 64-channel chunks (each pixel's chunk of the output one whole 128-byte
+  // line) where they divide Ce and still leave 384 or more blocks; else 48
+  const long tiles = (long)N * a.tiles_h * a.tiles_w;
+  const int cb = (Ce % 64 == 0 && (Ce % 48 != 0 || tiles * (Ce / 64) >= 384)) ? 64 : 48;
+  a.chunks = Ce / cb;
+  const long blocks = tiles * a.chunks;
   DS_CHECK(blocks < (1L << 31), DSTACK_E_UNSUPPORTED, "expand_dw: grid too large");
   a.blocks = (int)blocks;
-  expand_dw_launch_cb<48>(a, ceil_div(Cin, 32), st);
+  if (cb == 64)
+    expand_dw_launch_cb<64>(a, ceil_div(Cin, 32), st);
+  else
+    expand_dw_launch_cb<48>(a, ceil_div(Cin, 32), st);
   DS_HIP(hipGetLastError());
   return DSTACK_OK;
 }

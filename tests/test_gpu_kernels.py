@@ -143,6 +143,7 @@ EXPAND_DW_CASES = [
     (2, 56, 56, 24, 144, 1, 2, 2),    # several tiles per image with halos
     (1, 28, 28, 32, 192, 2, 2, 2),
     (1, 5, 6, 8, 48, 1, 0, 1),        # one partial tile, depth 8
+    (2, 10, 9, 16, 64, 1, 2, 2),      # 64-channel chunks (Ce = 64)
 ]
 
 
@@ -255,9 +256,9 @@ def test_kernel_argument_errors(env):
     with pytest.raises(ds.DStackError) as e:  # RGB stem with a 5 x 5 filter
         ds.conv2d_rgb(x3, gu.empty_bf16((16, 5, 5, 4)), 16, 5, 1, 2, sc, sc, 0, gu.empty_bf16((1, 8, 8, 16)))
     assert e.value.status == ds.E_UNSUPPORTED
-    with pytest.raises(ds.DStackError) as e:  # expanded channels not a multiple of 48
-        ds.expand_dw(gu.empty_bf16((1, 4, 4, 16)), gu.empty_bf16((64, 16)), 64, sc, sc, 2, gu.empty_bf16((3, 3, 64)), 1,
-                     sc, sc, 2, gu.empty_bf16((1, 4, 4, 64)))
+    with pytest.raises(ds.DStackError) as e:  # expanded channels a multiple of neither 48 nor 64
+        ds.expand_dw(gu.empty_bf16((1, 4, 4, 16)), gu.empty_bf16((80, 16)), 80, sc, sc, 2, gu.empty_bf16((3, 3, 80)), 1,
+                     sc, sc, 2, gu.empty_bf16((1, 4, 4, 80)))
     assert e.value.status == ds.E_UNSUPPORTED
     xb = gu.empty_bf16((33, 64))
     with pytest.raises(ds.DStackError) as e:  # batch > 32
