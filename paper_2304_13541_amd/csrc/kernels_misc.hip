@@ -99,9 +99,10 @@ dstack_status launch_dwconv3x3(const bf16* x, int N, int H, int W, int C, const 
   DS_CHECK(N > 0 && H > 0 && W > 0, DSTACK_E_INVALID, "dwconv3x3: bad shape");
   DS_CHECK(scale && shift, DSTACK_E_INVALID, "dwconv3x3: scale and shift are required");
   const int Ho = out_dim(H, 3, stride, 1), Wo = out_dim(W, 3, stride, 1);
-  // outputs per thread along W: 8 on stride-1 rows at least 28 wide, else 4
+  // outputs per thread along W: 8 on stride-1 rows at least 28 wide with more
+  // than 32 channels, else 4
   if (stride == 1) {
-    if (Wo >= 28)
+    if (Wo >= 28 && C > 32)
       dw_launch<1, 8>(x, N, H, W, C, w_rsc, scale, shift, act, y, Ho, Wo, st);
     else
       dw_launch<1, 4>(x, N, H, W, C, w_rsc, scale, shift, act, y, Ho, Wo, st);

@@ -113,10 +113,11 @@ def test_conv2d_rgb(env, case):
 
 
 @pytest.mark.parametrize("case", [(2, 11, 9, 32, 1), (1, 12, 12, 96, 2), (3, 7, 7, 960, 1), (2, 15, 13, 144, 2),
+                                  (1, 30, 29, 32, 1),
                                   (1, 30, 30, 16, 1), (2, 7, 33, 24, 1), (1, 29, 29, 40, 2), (1, 5, 61, 8, 2)])
 def test_dwconv3x3(env, case):
-    """8 output pixels per thread on stride-1 output rows >= 28 wide, else 4;
-    ragged last segments; zero padding on all borders."""
+    """8 output pixels per thread on stride-1 output rows >= 28 wide with more
+    than 32 channels, else 4; ragged last segments; zero padding on all borders."""
     ds, gu, inputs, oracle, torch = env
     N, H, W, C, st = case
     xb = inputs.normal_bf16(5, (N, H, W, C))
