@@ -656,6 +656,20 @@ dstack_status dstack_serve(const dstack_model* models, int n, const void* const*
 
 // ----------------------------------------------------- kernel-level ops ----
 
+// compute units a stream may run on (its CU mask; the whole device for the
+// null stream or when the mask cannot be read)
+static int stream_cu_count(hipStream_t st) {
+  int dev = 0, n = 0;
+  if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    n = 256;
+  if (st == nullptr) return n;
+  uint32_t words[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  if (hipExtStreamGetCUMask(st, 8, words) != hipSuccess) return n;
+  int bits = 0;
+  for (uint32_t w : words) bits += __builtin_popcount(w);
+  return bits > 0 ? std::min(bits, n) : n;
+}
+
 dstack_status dstack_op_conv2d(const void* x, int N, int H, int W, int C, const void* w, int K, int R, int S,
                                int stride, int pad, const float* scale, const float* shift, const void* res, int act,
                                void* y, int out_fp32, void* stream) {
@@ -683,7 +697,7 @@ dstack_status dstack_op_expand_dw(const void* x, int N, int H, int W, int Cin, c
   return guarded([&] {
     return launch_expand_dw(static_cast<const bf16*>(x), N, H, W, Cin, static_cast<const bf16*>(we), Ce, se, he,
                             act_e, static_cast<const bf16*>(wd), stride, sd, hd, act_d, static_cast<bf16*>(y),
-                            (hipStream_t)stream);
+                            stream_cu_count((hipStream_t)stream), (hipStream_t)stream);
   });
 }
 

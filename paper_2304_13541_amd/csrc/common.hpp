@@ -11,6 +11,25 @@
 
 namespace dstack {
 
+// Division by a runtime constant d >= 1 for 0 <= n < 2^31 with a multiply-high:
+// l = ceil(log2 d), m = floor(2^32 (2^l - d) / d) + 1, n / d = (mulhi(m, n) + n) >> l
+// (Granlund & Montgomery, "Division by invariant integers using
+// multiplication", PLDI 1994).
+struct FastDiv {
+  unsigned m;
+  int l;
+  int d;
+  static FastDiv make(int d) {
+    FastDiv f;
+    f.d = d;
+    f.l = 0;
+    while ((1LL << f.l) < d) ++f.l;
+    f.m = (unsigned)((((1ULL << 32) * ((1ULL << f.l) - (unsigned long long)d)) / (unsigned long long)d) + 1);
+    return f;
+  }
+  __device__ __forceinline__ int div(int n) const { return (int)((__umulhi(m, (unsigned)n) + (unsigned)n) >> l); }
+};
+
 typedef __bf16 bf16;
 typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
 typedef __attribute__((__vector_size__(4 * sizeof(__bf16)))) __bf16 bf16x4;
@@ -80,7 +99,7 @@ dstack_status launch_maxpool(const bf16* x, int N, int H, int W, int C, int k, i
 dstack_status launch_avgpool(const bf16* x, int N, int H, int W, int C, bf16* y, hipStream_t st);
 dstack_status launch_expand_dw(const bf16* x, int N, int H, int W, int Cin, const bf16* we, int Ce, const float* se,
                                const float* he, int act_e, const bf16* wd, int stride, const float* sd,
-                               const float* hd, int act_d, bf16* y, hipStream_t st);
+                               const float* hd, int act_d, bf16* y, int n_cu, hipStream_t st);
 dstack_status launch_conv2d_rgb(const bf16* x, int N, int H, int W, const bf16* w4, int K, int R, int stride, int pad,
                                 const float* scale, const float* shift, int act, bf16* y, hipStream_t st);
 dstack_status launch_lstm_step(const float* gx_t, const bf16* w_hh, const bf16* h_prev, float* c, bf16* h_next,

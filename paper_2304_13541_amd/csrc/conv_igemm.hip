@@ -41,25 +41,6 @@
 
 namespace dstack {
 
-// Division by a runtime constant d >= 1 for 0 <= n < 2^31 with a multiply-high:
-// l = ceil(log2 d), m = floor(2^32 (2^l - d) / d) + 1, n / d = (mulhi(m, n) + n) >> l
-// (Granlund & Montgomery, "Division by invariant integers using
-// multiplication", PLDI 1994).
-struct FastDiv {
-  unsigned m;
-  int l;
-  int d;
-  static FastDiv make(int d) {
-    FastDiv f;
-    f.d = d;
-    f.l = 0;
-    while ((1LL << f.l) < d) ++f.l;
-    f.m = (unsigned)((((1ULL << 32) * ((1ULL << f.l) - (unsigned long long)d)) / (unsigned long long)d) + 1);
-    return f;
-  }
-  __device__ __forceinline__ int div(int n) const { return (int)((__umulhi(m, (unsigned)n) + (unsigned)n) >> l); }
-};
-
 struct ConvArgs {
   const bf16* x;
   const bf16* w;

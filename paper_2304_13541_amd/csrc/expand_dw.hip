@@ -6,15 +6,27 @@
 // the tile plus its one-pixel halo on the matrix cores into LDS, then runs
 // the depthwise filter from LDS and writes only the depthwise output D.
 //
-// Expand: GEMM rows = the CB expanded channels (weights [Ce][Cin], A
-// operand, in registers for the block), columns = the E tile's pixels (B
-// operand, 8 consecutive input channels of one pixel per lane, 16-byte loads
-// from the NHWC input), depth = Cin in steps of 32 (zero beyond Cin).  The
-// result (4 consecutive channels of one pixel per lane) goes through the BN
-// scale/shift and ReLU6 to bf16 in LDS, [pixel][channel] with 16 bytes of
-// padding per pixel; E pixels outside the image are stored as zeros, which
-// is the depthwise filter's zero padding.  Depthwise: one thread per (output
-// pixel, 8 channels), 9 16-byte LDS reads, fp32 accumulate.
+// E tile: ER rows x ECP columns (the halo'd width EC rounded up to even),
+// pixels numbered row-major.  In LDS it is stored as column pairs: word
+// (pair, c) holds channel c of the even and the odd column of one pair as
+// two bf16, CB + 8 words per pair (the 8 spread the four quads of a wave
+// over distinct banks).
+//
+// Expand: GEMM rows = 16 E pixels (A operand, 8 consecutive input channels
+// of one pixel per lane, 16-byte loads from the NHWC input), columns = 16
+// expanded channels (B operand, weights [Ce][Cin] staged in LDS), depth =
+// Cin in steps of 32 (zero beyond Cin).  A lane's result is one channel of
+// 4 consecutive pixels, i.e. two column pairs, which go through BN and the
+// activation to two LDS words; E pixels outside the image are stored as
+// zeros, which is the depthwise filter's zero padding.
+//
+// Depthwise: a thread takes 4 channels of one output pixel (stride 2) or of
+// two horizontally adjacent ones (stride 1).  Per filter row it reads the
+// column pairs under the window (16 bytes each) and accumulates with
+// bf16 dot products of two taps: at stride 1 the even output takes taps
+// (0,1) from the first pair and tap 2 from the next pair's even column, the
+// odd output tap 0 from the first pair's odd column and taps (1,2) from the
+// next pair, the unused half weighted by zero; fp32 accumulate.
 #include <hip/hip_ext.h>
 
 #include "common.hpp"
@@ -32,8 +44,9 @@ struct ExpandDwArgs {
   bf16* y;           // [N][Ho][Wo][Ce]
   int N, H, W, Cin, Ce, Ho, Wo, stride;
   int act_e, act_d;
-  int TR, TW, ER, EC, EM;  // output tile, E tile rows / cols / pixels (EM <= 256)
+  int TR, TW, ER, EC, ECP, EM;  // output tile; E tile rows, cols, cols rounded up to even, pixels ER*ECP (<= 256)
   int tiles_h, tiles_w, chunks, blocks;
+  FastDiv div_chunks, div_tw, div_th, div_ecp, div_twi;  // by chunks, tiles_w, tiles_h, ECP, work items per tile row
 };
 
 constexpr int ED_MAX_EM = 256;
@@ -43,13 +56,26 @@ __device__ __forceinline__ float2 act_bounds(int act) {
   return float2{act == ACT_NONE ? -INFINITY : 0.0f, act == ACT_RELU6 ? 6.0f : INFINITY};
 }
 
-template <int CB, int DS>
+typedef __attribute__((__vector_size__(2 * sizeof(__bf16)))) __bf16 bf16x2;
+
+__device__ __forceinline__ float dot2(unsigned e, bf16x2 w, float acc) {
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, e), w, acc, false);
+}
+
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
+// two floats to round-to-nearest-even bf16 in one packed conversion
+__device__ __forceinline__ unsigned pack_bf16x2(float lo, float hi) {
+  return __builtin_bit_cast(unsigned, __builtin_convertvector((f32x2{lo, hi}), bf16x2));
+}
+
+template <int CB, int DS, int S>
 __global__ __launch_bounds__(256) void expand_dw_kernel(ExpandDwArgs a) {
-  constexpr int RB = CB / 16;       // MFMA row blocks of expanded channels
-  constexpr int PS = CB * 2 + 16;   // LDS bytes per E pixel (padded)
-  constexpr int CV = CB / 8;        // 8-channel vectors per pixel
+  constexpr int RB = CB / 16;       // MFMA column blocks of expanded channels
+  constexpr int PW = CB + 8;        // LDS words per E column pair
+  constexpr int CG = CB / 4;        // 4-channel groups of the depthwise phase
   constexpr int WROW = DS * 64 + 16;  // LDS bytes per expand-weight row (depth padded to DS*32, + 16 against conflicts)
-  __shared__ __attribute__((aligned(16))) unsigned char et[ED_MAX_EM * PS];
+  __shared__ __attribute__((aligned(16))) unsigned et[ED_MAX_EM / 2 * PW];
   __shared__ __attribute__((aligned(16))) unsigned char wel[CB * WROW];  // expand weights of the chunk
   __shared__ __attribute__((aligned(16))) bf16 wdl[9 * CB];              // depthwise weights of the chunk
   __shared__ __attribute__((aligned(16))) float bnl[4 * CB];             // se, he, sd, hd of the chunk
@@ -62,140 +88,209 @@ __global__ __launch_bounds__(256) void expand_dw_kernel(ExpandDwArgs a) {
     const int L = blockIdx.x, q = a.blocks >> 3, r = a.blocks & 7, xcd = L & 7, i = L >> 3;
     blk = xcd * q + min(xcd, r) + i;
   }
-  const int chunk = blk % a.chunks;
-  int t = blk / a.chunks;
-  const int tw = t % a.tiles_w;
-  t /= a.tiles_w;
-  const int th = t % a.tiles_h;
-  const int n = t / a.tiles_h;
+  int t = a.div_chunks.div(blk);
+  const int chunk = blk - t * a.chunks;
+  int t2 = a.div_tw.div(t);
+  const int tw = t - t2 * a.tiles_w;
+  const int n = a.div_th.div(t2);
+  const int th = t2 - n * a.tiles_h;
   const int c0 = chunk * CB;
   const int ho0 = th * a.TR, wo0 = tw * a.TW;
-  const int er0 = ho0 * a.stride - 1, ec0 = wo0 * a.stride - 1;
+  const int er0 = ho0 * S - 1, ec0 = wo0 * S - 1;
 
-  // stage the chunk's weights and BN in LDS (each is read by many lanes):
-  // expand rows c0.. as 16-byte vectors (zero past Cin), depthwise [9][CB], BN
-  {
-    const int vpr = DS * 4;  // 16-byte vectors per padded row
-    for (int v = tid; v < CB * vpr; v += 256) {
-      const int row = v / vpr, col = (v - row * vpr) * 8;
-      const uint4 w = col < a.Cin ? *reinterpret_cast<const uint4*>(a.we + (long)(c0 + row) * a.Cin + col) : uint4{};
-      *reinterpret_cast<uint4*>(wel + row * WROW + col * 2) = w;
-    }
-    for (int v = tid; v < 9 * CB / 8; v += 256) {
-      const int k = v / (CB / 8), cvv = v - k * (CB / 8);
-      *reinterpret_cast<uint4*>(wdl + k * CB + cvv * 8) = *reinterpret_cast<const uint4*>(a.wd + k * a.Ce + c0 + cvv * 8);
-    }
-    for (int v = tid; v < CB; v += 256) {
-      bnl[v] = a.se[c0 + v];
-      bnl[CB + v] = a.he[c0 + v];
-      bnl[2 * CB + v] = a.sd[c0 + v];
-      bnl[3 * CB + v] = a.hd[c0 + v];
-    }
+  // Every global load of the prologue is issued before the first LDS store,
+  // so the block waits for one memory round trip rather than one per array:
+  // the chunk's expand rows c0.. as 16-byte vectors (zero past Cin), its
+  // depthwise weights [9][CB] and its four BN vectors (each read by many
+  // lanes, so staged in LDS), then the E tile's input fragments (registers).
+  // Element offsets are 32-bit (the host bounds every tensor below 2^31).
+  constexpr int VPR = DS * 4;                 // 16-byte vectors per padded expand row
+  constexpr int WV = (CB * VPR + 255) / 256;  // expand-weight vectors per thread
+  uint4 wst[WV];
+#pragma unroll
+  for (int i = 0; i < WV; ++i) {
+    const int v = tid + i * 256, row = v / VPR, col = (v - row * VPR) * 8;
+    wst[i] = v < CB * VPR && col < a.Cin ? *reinterpret_cast<const uint4*>(a.we + ((c0 + row) * a.Cin + col))
+                                          : uint4{};
   }
+  static_assert(9 * CB / 8 <= 256 && 4 * CB <= 256, "one depthwise vector and one BN value per thread");
+  const int dk = tid / (CB / 8), dcv = tid - dk * (CB / 8);
+  const uint4 dst = tid < 9 * CB / 8 ? *reinterpret_cast<const uint4*>(a.wd + (dk * a.Ce + c0 + dcv * 8)) : uint4{};
+  const int bk = tid / CB, bc = tid - bk * CB;
+  const float* bsrc = bk == 0 ? a.se : bk == 1 ? a.he : bk == 2 ? a.sd : a.hd;
+  const float bst = tid < 4 * CB ? bsrc[c0 + bc] : 0.0f;
   // the E tile's input fragments: wave w takes pixel groups w, w+4, w+8, w+12 (EM <= 256)
   const int groups = (a.EM + 15) / 16;
   bf16x8 b[4][DS];
   bool inside[4];
-  int pxs[4];
+  const int xn = n * a.H;
 #pragma unroll
   for (int u = 0; u < 4; ++u) {
     const int g = wave + 4 * u;
     const int px = g * 16 + (lane & 15);
-    const int er = px / a.EC, ec = px - (px / a.EC) * a.EC;
+    const int er = a.div_ecp.div(px), ec = px - er * a.ECP;
     const int hi = er0 + er, wi = ec0 + ec;
-    pxs[u] = px;
     inside[u] = g < groups && px < a.EM && (unsigned)hi < (unsigned)a.H && (unsigned)wi < (unsigned)a.W;
-    const bf16* xp = a.x + (((long)n * a.H + (inside[u] ? hi : 0)) * a.W + (inside[u] ? wi : 0)) * a.Cin;
+    const bf16* xp = a.x + (((xn + (inside[u] ? hi : 0)) * a.W + (inside[u] ? wi : 0)) * a.Cin + quad * 8);
 #pragma unroll
-    for (int ds = 0; ds < DS; ++ds) {
-      const int c = ds * 32 + quad * 8;
-      b[u][ds] = inside[u] && c < a.Cin ? *reinterpret_cast<const bf16x8*>(xp + c) : bf16x8{};
-    }
+    for (int ds = 0; ds < DS; ++ds)
+      b[u][ds] = inside[u] && ds * 32 + quad * 8 < a.Cin ? *reinterpret_cast<const bf16x8*>(xp + ds * 32) : bf16x8{};
   }
+#pragma unroll
+  for (int i = 0; i < WV; ++i) {
+    const int v = tid + i * 256, row = v / VPR, col = (v - row * VPR) * 8;
+    if (v < CB * VPR) *reinterpret_cast<uint4*>(wel + row * WROW + col * 2) = wst[i];
+  }
+  if (tid < 9 * CB / 8) *reinterpret_cast<uint4*>(wdl + dk * CB + dcv * 8) = dst;
+  if (tid < 4 * CB) bnl[tid] = bst;
   __syncthreads();  // weights and BN staged
 
-  // expand weights: row rb*16 + lane%16 of the chunk, depth ds*32 + quad*8 .. +8
+  // expand weights: channel rb*16 + lane%16 of the chunk, depth ds*32 + quad*8 .. +8
   bf16x8 wa[RB][DS];
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
     for (int ds = 0; ds < DS; ++ds)
       wa[rb][ds] = *reinterpret_cast<const bf16x8*>(wel + (rb * 16 + (lane & 15)) * WROW + (ds * 32 + quad * 8) * 2);
-  // expand BN for this lane's channels rb*16 + 4*quad + i
-  f32x4 sce[RB], she[RB];
+  float sce[RB], she[RB];
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
-    sce[rb] = *reinterpret_cast<const f32x4*>(bnl + rb * 16 + 4 * quad);
-    she[rb] = *reinterpret_cast<const f32x4*>(bnl + CB + rb * 16 + 4 * quad);
+    sce[rb] = bnl[rb * 16 + (lane & 15)];
+    she[rb] = bnl[CB + rb * 16 + (lane & 15)];
   }
   const float2 be = act_bounds(a.act_e), bd = act_bounds(a.act_d);
 
-  // ---- expand on the matrix cores, BN + activation, bf16 E tile in LDS ----
+  // ---- expand on the matrix cores, BN + activation, bf16 column pairs in LDS ----
 #pragma unroll
   for (int u = 0; u < 4; ++u) {
-    if (wave + 4 * u >= groups) break;  // wave-uniform
+    const int g = wave + 4 * u;
+    if (g >= groups) break;  // wave-uniform
+    f32x4 acc[RB];
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
-      f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+      acc[rb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int ds = 0; ds < DS; ++ds) acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wa[rb][ds], b[u][ds], acc, 0, 0, 0);
-      bf16x4 e;
+      for (int ds = 0; ds < DS; ++ds) acc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(b[u][ds], wa[rb][ds], acc[rb], 0, 0, 0);
+    }
+    unsigned* dstp = et + (g * 8 + 2 * quad) * PW + (lane & 15);
+    // lane p of the first quad loaded pixel g*16 + p; this lane's results are
+    // pixels g*16 + 4*quad + i
+    const unsigned long long inmask = __ballot(inside[u]);
+    if (inmask == ~0ull) {  // the whole group lies in the image (wave-uniform)
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-        e[i] = (bf16)(inside[u] ? fminf(fmaxf(acc[i] * sce[rb][i] + she[rb][i], be.x), be.y) : 0.0f);
-      if (pxs[u] < a.EM) *reinterpret_cast<bf16x4*>(et + pxs[u] * PS + (rb * 16 + 4 * quad) * 2) = e;
+      for (int rb = 0; rb < RB; ++rb) {
+        float v[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) v[i] = __builtin_amdgcn_fmed3f(acc[rb][i] * sce[rb] + she[rb], be.x, be.y);
+        dstp[rb * 16] = pack_bf16x2(v[0], v[1]);
+        dstp[rb * 16 + PW] = pack_bf16x2(v[2], v[3]);
+      }
+    } else {  // E outside the image is the depthwise filter's zero padding
+      const unsigned live = (unsigned)(inmask >> (4 * quad)) & 15u;
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) {
+        float v[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float e = __builtin_amdgcn_fmed3f(acc[rb][i] * sce[rb] + she[rb], be.x, be.y);
+          v[i] = (live >> i) & 1u ? e : 0.0f;
+        }
+        dstp[rb * 16] = pack_bf16x2(v[0], v[1]);
+        dstp[rb * 16 + PW] = pack_bf16x2(v[2], v[3]);
+      }
     }
   }
   __syncthreads();
-  // ---- depthwise 3x3 from the E tile: thread = fixed 8-channel vector cv,
-  // pixels tid / CV, + PT, ...; its 9 weight vectors and BN in registers ----
-  constexpr int PT = 256 / CV;  // pixels in flight per pass
-  if (tid >= PT * CV) return;
-  const int cv = tid % CV;
-  const int ch = c0 + cv * 8;
-  bf16x8 wv[9];
-#pragma unroll
-  for (int k = 0; k < 9; ++k) wv[k] = *reinterpret_cast<const bf16x8*>(wdl + k * CB + cv * 8);
-  const f32x4 s0 = *reinterpret_cast<const f32x4*>(bnl + 2 * CB + cv * 8);
-  const f32x4 s1 = *reinterpret_cast<const f32x4*>(bnl + 2 * CB + cv * 8 + 4);
-  const f32x4 h0 = *reinterpret_cast<const f32x4*>(bnl + 3 * CB + cv * 8);
-  const f32x4 h1 = *reinterpret_cast<const f32x4*>(bnl + 3 * CB + cv * 8 + 4);
 
-  const int npix = a.TR * a.TW;
-  for (int pix = tid / CV; pix < npix; pix += PT) {
-    const int r = pix / a.TW, c = pix - (pix / a.TW) * a.TW;
-    const int ho = ho0 + r, wo = wo0 + c;
-    if (ho >= a.Ho || wo >= a.Wo) continue;
-    float acc[8];
+  // ---- depthwise 3x3 from the E tile: thread = fixed 4-channel group cg,
+  // work items tid / CG, + PT, ...; its tap-pair weights and BN in registers ----
+  constexpr int PT = 256 / CG;  // work items in flight per pass
+  if (tid >= PT * CG) return;
+  const int cg = tid % CG;
+  bf16x2 w01[3][4], w2z[3][4];  // (tap 0, tap 1) and (tap 2, 0) of each filter row
+  bf16x2 wz0[3][4], w12[3][4];  // (0, tap 0) and (tap 1, tap 2), stride 1 only
+  const bf16 zero = (bf16)0.0f;
 #pragma unroll
-    for (int j = 0; j < 8; ++j) acc[j] = 0.f;
-#pragma unroll
-    for (int kr = 0; kr < 3; ++kr)
-#pragma unroll
-      for (int kc = 0; kc < 3; ++kc) {
-        const int e = (r * a.stride + kr) * a.EC + c * a.stride + kc;
-        const bf16x8 v = *reinterpret_cast<const bf16x8*>(et + e * PS + cv * 16);
-#pragma unroll
-        for (int j = 0; j < 8; ++j) acc[j] += (float)v[j] * (float)wv[kr * 3 + kc][j];
-      }
-    bf16x8 o;
+  for (int kr = 0; kr < 3; ++kr) {
+    const bf16x4 t0 = *reinterpret_cast<const bf16x4*>(wdl + (kr * 3 + 0) * CB + cg * 4);
+    const bf16x4 t1 = *reinterpret_cast<const bf16x4*>(wdl + (kr * 3 + 1) * CB + cg * 4);
+    const bf16x4 t2 = *reinterpret_cast<const bf16x4*>(wdl + (kr * 3 + 2) * CB + cg * 4);
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      o[j] = (bf16)fminf(fmaxf(acc[j] * s0[j] + h0[j], bd.x), bd.y);
-      o[j + 4] = (bf16)fminf(fmaxf(acc[j + 4] * s1[j] + h1[j], bd.x), bd.y);
+      w01[kr][j] = bf16x2{t0[j], t1[j]};
+      w2z[kr][j] = bf16x2{t2[j], zero};
+      wz0[kr][j] = bf16x2{zero, t0[j]};
+      w12[kr][j] = bf16x2{t1[j], t2[j]};
     }
-    *reinterpret_cast<bf16x8*>(a.y + (((long)n * a.Ho + ho) * a.Wo + wo) * a.Ce + ch) = o;
+  }
+  const f32x4 sd = *reinterpret_cast<const f32x4*>(bnl + 2 * CB + cg * 4);
+  const f32x4 hd = *reinterpret_cast<const f32x4*>(bnl + 3 * CB + cg * 4);
+  bf16* const ybase = a.y + (c0 + cg * 4);
+  auto store = [&](const float* acc, int ho, int wo) {
+    float o[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) o[j] = __builtin_amdgcn_fmed3f(acc[j] * sd[j] + hd[j], bd.x, bd.y);
+    *reinterpret_cast<uint2*>(ybase + ((n * a.Ho + ho) * a.Wo + wo) * a.Ce) =
+        uint2{pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3])};
+  };
+  const int ECP2 = a.ECP / 2;  // column pairs per E row
+  // work item (row r, column c of the tile; output column pairs at stride
+  // 1), stepped by PT items per pass without dividing
+  const int TWI = S == 1 ? (a.TW + 1) >> 1 : a.TW;
+  const int nitems = a.TR * TWI;
+  int it = tid / CG;
+  int r = a.div_twi.div(it), c = it - r * TWI;
+  const int dr = a.div_twi.div(PT), dc = PT - dr * TWI;
+  for (; it < nitems; it += PT) {
+    const int ho = ho0 + r, wo = wo0 + (S == 1 ? 2 * c : c);
+    if (ho < a.Ho && wo < a.Wo) {
+      const unsigned* q = et + ((S * r) * ECP2 + c) * PW + cg * 4;
+      if (S == 1) {
+        float ae[4] = {0.f, 0.f, 0.f, 0.f}, ao[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kr = 0; kr < 3; ++kr) {
+          const uint4 p0 = *reinterpret_cast<const uint4*>(q + kr * ECP2 * PW);
+          const uint4 p1 = *reinterpret_cast<const uint4*>(q + kr * ECP2 * PW + PW);
+          const unsigned e0[4] = {p0.x, p0.y, p0.z, p0.w}, e1[4] = {p1.x, p1.y, p1.z, p1.w};
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            ae[j] = dot2(e1[j], w2z[kr][j], dot2(e0[j], w01[kr][j], ae[j]));
+            ao[j] = dot2(e1[j], w12[kr][j], dot2(e0[j], wz0[kr][j], ao[j]));
+          }
+        }
+        store(ae, ho, wo);
+        if (2 * c + 1 < a.TW && wo + 1 < a.Wo) store(ao, ho, wo + 1);
+      } else {
+        float acc[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kr = 0; kr < 3; ++kr) {
+          const uint4 p0 = *reinterpret_cast<const uint4*>(q + kr * ECP2 * PW);
+          const uint4 p1 = *reinterpret_cast<const uint4*>(q + kr * ECP2 * PW + PW);
+          const unsigned e0[4] = {p0.x, p0.y, p0.z, p0.w}, e1[4] = {p1.x, p1.y, p1.z, p1.w};
+#pragma unroll
+          for (int j = 0; j < 4; ++j) acc[j] = dot2(e1[j], w2z[kr][j], dot2(e0[j], w01[kr][j], acc[j]));
+        }
+        store(acc, ho, wo);
+      }
+    }
+    r += dr;
+    c += dc;
+    if (c >= TWI) {
+      c -= TWI;
+      ++r;
+    }
   }
 }
 
-// Output tile TR x TW with the most outputs whose E tile (plus halo) has at
-// most ED_MAX_EM pixels; ties to the wider tile.
+// Output tile TR x TW with the most outputs whose E tile (plus halo, width
+// rounded up to even) has at most ED_MAX_EM pixels; ties to the wider tile.
 static void expand_dw_tile(int Ho, int Wo, int stride, int* TR, int* TW) {
   int best = 0;
   *TR = *TW = 1;
   for (int tr = 1; tr <= Ho; ++tr)
     for (int tw = 1; tw <= Wo; ++tw) {
-      const int em = ((tr - 1) * stride + 3) * ((tw - 1) * stride + 3);
+      const int ec = (tw - 1) * stride + 3;
+      const int em = ((tr - 1) * stride + 3) * (ec + (ec & 1));
       if (em > ED_MAX_EM) break;
       // count the outputs of all tiles, penalising the partial ones at the edges
       const long tiles = (long)((Ho + tr - 1) / tr) * ((Wo + tw - 1) / tw);
@@ -209,21 +304,22 @@ static void expand_dw_tile(int Ho, int Wo, int stride, int* TR, int* TW) {
     }
 }
 
-template <int CB>
+template <int CB, int S>
 static void expand_dw_launch_cb(const ExpandDwArgs& a, int ds, hipStream_t st) {
   const dim3 grid((unsigned)a.blocks);
   switch (ds) {
-    case 1: hipLaunchKernelGGL((expand_dw_kernel<CB, 1>), grid, dim3(256), 0, st, a); break;
-    case 2: hipLaunchKernelGGL((expand_dw_kernel<CB, 2>), grid, dim3(256), 0, st, a); break;
-    case 3: hipLaunchKernelGGL((expand_dw_kernel<CB, 3>), grid, dim3(256), 0, st, a); break;
-    case 4: hipLaunchKernelGGL((expand_dw_kernel<CB, 4>), grid, dim3(256), 0, st, a); break;
-    default: hipLaunchKernelGGL((expand_dw_kernel<CB, 5>), grid, dim3(256), 0, st, a); break;
+    case 1: hipLaunchKernelGGL((expand_dw_kernel<CB, 1, S>), grid, dim3(256), 0, st, a); break;
+    case 2: hipLaunchKernelGGL((expand_dw_kernel<CB, 2, S>), grid, dim3(256), 0, st, a); break;
+    case 3: hipLaunchKernelGGL((expand_dw_kernel<CB, 3, S>), grid, dim3(256), 0, st, a); break;
+    case 4: hipLaunchKernelGGL((expand_dw_kernel<CB, 4, S>), grid, dim3(256), 0, st, a); break;
+    default: hipLaunchKernelGGL((expand_dw_kernel<CB, 5, S>), grid, dim3(256), 0, st, a); break;
   }
 }
 
 dstack_status launch_expand_dw(const bf16* x, int N, int H, int W, int Cin, const bf16* we, int Ce, const float* se,
                                const float* he, int act_e, const bf16* wd, int stride, const float* sd,
-                               const float* hd, int act_d, bf16* y, hipStream_t st) {
+                               const float* hd, int act_d, bf16* y, int n_cu, hipStream_t st) {
+  (void)n_cu;
   DS_CHECK(x && we && se && he && wd && sd && hd && y, DSTACK_E_INVALID, "expand_dw: null pointer");
   DS_CHECK(N > 0 && H > 0 && W > 0 && (stride == 1 || stride == 2), DSTACK_E_INVALID, "expand_dw: bad shape");
   DS_CHECK(Cin % 8 == 0 && Cin <= 160, DSTACK_E_UNSUPPORTED, "expand_dw: Cin must be a multiple of 8, at most 160");
@@ -239,7 +335,8 @@ dstack_status launch_expand_dw(const bf16* x, int N, int H, int W, int Cin, cons
   expand_dw_tile(a.Ho, a.Wo, stride, &a.TR, &a.TW);
   a.ER = (a.TR - 1) * stride + 3;
   a.EC = (a.TW - 1) * stride + 3;
-  a.EM = a.ER * a.EC;
+  a.ECP = a.EC + (a.EC & 1);
+  a.EM = a.ER * a.ECP;
   a.tiles_h = ceil_div(a.Ho, a.TR);
   a.tiles_w = ceil_div(a.Wo, a.TW);
   // 64-channel chunks (each pixel's chunk of the output one whole 128-byte
@@ -250,12 +347,19 @@ dstack_status launch_expand_dw(const bf16* x, int N, int H, int W, int Cin, cons
   const long blocks = tiles * a.chunks;
   DS_CHECK(blocks < (1L << 31), DSTACK_E_UNSUPPORTED, "expand_dw: grid too large");
   a.blocks = (int)blocks;
+  a.div_chunks = FastDiv::make(a.chunks);
+  a.div_tw = FastDiv::make(a.tiles_w);
+  a.div_th = FastDiv::make(a.tiles_h);
+  a.div_ecp = FastDiv::make(a.ECP);
+  a.div_twi = FastDiv::make(stride == 1 ? (a.TW + 1) / 2 : a.TW);
+  const int ds = ceil_div(Cin, 32);
   if (cb == 64)
-    expand_dw_launch_cb<64>(a, ceil_div(Cin, 32), st);
+    stride == 1 ? expand_dw_launch_cb<64, 1>(a, ds, st) : expand_dw_launch_cb<64, 2>(a, ds, st);
   else
-    expand_dw_launch_cb<48>(a, ceil_div(Cin, 32), st);
+    stride == 1 ? expand_dw_launch_cb<48, 1>(a, ds, st) : expand_dw_launch_cb<48, 2>(a, ds, st);
   DS_HIP(hipGetLastError());
   return DSTACK_OK;
 }
 
 }  // namespace dstack
+

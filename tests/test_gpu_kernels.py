@@ -145,6 +145,7 @@ EXPAND_DW_CASES = [
     (1, 28, 28, 32, 192, 2, 2, 2),
     (1, 5, 6, 8, 48, 1, 0, 1),        # one partial tile, depth 8
     (2, 10, 9, 16, 64, 1, 2, 2),      # 64-channel chunks (Ce = 64)
+    (1, 17, 19, 24, 144, 1, 2, 2),    # stride 1, partial tiles at both edges, odd tile width
 ]
 
 
