@@ -48,49 +48,84 @@ __global__ __launch_bounds__(256) void conv_rgb_kernel(const uint16_t* __restric
   const long base = ((long)n * H + lo) * W * 3;  // first element
   const int cpx = (hi - lo + 1) * W;             // pixels in the patch
 
-  // stage the weights (K * RR 8-byte groups) and the patch, widened to 4 channels
+  // Stage the weights (K * RR 8-byte groups), the BN vectors and the patch
+  // (widened to 4 channels) in LDS.  Every global load of a round is issued
+  // before its LDS stores, so a block waits for one memory round trip (two
+  // patch passes per round) rather than one per loop iteration.
+  constexpr int WPT = (K * RR + 255) / 256;  // weight groups per thread
   {
     const uint2* wsrc = reinterpret_cast<const uint2*>(w4);
-    for (int i = tid; i < K * RR; i += 256) wl[i] = wsrc[i];
-    if (tid < K) {
-      bnl[tid] = scale[tid];
-      bnl[K + tid] = shift[tid];
-    }
-  }
-  if (vec16) {  // W % 8 == 0, 16-byte aligned image: 8 pixels = 3 16-byte loads -> 4 16-byte LDS writes
-    const uint4* src = reinterpret_cast<const uint4*>(x + base);
-    uint4* dst = reinterpret_cast<uint4*>(smem);
-    for (int g8 = tid; g8 < cpx / 8; g8 += 256) {
-      const uint4 v0 = src[3 * g8], v1 = src[3 * g8 + 1], v2 = src[3 * g8 + 2];
-      const uint32_t d[12] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w, v2.x, v2.y, v2.z, v2.w};
-      uint32_t w[16];  // pixel j -> (c0 | c1 << 16, c2)
+    uint2 wv[WPT];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const int e = 3 * j;  // first element of pixel j; dword e / 2
-        if ((j & 1) == 0) {
-          w[2 * j] = d[e / 2];
-          w[2 * j + 1] = d[e / 2 + 1] & 0xffffu;
-        } else {
-          w[2 * j] = (d[e / 2] >> 16) | (d[e / 2 + 1] << 16);
-          w[2 * j + 1] = d[e / 2 + 1] >> 16;
+    for (int i = 0; i < WPT; ++i) {
+      const int idx = tid + i * 256;
+      wv[i] = idx < K * RR ? wsrc[idx] : uint2{0u, 0u};
+    }
+    const float bv = tid < 2 * K ? (tid < K ? scale[tid] : shift[tid - K]) : 0.0f;
+    if (vec16) {  // W % 8 == 0, 16-byte aligned image: 8 pixels = 3 16-byte loads -> 4 16-byte LDS writes
+      const uint4* src = reinterpret_cast<const uint4*>(x + base);
+      uint4* dst = reinterpret_cast<uint4*>(smem);
+      const int n8 = cpx / 8;
+      for (int g0 = tid; g0 < n8; g0 += 2 * 256) {
+        uint4 v[2][3];
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+          const int g8 = min(g0 + u * 256, n8 - 1);
+#pragma unroll
+          for (int e = 0; e < 3; ++e) v[u][e] = src[3 * g8 + e];
+        }
+        if (g0 == tid) {  // first pass: the weights and BN go to LDS while the patch loads are in flight
+#pragma unroll
+          for (int i = 0; i < WPT; ++i)
+            if (tid + i * 256 < K * RR) wl[tid + i * 256] = wv[i];
+          if (tid < 2 * K) bnl[tid] = bv;
+        }
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+          const int g8 = g0 + u * 256;
+          if (g8 >= n8) break;
+          const uint32_t d[12] = {v[u][0].x, v[u][0].y, v[u][0].z, v[u][0].w, v[u][1].x, v[u][1].y,
+                                  v[u][1].z, v[u][1].w, v[u][2].x, v[u][2].y, v[u][2].z, v[u][2].w};
+          uint32_t w[16];  // pixel j -> (c0 | c1 << 16, c2)
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            const int e = 3 * j;  // first element of pixel j; dword e / 2
+            if ((j & 1) == 0) {
+              w[2 * j] = d[e / 2];
+              w[2 * j + 1] = d[e / 2 + 1] & 0xffffu;
+            } else {
+              w[2 * j] = (d[e / 2] >> 16) | (d[e / 2 + 1] << 16);
+              w[2 * j + 1] = d[e / 2 + 1] >> 16;
+            }
+          }
+#pragma unroll
+          for (int q = 0; q < 4; ++q) dst[4 * g8 + q] = uint4{w[4 * q], w[4 * q + 1], w[4 * q + 2], w[4 * q + 3]};
         }
       }
+      if (tid >= n8) {  // no patch pass ran on this thread
 #pragma unroll
-      for (int q = 0; q < 4; ++q) dst[4 * g8 + q] = uint4{w[4 * q], w[4 * q + 1], w[4 * q + 2], w[4 * q + 3]};
-    }
-  } else {
-    for (int i0 = tid; i0 < cpx; i0 += 256 * 4) {
-      uint32_t c0[4], c1[4], c2[4];
+        for (int i = 0; i < WPT; ++i)
+          if (tid + i * 256 < K * RR) wl[tid + i * 256] = wv[i];
+        if (tid < 2 * K) bnl[tid] = bv;
+      }
+    } else {
+      for (int i0 = tid; i0 < cpx; i0 += 256 * 4) {
+        uint32_t c0[4], c1[4], c2[4];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int i = min(i0 + u * 256, cpx - 1);
-        c0[u] = x[base + 3L * i];
-        c1[u] = x[base + 3L * i + 1];
-        c2[u] = x[base + 3L * i + 2];
+        for (int u = 0; u < 4; ++u) {
+          const int i = min(i0 + u * 256, cpx - 1);
+          c0[u] = x[base + 3L * i];
+          c1[u] = x[base + 3L * i + 1];
+          c2[u] = x[base + 3L * i + 2];
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          if (i0 + u * 256 < cpx) patch[i0 + u * 256] = uint2{c0[u] | (c1[u] << 16), c2[u]};
       }
 #pragma unroll
-      for (int u = 0; u < 4; ++u)
-        if (i0 + u * 256 < cpx) patch[i0 + u * 256] = uint2{c0[u] | (c1[u] << 16), c2[u]};
+      for (int i = 0; i < WPT; ++i)
+        if (tid + i * 256 < K * RR) wl[tid + i * 256] = wv[i];
+      if (tid < 2 * K) bnl[tid] = bv;
     }
   }
   __syncthreads();
@@ -110,7 +145,20 @@ __global__ __launch_bounds__(256) void conv_rgb_kernel(const uint16_t* __restric
     }
   __syncthreads();  // the weight area becomes the output tile [256 pixels][K] (rows padded to ROW bytes)
 
-  const float hi_clamp = act == ACT_RELU6 ? 6.0f : INFINITY;
+  const float lo_clamp = act == ACT_NONE ? -INFINITY : 0.0f, hi_clamp = act == ACT_RELU6 ? 6.0f : INFINITY;
+  // patch offset (r * W + s) of this lane's window positions q = dc*8 +
+  // quad*2 + h, and whether q is a real position (the depth tail is zero)
+  int qoff[DC][2];
+  unsigned qreal = 0;
+#pragma unroll
+  for (int dc = 0; dc < DC; ++dc)
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int q = dc * 8 + quad * 2 + h;
+      const int r = q / R, s = q - (q / R) * R;
+      qoff[dc][h] = q < RR ? r * W + s : 0;
+      if (q < RR) qreal |= 1u << (dc * 2 + h);
+    }
 #pragma unroll 1
   for (int g = 0; g < 4; ++g) {
     const int p = p0 + wave * 64 + g * 16 + (lane & 15);
@@ -118,18 +166,34 @@ __global__ __launch_bounds__(256) void conv_rgb_kernel(const uint16_t* __restric
     const int ho = pc / Wo, wo = pc - (pc / Wo) * Wo;
     const int hr0 = ho * stride - pad, ws0 = wo * stride - pad;
     bf16x8 b[DC];
+    // windows wholly inside the image (wave-uniform test): no per-position checks
+    const bool inner = hr0 >= 0 && hr0 + R <= H && ws0 >= 0 && ws0 + R <= W;
+    if (__ballot(inner) == ~0ull) {
+      const uint2* pp = patch + (hr0 - lo) * W + ws0;
 #pragma unroll
-    for (int dc = 0; dc < DC; ++dc) {
-      uint2 v[2];
+      for (int dc = 0; dc < DC; ++dc) {
+        uint2 v[2];
 #pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const int q = dc * 8 + quad * 2 + h;
-        const int r = q / R, s = q - (q / R) * R;
-        const int hr = hr0 + r, ws = ws0 + s;
-        const bool ok = q < RR && (unsigned)hr < (unsigned)H && (unsigned)ws < (unsigned)W;
-        v[h] = ok ? patch[(hr - lo) * W + ws] : uint2{0u, 0u};
+        for (int h = 0; h < 2; ++h) {
+          v[h] = pp[qoff[dc][h]];
+          if (dc * 8 + 8 > RR && !((qreal >> (dc * 2 + h)) & 1u)) v[h] = uint2{0u, 0u};
+        }
+        b[dc] = __builtin_bit_cast(bf16x8, uint4{v[0].x, v[0].y, v[1].x, v[1].y});
       }
-      b[dc] = __builtin_bit_cast(bf16x8, uint4{v[0].x, v[0].y, v[1].x, v[1].y});
+    } else {
+#pragma unroll
+      for (int dc = 0; dc < DC; ++dc) {
+        uint2 v[2];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int q = dc * 8 + quad * 2 + h;
+          const int r = q / R, s = q - (q / R) * R;
+          const int hr = hr0 + r, ws = ws0 + s;
+          const bool ok = q < RR && (unsigned)hr < (unsigned)H && (unsigned)ws < (unsigned)W;
+          v[h] = ok ? patch[(hr - lo) * W + ws] : uint2{0u, 0u};
+        }
+        b[dc] = __builtin_bit_cast(bf16x8, uint4{v[0].x, v[0].y, v[1].x, v[1].y});
+      }
     }
     // depth outer, channel blocks inner: KB independent accumulation chains in flight
     f32x4 accs[KB];
@@ -146,11 +210,7 @@ __global__ __launch_bounds__(256) void conv_rgb_kernel(const uint16_t* __restric
       const f32x4 sh = *reinterpret_cast<const f32x4*>(bnl + K + kb * 16 + 4 * quad);
       bf16x4 o;  // this lane's channels kb*16 + 4*quad.. of its pixel
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        float t = acc[i] * sc[i] + sh[i];
-        if (act != ACT_NONE) t = fminf(fmaxf(t, 0.0f), hi_clamp);
-        o[i] = (bf16)t;
-      }
+      for (int i = 0; i < 4; ++i) o[i] = (bf16)__builtin_amdgcn_fmed3f(acc[i] * sc[i] + sh[i], lo_clamp, hi_clamp);
       *reinterpret_cast<bf16x4*>(ot + (wave * 64 + g * 16 + (lane & 15)) * ROW + (kb * 16 + 4 * quad) * 2) = o;
     }
   }
