@@ -326,9 +326,49 @@ def config1(ds):
                 latency_us=r["latency_us"], p99_us=r["p99_us"], inferences_per_s=[4e6 / L for L in r["latency_us"]])
 
 
-def config2(ds, args):
+def knee_model_prediction(ds, torch, m, b, n_cu_grid, latency_us):
+    """Sec. 4.2's analytical model with this library's own kernels: N_i =
+    workgroups of unit i / workgroups one CU holds (dstack_kernel_shapes),
+    t_p from the unit's event-timed duration on the whole GPU (the durations
+    scaled so that they sum to the measured latency there), t_np = 0.  E_t is
+    predicted on the sweep's CU counts and its knee compared with the
+    measured one; a second prediction adds the memory term d_i / (M S) with
+    the unit's algorithmic bytes and M = measured HBM bandwidth per CU."""
+    from tests import gpu_util as gu
+    from tests import inputs
+    p = ds.Partition(1.0)
+    x = gu.dev_bf16(inputs.image_batch(1021, b))
+    y = gu.empty_f32(m.output_shape(b))
+    for _ in range(3):
+        m.infer(b, x, y, p)
+    p.synchronize()
+    shapes = m.kernel_shapes(b, x, y, p)
+    recs = [m.profile_layers(b, x, y, p) for _ in range(3)]
+    assert len(shapes) == len(recs[0]) and all(s["kind"] == r["kind"] for s, r in zip(shapes, recs[0]))
+    full = p.n_cu
+    t = [1000.0 * sorted(r[i]["ms"] for r in recs)[1] for i in range(len(shapes))]
+    scale = latency_us[n_cu_grid.index(full)] / sum(t)
+    n = [s["workgroups"] / max(1, s["blocks_per_cu"]) for s in shapes]
+    tp = [scale * ti * max(1.0, min(full, ni)) / ni for ti, ni in zip(t, n)]
+    et, k = ds.knee_model_eval(n, tp, n_cu_grid, 0.0)
+    mb = bw_probe(torch, p) * 1e3 / full  # bytes per us per CU
+    d = [s["bytes"] for s in shapes]
+    tp_m = [max(0.0, scale * ti - di / (mb * full)) * max(1.0, min(full, ni)) / ni for ti, ni, di in zip(t, n, d)]
+    et_m, k_m = ds.knee_model_eval(n, tp_m, n_cu_grid, 0.0, 1.0, None, d, mb)
+    p.destroy()
+    err = lambda e: sum(abs(a - L) / L for a, L in zip(e, latency_us)) / len(latency_us)
+    return dict(units=len(shapes), n_par_max=max(n), n_par_median=sorted(n)[len(n) // 2],
+                predicted_knee_slots=n_cu_grid[k] // 8, predicted_latency_us=[round(v, 1) for v in et],
+                mean_abs_rel_error=err(et),
+                with_memory_term=dict(predicted_knee_slots=n_cu_grid[k_m] // 8,
+                                      predicted_latency_us=[round(v, 1) for v in et_m], mean_abs_rel_error=err(et_m),
+                                      bw_per_cu_bytes_per_us=mb))
+
+
+def config2(ds, torch, args):
     """ResNet-50 at batch 1, 8 and 32 over the 10 fractions: latency, inf/s,
-    efficacy b / (L^2 * CUs) and the knee (Sec. 3.2)."""
+    efficacy b / (L^2 * CUs) and the knee (Sec. 3.2), beside the knee the
+    analytical model of Sec. 4.2 predicts from the kernels' parallelism."""
     m = ds.Model("resnet50", 1020)
     rows = []
     for b in (1, 8, 32):
@@ -336,7 +376,9 @@ def config2(ds, args):
         rows.append(dict(batch=b, n_cu=r["n_cu"], latency_us=r["latency_us"], p99_us=r["p99_us"],
                          inferences_per_s=[b * 1e6 / L for L in r["latency_us"]],
                          eta=[b / (L * L * c) for L, c in zip(r["latency_us"], r["n_cu"])],
-                         knee_slots=r["knee_slots"], deployed_slots=r["deployed_slots"]))
+                         knee_slots=r["knee_slots"], deployed_slots=r["deployed_slots"],
+                         knee_model=knee_model_prediction(ds, torch, m, b, list(r["n_cu"]),
+                                                          [float(v) for v in r["latency_us"]])))
     m.destroy()
     return dict(workload="ResNet-50 v1.5, 224x224x3, seed 1020", fractions=FRACTIONS, rows=rows)
 
@@ -550,7 +592,7 @@ def main():
     c1 = c2 = c4 = c5 = None
     if not args.headline_only:
         c1 = config1(ds)
-        c2 = config2(ds, args)
+        c2 = config2(ds, torch, args)
         c4 = config4(ds, torch, args)
         extra = [("vgg19", 1052, [1, 2, 4, 8]), ("lstm2", 1053, [1, 2, 4, 8, 16, 32])]
         m4 = [ds.Model(a, s) for a, s, _ in extra]

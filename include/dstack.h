@@ -166,6 +166,29 @@ typedef struct {
 dstack_status dstack_profile_layers(dstack_model m, int batch, const void* d_in, void* d_out, dstack_partition p,
                                     dstack_layer_time* out, int max_layers, int* n_layers);
 
+/* Launch shapes of one forward (the per-kernel parallelism N_i of Sec.
+ * 4.2's analytical model, taken from this library's own kernels): one entry
+ * per timed unit of dstack_profile_layers, in the same order, with the
+ * unit's kernel class, its number of kernel launches, the workgroups of its
+ * largest launch and how many of those workgroups one CU holds at once
+ * (occupancy from the kernel's registers and LDS), plus its algorithmic
+ * FLOPs and bytes.  Nothing is launched and d_in / d_out (the buffers a
+ * forward would use, as in dstack_infer) are neither read nor written: the
+ * forward's host logic runs with kernel launches recorded instead (launch
+ * plans use the partition's CU count).  Needs a GPU (occupancy queries);
+ * fills at most max_units entries. */
+typedef struct {
+  int kind;
+  int launches;
+  int64_t workgroups;
+  int blocks_per_cu;
+  int pad;
+  double flops;
+  double bytes;
+} dstack_kernel_shape;
+dstack_status dstack_kernel_shapes(dstack_model m, int batch, const void* d_in, void* d_out, dstack_partition p,
+                                   dstack_kernel_shape* out, int max_units, int* n_units);
+
 /* ------------------------------------------------------------------ */
 /* Knee sweep (Sec. 3.2 measurement; Sec. 4.3 Eq. first_order_derivative;  */
 /* Sec. 5 Eq. efficiencySquareLatency)                                 */
@@ -227,6 +250,45 @@ dstack_status dstack_knee_search_table(int batch, const int* slots, const int64_
                                        dstack_knee_search_result* out);
 dstack_status dstack_knee_search(dstack_model m, int batch, const double* fractions, int n, int start_slots,
                                  int warmup, int reps, dstack_knee_search_result* out);
+
+/* ------------------------------------------------------------------ */
+/* Analytical DNN model (Sec. 4.2, Eqs. layer_num_ops,                  */
+/* execution_time_per_layer, memory_latency,                           */
+/* total_non_paralleizable_time, total_time_shrinking_kernel;          */
+/* Eq. first_order_derivative), host only                              */
+/* ------------------------------------------------------------------ */
+/* A DNN of n_kernels kernels: kernel i has n_par[i] (N_i >= 0) parallel
+ * operations of t_p[i] each, repeats reps[i] times (NULL: 1) and moves
+ * data[i] bytes (NULL: no memory term).  On S CUs
+ *   E_i  = N_i t_p / max(1, min(S, N_i)),
+ *   E_m  = d_i / (M S)   (M = mem_bw_per_sm, bandwidth per CU; <= 0: none;
+ *                         the printed d_i S / M is read as d_i / (M S), the
+ *                         total bandwidth growing with S as the text says),
+ *   W_se = batch_serial * sum_i R_i (t_np + E_m),
+ *   E_t  = W_se + sum_i R_i E_i,
+ * sums in kernel order, fp64.  dstack_knee_model_eval writes E_t for each of
+ * the n_s candidates s_values[j] >= 1 into et_out and the index of the
+ * knee, the first candidate with the least E_t^2 S (the largest
+ * 1 / (E_t^2 S)).  Negative or non-finite N_i, t_p, R_i, d_i, t_np or
+ * batch_serial -> E_INVALID.  Times are in any one unit. */
+typedef struct {
+  int n_kernels;
+  int pad;
+  const double* n_par;
+  const double* t_p;
+  const double* reps;
+  const double* data;
+  double t_np;
+  double mem_bw_per_sm;
+  double batch_serial;
+} dstack_knee_model;
+dstack_status dstack_knee_model_eval(const dstack_knee_model* m, const int* s_values, int n_s, double* et_out,
+                                     int* knee_index);
+/* The paper's synthetic kernel sequence (Eq. layer_num_ops): N_1 = p*b,
+ * N_i = max(0, floor(N_{i-1} - p*b/kmax)) for i = 2..kmax (clamped at 0
+ * once the work is used up), into n_out[kmax].  p >= 0, b >= 1,
+ * kmax >= 1. */
+dstack_status dstack_knee_model_sequence(int p, int b, int kmax, double* n_out);
 
 /* GPU% change of a running model (Sec. 3.5).  A GPU% is a CU-masked stream
  * here, so a change creates a stream (no model reload: weights are shared).

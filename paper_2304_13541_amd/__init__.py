@@ -41,6 +41,19 @@ class LayerTime(ctypes.Structure):
                 ("gemm_m", ctypes.c_int), ("gemm_n", ctypes.c_int), ("gemm_k", ctypes.c_int)]
 
 
+class KernelShape(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int), ("launches", ctypes.c_int), ("workgroups", ctypes.c_int64),
+                ("blocks_per_cu", ctypes.c_int), ("pad", ctypes.c_int), ("flops", ctypes.c_double),
+                ("bytes", ctypes.c_double)]
+
+
+class KneeModel(ctypes.Structure):
+    _fields_ = [("n_kernels", ctypes.c_int), ("pad", ctypes.c_int), ("n_par", ctypes.POINTER(ctypes.c_double)),
+                ("t_p", ctypes.POINTER(ctypes.c_double)), ("reps", ctypes.POINTER(ctypes.c_double)),
+                ("data", ctypes.POINTER(ctypes.c_double)), ("t_np", ctypes.c_double),
+                ("mem_bw_per_sm", ctypes.c_double), ("batch_serial", ctypes.c_double)]
+
+
 class KneeResult(ctypes.Structure):
     _fields_ = [("n", ctypes.c_int), ("batch", ctypes.c_int), ("slots", ctypes.c_int * MAX_SWEEP),
                 ("n_cu", ctypes.c_int * MAX_SWEEP), ("latency_us", ctypes.c_int64 * MAX_SWEEP),
@@ -129,6 +142,10 @@ _SIGS = {
     "dstack_generate_params": ([ctypes.c_char_p, _u64, _i, _vp, _sz, ctypes.POINTER(ctypes.c_int64)], _i),
     "dstack_infer": ([_vp, _i, _vp, _vp, _vp], _i),
     "dstack_profile_layers": ([_vp, _i, _vp, _vp, _vp, ctypes.POINTER(LayerTime), _i, ctypes.POINTER(_i)], _i),
+    "dstack_kernel_shapes": ([_vp, _i, _vp, _vp, _vp, ctypes.POINTER(KernelShape), _i, ctypes.POINTER(_i)], _i),
+    "dstack_knee_model_eval": ([ctypes.POINTER(KneeModel), ctypes.POINTER(_i), _i, ctypes.POINTER(_d),
+                                ctypes.POINTER(_i)], _i),
+    "dstack_knee_model_sequence": ([_i, _i, _i, ctypes.POINTER(_d)], _i),
     "dstack_knee_sweep": ([_vp, _i, ctypes.POINTER(_d), _i, _i, _i, ctypes.POINTER(KneeResult)], _i),
     "dstack_schedule": ([ctypes.POINTER(SchedModel), _i, ctypes.POINTER(SchedParams), ctypes.POINTER(ScheduleOut)], _i),
     "dstack_simulate": ([ctypes.POINTER(SchedModel), _i, ctypes.POINTER(SchedParams), ctypes.POINTER(SimParams),
@@ -287,6 +304,17 @@ class Model:
         return [dict(kind=arr[i].kind, ms=arr[i].ms, flops=arr[i].flops, bytes=arr[i].bytes,
                      gemm=(arr[i].gemm_m, arr[i].gemm_n, arr[i].gemm_k)) for i in range(n.value)]
 
+    def kernel_shapes(self, batch, x, y, partition, max_units=4096):
+        """Per timed unit of profile_layers: kind, launches, workgroups of the largest launch,
+        workgroups one CU holds at once, FLOPs and bytes; launches nothing (see dstack_kernel_shapes)."""
+        arr = (KernelShape * max_units)()
+        n = ctypes.c_int()
+        _check(lib().dstack_kernel_shapes(self.h, batch, _ptr(x), _ptr(y), partition.h, arr, max_units,
+                                          ctypes.byref(n)))
+        return [dict(kind=arr[i].kind, launches=arr[i].launches, workgroups=arr[i].workgroups,
+                     blocks_per_cu=arr[i].blocks_per_cu, flops=arr[i].flops, bytes=arr[i].bytes)
+                for i in range(n.value)]
+
     def knee_search(self, batch, fractions=None, start_slots=10, warmup=5, reps=20):
         """Binary-search the knee from live latency over the GPU% grid (see dstack_knee_search)."""
         fractions = fractions or [0.1 * i for i in range(1, 11)]
@@ -316,6 +344,26 @@ def _search_dict(r):
     n = min(r.n_probes, MAX_PROBES)
     return dict(batch=r.batch, knee_slots=r.knee_slots, deployed_slots=r.deployed_slots, n_probes=r.n_probes,
                 probes=[(r.probe_slots[i], r.probe_latency_us[i]) for i in range(n)], seconds=r.seconds)
+
+
+def knee_model_sequence(p, b, kmax):
+    """N_1..N_kmax of the analytical model's synthetic kernel sequence (host only)."""
+    out = (_d * kmax)()
+    _check(lib().dstack_knee_model_sequence(p, b, kmax, out))
+    return list(out)
+
+
+def knee_model_eval(n_par, t_p, s_values, t_np, batch_serial=1.0, reps=None, data=None, mem_bw_per_sm=0.0):
+    """E_t on each candidate S and the knee index of the analytical model (host only)."""
+    k = len(n_par)
+    arr = lambda v: None if v is None else (_d * k)(*[float(x) for x in v])
+    npar, tp, rp, dt = arr(n_par), arr(t_p), arr(reps), arr(data)
+    m = KneeModel(k, 0, npar, tp, rp, dt, float(t_np), float(mem_bw_per_sm), float(batch_serial))
+    sv = (_i * len(s_values))(*s_values)
+    et = (_d * len(s_values))()
+    ki = _i()
+    _check(lib().dstack_knee_model_eval(ctypes.byref(m), sv, len(s_values), et, ctypes.byref(ki)))
+    return list(et), ki.value
 
 
 def knee_search_table(batch, table, total=TOTAL_SLOTS, start_slots=10, overprov_slots=2):

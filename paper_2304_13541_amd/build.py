@@ -3,8 +3,9 @@
 Every HIP / C++ source under csrc/ is compiled to an object in _build/ (in
 parallel), then linked into paper_2304_13541_amd/libdstack.so.  All device
 code is built with packed-FP32 instructions disabled.  The weight generator
-(rng.cpp) is built with floating-point contraction off so that its fp64
-arithmetic rounds exactly as written.
+(rng.cpp) and the analytical knee model (knee_model.cpp) are built with
+floating-point contraction off so that their fp64 arithmetic rounds exactly
+as written.
 """
 import concurrent.futures as cf
 import os
@@ -17,10 +18,10 @@ OUT = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libdstack.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
-SOURCES = ["conv_igemm.hip", "conv_rgb.hip", "expand_dw.hip", "kernels_misc.hip", "kernels_seq.hip", "model.cpp", "rng.cpp", "sched.cpp", "launcher.cpp", "serve.cpp", "capi.cpp"]
+SOURCES = ["conv_igemm.hip", "conv_rgb.hip", "expand_dw.hip", "kernels_misc.hip", "kernels_seq.hip", "model.cpp", "rng.cpp", "sched.cpp", "knee_model.cpp", "launcher.cpp", "serve.cpp", "capi.cpp"]
 BASE_FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-result",
               "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
-PER_FILE = {"rng.cpp": ["-ffp-contract=off"]}
+PER_FILE = {"rng.cpp": ["-ffp-contract=off"], "knee_model.cpp": ["-ffp-contract=off"]}
 
 
 def _compile(src):

@@ -452,6 +452,52 @@ int64_t round_us(double us) { return std::max<int64_t>(1, (int64_t)std::floor(us
 
 }  // namespace
 
+dstack_status dstack_kernel_shapes(dstack_model h, int batch, const void* d_in, void* d_out, dstack_partition p,
+                                   dstack_kernel_shape* out, int max_units, int* n_units) {
+  return guarded([&] {
+    DS_CHECK(h && p && out && n_units, DSTACK_E_INVALID, "kernel_shapes: null pointer");
+    DS_CHECK(max_units >= 0, DSTACK_E_INVALID, "kernel_shapes: max_units must be >= 0");
+    dstack_status s = check_batch(h->m, batch);
+    if (s != DSTACK_OK) return s;
+    std::vector<LaunchShape> rec;
+    struct Install {  // the recorder is removed on every exit path
+      explicit Install(std::vector<LaunchShape>* r) { shape_recorder() = r; }
+      ~Install() { shape_recorder() = nullptr; }
+    } install(&rec);
+    KernelTimer timer;
+    timer.st = p->stream;
+    timer.dry = true;
+    s = infer_impl(h->m, batch, d_in, d_out, p, &timer);
+    if (s != DSTACK_OK) return s;
+    int n = 0;
+    for (const auto& u : timer.units) {
+      if (n >= max_units) break;
+      dstack_kernel_shape k{};
+      k.kind = u.kind;
+      k.launches = (int)(u.l1 - u.l0);
+      for (size_t i = u.l0; i < u.l1; ++i)
+        if (rec[i].workgroups > k.workgroups) {
+          k.workgroups = rec[i].workgroups;
+          k.blocks_per_cu = rec[i].per_cu;
+        }
+      k.flops = u.flops;
+      k.bytes = u.bytes;
+      out[n++] = k;
+    }
+    *n_units = n;
+    return DSTACK_OK;
+  });
+}
+
+dstack_status dstack_knee_model_eval(const dstack_knee_model* m, const int* s_values, int n_s, double* et_out,
+                                     int* knee_index) {
+  return guarded([&] { return knee_model_eval(m, s_values, n_s, et_out, knee_index); });
+}
+
+dstack_status dstack_knee_model_sequence(int p, int b, int kmax, double* n_out) {
+  return guarded([&] { return knee_model_sequence(p, b, kmax, n_out); });
+}
+
 dstack_status dstack_knee_sweep(dstack_model h, int batch, const double* fractions, int n, int warmup, int reps,
                                 dstack_knee_result* out) {
   return guarded([&] {

@@ -6,6 +6,7 @@
 #include <cstdint>
 #include <cstdio>
 #include <string>
+#include <vector>
 
 #include "../../include/dstack.h"
 
@@ -50,6 +51,35 @@ struct DispatchEvents {
   hipEvent_t start = nullptr, stop = nullptr;
 };
 DispatchEvents& dispatch_events();
+
+// Launch-shape recording, for the analytical model's per-kernel parallelism:
+// while a recorder is installed on the calling thread, launch() notes each
+// kernel's workgroup count and how many of its workgroups one CU holds at
+// once, and does not launch it.  Every kernel of the library goes through
+// launch().
+struct LaunchShape {
+  long workgroups;
+  int per_cu;
+};
+std::vector<LaunchShape>*& shape_recorder();
+
+template <typename... KArgs, typename... Args>
+inline void launch(void (*kernel)(KArgs...), dim3 grid, dim3 block, size_t shmem, hipStream_t st, Args... args) {
+  if (std::vector<LaunchShape>* rec = shape_recorder()) {
+    int per_cu = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, (int)(block.x * block.y * block.z), shmem) !=
+        hipSuccess)
+      per_cu = 0;
+    rec->push_back(LaunchShape{(long)grid.x * grid.y * grid.z, per_cu});
+    return;
+  }
+  hipLaunchKernelGGL(kernel, grid, block, shmem, st, args...);
+}
+
+// Analytical DNN model (Sec. 4.2); the C ABI wraps these.
+dstack_status knee_model_sequence(int p, int b, int kmax, double* n_out);
+dstack_status knee_model_eval(const dstack_knee_model* km, const int* s_values, int n_s, double* et_out,
+                              int* knee_index);
 
 inline dstack_status fail(dstack_status st, const std::string& msg) {
   set_error(msg);

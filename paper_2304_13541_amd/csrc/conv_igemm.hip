@@ -516,13 +516,14 @@ __global__ __launch_bounds__(256) void conv_igemm_kernel(ConvArgs a) {
     rows(std::true_type{});
 }
 
-// 256-thread launch; through hipExtLaunchKernelGGL when dispatch events are armed
+// 256-thread launch; through hipExtLaunchKernelGGL when dispatch events are
+// armed (and not while launch shapes are being recorded)
 template <typename K, typename... Args>
 static void launch_k(K kernel, dim3 grid, hipStream_t st, hipEvent_t e0, hipEvent_t e1, Args... args) {
-  if (e0 || e1)
+  if ((e0 || e1) && !shape_recorder())
     hipExtLaunchKernelGGL(kernel, grid, dim3(256), 0, st, e0, e1, 0, args...);
   else
-    hipLaunchKernelGGL(kernel, grid, dim3(256), 0, st, args...);
+    launch(kernel, grid, dim3(256), 0, st, args...);
 }
 
 // 1x1, stride-1 convolution of small depth (C <= 32): a streaming GEMM that

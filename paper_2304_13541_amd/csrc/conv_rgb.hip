@@ -239,7 +239,7 @@ static dstack_status rgb_launch(const bf16* x, int N, int H, int W, const bf16* 
                ((uintptr_t)shift & 15) == 0,
            DSTACK_E_INVALID, "conv2d_rgb: w4 must be 8-byte aligned; y, scale and shift 16-byte aligned");
   const int tiles = (Ho * Wo + RGB_PIX - 1) / RGB_PIX;
-  hipLaunchKernelGGL((conv_rgb_kernel<R, K>), dim3((unsigned)(N * tiles)), dim3(256), (size_t)lds, st,
+  launch(conv_rgb_kernel<R, K>, dim3((unsigned)(N * tiles)), dim3(256), (size_t)lds, st,
                      reinterpret_cast<const uint16_t*>(x), H, W, w4, stride, pad, scale, shift, act, y, Ho, Wo, tiles,
                      (W % 8 == 0 && ((uintptr_t)x & 15) == 0) ? 1 : 0, (int)patch);
   return DSTACK_OK;

@@ -308,11 +308,11 @@ template <int CB, int S>
 static void expand_dw_launch_cb(const ExpandDwArgs& a, int ds, hipStream_t st) {
   const dim3 grid((unsigned)a.blocks);
   switch (ds) {
-    case 1: hipLaunchKernelGGL((expand_dw_kernel<CB, 1, S>), grid, dim3(256), 0, st, a); break;
-    case 2: hipLaunchKernelGGL((expand_dw_kernel<CB, 2, S>), grid, dim3(256), 0, st, a); break;
-    case 3: hipLaunchKernelGGL((expand_dw_kernel<CB, 3, S>), grid, dim3(256), 0, st, a); break;
-    case 4: hipLaunchKernelGGL((expand_dw_kernel<CB, 4, S>), grid, dim3(256), 0, st, a); break;
-    default: hipLaunchKernelGGL((expand_dw_kernel<CB, 5, S>), grid, dim3(256), 0, st, a); break;
+    case 1: launch(expand_dw_kernel<CB, 1, S>, grid, dim3(256), 0, st, a); break;
+    case 2: launch(expand_dw_kernel<CB, 2, S>, grid, dim3(256), 0, st, a); break;
+    case 3: launch(expand_dw_kernel<CB, 3, S>, grid, dim3(256), 0, st, a); break;
+    case 4: launch(expand_dw_kernel<CB, 4, S>, grid, dim3(256), 0, st, a); break;
+    default: launch(expand_dw_kernel<CB, 5, S>, grid, dim3(256), 0, st, a); break;
   }
 }
 

@@ -88,7 +88,7 @@ template <int STRIDE, int V>
 static void dw_launch(const bf16* x, int N, int H, int W, int C, const bf16* w, const float* scale,
                       const float* shift, int act, bf16* y, int Ho, int Wo, hipStream_t st) {
   const long total = (long)N * Ho * ((Wo + V - 1) / V) * (C / 8);
-  hipLaunchKernelGGL((dwconv3x3_kernel<STRIDE, V>), dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st, x, N, H,
+  launch(dwconv3x3_kernel<STRIDE, V>, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st, x, N, H,
                      W, C, w, scale, shift, act, y, Ho, Wo);
 }
 
@@ -154,7 +154,7 @@ dstack_status launch_maxpool(const bf16* x, int N, int H, int W, int C, int k, i
   int Ho = out_dim(H, k, stride, pad), Wo = out_dim(W, k, stride, pad);
   DS_CHECK(Ho > 0 && Wo > 0, DSTACK_E_INVALID, "maxpool: empty output");
   long total = (long)N * Ho * Wo * (C / 8);
-  hipLaunchKernelGGL(maxpool_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st, x, N, H, W, C, k,
+  launch(maxpool_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st, x, N, H, W, C, k,
                      stride, pad, y, Ho, Wo);
   DS_HIP(hipGetLastError());
   return DSTACK_OK;
@@ -199,7 +199,7 @@ __global__ __launch_bounds__(256) void avgpool_kernel(const bf16* __restrict__ x
 dstack_status launch_avgpool(const bf16* x, int N, int H, int W, int C, bf16* y, hipStream_t st) {
   DS_CHECK(C % 8 == 0, DSTACK_E_UNSUPPORTED, "avgpool: C must be a multiple of 8");
   DS_CHECK(N > 0 && H > 0 && W > 0 && N <= 65535, DSTACK_E_INVALID, "avgpool: bad shape");
-  hipLaunchKernelGGL(avgpool_kernel, dim3(ceil_div(C / 8, 32), N), dim3(256), 0, st, x, N, H * W, C, y);
+  launch(avgpool_kernel, dim3(ceil_div(C / 8, 32), N), dim3(256), 0, st, x, N, H * W, C, y);
   DS_HIP(hipGetLastError());
   return DSTACK_OK;
 }
@@ -221,7 +221,7 @@ __global__ void probe_kernel(uint32_t* out, int n) {
 }
 
 dstack_status launch_probe(uint32_t* d_out, int n_blocks, hipStream_t st) {
-  hipLaunchKernelGGL(probe_kernel, dim3(n_blocks), dim3(64), 0, st, d_out, n_blocks);
+  launch(probe_kernel, dim3(n_blocks), dim3(64), 0, st, d_out, n_blocks);
   DS_HIP(hipGetLastError());
   return DSTACK_OK;
 }

@@ -13,13 +13,6 @@ namespace {
 
 __device__ __forceinline__ bf16x8 ld8(const bf16* p) { return *reinterpret_cast<const bf16x8*>(p); }
 
-__device__ __forceinline__ float dot8(bf16x8 a, bf16x8 b) {
-  float s = 0.f;
-#pragma unroll
-  for (int e = 0; e < 8; ++e) s += (float)a[e] * (float)b[e];
-  return s;
-}
-
 }  // namespace
 
 // ------------------------------------------------------------------ FC ----
@@ -153,12 +146,12 @@ dstack_status launch_fc(const bf16* x, int B, int I, const bf16* w, const float*
   dim3 grid((O + 15) / 16, s);
   const int f = out_fp32 ? 1 : 0;
   if (B <= 16)
-    hipLaunchKernelGGL(fc_kernel<1>, grid, dim3(256), 0, st, x, B, I, w, bias, O, act, y, f, ws, sps);
+    launch(fc_kernel<1>, grid, dim3(256), 0, st, x, B, I, w, bias, O, act, y, f, ws, sps);
   else
-    hipLaunchKernelGGL(fc_kernel<2>, grid, dim3(256), 0, st, x, B, I, w, bias, O, act, y, f, ws, sps);
+    launch(fc_kernel<2>, grid, dim3(256), 0, st, x, B, I, w, bias, O, act, y, f, ws, sps);
   DS_HIP(hipGetLastError());
   if (s > 1) {
-    hipLaunchKernelGGL(fc_reduce_kernel, dim3((B * O + 255) / 256), dim3(256), 0, st, ws, s, B, O, bias, act, y, f);
+    launch(fc_reduce_kernel, dim3((B * O + 255) / 256), dim3(256), 0, st, ws, s, B, O, bias, act, y, f);
     DS_HIP(hipGetLastError());
   }
   return DSTACK_OK;
@@ -254,13 +247,13 @@ dstack_status launch_lstm_step(const float* gx_t, const bf16* w_hh, const bf16* 
   dim3 grid(H / 4), blk(256);
   const int f = first ? 1 : 0;
   if (ksw <= 2)
-    hipLaunchKernelGGL(lstm_step_kernel<2>, grid, blk, 0, st, gx_t, w_hh, h_prev, c, h_next, h_f32, B, H, f);
+    launch(lstm_step_kernel<2>, grid, blk, 0, st, gx_t, w_hh, h_prev, c, h_next, h_f32, B, H, f);
   else if (ksw <= 4)
-    hipLaunchKernelGGL(lstm_step_kernel<4>, grid, blk, 0, st, gx_t, w_hh, h_prev, c, h_next, h_f32, B, H, f);
+    launch(lstm_step_kernel<4>, grid, blk, 0, st, gx_t, w_hh, h_prev, c, h_next, h_f32, B, H, f);
   else if (ksw <= 8)
-    hipLaunchKernelGGL(lstm_step_kernel<8>, grid, blk, 0, st, gx_t, w_hh, h_prev, c, h_next, h_f32, B, H, f);
+    launch(lstm_step_kernel<8>, grid, blk, 0, st, gx_t, w_hh, h_prev, c, h_next, h_f32, B, H, f);
   else
-    hipLaunchKernelGGL(lstm_step_kernel<16>, grid, blk, 0, st, gx_t, w_hh, h_prev, c, h_next, h_f32, B, H, f);
+    launch(lstm_step_kernel<16>, grid, blk, 0, st, gx_t, w_hh, h_prev, c, h_next, h_f32, B, H, f);
   DS_HIP(hipGetLastError());
   return DSTACK_OK;
 }

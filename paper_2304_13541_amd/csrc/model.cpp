@@ -576,7 +576,16 @@ dstack_status get_workspace(Model& m, int pid, int n_cu, hipStream_t st, Workspa
   return DSTACK_OK;
 }
 
+std::vector<LaunchShape>*& shape_recorder() {
+  static thread_local std::vector<LaunchShape>* rec = nullptr;
+  return rec;
+}
+
 void KernelTimer::before() {
+  if (dry) {
+    unit_l0 = shape_recorder() ? shape_recorder()->size() : 0;
+    return;
+  }
   if (!pending) {
     (void)hipEventCreate(&pending);
     (void)hipEventRecord(pending, st);
@@ -589,12 +598,20 @@ DispatchEvents& dispatch_events() {
 }
 
 void KernelTimer::before_dispatch() {
+  if (dry) {
+    before();
+    return;
+  }
   (void)hipEventCreate(&ds_start);
   (void)hipEventCreate(&ds_stop);
   dispatch_events() = DispatchEvents{ds_start, ds_stop};
 }
 
 void KernelTimer::after(int kind, double flops, double bytes, int m, int n, int k) {
+  if (dry) {
+    units.push_back(Unit{kind, unit_l0, shape_recorder() ? shape_recorder()->size() : unit_l0, flops, bytes});
+    return;
+  }
   if (ds_start) {  // timed by the kernels' own dispatch packets
     recs.push_back(Rec{kind, flops, bytes, ds_start, ds_stop, m, n, k});
     ds_start = ds_stop = nullptr;

@@ -145,6 +145,16 @@ struct KernelTimer {
   std::vector<Rec> recs;
   hipEvent_t pending = nullptr;
   hipEvent_t ds_start = nullptr, ds_stop = nullptr;  // armed dispatch events (before_dispatch)
+  // dry mode: no events; each timed unit notes the range of launch shapes
+  // the installed recorder took for it
+  bool dry = false;
+  struct Unit {
+    int kind;
+    size_t l0, l1;
+    double flops, bytes;
+  };
+  std::vector<Unit> units;
+  size_t unit_l0 = 0;
   void before();
   void before_dispatch();
   void after(int kind, double flops, double bytes, int m = 0, int n = 0, int k = 0);

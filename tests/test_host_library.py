@@ -175,3 +175,44 @@ def test_knee_search_table_parity():
         ds.knee_search_table(1, {3: 0, 6: 10})
     with pytest.raises(ds.DStackError):  # a slot count above the total
         ds.knee_search_table(1, {3: 5, 40: 10})
+
+
+def test_knee_model_parity_random():
+    """dstack_knee_model_eval reproduces the analytical-model oracle bit for
+    bit (E_t on every candidate, the knee index) on random kernel sequences,
+    with and without repetitions and the memory term."""
+    from oracle import knee_model as km
+    rnd = random.Random(77)
+    for trial in range(400):
+        k = rnd.randint(1, 60)
+        n = [rnd.choice([0.0, float(rnd.randint(1, 300)), rnd.uniform(0.0, 2.0), rnd.uniform(1.0, 900.0)])
+             for _ in range(k)]
+        tp = [rnd.uniform(0.0, 80.0) for _ in range(k)]
+        reps = None if rnd.random() < 0.5 else [float(rnd.randint(0, 4)) for _ in range(k)]
+        data = None if rnd.random() < 0.5 else [rnd.uniform(0.0, 1e7) for _ in range(k)]
+        m = rnd.choice([0.0, -1.0, rnd.uniform(1.0, 5e4)])
+        tnp = rnd.uniform(0.0, 30.0)
+        b = float(rnd.randint(0, 32))
+        s_values = sorted(rnd.sample(range(1, 300), rnd.randint(1, 20)))
+        et, ki = ds.knee_model_eval(n, tp, s_values, tnp, b, reps, data, m)
+        et_o, ki_o = km.knee(n, tp, s_values, tnp, b, reps, data, m)
+        assert et == et_o and ki == ki_o, trial
+
+
+def test_knee_model_sequence_parity():
+    from oracle import knee_model as km
+    for p, b, kmax in [(20, 1, 50), (40, 1, 50), (60, 1, 50), (20, 2, 50), (7, 3, 11), (0, 1, 5), (1000, 32, 53)]:
+        assert ds.knee_model_sequence(p, b, kmax) == km.sequence(p, b, kmax)
+
+
+def test_knee_model_rejects_bad_arguments():
+    with pytest.raises(ds.DStackError):
+        ds.knee_model_eval([1.0, -2.0], [1.0, 1.0], [1, 2], 0.0)   # negative N_i
+    with pytest.raises(ds.DStackError):
+        ds.knee_model_eval([1.0], [float("nan")], [1], 0.0)        # non-finite t_p
+    with pytest.raises(ds.DStackError):
+        ds.knee_model_eval([1.0], [1.0], [0, 2], 0.0)               # S < 1
+    with pytest.raises(ds.DStackError):
+        ds.knee_model_eval([], [], [1], 0.0)                        # no kernels
+    with pytest.raises(ds.DStackError):
+        ds.knee_model_sequence(5, 0, 10)                            # b < 1
