@@ -405,13 +405,22 @@ dstack_status dstack_schedule(const dstack_sched_model* models, int n_models, co
  *    started job ends both count as violations.
  * arrivals_us[i] must be sorted and inside [0, duration_us).  job_hash is
  * FNV-1a (64-bit) over (start, model, batch, slot mask, duration, kind) of
- * every started job, kind 0 planned / 1 FOD, each as 8 little-endian bytes. */
+ * every started job, kind 0 planned / 1 FOD, each as 8 little-endian bytes.
+ *
+ * policy selects the scheduler (Sec. 7's comparators; dstack_serve takes
+ * 0 only): 0 D-STACK (the plan plus the FOD fill above); 1 max-throughput
+ * and 2 max-min fair run no plan, only the fill on every trigger (fod is
+ * ignored) with no planned start to respect and the candidates in another
+ * order: 1 by the model's SLO-optimal latency at its knee (least runtime
+ * first), then index; 2 by deployed slots (smallest GPU% demand first),
+ * then busy time, then index.  Other values -> E_INVALID. */
 typedef struct {
   int64_t duration_us;
   int fod;
   int sessions_window;                          /* 10 */
   const int64_t* arrivals_us[DSTACK_MAX_MODELS];
   int n_arrivals[DSTACK_MAX_MODELS];
+  int policy;                                   /* 0 D-STACK, 1 max-throughput, 2 max-min fair */
 } dstack_sim_params;
 
 typedef struct {
@@ -430,6 +439,41 @@ typedef struct {
 
 dstack_status dstack_simulate(const dstack_sched_model* models, int n_models, const dstack_sched_params* params,
                               const dstack_sim_params* sim, dstack_run_out* out);
+
+/* The ideal spatio-temporal schedule of Sec. 7 (Eqs. maximization and
+ * constraints): time slots of slot_us, kernel granularity, preemption.
+ * Model i runs forwards of n_kernels kernels in order, kernel k at its own
+ * knee share slots[k] (1..total) for dur_us[k] >= 1 us, batch items each;
+ * closed loop: the next forward is released when one ends, due release +
+ * slo_us.  In every slot the eligible kernels are each model's current
+ * kernel; of all model subsets whose shares sum to at most total_slots the
+ * one with the largest sum runs (exhaustive), ties to the subset whose
+ * inclusion bits, taken in (deadline, index) order with the earliest first,
+ * form the largest number.  A running kernel's remaining time drops by
+ * slot_us; at or below 0 the model moves to its next kernel from the next
+ * slot on, and after its last kernel the forward ends at the slot's end
+ * (late if past its deadline).  Slots start at 0 while < horizon_us.
+ * utilisation_ppm = floor(1e6 * sum of used shares over slots / (total *
+ * slots)); hash = FNV-1a over (slot start, chosen subset bits) of every slot.
+ * n_models 1..8, horizon_us >= 1, slot_us >= 1, else E_INVALID. */
+typedef struct {
+  int n_kernels;
+  int batch;
+  const int* slots;
+  const int64_t* dur_us;
+  int64_t slo_us;
+} dstack_ideal_model;
+typedef struct {
+  int n_models;
+  int64_t items[DSTACK_MAX_MODELS];
+  int64_t forwards[DSTACK_MAX_MODELS];
+  int64_t late[DSTACK_MAX_MODELS];
+  int64_t busy_slot_us[DSTACK_MAX_MODELS];   /* share x slot length of every slot it ran in */
+  int64_t utilisation_ppm;
+  uint64_t hash;
+} dstack_ideal_out;
+dstack_status dstack_simulate_ideal(const dstack_ideal_model* models, int n_models, int64_t horizon_us, int64_t slot_us,
+                                    int total_slots, dstack_ideal_out* out);
 
 /* ------------------------------------------------------------------ */
 /* Live launcher (Sec. 6.1.2 on the GPU)                                */

@@ -376,16 +376,27 @@ def _nearest_rank(sorted_vals, pct):
 
 
 def simulate(models, period, duration, arrivals, total=TOTAL_SLOTS, overprov=OVERPROVISION_SLOTS, fod=True,
-             sessions_window=10, placement="lowest"):
+             sessions_window=10, placement="lowest", policy="dstack"):
     """models: as for schedule(); arrivals: per model sorted list of integer us in [0, duration).
-    Returns dict with per-model counters, utilisation_ppm and a hash of the job log."""
+    Returns dict with per-model counters, utilisation_ppm and a hash of the job log.
+
+    policy "dstack": the session plan plus the FOD fill (Sec. 6.1.2).  The
+    comparators of Sec. 7 run the same fill with no plan and another order
+    of the candidates (a reading: each is a non-preemptive greedy fill at the
+    model's deployed share and largest queued grid batch):
+    "maxthroughput" -- least runtime first (the model's SLO-optimal latency
+    at its deployed slots, then index), the schedule that favours the sum of
+    throughputs; "maxmin" -- smallest demand first (deployed slots, then
+    busy time, then index), max-min fairness over GPU% demands."""
     import collections
     import heapq
     choices, jobs, _, _ = schedule(models, period, total, overprov, placement)
     n = len(models)
     dep = [deployed_slots(c.slots, overprov, total) for c in choices]
     homes = home_offsets(dep, total) if placement == "home" else None
-    planned = [j for j in jobs if not j.missed]
+    planned = [j for j in jobs if not j.missed] if policy == "dstack" else []
+    if policy != "dstack":
+        fod = True
     # next planned start of each model after time t (over all periods)
     n_periods = ceil_div(duration, period)
 
@@ -449,7 +460,12 @@ def simulate(models, period, duration, arrivals, total=TOTAL_SLOTS, overprov=OVE
             return
         cands = [i for i in range(n) if i not in running and queue[i]]
         cur = t // period
-        cands.sort(key=lambda i: (sum(runs[i][s] for s in range(cur - sessions_window + 1, cur + 1)), busy[i], i))
+        if policy == "maxthroughput":
+            cands.sort(key=lambda i: (choices[i].latency, i))
+        elif policy == "maxmin":
+            cands.sort(key=lambda i: (dep[i], busy[i], i))
+        else:
+            cands.sort(key=lambda i: (sum(runs[i][s] for s in range(cur - sessions_window + 1, cur + 1)), busy[i], i))
         for i in cands:
             s = dep[i]
             if homes is not None:  # its own range, all of it free
@@ -511,3 +527,74 @@ def simulate(models, period, duration, arrivals, total=TOTAL_SLOTS, overprov=OVE
                         p50_us=_nearest_rank(L, 50), p99_us=_nearest_rank(L, 99), plan_skips=plan_skips[i]))
     return dict(models=out, utilisation_ppm=slot_us * 1000000 // (total * max(duration, 1)), job_hash=h,
                 last_end_us=last_end, log=log)
+
+
+def simulate_ideal(models, horizon, slot, total=TOTAL_SLOTS):
+    """The ideal spatio-temporal schedule of Sec. 7 (Eqs. maximization and
+    constraints), time-slotted at kernel granularity with preemption.
+
+    models: dicts with "slots" and "dur" (per kernel of one forward: its knee
+    share and its duration there, integer us), "batch" and "slo_us".  Closed
+    loop: a model's next forward is released when the previous one ends.
+    In every slot [t, t + slot) the eligible kernels are each model's current
+    kernel (its predecessors done: kernels of a model run in order); among
+    all subsets whose shares sum to at most `total`, the one with the largest
+    sum runs (exhaustive search), ties going to the subset that includes the
+    earliest-deadline models (the inclusion bits in (deadline, index) order,
+    read as a number, largest first).  A running kernel's remaining time
+    drops by the slot length; when it reaches 0 the model moves to its next
+    kernel in the next slot (the rest of the slot stays unused by it); after
+    the last kernel the forward completes at the slot's end (late if that
+    is past release + SLO).  Utilisation = sum over slots of the used shares
+    / (total x number of slots)."""
+    n = len(models)
+    k = [0] * n
+    rem = [models[i]["dur"][0] for i in range(n)]
+    release = [0] * n
+    deadline = [models[i]["slo_us"] for i in range(n)]
+    items = [0] * n
+    forwards = [0] * n
+    late = [0] * n
+    busy = [0] * n
+    used_sum = 0
+    n_slots = 0
+    h = FNV_OFFSET
+    t = 0
+    while t < horizon:
+        order = sorted(range(n), key=lambda i: (deadline[i], i))
+        best_key, best = None, 0
+        for sub in range(1 << n):
+            s = sum(models[i]["slots"][k[i]] for i in range(n) if (sub >> i) & 1)
+            if s > total:
+                continue
+            bits = 0
+            for i in order:
+                bits = (bits << 1) | ((sub >> i) & 1)
+            key = (s, bits)
+            if best_key is None or key > best_key:
+                best_key, best = key, sub
+        used_sum += best_key[0]
+        n_slots += 1
+        h = _fnv(h, t)
+        h = _fnv(h, best)
+        end = t + slot
+        for i in range(n):
+            if not (best >> i) & 1:
+                continue
+            busy[i] += models[i]["slots"][k[i]] * slot
+            rem[i] -= slot
+            if rem[i] <= 0:
+                k[i] += 1
+                if k[i] == len(models[i]["dur"]):
+                    forwards[i] += 1
+                    items[i] += models[i]["batch"]
+                    if end > deadline[i]:
+                        late[i] += 1
+                    k[i] = 0
+                    release[i] = end
+                    deadline[i] = end + models[i]["slo_us"]
+                rem[i] = models[i]["dur"][k[i]]
+        t = end
+    return dict(items=items, forwards=forwards, late=late, busy_slot_us=busy,
+                utilisation_ppm=used_sum * 1000000 // (total * max(n_slots, 1)), hash=h)
+

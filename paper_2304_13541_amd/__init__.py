@@ -102,7 +102,19 @@ class ScheduleOut(ctypes.Structure):
 
 class SimParams(ctypes.Structure):
     _fields_ = [("duration_us", ctypes.c_int64), ("fod", ctypes.c_int), ("sessions_window", ctypes.c_int),
-                ("arrivals_us", ctypes.POINTER(ctypes.c_int64) * MAX_MODELS), ("n_arrivals", ctypes.c_int * MAX_MODELS)]
+                ("arrivals_us", ctypes.POINTER(ctypes.c_int64) * MAX_MODELS), ("n_arrivals", ctypes.c_int * MAX_MODELS),
+                ("policy", ctypes.c_int)]
+
+
+class IdealModel(ctypes.Structure):
+    _fields_ = [("n_kernels", ctypes.c_int), ("batch", ctypes.c_int), ("slots", ctypes.POINTER(ctypes.c_int)),
+                ("dur_us", ctypes.POINTER(ctypes.c_int64)), ("slo_us", ctypes.c_int64)]
+
+
+class IdealOut(ctypes.Structure):
+    _fields_ = [("n_models", ctypes.c_int)] + [(n, ctypes.c_int64 * MAX_MODELS) for n in
+                                               ("items", "forwards", "late", "busy_slot_us")] + \
+               [("utilisation_ppm", ctypes.c_int64), ("hash", ctypes.c_uint64)]
 
 
 class ModelStats(ctypes.Structure):
@@ -150,6 +162,8 @@ _SIGS = {
     "dstack_schedule": ([ctypes.POINTER(SchedModel), _i, ctypes.POINTER(SchedParams), ctypes.POINTER(ScheduleOut)], _i),
     "dstack_simulate": ([ctypes.POINTER(SchedModel), _i, ctypes.POINTER(SchedParams), ctypes.POINTER(SimParams),
                          ctypes.POINTER(RunOut)], _i),
+    "dstack_simulate_ideal": ([ctypes.POINTER(IdealModel), _i, ctypes.c_int64, ctypes.c_int64, _i,
+                               ctypes.POINTER(IdealOut)], _i),
     "dstack_knee_search_table": ([_i, ctypes.POINTER(_i), ctypes.POINTER(ctypes.c_int64), _i, _i, _i, _i,
                                   ctypes.POINTER(KneeSearchResult)], _i),
     "dstack_knee_search": ([_vp, _i, ctypes.POINTER(_d), _i, _i, _i, _i, ctypes.POINTER(KneeSearchResult)], _i),
@@ -414,12 +428,16 @@ def _stats(out):
 PLACEMENTS = {"lowest": 0, "home": 1}
 
 
-def _sim_params(duration_us, arrivals, fod, sessions_window):
+POLICIES = {"dstack": 0, "maxthroughput": 1, "maxmin": 2}
+
+
+def _sim_params(duration_us, arrivals, fod, sessions_window, policy="dstack"):
     """SimParams plus the arrival buffers it points into (keep them alive)."""
     sp = SimParams()
     sp.duration_us = duration_us
     sp.fod = int(fod)
     sp.sessions_window = sessions_window
+    sp.policy = POLICIES[policy]
     keep = []
     for i, a in enumerate(arrivals):
         buf = (ctypes.c_int64 * max(1, len(a)))(*a)
@@ -430,16 +448,35 @@ def _sim_params(duration_us, arrivals, fod, sessions_window):
 
 
 def simulate(models, period_us, duration_us, arrivals, total_slots=TOTAL_SLOTS, overprov_slots=2, fod=True,
-             sessions_window=10, placement="lowest"):
-    """Launcher simulation on the timing table (see dstack_simulate).
-    arrivals: per model sorted integer-us arrival times.  Returns a dict."""
+             sessions_window=10, placement="lowest", policy="dstack"):
+    """Launcher simulation on the timing table (see dstack_simulate); policy
+    "dstack", "maxthroughput" or "maxmin".  arrivals: per model sorted
+    integer-us arrival times.  Returns a dict."""
     arr = _sched_models(models)
-    sp, keep = _sim_params(duration_us, arrivals, fod, sessions_window)
+    sp, keep = _sim_params(duration_us, arrivals, fod, sessions_window, policy)
     out = RunOut()
     prm = SchedParams(period_us, total_slots, overprov_slots, PLACEMENTS[placement])
     _check(lib().dstack_simulate(arr, len(models), ctypes.byref(prm), ctypes.byref(sp), ctypes.byref(out)))
     return dict(models=_stats(out), utilisation_ppm=out.utilisation_ppm, job_hash=out.job_hash,
                 last_end_us=out.last_end_us)
+
+
+def simulate_ideal(models, horizon_us, slot_us, total_slots=TOTAL_SLOTS):
+    """The ideal slotted, preemptive, kernel-granularity schedule (see
+    dstack_simulate_ideal).  models: dicts with per-kernel "slots" and "dur"
+    lists, "batch" and "slo_us"."""
+    n = len(models)
+    keep = []
+    arr = (IdealModel * n)()
+    for i, m in enumerate(models):
+        sl = (_i * len(m["slots"]))(*m["slots"])
+        du = (ctypes.c_int64 * len(m["dur"]))(*m["dur"])
+        keep += [sl, du]
+        arr[i] = IdealModel(len(m["dur"]), m["batch"], sl, du, m["slo_us"])
+    out = IdealOut()
+    _check(lib().dstack_simulate_ideal(arr, n, horizon_us, slot_us, total_slots, ctypes.byref(out)))
+    return dict(items=list(out.items[:n]), forwards=list(out.forwards[:n]), late=list(out.late[:n]),
+                busy_slot_us=list(out.busy_slot_us[:n]), utilisation_ppm=out.utilisation_ppm, hash=out.hash)
 
 
 def serve(handles, tables, inputs, outputs, period_us, duration_us, arrivals, total_slots=TOTAL_SLOTS,

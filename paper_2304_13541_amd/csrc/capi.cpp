@@ -693,6 +693,11 @@ dstack_status dstack_simulate(const dstack_sched_model* models, int n, const dst
   return guarded([&] { return simulate(models, n, prm, sim, out); });
 }
 
+dstack_status dstack_simulate_ideal(const dstack_ideal_model* models, int n, int64_t horizon_us, int64_t slot_us,
+                                    int total_slots, dstack_ideal_out* out) {
+  return guarded([&] { return simulate_ideal(models, n, horizon_us, slot_us, total_slots, out); });
+}
+
 dstack_status dstack_serve(const dstack_model* models, int n, const void* const* d_in, void* const* d_out,
                            const dstack_sched_model* tables, const dstack_sched_params* prm,
                            const dstack_sim_params* sim, dstack_run_out* out, dstack_job_record* log,

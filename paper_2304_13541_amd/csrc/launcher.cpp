@@ -71,7 +71,7 @@ int64_t nearest_rank(std::vector<int64_t>& v, int pct) {
 }
 
 bool check_trace(int n, const dstack_sim_params* sim) {
-  if (sim->duration_us <= 0 || sim->sessions_window < 1) return false;
+  if (sim->duration_us <= 0 || sim->sessions_window < 1 || sim->policy < 0 || sim->policy > 2) return false;
   for (int i = 0; i < n; ++i) {
     if (sim->n_arrivals[i] < 0 || (sim->n_arrivals[i] > 0 && !sim->arrivals_us[i])) return false;
     for (int k = 0; k < sim->n_arrivals[i]; ++k) {
@@ -86,7 +86,7 @@ LaunchState::LaunchState(const dstack_sched_model* models, int n, const dstack_s
                          const dstack_sim_params* sim, const dstack_schedule_out* plan)
     : models_(models), n_(n), prm_(prm), sim_(sim), plan_(plan), T_(prm->period_us), D_(sim->duration_us),
       queue_(n), running_(n, 0), run_mask_(n, 0), runs_(n), busy_(n, 0) {
-  const int64_t n_periods = (D_ + T_ - 1) / T_;
+  const int64_t n_periods = sim->policy == 0 ? (D_ + T_ - 1) / T_ : 0;  // the comparators run no plan
   for (int64_t p = 0; p < n_periods; ++p)
     for (int j = 0; j < plan->n_jobs; ++j) {
       const dstack_job& job = plan->jobs[j];
@@ -124,6 +124,16 @@ bool LaunchState::fod_pick(int64_t t, Pick* out) const {
     return r;
   };
   std::stable_sort(cands.begin(), cands.end(), [&](int a, int b) {
+    if (sim_->policy == 1) {  // least runtime first
+      if (plan_->latency_us[a] != plan_->latency_us[b]) return plan_->latency_us[a] < plan_->latency_us[b];
+      return a < b;
+    }
+    if (sim_->policy == 2) {  // smallest GPU% demand first
+      if (plan_->deployed_slots[a] != plan_->deployed_slots[b])
+        return plan_->deployed_slots[a] < plan_->deployed_slots[b];
+      if (busy_[a] != busy_[b]) return busy_[a] < busy_[b];
+      return a < b;
+    }
     int64_t ra = recent(a), rb = recent(b);
     if (ra != rb) return ra < rb;
     if (busy_[a] != busy_[b]) return busy_[a] < busy_[b];
@@ -194,7 +204,7 @@ dstack_status simulate(const dstack_sched_model* models, int n, const dstack_sch
   DS_CHECK(sim && out && prm, DSTACK_E_INVALID, "simulate: null pointer");
   DS_CHECK(n >= 1 && n <= DSTACK_MAX_MODELS, DSTACK_E_INVALID, "simulate: bad model count");
   DS_CHECK(check_trace(n, sim), DSTACK_E_INVALID,
-           "simulate: bad trace (duration > 0, window >= 1, arrivals sorted inside [0, duration))");
+           "simulate: bad trace (duration > 0, window >= 1, policy 0..2, arrivals sorted inside [0, duration))");
   std::vector<dstack_schedule_out> plan_box(1);
   dstack_schedule_out* plan = &plan_box[0];
   dstack_status st = schedule(models, n, prm, plan);
@@ -225,7 +235,7 @@ dstack_status simulate(const dstack_sched_model* models, int n, const dstack_sch
   };
   auto fod_pass = [&](int64_t t) {
     LaunchState::Pick pk;
-    if (sim->fod && ls.fod_pick(t, &pk)) launch(t, pk.model, pk.mask, pk.latency, pk.batch, 1);
+    if ((sim->fod || sim->policy != 0) && ls.fod_pick(t, &pk)) launch(t, pk.model, pk.mask, pk.latency, pk.batch, 1);
   };
 
   while (!ev.empty()) {
@@ -268,6 +278,88 @@ dstack_status simulate(const dstack_sched_model* models, int n, const dstack_sch
   out->utilisation_ppm = (int64_t)((unsigned __int128)slot_us * 1000000 / ((unsigned __int128)total * (uint64_t)D));
   out->job_hash = h;
   out->last_end_us = last_end;
+  return DSTACK_OK;
+}
+
+// The ideal spatio-temporal schedule of Sec. 7 (Eqs. maximization and
+// constraints): slotted, kernel granularity, preemptive; every slot runs the
+// subset of the models' current kernels with the largest summed share that
+// fits, found by exhaustive search (2^n subsets, n <= 8).
+dstack_status simulate_ideal(const dstack_ideal_model* models, int n, int64_t horizon, int64_t slot, int total,
+                             dstack_ideal_out* out) {
+  DS_CHECK(models && out, DSTACK_E_INVALID, "simulate_ideal: null pointer");
+  DS_CHECK(n >= 1 && n <= 8 && horizon >= 1 && slot >= 1 && total >= 1 && total <= 64, DSTACK_E_INVALID,
+           "simulate_ideal: 1..8 models, horizon >= 1, slot >= 1, total 1..64");
+  for (int i = 0; i < n; ++i) {
+    const dstack_ideal_model& m = models[i];
+    DS_CHECK(m.n_kernels >= 1 && m.slots && m.dur_us && m.batch >= 1 && m.slo_us >= 1, DSTACK_E_INVALID,
+             "simulate_ideal: a model needs kernels, batch >= 1 and slo >= 1");
+    for (int k = 0; k < m.n_kernels; ++k)
+      DS_CHECK(m.slots[k] >= 1 && m.slots[k] <= total && m.dur_us[k] >= 1, DSTACK_E_INVALID,
+               "simulate_ideal: kernel shares 1..total and durations >= 1 us");
+  }
+  std::vector<int> k(n, 0);
+  std::vector<int64_t> rem(n), deadline(n), items(n, 0), fwd(n, 0), late(n, 0), busy(n, 0);
+  for (int i = 0; i < n; ++i) {
+    rem[i] = models[i].dur_us[0];
+    deadline[i] = models[i].slo_us;
+  }
+  int64_t used_sum = 0, n_slots = 0;
+  uint64_t h = kFnvOffset;
+  std::vector<int> order(n);
+  for (int64_t t = 0; t < horizon; t += slot) {
+    for (int i = 0; i < n; ++i) order[i] = i;
+    std::stable_sort(order.begin(), order.end(), [&](int a, int b) {
+      if (deadline[a] != deadline[b]) return deadline[a] < deadline[b];
+      return a < b;
+    });
+    int best = 0, best_sum = -1;
+    unsigned best_bits = 0;
+    for (int sub = 0; sub < (1 << n); ++sub) {
+      int s = 0;
+      for (int i = 0; i < n; ++i)
+        if ((sub >> i) & 1) s += models[i].slots[k[i]];
+      if (s > total) continue;
+      unsigned bits = 0;
+      for (int i : order) bits = (bits << 1) | ((sub >> i) & 1);
+      if (s > best_sum || (s == best_sum && bits > best_bits)) {
+        best_sum = s;
+        best_bits = bits;
+        best = sub;
+      }
+    }
+    used_sum += best_sum;
+    n_slots += 1;
+    h = fnv_mix(h, t);
+    h = fnv_mix(h, best);
+    const int64_t end = t + slot;
+    for (int i = 0; i < n; ++i) {
+      if (!((best >> i) & 1)) continue;
+      busy[i] += (int64_t)models[i].slots[k[i]] * slot;
+      rem[i] -= slot;
+      if (rem[i] <= 0) {
+        k[i] += 1;
+        if (k[i] == models[i].n_kernels) {
+          fwd[i] += 1;
+          items[i] += models[i].batch;
+          if (end > deadline[i]) late[i] += 1;
+          k[i] = 0;
+          deadline[i] = end + models[i].slo_us;
+        }
+        rem[i] = models[i].dur_us[k[i]];
+      }
+    }
+  }
+  std::memset(out, 0, sizeof(*out));
+  out->n_models = n;
+  for (int i = 0; i < n; ++i) {
+    out->items[i] = items[i];
+    out->forwards[i] = fwd[i];
+    out->late[i] = late[i];
+    out->busy_slot_us[i] = busy[i];
+  }
+  out->utilisation_ppm = used_sum * 1000000 / ((int64_t)total * std::max<int64_t>(n_slots, 1));
+  out->hash = h;
   return DSTACK_OK;
 }
 

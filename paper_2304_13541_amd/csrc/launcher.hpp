@@ -72,6 +72,9 @@ int64_t nearest_rank(std::vector<int64_t>& v, int pct);
 // duration > 0, window >= 1, each model's arrivals sorted inside [0, duration)
 bool check_trace(int n, const dstack_sim_params* sim);
 
+dstack_status simulate_ideal(const dstack_ideal_model* models, int n, int64_t horizon, int64_t slot, int total,
+                             dstack_ideal_out* out);
+
 dstack_status serve(const dstack_model* models, int n, const void* const* d_in, void* const* d_out,
                     const dstack_sched_model* tables, const dstack_sched_params* prm, const dstack_sim_params* sim,
                     dstack_run_out* out, dstack_job_record* log, int log_capacity, int* n_log);

@@ -63,6 +63,7 @@ dstack_status serve(const dstack_model* models, int n, const void* const* d_in, 
   DS_CHECK(prm->placement == 1, DSTACK_E_INVALID, "serve: placement must be 1 (home ranges)");
   DS_CHECK(log_capacity >= 0 && (log || log_capacity == 0), DSTACK_E_INVALID, "serve: bad log buffer");
   DS_CHECK(check_trace(n, sim), DSTACK_E_INVALID, "serve: bad trace (see dstack_simulate)");
+  DS_CHECK(sim->policy == 0, DSTACK_E_INVALID, "serve: runs the D-STACK policy only (policy 0)");
   for (int i = 0; i < n; ++i) {
     DS_CHECK(models[i] && d_in[i] && d_out[i], DSTACK_E_INVALID, "serve: null model or buffer");
     dstack_model_info q;

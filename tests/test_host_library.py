@@ -216,3 +216,24 @@ def test_knee_model_rejects_bad_arguments():
         ds.knee_model_eval([], [], [1], 0.0)                        # no kernels
     with pytest.raises(ds.DStackError):
         ds.knee_model_sequence(5, 0, 10)                            # b < 1
+
+
+def test_ideal_schedule_parity_random():
+    """dstack_simulate_ideal reproduces the oracle's slotted, preemptive
+    kernel-level schedule (every slot's chosen subset through the hash)."""
+    rnd = random.Random(91)
+    for trial in range(120):
+        n = rnd.randint(1, 6)
+        total = rnd.choice([8, 16, 32])
+        ms = []
+        for _ in range(n):
+            k = rnd.randint(1, 12)
+            ms.append(dict(slots=[rnd.randint(1, total) for _ in range(k)],
+                           dur=[rnd.randint(1, 400) for _ in range(k)],
+                           batch=rnd.choice([1, 8, 32]), slo_us=rnd.randint(50, 5000)))
+        horizon, slot = rnd.randint(1, 20000), rnd.choice([1, 7, 10, 100])
+        assert ds.simulate_ideal(ms, horizon, slot, total) == sched.simulate_ideal(ms, horizon, slot, total), trial
+    with pytest.raises(ds.DStackError):
+        ds.simulate_ideal([dict(slots=[40], dur=[5], batch=1, slo_us=10)], 100, 10)   # share above the total
+    with pytest.raises(ds.DStackError):
+        ds.simulate_ideal([dict(slots=[4], dur=[0], batch=1, slo_us=10)], 100, 10)    # zero duration

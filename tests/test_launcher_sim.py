@@ -1,8 +1,10 @@
-"""Launcher simulation (Sec. 6.1.2 FOD fill on the session plan): the library's
+"""Launcher simulation (Sec. 6.1.2 FOD fill on the session plan) and the
+comparator schedulers of Sec. 7 (max-throughput, max-min fair): the library's
 dstack_simulate against the scheduler oracle's simulate(), bit-exact, on
 random timing tables and Poisson traces and on the four-model workload shape
 (ResNet-50, MobileNetV2, VGG-19, LSTM at 400/800/150/300 req/s, SLOs
-25/15/50/30 ms, 100 ms sessions, 10 s)."""
+25/15/50/30 ms, 100 ms sessions, 10 s); the comparators' orders pinned on
+two-model cases whose outcome follows by hand."""
 import random
 
 import pytest
@@ -18,9 +20,9 @@ def amdahl(a, c, batches, slots=SWEEP):
     return {b: {s: int(a * (1 + 0.05 * b) + c * b / s) for s in slots} for b in batches}
 
 
-def compare(models, period, duration, arrivals, total=32, overprov=2, fod=True, placement="lowest"):
-    got = ds.simulate(models, period, duration, arrivals, total, overprov, fod, placement=placement)
-    ref = sched.simulate(models, period, duration, arrivals, total, overprov, fod, placement=placement)
+def compare(models, period, duration, arrivals, total=32, overprov=2, fod=True, placement="lowest", policy="dstack"):
+    got = ds.simulate(models, period, duration, arrivals, total, overprov, fod, placement=placement, policy=policy)
+    ref = sched.simulate(models, period, duration, arrivals, total, overprov, fod, placement=placement, policy=policy)
     assert got["models"] == ref["models"]
     assert got["utilisation_ppm"] == ref["utilisation_ppm"]
     assert got["last_end_us"] == ref["last_end_us"]
@@ -117,3 +119,61 @@ def test_simulation_invariants():
                 assert acc & j[3] == 0
                 acc |= j[3]
             assert len({j[2] for j in act}) == len(act)
+
+
+@pytest.mark.parametrize("policy", ["maxthroughput", "maxmin"])
+@pytest.mark.parametrize("scale", [1, 8])
+def test_comparator_policies_parity(policy, scale):
+    models, arrivals = four_model_mix(scale=scale)
+    got = compare(models, 100000, 10_000_000, arrivals, policy=policy)
+    assert all(m["planned_runs"] == 0 for m in got["models"])  # no plan
+
+
+def test_comparator_policies_random_parity():
+    rnd = random.Random(11)
+    for trial in range(40):
+        n = rnd.randint(1, 4)
+        models, arrivals = [], []
+        for i in range(n):
+            batches = sorted(rnd.sample([1, 2, 4, 8, 16, 32], rnd.randint(1, 4)))
+            tab = amdahl(rnd.randint(100, 3000), rnd.randint(500, 40000), batches,
+                         sorted(rnd.sample(range(1, 33), rnd.randint(2, 8))))
+            models.append(dict(slo_us=rnd.choice([10000, 25000, 50000]), max_batch=rnd.choice([4, 16, 32]),
+                               rate_per_s=rnd.choice([0, 200, 800]), table=tab))
+            arrivals.append(poisson_arrivals(500 + trial * 10 + i, rnd.choice([50, 300, 1500]), 1_000_000))
+        compare(models, 100000, 1_000_000, arrivals, overprov=rnd.choice([0, 2]),
+                placement=rnd.choice(["lowest", "home"]), policy=rnd.choice(["maxthroughput", "maxmin"]))
+
+
+def two_models(slots_a, lat_a, slots_b, lat_b):
+    """Two models that are always queued, each with one batch size and one
+    swept share (so its knee and deployed share are that share)."""
+    models = [dict(slo_us=100000, max_batch=1, table={1: {slots_a: lat_a}}),
+              dict(slo_us=100000, max_batch=1, table={1: {slots_b: lat_b}})]
+    dense = [list(range(0, 200000, 50)) for _ in range(2)]
+    return models, dense
+
+
+def test_max_throughput_starves_the_slower_model():
+    # shares 20 + 20 > 32: one at a time.  Model 0's arrival at t = 0 comes
+    # first and it starts alone ([0, 900)); from then on the shorter runtime
+    # always wins: model 1 starts at 900 + 500 k < 200000, 399 times
+    models, dense = two_models(20, 900, 20, 500)
+    got = compare(models, 100000, 200000, dense, overprov=0, policy="maxthroughput")
+    assert got["models"][0]["served"] == 1
+    assert got["models"][1]["served"] == 399
+
+
+def test_max_min_runs_the_smallest_demand_first():
+    # shares 24 + 12 > 32: model 0 starts alone at t = 0 ([0, 400)); from then
+    # on the 12-slot model always goes first: 400 + 700 k < 200000, 286 times
+    models, dense = two_models(24, 400, 12, 700)
+    got = compare(models, 100000, 200000, dense, overprov=0, policy="maxmin")
+    assert got["models"][0]["served"] == 1
+    assert got["models"][1]["served"] == 286
+
+
+def test_dstack_shares_where_the_comparators_starve():
+    models, dense = two_models(20, 900, 20, 500)
+    got = compare(models, 100000, 200000, dense, overprov=0)
+    assert got["models"][0]["served"] > 0 and got["models"][1]["served"] > 0

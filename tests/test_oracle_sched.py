@@ -311,3 +311,37 @@ def test_knee_search_hand_cases():
     # a start below every candidate begins at the first
     k, probes = sched.knee_search(lambda s: 1000, 1, GRID, 1)
     assert probes[0][0] == 3 and k == 3
+
+
+def test_ideal_single_model_closed_form():
+    # kernels (32 slots, 30 us), (16 slots, 10 us) in 10 us slots: 4 slots per
+    # forward, 3 x 32 + 16 = 112 of 128 share-slots used
+    m = dict(slots=[32, 16], dur=[30, 10], batch=8, slo_us=10**9)
+    r = sched.simulate_ideal([m], 1000, 10)
+    assert r["forwards"] == [25] and r["items"] == [200] and r["late"] == [0]
+    assert r["utilisation_ppm"] == 875000
+    assert r["busy_slot_us"] == [25 * (3 * 32 + 16) * 10]
+
+
+def test_ideal_models_that_fit_together_run_as_alone():
+    a = dict(slots=[16, 16], dur=[20, 40], batch=1, slo_us=10**9)
+    r = sched.simulate_ideal([a, dict(a)], 1200, 10)
+    assert r["forwards"] == [20, 20] and r["utilisation_ppm"] == 1000000
+
+
+def test_ideal_largest_fitting_sum():
+    # shares 10, 12, 22 of 32: {10, 22} fills the GPU, 12 waits
+    ms = [dict(slots=[s], dur=[1000], batch=1, slo_us=10**9) for s in (10, 12, 22)]
+    r = sched.simulate_ideal(ms, 10, 10)
+    assert r["busy_slot_us"] == [100, 0, 220] and r["utilisation_ppm"] == 1000000
+
+
+def test_ideal_ties_go_to_the_earliest_deadline():
+    # two 20-slot models (never together), one 20 us kernel each, 10 us slots,
+    # SLOs 100 and 50 us: by hand, model 1 runs [0, 60) (deadlines 50, 70, 90
+    # against 100), model 0 [60, 80), model 1 again from 80 (deadline 110 < 180)
+    ms = [dict(slots=[20], dur=[20], batch=1, slo_us=100), dict(slots=[20], dur=[20], batch=1, slo_us=50)]
+    r = sched.simulate_ideal(ms, 80, 10)
+    assert r["forwards"] == [1, 3] and r["late"] == [0, 0]
+    r = sched.simulate_ideal(ms, 100, 10)
+    assert r["forwards"] == [1, 4]
