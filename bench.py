@@ -472,9 +472,10 @@ def config5(ds, torch, models4, tables4, args):
                 capacity_seconds=args.capacity_seconds)
 
 
-def comparators(ds, tables4, k=8, seconds=2.0):
+def comparators(ds, tables4, k=32, seconds=2.0):
     """Sec. 7's comparators in simulate mode on the four-model mix's measured
-    timing tables at k x the stated rates (past the 1% capacity): D-STACK
+    timing tables at k x the stated rates (far past the 1% capacity, so that
+    every policy is bound by the GPU): D-STACK
     (plan + FOD), max-throughput (least runtime first) and max-min fair
     (smallest GPU% demand first), all non-preemptive on the lowest free
     slots.  Per model: served/s and GPU busy time."""
