@@ -5,7 +5,8 @@ the CPU-baseline leg of ``bench.py`` may import this package.  It shares no
 code with the HIP library and never imports it.
 
 * ``oracle_numerics.c`` -- fp64 forward passes (direct convolution, naive
-  products, LSTM), built here with gcc into ``liboracle.so``.
+  products, LSTM, layer norm and attention for the BERT encoder), built here
+  with gcc into ``liboracle.so``.
 * ``sched.py`` -- the scheduling decisions (knee, SLO-constrained batch
   optimisation, spatio-temporal session plan, utilisation) in integer Python.
 * ``knee_model.py`` -- the analytical DNN latency model of Sec. 4.2 and its
@@ -60,6 +61,9 @@ def lib():
         L.oracle_maxpool.argtypes = [dp, i, i, i, i, i, i, i, dp]
         L.oracle_avgpool.argtypes = [dp, i, i, i, i, dp]
         L.oracle_lstm_layer.argtypes = [dp, i, i, i, i, dp, dp, dp, dp, i, dp, dp]
+        L.oracle_layernorm.argtypes = [dp, ctypes.c_long, i, dp, dp, ctypes.c_double, dp]
+        L.oracle_attention.argtypes = [dp, i, i, i, i, dp]
+        L.oracle_bert_forward.argtypes = [ctypes.c_void_p, i, ctypes.c_void_p, i, dp]
         _lib = L
     return _lib
 
@@ -154,10 +158,31 @@ def lstm_layer(x, w_ih, w_hh, b_ih, b_hh, round_h=False):
     return h, c
 
 
+def layernorm(x, gamma, beta, eps):
+    """Rows of x [..., C] normalised by their mean and biased variance, then * gamma + beta."""
+    x = _f64(x)
+    C = x.shape[-1]
+    rows = x.size // C
+    y = np.empty_like(x)
+    lib().oracle_layernorm(_dp(x), rows, C, _dp(_f64(gamma)), _dp(_f64(beta)), float(eps), _dp(y))
+    return y
+
+
+def attention(qkv, heads):
+    """qkv [B,T,3*Hm] (queries, keys, values) -> softmax(q k^T / sqrt(dh)) v per head, [B,T,Hm]."""
+    qkv = _f64(qkv)
+    B, T, H3 = qkv.shape
+    Hm = H3 // 3
+    out = np.empty((B, T, Hm))
+    lib().oracle_attention(_dp(qkv), B, T, heads, Hm // heads, _dp(out))
+    return out
+
+
 # ------------------------------------------------------------ models ----
 
-ARCHS = ("tinycnn", "resnet50", "mobilenetv2", "vgg19", "lstm2")
-NUM_CLASSES = {"tinycnn": 10, "resnet50": 1000, "mobilenetv2": 1000, "vgg19": 1000}
+ARCHS = ("tinycnn", "resnet50", "mobilenetv2", "vgg19", "lstm2", "bert", "bert_long")
+NUM_CLASSES = {"tinycnn": 10, "resnet50": 1000, "mobilenetv2": 1000, "vgg19": 1000, "bert": 2, "bert_long": 2}
+BERT_TOKENS = {"bert": 20, "bert_long": 40}
 
 
 class Model:
@@ -193,7 +218,15 @@ class Model:
         assert lib().oracle_model_set_tensor(self.h, i, _dp(v)) == 0
 
     def forward(self, x_bits, parity=True):
-        """x_bits: bf16 bit patterns. CNN [n,H,W,3] -> [n,classes]; LSTM [50,n,512] -> [50,n,1024]."""
+        """x_bits: bf16 bit patterns. CNN [n,H,W,3] -> [n,classes]; LSTM [50,n,512] -> [50,n,1024];
+        BERT: int32 token ids [n,T] -> [n,2]."""
+        if self.arch in BERT_TOKENS:
+            ids = np.ascontiguousarray(x_bits, dtype=np.int32)
+            n = ids.shape[0]
+            assert ids.shape == (n, BERT_TOKENS[self.arch])
+            out = np.empty((n, 2))
+            assert lib().oracle_bert_forward(self.h, n, ids.ctypes.data, int(parity), _dp(out)) == 0
+            return out
         x_bits = np.ascontiguousarray(x_bits, dtype=np.uint16)
         if self.arch == "lstm2":
             T, n, _ = x_bits.shape

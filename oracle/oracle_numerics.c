@@ -8,9 +8,11 @@
  * What it computes: the plain definition of each network's forward pass in
  * fp64 -- direct cross-correlation convolution, depthwise convolution, naive
  * matrix products, max/average pooling, inference-mode batch norm, ReLU /
- * ReLU6 and the LSTM cell -- over the five architectures the paper evaluates
- * or the workloads name: a tiny 4-conv CNN, ResNet-50 (v1.5), MobileNetV2,
- * VGG-19 and a 2-layer LSTM.  The paper itself runs stock framework kernels
+ * ReLU6 and the LSTM cell, and for the transformer layer normalisation,
+ * scaled dot-product self-attention with a softmax, GELU and tanh -- over
+ * the architectures the paper evaluates or the workloads name: a tiny 4-conv
+ * CNN, ResNet-50 (v1.5), MobileNetV2, VGG-19, a 2-layer LSTM and a
+ * BERT-base encoder (Sec. 4.4's transformer, 10- and 20-word sentences).  The paper itself runs stock framework kernels
  * (Sec. 3, Sec. 4.1 and its A.int table); the layers' mathematics is the
  * textbook one, written out here loop by loop.
  *
@@ -265,11 +267,64 @@ void oracle_lstm_layer(const double* x, int T, int B, int I, int Hd, const doubl
   free(g);
 }
 
+/* Layer normalisation of each of `rows` rows of C values:
+ * y = (x - mean) / sqrt(var + eps) * gamma + beta, mean and (biased)
+ * variance over the row. */
+void oracle_layernorm(const double* x, long rows, int C, const double* gamma, const double* beta, double eps,
+                      double* y) {
+  for (long r = 0; r < rows; ++r) {
+    const double* xr = x + r * C;
+    double mean = 0.0;
+    for (int c = 0; c < C; ++c) mean += xr[c];
+    mean /= C;
+    double var = 0.0;
+    for (int c = 0; c < C; ++c) var += (xr[c] - mean) * (xr[c] - mean);
+    var /= C;
+    const double inv = 1.0 / sqrt(var + eps);
+    for (int c = 0; c < C; ++c) y[r * C + c] = (xr[c] - mean) * inv * gamma[c] + beta[c];
+  }
+}
+
+/* Multi-head self-attention core of one batch of B sequences of T tokens:
+ * qkv [B][T][3*Hm] holds per token the queries, keys and values (each Hm =
+ * heads * dh wide, head h at columns h*dh..); for every sequence and head,
+ * s[i][j] = q_i . k_j / sqrt(dh), p = softmax over j, o_i = sum_j p[i][j] v_j
+ * written to out [B][T][Hm] at the head's columns.  No mask. */
+void oracle_attention(const double* qkv, int B, int T, int heads, int dh, double* out) {
+  const int Hm = heads * dh;
+  double* s = malloc(sizeof(double) * (size_t)T);
+  for (int b = 0; b < B; ++b)
+    for (int h = 0; h < heads; ++h)
+      for (int i = 0; i < T; ++i) {
+        const double* q = qkv + ((long)b * T + i) * 3 * Hm + h * dh;
+        double mx = -INFINITY;
+        for (int j = 0; j < T; ++j) {
+          const double* k = qkv + ((long)b * T + j) * 3 * Hm + Hm + h * dh;
+          double d = 0.0;
+          for (int e = 0; e < dh; ++e) d += q[e] * k[e];
+          s[j] = d / sqrt((double)dh);
+          if (s[j] > mx) mx = s[j];
+        }
+        double sum = 0.0;
+        for (int j = 0; j < T; ++j) {
+          s[j] = exp(s[j] - mx);
+          sum += s[j];
+        }
+        double* o = out + ((long)b * T + i) * Hm + h * dh;
+        for (int e = 0; e < dh; ++e) {
+          double a = 0.0;
+          for (int j = 0; j < T; ++j) a += s[j] / sum * qkv[((long)b * T + j) * 3 * Hm + 2 * Hm + h * dh + e];
+          o[e] = a;
+        }
+      }
+  free(s);
+}
+
 /* ------------------------------------------------------------------ */
 /* models                                                              */
 /* ------------------------------------------------------------------ */
 
-enum { ARCH_TINY = 0, ARCH_R50 = 1, ARCH_MBV2 = 2, ARCH_VGG = 3, ARCH_LSTM = 4 };
+enum { ARCH_TINY = 0, ARCH_R50 = 1, ARCH_MBV2 = 2, ARCH_VGG = 3, ARCH_LSTM = 4, ARCH_BERT = 5, ARCH_BERT_LONG = 6 };
 enum { DIST_HE = 0, DIST_ZERO = 1, DIST_UNIF = 2 };
 
 typedef struct {
@@ -316,6 +371,13 @@ static const int MBV2_CFG[7][4] = {{1, 16, 1, 1}, {6, 24, 2, 2}, {6, 32, 3, 2}, 
 /* VGG-19 conv channels per stage (4 stages of 2/2/4/4/4 convs) */
 static const int VGG_STAGE_CONVS[5] = {2, 2, 4, 4, 4};
 static const int VGG_STAGE_CH[5] = {64, 128, 256, 512, 512};
+/* BERT-base: 12 layers, width 768, 12 heads of 64, feed-forward 3072,
+ * WordPiece vocabulary 30522, 512 positions, 2 token types, 2 classes.
+ * Weights and biases N(0, 0.02^2) (the normal rule with fan-in 5000:
+ * sqrt(2 / 5000) = 0.02); layer-norm gain 1 and bias 0 (constants, like the
+ * CNNs' BN statistics); eps 1e-12. */
+enum { BERT_L = 12, BERT_H = 768, BERT_HEADS = 12, BERT_DH = 64, BERT_FF = 3072, BERT_VOCAB = 30522,
+       BERT_POS = 512, BERT_CLASSES = 2, BERT_FAN = 5000 };
 
 static void build_tensors(model_t* m) {
   switch (m->arch) {
@@ -389,6 +451,27 @@ static void build_tensors(model_t* m) {
       }
       break;
     }
+    case ARCH_BERT:
+    case ARCH_BERT_LONG: {
+      add_tensor(m, (long)BERT_VOCAB * BERT_H, DIST_HE, BERT_FAN); /* word embeddings */
+      add_tensor(m, (long)BERT_POS * BERT_H, DIST_HE, BERT_FAN);   /* position embeddings */
+      add_tensor(m, 2L * BERT_H, DIST_HE, BERT_FAN);               /* token-type embeddings */
+      for (int l = 0; l < BERT_L; ++l) {
+        add_tensor(m, 3L * BERT_H * BERT_H, DIST_HE, BERT_FAN); /* W_qkv [3H][H] (q, k, v rows) */
+        add_tensor(m, 3L * BERT_H, DIST_HE, BERT_FAN);
+        add_tensor(m, (long)BERT_H * BERT_H, DIST_HE, BERT_FAN); /* attention output */
+        add_tensor(m, BERT_H, DIST_HE, BERT_FAN);
+        add_tensor(m, (long)BERT_FF * BERT_H, DIST_HE, BERT_FAN); /* feed-forward in */
+        add_tensor(m, BERT_FF, DIST_HE, BERT_FAN);
+        add_tensor(m, (long)BERT_H * BERT_FF, DIST_HE, BERT_FAN); /* feed-forward out */
+        add_tensor(m, BERT_H, DIST_HE, BERT_FAN);
+      }
+      add_tensor(m, (long)BERT_H * BERT_H, DIST_HE, BERT_FAN); /* pooler */
+      add_tensor(m, BERT_H, DIST_HE, BERT_FAN);
+      add_tensor(m, (long)BERT_CLASSES * BERT_H, DIST_HE, BERT_FAN); /* classifier */
+      add_tensor(m, BERT_CLASSES, DIST_HE, BERT_FAN);
+      break;
+    }
   }
 }
 
@@ -398,6 +481,8 @@ static int arch_id(const char* a) {
   if (!strcmp(a, "mobilenetv2")) return ARCH_MBV2;
   if (!strcmp(a, "vgg19")) return ARCH_VGG;
   if (!strcmp(a, "lstm2")) return ARCH_LSTM;
+  if (!strcmp(a, "bert")) return ARCH_BERT;
+  if (!strcmp(a, "bert_long")) return ARCH_BERT_LONG;
   return -1;
 }
 
@@ -644,10 +729,10 @@ static act_t forward_vgg(model_t* m, act_t x, int parity) {
 /* Forward pass of n_items independent samples.
  * CNN: in = [n][H][W][3] bf16 bits, out = [n][classes] fp64.
  * LSTM: in = [50][n][512] bf16 bits, out = [50][n][1024] fp64 (layer-2 h).
- * Returns 0, or -1 for an unknown model. */
+ * Returns 0, or -1 for an unknown model or a BERT (oracle_bert_forward). */
 int oracle_model_forward(void* h, int n, const uint16_t* in, int parity, double* out) {
   model_t* m = h;
-  if (!m) return -1;
+  if (!m || m->arch == ARCH_BERT || m->arch == ARCH_BERT_LONG) return -1; /* token input: oracle_bert_forward */
   m->cursor = 0;
   if (m->arch == ARCH_LSTM) {
     const int T = 50, I = 512, Hd = 1024;
@@ -676,5 +761,87 @@ int oracle_model_forward(void* h, int n, const uint16_t* in, int parity, double*
   memcpy(out, y.v, sizeof(double) * (size_t)act_numel(&y));
   act_free(&x);
   act_free(&y);
+  return 0;
+}
+
+/* ---- BERT encoder ---- */
+
+static double gelu(double v) { return 0.5 * v * (1.0 + erf(v / sqrt(2.0))); }
+
+/* y [rows][O] = x [rows][I] w^T + b (+ res) then act (0 none, 3 GELU, 4
+ * tanh), bf16 storage in parity mode */
+static void bert_linear(const double* x, long rows, int I, const double* w, const double* b, int O,
+                        const double* res, int act, int parity, double* y) {
+  oracle_fc(x, (int)rows, I, w, b, O, y);
+  for (long i = 0; i < rows * O; ++i) {
+    double v = y[i] + (res ? res[i] : 0.0);
+    if (act == 3) v = gelu(v);
+    if (act == 4) v = tanh(v);
+    y[i] = v;
+  }
+  round_all(y, rows * O, parity);
+}
+
+static void bert_ln(double* x, long rows, int parity) {
+  double* g = malloc(sizeof(double) * BERT_H);
+  double* z = calloc(BERT_H, sizeof(double));
+  for (int c = 0; c < BERT_H; ++c) g[c] = 1.0;
+  oracle_layernorm(x, rows, BERT_H, g, z, 1e-12, x);
+  round_all(x, rows * BERT_H, parity);
+  free(g);
+  free(z);
+}
+
+/* Forward pass of n sequences of T token ids (token type 0, no padding):
+ * embeddings (word + position + type) -> layer norm -> 12 post-norm encoder
+ * layers (self-attention + residual -> layer norm, GELU feed-forward +
+ * residual -> layer norm) -> pooler tanh(W_p h_[CLS] + b_p) -> classifier,
+ * out [n][2] fp64.  T is 20 for "bert" and 40 for "bert_long".  Returns 0,
+ * or -1 for a model that is not a BERT or an id outside the vocabulary. */
+int oracle_bert_forward(void* h, int n, const int32_t* ids, int parity, double* out) {
+  model_t* m = h;
+  if (!m || (m->arch != ARCH_BERT && m->arch != ARCH_BERT_LONG)) return -1;
+  const int T = m->arch == ARCH_BERT ? 20 : 40;
+  const long rows = (long)n * T;
+  for (long i = 0; i < rows; ++i)
+    if (ids[i] < 0 || ids[i] >= BERT_VOCAB) return -1;
+  m->cursor = 0;
+  const double *we = next_tensor(m), *pe = next_tensor(m), *te = next_tensor(m);
+  double* x = malloc(sizeof(double) * (size_t)rows * BERT_H);
+  for (long r = 0; r < rows; ++r) {
+    const int t = (int)(r % T);
+    for (int c = 0; c < BERT_H; ++c)
+      x[r * BERT_H + c] = we[(long)ids[r] * BERT_H + c] + pe[(long)t * BERT_H + c] + te[c];
+  }
+  bert_ln(x, rows, parity);
+  double* qkv = malloc(sizeof(double) * (size_t)rows * 3 * BERT_H);
+  double* att = malloc(sizeof(double) * (size_t)rows * BERT_H);
+  double* a = malloc(sizeof(double) * (size_t)rows * BERT_H);
+  double* f = malloc(sizeof(double) * (size_t)rows * BERT_FF);
+  for (int l = 0; l < BERT_L; ++l) {
+    const double *wqkv = next_tensor(m), *bqkv = next_tensor(m), *wo = next_tensor(m), *bo = next_tensor(m);
+    const double *w1 = next_tensor(m), *b1 = next_tensor(m), *w2 = next_tensor(m), *b2 = next_tensor(m);
+    bert_linear(x, rows, BERT_H, wqkv, bqkv, 3 * BERT_H, NULL, 0, parity, qkv);
+    oracle_attention(qkv, n, T, BERT_HEADS, BERT_DH, att);
+    round_all(att, rows * BERT_H, parity);
+    bert_linear(att, rows, BERT_H, wo, bo, BERT_H, x, 0, parity, a);
+    bert_ln(a, rows, parity);
+    bert_linear(a, rows, BERT_H, w1, b1, BERT_FF, NULL, 3, parity, f);
+    bert_linear(f, rows, BERT_FF, w2, b2, BERT_H, a, 0, parity, x);
+    bert_ln(x, rows, parity);
+  }
+  const double *wp = next_tensor(m), *bp = next_tensor(m), *wc = next_tensor(m), *bc = next_tensor(m);
+  double* cls = malloc(sizeof(double) * (size_t)n * BERT_H);
+  double* pooled = malloc(sizeof(double) * (size_t)n * BERT_H);
+  for (int b = 0; b < n; ++b) memcpy(cls + (long)b * BERT_H, x + (long)b * T * BERT_H, sizeof(double) * BERT_H);
+  bert_linear(cls, n, BERT_H, wp, bp, BERT_H, NULL, 4, parity, pooled);
+  oracle_fc(pooled, n, BERT_H, wc, bc, BERT_CLASSES, out);
+  free(x);
+  free(qkv);
+  free(att);
+  free(a);
+  free(f);
+  free(cls);
+  free(pooled);
   return 0;
 }
