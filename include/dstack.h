@@ -109,20 +109,29 @@ dstack_status dstack_probe_cu_ids(dstack_partition p, int n_blocks, int via_grap
  *   (ResNet block: conv1, conv2, conv3, downsample).  Logical layouts:
  *   conv [K][R][S][C], depthwise [C][3][3], FC [out][in], LSTM [4H][in]
  *   with gate order i, f, g, o.  BN layers have gamma 1, beta 0, mean 0,
- *   var 1, eps 1e-5 (folded into per-channel fp32 scale/shift). */
+ *   var 1, eps 1e-5 (folded into per-channel fp32 scale/shift).
+ *   "bert" / "bert_long": BERT-base encoders (Sec. 4.4's transformer) on 20
+ *   / 40 tokens, 2 classes: word [30522][768], position [512][768] and
+ *   type [2][768] embeddings, then per layer q|k|v [2304][768] + bias,
+ *   output [768][768] + bias, feed-forward [3072][768] + bias and
+ *   [768][3072] + bias, then pooler [768][768] + bias and classifier
+ *   [2][768] + bias; all N(0, 0.02^2) (the normal rule with fan-in 5000);
+ *   layer norms gain 1, bias 0, eps 1e-12. */
 typedef struct {
   char arch[16];
-  int is_lstm;              /* 0: image classifier, 1: sequence model */
+  int is_lstm;              /* 0: image classifier or transformer, 1: LSTM */
   int max_batch;            /* largest batch dstack_infer accepts */
   int in_h, in_w, in_c;     /* CNN: per-item input [H][W][C] bf16 NHWC */
   int seq_len, in_features; /* LSTM: input [T][batch][in_features] bf16 */
-  int out_features;         /* CNN: classes (fp32 logits); LSTM: hidden (fp32 h) */
+  int out_features;         /* CNN, transformer: classes (fp32 logits); LSTM: hidden (fp32 h) */
   int num_tensors;
   int64_t num_params;
   int num_kernels;          /* kernel launches per forward */
   double flops_per_item;    /* algorithmic FLOPs (2 per MAC) per inference */
   double mfma_flops_per_item; /* of which in MFMA convolution/GEMM kernels */
   double weight_bytes;      /* bf16 weights read per forward */
+  int input_tokens;         /* 1: transformer, input int32 token ids [batch][seq_len]
+                               (ids outside the vocabulary read its last row) */
 } dstack_model_info;
 
 dstack_status dstack_model_load(const char* arch, uint64_t seed, dstack_model* out);
@@ -526,6 +535,7 @@ dstack_status dstack_serve(const dstack_model* models, int n_models, const void*
  *
  * conv2d: y = act(scale[k] * sum_{r,s,c} x[n, ho*st-pad+r, wo*st-pad+s, c]
  *   * w[k,r,s,c] + shift[k] (+ res[n,ho,wo,k])), zero outside the image;
+ *   act 0 none, 1 ReLU, 2 ReLU6, 3 GELU (erf form), 4 tanh;
  *   C % 8 == 0 and K % 4 == 0 (else E_UNSUPPORTED); res may be NULL;
  *   out_fp32 selects an fp32 instead of bf16 output.
  * dwconv3x3: per-channel 3x3, pad 1, stride 1 or 2, w [3][3][C] (device
@@ -577,6 +587,25 @@ dstack_status dstack_op_avgpool(const void* x, int N, int H, int W, int C, void*
 size_t dstack_lstm_workspace_bytes(int T, int B, int H);
 dstack_status dstack_op_lstm_layer(const void* x, int T, int B, int I, int H, const void* w_ih, const void* w_hh,
                                    const float* bias, void* h_bf16, float* h_f32, void* workspace, void* stream);
+/* Transformer kernels (the BERT encoder of Sec. 4.4's transformer workload).
+ * embed_ln: for each of `rows` tokens (ids int32 [rows], position = row %
+ *   T, token type 0): e = we[id] + pe[row % T] + te[0] (tables bf16
+ *   [vocab][H], [>= T][H], [>= 1][H]), then layer norm y = (e - mean) /
+ *   sqrt(var + eps) * gamma + beta over the H values (biased variance; gamma
+ *   / beta fp32 [H] or NULL for 1 / 0), y bf16 [rows][H].  Ids outside
+ *   [0, vocab) read row vocab - 1.  H <= 2048 (else E_UNSUPPORTED).
+ * layernorm: the same normalisation of x bf16 [rows][H] into y bf16.
+ * attention: qkv bf16 [B][T][3 * heads * dh] (queries, keys, values, head h
+ *   at columns h*dh of each) -> out bf16 [B][T][heads * dh] with, per
+ *   sequence and head, out_i = sum_j softmax_j(q_i . k_j / sqrt(dh)) v_j
+ *   (no mask, fp32 arithmetic).  dh == 64 and T <= 48 (else
+ *   E_UNSUPPORTED). */
+dstack_status dstack_op_embed_ln(const int32_t* ids, int rows, int T, int vocab, const void* we, const void* pe,
+                                 const void* te, int H, const float* gamma, const float* beta, float eps, void* y,
+                                 void* stream);
+dstack_status dstack_op_layernorm(const void* x, int rows, int H, const float* gamma, const float* beta, float eps,
+                                  void* y, void* stream);
+dstack_status dstack_op_attention(const void* qkv, int B, int T, int heads, int dh, void* out, void* stream);
 
 #ifdef __cplusplus
 }

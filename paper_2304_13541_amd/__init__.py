@@ -17,8 +17,9 @@ OK, E_INVALID, E_UNSUPPORTED, E_HIP, E_OOM, E_INFEASIBLE, E_STATE = 0, -1, -2, -
 TOTAL_SLOTS = 32
 CUS_PER_SLOT = 8
 MAX_SWEEP, MAX_BATCHES, MAX_MODELS, MAX_JOBS = 32, 8, 16, 512
-ARCHS = ("tinycnn", "resnet50", "mobilenetv2", "vgg19", "lstm2")
-KIND_NAMES = {0: "mfma", 1: "depthwise", 2: "fc", 3: "lstm_step", 4: "glue", 5: "direct_conv", 6: "expand_dw"}
+ARCHS = ("tinycnn", "resnet50", "mobilenetv2", "vgg19", "lstm2", "bert", "bert_long")
+KIND_NAMES = {0: "mfma", 1: "depthwise", 2: "fc", 3: "lstm_step", 4: "glue", 5: "direct_conv", 6: "expand_dw",
+              7: "attention"}
 
 
 class DStackError(RuntimeError):
@@ -33,7 +34,7 @@ class ModelInfo(ctypes.Structure):
                 ("seq_len", ctypes.c_int), ("in_features", ctypes.c_int), ("out_features", ctypes.c_int),
                 ("num_tensors", ctypes.c_int), ("num_params", ctypes.c_int64), ("num_kernels", ctypes.c_int),
                 ("flops_per_item", ctypes.c_double), ("mfma_flops_per_item", ctypes.c_double),
-                ("weight_bytes", ctypes.c_double)]
+                ("weight_bytes", ctypes.c_double), ("input_tokens", ctypes.c_int)]
 
 
 class LayerTime(ctypes.Structure):
@@ -180,6 +181,9 @@ _SIGS = {
     "dstack_op_maxpool": ([_vp, _i, _i, _i, _i, _i, _i, _i, _vp, _vp], _i),
     "dstack_op_avgpool": ([_vp, _i, _i, _i, _i, _vp, _vp], _i),
     "dstack_lstm_workspace_bytes": ([_i, _i, _i], _sz),
+    "dstack_op_embed_ln": ([_vp, _i, _i, _i, _vp, _vp, _vp, _i, _vp, _vp, ctypes.c_float, _vp, _vp], _i),
+    "dstack_op_layernorm": ([_vp, _i, _i, _vp, _vp, ctypes.c_float, _vp, _vp], _i),
+    "dstack_op_attention": ([_vp, _i, _i, _i, _i, _vp, _vp], _i),
     "dstack_op_lstm_layer": ([_vp, _i, _i, _i, _i, _vp, _vp, _vp, _vp, _vp, _vp, _vp], _i),
 }
 
@@ -291,7 +295,10 @@ class Model:
             pass
 
     def input_shape(self, batch):
+        """Shape of the input tensor: CNN [b,H,W,3] bf16, LSTM [T,b,I] bf16, transformer [b,T] int32 ids."""
         i = self.info
+        if i.input_tokens:
+            return (batch, i.seq_len)
         return (i.seq_len, batch, i.in_features) if i.is_lstm else (batch, i.in_h, i.in_w, i.in_c)
 
     def output_shape(self, batch):
@@ -602,3 +609,24 @@ def lstm_layer(x, w_ih, w_hh, bias, h_bf16, h_f32, workspace, stream=None):
     H = w_hh.shape[1]
     _check(lib().dstack_op_lstm_layer(_ptr(x), T, B, I, H, _ptr(w_ih), _ptr(w_hh), _ptr(bias), _ptr(h_bf16),
                                       _ptr(h_f32), _ptr(workspace), _stream(stream)))
+
+
+def embed_ln(ids, T, we, pe, te, gamma, beta, eps, y, stream=None):
+    """ids [rows] int32 -> y [rows,H] bf16 (see dstack_op_embed_ln)."""
+    vocab, H = we.shape
+    _check(lib().dstack_op_embed_ln(_ptr(ids), ids.numel(), T, vocab, _ptr(we), _ptr(pe), _ptr(te), H, _ptr(gamma),
+                                    _ptr(beta), float(eps), _ptr(y), _stream(stream)))
+
+
+def layernorm(x, gamma, beta, eps, y, stream=None):
+    """x [rows,H] bf16 -> y bf16 (see dstack_op_layernorm)."""
+    H = x.shape[-1]
+    _check(lib().dstack_op_layernorm(_ptr(x), x.numel() // H, H, _ptr(gamma), _ptr(beta), float(eps), _ptr(y),
+                                     _stream(stream)))
+
+
+def attention(qkv, heads, out, stream=None):
+    """qkv [B,T,3*heads*dh] bf16 -> out [B,T,heads*dh] bf16 (see dstack_op_attention)."""
+    B, T, H3 = qkv.shape
+    _check(lib().dstack_op_attention(_ptr(qkv), B, T, heads, H3 // 3 // heads, _ptr(out), _stream(stream)))
+

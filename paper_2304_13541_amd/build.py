@@ -18,7 +18,7 @@ OUT = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libdstack.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
-SOURCES = ["conv_igemm.hip", "conv_rgb.hip", "expand_dw.hip", "kernels_misc.hip", "kernels_seq.hip", "model.cpp", "rng.cpp", "sched.cpp", "knee_model.cpp", "launcher.cpp", "serve.cpp", "capi.cpp"]
+SOURCES = ["conv_igemm.hip", "conv_rgb.hip", "expand_dw.hip", "kernels_misc.hip", "kernels_seq.hip", "kernels_tf.hip", "model.cpp", "rng.cpp", "sched.cpp", "knee_model.cpp", "launcher.cpp", "serve.cpp", "capi.cpp"]
 BASE_FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-result",
               "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 PER_FILE = {"rng.cpp": ["-ffp-contract=off"], "knee_model.cpp": ["-ffp-contract=off"]}

@@ -208,6 +208,7 @@ dstack_status dstack_model_query(dstack_model h, dstack_model_info* out) {
     out->seq_len = m.seq_len;
     out->in_features = m.in_features;
     out->out_features = m.out_features;
+    out->input_tokens = m.input_tokens;
     out->num_tensors = (int)m.tensors.size();
     int64_t np = 0;
     for (const auto& t : m.tensors) np += t.numel;
@@ -392,17 +393,28 @@ dstack_status dstack_profile_layers(dstack_model h, int batch, const void* d_in,
 namespace {
 
 // Scratch input/output of the model at its maximum batch for profiling runs
-// (contents: a fixed xorshift pattern of values in about [-1, 1)).
+// (contents: a fixed xorshift pattern of values in about [-1, 1), or of
+// token ids for a transformer).
 dstack_status ensure_sweep_buffers(Model& m) {
   if (m.sweep_in) return DSTACK_OK;
-  size_t in_bytes = m.is_lstm ? (size_t)m.seq_len * m.max_batch * m.in_features * 2
-                              : (size_t)m.max_batch * m.in_h * m.in_w * m.in_c * 2;
+  size_t in_bytes = m.is_lstm        ? (size_t)m.seq_len * m.max_batch * m.in_features * 2
+                    : m.input_tokens ? (size_t)m.seq_len * m.max_batch * 4
+                                     : (size_t)m.max_batch * m.in_h * m.in_w * m.in_c * 2;
   size_t out_bytes = m.is_lstm ? (size_t)m.seq_len * m.max_batch * m.out_features * 4
                                : (size_t)m.max_batch * m.out_features * 4;
   DS_HIP(hipMalloc(&m.sweep_in, in_bytes));
   DS_HIP(hipMalloc(&m.sweep_out, out_bytes));
-  std::vector<uint16_t> pat(in_bytes / 2);
   uint64_t z = 0x2545F4914F6CDD1DULL;
+  if (m.input_tokens) {  // token ids below 30000
+    std::vector<int32_t> ids(in_bytes / 4);
+    for (auto& v : ids) {
+      z ^= z << 13; z ^= z >> 7; z ^= z << 17;
+      v = (int32_t)(z % 30000);
+    }
+    DS_HIP(hipMemcpy(m.sweep_in, ids.data(), in_bytes, hipMemcpyHostToDevice));
+    return DSTACK_OK;
+  }
+  std::vector<uint16_t> pat(in_bytes / 2);
   for (auto& v : pat) {
     z ^= z << 13; z ^= z >> 7; z ^= z << 17;
     v = bf16_from_double(((double)(z >> 11) * (1.0 / 9007199254740992.0)) * 2.0 - 1.0);
@@ -726,7 +738,7 @@ dstack_status dstack_op_conv2d(const void* x, int N, int H, int W, int C, const 
                                void* y, int out_fp32, void* stream) {
   return guarded([&] {
     DS_CHECK(x && w && y, DSTACK_E_INVALID, "conv2d: null pointer");
-    DS_CHECK(act >= 0 && act <= 2, DSTACK_E_INVALID, "conv2d: act must be 0, 1 or 2");
+    DS_CHECK(act >= 0 && act <= 4, DSTACK_E_INVALID, "conv2d: act must be 0..4");
     return launch_conv2d(static_cast<const bf16*>(x), N, H, W, C, static_cast<const bf16*>(w), K, R, S, stride, pad,
                          scale, shift, static_cast<const bf16*>(res), act, y, out_fp32 != 0, 256, (hipStream_t)stream);
   });
@@ -810,6 +822,31 @@ dstack_status dstack_op_lstm_layer(const void* x, int T, int B, int I, int H, co
     return lstm_layer_run(static_cast<const bf16*>(x), T, B, I, H, static_cast<const bf16*>(w_ih),
                           static_cast<const bf16*>(w_hh), bias, static_cast<bf16*>(h_bf16), h_f32, gx, c, 256,
                           (hipStream_t)stream, nullptr);
+  });
+}
+
+dstack_status dstack_op_embed_ln(const int32_t* ids, int rows, int T, int vocab, const void* we, const void* pe,
+                                 const void* te, int H, const float* gamma, const float* beta, float eps, void* y,
+                                 void* stream) {
+  return guarded([&] {
+    return launch_embed_ln(ids, rows, T, vocab, static_cast<const bf16*>(we), static_cast<const bf16*>(pe),
+                           static_cast<const bf16*>(te), H, gamma, beta, eps, static_cast<bf16*>(y),
+                           (hipStream_t)stream);
+  });
+}
+
+dstack_status dstack_op_layernorm(const void* x, int rows, int H, const float* gamma, const float* beta, float eps,
+                                  void* y, void* stream) {
+  return guarded([&] {
+    return launch_layernorm(static_cast<const bf16*>(x), rows, H, gamma, beta, eps, static_cast<bf16*>(y),
+                            (hipStream_t)stream);
+  });
+}
+
+dstack_status dstack_op_attention(const void* qkv, int B, int T, int heads, int dh, void* out, void* stream) {
+  return guarded([&] {
+    return launch_attention(static_cast<const bf16*>(qkv), B, T, heads, dh, static_cast<bf16*>(out),
+                            (hipStream_t)stream);
   });
 }
 

@@ -37,7 +37,7 @@ typedef __attribute__((__vector_size__(4 * sizeof(__bf16)))) __bf16 bf16x4;
 typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
 typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16;
 
-enum Act { ACT_NONE = 0, ACT_RELU = 1, ACT_RELU6 = 2 };
+enum Act { ACT_NONE = 0, ACT_RELU = 1, ACT_RELU6 = 2, ACT_GELU = 3, ACT_TANH = 4 };
 
 // Thread-local error text behind dstack_last_error().
 void set_error(const std::string& msg);
@@ -104,9 +104,14 @@ inline dstack_status hip_fail(hipError_t e, const char* what) {
 inline int ceil_div(int a, int b) { return (a + b - 1) / b; }
 inline int out_dim(int in, int k, int stride, int pad) { return (in + 2 * pad - k) / stride + 1; }
 
+// GELU with the Gaussian CDF through erf (the transformer's activation)
+__device__ __forceinline__ float gelu_erf(float v) { return 0.5f * v * (1.0f + erff(v * 0.70710678118654752f)); }
+
 __device__ __forceinline__ float apply_act(float v, int act) {
   if (act == ACT_RELU) return fmaxf(v, 0.0f);
   if (act == ACT_RELU6) return fminf(fmaxf(v, 0.0f), 6.0f);
+  if (act == ACT_GELU) return gelu_erf(v);
+  if (act == ACT_TANH) return tanhf(v);
   return v;
 }
 
@@ -130,6 +135,12 @@ dstack_status launch_avgpool(const bf16* x, int N, int H, int W, int C, bf16* y,
 dstack_status launch_expand_dw(const bf16* x, int N, int H, int W, int Cin, const bf16* we, int Ce, const float* se,
                                const float* he, int act_e, const bf16* wd, int stride, const float* sd,
                                const float* hd, int act_d, bf16* y, int n_cu, hipStream_t st);
+dstack_status launch_embed_ln(const int* ids, int rows, int T, int vocab, const bf16* we, const bf16* pe,
+                              const bf16* te, int H, const float* gamma, const float* beta, float eps, bf16* y,
+                              hipStream_t st);
+dstack_status launch_layernorm(const bf16* x, int rows, int H, const float* gamma, const float* beta, float eps,
+                               bf16* y, hipStream_t st);
+dstack_status launch_attention(const bf16* qkv, int B, int T, int heads, int dh, bf16* out, hipStream_t st);
 dstack_status launch_conv2d_rgb(const bf16* x, int N, int H, int W, const bf16* w4, int K, int R, int stride, int pad,
                                 const float* scale, const float* shift, int act, bf16* y, hipStream_t st);
 dstack_status launch_lstm_step(const float* gx_t, const bf16* w_hh, const bf16* h_prev, float* c, bf16* h_next,

@@ -495,25 +495,27 @@ __global__ __launch_bounds__(256) void conv_igemm_kernel(ConvArgs a) {
   // (M * K < 2^31 is checked at launch)
   const int idx0 = (m0 + pl0) * a.K + ch0;
   const int dstep = RSTEP * a.K;
-  // the activation is chosen once: none, or a clamp to [0, hi] (ReLU: hi = inf)
+  // the activation is chosen once: none, a clamp to [0, hi] (ReLU: hi =
+  // inf), GELU or tanh
   const float hi = a.act == ACT_RELU6 ? 6.0f : INFINITY;
-  auto rows = [&](auto clamp) {
+  auto rows = [&](auto act) {
 #pragma unroll
     for (int k = 0; k < ROWS_PT; ++k) {
       if (m0 + pl0 + k * RSTEP >= a.M) continue;
       float v[4];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        v[e] = t[k][e] * sc[e] + sh[e] + (float)rv[k][e];
-        if (decltype(clamp)::value) v[e] = fminf(fmaxf(v[e], 0.0f), hi);
-      }
+      for (int e = 0; e < 4; ++e) v[e] = act(t[k][e] * sc[e] + sh[e] + (float)rv[k][e]);
       store_out4(a.y, OUT_F32, idx0 + k * dstep, v);
     }
   };
   if (a.act == ACT_NONE)
-    rows(std::false_type{});
+    rows([](float v) { return v; });
+  else if (a.act == ACT_GELU)
+    rows([](float v) { return gelu_erf(v); });
+  else if (a.act == ACT_TANH)
+    rows([](float v) { return tanhf(v); });
   else
-    rows(std::true_type{});
+    rows([hi](float v) { return fminf(fmaxf(v, 0.0f), hi); });
 }
 
 // 256-thread launch; through hipExtLaunchKernelGGL when dispatch events are
@@ -803,6 +805,7 @@ dstack_status launch_conv2d_ws(const bf16* x, int N, int H, int W, int C, const 
   DS_CHECK(K % 4 == 0, DSTACK_E_UNSUPPORTED, "conv2d: K must be a multiple of 4");
   DS_CHECK(N > 0 && H > 0 && W > 0 && K > 0 && R > 0 && S > 0 && stride > 0 && pad >= 0, DSTACK_E_INVALID,
            "conv2d: bad shape");
+  DS_CHECK(act >= ACT_NONE && act <= ACT_TANH, DSTACK_E_INVALID, "conv2d: act must be 0..4");
   ConvArgs a;
   a.x = x; a.w = w; a.scale = scale; a.shift = shift; a.res = res; a.y = y; a.partial = nullptr;
   a.N = N; a.H = H; a.W = W; a.C = C; a.K = K; a.R = R; a.S = S; a.stride = stride; a.pad = pad;
@@ -821,7 +824,7 @@ dstack_status launch_conv2d_ws(const bf16* x, int N, int H, int W, int C, const 
   a.div_c = FastDiv::make(C);
   a.div_s = FastDiv::make(S);
   const bool one = R == 1 && S == 1 && pad == 0;
-  if (one && stride == 1 && C <= 32 && K % 16 == 0) {  // small depth: the streaming kernel
+  if (one && stride == 1 && C <= 32 && K % 16 == 0 && act <= ACT_RELU6) {  // small depth: the streaming kernel
     launch_1x1s(a, out_fp32, n_cu > 0 ? n_cu : 256, st);
     DS_HIP(hipGetLastError());
     return DSTACK_OK;

@@ -12,9 +12,17 @@
 //   vgg19        16 conv3x3 (+bias, ReLU, no BN) in 5 stages, 2x2 max pools,
 //                FC 25088 -> 4096 -> 4096 -> 1000 (flattened in (h, w, c) order)
 //   lstm2        2-layer LSTM, input 512, hidden 1024, 50 steps
+//   bert         BERT-base encoder on 20-token sequences (10-word sentences):
+//                embeddings + layer norm, 12 post-norm layers (fused q|k|v
+//                projection, 12-head attention, output projection +
+//                residual, layer norm, GELU feed-forward 3072 + residual,
+//                layer norm), tanh pooler on the first token, 2 classes
+//   bert_long    the same on 40-token sequences (20-word sentences)
 // Tensor indices follow layer order with weight before bias; BN statistics
 // are the constants gamma 1, beta 0, mean 0, var 1, eps 1e-5, folded into a
-// per-channel fp32 scale/shift of the producing convolution's epilogue.
+// per-channel fp32 scale/shift of the producing convolution's epilogue.  The
+// transformer's weights and biases are N(0, 0.02^2) (the He rule with fan-in
+// 5000) and its layer norms have gain 1, bias 0 and eps 1e-12.
 #include "model.hpp"
 
 #include <algorithm>
@@ -181,6 +189,40 @@ class ArchBuilder {
     op.out = b.alloc(s.C);
     push(op);
     return Shape{op.out, 1, 1, s.C};
+  }
+  // token ids -> word + position + type embedding -> layer norm, [T][H] per item
+  Shape embed_ln(int T, int vocab, int H, int we, int pe, int te) {
+    Op op;
+    op.kind = OP_EMBED_LN;
+    op.in = BUF_IN;
+    op.T = T; op.C = H; op.K = vocab;
+    op.H = 1; op.W = T; op.Ho = 1; op.Wo = T;
+    op.w_off = m.tensors[we].dev_off;
+    op.w2_off = m.tensors[pe].dev_off;
+    op.w3_off = m.tensors[te].dev_off;
+    op.out = b.alloc((int64_t)T * H);
+    push(op);
+    return Shape{op.out, 1, T, H};
+  }
+  Shape layernorm(const Shape& s) {
+    Op op;
+    op.kind = OP_LAYERNORM;
+    op.in = s.buf;
+    op.H = s.H; op.W = s.W; op.C = s.C; op.Ho = s.H; op.Wo = s.W;
+    op.out = b.alloc((int64_t)s.H * s.W * s.C);
+    push(op);
+    return Shape{op.out, s.H, s.W, s.C};
+  }
+  // fused q|k|v [T][3*width] -> attention output [T][width]
+  Shape attention(const Shape& s, int heads) {
+    Op op;
+    op.kind = OP_ATTENTION;
+    op.in = s.buf;
+    op.T = s.W; op.C = s.C / 3; op.K = heads;
+    op.H = 1; op.W = s.W; op.Ho = 1; op.Wo = s.W;
+    op.out = b.alloc((int64_t)s.W * (s.C / 3));
+    push(op);
+    return Shape{op.out, 1, s.W, s.C / 3};
   }
   Shape fc(const Shape& s, int wt, int bt, int O, int act, bool last) {
     Op op;
@@ -409,6 +451,54 @@ void build_lstm(ArchBuilder& A) {
   }
 }
 
+void build_bert(ArchBuilder& A, int T) {
+  Model& m = A.m;
+  const int H = 768, heads = 12, FF = 3072, vocab = 30522, L = 12, FAN = 5000;
+  m.input_tokens = 1;
+  m.seq_len = T;
+  m.out_features = 2;
+  int we = A.b.tensor((int64_t)vocab * H, DIST_HE, FAN);
+  int pe = A.b.tensor(512L * H, DIST_HE, FAN);
+  int te = A.b.tensor(2L * H, DIST_HE, FAN);
+  std::vector<int> t;
+  for (int l = 0; l < L; ++l) {
+    t.push_back(A.b.tensor(3L * H * H, DIST_HE, FAN));
+    t.push_back(A.b.tensor(3L * H, DIST_HE, FAN));
+    t.push_back(A.b.tensor((int64_t)H * H, DIST_HE, FAN));
+    t.push_back(A.b.tensor(H, DIST_HE, FAN));
+    t.push_back(A.b.tensor((int64_t)FF * H, DIST_HE, FAN));
+    t.push_back(A.b.tensor(FF, DIST_HE, FAN));
+    t.push_back(A.b.tensor((int64_t)H * FF, DIST_HE, FAN));
+    t.push_back(A.b.tensor(H, DIST_HE, FAN));
+  }
+  int wp = A.b.tensor((int64_t)H * H, DIST_HE, FAN), bp = A.b.tensor(H, DIST_HE, FAN);
+  int wc = A.b.tensor(2L * H, DIST_HE, FAN), bc = A.b.tensor(2, DIST_HE, FAN);
+
+  Shape x = A.embed_ln(T, vocab, H, we, pe, te);
+  for (int l = 0; l < L; ++l) {
+    const int* w = &t[8 * l];
+    Shape qkv = A.conv(x, w[0], 3 * H, 1, 1, 0, false, w[1], ACT_NONE, BUF_NONE, H);
+    Shape att = A.attention(qkv, heads);
+    A.b.release(qkv.buf);
+    Shape a = A.conv(att, w[2], H, 1, 1, 0, false, w[3], ACT_NONE, x.buf, H);  // + residual x
+    A.b.release(att.buf);
+    A.b.release(x.buf);
+    Shape a1 = A.layernorm(a);
+    A.b.release(a.buf);
+    Shape f = A.conv(a1, w[4], FF, 1, 1, 0, false, w[5], ACT_GELU, BUF_NONE, H);
+    Shape g = A.conv(f, w[6], H, 1, 1, 0, false, w[7], ACT_NONE, a1.buf, FF);  // + residual a1
+    A.b.release(f.buf);
+    A.b.release(a1.buf);
+    x = A.layernorm(g);
+    A.b.release(g.buf);
+  }
+  // pooler on the first token of each sequence: a 1x1 convolution of stride T over the row of T tokens
+  Shape p = A.conv(x, wp, H, 1, T, 0, false, bp, ACT_TANH, BUF_NONE, H);
+  A.b.release(x.buf);
+  A.fc(p, wc, bc, 2, ACT_NONE, true);
+  A.b.release(p.buf);
+}
+
 }  // namespace
 
 dstack_status build_arch(const std::string& arch, Model& m) {
@@ -424,6 +514,10 @@ dstack_status build_arch(const std::string& arch, Model& m) {
     build_vgg(A);
   else if (arch == "lstm2")
     build_lstm(A);
+  else if (arch == "bert")
+    build_bert(A, 20);
+  else if (arch == "bert_long")
+    build_bert(A, 40);
   else
     return fail(DSTACK_E_UNSUPPORTED, "unknown arch '" + arch + "'");
   return DSTACK_OK;
@@ -748,6 +842,21 @@ dstack_status forward(Model& m, int batch, const void* d_in, void* d_out, Worksp
         s = launch_avgpool(src, batch, op.H, op.W, op.C, (bf16*)dst, st);
         by = (double)batch * (op.H * op.W + 1) * op.C * 2;
         break;
+      case OP_EMBED_LN:
+        s = launch_embed_ln((const int*)src, batch * op.T, op.T, op.K, m.d_w + op.w_off, m.d_w + op.w2_off,
+                            m.d_w + op.w3_off, op.C, nullptr, nullptr, 1e-12f, (bf16*)dst, st);
+        by = (double)batch * op.T * (4 + 3.0 * op.C * 2 + op.C * 2);
+        break;
+      case OP_LAYERNORM:
+        s = launch_layernorm(src, batch * op.H * op.W, op.C, nullptr, nullptr, 1e-12f, (bf16*)dst, st);
+        by = (double)batch * op.H * op.W * op.C * 4;
+        break;
+      case OP_ATTENTION:
+        s = launch_attention(src, batch, op.T, op.K, op.C / op.K, (bf16*)dst, st);
+        kind = KC_ATTENTION;
+        fl = 4.0 * batch * op.T * (double)op.T * op.C;
+        by = (double)batch * op.T * op.C * 2 * 4;
+        break;
       case OP_FC:
         s = launch_fc(src, batch, op.C, m.d_w + op.w_off, f32 + op.shift_off, op.K, op.act, dst, op.out_f32 != 0, n_cu,
                       ws.splitk, ws.splitk_bytes, st);
@@ -789,6 +898,10 @@ void model_cost(const Model& m, int b, double* flops, double* mfma, double* wbyt
         break;
       case OP_FC:
         f += 2.0 * b * op.C * (double)op.K;
+        ++n;
+        break;
+      case OP_ATTENTION:
+        f += 4.0 * b * op.T * (double)op.T * op.C;
         ++n;
         break;
       case OP_LSTM: {

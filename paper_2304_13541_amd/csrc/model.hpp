@@ -36,8 +36,10 @@ inline int64_t dev_numel(const TensorSpec& t) {
 uint16_t bf16_from_double(double x);
 void generate_tensor(uint64_t seed, int index, const TensorSpec& t, uint16_t* out);
 
-enum OpKind { OP_CONV, OP_DW, OP_MAXPOOL, OP_AVGPOOL, OP_FC, OP_LSTM, OP_CONV_RGB, OP_EXPAND_DW };
-enum KernelClass { KC_MFMA = 0, KC_DW = 1, KC_FC = 2, KC_LSTM = 3, KC_GLUE = 4, KC_DIRECT = 5, KC_EXPAND_DW = 6 };
+enum OpKind { OP_CONV, OP_DW, OP_MAXPOOL, OP_AVGPOOL, OP_FC, OP_LSTM, OP_CONV_RGB, OP_EXPAND_DW, OP_EMBED_LN,
+              OP_LAYERNORM, OP_ATTENTION };
+enum KernelClass { KC_MFMA = 0, KC_DW = 1, KC_FC = 2, KC_LSTM = 3, KC_GLUE = 4, KC_DIRECT = 5, KC_EXPAND_DW = 6,
+                   KC_ATTENTION = 7 };
 
 constexpr int BUF_IN = -1;
 constexpr int BUF_OUT = -2;
@@ -52,8 +54,9 @@ struct Op {
   int64_t scale_off = -1;   // fp32 elements into the fp32 arena (-1: none)
   int64_t shift_off = -1;
   int out_f32 = 0;
-  // fused expand + depthwise: the depthwise weights, BN and activation
-  int64_t w2_off = 0, scale2_off = -1, shift2_off = -1;
+  // fused expand + depthwise: the depthwise weights, BN and activation;
+  // token embedding: position (w2_off) and token-type (w3_off) tables
+  int64_t w2_off = 0, scale2_off = -1, shift2_off = -1, w3_off = 0;
   int act2 = 0;
   // LSTM layer
   int T = 0, I = 0, Hd = 0;
@@ -102,6 +105,7 @@ struct Model {
   int max_batch = 32;
   int in_h = 0, in_w = 0, in_c = 0;
   int seq_len = 0, in_features = 0, out_features = 0;
+  int input_tokens = 0;  // 1: the input is int32 token ids [batch][seq_len]
   std::vector<TensorSpec> tensors;
   std::vector<Op> ops;
   std::vector<int64_t> buf_elems;   // per-item bf16 elements of each buffer id

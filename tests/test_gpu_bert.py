@@ -1,0 +1,116 @@
+"""The transformer workload on the GPU through the C ABI: layer norm, token
+embedding + layer norm and the attention core against the fp64 oracle on
+seeded inputs (several row widths, 1..48 tokens, ids at the vocabulary's
+ends), and the whole BERT encoder ("bert", 20 tokens; "bert_long", 40)
+against the oracle in parity mode (bf16 storage at the same points).
+
+Bar: infinity-norm relative error <= 2e-2 for the kernels; for the model's
+two logits max(2e-2, twice the oracle's own parity-vs-pure spread)."""
+import numpy as np
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+TOL = 2e-2
+
+
+@pytest.fixture(scope="module")
+def env(oracle_mod):
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2304_13541_amd as ds
+    from tests import gpu_util as gu
+    from tests import inputs
+    return ds, gu, inputs, oracle_mod, torch
+
+
+@pytest.mark.parametrize("rows,H", [(7, 768), (40, 768), (3, 100), (2, 2048)])
+def test_layernorm(env, rows, H):
+    ds, gu, inputs, oracle, torch = env
+    print("layernorm", rows, H, flush=True)
+    xb = inputs.normal_bf16(31, (rows, H), scale=3.0)
+    rng = np.random.default_rng(32)
+    g, b = rng.normal(1, 0.3, H).astype(np.float32), rng.normal(0, 0.3, H).astype(np.float32)
+    y = gu.empty_bf16((rows, H))
+    ds.layernorm(gu.dev_bf16(xb), gu.dev_f32(g), gu.dev_f32(b), 1e-12, y)
+    torch.cuda.synchronize()
+    ref = oracle.layernorm(oracle.bf16_bits_to_f64(xb), g.astype(np.float64), b.astype(np.float64), 1e-12)
+    assert oracle.rel_err(gu.host(y), ref) <= TOL
+
+
+@pytest.mark.parametrize("B,T,vocab,H,with_gamma", [(2, 20, 1000, 768, False), (1, 40, 30522, 768, True),
+                                                    (3, 5, 17, 64, True)])
+def test_embed_ln(env, B, T, vocab, H, with_gamma):
+    ds, gu, inputs, oracle, torch = env
+    print("embed_ln", B, T, vocab, H, flush=True)
+    rng = np.random.default_rng(33)
+    ids = rng.integers(0, vocab, (B, T)).astype(np.int32)
+    ids[0, 0], ids[-1, -1] = 0, vocab - 1
+    we = inputs.normal_bf16(34, (vocab, H), scale=0.5)
+    pe = inputs.normal_bf16(35, (T + 3, H), scale=0.5)
+    te = inputs.normal_bf16(36, (2, H), scale=0.5)
+    g = rng.normal(1, 0.3, H).astype(np.float32) if with_gamma else None
+    b = rng.normal(0, 0.3, H).astype(np.float32) if with_gamma else None
+    y = gu.empty_bf16((B * T, H))
+    ids_d = torch.from_numpy(ids.ravel()).to("cuda:0")
+    ds.embed_ln(ids_d, T, gu.dev_bf16(we), gu.dev_bf16(pe), gu.dev_bf16(te),
+                gu.dev_f32(g) if with_gamma else None, gu.dev_f32(b) if with_gamma else None, 1e-12, y)
+    torch.cuda.synchronize()
+    W, P, Te = (oracle.bf16_bits_to_f64(a) for a in (we, pe, te))
+    e = W[ids.ravel()] + np.tile(P[:T], (B, 1)) + Te[0]
+    ref = oracle.layernorm(e, g.astype(np.float64) if with_gamma else np.ones(H),
+                           b.astype(np.float64) if with_gamma else np.zeros(H), 1e-12)
+    assert oracle.rel_err(gu.host(y), ref) <= TOL
+
+
+@pytest.mark.parametrize("B,T,heads", [(2, 20, 12), (1, 40, 12), (3, 1, 2), (1, 48, 4), (2, 7, 12)])
+def test_attention(env, B, T, heads):
+    ds, gu, inputs, oracle, torch = env
+    print("attention", B, T, heads, flush=True)
+    qkvb = inputs.normal_bf16(37, (B, T, 3 * heads * 64), scale=0.4)
+    out = gu.empty_bf16((B, T, heads * 64))
+    ds.attention(gu.dev_bf16(qkvb), heads, out)
+    torch.cuda.synchronize()
+    ref = oracle.attention(oracle.bf16_bits_to_f64(qkvb), heads)
+    assert oracle.rel_err(gu.host(out), ref) <= TOL
+
+
+def test_attention_rejects_long_sequences(env):
+    ds, gu, inputs, oracle, torch = env
+    qkv = gu.empty_bf16((1, 49, 3 * 64))
+    with pytest.raises(ds.DStackError):
+        ds.attention(qkv, 1, gu.empty_bf16((1, 49, 64)))
+
+
+@pytest.mark.parametrize("arch,batch,frac", [("bert", 2, 0.5), ("bert_long", 1, 0.25), ("bert", 5, 1.0)])
+def test_bert_model_parity(env, arch, batch, frac):
+    ds, gu, inputs, oracle, torch = env
+    print("bert model", arch, batch, frac, flush=True)
+    m = ds.Model(arch, 77)
+    p = ds.Partition(frac)
+    T = m.input_shape(batch)[1]
+    ids = np.random.default_rng(38).integers(0, 30522, (batch, T)).astype(np.int32)
+    ids[0, 0] = 101
+    x = torch.from_numpy(ids).to("cuda:0")
+    y = gu.empty_f32(m.output_shape(batch))
+    m.infer(batch, x, y, p)
+    p.synchronize()
+    om = oracle.Model(arch, 77)
+    ref = om.forward(ids, parity=True)
+    # The two logits are short sums with heavy cancellation, so their
+    # relative error is large even for bf16 storage alone: the bar is the
+    # kernels' usual 2e-2, or twice the distance that bf16 storage puts
+    # between the oracle's parity and pure (fp64 throughout) results,
+    # whichever is larger.  A wrong layer moves them by O(1).
+    spread = oracle.rel_err(ref, om.forward(ids, parity=False))
+    err = oracle.rel_err(gu.host(y), ref)
+    print("rel_err", err, "bf16-storage spread", spread, gu.host(y)[0], ref[0])
+    assert err <= max(TOL, 2.0 * spread)
+    # a graph replay gives the same logits
+    y2 = gu.empty_f32(m.output_shape(batch))
+    m.infer(batch, x, y2, p)
+    p.synchronize()
+    assert np.array_equal(gu.host(y), gu.host(y2))
+    m.destroy()
+    p.destroy()

@@ -1,7 +1,8 @@
 """Kernel-level parity on the GPU: each HIP kernel, called through the C ABI,
 against the fp64 oracle on the same seeded bf16 inputs.  Shapes span several
 tiles with ragged tails in every GEMM dimension, odd spatial sizes with
-stride 2, K not a multiple of the tile, and every epilogue variant.
+stride 2, K not a multiple of the tile, and every epilogue variant
+(ReLU, ReLU6, GELU, tanh, residual, fp32 output).
 
 Bar: infinity-norm relative error <= 2e-2 (bf16 inputs, fp32 accumulation,
 bf16 or fp32 output)."""
@@ -43,6 +44,11 @@ CONV_CASES = [
     (2, 6, 6, 64, 256, 1, 1, 0, 1, True, False),
     (1, 3, 3, 8, 48, 1, 1, 0, 1, False, False),
     (1, 4, 5, 40, 80, 1, 1, 0, 2, True, True),
+    # the transformer's epilogues: GELU (feed-forward in) and tanh (pooler, a
+    # 1x1 convolution of stride T picking each sequence's first token)
+    (2, 1, 20, 768, 3072, 1, 1, 0, 3, False, False),
+    (3, 1, 20, 768, 768, 1, 20, 0, 4, False, False),
+    (1, 1, 7, 24, 64, 1, 1, 0, 3, True, False),
 ]
 
 
@@ -67,7 +73,15 @@ def test_conv2d(env, case):
     ref = oracle.conv2d(x, w, st, pad) * scale.astype(np.float64) + shift.astype(np.float64)
     if use_res:
         ref = ref + oracle.bf16_bits_to_f64(resb)
-    ref = np.maximum(ref, 0) if act == 1 else (np.clip(ref, 0, 6) if act == 2 else ref)
+    if act == 1:
+        ref = np.maximum(ref, 0)
+    elif act == 2:
+        ref = np.clip(ref, 0, 6)
+    elif act == 3:
+        from scipy.special import erf
+        ref = 0.5 * ref * (1.0 + erf(ref / np.sqrt(2.0)))
+    elif act == 4:
+        ref = np.tanh(ref)
     err = oracle.rel_err(gu.host(y), ref)
     print("rel_err", err)
     assert err <= TOL

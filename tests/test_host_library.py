@@ -42,11 +42,14 @@ def test_fraction_to_slots():
         assert e.value.status == ds.E_INVALID
 
 
-@pytest.mark.parametrize("arch", ["tinycnn", "resnet50", "mobilenetv2", "lstm2", "vgg19"])
+@pytest.mark.parametrize("arch", ["tinycnn", "resnet50", "mobilenetv2", "lstm2", "vgg19", "bert"])
 def test_weights_bit_identical_to_oracle(oracle_mod, arch):
     m = oracle_mod.Model(arch, 1234)
     n = m.num_tensors()
-    idxs = range(n) if arch != "vgg19" else [0, 1, 2, 5, 17, 30, 33, 35, 37]
+    idxs = {"vgg19": [0, 1, 2, 5, 17, 30, 33, 35, 37],
+            "bert": [0, 1, 2, 3, 4, 5, 6, 7, 8, 9, 10, 50, 99, 100, 101, 102]}.get(arch, range(n))
+    if arch == "bert":
+        assert n == 3 + 12 * 8 + 4
     for i in idxs:
         lib_bits = ds.generate_params(arch, 1234, i)
         assert np.array_equal(lib_bits, m.tensor_bf16(i)), (arch, i)
