@@ -383,6 +383,24 @@ def config2(ds, torch, args):
     return dict(workload="ResNet-50 v1.5, 224x224x3, seed 1020", fractions=FRACTIONS, rows=rows)
 
 
+def config6(ds, args):
+    """The transformer workload (Sec. 4.4): BERT-base on 10-word (20-token)
+    and 20-word (40-token) sentences at batch 1 and 16 over the 10
+    fractions: latency, inf/s and the knee (the paper's knees were about 30%
+    and 40% of a V100 for the two lengths)."""
+    rows = []
+    for arch, words in (("bert", 10), ("bert_long", 20)):
+        m = ds.Model(arch, 1060)
+        for b in (1, 16):
+            r = m.knee_sweep(b, FRACTIONS, warmup=args.sweep_warmup, reps=args.sweep_reps)
+            rows.append(dict(arch=arch, words=words, tokens=m.input_shape(b)[1], batch=b, n_cu=r["n_cu"],
+                             latency_us=r["latency_us"], inferences_per_s=[b * 1e6 / L for L in r["latency_us"]],
+                             knee_slots=r["knee_slots"], knee_fraction=r["knee_slots"] / 32.0,
+                             deployed_slots=r["deployed_slots"]))
+        m.destroy()
+    return dict(workload="BERT-base encoder (12 layers, 768 wide, 12 heads), 2 classes, seed 1060", rows=rows)
+
+
 def config4(ds, torch, args):
     """VGG-19 batch 8 + 2-layer LSTM batch 32, closed loop on deployed-knee
     partitions (shrunk proportionally to fit), vs time-sliced full GPU."""
@@ -675,10 +693,11 @@ def main():
                            switch_from_slots=10, switch_to_slots=dep[i], **sw))
 
     # ---- the other workloads: VGG-19 + LSTM pair, four-model Poisson mix through the live launcher ----
-    c1 = c2 = c4 = c5 = cmp = ideal = None
+    c1 = c2 = c4 = c5 = c6 = cmp = ideal = None
     if not args.headline_only:
         c1 = config1(ds)
         c2 = config2(ds, torch, args)
+        c6 = config6(ds, args)
         c4 = config4(ds, torch, args)
         extra = [("vgg19", 1052, [1, 2, 4, 8]), ("lstm2", 1053, [1, 2, 4, 8, 16, 32])]
         m4 = [ds.Model(a, s) for a, s, _ in extra]
@@ -749,6 +768,7 @@ def main():
         "config2": c2,
         "config4": c4,
         "config5": c5,
+        "config6": c6,
         "comparators": cmp,
         "ideal_vs_dstack": ideal,
         "timing_tables": {t["arch"]: {str(b): row for b, row in t["table"].items()} for t in tables},
