@@ -37,13 +37,17 @@ CONV_CASES = [
     (1, 1, 1, 520, 4, 1, 1, 0, 0, False, True),
     # 1x1 stride 1 with C <= 32 and K % 16 == 0: the streaming small-depth kernel
     # (ragged pixel counts, depth tails inside a 32-deep step, 1..8 channel blocks per wave);
-    # C = 64 and 40 take the tiled kernel
+    # C = 40..128 take the tiled kernel with its two-tile ring (one or two depth tiles)
     (2, 9, 7, 16, 96, 1, 1, 0, 2, False, False),
     (1, 11, 11, 24, 144, 1, 1, 0, 2, False, False),
     (3, 5, 7, 32, 16, 1, 1, 0, 0, False, True),
     (2, 6, 6, 64, 256, 1, 1, 0, 1, True, False),
     (1, 3, 3, 8, 48, 1, 1, 0, 1, False, False),
     (1, 4, 5, 40, 80, 1, 1, 0, 2, True, True),
+    (2, 7, 9, 128, 512, 1, 1, 0, 1, True, False),
+    (1, 5, 9, 96, 48, 1, 1, 0, 0, False, False),
+    (3, 4, 7, 64, 64, 1, 1, 0, 0, True, True),
+    (1, 3, 11, 120, 32, 1, 1, 0, 2, False, False),
     # the transformer's epilogues: GELU (feed-forward in) and tanh (pooler, a
     # 1x1 convolution of stride T picking each sequence's first token)
     (2, 1, 20, 768, 3072, 1, 1, 0, 3, False, False),
