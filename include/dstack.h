@@ -537,7 +537,9 @@ dstack_status dstack_serve(const dstack_model* models, int n_models, const void*
  *   * w[k,r,s,c] + shift[k] (+ res[n,ho,wo,k])), zero outside the image;
  *   act 0 none, 1 ReLU, 2 ReLU6, 3 GELU (erf form), 4 tanh;
  *   C % 8 == 0 and K % 4 == 0 (else E_UNSUPPORTED); res may be NULL;
- *   out_fp32 selects an fp32 instead of bf16 output.
+ *   out_fp32 selects an fp32 instead of bf16 output.  The tile plan is
+ *   chosen for the CUs the stream's CU mask enables (the whole device for
+ *   the null stream); no split-K workspace is used here.
  * dwconv3x3: per-channel 3x3, pad 1, stride 1 or 2, w [3][3][C] (device
  *   layout), then scale/shift and act; C % 8 == 0.
  * fc: y[b][o] = act(sum_i x[b][i] * w[o][i] + bias[o]); batch 1..32,

@@ -740,7 +740,8 @@ dstack_status dstack_op_conv2d(const void* x, int N, int H, int W, int C, const 
     DS_CHECK(x && w && y, DSTACK_E_INVALID, "conv2d: null pointer");
     DS_CHECK(act >= 0 && act <= 4, DSTACK_E_INVALID, "conv2d: act must be 0..4");
     return launch_conv2d(static_cast<const bf16*>(x), N, H, W, C, static_cast<const bf16*>(w), K, R, S, stride, pad,
-                         scale, shift, static_cast<const bf16*>(res), act, y, out_fp32 != 0, 256, (hipStream_t)stream);
+                         scale, shift, static_cast<const bf16*>(res), act, y, out_fp32 != 0,
+                         stream_cu_count((hipStream_t)stream), (hipStream_t)stream);
   });
 }
 
@@ -760,7 +761,7 @@ dstack_status dstack_op_expand_dw(const void* x, int N, int H, int W, int Cin, c
   return guarded([&] {
     return launch_expand_dw(static_cast<const bf16*>(x), N, H, W, Cin, static_cast<const bf16*>(we), Ce, se, he,
                             act_e, static_cast<const bf16*>(wd), stride, sd, hd, act_d, static_cast<bf16*>(y),
-                            stream_cu_count((hipStream_t)stream), (hipStream_t)stream);
+                            (hipStream_t)stream);
   });
 }
 

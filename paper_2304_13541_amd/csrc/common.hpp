@@ -134,7 +134,7 @@ dstack_status launch_maxpool(const bf16* x, int N, int H, int W, int C, int k, i
 dstack_status launch_avgpool(const bf16* x, int N, int H, int W, int C, bf16* y, hipStream_t st);
 dstack_status launch_expand_dw(const bf16* x, int N, int H, int W, int Cin, const bf16* we, int Ce, const float* se,
                                const float* he, int act_e, const bf16* wd, int stride, const float* sd,
-                               const float* hd, int act_d, bf16* y, int n_cu, hipStream_t st);
+                               const float* hd, int act_d, bf16* y, hipStream_t st);
 dstack_status launch_embed_ln(const int* ids, int rows, int T, int vocab, const bf16* we, const bf16* pe,
                               const bf16* te, int H, const float* gamma, const float* beta, float eps, bf16* y,
                               hipStream_t st);

@@ -318,8 +318,7 @@ static void expand_dw_launch_cb(const ExpandDwArgs& a, int ds, hipStream_t st) {
 
 dstack_status launch_expand_dw(const bf16* x, int N, int H, int W, int Cin, const bf16* we, int Ce, const float* se,
                                const float* he, int act_e, const bf16* wd, int stride, const float* sd,
-                               const float* hd, int act_d, bf16* y, int n_cu, hipStream_t st) {
-  (void)n_cu;
+                               const float* hd, int act_d, bf16* y, hipStream_t st) {
   DS_CHECK(x && we && se && he && wd && sd && hd && y, DSTACK_E_INVALID, "expand_dw: null pointer");
   DS_CHECK(N > 0 && H > 0 && W > 0 && (stride == 1 || stride == 2), DSTACK_E_INVALID, "expand_dw: bad shape");
   DS_CHECK(Cin % 8 == 0 && Cin <= 160, DSTACK_E_UNSUPPORTED, "expand_dw: Cin must be a multiple of 8, at most 160");

@@ -801,7 +801,7 @@ dstack_status forward(Model& m, int batch, const void* d_in, void* d_out, Worksp
       case OP_EXPAND_DW:
         s = launch_expand_dw(src, batch, op.H, op.W, op.C, m.d_w + op.w_off, op.K, f32 + op.scale_off,
                              f32 + op.shift_off, op.act, m.d_w + op.w2_off, op.stride, f32 + op.scale2_off,
-                             f32 + op.shift2_off, op.act2, (bf16*)dst, n_cu, st);
+                             f32 + op.shift2_off, op.act2, (bf16*)dst, st);
         kind = KC_EXPAND_DW;
         fl = 2.0 * batch * op.H * op.W * (double)op.C * op.K + 2.0 * batch * op.Ho * op.Wo * op.K * 9;
         by = (double)batch * op.H * op.W * op.C * 2 + (double)op.K * op.C * 2 + 9.0 * op.K * 2 +

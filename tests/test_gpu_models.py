@@ -163,6 +163,31 @@ def test_disjoint_partitions_concurrent_equal_sequential(env):
     assert torch.equal(ya1, ya2) and torch.equal(yb1, yb2)
 
 
+def test_two_model_mix_launch_configuration(env):
+    """The timed two-model mix as the bench launches it: ResNet-50 batch 16
+    on slots 0..15 and MobileNetV2 batch 32 on slots 16..31, both replayed
+    concurrently (captured graphs, 4 and 7 batches per step); sampled items
+    of the last replay of each against the oracle."""
+    ds, gu, inputs, oracle, torch = env
+    cfg = [("resnet50", 1030, 16, 0, 4), ("mobilenetv2", 1031, 32, 16, 7)]
+    runs = []
+    for arch, seed, b, off, reps in cfg:
+        m = ds.Model(arch, seed)
+        p = ds.Partition(slot_offset=off, n_slots=16)
+        assert p.n_cu == 128
+        xb = inputs.image_batch(seed + 1, b)
+        runs.append((arch, seed, b, reps, m, p, xb, gu.dev_bf16(xb), gu.empty_f32((b, 1000))))
+    for step in range(max(r[3] for r in runs)):
+        for arch, seed, b, reps, m, p, xb, x, y in runs:
+            if step < reps:
+                m.infer(b, x, y, p)
+    for r in runs:
+        r[5].synchronize()
+    for arch, seed, b, reps, m, p, xb, x, y in runs:
+        items = sample_items(b, seed)[:2]
+        check_against_oracle(env, arch, seed, xb, gu.host(y), items)
+
+
 @pytest.mark.parametrize("arch,batch,fraction", [("mobilenetv2", 4, 0.25), ("resnet50", 2, 0.5), ("lstm2", 3, 0.3)])
 def test_graph_replays_equal_eager(env, arch, batch, fraction):
     """dstack_infer replays a captured graph; dstack_profile_layers runs the
