@@ -719,13 +719,18 @@ constexpr double kRampUs = 1.4;
 constexpr double kSliceWriteUs = 2.6;   // device-scope slice stores until acknowledged
 constexpr double kSliceReadUs = 0.75;   // per slice of 8192 fp32 values, the last block's read-back
 
-// Launches whose blocks walk at most kShortTiles depth tiles run with a
-// two-tile ring, so that more blocks share a CU: as many as its 160 KB of LDS
-// hold, at most as many as the registers allow (VGPR + AGPR per lane of the
-// tile shapes).  Measured on MI355X (128 CUs): ResNet-50's 56x56 1x1 layers
-// of depth 64 went from 19.3 to 16.6 us, MobileNetV2's 56x56 projections of
-// depth 96 and 144 from 12.2 and 14.4 to 9.2 and 12.0 us.
-constexpr int kShortTiles = 3;
+// Launches whose blocks walk at most kShortTiles depth tiles (split-K
+// slices: at most kShortSplitTiles) run with a two-tile ring, so that more
+// blocks share a CU: as many as its 160 KB of LDS hold, at most as many as
+// the registers allow (VGPR + AGPR per lane of the tile shapes).  Measured on
+// MI355X (128 CUs): ResNet-50's 56x56 1x1 layers of depth 64 went from 19.3
+// to 16.6 us and its 56x56 3x3 layers of 64 channels (9 depth tiles) from
+// 17.8 to 15 us, MobileNetV2's 56x56 projections of depth 96 and 144 from
+// 12.2 and 14.4 to 9.2 and 12.0 us; split plans of MobileNetV2's 7x7 layers
+// were slower with the short ring beyond 3 tiles per slice.
+constexpr int kShortTiles = 9;
+constexpr int kShortSplitTiles = 3;
+static bool short_ring(int per, int splits) { return per <= (splits > 1 ? kShortSplitTiles : kShortTiles); }
 static int short_blocks_per_cu(int bn, int bm, bool split) {
   const int ring = 2 * (bn + bm) * ROW_BYTES;
   const int regs = bn * bm >= 16384 ? (split ? 240 : 200) : bn * bm >= 8192 ? (split ? 144 : 128) : (split ? 112 : 80);
@@ -736,7 +741,7 @@ static double plan_cost(const TileCost& t, int M, int K, int nkt, int splits, in
   const int per = ceil_div(nkt, splits);
   const int s = ceil_div(nkt, per);
   const long blocks = (long)ceil_div(M, t.bm) * ceil_div(K, t.bn) * s;
-  const long bpc = per <= kShortTiles ? short_blocks_per_cu(t.bn, t.bm, s > 1) : 2;
+  const long bpc = short_ring(per, s) ? short_blocks_per_cu(t.bn, t.bm, s > 1) : 2;
   const long rounds = (blocks + bpc * n_cu - 1) / (bpc * n_cu);
   double blk = kRampUs + per * t.step_us + 0.6 + 1.5 * (t.bn * t.bm) / 16384.0;
   if (s > 1) blk += kSliceWriteUs + kSliceReadUs * s * (t.bn * t.bm) / 8192.0;
@@ -792,7 +797,7 @@ static void launch_mode(ConvArgs a, bool f32, int splits, hipStream_t st) {
   // with dispatch events armed: both on this kernel (the split-K reduction is in it)
   const DispatchEvents& de = dispatch_events();
   hipEvent_t e0 = de.start, e1 = de.stop;
-  if (STAGES > 2 && a.kt_per_split <= kShortTiles) {
+  if (STAGES > 2 && short_ring(a.kt_per_split, splits)) {
     if (splits > 1)
       launch_k(conv_igemm_kernel<BN, BM, WN, WM, 2, MODE, false, true>, grid, st, e0, e1, a);
     else if (f32)
