@@ -56,6 +56,7 @@ struct ConvArgs {
   int kt_per_split;
   int tiles_n;         // output-channel tiles (fastest-varying in the tile order)
   int tiles;           // tiles per split slice
+  int n_cu;            // CUs of the launch's partition (host-side planning only)
   FastDiv div_wo, div_ho, div_c, div_s, div_tn;
 };
 
@@ -730,7 +731,11 @@ constexpr double kSliceReadUs = 0.75;   // per slice of 8192 fp32 values, the la
 // were slower with the short ring beyond 3 tiles per slice.
 constexpr int kShortTiles = 9;
 constexpr int kShortSplitTiles = 3;
-static bool short_ring(int per, int splits) { return per <= (splits > 1 ? kShortSplitTiles : kShortTiles); }
+// (and only where the grid has more blocks than two per CU: a smaller grid
+// gains nothing from the extra room and loses the deeper prefetch)
+static bool short_ring(int per, int splits, long blocks, int n_cu) {
+  return per <= (splits > 1 ? kShortSplitTiles : kShortTiles) && blocks > 2L * n_cu;
+}
 static int short_blocks_per_cu(int bn, int bm, bool split) {
   const int ring = 2 * (bn + bm) * ROW_BYTES;
   const int regs = bn * bm >= 16384 ? (split ? 240 : 200) : bn * bm >= 8192 ? (split ? 144 : 128) : (split ? 112 : 80);
@@ -741,7 +746,7 @@ static double plan_cost(const TileCost& t, int M, int K, int nkt, int splits, in
   const int per = ceil_div(nkt, splits);
   const int s = ceil_div(nkt, per);
   const long blocks = (long)ceil_div(M, t.bm) * ceil_div(K, t.bn) * s;
-  const long bpc = short_ring(per, s) ? short_blocks_per_cu(t.bn, t.bm, s > 1) : 2;
+  const long bpc = short_ring(per, s, blocks, n_cu) ? short_blocks_per_cu(t.bn, t.bm, s > 1) : 2;
   const long rounds = (blocks + bpc * n_cu - 1) / (bpc * n_cu);
   double blk = kRampUs + per * t.step_us + 0.6 + 1.5 * (t.bn * t.bm) / 16384.0;
   if (s > 1) blk += kSliceWriteUs + kSliceReadUs * s * (t.bn * t.bm) / 8192.0;
@@ -797,7 +802,7 @@ static void launch_mode(ConvArgs a, bool f32, int splits, hipStream_t st) {
   // with dispatch events armed: both on this kernel (the split-K reduction is in it)
   const DispatchEvents& de = dispatch_events();
   hipEvent_t e0 = de.start, e1 = de.stop;
-  if (STAGES > 2 && short_ring(a.kt_per_split, splits)) {
+  if (STAGES > 2 && short_ring(a.kt_per_split, splits, (long)a.tiles * splits, a.n_cu)) {
     if (splits > 1)
       launch_k(conv_igemm_kernel<BN, BM, WN, WM, 2, MODE, false, true>, grid, st, e0, e1, a);
     else if (f32)
@@ -846,13 +851,15 @@ dstack_status launch_conv2d_ws(const bf16* x, int N, int H, int W, int C, const 
   a.M = N * a.Ho * a.Wo;
   a.Kg = R * S * C;
   a.act = act;
+  if (n_cu <= 0) n_cu = 256;  // unknown: plan for the whole device
+  a.n_cu = n_cu;
   a.div_wo = FastDiv::make(a.Wo);
   a.div_ho = FastDiv::make(a.Ho);
   a.div_c = FastDiv::make(C);
   a.div_s = FastDiv::make(S);
   const bool one = R == 1 && S == 1 && pad == 0;
   if (one && stride == 1 && C <= 32 && K % 16 == 0 && act <= ACT_RELU6) {  // small depth: the streaming kernel
-    launch_1x1s(a, out_fp32, n_cu > 0 ? n_cu : 256, st);
+    launch_1x1s(a, out_fp32, n_cu, st);
     DS_HIP(hipGetLastError());
     return DSTACK_OK;
   }
