@@ -256,12 +256,24 @@ class Mix:
                     self.models[mi].infer(self.batch[mi], self.xs[mi], self.ys[li], self.parts[li])
 
     def timed(self, steps, warmup, lanes=None):
+        """Wall time of `steps` closed-loop steps; each lane's own span (its
+        partition stream, from the host's start to its last batch) is kept in
+        self.lane_s."""
+        sel = list(range(len(self.lanes))) if lanes is None else list(lanes)
         self.run(warmup, lanes)
         self._sync(self.parts)
+        ev = [(self.torch.cuda.Event(enable_timing=True), self.torch.cuda.Event(enable_timing=True)) for _ in sel]
+        streams = [self.parts[li].torch_stream() for li in sel]
+        for (e0, _), s in zip(ev, streams):
+            e0.record(s)
         t0 = time.perf_counter()
         self.run(steps, lanes)
+        for (_, e1), s in zip(ev, streams):
+            e1.record(s)
         self._sync(self.parts)
-        return time.perf_counter() - t0
+        dt = time.perf_counter() - t0
+        self.lane_s = {li: e0.elapsed_time(e1) / 1e3 for li, (e0, e1) in zip(sel, ev)}
+        return dt
 
     def timesliced(self, steps, warmup, out_shapes):
         from tests import gpu_util as gu
@@ -284,13 +296,17 @@ class Mix:
 
     def interference(self, steps, warmup, t_mix, mix_steps):
         """Per lane: time per batch alone on its partition (steps steps) vs in
-        the mix (t_mix over mix_steps steps)."""
+        the mix (the lane's own span in the timed mix over its batches there;
+        call right after the timed mix), and the mix's wall time per batch of
+        the lane (the step is set by the slowest lane)."""
+        mix_lane_s = dict(self.lane_s)
         out = []
         for li, (mi, o, s) in enumerate(self.lanes):
             alone = self.timed(steps, warmup, [li]) / (steps * self.reps[mi])
-            mixed = t_mix / (mix_steps * self.reps[mi])
+            mixed = mix_lane_s[li] / (mix_steps * self.reps[mi])
+            wall = t_mix / (mix_steps * self.reps[mi])
             out.append(dict(lane=li, model=mi, slot_offset=o, slots=s, alone_us=1e6 * alone, mixed_us=1e6 * mixed,
-                            slowdown=mixed / alone))
+                            slowdown=mixed / alone, mix_wall_us_per_batch=1e6 * wall))
         return out
 
     def destroy(self):
