@@ -343,7 +343,7 @@ def config1(ds):
 
 
 def knee_model_prediction(ds, torch, m, b, n_cu_grid, latency_us):
-    """Sec. 4.2's analytical model with this library's own kernels: N_i =
+    """Sec. 4.3's analytical model with this library's own kernels: N_i =
     workgroups of unit i / workgroups one CU holds (dstack_kernel_shapes),
     t_p from the unit's event-timed duration on the whole GPU (the durations
     scaled so that they sum to the measured latency there), t_np = 0.  E_t is
@@ -384,7 +384,7 @@ def knee_model_prediction(ds, torch, m, b, n_cu_grid, latency_us):
 def config2(ds, torch, args):
     """ResNet-50 at batch 1, 8 and 32 over the 10 fractions: latency, inf/s,
     efficacy b / (L^2 * CUs) and the knee (Sec. 3.2), beside the knee the
-    analytical model of Sec. 4.2 predicts from the kernels' parallelism."""
+    analytical model of Sec. 4.3 predicts from the kernels' parallelism."""
     m = ds.Model("resnet50", 1020)
     rows = []
     for b in (1, 8, 32):
@@ -507,7 +507,7 @@ def config5(ds, torch, models4, tables4, args):
 
 
 def comparators(ds, tables4, k=32, seconds=2.0):
-    """Sec. 7's comparators in simulate mode on the four-model mix's measured
+    """Sec. 6.3's comparators in simulate mode on the four-model mix's measured
     timing tables at k x the stated rates (far past the 1% capacity, so that
     every policy is bound by the GPU): D-STACK
     (plan + FOD), max-throughput (least runtime first) and max-min fair
@@ -544,7 +544,7 @@ def kernel_knee_table(ds, m, b, x, y):
     """Per kernel of one forward (the timed units of the layer profile): its
     duration on each of the sweep's shares and its own knee (argmax of
     1/(d^2 s), ties to fewer slots) -- the per-kernel GPU% the ideal
-    schedule of Sec. 7 assumes known."""
+    schedule of Sec. 6.2 assumes known."""
     durs = []
     for f in FRACTIONS:
         p = ds.Partition(f)
@@ -565,7 +565,7 @@ def kernel_knee_table(ds, m, b, x, y):
 
 
 def ideal_vs_dstack(ds, models, tables, batch, xs, ys, seconds=0.2, slot_us=1):
-    """The headline pair under the ideal schedule of Sec. 7 (slotted, kernel
+    """The headline pair under the ideal schedule of Sec. 6.2 (slotted, kernel
     granularity, preemptive, every kernel at its own knee) and under D-STACK
     in simulate mode (plan + FOD, model granularity, non-preemptive) with the
     same batches, requests always waiting.  Both take their times from the

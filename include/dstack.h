@@ -75,15 +75,26 @@ const char* dstack_last_error(void);
  * has bits 8j..8j+7 set for every slot j (mask bit i selects CU i/8 of XCD
  * i%8).  Several partitions may overlap; keeping concurrent ones disjoint
  * is the scheduler's job.
+ * At most 4 partitions may be live at once in a process (a CU-masked stream
+ * has a hardware queue of its own; a run with five live masked streams stopped
+ * making progress on MI355X, runs with four completed).  A fifth create call
+ * returns E_UNSUPPORTED before any stream is made.  The library's own calls
+ * count too: a knee sweep or search needs 1 free, dstack_switch_probe 2,
+ * dstack_serve one per model.
  * dstack_partition_query: n_cu, the 8 CU-mask words and the hipStream_t (as
  *   void*, usable with torch.cuda.ExternalStream).  Any out pointer may be
- *   NULL. */
+ *   NULL.
+ * dstack_partition_count: live partitions and the limit (either may be NULL).
+ * dstack_partition_destroy waits for the partition's stream, frees the
+ *   workspaces that models hold for it (activations, split-K slices,
+ *   captured graphs) and destroys the stream. */
 dstack_status dstack_fraction_to_slots(double cu_fraction, int* slots);
 dstack_status dstack_partition_create(double cu_fraction, dstack_partition* out);
 dstack_status dstack_partition_create_at(int slot_offset, int n_slots, dstack_partition* out);
 dstack_status dstack_partition_create_mask(uint32_t slot_mask, dstack_partition* out);
 dstack_status dstack_partition_query(dstack_partition p, int* n_cu, uint32_t mask_words[8], void** hip_stream);
 dstack_status dstack_synchronize(dstack_partition p);
+dstack_status dstack_partition_count(int* live, int* max_live);
 void dstack_partition_destroy(dstack_partition p);
 
 /* Probe (verification of the slot -> CU mapping): launches n_blocks
@@ -176,7 +187,7 @@ dstack_status dstack_profile_layers(dstack_model m, int batch, const void* d_in,
                                     dstack_layer_time* out, int max_layers, int* n_layers);
 
 /* Launch shapes of one forward (the per-kernel parallelism N_i of Sec.
- * 4.2's analytical model, taken from this library's own kernels): one entry
+ * 4.3's analytical model, taken from this library's own kernels): one entry
  * per timed unit of dstack_profile_layers, in the same order, with the
  * unit's kernel class, its number of kernel launches, the workgroups of its
  * largest launch and how many of those workgroups one CU holds at once
@@ -261,7 +272,7 @@ dstack_status dstack_knee_search(dstack_model m, int batch, const double* fracti
                                  int warmup, int reps, dstack_knee_search_result* out);
 
 /* ------------------------------------------------------------------ */
-/* Analytical DNN model (Sec. 4.2, Eqs. layer_num_ops,                  */
+/* Analytical DNN model (Sec. 4.3, Eqs. layer_num_ops,                  */
 /* execution_time_per_layer, memory_latency,                           */
 /* total_non_paralleizable_time, total_time_shrinking_kernel;          */
 /* Eq. first_order_derivative), host only                              */
@@ -416,7 +427,7 @@ dstack_status dstack_schedule(const dstack_sched_model* models, int n_models, co
  * FNV-1a (64-bit) over (start, model, batch, slot mask, duration, kind) of
  * every started job, kind 0 planned / 1 FOD, each as 8 little-endian bytes.
  *
- * policy selects the scheduler (Sec. 7's comparators; dstack_serve takes
+ * policy selects the scheduler (Sec. 6.3's comparators; dstack_serve takes
  * 0 only): 0 D-STACK (the plan plus the FOD fill above); 1 max-throughput
  * and 2 max-min fair run no plan, only the fill on every trigger (fod is
  * ignored) with no planned start to respect and the candidates in another
@@ -449,7 +460,7 @@ typedef struct {
 dstack_status dstack_simulate(const dstack_sched_model* models, int n_models, const dstack_sched_params* params,
                               const dstack_sim_params* sim, dstack_run_out* out);
 
-/* The ideal spatio-temporal schedule of Sec. 7 (Eqs. maximization and
+/* The ideal spatio-temporal schedule of Sec. 6.2 (Eqs. maximization and
  * constraints): time slots of slot_us, kernel granularity, preemption.
  * Model i runs forwards of n_kernels kernels in order, kernel k at its own
  * knee share slots[k] (1..total) for dur_us[k] >= 1 us, batch items each;
@@ -539,7 +550,8 @@ dstack_status dstack_serve(const dstack_model* models, int n_models, const void*
  *   C % 8 == 0 and K % 4 == 0 (else E_UNSUPPORTED); res may be NULL;
  *   out_fp32 selects an fp32 instead of bf16 output.  The tile plan is
  *   chosen for the CUs the stream's CU mask enables (the whole device for
- *   the null stream); no split-K workspace is used here.
+ *   the null stream); no split-K workspace is used here (dstack_op_conv2d_ws
+ *   takes one).
  * dwconv3x3: per-channel 3x3, pad 1, stride 1 or 2, w [3][3][C] (device
  *   layout), then scale/shift and act; C % 8 == 0.
  * fc: y[b][o] = act(sum_i x[b][i] * w[o][i] + bias[o]); batch 1..32,
@@ -558,6 +570,47 @@ dstack_status dstack_serve(const dstack_model* models, int n_models, const void*
 dstack_status dstack_op_conv2d(const void* x, int N, int H, int W, int C, const void* w, int K, int R, int S,
                                int stride, int pad, const float* scale, const float* shift, const void* res, int act,
                                void* y, int out_fp32, void* stream);
+/* conv2d_ws: conv2d with the library's depth split (split-K): the depth
+ *   R*S*C is cut into `splits` slices run by separate workgroups, each writes
+ *   fp32 partial sums, and the last workgroup of each output tile (counted
+ *   by a per-tile arrival counter) sums the slices in slice order and applies
+ *   the epilogue, all in one kernel launch.  The plan (tile, splits, LDS ring)
+ *   is chosen for n_cu CUs (n_cu <= 0: the CUs of the stream's CU mask), as
+ *   dstack_conv2d_plan reports.  workspace (device, 256-byte aligned, caller
+ *   owned, may be NULL) = 16 KiB of arrival counters followed by the slices;
+ *   the counters must be zero before the first call that uses the workspace
+ *   and every call leaves them zero.  A workspace smaller than the plan's
+ *   workspace_bytes (or NULL) runs fewer splits (same result up to fp32
+ *   summation order).  out_fp32 never splits.  Calls sharing a workspace must
+ *   not overlap in time.
+ * conv2d_plan (host only): the launch dstack_op_conv2d_ws takes for a shape
+ *   on n_cu CUs (<= 0: 256) with a workspace of `workspace_bytes` bytes
+ *   (SIZE_MAX: unlimited), and the workspace that plan needs (0 without a
+ *   split).  Same shape checks as conv2d.
+ * arch_convs (host only): the implicit-GEMM convolutions of one forward of
+ *   an architecture at `batch`, in launch order, as conv2d arguments (the
+ *   LSTM's input projections as 1x1 convolutions over T*batch pixels with an
+ *   fp32 output); fills at most max_convs, *n_convs = the total. */
+typedef struct {
+  int kernel;          /* 0: tiled implicit GEMM; 1: streaming 1x1 (C <= 32) */
+  int mode;            /* activation addressing: 0 1x1 strided, 1 C % 64 == 0, 2 general, 3 1x1 stride 1 */
+  int tile_n, tile_m;  /* output channels x output pixels per workgroup (kernel 1: channels per wave, 0) */
+  int splits;          /* depth slices (1: no split) */
+  int tiles_per_split; /* 64-deep depth tiles per slice */
+  int stages;          /* LDS ring depth (kernel 0) */
+  int pad;
+  size_t workspace_bytes;
+} dstack_conv_plan;
+typedef struct {
+  int N, H, W, C, K, R, S, stride, pad, act, has_residual, out_fp32;
+} dstack_conv_shape;
+dstack_status dstack_op_conv2d_ws(const void* x, int N, int H, int W, int C, const void* w, int K, int R, int S,
+                                  int stride, int pad, const float* scale, const float* shift, const void* res,
+                                  int act, void* y, int out_fp32, int n_cu, void* workspace, size_t workspace_bytes,
+                                  void* stream);
+dstack_status dstack_conv2d_plan(int N, int H, int W, int C, int K, int R, int S, int stride, int pad, int act,
+                                 int out_fp32, int n_cu, size_t workspace_bytes, dstack_conv_plan* out);
+dstack_status dstack_arch_convs(const char* arch, int batch, dstack_conv_shape* out, int max_convs, int* n_convs);
 /* conv2d_rgb: the conv2d above for a 3-channel image x [N][H][W][3] read as
  *   it is (the stems of Sec. 3's CNNs; no packing to 8 channels), with
  *   weights w4 [K][R][R][4] bf16 (channel 3 zero: the stem layout the

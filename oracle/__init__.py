@@ -9,7 +9,7 @@ code with the HIP library and never imports it.
   with gcc into ``liboracle.so``.
 * ``sched.py`` -- the scheduling decisions (knee, SLO-constrained batch
   optimisation, spatio-temporal session plan, utilisation) in integer Python.
-* ``knee_model.py`` -- the analytical DNN latency model of Sec. 4.2 and its
+* ``knee_model.py`` -- the analytical DNN latency model of Sec. 4.3 and its
   knee in plain fp64 Python.
 """
 import ctypes

@@ -1,11 +1,11 @@
-"""Analytical DNN latency model and its knee (Sec. 4.2), plain fp64 Python.
+"""Analytical DNN latency model and its knee (Sec. 4.3), plain fp64 Python.
 
 TEST INFRASTRUCTURE ONLY (see the package docstring).  This is the slow,
 literal statement of the model the library's ``dstack_knee_model_*`` calls
 must reproduce exactly (same operations in the same order, so the fp64
 results are equal bit for bit).
 
-The model (Sec. 4.2):
+The model (Sec. 4.3):
 * Eq. layer_num_ops: the parallelizable operations of kernel i are
   N_1 = p*b and N_i = floor(N_{i-1} - p*b/Kmax) for i >= 2;
 * W_i = N_i * t_p (the kernel's parallel work);

@@ -368,7 +368,7 @@ static const int R50_STAGES[4][3] = {{3, 64, 1}, {4, 128, 2}, {6, 256, 2}, {3, 5
 /* MobileNetV2 inverted-residual table (t, c, n, s) */
 static const int MBV2_CFG[7][4] = {{1, 16, 1, 1}, {6, 24, 2, 2}, {6, 32, 3, 2}, {6, 64, 4, 2},
                                    {6, 96, 3, 1}, {6, 160, 3, 2}, {6, 320, 1, 1}};
-/* VGG-19 conv channels per stage (4 stages of 2/2/4/4/4 convs) */
+/* VGG-19 conv channels per stage (5 stages of 2/2/4/4/4 convs) */
 static const int VGG_STAGE_CONVS[5] = {2, 2, 4, 4, 4};
 static const int VGG_STAGE_CH[5] = {64, 128, 256, 512, 512};
 /* BERT-base: 12 layers, width 768, 12 heads of 64, feed-forward 3072,

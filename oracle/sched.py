@@ -381,7 +381,7 @@ def simulate(models, period, duration, arrivals, total=TOTAL_SLOTS, overprov=OVE
     Returns dict with per-model counters, utilisation_ppm and a hash of the job log.
 
     policy "dstack": the session plan plus the FOD fill (Sec. 6.1.2).  The
-    comparators of Sec. 7 run the same fill with no plan and another order
+    comparators of Sec. 6.3 run the same fill with no plan and another order
     of the candidates (a reading: each is a non-preemptive greedy fill at the
     model's deployed share and largest queued grid batch):
     "maxthroughput" -- least runtime first (the model's SLO-optimal latency
@@ -530,7 +530,7 @@ def simulate(models, period, duration, arrivals, total=TOTAL_SLOTS, overprov=OVE
 
 
 def simulate_ideal(models, horizon, slot, total=TOTAL_SLOTS):
-    """The ideal spatio-temporal schedule of Sec. 7 (Eqs. maximization and
+    """The ideal spatio-temporal schedule of Sec. 6.2 (Eqs. maximization and
     constraints), time-slotted at kernel granularity with preemption.
 
     models: dicts with "slots" and "dur" (per kernel of one forward: its knee

@@ -134,6 +134,16 @@ class RunOut(ctypes.Structure):
                 ("job_hash", ctypes.c_uint64), ("last_end_us", ctypes.c_int64)]
 
 
+class ConvPlan(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int) for n in ("kernel", "mode", "tile_n", "tile_m", "splits", "tiles_per_split",
+                                            "stages", "pad")] + [("workspace_bytes", ctypes.c_size_t)]
+
+
+class ConvShape(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int) for n in ("N", "H", "W", "C", "K", "R", "S", "stride", "pad", "act",
+                                            "has_residual", "out_fp32")]
+
+
 _lib = None
 _vp, _i, _d, _u64, _sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_double, ctypes.c_uint64, ctypes.c_size_t
 _fp = ctypes.POINTER(ctypes.c_float)
@@ -146,6 +156,7 @@ _SIGS = {
     "dstack_partition_create_mask": ([ctypes.c_uint32, ctypes.POINTER(_vp)], _i),
     "dstack_partition_query": ([_vp, ctypes.POINTER(_i), ctypes.POINTER(ctypes.c_uint32), ctypes.POINTER(_vp)], _i),
     "dstack_synchronize": ([_vp], _i),
+    "dstack_partition_count": ([ctypes.POINTER(_i), ctypes.POINTER(_i)], _i),
     "dstack_partition_destroy": ([_vp], None),
     "dstack_probe_cu_ids": ([_vp, _i, _i, ctypes.POINTER(ctypes.c_uint32)], _i),
     "dstack_model_load": ([ctypes.c_char_p, _u64, ctypes.POINTER(_vp)], _i),
@@ -173,6 +184,10 @@ _SIGS = {
                       ctypes.POINTER(SchedParams), ctypes.POINTER(SimParams), ctypes.POINTER(RunOut),
                       ctypes.POINTER(JobRecord), _i, ctypes.POINTER(_i)], _i),
     "dstack_op_conv2d": ([_vp, _i, _i, _i, _i, _vp, _i, _i, _i, _i, _i, _vp, _vp, _vp, _i, _vp, _i, _vp], _i),
+    "dstack_op_conv2d_ws": ([_vp, _i, _i, _i, _i, _vp, _i, _i, _i, _i, _i, _vp, _vp, _vp, _i, _vp, _i, _i, _vp, _sz,
+                             _vp], _i),
+    "dstack_conv2d_plan": ([_i, _i, _i, _i, _i, _i, _i, _i, _i, _i, _i, _i, _sz, ctypes.POINTER(ConvPlan)], _i),
+    "dstack_arch_convs": ([ctypes.c_char_p, _i, ctypes.POINTER(ConvShape), _i, ctypes.POINTER(_i)], _i),
     "dstack_op_conv2d_rgb": ([_vp, _i, _i, _i, _vp, _i, _i, _i, _i, _vp, _vp, _i, _vp, _vp], _i),
     "dstack_op_dwconv3x3": ([_vp, _i, _i, _i, _i, _vp, _i, _vp, _vp, _i, _vp, _vp], _i),
     "dstack_op_expand_dw": ([_vp, _i, _i, _i, _i, _vp, _i, _vp, _vp, _i, _vp, _i, _vp, _vp, _i, _vp, _vp], _i),
@@ -554,6 +569,43 @@ def conv2d(x, w, K, R, S, stride, pad, scale, shift, res, act, y, out_fp32=False
     N, H, W, C = x.shape
     _check(lib().dstack_op_conv2d(_ptr(x), N, H, W, C, _ptr(w), K, R, S, stride, pad, _ptr(scale), _ptr(shift),
                                   _ptr(res), act, _ptr(y), int(out_fp32), _stream(stream)))
+
+
+def conv2d_ws(x, w, K, R, S, stride, pad, scale, shift, res, act, y, workspace, out_fp32=False, n_cu=0,
+              stream=None):
+    """conv2d with the depth split; workspace: a 256-byte aligned device
+    buffer (torch tensor or None) whose first 16 KiB are zero before its first use."""
+    N, H, W, C = x.shape
+    wsb = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    _check(lib().dstack_op_conv2d_ws(_ptr(x), N, H, W, C, _ptr(w), K, R, S, stride, pad, _ptr(scale), _ptr(shift),
+                                     _ptr(res), act, _ptr(y), int(out_fp32), int(n_cu), _ptr(workspace), wsb,
+                                     _stream(stream)))
+
+
+UNLIMITED = ctypes.c_size_t(-1).value
+
+
+def conv2d_plan(N, H, W, C, K, R, S, stride, pad, act=0, out_fp32=False, n_cu=0, workspace_bytes=UNLIMITED):
+    p = ConvPlan()
+    _check(lib().dstack_conv2d_plan(N, H, W, C, K, R, S, stride, pad, act, int(out_fp32), int(n_cu),
+                                    workspace_bytes, ctypes.byref(p)))
+    return dict((f, getattr(p, f)) for f, _ in ConvPlan._fields_ if f != "pad")
+
+
+def arch_convs(arch, batch):
+    """The implicit-GEMM convolutions of one forward (host only), as dicts of conv2d arguments."""
+    n = ctypes.c_int()
+    _check(lib().dstack_arch_convs(arch.encode(), batch, None, 0, ctypes.byref(n)))
+    out = (ConvShape * n.value)()
+    _check(lib().dstack_arch_convs(arch.encode(), batch, out, n.value, ctypes.byref(n)))
+    return [dict((f, getattr(c, f)) for f, _ in ConvShape._fields_) for c in out]
+
+
+def partition_count():
+    """(live partitions, the limit)."""
+    a, b = ctypes.c_int(), ctypes.c_int()
+    _check(lib().dstack_partition_count(ctypes.byref(a), ctypes.byref(b)))
+    return a.value, b.value
 
 
 def conv2d_rgb(x, w4, K, R, stride, pad, scale, shift, act, y, stream=None):

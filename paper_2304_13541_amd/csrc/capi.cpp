@@ -8,8 +8,11 @@
 #include <atomic>
 #include <cmath>
 #include <cstdlib>
+#include <cstdint>
 #include <cstring>
+#include <mutex>
 #include <new>
+#include <set>
 #include <string>
 #include <vector>
 
@@ -42,7 +45,24 @@ struct dstack_model_s {
 
 namespace {
 
-std::atomic<int> g_next_partition_id{1};
+// Partition ids start at 16: workspace ids below that are the library's own
+// (knee sweeps, GPU% change probes), never a partition's.
+std::atomic<int> g_next_partition_id{16};
+
+// Live partitions.  Each owns one CU-masked HIP stream, and a CU-masked
+// stream gets a hardware queue of its own.  A run with five live masked
+// streams (four of them busy) beside one unmasked stream stopped making
+// progress, while runs with up to four live masked streams (all of them busy
+// at once) completed; the cause is not known, so a fifth live partition is
+// refused before its stream is created.
+constexpr int kMaxLivePartitions = 4;
+std::mutex g_part_mu;
+int g_live_partitions = 0;
+
+// Loaded models, so that destroying a partition can release the workspaces
+// (activations, split-K slices, captured graphs) each model holds for it.
+std::mutex g_model_mu;
+std::set<dstack_model_s*> g_models;
 
 template <typename F>
 dstack_status guarded(F&& f) {
@@ -61,7 +81,22 @@ dstack_status guarded(F&& f) {
 dstack_status make_partition(uint32_t slot_mask, dstack_partition* out) {
   DS_CHECK(out, DSTACK_E_INVALID, "partition: null out pointer");
   DS_CHECK(slot_mask != 0, DSTACK_E_INVALID, "partition: empty slot set");
-  auto* p = new dstack_partition_s();
+  {
+    std::lock_guard<std::mutex> g(g_part_mu);
+    DS_CHECK(g_live_partitions < kMaxLivePartitions, DSTACK_E_UNSUPPORTED,
+             "partition: at most " + std::to_string(kMaxLivePartitions) +
+                 " live partitions (CU-masked streams); destroy one first");
+    ++g_live_partitions;  // reserved before the stream exists
+  }
+  auto unreserve = [] {
+    std::lock_guard<std::mutex> g(g_part_mu);
+    --g_live_partitions;
+  };
+  auto* p = new (std::nothrow) dstack_partition_s();
+  if (!p) {
+    unreserve();
+    return fail(DSTACK_E_OOM, "partition: host allocation failed");
+  }
   p->id = g_next_partition_id++;
   p->slot_mask = slot_mask;
   p->n_slots = __builtin_popcount(slot_mask);
@@ -73,6 +108,7 @@ dstack_status make_partition(uint32_t slot_mask, dstack_partition* out) {
   hipError_t e = hipExtStreamCreateWithCUMask(&p->stream, 8, p->words);
   if (e != hipSuccess) {
     delete p;
+    unreserve();
     return hip_fail(e, "hipExtStreamCreateWithCUMask");
   }
   *out = p;
@@ -136,11 +172,26 @@ dstack_status dstack_synchronize(dstack_partition p) {
   });
 }
 
+dstack_status dstack_partition_count(int* live, int* max_live) {
+  return guarded([&] {
+    std::lock_guard<std::mutex> g(g_part_mu);
+    if (live) *live = g_live_partitions;
+    if (max_live) *max_live = kMaxLivePartitions;
+    return DSTACK_OK;
+  });
+}
+
 void dstack_partition_destroy(dstack_partition p) {
   if (!p) return;
   (void)hipStreamSynchronize(p->stream);
+  {
+    std::lock_guard<std::mutex> g(g_model_mu);
+    for (dstack_model_s* h : g_models) release_workspace(h->m, p->id);
+  }
   (void)hipStreamDestroy(p->stream);
   delete p;
+  std::lock_guard<std::mutex> g(g_part_mu);
+  --g_live_partitions;
 }
 
 dstack_status dstack_probe_cu_ids(dstack_partition p, int n_blocks, int via_graph, uint32_t* host_out) {
@@ -188,6 +239,10 @@ dstack_status dstack_model_load(const char* arch, uint64_t seed, dstack_model* o
       delete h;
       set_error(msg);
       return s;
+    }
+    {
+      std::lock_guard<std::mutex> g(g_model_mu);
+      g_models.insert(h);
     }
     *out = h;
     return DSTACK_OK;
@@ -260,6 +315,10 @@ dstack_status dstack_model_export_params(dstack_model h, int idx, void* dst, siz
 void dstack_model_destroy(dstack_model h) {
   if (!h) return;
   (void)hipDeviceSynchronize();
+  {
+    std::lock_guard<std::mutex> g(g_model_mu);
+    g_models.erase(h);
+  }
   delete h;
 }
 
@@ -742,6 +801,84 @@ dstack_status dstack_op_conv2d(const void* x, int N, int H, int W, int C, const 
     return launch_conv2d(static_cast<const bf16*>(x), N, H, W, C, static_cast<const bf16*>(w), K, R, S, stride, pad,
                          scale, shift, static_cast<const bf16*>(res), act, y, out_fp32 != 0,
                          stream_cu_count((hipStream_t)stream), (hipStream_t)stream);
+  });
+}
+
+namespace {
+
+constexpr size_t kConvCounterBytes = SPLITK_TILE_COUNTERS * sizeof(unsigned);  // 16 KiB, 256-aligned
+
+void fill_conv_plan(const ConvLaunchPlan& p, dstack_conv_plan* out) {
+  std::memset(out, 0, sizeof(*out));
+  out->kernel = p.kernel;
+  out->mode = p.mode;
+  out->tile_n = p.bn;
+  out->tile_m = p.bm;
+  out->splits = p.splits;
+  out->tiles_per_split = p.kt_per_split;
+  out->stages = p.stages;
+  out->workspace_bytes = p.splits > 1 ? kConvCounterBytes + p.split_bytes : 0;
+}
+
+// slice bytes a workspace of `bytes` leaves after its counters
+size_t slice_room(const void* ws, size_t bytes) { return ws && bytes > kConvCounterBytes ? bytes - kConvCounterBytes : 0; }
+
+}  // namespace
+
+dstack_status dstack_conv2d_plan(int N, int H, int W, int C, int K, int R, int S, int stride, int pad, int act,
+                                 int out_fp32, int n_cu, size_t workspace_bytes, dstack_conv_plan* out) {
+  return guarded([&] {
+    DS_CHECK(out, DSTACK_E_INVALID, "conv2d_plan: null pointer");
+    ConvLaunchPlan p;
+    dstack_status s = conv2d_plan(N, H, W, C, K, R, S, stride, pad, act, out_fp32 != 0, n_cu,
+                                  workspace_bytes > kConvCounterBytes ? workspace_bytes - kConvCounterBytes : 0, &p);
+    if (s != DSTACK_OK) return s;
+    fill_conv_plan(p, out);
+    return DSTACK_OK;
+  });
+}
+
+dstack_status dstack_op_conv2d_ws(const void* x, int N, int H, int W, int C, const void* w, int K, int R, int S,
+                                  int stride, int pad, const float* scale, const float* shift, const void* res,
+                                  int act, void* y, int out_fp32, int n_cu, void* workspace, size_t workspace_bytes,
+                                  void* stream) {
+  return guarded([&] {
+    DS_CHECK(x && w && y, DSTACK_E_INVALID, "conv2d_ws: null pointer");
+    DS_CHECK(act >= 0 && act <= 4, DSTACK_E_INVALID, "conv2d_ws: act must be 0..4");
+    DS_CHECK(!workspace || ((uintptr_t)workspace % 256) == 0, DSTACK_E_INVALID,
+             "conv2d_ws: workspace must be 256-byte aligned");
+    const int cus = n_cu > 0 ? n_cu : stream_cu_count((hipStream_t)stream);
+    char* base = static_cast<char*>(workspace);
+    const size_t room = slice_room(workspace, workspace_bytes);
+    return launch_conv2d_ws(static_cast<const bf16*>(x), N, H, W, C, static_cast<const bf16*>(w), K, R, S, stride,
+                            pad, scale, shift, static_cast<const bf16*>(res), act, y, out_fp32 != 0, cus,
+                            room ? reinterpret_cast<float*>(base + kConvCounterBytes) : nullptr, room,
+                            room ? reinterpret_cast<unsigned*>(base) : nullptr, (hipStream_t)stream);
+  });
+}
+
+dstack_status dstack_arch_convs(const char* arch, int batch, dstack_conv_shape* out, int max_convs, int* n_convs) {
+  return guarded([&] {
+    DS_CHECK(arch && n_convs && (out || max_convs == 0), DSTACK_E_INVALID, "arch_convs: null pointer");
+    Model m;
+    dstack_status s = build_arch(arch, m);
+    if (s != DSTACK_OK) return s;
+    DS_CHECK(batch >= 1 && batch <= m.max_batch, DSTACK_E_INVALID, "arch_convs: batch out of range");
+    int n = 0;
+    auto put = [&](const dstack_conv_shape& c) {
+      if (n < max_convs) out[n] = c;
+      ++n;
+    };
+    for (const Op& op : m.ops) {
+      if (op.kind == OP_CONV) {
+        put(dstack_conv_shape{batch, op.H, op.W, op.C, op.K, op.R, op.S, op.stride, op.pad, op.act,
+                              op.res != BUF_NONE ? 1 : 0, 0});
+      } else if (op.kind == OP_LSTM) {  // the input projection of all steps: a 1x1 convolution with fp32 output
+        put(dstack_conv_shape{op.T * batch, 1, 1, op.I, 4 * op.Hd, 1, 1, 1, 0, ACT_NONE, 0, 1});
+      }
+    }
+    *n_convs = n;
+    return DSTACK_OK;
   });
 }
 

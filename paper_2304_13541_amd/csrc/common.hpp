@@ -76,7 +76,7 @@ inline void launch(void (*kernel)(KArgs...), dim3 grid, dim3 block, size_t shmem
   hipLaunchKernelGGL(kernel, grid, block, shmem, st, args...);
 }
 
-// Analytical DNN model (Sec. 4.2); the C ABI wraps these.
+// Analytical DNN model (Sec. 4.3); the C ABI wraps these.
 dstack_status knee_model_sequence(int p, int b, int kmax, double* n_out);
 dstack_status knee_model_eval(const dstack_knee_model* km, const int* s_values, int n_s, double* et_out,
                               int* knee_index);
@@ -117,6 +117,20 @@ __device__ __forceinline__ float apply_act(float v, int act) {
 
 // split-K arrival counters per model workspace (conv tiles of one launch)
 constexpr int SPLITK_TILE_COUNTERS = 4096;
+
+// The launch a convolution gets: kernel 0 = the tiled implicit GEMM (tile
+// bn x bm, split-K slices of kt_per_split depth tiles, an LDS ring of
+// `stages` tiles, activation addressing `mode`), 1 = the streaming 1x1
+// kernel of small depth (bn = channels per wave); split_bytes = fp32 slice
+// bytes of a split plan (0 without a split).
+struct ConvLaunchPlan {
+  int kernel, mode, bn, bm, splits, kt_per_split, stages;
+  size_t split_bytes;
+};
+// Host only: the plan launch_conv2d_ws would take on n_cu CUs with
+// split_bytes of slice workspace (and arrival counters).
+dstack_status conv2d_plan(int N, int H, int W, int C, int K, int R, int S, int stride, int pad, int act,
+                          bool out_fp32, int n_cu, size_t split_bytes, ConvLaunchPlan* out);
 
 // ---- kernel launchers (defined in the .hip files) ----
 dstack_status launch_conv2d(const bf16* x, int N, int H, int W, int C, const bf16* w, int K, int R, int S,

@@ -8,7 +8,7 @@
 //   depth   = (r, s, c)                (Kg = R*S*C, contiguous in both operands)
 // The weight row for channel k is contiguous over (r,s,c); the im2col row of
 // a pixel is gathered on the fly, 8 channels (16 bytes) at a time, which
-// needs C % 8 == 0 (3-channel stems are zero-padded to 8 before the call).
+// needs C % 8 == 0 (3-channel stems run in the direct RGB kernel instead).
 //
 // Data movement.  Each depth tile (BK = 64) of both operands is copied from
 // global memory straight into LDS with buffer_load_dwordx4 ... lds: a wave's
@@ -789,12 +789,8 @@ constexpr int conv_stages(int bn, int bm) {
 }
 
 template <int BN, int BM, int WN, int WM, int MODE>
-static void launch_mode(ConvArgs a, bool f32, int splits, hipStream_t st) {
-#ifdef DS_CONV_STAGES
-  constexpr int STAGES = DS_CONV_STAGES;
-#else
+static void launch_mode(ConvArgs a, bool f32, int splits, int stages, hipStream_t st) {
   constexpr int STAGES = conv_stages(BN, BM);
-#endif
   a.tiles_n = ceil_div(a.K, BN);
   a.tiles = ceil_div(a.M, BM) * a.tiles_n;
   a.div_tn = FastDiv::make(a.tiles_n);
@@ -802,7 +798,7 @@ static void launch_mode(ConvArgs a, bool f32, int splits, hipStream_t st) {
   // with dispatch events armed: both on this kernel (the split-K reduction is in it)
   const DispatchEvents& de = dispatch_events();
   hipEvent_t e0 = de.start, e1 = de.stop;
-  if (STAGES > 2 && short_ring(a.kt_per_split, splits, (long)a.tiles * splits, a.n_cu)) {
+  if (STAGES > 2 && stages == 2) {
     if (splits > 1)
       launch_k(conv_igemm_kernel<BN, BM, WN, WM, 2, MODE, false, true>, grid, st, e0, e1, a);
     else if (f32)
@@ -818,73 +814,116 @@ static void launch_mode(ConvArgs a, bool f32, int splits, hipStream_t st) {
 }
 
 template <int BN, int BM, int WN, int WM>
-static void launch_cfg(const ConvArgs& a, int mode, bool f32, int splits, hipStream_t st) {
+static void launch_cfg(const ConvArgs& a, int mode, bool f32, int splits, int stages, hipStream_t st) {
   if (mode == MODE_1X1S1)
-    launch_mode<BN, BM, WN, WM, MODE_1X1S1>(a, f32, splits, st);
+    launch_mode<BN, BM, WN, WM, MODE_1X1S1>(a, f32, splits, stages, st);
   else if (mode == MODE_1X1)
-    launch_mode<BN, BM, WN, WM, MODE_1X1>(a, f32, splits, st);
+    launch_mode<BN, BM, WN, WM, MODE_1X1>(a, f32, splits, stages, st);
   else if (mode == MODE_TILED)
-    launch_mode<BN, BM, WN, WM, MODE_TILED>(a, f32, splits, st);
+    launch_mode<BN, BM, WN, WM, MODE_TILED>(a, f32, splits, stages, st);
   else
-    launch_mode<BN, BM, WN, WM, MODE_GENERIC>(a, f32, splits, st);
+    launch_mode<BN, BM, WN, WM, MODE_GENERIC>(a, f32, splits, stages, st);
+}
+
+// Checks a convolution's shape and fills the launch arguments it implies
+// (everything but the pointers).
+static dstack_status conv_shape(int N, int H, int W, int C, int K, int R, int S, int stride, int pad, int act,
+                                int n_cu, ConvArgs* a) {
+  DS_CHECK(C % 8 == 0, DSTACK_E_UNSUPPORTED, "conv2d: C must be a multiple of 8");
+  DS_CHECK(K % 4 == 0, DSTACK_E_UNSUPPORTED, "conv2d: K must be a multiple of 4");
+  DS_CHECK(N > 0 && H > 0 && W > 0 && K > 0 && R > 0 && S > 0 && stride > 0 && pad >= 0, DSTACK_E_INVALID,
+           "conv2d: bad shape");
+  DS_CHECK(act >= ACT_NONE && act <= ACT_TANH, DSTACK_E_INVALID, "conv2d: act must be 0..4");
+  a->N = N; a->H = H; a->W = W; a->C = C; a->K = K; a->R = R; a->S = S; a->stride = stride; a->pad = pad;
+  a->Ho = out_dim(H, R, stride, pad);
+  a->Wo = out_dim(W, S, stride, pad);
+  DS_CHECK(a->Ho > 0 && a->Wo > 0, DSTACK_E_INVALID, "conv2d: empty output");
+  // buffer offsets are 32-bit with bit 31 reserved as the out-of-range marker
+  DS_CHECK((long)N * H * W * C * 2 < (1L << 31) && (long)N * a->Ho * a->Wo * K < (1L << 31) &&
+               (long)K * R * S * C * 2 < (1L << 31),
+           DSTACK_E_UNSUPPORTED, "conv2d: tensor too large for 31-bit byte offsets");
+  a->M = N * a->Ho * a->Wo;
+  a->Kg = R * S * C;
+  a->act = act;
+  a->n_cu = n_cu <= 0 ? 256 : n_cu;  // unknown: plan for the whole device
+  return DSTACK_OK;
+}
+
+// The launch a convolution gets: the streaming 1x1 kernel, or the tiled
+// kernel with its tile, split and ring depth.  Split-K is considered only
+// with a workspace and arrival counters, and not for an fp32 output (the
+// fused reduction stores bf16).
+static ConvLaunchPlan conv_launch_plan(const ConvArgs& a, bool out_fp32, bool can_split, size_t split_bytes) {
+  ConvLaunchPlan L{};
+  const bool one = a.R == 1 && a.S == 1 && a.pad == 0;
+  if (one && a.stride == 1 && a.C <= 32 && a.K % 16 == 0 && a.act <= ACT_RELU6) {  // small depth: streaming
+    L.kernel = 1;
+    int nb = 8;
+    while ((a.K / 16) % nb) --nb;
+    L.bn = 16 * nb;
+    L.mode = MODE_1X1S1;
+    L.splits = 1;
+    return L;
+  }
+  L.kernel = 0;
+  L.mode = one ? (a.stride == 1 ? MODE_1X1S1 : MODE_1X1) : (a.C % BK == 0 && a.R * a.S <= 32 ? MODE_TILED : MODE_GENERIC);
+  const ConvPlan p = choose_plan(a.M, a.K, a.Kg, a.n_cu, can_split && !out_fp32, split_bytes);
+  const int nkt = ceil_div(a.Kg, BK);
+  L.kt_per_split = ceil_div(nkt, p.splits);
+  L.splits = ceil_div(nkt, L.kt_per_split);  // no empty slices
+  L.bn = p.bn;
+  L.bm = p.bm;
+  const long tiles = (long)ceil_div(a.M, p.bm) * ceil_div(a.K, p.bn);
+  L.stages = conv_stages(p.bn, p.bm);
+  if (L.stages > 2 && short_ring(L.kt_per_split, L.splits, tiles * L.splits, a.n_cu)) L.stages = 2;
+  return L;
+}
+
+dstack_status conv2d_plan(int N, int H, int W, int C, int K, int R, int S, int stride, int pad, int act,
+                          bool out_fp32, int n_cu, size_t split_bytes, ConvLaunchPlan* out) {
+  ConvArgs a{};
+  dstack_status s = conv_shape(N, H, W, C, K, R, S, stride, pad, act, n_cu, &a);
+  if (s != DSTACK_OK) return s;
+  *out = conv_launch_plan(a, out_fp32, true, split_bytes);
+  out->split_bytes = out->splits > 1 ? (size_t)out->splits * a.M * a.K * sizeof(float) : 0;
+  return DSTACK_OK;
 }
 
 dstack_status launch_conv2d_ws(const bf16* x, int N, int H, int W, int C, const bf16* w, int K, int R, int S,
                                int stride, int pad, const float* scale, const float* shift, const bf16* res,
                                int act, void* y, bool out_fp32, int n_cu, float* splitk_ws, size_t splitk_bytes,
                                unsigned* tile_counters, hipStream_t st) {
-  DS_CHECK(C % 8 == 0, DSTACK_E_UNSUPPORTED, "conv2d: C must be a multiple of 8");
-  DS_CHECK(K % 4 == 0, DSTACK_E_UNSUPPORTED, "conv2d: K must be a multiple of 4");
-  DS_CHECK(N > 0 && H > 0 && W > 0 && K > 0 && R > 0 && S > 0 && stride > 0 && pad >= 0, DSTACK_E_INVALID,
-           "conv2d: bad shape");
-  DS_CHECK(act >= ACT_NONE && act <= ACT_TANH, DSTACK_E_INVALID, "conv2d: act must be 0..4");
-  ConvArgs a;
+  ConvArgs a{};
+  dstack_status s = conv_shape(N, H, W, C, K, R, S, stride, pad, act, n_cu, &a);
+  if (s != DSTACK_OK) return s;
   a.x = x; a.w = w; a.scale = scale; a.shift = shift; a.res = res; a.y = y; a.partial = nullptr;
-  a.N = N; a.H = H; a.W = W; a.C = C; a.K = K; a.R = R; a.S = S; a.stride = stride; a.pad = pad;
-  a.Ho = out_dim(H, R, stride, pad);
-  a.Wo = out_dim(W, S, stride, pad);
-  DS_CHECK(a.Ho > 0 && a.Wo > 0, DSTACK_E_INVALID, "conv2d: empty output");
-  // buffer offsets are 32-bit with bit 31 reserved as the out-of-range marker
-  DS_CHECK((long)N * H * W * C * 2 < (1L << 31) && (long)N * a.Ho * a.Wo * K < (1L << 31) &&
-               (long)K * R * S * C * 2 < (1L << 31),
-           DSTACK_E_UNSUPPORTED, "conv2d: tensor too large for 31-bit byte offsets");
-  a.M = N * a.Ho * a.Wo;
-  a.Kg = R * S * C;
-  a.act = act;
-  if (n_cu <= 0) n_cu = 256;  // unknown: plan for the whole device
-  a.n_cu = n_cu;
+  a.counters = nullptr;
   a.div_wo = FastDiv::make(a.Wo);
   a.div_ho = FastDiv::make(a.Ho);
   a.div_c = FastDiv::make(C);
   a.div_s = FastDiv::make(S);
-  const bool one = R == 1 && S == 1 && pad == 0;
-  if (one && stride == 1 && C <= 32 && K % 16 == 0 && act <= ACT_RELU6) {  // small depth: the streaming kernel
-    launch_1x1s(a, out_fp32, n_cu, st);
+  const ConvLaunchPlan p =
+      conv_launch_plan(a, out_fp32, splitk_ws != nullptr && tile_counters != nullptr, splitk_bytes);
+  if (p.kernel == 1) {
+    launch_1x1s(a, out_fp32, a.n_cu, st);
     DS_HIP(hipGetLastError());
     return DSTACK_OK;
   }
-  const int mode = one ? (stride == 1 ? MODE_1X1S1 : MODE_1X1)
-                       : (C % BK == 0 && R * S <= 32 ? MODE_TILED : MODE_GENERIC);
-  // split-K only with a workspace and the counters of the fused reduction
-  ConvPlan p = choose_plan(a.M, K, a.Kg, n_cu, splitk_ws != nullptr && tile_counters != nullptr, splitk_bytes);
-  int nkt = ceil_div(a.Kg, BK);
-  a.kt_per_split = ceil_div(nkt, p.splits);
-  p.splits = ceil_div(nkt, a.kt_per_split);  // no empty slices
-  a.counters = nullptr;
+  a.kt_per_split = p.kt_per_split;
   if (p.splits > 1) {
     a.partial = splitk_ws;
     a.counters = tile_counters;
   }
   if (p.bn == 128 && p.bm == 128)
-    launch_cfg<128, 128, 2, 2>(a, mode, out_fp32, p.splits, st);
+    launch_cfg<128, 128, 2, 2>(a, p.mode, out_fp32, p.splits, p.stages, st);
   else if (p.bn == 128 && p.bm == 64)
-    launch_cfg<128, 64, 2, 2>(a, mode, out_fp32, p.splits, st);
+    launch_cfg<128, 64, 2, 2>(a, p.mode, out_fp32, p.splits, p.stages, st);
   else if (p.bn == 64 && p.bm == 128)
-    launch_cfg<64, 128, 2, 2>(a, mode, out_fp32, p.splits, st);
+    launch_cfg<64, 128, 2, 2>(a, p.mode, out_fp32, p.splits, p.stages, st);
   else if (p.bn == 64 && p.bm == 64)
-    launch_cfg<64, 64, 2, 2>(a, mode, out_fp32, p.splits, st);
+    launch_cfg<64, 64, 2, 2>(a, p.mode, out_fp32, p.splits, p.stages, st);
   else
-    launch_cfg<32, 128, 1, 4>(a, mode, out_fp32, p.splits, st);
+    launch_cfg<32, 128, 1, 4>(a, p.mode, out_fp32, p.splits, p.stages, st);
   DS_HIP(hipGetLastError());
   return DSTACK_OK;
 }

@@ -1,4 +1,4 @@
-// Analytical DNN latency model and its knee (Sec. 4.2), host only.
+// Analytical DNN latency model and its knee (Sec. 4.3), host only.
 //
 // A DNN is a sequence of kernels; kernel i has N_i parallelizable operations
 // of t_p each (Eq. layer_num_ops generates the paper's synthetic sequence),

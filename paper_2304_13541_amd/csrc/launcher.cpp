@@ -281,7 +281,7 @@ dstack_status simulate(const dstack_sched_model* models, int n, const dstack_sch
   return DSTACK_OK;
 }
 
-// The ideal spatio-temporal schedule of Sec. 7 (Eqs. maximization and
+// The ideal spatio-temporal schedule of Sec. 6.2 (Eqs. maximization and
 // constraints): slotted, kernel granularity, preemptive; every slot runs the
 // subset of the models' current kernels with the largest summed share that
 // fits, found by exhaustive search (2^n subsets, n <= 8).

@@ -604,6 +604,15 @@ Model::~Model() {
 
 static size_t align256(size_t b) { return (b + 255) / 256 * 256; }
 
+void release_workspace(Model& m, int pid) {
+  std::lock_guard<std::mutex> g(m.ws_mu);
+  auto it = m.ws.find(pid);
+  if (it == m.ws.end() || it->second->busy.load()) return;
+  void* base = it->second->base;
+  m.ws.erase(it);  // destroys its graph execs
+  if (base) (void)hipFree(base);
+}
+
 dstack_status get_workspace(Model& m, int pid, int n_cu, hipStream_t st, Workspace** out) {
   std::lock_guard<std::mutex> g(m.ws_mu);
   auto it = m.ws.find(pid);

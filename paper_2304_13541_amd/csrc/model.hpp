@@ -130,6 +130,9 @@ dstack_status build_arch(const std::string& arch, Model& m);
 dstack_status upload_weights(Model& m);
 // Workspace for batch <= max_batch, on demand.
 dstack_status get_workspace(Model& m, int partition_id, int n_cu, hipStream_t st, Workspace** out);
+// Frees the workspace (and its captured graphs) kept for a partition id, if
+// any and not in use; called when the partition is destroyed.
+void release_workspace(Model& m, int partition_id);
 
 // Enqueue one forward pass on `st`.  `timer` may be null.
 dstack_status forward(Model& m, int batch, const void* d_in, void* d_out, Workspace& ws, int n_cu, hipStream_t st,

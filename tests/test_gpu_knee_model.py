@@ -1,5 +1,5 @@
 """Launch shapes of the library's own kernels (the per-kernel parallelism of
-Sec. 4.2's analytical model), through the C ABI on the GPU: one entry per
+Sec. 4.3's analytical model), through the C ABI on the GPU: one entry per
 timed unit of dstack_profile_layers with the same kind, FLOPs and bytes;
 workgroup counts of kernels whose grid has a closed form (pools, the
 depthwise kernel) equal that form; occupancy is at least one workgroup per

@@ -28,11 +28,13 @@ def env(oracle_mod):
 
 
 def sample_items(b, seed):
+    """{0, b-1} (the last item holds the ragged last pixel tile) plus two
+    seeded picks from the items between them; every item when b <= 4."""
+    if b <= 4:
+        return list(range(b))
     rng = np.random.default_rng(seed)
-    picks = {0, b - 1}
-    while len(picks) < min(b, 4):
-        picks.add(int(rng.integers(0, b)))
-    return sorted(picks)
+    picks = rng.choice(np.arange(1, b - 1), size=2, replace=False)
+    return sorted({0, b - 1} | {int(p) for p in picks})
 
 
 def run_model(env, arch, seed, batch, part):
@@ -80,28 +82,84 @@ def test_resnet50(env, batch, fraction):
     ds, gu, inputs, oracle, torch = env
     part = ds.Partition(fraction)
     m, xb, got = run_model(env, "resnet50", 1020, batch, part)
-    check_against_oracle(env, "resnet50", 1020, xb, got, sample_items(batch, 7)[:2])
+    check_against_oracle(env, "resnet50", 1020, xb, got, sample_items(batch, 7))
+
+
+@pytest.mark.parametrize("arch,seed,batch,fraction", [
+    ("resnet50", 1022, 16, 0.1), ("resnet50", 1022, 16, 0.5), ("resnet50", 1022, 16, 0.7),
+    ("mobilenetv2", 1033, 32, 0.5), ("mobilenetv2", 1033, 32, 1.0), ("vgg19", 1042, 8, 0.2),
+    ("vgg19", 1042, 8, 1.0), ("lstm2", 1043, 32, 1.0)])
+def test_models_at_more_fractions(env, arch, seed, batch, fraction):
+    """The launch plans change with the partition's CU count: the measured
+    workloads' batches at further points of the sweep grid."""
+    ds, gu, inputs, oracle, torch = env
+    part = ds.Partition(fraction)
+    m, xb, got = run_model(env, arch, seed, batch, part)
+    check_against_oracle(env, arch, seed, xb, got, sample_items(batch, seed))
+
+
+def test_partition_limit_refuses_fifth(env):
+    """At most four live partitions (CU-masked streams): the fifth create
+    call is refused with E_UNSUPPORTED before any stream exists, and the
+    count is back to where it was once they are destroyed."""
+    import gc
+    ds, gu, inputs, oracle, torch = env
+    gc.collect()
+    live0, limit = ds.partition_count()
+    assert limit == 4 and 0 <= live0 <= limit
+    parts = [ds.Partition(slot_offset=8 * i, n_slots=8) for i in range(limit - live0)]
+    assert ds.partition_count()[0] == limit
+    for kw in (dict(fraction=0.5), dict(slot_offset=0, n_slots=1), dict(slot_mask=0x3)):
+        with pytest.raises(ds.DStackError) as e:
+            ds.Partition(**kw)
+        assert e.value.status == ds.E_UNSUPPORTED
+        assert ds.partition_count()[0] == limit
+    parts.pop().destroy()
+    p = ds.Partition(slot_offset=24, n_slots=8)
+    assert ds.partition_count()[0] == limit
+    p.destroy()
+    for q in parts:
+        q.destroy()
+    assert ds.partition_count()[0] == live0
+
+
+def test_partition_destroy_releases_workspaces(env):
+    """A model's workspace for a partition (activations, split-K slices,
+    captured graphs) is freed when the partition is destroyed."""
+    ds, gu, inputs, oracle, torch = env
+    m = ds.Model("resnet50", 9)
+    x = gu.dev_bf16(inputs.image_batch(3, 16))
+    y = gu.empty_f32((16, 1000))
+    torch.cuda.synchronize()
+    free0 = torch.cuda.mem_get_info()[0]
+    for _ in range(3):
+        p = ds.Partition(0.5)
+        m.infer(16, x, y, p)
+        p.synchronize()
+        p.destroy()
+    free1 = torch.cuda.mem_get_info()[0]
+    assert free0 - free1 < 64 * 1024 * 1024, (free0, free1)
 
 
 def test_mobilenetv2(env):
     ds, gu, inputs, oracle, torch = env
     part = ds.Partition(0.3)
     m, xb, got = run_model(env, "mobilenetv2", 1031, 32, part)
-    check_against_oracle(env, "mobilenetv2", 1031, xb, got, sample_items(32, 8)[:3])
+    check_against_oracle(env, "mobilenetv2", 1031, xb, got, sample_items(32, 8))
 
 
 def test_vgg19(env):
     ds, gu, inputs, oracle, torch = env
     part = ds.Partition(0.5)
     m, xb, got = run_model(env, "vgg19", 1040, 8, part)
-    check_against_oracle(env, "vgg19", 1040, xb, got, [0, 7])
+    check_against_oracle(env, "vgg19", 1040, xb, got, sample_items(8, 10))
 
 
 def test_lstm2(env):
     ds, gu, inputs, oracle, torch = env
     part = ds.Partition(0.25)
     m, xb, got = run_model(env, "lstm2", 1041, 32, part)
-    check_against_oracle(env, "lstm2", 1041, xb, got, sample_items(32, 9)[:3])
+    check_against_oracle(env, "lstm2", 1041, xb, got, sample_items(32, 9))
 
 
 @pytest.mark.parametrize("arch", ["tinycnn", "mobilenetv2", "lstm2"])
@@ -184,7 +242,7 @@ def test_two_model_mix_launch_configuration(env):
     for r in runs:
         r[5].synchronize()
     for arch, seed, b, reps, m, p, xb, x, y in runs:
-        items = sample_items(b, seed)[:2]
+        items = sample_items(b, seed)
         check_against_oracle(env, arch, seed, xb, gu.host(y), items)
 
 

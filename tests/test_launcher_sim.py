@@ -1,5 +1,5 @@
 """Launcher simulation (Sec. 6.1.2 FOD fill on the session plan) and the
-comparator schedulers of Sec. 7 (max-throughput, max-min fair): the library's
+comparator schedulers of Sec. 6.3 (max-throughput, max-min fair): the library's
 dstack_simulate against the scheduler oracle's simulate(), bit-exact, on
 random timing tables and Poisson traces and on the four-model workload shape
 (ResNet-50, MobileNetV2, VGG-19, LSTM at 400/800/150/300 req/s, SLOs
