@@ -1,41 +1,48 @@
-"""Benchmark: multi-DNN spatial multiplexing on one MI355X.
+"""Benchmark: multi-DNN spatio-temporal multiplexing on one MI355X.
 
-Headline workload (one GPU): ResNet-50 v1.5 at batch 16 (SLO 25 ms) and
-MobileNetV2 1.0 at batch 32 (SLO 15 ms), synthetic N(0,1) 224x224x3 bf16
-images standing in for ImageNet, random-weight bf16 models.
+Headline workload (one GPU): the four-model Poisson mix -- ResNet-50 v1.5,
+MobileNetV2 1.0, VGG-19 (224x224x3 synthetic N(0,1) bf16 images standing in
+for ImageNet) and the 2-layer LSTM (512 -> 1024, 50 steps, N(0,1) sequences
+standing in for IMDB sentences), random-weight bf16 models -- with requests
+arriving as Poisson processes at 400/800/150/300 req/s x k and SLOs of
+25/15/50/30 ms, served by the library's live launcher (dstack_serve): the
+SLO-constrained batch and GPU% of dstack_schedule (with each model's arrival
+rate), the 100 ms session plan and the fair, opportunistic, dynamic fill on
+each model's home CU range.
 
-Setup (untimed): load both models and sweep each over batches {1,2,4,8,16[,32]}
-x CU fractions 10%..100% (knee sweep: median latency of 20 timed forwards per
-point).  At the workload's batch each model's knee is the efficacy optimum
-b/(L^2 s) over the swept slot counts; it is deployed with 2 slots of
-over-provisioning (shrunk proportionally when the models do not fit together).
-The CU-masked partitions (disjoint slot ranges) are packed over the 32 slots
-round-robin over the models, up to 4 partitions (more concurrently active
-masked queues are avoided on this part).  The SLO-constrained (batch, slots)
-choice of dstack_schedule over the whole table is reported alongside.
+Setup (untimed): load the four models and sweep each over its batches x CU
+fractions 10%..100% (knee sweep: median latency of 20 timed forwards per
+point); these timing tables are the scheduler's only input.  Capacity (the
+comparison of the paper's throughput claims, at a fixed SLO bar): the largest
+rate scale k with at most 1% of the requests violating their SLO or left
+unserved, found by doubling k and then bisecting it on a geometric grid,
+each probe a short live run on the same Poisson traces (seeds 2026+i).  The
+same search runs the time-sliced full-GPU baseline (temporal sharing, Sec.
+6.1 and Sec. 7's "T": one model at a time on all 256 CUs, slices
+proportional to the SLOs) for slice cycles of 15 and 7.5 ms, and D-STACK
+for an over-provision of 0 and 2 slots; each policy's best is reported (both
+settings are in the output).
 
-One step = ceil(100 ms / SLO) batches of each partition's model, back to back,
-all partitions concurrently (closed loop).  Value = aggregate inferences/s
-over K steps.  The time-sliced full-GPU baseline runs the same per-model batch
-counts one batch at a time on an unmasked partition.  Per-kernel HIP-event
-timing on each partition's stream gives the conv MFMA TFLOP/s at the knee and
-the roofline fraction of the dominant kernel (the implicit-GEMM convolution);
-each partition's batch time alone vs in the mix gives the interference.
-Rooflines per model use P(n) = 2516.6 TFLOP/s * n/256 and BW(n) measured by a
-device copy on the partition's stream ("per_model[].roofline"); "mix" holds
-the same-work makespan ratio, the FLOP-weighted work rate, the CU-weighted
-roofline busy fraction and the same models on unmasked concurrent streams.
+One step = one 100 ms session of live serving at the D-STACK capacity rate;
+the timed region is one dstack_serve call of K sessions (its warm-up of
+graph captures runs before its clock starts).  Value = requests completed
+within their SLO per second of the run (inputs resident in HBM; requests
+carry no data).  The time-sliced baseline runs the same number of sessions
+at its own capacity rate (and, for context, at D-STACK's).
 
-Also reported (not the headline): the tiny CNN at 100/50/25% ("config1");
-ResNet-50 at batch 1/8/32 over the 10 fractions ("config2"); for each
-headline model the knee found by a binary search from 30% against the sweep's
-knee, and the cost of a GPU% change, cold and active-standby
-("reconfiguration"); the VGG-19 batch 8 + LSTM batch 32 pair in the same
-closed-loop form ("config4"), and the four-model Poisson mix (ResNet-50,
-MobileNetV2, VGG-19, LSTM at 400/800/150/300 req/s, SLOs 25/15/50/30 ms,
-100 ms sessions) through the live launcher dstack_serve for 10 s at the
-stated rates plus a capacity sweep of 2 s runs at k x the rates ("config5");
---headline-only skips these.
+Also reported: the dominant kernel's roofline (the implicit-GEMM
+convolution: algorithmic FLOP per launch over its launch duration, timed by
+events on the kernels' own dispatch packets on each model's deployed
+partition); per-model rooflines (P(n) = 2516.6 TFLOP/s x n/256, BW(n)
+measured by a device copy on the partition's stream); the oracle on the
+host's cores; config 3 (ResNet-50 + MobileNetV2, SLOs 25/15 ms) closed loop
+at dstack_schedule's batches and partitions vs time-sliced, plus the
+fixed-batch 16/32 run as a labelled extra; config 1 (tiny CNN at
+100/50/25%); config 2 (ResNet-50 b1/8/32 knee curves with the model
+roofline fraction at each CU fraction and the analytical model's knee);
+config 4 (VGG-19 b8 + LSTM b32 closed loop); BERT knees (config6); the GPU%
+reconfiguration probes; the comparator and ideal schedules in simulate
+mode.  --headline-only skips the extras.
 """
 import argparse
 import hashlib
@@ -52,14 +59,22 @@ METRIC = "aggregate inferences/s (multi-DNN, one GPU) + conv MFMA TFLOP/s at kne
 PEAK_BF16_TFLOPS = 2516.6   # dense bf16 MFMA, 256 CUs at 2.4 GHz
 FRACTIONS = [0.1 * i for i in range(1, 11)]
 PERIOD_US = 100000
-MAX_PARTITIONS = 4
+MAX_PARTITIONS = 4          # live CU-masked streams the library allows at once
 OVERPROV = 2
+VIOLATION_BAR = 0.01
 
-MODELS = [
-    # arch, seed, SLO us, workload batch, batches swept
-    ("resnet50", 1030, 25000, 16, [1, 2, 4, 8, 16]),
-    ("mobilenetv2", 1031, 15000, 32, [1, 2, 4, 8, 16, 32]),
+# the four-model mix (seeds 1000 + 10 * config + model index, inputs seed + 1)
+MIX4 = [
+    # arch, seed, SLO us, rate req/s, Bmax, batches swept
+    ("resnet50", 1050, 25000, 400, 16, [1, 2, 4, 8, 16]),
+    ("mobilenetv2", 1051, 15000, 800, 32, [1, 2, 4, 8, 16, 32]),
+    ("vgg19", 1052, 50000, 150, 8, [1, 2, 4, 8]),
+    ("lstm2", 1053, 30000, 300, 32, [1, 2, 4, 8, 16, 32]),
 ]
+TEMPORAL_CYCLES = [15000, 7500]   # temporal sharing: slice cycles tried (the best is the baseline)
+DSTACK_OVERPROV = [0, 2]          # D-STACK: over-provision (slots) tried (the best is the headline)
+# config 3: ResNet-50 (SLO 25 ms) + MobileNetV2 (SLO 15 ms); indices into MIX4
+PAIR = [(0, 25000, 16), (1, 15000, 32)]
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "conv_igemm_mix_traffic.md")
 CONV_SRC = os.path.join(ROOT, "paper_2304_13541_amd", "csrc", "conv_igemm.hip")
@@ -68,30 +83,30 @@ CONV_SRC = os.path.join(ROOT, "paper_2304_13541_amd", "csrc", "conv_igemm.hip")
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=200)
-    p.add_argument("--warmup", type=int, default=3)
+    p.add_argument("--steps", type=int, default=20, help="timed 100 ms sessions of live serving")
+    p.add_argument("--warmup", type=int, default=3, help="untimed sessions before them")
     p.add_argument("--sweep-warmup", type=int, default=5)
     p.add_argument("--sweep-reps", type=int, default=20)
     p.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the oracle CPU baseline")
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--table", default=None, help="load a timing table JSON instead of sweeping")
+    p.add_argument("--table", default=None, help="load the timing tables (JSON) instead of sweeping")
     p.add_argument("--save-table", default=None)
+    p.add_argument("--probe-seconds", type=float, default=1.5, help="length of each capacity probe")
+    p.add_argument("--steps3", type=int, default=20, help="steps of the config-3 closed-loop pair")
     p.add_argument("--steps4", type=int, default=40, help="steps of the VGG-19 + LSTM pair")
-    p.add_argument("--serve-seconds", type=float, default=10.0, help="four-model mix at the stated rates")
-    p.add_argument("--capacity-seconds", type=float, default=2.0, help="each point of the capacity sweep")
-    p.add_argument("--headline-only", action="store_true", help="skip the GPU%% reconfiguration probes, the VGG-19 + LSTM pair and the four-model mix")
+    p.add_argument("--headline-only", action="store_true", help="skip everything but the four-model mix")
     return p.parse_args()
 
 
-def sweep_tables(models, args):
+def sweep_tables(models, specs, args):
+    """Timing table {batch: {slots: median latency us}} of each model."""
     tables = []
-    for (arch, seed, slo, b_work, batches), m in zip(MODELS, models):
-        tab, knees = {}, {}
-        for b in batches:
+    for spec, m in zip(specs, models):
+        tab = {}
+        for b in spec[-1]:
             r = m.knee_sweep(b, FRACTIONS, warmup=args.sweep_warmup, reps=args.sweep_reps)
             tab[b] = dict(zip(r["slots"], r["latency_us"]))
-            knees[b] = r["knee_slots"]
-        tables.append(dict(arch=arch, table=tab, knee_slots_per_batch=knees))
+        tables.append(tab)
     return tables
 
 
@@ -112,30 +127,36 @@ def measured_traffic():
 
 
 def cpu_baseline(budget_s, sched_in):
-    """The oracle, as it stands, on the host cores: sampled items of the same
-    workload (batch items are independent), parity mode; and the scheduler
-    oracle's time for the same scheduling decision as the library's."""
+    """The oracle, as it stands, on the host cores: single items of the same
+    workload round-robin over the four models (batch items are independent),
+    parity mode; and the scheduler oracle's time for the same scheduling
+    decision as the library's."""
     import oracle
     from oracle import sched as osched
     from tests import inputs
     t_s = time.perf_counter()
-    osched.schedule(sched_in, PERIOD_US)
+    osched.schedule(sched_in, PERIOD_US, placement="home")
     sched_s = time.perf_counter() - t_s
-    done, t0 = 0, time.perf_counter()
-    models = {a: oracle.Model(a, s) for a, s, *_ in MODELS}
-    i = 0
+    models = [oracle.Model(a, seed) for a, seed, *_ in MIX4]
+    done, i, counts = 0, 0, [0] * len(MIX4)
+    t0 = time.perf_counter()
     while True:
-        arch, seed = MODELS[i % 2][0], MODELS[i % 2][1]
-        models[arch].forward(inputs.image_batch(seed + 1 + i, 1), parity=True)
+        k = i % len(MIX4)
+        arch, seed = MIX4[k][0], MIX4[k][1]
+        x = inputs.sequence_batch(seed + 1 + i, 1) if arch == "lstm2" else inputs.image_batch(seed + 1 + i, 1)
+        models[k].forward(x, parity=True)
         done += 1
+        counts[k] += 1
         i += 1
         el = time.perf_counter() - t0
-        if el >= budget_s and i % 2 == 0:
+        if el >= budget_s and i % len(MIX4) == 0:
             break
     threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
     return dict(value=done / el, unit="inferences/s", cores=threads, kind="oracle",
-                sample="%d single 224x224 images alternating ResNet-50 / MobileNetV2 (fp64 oracle, parity mode), "
-                       "%.1f s" % (done, el), scheduler_oracle_seconds=sched_s)
+                sample="%d single items round-robin over ResNet-50 / MobileNetV2 / VGG-19 images (224x224) and "
+                       "LSTM sequences (50 x 512): %s each (fp64 oracle, parity mode), %.1f s" %
+                       (done, "/".join(map(str, counts)), el),
+                scheduler_oracle_seconds=sched_s)
 
 
 def knee_at(row, b):
@@ -381,10 +402,34 @@ def knee_model_prediction(ds, torch, m, b, n_cu_grid, latency_us):
                                       bw_per_cu_bytes_per_us=mb))
 
 
+def roofline_curve(ds, torch, m, b, latency_us):
+    """Per sweep fraction: the model's roofline on a partition of that size
+    (per-layer kernel times of three profiled forwards, BW(n) measured on the
+    partition's stream) against the sweep's latency there."""
+    from tests import gpu_util as gu
+    from tests import inputs
+    x = gu.dev_bf16(inputs.image_batch(1021, b))
+    y = gu.empty_f32(m.output_shape(b))
+    out = []
+    for f, L in zip(FRACTIONS, latency_us):
+        p = ds.Partition(f)
+        for _ in range(2):
+            m.infer(b, x, y, p)
+        p.synchronize()
+        recs, _ = layer_stats(ds, m, b, x, y, p)
+        rf = model_roofline(ds, recs, p.n_cu, bw_probe(torch, p), float(L))
+        out.append(dict(n_cu=p.n_cu, model_roofline_frac=rf["model_roofline_frac"],
+                        conv_mfma_frac=rf["conv_mfma_frac"], t_roof_us=rf["t_roof_us"],
+                        hbm_gbs_measured=rf["hbm_gbs_measured"]))
+        p.destroy()
+    return out
+
+
 def config2(ds, torch, args):
     """ResNet-50 at batch 1, 8 and 32 over the 10 fractions: latency, inf/s,
-    efficacy b / (L^2 * CUs) and the knee (Sec. 3.2), beside the knee the
-    analytical model of Sec. 4.3 predicts from the kernels' parallelism."""
+    efficacy b / (L^2 * CUs), the knee (Sec. 3.2) and the roofline fraction
+    at each fraction, beside the knee the analytical model of Sec. 4.3
+    predicts from the kernels' parallelism."""
     m = ds.Model("resnet50", 1020)
     rows = []
     for b in (1, 8, 32):
@@ -393,6 +438,7 @@ def config2(ds, torch, args):
                          inferences_per_s=[b * 1e6 / L for L in r["latency_us"]],
                          eta=[b / (L * L * c) for L, c in zip(r["latency_us"], r["n_cu"])],
                          knee_slots=r["knee_slots"], deployed_slots=r["deployed_slots"],
+                         roofline=roofline_curve(ds, torch, m, b, r["latency_us"]),
                          knee_model=knee_model_prediction(ds, torch, m, b, list(r["n_cu"]),
                                                           [float(v) for v in r["latency_us"]])))
     m.destroy()
@@ -458,52 +504,189 @@ def gu_dev(a):
     return gu.dev_bf16(a)
 
 
-def config5(ds, torch, models4, tables4, args):
-    """Four-model Poisson mix through the live launcher (plan + FOD on home
-    ranges): stated rates for args.serve_seconds, then a capacity sweep."""
-    from tests import inputs
-    rates = [400, 800, 150, 300]
-    slos = [25000, 15000, 50000, 30000]
-    bmax = [16, 32, 8, 32]
-    xs, ys = [], []
-    for m, b in zip(models4, bmax):
-        shp = m.input_shape(b)
-        if len(shp) == 3:
-            xs.append(gu_dev(inputs.sequence_batch(1051, shp[1], shp[0], shp[2])))
-        else:
-            xs.append(gu_dev(inputs.image_batch(1050, b)))
-        ys.append(torch.empty(m.output_shape(b), device="cuda", dtype=torch.float32))
+class Mix4:
+    """The four-model Poisson mix on the live launcher: inputs at each
+    model's largest batch, Poisson traces (seeds 2026 + i) at k x the stated
+    rates, one dstack_serve call per run."""
 
-    def one(k, dur_us):
-        tabs = [dict(slo_us=slo, max_batch=b, rate_per_s=r * k, table=t)
-                for slo, b, r, t in zip(slos, bmax, rates, tables4)]
-        arr = [inputs.poisson_arrivals(2026 + i, r * k, dur_us) for i, r in enumerate(rates)]
-        r = ds.serve(models4, tabs, xs, ys, PERIOD_US, dur_us, arr, log_capacity=0)
-        n_req = sum(len(a) for a in arr)
-        viol = sum(s["violations"] for s in r["models"])
-        st, plan = ds.schedule(tabs, PERIOD_US, placement="home")
-        return dict(k=k, offered_req_s=n_req / (dur_us * 1e-6), served_req_s=sum(s["served"] for s in r["models"]) /
-                    (dur_us * 1e-6), violations_per_s=viol / (dur_us * 1e-6), violation_frac=viol / max(1, n_req),
-                    utilisation_ppm=r["utilisation_ppm"], n_jobs=r["n_jobs"],
-                    plan=dict(batch=plan["batch"], deployed_slots=plan["deployed_slots"],
-                              home_offset=plan["home_offset"], utilisation_ppm=plan["utilisation_ppm"],
-                              status="ok" if st == ds.OK else "infeasible"),
-                    per_model=[dict(arch=m.arch, **s) for m, s in zip(models4, r["models"])])
-    stated = one(1, int(args.serve_seconds * 1e6))
-    sweep, capacity = [], None
-    for k in (2, 4, 8, 16):
-        r = one(k, int(args.capacity_seconds * 1e6))
-        sweep.append({kk: r[kk] for kk in ("k", "offered_req_s", "served_req_s", "violation_frac", "utilisation_ppm")})
-        if r["violation_frac"] <= 0.01:
-            capacity = r["offered_req_s"]
+    def __init__(self, ds, torch, models, tables):
+        from tests import gpu_util as gu
+        from tests import inputs
+        self.ds, self.torch, self.models, self.tables = ds, torch, models, tables
+        self.xs, self.ys = [], []
+        for (arch, seed, slo, rate, bmax, _), m in zip(MIX4, models):
+            x = inputs.sequence_batch(seed + 1, bmax) if arch == "lstm2" else inputs.image_batch(seed + 1, bmax)
+            self.xs.append(gu.dev_bf16(x))
+            self.ys.append(gu.empty_f32(m.output_shape(bmax)))
+        self.rate = sum(spec[3] for spec in MIX4)
+
+    def tabs(self, k):
+        # rate-aware assembly time C(b) = ceil(b * 1e6 / rate) (Sec. 5.1) at k x the stated rates
+        return [dict(slo_us=slo, max_batch=bmax, rate_per_s=max(1, int(round(rate * k))), table=t)
+                for (arch, seed, slo, rate, bmax, _), t in zip(MIX4, self.tables)]
+
+    def arrivals(self, k, dur_us):
+        from tests import inputs
+        return [inputs.poisson_arrivals(2026 + i, spec[3] * k, dur_us) for i, spec in enumerate(MIX4)]
+
+    def run(self, k, dur_us, policy, param=0):
+        """One live run; param: D-STACK over-provision slots, or the temporal slice cycle (us)."""
+        arr = self.arrivals(k, dur_us)
+        t0 = time.perf_counter()
+        if policy == "dstack":
+            r = self.ds.serve(self.models, self.tabs(k), self.xs, self.ys, PERIOD_US, dur_us, arr, policy=policy,
+                              overprov_slots=param, log_capacity=0)
         else:
-            break
-    if capacity is None and stated["violation_frac"] <= 0.01:
-        capacity = stated["offered_req_s"]
-    return dict(workload="four-model Poisson mix (ResNet-50, MobileNetV2, VGG-19, LSTM at 400/800/150/300 req/s, "
-                         "SLOs 25/15/50/30 ms, 100 ms sessions) through dstack_serve on home CU ranges",
-                stated_rates=stated, capacity_sweep=sweep, capacity_req_s_at_1pct=capacity,
-                capacity_seconds=args.capacity_seconds)
+            r = self.ds.serve(self.models, self.tabs(k), self.xs, self.ys, PERIOD_US, dur_us, arr, policy=policy,
+                              slice_cycle_us=param, log_capacity=0)
+        wall = time.perf_counter() - t0
+        n_req = sum(len(a) for a in arr)
+        served = sum(m["served"] for m in r["models"])
+        late = sum(m["violations"] - m["unserved"] for m in r["models"])
+        viol = sum(m["violations"] for m in r["models"])
+        run_us = max(dur_us, r["last_end_us"])
+        return dict(k=k, policy=policy, param=param, requests=n_req, offered_req_s=n_req / (dur_us * 1e-6),
+                    served=served, on_time=served - late, violations=viol, violation_frac=viol / max(1, n_req),
+                    run_us=run_us, on_time_per_s=(served - late) / (run_us * 1e-6), call_wall_s=wall,
+                    utilisation_ppm=r["utilisation_ppm"],
+                    per_model=[dict(arch=spec[0], **st) for spec, st in zip(MIX4, r["models"])])
+
+    def capacity(self, policy, param, seconds):
+        """Largest k (offered rate k x the stated rates) with at most 1% of the
+        requests late or unserved: double from 1 until a probe fails (halve
+        if 1 fails), then bisect three times on the geometric mean."""
+        dur = int(seconds * 1e6)
+        probes = []
+
+        def ok(k):
+            r = self.run(k, dur, policy, param)
+            probes.append({kk: r[kk] for kk in ("k", "offered_req_s", "on_time_per_s", "violation_frac",
+                                                "utilisation_ppm")})
+            return r["violation_frac"] <= VIOLATION_BAR
+
+        k_ok = k_bad = None
+        k = 1.0
+        while k <= 256:
+            if ok(k):
+                k_ok, k = k, 2 * k
+            else:
+                k_bad = k
+                break
+        if k_ok is None:
+            k = 0.5
+            while k >= 1.0 / 64:
+                if ok(k):
+                    k_ok = k
+                    break
+                k_bad, k = k, k / 2
+        if k_ok is not None and k_bad is not None:
+            for _ in range(3):
+                mid = math.sqrt(k_ok * k_bad)
+                if ok(mid):
+                    k_ok = mid
+                else:
+                    k_bad = mid
+        return (k_ok or 0.0), probes
+
+    def timed(self, k, policy, param, steps, warmup):
+        """`warmup` untimed sessions, then the timed run of `steps` sessions."""
+        if warmup:
+            self.run(k, warmup * PERIOD_US, policy, param)
+        self.torch.cuda.synchronize()
+        return self.run(k, steps * PERIOD_US, policy, param)
+
+
+def mix_rooflines(ds, torch, mix, k, overprov):
+    """Each model of the four-model mix on its deployed home partition at the
+    plan's batch (dstack_schedule with the rates at k): per-layer kernel
+    times of three profiled forwards, the partition's measured bandwidth and
+    the model's roofline; the conv launches of all four pooled."""
+    st, plan = ds.schedule(mix.tabs(k), PERIOD_US, overprov_slots=overprov, placement="home")
+    per_model, conv = [], dict(fl=0.0, ms=0.0, n=0, by=0.0, cu_ms=0.0)
+    for i, (m, spec) in enumerate(zip(mix.models, MIX4)):
+        b, dep, off = plan["batch"][i], plan["deployed_slots"][i], plan["home_offset"][i]
+        p = ds.Partition(slot_offset=off, n_slots=dep)
+        for _ in range(2):
+            m.infer(b, mix.xs[i], mix.ys[i], p)
+        p.synchronize()
+        recs, by_kind = layer_stats(ds, m, b, mix.xs[i], mix.ys[i], p)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        sp = p.torch_stream()
+        e0.record(sp)
+        for _ in range(5):
+            m.infer(b, mix.xs[i], mix.ys[i], p)
+        e1.record(sp)
+        p.synchronize()
+        torch.cuda.synchronize()
+        lat_us = 1000.0 * e0.elapsed_time(e1) / 5
+        rf = model_roofline(ds, recs, p.n_cu, bw_probe(torch, p), lat_us)
+        mf = [r for r in recs if r["kind"] == 0]
+        fl, ms = sum(r["flops"] for r in mf), sum(r["ms"] for r in mf)
+        conv["fl"] += fl
+        conv["ms"] += ms
+        conv["n"] += len(mf)
+        conv["by"] += sum(r["bytes"] for r in mf)
+        conv["cu_ms"] += p.n_cu * ms
+        tf = fl / (ms * 1e-3) / 1e12 if ms > 0 else None
+        per_model.append(dict(arch=spec[0], batch=b, slots=dep, slot_offset=off, n_cu=p.n_cu, latency_us=lat_us,
+                              table_latency_us=plan["latency_us"][i], conv_mfma_tflops=tf,
+                              conv_frac_of_partition_peak=tf / (PEAK_BF16_TFLOPS * p.n_cu / 256) if tf else None,
+                              kernels=by_kind, roofline=rf))
+        p.destroy()
+    return plan, per_model, conv
+
+
+def pair_run(ds, torch, models, tables, batch, dep, slos, steps, warmup, label):
+    """Two models closed loop on disjoint CU-masked partitions (packed over
+    the 32 slots, at most four), ceil(100 ms / SLO) batches per partition
+    per step, vs the same batches one at a time on the whole GPU, and vs
+    the same models on unmasked concurrent streams."""
+    from tests import gpu_util as gu
+    from tests import inputs
+    reps = [math.ceil(PERIOD_US / slo) for slo in slos]
+    lanes = pack_lanes(dep, ds.TOTAL_SLOTS, MAX_PARTITIONS)
+    xs = [gu.dev_bf16(inputs.image_batch(1031 + i, b)) for i, b in enumerate(batch)]
+    shapes = [(b, 1000) for b in batch]
+    mix = Mix(ds, torch, models, batch, xs, shapes, lanes, reps)
+    t_mix = mix.timed(steps, warmup)
+    inter = mix.interference(max(3, steps // 4), warmup, t_mix, steps)
+    mix.destroy()
+    t_seq = mix.timesliced(steps, warmup, shapes)
+    full_lanes = [(mi, 0, ds.TOTAL_SLOTS) for mi, _, _ in lanes]
+    umix = Mix(ds, torch, models, batch, xs, shapes, full_lanes, reps)
+    t_umix = umix.timed(steps, warmup)
+    umix.destroy()
+    items = mix.items_per_step * steps
+    full_us = sum(mix.lane_count[i] * reps[i] * tables[i][batch[i]][ds.TOTAL_SLOTS] for i in range(len(models)))
+    return dict(label=label, batch=batch, deployed_slots=dep, partitions=lanes, jobs_per_step=reps, steps=steps,
+                inferences_per_s=items / t_mix, timesliced_inferences_per_s=items / t_seq,
+                speedup_vs_timesliced=t_seq / t_mix, unmasked_concurrent_inferences_per_s=items / t_umix,
+                same_work_makespan_ratio=full_us / (1e6 * t_mix / steps), interference=inter,
+                per_model_inf_s=[mix.lane_count[i] * reps[i] * batch[i] * steps / t_mix for i in range(len(models))])
+
+
+def config3(ds, torch, models, tables, args):
+    """ResNet-50 (SLO 25 ms, Bmax 16) + MobileNetV2 (SLO 15 ms, Bmax 32):
+    batch and GPU% from dstack_schedule (Sec. 5.1, assembly time 482 us per
+    item), closed loop on the deployed partitions; and, labelled as an
+    extra, the fixed batches 16 / 32 at their knees."""
+    pm = [models[i] for i, _, _ in PAIR]
+    pt = [tables[i] for i, _, _ in PAIR]
+    slos = [slo for _, slo, _ in PAIR]
+    sched_in = [dict(slo_us=slo, max_batch=bmax, rate_per_s=0, table=t) for (_, slo, bmax), t in zip(PAIR, pt)]
+    st, plan = ds.schedule(sched_in, PERIOD_US)
+    batch = plan["batch"]
+    dep = fit_slots(plan["deployed_slots"], ds.TOTAL_SLOTS)
+    chosen = pair_run(ds, torch, pm, pt, batch, dep, slos, args.steps3, 3, "dstack_schedule batches and partitions")
+    chosen.update(schedule_status="ok" if st == ds.OK else "infeasible", knee_slots=plan["knee_slots"],
+                  table_latency_us=plan["latency_us"])
+    fb = [bmax for _, _, bmax in PAIR]
+    knee = [knee_at(t[b], b) for t, b in zip(pt, fb)]
+    fixed = pair_run(ds, torch, pm, pt, fb, fit_slots([min(32, k + OVERPROV) for k in knee], ds.TOTAL_SLOTS), slos,
+                     args.steps3, 3, "extra: fixed batches 16 / 32 at their knees + 2 slots")
+    fixed["knee_slots"] = knee
+    return dict(workload="ResNet-50 v1.5 (SLO 25 ms) + MobileNetV2 1.0 (SLO 15 ms), 224x224x3, seeds 1050/1051",
+                schedule_driven=chosen, fixed_batch=fixed)
 
 
 def comparators(ds, tables4, k=32, seconds=2.0):
@@ -564,7 +747,7 @@ def kernel_knee_table(ds, m, b, x, y):
     return slots, dur, table
 
 
-def ideal_vs_dstack(ds, models, tables, batch, xs, ys, seconds=0.2, slot_us=1):
+def ideal_vs_dstack(ds, models, slos, batch, xs, ys, seconds=0.2, slot_us=1):
     """The headline pair under the ideal schedule of Sec. 6.2 (slotted, kernel
     granularity, preemptive, every kernel at its own knee) and under D-STACK
     in simulate mode (plan + FOD, model granularity, non-preemptive) with the
@@ -574,13 +757,13 @@ def ideal_vs_dstack(ds, models, tables, batch, xs, ys, seconds=0.2, slot_us=1):
     only.  Slot 1 us: these kernels last 5-50 us, where the paper's 100 us
     slots fitted its millisecond ones."""
     ideal_models, tabs = [], []
-    for (arch, seed, slo, b, _), m, x, y in zip(MODELS, models, xs, ys):
+    for slo, b, m, x, y in zip(slos, batch, models, xs, ys):
         sl, du, table = kernel_knee_table(ds, m, b, x, y)
         ideal_models.append(dict(slots=sl, dur=du, batch=b, slo_us=slo))
         tabs.append(dict(slo_us=slo, max_batch=b, table={b: table}))
     hor = int(seconds * 1e6)
     idl = ds.simulate_ideal(ideal_models, hor, slot_us)
-    dense = [list(range(0, hor, 20)) for _ in MODELS]
+    dense = [list(range(0, hor, 20)) for _ in models]
     sim = ds.simulate(tabs, PERIOD_US, hor, dense)
     d_items = [mm["served"] for mm in sim["models"]]
     return dict(slot_us=slot_us, seconds=seconds, kernel_sum_tables=[t["table"][b] for t, b in zip(tabs, batch)],
@@ -604,141 +787,85 @@ def main():
     from tests import inputs
 
     torch.cuda.init()
-    models = [ds.Model(a, s) for a, s, *_ in MODELS]
-    n_models = len(MODELS)
+    models = [ds.Model(a, seed) for a, seed, *_ in MIX4]
 
-    # ---- setup: timing tables, knees, partitions ----
+    # ---- setup: timing tables (the scheduler's only input) ----
     sweep_s = None
     if args.table:
         with open(args.table) as f:
-            tables = json.load(f)
-        for t in tables:
-            t["table"] = {int(b): {int(s): int(L) for s, L in row.items()} for b, row in t["table"].items()}
+            tables = [{int(b): {int(sl): int(L) for sl, L in row.items()} for b, row in t.items()} for t in json.load(f)]
     else:
         t0 = time.perf_counter()
-        tables = sweep_tables(models, args)
+        tables = sweep_tables(models, MIX4, args)
         sweep_s = time.perf_counter() - t0
     if args.save_table:
         with open(args.save_table, "w") as f:
             json.dump(tables, f)
+    mix = Mix4(ds, torch, models, tables)
 
-    batch = [b for _, _, _, b, _ in MODELS]
-    knee = [knee_at(t["table"][b], b) for t, b in zip(tables, batch)]
-    dep = fit_slots([min(ds.TOTAL_SLOTS, k + OVERPROV) for k in knee], ds.TOTAL_SLOTS)
-    reps = [math.ceil(PERIOD_US / slo) for _, _, slo, _, _ in MODELS]
-    lanes = pack_lanes(dep, ds.TOTAL_SLOTS, MAX_PARTITIONS)
+    # ---- capacity at <= 1% violations: D-STACK and temporal sharing, same traces ----
+    t_cap = time.perf_counter()
+    dstack = []
+    for ov in DSTACK_OVERPROV:
+        k_d, probes_d = mix.capacity("dstack", ov, args.probe_seconds)
+        dstack.append(dict(overprov_slots=ov, k=k_d, capacity_req_s=k_d * mix.rate, probes=probes_d))
+    best_d = max(dstack, key=lambda d: d["k"])
+    temporal = []
+    for cyc in TEMPORAL_CYCLES:
+        k_t, probes_t = mix.capacity("temporal", cyc, args.probe_seconds)
+        temporal.append(dict(cycle_us=cyc, k=k_t, capacity_req_s=k_t * mix.rate, probes=probes_t))
+    best_t = max(temporal, key=lambda d: d["k"])
+    capacity_s = time.perf_counter() - t_cap
+    k_ds, ov = best_d["k"], best_d["overprov_slots"]
 
-    # the SLO-constrained choice over the whole table (reported; Sec. 5.1)
-    sched_in = [dict(slo_us=slo, max_batch=b, rate_per_s=0, table=t["table"])
-                for (arch, seed, slo, b, _), t in zip(MODELS, tables)]
-    sched_st, plan = ds.schedule(sched_in, PERIOD_US)
+    # ---- timed: K sessions of live serving at each policy's capacity ----
+    k_run = k_ds if k_ds > 0 else 1.0
+    run_ds = mix.timed(k_run, "dstack", ov, args.steps, args.warmup)
+    run_t = mix.timed(best_t["k"] if best_t["k"] > 0 else 1.0, "temporal", best_t["cycle_us"], args.steps,
+                      args.warmup)
+    run_t_same = mix.run(k_run, args.steps * PERIOD_US, "temporal", best_t["cycle_us"])
+    value = run_ds["on_time_per_s"]
 
-    xs = [gu.dev_bf16(inputs.image_batch(seed + 1, b)) for (a, seed, *_), b in zip(MODELS, batch)]
-    shapes = [(b, 1000) for b in batch]
-    mix = Mix(ds, torch, models, batch, xs, shapes, lanes, reps)
-    t_mix = mix.timed(args.steps, args.warmup)
-    value = mix.items_per_step * args.steps / t_mix
-    t_seq = mix.timesliced(args.steps, args.warmup, shapes)
-    seq_value = mix.items_per_step * args.steps / t_seq
-    inter = mix.interference(max(5, args.steps // 4), args.warmup, t_mix, args.steps)
-    # the same models concurrently on unmasked streams (each stream may use every CU): the
-    # MPS-default analogue, a second, non-target baseline
-    full_lanes = [(mi, 0, ds.TOTAL_SLOTS) for mi, _, _ in lanes]
-    umix = Mix(ds, torch, models, batch, xs, shapes, full_lanes, reps)
-    t_umix = umix.timed(args.steps, args.warmup)
-    umix.destroy()
-    unmasked_value = mix.items_per_step * args.steps / t_umix
-    # HBM bandwidth each deployed partition (and the whole GPU) can draw: BW(n) of the rooflines
-    bw_lane = [bw_probe(torch, p) for p in mix.parts]
-    pfull = ds.Partition(1.0)
-    bw_full = bw_probe(torch, pfull)
-    pfull.destroy()
+    # ---- the dominant kernel (implicit-GEMM convolution) and per-model rooflines at the deployment ----
+    plan, per_model, conv = mix_rooflines(ds, torch, mix, k_run, ov)
+    avg_ms = conv["ms"] / max(conv["n"], 1)
+    achieved = (conv["fl"] / max(conv["n"], 1)) / (avg_ms * 1e-3) / 1e12 if avg_ms > 0 else 0.0
+    knee_cu = conv["cu_ms"] / max(conv["ms"], 1e-12)
 
-    # ---- per-kernel timing at the deployed partitions (HIP events on each partition's stream) ----
-    per_model = []
-    conv_fl, conv_ms, conv_n, conv_by = 0.0, 0.0, 0, 0.0
-    for i, m in enumerate(models):
-        li = next(k for k, l in enumerate(lanes) if l[0] == i)
-        recs, by_kind = layer_stats(ds, m, batch[i], xs[i], mix.ys[li], mix.parts[li])
-        mf = [r for r in recs if r["kind"] == 0]
-        fl = sum(r["flops"] for r in mf)
-        ms = sum(r["ms"] for r in mf)
-        conv_fl += fl
-        conv_ms += ms
-        conv_n += len(mf)
-        conv_by += sum(r["bytes"] for r in mf)
-        n_cu = mix.parts[li].n_cu
-        tf = fl / (ms * 1e-3) / 1e12 if ms > 0 else None
-        per_model.append(dict(
-            arch=MODELS[i][0], batch=batch[i], knee_slots=knee[i], slots=dep[i], n_cu=n_cu,
-            partitions=mix.lane_count[i], jobs_per_step=reps[i],
-            latency_us_at_knee=tables[i]["table"][batch[i]][knee[i]],
-            conv_mfma_tflops=tf, conv_frac_of_partition_peak=tf / (PEAK_BF16_TFLOPS * n_cu / 256) if tf else None,
-            slo_optimal=dict(batch=plan["batch"][i], knee_slots=plan["knee_slots"][i],
-                             deployed_slots=plan["deployed_slots"][i], latency_us=plan["latency_us"][i],
-                             feasible=plan["feasible"][i]),
-            kernels=by_kind,
-            inferences_per_s_in_mix=mix.lane_count[i] * reps[i] * batch[i] * args.steps / t_mix,
-            roofline=model_roofline(ds, recs, n_cu, bw_lane[li],
-                                    next(x["alone_us"] for x in inter if x["lane"] == li))))
-    mix.destroy()
-    # mix-level: same-work makespan ratio (one step's jobs run one by one on the whole GPU, from the
-    # timing table, over the measured step), FLOP-weighted work rate, CU-weighted roofline busy time
-    full_us = sum(mix.lane_count[i] * reps[i] * tables[i]["table"][batch[i]][ds.TOTAL_SLOTS] for i in range(n_models))
-    step_us = 1e6 * t_mix / args.steps
-    flops_item = [m.info.flops_per_item for m in models]
-    mix_metrics = dict(
-        same_work_makespan_ratio=full_us / step_us,
-        flop_weighted_tflops=sum(p["inferences_per_s_in_mix"] * f for p, f in zip(per_model, flops_item)) / 1e12,
-        mix_roofline_frac=sum(mix.lane_count[i] * reps[i] * per_model[i]["roofline"]["t_roof_us"] *
-                              per_model[i]["n_cu"] / 256 for i in range(n_models)) / step_us,
-        unmasked_concurrent_inferences_per_s=unmasked_value,
-        hbm_gbs_full_gpu=bw_full)
-    avg_ms = conv_ms / max(conv_n, 1)
-    achieved = (conv_fl / max(conv_n, 1)) / (avg_ms * 1e-3) / 1e12
-    knee_cu = sum(p["n_cu"] * p["kernels"]["mfma"]["ms"] for p in per_model) / max(
-        sum(p["kernels"]["mfma"]["ms"] for p in per_model), 1e-9)
-
-    # ---- GPU% reconfiguration (Sec. 3.5, 3.6): knee search from 30% vs the sweep, cost of a change ----
+    # ---- the other workloads ----
+    c1 = c2 = c3 = c4 = c6 = cmp = ideal = None
     reconf = []
-    for i, m in enumerate(models if not args.headline_only else []):
-        ks = m.knee_search(batch[i], FRACTIONS, 10, args.sweep_warmup, args.sweep_reps)
-        sw = m.switch_probe(batch[i], 10, dep[i], reps=10)
-        reconf.append(dict(arch=MODELS[i][0], batch=batch[i], search_knee_slots=ks["knee_slots"],
-                           sweep_knee_slots=knee[i], search_probes=ks["probes"], search_seconds=ks["seconds"],
-                           switch_from_slots=10, switch_to_slots=dep[i], **sw))
-
-    # ---- the other workloads: VGG-19 + LSTM pair, four-model Poisson mix through the live launcher ----
-    c1 = c2 = c4 = c5 = c6 = cmp = ideal = None
     if not args.headline_only:
+        c3 = config3(ds, torch, models, tables, args)
+        pair = [models[i] for i, _, _ in PAIR]
+        for (i, slo, bmax), m in zip(PAIR, pair):
+            dep = min(ds.TOTAL_SLOTS, knee_at(tables[i][bmax], bmax) + OVERPROV)
+            ks = m.knee_search(bmax, FRACTIONS, 10, args.sweep_warmup, args.sweep_reps)
+            sw = m.switch_probe(bmax, 10, dep, reps=10)
+            reconf.append(dict(arch=MIX4[i][0], batch=bmax, search_knee_slots=ks["knee_slots"],
+                               sweep_knee_slots=knee_at(tables[i][bmax], bmax), search_probes=ks["probes"],
+                               search_seconds=ks["seconds"], switch_from_slots=10, switch_to_slots=dep, **sw))
         c1 = config1(ds)
         c2 = config2(ds, torch, args)
         c6 = config6(ds, args)
         c4 = config4(ds, torch, args)
-        extra = [("vgg19", 1052, [1, 2, 4, 8]), ("lstm2", 1053, [1, 2, 4, 8, 16, 32])]
-        m4 = [ds.Model(a, s) for a, s, _ in extra]
-        t4 = [t["table"] for t in tables]
-        for (a, s, bs), m in zip(extra, m4):
-            tab = {}
-            for b in bs:
-                r = m.knee_sweep(b, FRACTIONS, warmup=args.sweep_warmup, reps=args.sweep_reps)
-                tab[b] = dict(zip(r["slots"], r["latency_us"]))
-            t4.append(tab)
-        c5 = config5(ds, torch, models + m4, t4, args)
-        for m in m4:
-            m.destroy()
-        cmp = comparators(ds, t4)
-        ideal = ideal_vs_dstack(ds, models, tables, batch, xs, [gu.empty_f32(m.output_shape(b))
-                                                                for m, b in zip(models, batch)])
+        cmp = comparators(ds, tables)
+        pb = [bmax for _, _, bmax in PAIR]
+        ideal = ideal_vs_dstack(ds, pair, [slo for _, slo, _ in PAIR], pb,
+                                [gu.dev_bf16(inputs.image_batch(1061 + j, b)) for j, b in enumerate(pb)],
+                                [gu.empty_f32(m.output_shape(b)) for m, b in zip(pair, pb)])
 
     # calibration copy for the HBM byte counters (a plain 256 MiB device copy)
     a = torch.empty(64 * 1024 * 1024, dtype=torch.float32, device="cuda:0")
     b = torch.empty_like(a)
     b.copy_(a)
     torch.cuda.synchronize()
+    del a, b
 
+    sched_in = mix.tabs(k_run)
     cpu = None if args.no_cpu_baseline else cpu_baseline(args.cpu_seconds, sched_in)
-
+    run_keys = ("k", "offered_req_s", "requests", "served", "on_time", "violation_frac", "on_time_per_s", "run_us",
+                "call_wall_s", "utilisation_ppm", "per_model", "param")
     out = {
         "metric": METRIC,
         "value": value,
@@ -746,48 +873,54 @@ def main():
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": 1000.0 * t_mix / args.steps,
+        "ms_per_step": run_ds["run_us"] / 1000.0 / args.steps,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
         "config": {
-            "workload": "two-model mix: ResNet-50 v1.5 batch 16 (SLO 25 ms) + MobileNetV2 1.0 batch 32 "
-                        "(SLO 15 ms), 224x224x3, each on CU-masked partitions of its knee + 2 slots packed "
-                        "over the 32 slots; one step = ceil(100 ms / SLO) batches per partition, closed loop",
-            "batch": batch, "knee_slots": knee, "deployed_slots": dep,
-            "partitions": [(MODELS[mi][0], o, s) for mi, o, s in lanes],
-            "jobs_per_step": reps, "items_per_step": mix.items_per_step, "seeds": [s for _, s, *_ in MODELS],
-            "parallelism": "spatial (CU masks), 1 GPU",
+            "workload": "four-model Poisson mix on one MI355X: ResNet-50 v1.5 / MobileNetV2 1.0 / VGG-19 (224x224x3) "
+                        "and a 2-layer LSTM (512->1024, 50 steps) at 400/800/150/300 req/s x k, SLOs 25/15/50/30 ms, "
+                        "100 ms sessions, live D-STACK launcher (dstack_schedule batches and GPU% with the rates, "
+                        "session plan + FOD fill on home CU ranges) at its capacity k (<= 1% of requests late or "
+                        "unserved); value = requests completed within their SLO per second over K sessions",
+            "capacity_k": k_ds, "capacity_req_s": k_ds * mix.rate, "overprov_slots": ov,
+            "batch": plan["batch"], "deployed_slots": plan["deployed_slots"], "home_offset": plan["home_offset"],
+            "knee_slots": plan["knee_slots"], "model_seeds": [spec[1] for spec in MIX4],
+            "arrival_seeds": [2026 + i for i in range(len(MIX4))], "parallelism": "spatial (CU masks), 1 GPU",
         },
-        "conv_mfma_tflops_at_knee": conv_fl / (conv_ms * 1e-3) / 1e12,
+        "timesliced_inferences_per_s": run_t["on_time_per_s"],
+        "speedup_vs_timesliced": value / run_t["on_time_per_s"] if run_t["on_time_per_s"] > 0 else None,
+        "capacity_ratio_vs_timesliced": k_ds / best_t["k"] if best_t["k"] > 0 else None,
+        "dstack_run": {k: run_ds[k] for k in run_keys},
+        "timesliced_run": {k: run_t[k] for k in run_keys},
+        "timesliced_at_dstack_rate": {k: run_t_same[k] for k in run_keys},
+        "capacity": dict(dstack=dstack, temporal=temporal, probe_seconds=args.probe_seconds,
+                         violation_bar=VIOLATION_BAR, search_seconds=capacity_s),
+        "conv_mfma_tflops_at_knee": conv["fl"] / (conv["ms"] * 1e-3) / 1e12 if conv["ms"] > 0 else None,
         "conv_knee_cu": knee_cu,
-        "timesliced_inferences_per_s": seq_value,
-        "speedup_vs_timesliced": value / seq_value,
-        "interference": inter,
-        "mix": mix_metrics,
         "roofline": {
-            "bound": "mfma", "kernel": "conv_igemm (all launches of both models at their partitions)",
+            "bound": "mfma", "kernel": "conv_igemm (all launches of the four models at their deployed partitions)",
             "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS,
             "n_cu": knee_cu, "peak_partition": PEAK_BF16_TFLOPS * knee_cu / 256,
             "frac_partition": achieved / (PEAK_BF16_TFLOPS * knee_cu / 256),
-            "launches": conv_n, "avg_launch_us": 1000.0 * avg_ms, "flops_per_launch": conv_fl / max(conv_n, 1),
-            "algorithmic_bytes_per_launch": conv_by / max(conv_n, 1),
+            "launches": conv["n"], "avg_launch_us": 1000.0 * avg_ms,
+            "flops_per_launch": conv["fl"] / max(conv["n"], 1),
+            "algorithmic_bytes_per_launch": conv["by"] / max(conv["n"], 1),
             "traffic": measured_traffic(),
         },
         "cpu_baseline": cpu,
-        "schedule_status": "ok" if sched_st == ds.OK else "infeasible",
         "per_model": per_model,
+        "config3": c3,
         "reconfiguration": reconf,
         "config1": c1,
         "config2": c2,
         "config4": c4,
-        "config5": c5,
         "config6": c6,
         "comparators": cmp,
         "ideal_vs_dstack": ideal,
-        "timing_tables": {t["arch"]: {str(b): row for b, row in t["table"].items()} for t in tables},
+        "timing_tables": {spec[0]: {str(b): row for b, row in t.items()} for spec, t in zip(MIX4, tables)},
         "sweep_seconds": sweep_s,
     }
     print(json.dumps(out))

@@ -433,14 +433,28 @@ dstack_status dstack_schedule(const dstack_sched_model* models, int n_models, co
  * ignored) with no planned start to respect and the candidates in another
  * order: 1 by the model's SLO-optimal latency at its knee (least runtime
  * first), then index; 2 by deployed slots (smallest GPU% demand first),
- * then busy time, then index.  Other values -> E_INVALID. */
+ * then busy time, then index.
+ * 3 temporal sharing (the time-sliced full-GPU baseline of Sec. 6.1 and the
+ * "T" arm of Sec. 7): one model at a time holds all total_slots during its
+ * time slice; slices are proportional to the SLOs and repeat every
+ * slice_cycle_us (0: the smallest SLO, so every model gets a turn inside
+ * each of its SLO intervals): model i's slice is [off_i, off_i + len_i) of
+ * each cycle, len_i = floor(cycle * SLO_i / sum of SLOs), offsets in model
+ * order, the remainder of the cycle idle.  At every slice start, completion
+ * and arrival, if no job runs and the instant lies in the slice of a model
+ * with queued requests, that model starts a job (kind 0) on all the slots
+ * with the largest grid batch (<= max_batch, <= queued) whose table latency
+ * at total_slots ends by its slice's end; none fits: it waits.  No plan, no
+ * FOD (fod is ignored).  Other values -> E_INVALID. */
 typedef struct {
   int64_t duration_us;
   int fod;
   int sessions_window;                          /* 10 */
   const int64_t* arrivals_us[DSTACK_MAX_MODELS];
   int n_arrivals[DSTACK_MAX_MODELS];
-  int policy;                                   /* 0 D-STACK, 1 max-throughput, 2 max-min fair */
+  int policy;                                   /* 0 D-STACK, 1 max-throughput, 2 max-min fair, 3 temporal */
+  int pad;
+  int64_t slice_cycle_us;                       /* policy 3: slice cycle (0: the smallest SLO); >= 0 */
 } dstack_sim_params;
 
 typedef struct {
@@ -520,9 +534,22 @@ dstack_status dstack_simulate_ideal(const dstack_ideal_model* models, int n_mode
  *  - the call blocks for about duration_us plus the last job, then waits for
  *    the device; log (may be NULL) receives up to log_capacity job records,
  *    *n_log the number of jobs started.
- * Errors: E_INVALID (bad arguments, placement != 1), E_UNSUPPORTED (more
- * than 4 models), E_HIP; the plan's E_INFEASIBLE is not an error here (the
- * filled plan runs, as in dstack_simulate). */
+ *  - sim->policy 0 (D-STACK) or 3 (temporal sharing, see dstack_simulate):
+ *    with 3 every model runs on one partition of all total_slots (<= 32),
+ *    one job at a time, in the slices dstack_simulate describes, with slice
+ *    starts in place of planned starts;
+ *  - events (may be NULL) receives up to event_capacity triggers in the order
+ *    the launcher handled them, *n_events the number handled: kind 0 a
+ *    completion seen (model), kind 1 a planned start due (model, value_us =
+ *    its planned time, slot_mask = its slots; temporal: a slice start, mask
+ *    all slots), kind 2 an arrival admitted (model, value_us = its trace
+ *    time); t_us is the clock value the decision taken at that trigger used
+ *    (a job started there has start_us == t_us), so that the decisions can be
+ *    replayed from the table and this list alone.
+ * Errors: E_INVALID (bad arguments, D-STACK without placement 1, a policy
+ * other than 0 or 3), E_UNSUPPORTED (more than 4 models), E_HIP; the plan's
+ * E_INFEASIBLE is not an error here (the filled plan runs, as in
+ * dstack_simulate). */
 typedef struct {
   int64_t start_us;     /* host clock at launch */
   int64_t end_us;       /* host clock when completion was seen */
@@ -532,10 +559,19 @@ typedef struct {
   uint64_t slot_mask;
 } dstack_job_record;
 
+typedef struct {
+  int64_t t_us;        /* clock value of the decision at this trigger */
+  int64_t value_us;    /* arrival: trace time; planned / slice start: its planned time; else 0 */
+  uint64_t slot_mask;  /* planned / slice start: its slots; else 0 */
+  int kind;            /* 0 completion seen, 1 planned or slice start due, 2 arrival admitted */
+  int model;
+} dstack_serve_event;
+
 dstack_status dstack_serve(const dstack_model* models, int n_models, const void* const* d_in, void* const* d_out,
                            const dstack_sched_model* tables, const dstack_sched_params* params,
                            const dstack_sim_params* sim, dstack_run_out* out, dstack_job_record* log,
-                           int log_capacity, int* n_log);
+                           int log_capacity, int* n_log, dstack_serve_event* events, int event_capacity,
+                           int* n_events);
 
 /* ------------------------------------------------------------------ */
 /* Kernel-level entry points (the layers of Sec. 4.1's A.int table)     */

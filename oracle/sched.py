@@ -376,7 +376,7 @@ def _nearest_rank(sorted_vals, pct):
 
 
 def simulate(models, period, duration, arrivals, total=TOTAL_SLOTS, overprov=OVERPROVISION_SLOTS, fod=True,
-             sessions_window=10, placement="lowest", policy="dstack"):
+             sessions_window=10, placement="lowest", policy="dstack", slice_cycle=0, replay_events=None):
     """models: as for schedule(); arrivals: per model sorted list of integer us in [0, duration).
     Returns dict with per-model counters, utilisation_ppm and a hash of the job log.
 
@@ -387,7 +387,29 @@ def simulate(models, period, duration, arrivals, total=TOTAL_SLOTS, overprov=OVE
     "maxthroughput" -- least runtime first (the model's SLO-optimal latency
     at its deployed slots, then index), the schedule that favours the sum of
     throughputs; "maxmin" -- smallest demand first (deployed slots, then
-    busy time, then index), max-min fairness over GPU% demands."""
+    busy time, then index), max-min fairness over GPU% demands.
+
+    "temporal": the time-sliced full-GPU baseline of Sec. 6.1 and Sec. 7
+    (temporal sharing, "T"): one model at a time holds the whole GPU during
+    its time slice, slices proportional to the models' SLOs.  Reading: the
+    slices repeat every C = slice_cycle us (0: the smallest SLO, so that every
+    model gets a turn within every one of its SLO intervals); model i's slice is [off_i, off_i +
+    len_i) of each cycle with len_i = floor(C * SLO_i / sum of SLOs) and the
+    offsets in model order (the remainder of the cycle idles).  At every slice
+    start, completion and arrival, if no job runs and the instant lies in a
+    slice whose model has queued requests, that model starts a job on all
+    the slots with the largest grid batch (<= max_batch, <= queued) whose
+    table latency at all the slots ends by its slice's end (the adaptive
+    batch of the slice); none fits: it waits.  No plan, no FOD.
+
+    replay_events: instead of the virtual clock, the triggers a live launcher
+    handled, in its order, as dicts (kind, t_us, model, value_us, slot_mask):
+    kind 0 a completion seen (the model's job ends), 1 a planned start due
+    (value_us its planned time, slot_mask its slots; temporal: a slice
+    start), 2 an arrival admitted (value_us its trace time); each decision is
+    taken at t_us with the same rules (a planned start also needs its slots
+    free, since a measured job may overrun its table time).  The jobs started
+    are then in "log" as (start, table end, model, mask, kind, batch)."""
     import collections
     import heapq
     choices, jobs, _, _ = schedule(models, period, total, overprov, placement)
@@ -397,6 +419,11 @@ def simulate(models, period, duration, arrivals, total=TOTAL_SLOTS, overprov=OVE
     planned = [j for j in jobs if not j.missed] if policy == "dstack" else []
     if policy != "dstack":
         fod = True
+    if policy == "temporal":
+        cycle = slice_cycle if slice_cycle > 0 else min(m["slo_us"] for m in models)
+        slo_sum = sum(m["slo_us"] for m in models)
+        slice_len = [cycle * m["slo_us"] // slo_sum for m in models]
+        slice_off = [sum(slice_len[:i]) for i in range(n)]
     # next planned start of each model after time t (over all periods)
     n_periods = ceil_div(duration, period)
 
@@ -413,6 +440,13 @@ def simulate(models, period, duration, arrivals, total=TOTAL_SLOTS, overprov=OVE
             if t < duration:
                 heapq.heappush(ev, (t, 1, j.model, seq, (j.slot_mask, j.duration)))
                 seq += 1
+    if policy == "temporal":  # slice starts take the place of planned starts
+        for k in range(ceil_div(duration, cycle)):
+            for i in range(n):
+                t = k * cycle + slice_off[i]
+                if slice_len[i] > 0 and t < duration:
+                    heapq.heappush(ev, (t, 1, i, seq, None))
+                    seq += 1
     for i in range(n):
         for a in arrivals[i]:
             heapq.heappush(ev, (a, 2, i, seq, None))
@@ -455,7 +489,29 @@ def simulate(models, period, duration, arrivals, total=TOTAL_SLOTS, overprov=OVE
         else:
             fod_runs[i] += 1
 
+    def temporal_pass(t):
+        if t >= duration or running:
+            return
+        r = t % cycle
+        owner = [i for i in range(n) if slice_off[i] <= r < slice_off[i] + slice_len[i]]
+        if not owner or not queue[owner[0]]:
+            return
+        i = owner[0]
+        left = slice_off[i] + slice_len[i] - r
+        best = None
+        for b in BATCH_GRID:
+            if b > models[i]["max_batch"] or b > len(queue[i]):
+                continue
+            L = lat(i, b, total)
+            if L is not None and L <= left:
+                best = (b, L)
+        if best is not None:
+            start_job(t, i, range_mask(0, total), best[1], best[0], 0)
+
     def fod_pass(t):
+        if policy == "temporal":
+            temporal_pass(t)
+            return
         if t >= duration:  # nothing starts once the trace has ended
             return
         cands = [i for i in range(n) if i not in running and queue[i]]
@@ -497,8 +553,35 @@ def simulate(models, period, duration, arrivals, total=TOTAL_SLOTS, overprov=OVE
             start_job(t, i, mask, best[1], best[0], 1)
             return
 
+    if replay_events is not None:
+        plan_dur = {(p * period + j.start, j.model, j.slot_mask): j.duration for p in range(n_periods) for j in planned}
+        for e in replay_events:
+            t, i = e["t_us"], e["model"]
+            if e["kind"] == 0:
+                _, mask = running.pop(i)
+                used &= ~mask
+                if fod:
+                    fod_pass(t)
+            elif e["kind"] == 1 and policy == "temporal":
+                temporal_pass(t)
+            elif e["kind"] == 1:
+                mask, dur = e["slot_mask"], plan_dur[(e["value_us"], i, e["slot_mask"])]
+                if queue[i] and i not in running and not used & mask:
+                    start_job(t, i, mask, dur, min(choices[i].batch, len(queue[i])), 0)
+                else:
+                    plan_skips[i] += 1
+            else:
+                queue[i].append(e["value_us"])
+                if fod:
+                    fod_pass(t)
+        return dict(log=log, plan_skips=plan_skips, job_hash=h)
+
+    events = []  # the triggers in the order handled, in the form replay_events takes
     while ev:
         t, kind, i, _, payload = heapq.heappop(ev)
+        events.append(dict(kind=kind, t_us=t, model=i, value_us=0 if kind == 0 else t,
+                           slot_mask=payload[0] if kind == 1 and payload else
+                           (range_mask(0, total) if kind == 1 else 0)))
         if kind == 0:
             end, mask = running.pop(i)
             used &= ~mask
@@ -509,6 +592,8 @@ def simulate(models, period, duration, arrivals, total=TOTAL_SLOTS, overprov=OVE
                     late[i] += 1
             if fod:
                 fod_pass(t)
+        elif kind == 1 and policy == "temporal":
+            temporal_pass(t)
         elif kind == 1:
             mask, dur = payload
             if queue[i] and i not in running:
@@ -526,7 +611,7 @@ def simulate(models, period, duration, arrivals, total=TOTAL_SLOTS, overprov=OVE
                         planned_runs=planned_runs[i], fod_runs=fod_runs[i], busy_us=busy[i],
                         p50_us=_nearest_rank(L, 50), p99_us=_nearest_rank(L, 99), plan_skips=plan_skips[i]))
     return dict(models=out, utilisation_ppm=slot_us * 1000000 // (total * max(duration, 1)), job_hash=h,
-                last_end_us=last_end, log=log)
+                last_end_us=last_end, log=log, events=events)
 
 
 def simulate_ideal(models, horizon, slot, total=TOTAL_SLOTS):

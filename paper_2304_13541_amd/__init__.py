@@ -104,7 +104,12 @@ class ScheduleOut(ctypes.Structure):
 class SimParams(ctypes.Structure):
     _fields_ = [("duration_us", ctypes.c_int64), ("fod", ctypes.c_int), ("sessions_window", ctypes.c_int),
                 ("arrivals_us", ctypes.POINTER(ctypes.c_int64) * MAX_MODELS), ("n_arrivals", ctypes.c_int * MAX_MODELS),
-                ("policy", ctypes.c_int)]
+                ("policy", ctypes.c_int), ("pad", ctypes.c_int), ("slice_cycle_us", ctypes.c_int64)]
+
+
+class ServeEvent(ctypes.Structure):
+    _fields_ = [("t_us", ctypes.c_int64), ("value_us", ctypes.c_int64), ("slot_mask", ctypes.c_uint64),
+                ("kind", ctypes.c_int), ("model", ctypes.c_int)]
 
 
 class IdealModel(ctypes.Structure):
@@ -182,7 +187,8 @@ _SIGS = {
     "dstack_switch_probe": ([_vp, _i, _i, _i, _i, ctypes.POINTER(SwitchResult)], _i),
     "dstack_serve": ([ctypes.POINTER(_vp), _i, ctypes.POINTER(_vp), ctypes.POINTER(_vp), ctypes.POINTER(SchedModel),
                       ctypes.POINTER(SchedParams), ctypes.POINTER(SimParams), ctypes.POINTER(RunOut),
-                      ctypes.POINTER(JobRecord), _i, ctypes.POINTER(_i)], _i),
+                      ctypes.POINTER(JobRecord), _i, ctypes.POINTER(_i), ctypes.POINTER(ServeEvent), _i,
+                      ctypes.POINTER(_i)], _i),
     "dstack_op_conv2d": ([_vp, _i, _i, _i, _i, _vp, _i, _i, _i, _i, _i, _vp, _vp, _vp, _i, _vp, _i, _vp], _i),
     "dstack_op_conv2d_ws": ([_vp, _i, _i, _i, _i, _vp, _i, _i, _i, _i, _i, _vp, _vp, _vp, _i, _vp, _i, _i, _vp, _sz,
                              _vp], _i),
@@ -450,16 +456,17 @@ def _stats(out):
 PLACEMENTS = {"lowest": 0, "home": 1}
 
 
-POLICIES = {"dstack": 0, "maxthroughput": 1, "maxmin": 2}
+POLICIES = {"dstack": 0, "maxthroughput": 1, "maxmin": 2, "temporal": 3}
 
 
-def _sim_params(duration_us, arrivals, fod, sessions_window, policy="dstack"):
+def _sim_params(duration_us, arrivals, fod, sessions_window, policy="dstack", slice_cycle_us=0):
     """SimParams plus the arrival buffers it points into (keep them alive)."""
     sp = SimParams()
     sp.duration_us = duration_us
     sp.fod = int(fod)
     sp.sessions_window = sessions_window
     sp.policy = POLICIES[policy]
+    sp.slice_cycle_us = slice_cycle_us
     keep = []
     for i, a in enumerate(arrivals):
         buf = (ctypes.c_int64 * max(1, len(a)))(*a)
@@ -470,12 +477,12 @@ def _sim_params(duration_us, arrivals, fod, sessions_window, policy="dstack"):
 
 
 def simulate(models, period_us, duration_us, arrivals, total_slots=TOTAL_SLOTS, overprov_slots=2, fod=True,
-             sessions_window=10, placement="lowest", policy="dstack"):
+             sessions_window=10, placement="lowest", policy="dstack", slice_cycle_us=0):
     """Launcher simulation on the timing table (see dstack_simulate); policy
-    "dstack", "maxthroughput" or "maxmin".  arrivals: per model sorted
-    integer-us arrival times.  Returns a dict."""
+    "dstack", "maxthroughput", "maxmin" or "temporal".  arrivals: per model
+    sorted integer-us arrival times.  Returns a dict."""
     arr = _sched_models(models)
-    sp, keep = _sim_params(duration_us, arrivals, fod, sessions_window, policy)
+    sp, keep = _sim_params(duration_us, arrivals, fod, sessions_window, policy, slice_cycle_us)
     out = RunOut()
     prm = SchedParams(period_us, total_slots, overprov_slots, PLACEMENTS[placement])
     _check(lib().dstack_simulate(arr, len(models), ctypes.byref(prm), ctypes.byref(sp), ctypes.byref(out)))
@@ -502,13 +509,16 @@ def simulate_ideal(models, horizon_us, slot_us, total_slots=TOTAL_SLOTS):
 
 
 def serve(handles, tables, inputs, outputs, period_us, duration_us, arrivals, total_slots=TOTAL_SLOTS,
-          overprov_slots=2, fod=True, sessions_window=10, log_capacity=1 << 16):
+          overprov_slots=2, fod=True, sessions_window=10, log_capacity=1 << 16, policy="dstack", slice_cycle_us=0,
+          event_capacity=0):
     """Live launcher (see dstack_serve): handles are Model objects, tables the
     timing tables in the form simulate() takes, inputs/outputs device tensors
-    sized for each model's max batch.  Blocks for about duration_us."""
+    sized for each model's max batch; policy "dstack" or "temporal".  Blocks
+    for about duration_us.  With event_capacity > 0 the result holds the
+    launcher's triggers ("events") for a replay."""
     n = len(handles)
     arr = _sched_models(tables)
-    sp, keep = _sim_params(duration_us, arrivals, fod, sessions_window)
+    sp, keep = _sim_params(duration_us, arrivals, fod, sessions_window, policy, slice_cycle_us)
     hv = (_vp * n)(*[m.h.value for m in handles])
     iv = (_vp * n)(*[t.data_ptr() for t in inputs])
     ov = (_vp * n)(*[t.data_ptr() for t in outputs])
@@ -516,11 +526,14 @@ def serve(handles, tables, inputs, outputs, period_us, duration_us, arrivals, to
     out = RunOut()
     log = (JobRecord * max(1, log_capacity))()
     n_log = ctypes.c_int(0)
+    evs = (ServeEvent * max(1, event_capacity))()
+    n_ev = ctypes.c_int(0)
     _check(lib().dstack_serve(hv, n, iv, ov, arr, ctypes.byref(prm), ctypes.byref(sp), ctypes.byref(out), log,
-                              log_capacity, ctypes.byref(n_log)))
+                              log_capacity, ctypes.byref(n_log), evs, event_capacity, ctypes.byref(n_ev)))
     jobs = [dict((f, getattr(r, f)) for f, _ in JobRecord._fields_) for r in log[:min(n_log.value, log_capacity)]]
+    events = [dict((f, getattr(r, f)) for f, _ in ServeEvent._fields_) for r in evs[:min(n_ev.value, event_capacity)]]
     return dict(models=_stats(out), utilisation_ppm=out.utilisation_ppm, job_hash=out.job_hash,
-                last_end_us=out.last_end_us, n_jobs=n_log.value, log=jobs)
+                last_end_us=out.last_end_us, n_jobs=n_log.value, log=jobs, n_events=n_ev.value, events=events)
 
 
 def schedule(models, period_us, total_slots=TOTAL_SLOTS, overprov_slots=2, placement="lowest"):

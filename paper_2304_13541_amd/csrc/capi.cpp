@@ -772,8 +772,12 @@ dstack_status dstack_simulate_ideal(const dstack_ideal_model* models, int n, int
 dstack_status dstack_serve(const dstack_model* models, int n, const void* const* d_in, void* const* d_out,
                            const dstack_sched_model* tables, const dstack_sched_params* prm,
                            const dstack_sim_params* sim, dstack_run_out* out, dstack_job_record* log,
-                           int log_capacity, int* n_log) {
-  return guarded([&] { return serve(models, n, d_in, d_out, tables, prm, sim, out, log, log_capacity, n_log); });
+                           int log_capacity, int* n_log, dstack_serve_event* events, int event_capacity,
+                           int* n_events) {
+  return guarded([&] {
+    return serve(models, n, d_in, d_out, tables, prm, sim, out, log, log_capacity, n_log, events, event_capacity,
+                 n_events);
+  });
 }
 
 // ----------------------------------------------------- kernel-level ops ----

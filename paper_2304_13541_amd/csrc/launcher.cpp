@@ -71,7 +71,9 @@ int64_t nearest_rank(std::vector<int64_t>& v, int pct) {
 }
 
 bool check_trace(int n, const dstack_sim_params* sim) {
-  if (sim->duration_us <= 0 || sim->sessions_window < 1 || sim->policy < 0 || sim->policy > 2) return false;
+  if (sim->duration_us <= 0 || sim->sessions_window < 1 || sim->policy < 0 || sim->policy > 3 ||
+      sim->slice_cycle_us < 0)
+    return false;
   for (int i = 0; i < n; ++i) {
     if (sim->n_arrivals[i] < 0 || (sim->n_arrivals[i] > 0 && !sim->arrivals_us[i])) return false;
     for (int k = 0; k < sim->n_arrivals[i]; ++k) {
@@ -96,6 +98,50 @@ LaunchState::LaunchState(const dstack_sched_model* models, int n, const dstack_s
     }
   std::stable_sort(pstarts_.begin(), pstarts_.end(),
                    [](const PlannedStart& a, const PlannedStart& b) { return a.t < b.t; });
+  if (sim->policy == 3) {  // temporal: slices proportional to the SLOs, repeated every cycle
+    int64_t slo_min = models[0].slo_us, slo_sum = 0;
+    for (int i = 0; i < n; ++i) {
+      slo_min = std::min(slo_min, models[i].slo_us);
+      slo_sum += models[i].slo_us;
+    }
+    cycle_ = sim->slice_cycle_us > 0 ? sim->slice_cycle_us : slo_min;
+    int64_t off = 0;
+    for (int i = 0; i < n; ++i) {
+      const int64_t len = (int64_t)((unsigned __int128)cycle_ * (uint64_t)models[i].slo_us / (uint64_t)slo_sum);
+      slice_off_.push_back(off);
+      slice_len_.push_back(len);
+      off += len;
+    }
+    const uint64_t all = range_mask(0, prm->total_slots);
+    for (int64_t k = 0; k * cycle_ < D_; ++k)
+      for (int i = 0; i < n; ++i) {
+        const int64_t t = k * cycle_ + slice_off_[i];
+        if (slice_len_[i] > 0 && t < D_) slices_.push_back(PlannedStart{t, i, all, 0});
+      }
+  }
+}
+
+bool LaunchState::temporal_pick(int64_t t, Pick* out) const {
+  if (t >= D_ || used_ != 0) return false;
+  const int64_t r = t % cycle_;
+  int i = -1;
+  for (int j = 0; j < n_; ++j)
+    if (r >= slice_off_[j] && r < slice_off_[j] + slice_len_[j]) i = j;
+  if (i < 0 || queue_[i].empty()) return false;
+  const int64_t left = slice_off_[i] + slice_len_[i] - r;
+  const int total = prm_->total_slots;
+  int bb = -1;
+  int64_t bL = 0;
+  for (int b : kGrid) {
+    if (b > models_[i].max_batch || b > (int)queue_[i].size()) continue;
+    const int64_t L = table_latency(i, b, total);
+    if (L <= 0 || L > left) continue;
+    bb = b;
+    bL = L;
+  }
+  if (bb < 0) return false;
+  *out = Pick{i, range_mask(0, total), bb, bL};
+  return true;
 }
 
 int64_t LaunchState::table_latency(int i, int b, int slots) const {
@@ -216,6 +262,7 @@ dstack_status simulate(const dstack_sched_model* models, int n, const dstack_sch
   std::priority_queue<Event, std::vector<Event>, std::greater<Event>> ev;
   int64_t seq = 0;
   for (const PlannedStart& ps : ls.planned()) ev.push(Event{ps.t, 1, ps.model, seq++, ps.mask, ps.dur, {}});
+  for (const PlannedStart& ps : ls.slice_starts()) ev.push(Event{ps.t, 1, ps.model, seq++, ps.mask, 0, {}});
   for (int i = 0; i < n; ++i)
     for (int k = 0; k < sim->n_arrivals[i]; ++k) ev.push(Event{sim->arrivals_us[i][k], 2, i, seq++, 0, 0, {}});
 
@@ -235,7 +282,11 @@ dstack_status simulate(const dstack_sched_model* models, int n, const dstack_sch
   };
   auto fod_pass = [&](int64_t t) {
     LaunchState::Pick pk;
-    if ((sim->fod || sim->policy != 0) && ls.fod_pick(t, &pk)) launch(t, pk.model, pk.mask, pk.latency, pk.batch, 1);
+    if (ls.temporal()) {
+      if (ls.temporal_pick(t, &pk)) launch(t, pk.model, pk.mask, pk.latency, pk.batch, 0);
+    } else if ((sim->fod || sim->policy != 0) && ls.fod_pick(t, &pk)) {
+      launch(t, pk.model, pk.mask, pk.latency, pk.batch, 1);
+    }
   };
 
   while (!ev.empty()) {
@@ -249,6 +300,8 @@ dstack_status simulate(const dstack_sched_model* models, int n, const dstack_sch
         lats[i].push_back(e.t - a);
         if (e.t - a > models[i].slo_us) late[i] += 1;
       }
+      fod_pass(e.t);
+    } else if (e.kind == 1 && ls.temporal()) {
       fod_pass(e.t);
     } else if (e.kind == 1) {
       if (ls.queued(i) && !ls.running(i))

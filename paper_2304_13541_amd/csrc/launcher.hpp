@@ -43,6 +43,12 @@ class LaunchState {
   };
   // the FOD choice at time t (false: nothing fits)
   bool fod_pick(int64_t t, Pick* out) const;
+  // temporal policy: the slice starts in time order, and the job its slice
+  // owner starts at time t on the whole GPU (false: none)
+  const std::vector<PlannedStart>& slice_starts() const { return slices_; }
+  bool temporal_pick(int64_t t, Pick* out) const;
+  bool temporal() const { return sim_->policy == 3; }
+  bool any_running() const { return used_ != 0; }
   // a job starts: pops b requests (returned, oldest first), charges the run
   // and `charged_us` of busy time, marks its slots used
   std::vector<int64_t> start(int64_t t, int i, uint64_t mask, int64_t charged_us, int b);
@@ -59,6 +65,9 @@ class LaunchState {
   const dstack_schedule_out* plan_;
   int64_t T_, D_;
   std::vector<PlannedStart> pstarts_;  // by time, then plan order
+  int64_t cycle_ = 0;                  // temporal policy: slice cycle, slice offsets and lengths
+  std::vector<int64_t> slice_off_, slice_len_;
+  std::vector<PlannedStart> slices_;
   std::vector<std::deque<int64_t>> queue_;
   std::vector<char> running_;
   std::vector<uint64_t> run_mask_;
@@ -77,6 +86,7 @@ dstack_status simulate_ideal(const dstack_ideal_model* models, int n, int64_t ho
 
 dstack_status serve(const dstack_model* models, int n, const void* const* d_in, void* const* d_out,
                     const dstack_sched_model* tables, const dstack_sched_params* prm, const dstack_sim_params* sim,
-                    dstack_run_out* out, dstack_job_record* log, int log_capacity, int* n_log);
+                    dstack_run_out* out, dstack_job_record* log, int log_capacity, int* n_log,
+                    dstack_serve_event* events, int event_capacity, int* n_events);
 
 }  // namespace dstack

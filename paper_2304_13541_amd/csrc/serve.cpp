@@ -5,7 +5,11 @@
 // launches planned and FOD jobs through dstack_infer, and polls each job's
 // end event.  The decisions are those of the virtual-clock simulation (the
 // same LaunchState, fed with table latencies); only the completion times and
-// GPU durations are measured.
+// GPU durations are measured.  Every trigger (a completion seen, a planned
+// or slice start due, an arrival admitted) is logged with the clock value
+// its decision used, so that the decisions can be replayed off the GPU.
+// The temporal-sharing baseline (policy 3) runs the same loop with slice
+// starts in place of planned starts, every model on one whole-GPU partition.
 #include <hip/hip_runtime.h>
 
 #include <chrono>
@@ -56,14 +60,20 @@ struct Resources {
 
 dstack_status serve(const dstack_model* models, int n, const void* const* d_in, void* const* d_out,
                     const dstack_sched_model* tables, const dstack_sched_params* prm, const dstack_sim_params* sim,
-                    dstack_run_out* out, dstack_job_record* log, int log_capacity, int* n_log) {
+                    dstack_run_out* out, dstack_job_record* log, int log_capacity, int* n_log,
+                    dstack_serve_event* events, int event_capacity, int* n_events) {
   DS_CHECK(models && d_in && d_out && tables && prm && sim && out, DSTACK_E_INVALID, "serve: null pointer");
   DS_CHECK(n >= 1 && n <= DSTACK_MAX_MODELS, DSTACK_E_INVALID, "serve: bad model count");
   DS_CHECK(n <= kMaxServeModels, DSTACK_E_UNSUPPORTED, "serve: at most 4 models (one CU-masked stream each)");
-  DS_CHECK(prm->placement == 1, DSTACK_E_INVALID, "serve: placement must be 1 (home ranges)");
   DS_CHECK(log_capacity >= 0 && (log || log_capacity == 0), DSTACK_E_INVALID, "serve: bad log buffer");
+  DS_CHECK(event_capacity >= 0 && (events || event_capacity == 0), DSTACK_E_INVALID, "serve: bad event buffer");
   DS_CHECK(check_trace(n, sim), DSTACK_E_INVALID, "serve: bad trace (see dstack_simulate)");
-  DS_CHECK(sim->policy == 0, DSTACK_E_INVALID, "serve: runs the D-STACK policy only (policy 0)");
+  DS_CHECK(sim->policy == 0 || sim->policy == 3, DSTACK_E_INVALID,
+           "serve: runs the D-STACK policy (0) or temporal sharing (3)");
+  const bool temporal = sim->policy == 3;
+  DS_CHECK(temporal || prm->placement == 1, DSTACK_E_INVALID, "serve: D-STACK needs placement 1 (home ranges)");
+  DS_CHECK(prm->total_slots >= 1 && prm->total_slots <= DSTACK_TOTAL_SLOTS, DSTACK_E_INVALID,
+           "serve: total_slots must be in 1..32 (one GPU)");
   for (int i = 0; i < n; ++i) {
     DS_CHECK(models[i] && d_in[i] && d_out[i], DSTACK_E_INVALID, "serve: null model or buffer");
     dstack_model_info q;
@@ -77,18 +87,28 @@ dstack_status serve(const dstack_model* models, int n, const void* const* d_in, 
   dstack_status st = schedule(tables, n, prm, plan);
   if (st != DSTACK_OK && st != DSTACK_E_INFEASIBLE) return st;
 
+  // D-STACK: model i owns a partition on its home range.  Temporal sharing:
+  // one partition of all the slots, which every model's jobs use in turn.
   Resources res;
-  res.part.assign(n, nullptr);
+  const int n_parts = temporal ? 1 : n;
+  res.part.assign(n_parts, nullptr);
   res.ev0.assign(n, nullptr);
   res.ev1.assign(n, nullptr);
-  std::vector<hipStream_t> stream(n);
-  for (int i = 0; i < n; ++i) {
-    st = dstack_partition_create_at(plan->home_offset[i], plan->deployed_slots[i], &res.part[i]);
+  std::vector<hipStream_t> pstream(n_parts);
+  for (int q = 0; q < n_parts; ++q) {
+    st = temporal ? dstack_partition_create_at(0, prm->total_slots, &res.part[q])
+                  : dstack_partition_create_at(plan->home_offset[q], plan->deployed_slots[q], &res.part[q]);
     if (st != DSTACK_OK) return st;
     void* sp = nullptr;
-    st = dstack_partition_query(res.part[i], nullptr, nullptr, &sp);
+    st = dstack_partition_query(res.part[q], nullptr, nullptr, &sp);
     if (st != DSTACK_OK) return st;
-    stream[i] = (hipStream_t)sp;
+    pstream[q] = (hipStream_t)sp;
+  }
+  std::vector<dstack_partition> part(n);
+  std::vector<hipStream_t> stream(n);
+  for (int i = 0; i < n; ++i) {
+    part[i] = res.part[temporal ? 0 : i];
+    stream[i] = pstream[temporal ? 0 : i];
     DS_HIP(hipEventCreate(&res.ev0[i]));
     DS_HIP(hipEventCreate(&res.ev1[i]));
   }
@@ -96,18 +116,18 @@ dstack_status serve(const dstack_model* models, int n, const void* const* d_in, 
 
   // warm-up: every batch a job of this run can take (captures its graph)
   for (int i = 0; i < n; ++i) {
-    const int dep = plan->deployed_slots[i];
+    const int slots = temporal ? prm->total_slots : plan->deployed_slots[i];
     for (int b : kGrid) {
       if (b > tables[i].max_batch) continue;
-      if (b != plan->batch[i] && ls.table_latency(i, b, dep) <= 0) continue;
+      if ((temporal || b != plan->batch[i]) && ls.table_latency(i, b, slots) <= 0) continue;
       for (int r = 0; r < 2; ++r) {
-        st = dstack_infer(models[i], b, d_in[i], d_out[i], res.part[i]);
+        st = dstack_infer(models[i], b, d_in[i], d_out[i], part[i]);
         if (st != DSTACK_OK) return st;
       }
     }
   }
-  for (int i = 0; i < n; ++i) {
-    st = dstack_synchronize(res.part[i]);
+  for (int q = 0; q < n_parts; ++q) {
+    st = dstack_synchronize(res.part[q]);
     if (st != DSTACK_OK) return st;
   }
 
@@ -120,10 +140,15 @@ dstack_status serve(const dstack_model* models, int n, const void* const* d_in, 
   size_t next_plan = 0;
   int64_t slot_us = 0, last_end = 0;
   uint64_t h = 0xcbf29ce484222325ULL;
-  int jobs = 0;
-  const std::vector<PlannedStart>& P = ls.planned();
+  int jobs = 0, n_ev = 0;
+  // planned starts of the session plan (D-STACK) or slice starts (temporal)
+  const std::vector<PlannedStart>& P = temporal ? ls.slice_starts() : ls.planned();
   const int64_t t0 = host_us();
   auto clock = [&] { return host_us() - t0; };
+  auto note = [&](int64_t t, int kind, int model, int64_t value, uint64_t mask) {
+    if (n_ev < event_capacity) events[n_ev] = dstack_serve_event{t, value, mask, kind, model};
+    ++n_ev;
+  };
 
   auto launch = [&](int64_t t, int i, uint64_t mask, int64_t table_us, int b, int kind) -> dstack_status {
     Running& r = run[i];
@@ -135,7 +160,7 @@ dstack_status serve(const dstack_model* models, int n, const void* const* d_in, 
     r.batch = b;
     r.kind = kind;
     DS_HIP(hipEventRecord(res.ev0[i], stream[i]));
-    dstack_status s = dstack_infer(models[i], b, d_in[i], d_out[i], res.part[i]);
+    dstack_status s = dstack_infer(models[i], b, d_in[i], d_out[i], part[i]);
     if (s != DSTACK_OK) return s;
     DS_HIP(hipEventRecord(res.ev1[i], stream[i]));
     for (int64_t v : {t, (int64_t)i, (int64_t)b, (int64_t)mask, table_us, (int64_t)kind})
@@ -148,7 +173,11 @@ dstack_status serve(const dstack_model* models, int n, const void* const* d_in, 
   };
   auto fod_pass = [&](int64_t t) -> dstack_status {
     LaunchState::Pick pk;
-    if (sim->fod && ls.fod_pick(t, &pk)) return launch(t, pk.model, pk.mask, pk.latency, pk.batch, 1);
+    if (temporal) {
+      if (ls.temporal_pick(t, &pk)) return launch(t, pk.model, pk.mask, pk.latency, pk.batch, 0);
+    } else if (sim->fod && ls.fod_pick(t, &pk)) {
+      return launch(t, pk.model, pk.mask, pk.latency, pk.batch, 1);
+    }
     return DSTACK_OK;
   };
 
@@ -187,15 +216,21 @@ dstack_status serve(const dstack_model* models, int n, const void* const* d_in, 
       if (jobs < log_capacity)
         log[jobs] = dstack_job_record{r.start, te, gpu_us, r.table_us, i, r.batch, r.kind, r.mask};
       ++jobs;
+      note(te, 0, i, 0, 0);
       st = fod_pass(te);
       if (st != DSTACK_OK) return st;
     }
-    // planned starts that are due
+    // planned starts (temporal: slice starts) that are due
     while (next_plan < P.size() && P[next_plan].t <= t) {
       const PlannedStart& ps = P[next_plan++];
       const int i = ps.model;
-      if (ls.queued(i) && !ls.running(i) && ls.free(ps.mask)) {
-        st = launch(clock(), i, ps.mask, ps.dur, std::min<int>(ls.plan_batch(i), (int)ls.queued(i)), 0);
+      const int64_t tn = clock();
+      note(tn, 1, i, ps.t, ps.mask);
+      if (temporal) {
+        st = fod_pass(tn);
+        if (st != DSTACK_OK) return st;
+      } else if (ls.queued(i) && !ls.running(i) && ls.free(ps.mask)) {
+        st = launch(tn, i, ps.mask, ps.dur, std::min<int>(ls.plan_batch(i), (int)ls.queued(i)), 0);
         if (st != DSTACK_OK) return st;
         busy_now = true;
       } else {
@@ -210,9 +245,12 @@ dstack_status serve(const dstack_model* models, int n, const void* const* d_in, 
             (j < 0 || sim->arrivals_us[i][next_arr[i]] < sim->arrivals_us[j][next_arr[j]]))
           j = i;
       if (j < 0) break;
-      ls.arrive(j, sim->arrivals_us[j][next_arr[j]]);
+      const int64_t a = sim->arrivals_us[j][next_arr[j]];
+      ls.arrive(j, a);
       next_arr[j] += 1;
-      st = fod_pass(clock());
+      const int64_t tn = clock();
+      note(tn, 2, j, a, 0);
+      st = fod_pass(tn);
       if (st != DSTACK_OK) return st;
     }
     for (int i = 0; i < n; ++i) busy_now = busy_now || run[i].on;
@@ -222,8 +260,8 @@ dstack_status serve(const dstack_model* models, int n, const void* const* d_in, 
       return fail(DSTACK_E_HIP, "serve: a job did not complete within 60 s after the trace");
     }
   }
-  for (int i = 0; i < n; ++i) {
-    st = dstack_synchronize(res.part[i]);
+  for (int q = 0; q < n_parts; ++q) {
+    st = dstack_synchronize(res.part[q]);
     if (st != DSTACK_OK) return st;
   }
 
@@ -245,6 +283,7 @@ dstack_status serve(const dstack_model* models, int n, const void* const* d_in, 
   out->job_hash = h;
   out->last_end_us = last_end;
   if (n_log) *n_log = jobs;
+  if (n_events) *n_events = n_ev;
   return DSTACK_OK;
 }
 

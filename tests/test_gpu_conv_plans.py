@@ -152,6 +152,8 @@ FORCED = [
     (1, 14, 14, 1024, 256, 1, 1, 0, 1),
     (1, 13, 13, 512, 512, 3, 2, 1, 1),
     (2, 9, 9, 256, 384, 3, 1, 1, 0),
+    (8, 7, 7, 512, 256, 3, 1, 1, 1),   # 128 x 128 tiles, 4 slices at 24 CUs
+    (8, 15, 15, 256, 128, 3, 1, 1, 2),  # 128 x 128 tiles, 2 slices at 24 CUs, ragged pixels
 ]
 
 

@@ -6,7 +6,11 @@ Poisson traces.  Checked: every request is served or counted unserved; each
 job runs on its model's home range with a batch from the grid; one model
 never has two jobs at once and jobs whose ranges meet never overlap in time;
 nothing starts after the trace; the served outputs equal an eager inference
-of the same input rows."""
+of the same input rows.  Decision parity: the launcher's own trigger log
+(each completion seen, planned or slice start due and arrival admitted,
+with the clock value its decision used) replayed through the scheduler
+oracle starts exactly the same jobs (time, model, batch, slots, kind), for
+the D-STACK policy and for temporal sharing on the whole GPU."""
 import numpy as np
 import pytest
 
@@ -82,6 +86,38 @@ def test_serve_two_models(env):
         got, want = ys[i][:b].float().cpu().numpy(), ref[:b].float().cpu().numpy()
         assert np.max(np.abs(got - want)) <= 1e-2 * max(1e-6, np.max(np.abs(want)))
         p.destroy()
+    for m in models:
+        m.destroy()
+
+
+@pytest.mark.parametrize("policy", ["dstack", "temporal"])
+def test_serve_decisions_replay_through_the_oracle(env, policy):
+    ds, sched, poisson_arrivals, torch = env
+    models = [ds.Model("tinycnn", 17), ds.Model("mobilenetv2", 18)]
+    tables = [dict(slo_us=4000, max_batch=4, rate_per_s=0, table=measured_table(ds, models[0], [1, 2, 4])),
+              dict(slo_us=6000, max_batch=8, rate_per_s=0, table=measured_table(ds, models[1], [1, 2, 4, 8]))]
+    duration = 300_000
+    arrivals = [poisson_arrivals(21, 2500, duration), poisson_arrivals(22, 2000, duration)]
+    g = torch.Generator(device="cuda").manual_seed(4)
+    xs = [torch.randn(m.input_shape(t["max_batch"]), device="cuda", generator=g).to(torch.bfloat16)
+          for m, t in zip(models, tables)]
+    ys = [torch.zeros(m.output_shape(t["max_batch"]), device="cuda", dtype=torch.float32)
+          for m, t in zip(models, tables)]
+    r = ds.serve(models, tables, xs, ys, period_us=10_000, duration_us=duration, arrivals=arrivals, policy=policy,
+                 event_capacity=1 << 16)
+    torch.cuda.synchronize()
+    assert r["n_events"] == len(r["events"]) and r["n_jobs"] == len(r["log"]) > 20
+    rep = sched.simulate(tables, 10_000, duration, arrivals, placement="home" if policy == "dstack" else "lowest",
+                         policy=policy, replay_events=r["events"])
+    live = sorted((j["start_us"], j["model"], j["batch"], j["slot_mask"], j["kind"]) for j in r["log"])
+    replayed = sorted((j[0], j[2], j[5], j[3], j[4]) for j in rep["log"])
+    print(policy, "jobs", len(live), "events", len(r["events"]), flush=True)
+    assert live == replayed
+    assert [s["plan_skips"] for s in r["models"]] == rep["plan_skips"]
+    if policy == "temporal":
+        assert all(j["slot_mask"] == (1 << 32) - 1 for j in r["log"])
+        starts = sorted((j["start_us"], j["end_us"]) for j in r["log"])
+        assert all(b[0] >= a[1] for a, b in zip(starts, starts[1:]))  # one job at a time
     for m in models:
         m.destroy()
 

@@ -177,3 +177,48 @@ def test_dstack_shares_where_the_comparators_starve():
     models, dense = two_models(20, 900, 20, 500)
     got = compare(models, 100000, 200000, dense, overprov=0)
     assert got["models"][0]["served"] > 0 and got["models"][1]["served"] > 0
+
+
+# ---- temporal sharing (the time-sliced full-GPU baseline) and the replay ----
+
+@pytest.mark.parametrize("scale,cycle", [(1, 0), (8, 0), (8, 7500), (16, 3000), (1, 100000)])
+def test_temporal_four_model_mix_parity(scale, cycle):
+    models, arrivals = four_model_mix(scale)
+    got = ds.simulate(models, 100000, 10_000_000, arrivals, policy="temporal", slice_cycle_us=cycle)
+    ref = sched.simulate(models, 100000, 10_000_000, arrivals, policy="temporal", slice_cycle=cycle)
+    for k in ("models", "utilisation_ppm", "last_end_us", "job_hash"):
+        assert got[k] == ref[k], k
+    assert sum(m["planned_runs"] for m in got["models"]) > 0
+    assert all(m["fod_runs"] == 0 for m in got["models"])
+
+
+def test_temporal_random_parity():
+    rng = random.Random(31)
+    for trial in range(60):
+        n = rng.randint(1, 4)
+        models = []
+        for _ in range(n):
+            tab = {b: {s: max(1, int((150 + 400 * rng.random()) * b ** 0.7 * (32 / s) ** 0.5)) for s in SWEEP}
+                   for b in (1, 2, 4, 8, 16, 32) if rng.random() < 0.8} or {1: {32: 100}}
+            models.append(dict(slo_us=rng.choice([5000, 10000, 15000, 25000, 50000]),
+                               max_batch=rng.choice([4, 8, 16, 32]), rate_per_s=0, table=tab))
+        dur = rng.choice([50000, 300000])
+        arr = [sorted(rng.randrange(dur) for _ in range(rng.randint(0, 400))) for _ in range(n)]
+        cyc = rng.choice([0, 0, 2000, 20000])
+        got = ds.simulate(models, 100000, dur, arr, policy="temporal", slice_cycle_us=cyc)
+        ref = sched.simulate(models, 100000, dur, arr, policy="temporal", slice_cycle=cyc)
+        for k in ("models", "utilisation_ppm", "last_end_us", "job_hash"):
+            assert got[k] == ref[k], (trial, k)
+
+
+@pytest.mark.parametrize("policy,placement", [("dstack", "home"), ("dstack", "lowest"), ("temporal", "lowest")])
+def test_replay_of_own_triggers_reproduces_the_run(policy, placement):
+    """The replay mode (used on a live launcher's trigger log) fed with the
+    virtual-clock run's own triggers starts exactly the same jobs."""
+    models, arrivals = four_model_mix(scale=4)
+    run = sched.simulate(models, 100000, 2_000_000, [a[:len(a) // 5] for a in arrivals], placement=placement,
+                         policy=policy)
+    rep = sched.simulate(models, 100000, 2_000_000, [a[:len(a) // 5] for a in arrivals], placement=placement,
+                         policy=policy, replay_events=run["events"])
+    assert len(run["log"]) > 50
+    assert rep["log"] == run["log"] and rep["job_hash"] == run["job_hash"]

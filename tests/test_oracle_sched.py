@@ -345,3 +345,72 @@ def test_ideal_ties_go_to_the_earliest_deadline():
     assert r["forwards"] == [1, 3] and r["late"] == [0, 0]
     r = sched.simulate_ideal(ms, 100, 10)
     assert r["forwards"] == [1, 4]
+
+
+# ---- temporal sharing (Sec. 6.1's time slices proportional to the SLOs) ----
+
+def _dense(duration, every=10):
+    """A request every `every` us: the queue is never empty."""
+    return list(range(0, duration, every))
+
+
+def test_temporal_one_model_closed_form():
+    """One model owns the whole cycle (C = its SLO = 10 ms).  From the second
+    cycle on, batch 4 (3 ms) runs at 0, 3 and 6 ms into the cycle, then only
+    batch 1 (0.9 ms) fits the 1 ms left, then nothing; the first cycle starts
+    with one request queued (batch 1 at 0, then batch 4 at 0.9, 3.9 and 6.9
+    ms, and the 0.1 ms left fits nothing).  Either way 4 jobs, 13 items and
+    9.9 ms busy per cycle: 99% of the time on all slots."""
+    m = [dict(slo_us=10000, max_batch=4, rate_per_s=0, table={1: {32: 900}, 4: {32: 3000}})]
+    r = sched.simulate(m, 100000, 100000, [_dense(100000)], policy="temporal")
+    starts = [(j[0], j[5]) for j in r["log"]]
+    assert starts[:8] == [(0, 1), (900, 4), (3900, 4), (6900, 4), (10000, 4), (13000, 4), (16000, 4), (19000, 1)]
+    assert r["models"][0]["served"] == 130 and r["models"][0]["planned_runs"] == 40
+    assert r["utilisation_ppm"] == 990000
+
+
+def test_temporal_two_models_hand_worked():
+    """SLOs 10 and 30 ms: cycle 10 ms, slices 2.5 and 7.5 ms.  Model 0 fits
+    batch 2 (1.8 ms) then nothing in its 0.7 ms left (batch 1 takes 1 ms);
+    model 1 fits batch 8 (7 ms).  In the first cycle model 0 starts with one
+    request queued (batch 1 at 0) and then has 1.5 ms left (batch 1 again).
+    Per cycle 2 + 8 items."""
+    m = [dict(slo_us=10000, max_batch=32, rate_per_s=0, table={1: {32: 1000}, 2: {32: 1800}}),
+         dict(slo_us=30000, max_batch=8, rate_per_s=0, table={4: {32: 4000}, 8: {32: 7000}})]
+    r = sched.simulate(m, 100000, 50000, [_dense(50000), _dense(50000)], policy="temporal")
+    assert [(j[0], j[2], j[5]) for j in r["log"][:5]] == [(0, 0, 1), (1000, 0, 1), (2500, 1, 8), (10000, 0, 2),
+                                                          (12500, 1, 8)]
+    assert r["models"][0]["served"] == 10 and r["models"][1]["served"] == 40
+
+
+def test_temporal_slices_are_strict():
+    """A model with nothing queued leaves its slice idle: the other model
+    never runs outside its own slice, even with requests waiting."""
+    m = [dict(slo_us=20000, max_batch=8, rate_per_s=0, table={8: {32: 500}}),
+         dict(slo_us=20000, max_batch=8, rate_per_s=0, table={8: {32: 500}})]
+    r = sched.simulate(m, 100000, 100000, [[], _dense(100000)], policy="temporal")
+    assert all(10000 <= j[0] % 20000 and j[1] % 20000 <= 20000 and j[2] == 1 for j in r["log"])
+    assert r["models"][1]["served"] == 5 * 20 * 8
+
+
+def test_temporal_invariants_random():
+    """One job at a time, on every slot, inside its model's slice."""
+    rng = random.Random(17)
+    for _ in range(40):
+        n = rng.randint(1, 4)
+        models = [dict(slo_us=rng.choice([5000, 10000, 25000, 50000]), max_batch=rng.choice([8, 32]), rate_per_s=0,
+                       table={b: {32: rng.randint(100, 4000) * b // 4 + 50} for b in (1, 4, 8, 32)})
+                  for _ in range(n)]
+        cyc = rng.choice([0, 3000, 20000])
+        C = cyc or min(m["slo_us"] for m in models)
+        tot = sum(m["slo_us"] for m in models)
+        lens = [C * m["slo_us"] // tot for m in models]
+        offs = [sum(lens[:i]) for i in range(n)]
+        arr = [sorted(rng.randrange(200000) for _ in range(rng.randint(0, 300))) for _ in range(n)]
+        r = sched.simulate(models, 100000, 200000, arr, policy="temporal", slice_cycle=cyc)
+        log = sorted(r["log"])
+        for (s0, e0, i, mask, kind, b), nxt in zip(log, log[1:] + [None]):
+            assert mask == (1 << 32) - 1 and kind == 0
+            assert nxt is None or nxt[0] >= e0
+            k = s0 // C
+            assert k * C + offs[i] <= s0 and e0 <= k * C + offs[i] + lens[i]
