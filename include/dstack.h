@@ -170,6 +170,16 @@ dstack_status dstack_generate_params(const char* arch, uint64_t seed, int tensor
  * the first call for that pair. */
 dstack_status dstack_infer(dstack_model m, int batch, const void* d_in, void* d_out, dstack_partition p);
 
+/* Transformer models only (Sec. 4.4's BERT): the forward up to the end of
+ * encoder layer `layer` (0: the embeddings and their layer norm; 1..12: the
+ * output of that encoder layer, after its second layer norm; < 0: the
+ * last), run eagerly on the partition's stream, and that hidden state, bf16
+ * [batch][T][768], copied to the caller's d_hidden.  E_UNSUPPORTED for the
+ * other architectures, E_INVALID for a layer past the last.  Asynchronous;
+ * same workspace rules as dstack_infer. */
+dstack_status dstack_infer_hidden(dstack_model m, int batch, const void* d_in, int layer, void* d_hidden,
+                                  dstack_partition p);
+
 /* Per-kernel timing of one forward: fills up to max_layers entries with
  * the elapsed device time (ms, HIP events around each kernel on the
  * partition's stream), the kernel class (0 MFMA conv/GEMM, 1 depthwise,

@@ -64,6 +64,8 @@ def lib():
         L.oracle_layernorm.argtypes = [dp, ctypes.c_long, i, dp, dp, ctypes.c_double, dp]
         L.oracle_attention.argtypes = [dp, i, i, i, i, dp]
         L.oracle_bert_forward.argtypes = [ctypes.c_void_p, i, ctypes.c_void_p, i, dp]
+        L.oracle_bert_hidden.argtypes = [ctypes.c_void_p, i, ctypes.c_void_p, i, i, dp]
+        L.oracle_bert_layer.argtypes = [ctypes.c_void_p, i, i, dp, i, dp]
         _lib = L
     return _lib
 
@@ -237,6 +239,25 @@ class Model:
         rc = lib().oracle_model_forward(self.h, n, x_bits.ctypes.data, int(parity), _dp(out))
         assert rc == 0
         return out
+
+
+def bert_hidden(model, ids, parity=True, layers=12):
+    """The hidden state [n, T, 768] after encoder layer `layers` (0: the embeddings; 12: the
+    encoder's output) of a BERT model for int32 token ids [n, T]."""
+    ids = np.ascontiguousarray(ids, dtype=np.int32)
+    n, T = ids.shape
+    assert T == BERT_TOKENS[model.arch]
+    out = np.empty((n, T, 768))
+    assert lib().oracle_bert_hidden(model.h, n, ids.ctypes.data, int(parity), layers, _dp(out)) == 0
+    return out
+
+
+def bert_layer(model, layer, x, parity=True):
+    """Encoder layer `layer` (1..12) of a BERT model applied to x [n, T, 768]."""
+    x = _f64(x)
+    out = np.empty_like(x)
+    assert lib().oracle_bert_layer(model.h, x.shape[0], layer, _dp(x), int(parity), _dp(out)) == 0
+    return out
 
 
 def splitmix64(state, n):

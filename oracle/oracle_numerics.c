@@ -798,38 +798,85 @@ static void bert_ln(double* x, long rows, int parity) {
  * residual -> layer norm) -> pooler tanh(W_p h_[CLS] + b_p) -> classifier,
  * out [n][2] fp64.  T is 20 for "bert" and 40 for "bert_long".  Returns 0,
  * or -1 for a model that is not a BERT or an id outside the vocabulary. */
-int oracle_bert_forward(void* h, int n, const int32_t* ids, int parity, double* out) {
-  model_t* m = h;
-  if (!m || (m->arch != ARCH_BERT && m->arch != ARCH_BERT_LONG)) return -1;
-  const int T = m->arch == ARCH_BERT ? 20 : 40;
+/* Encoder layer l (1..12) of n sequences of T tokens, in place on x
+ * [n*T][768]: self-attention + residual -> layer norm, GELU feed-forward +
+ * residual -> layer norm (bf16 storage after each step in parity mode).
+ * Its tensors are 3 + 8 (l - 1) .. + 7 (after the three embedding tables). */
+static void bert_layer(model_t* m, int l, int n, int T, int parity, double* x) {
   const long rows = (long)n * T;
-  for (long i = 0; i < rows; ++i)
-    if (ids[i] < 0 || ids[i] >= BERT_VOCAB) return -1;
-  m->cursor = 0;
-  const double *we = next_tensor(m), *pe = next_tensor(m), *te = next_tensor(m);
-  double* x = malloc(sizeof(double) * (size_t)rows * BERT_H);
+  const tensor_t* t = &m->t[3 + 8 * (l - 1)];
+  const double *wqkv = t[0].v, *bqkv = t[1].v, *wo = t[2].v, *bo = t[3].v;
+  const double *w1 = t[4].v, *b1 = t[5].v, *w2 = t[6].v, *b2 = t[7].v;
+  double* qkv = malloc(sizeof(double) * (size_t)rows * 3 * BERT_H);
+  double* att = malloc(sizeof(double) * (size_t)rows * BERT_H);
+  double* a = malloc(sizeof(double) * (size_t)rows * BERT_H);
+  double* f = malloc(sizeof(double) * (size_t)rows * BERT_FF);
+  bert_linear(x, rows, BERT_H, wqkv, bqkv, 3 * BERT_H, NULL, 0, parity, qkv);
+  oracle_attention(qkv, n, T, BERT_HEADS, BERT_DH, att);
+  round_all(att, rows * BERT_H, parity);
+  bert_linear(att, rows, BERT_H, wo, bo, BERT_H, x, 0, parity, a);
+  bert_ln(a, rows, parity);
+  bert_linear(a, rows, BERT_H, w1, b1, BERT_FF, NULL, 3, parity, f);
+  bert_linear(f, rows, BERT_FF, w2, b2, BERT_H, a, 0, parity, x);
+  bert_ln(x, rows, parity);
+  free(qkv);
+  free(att);
+  free(a);
+  free(f);
+}
+
+/* The encoder up to layer `layers` (0: the embeddings word + position +
+ * type and their layer norm): x [n*T][768] receives that hidden state. */
+static void bert_encode(model_t* m, int n, int T, const int32_t* ids, int parity, int layers, double* x) {
+  const long rows = (long)n * T;
+  const double *we = m->t[0].v, *pe = m->t[1].v, *te = m->t[2].v;
   for (long r = 0; r < rows; ++r) {
     const int t = (int)(r % T);
     for (int c = 0; c < BERT_H; ++c)
       x[r * BERT_H + c] = we[(long)ids[r] * BERT_H + c] + pe[(long)t * BERT_H + c] + te[c];
   }
   bert_ln(x, rows, parity);
-  double* qkv = malloc(sizeof(double) * (size_t)rows * 3 * BERT_H);
-  double* att = malloc(sizeof(double) * (size_t)rows * BERT_H);
-  double* a = malloc(sizeof(double) * (size_t)rows * BERT_H);
-  double* f = malloc(sizeof(double) * (size_t)rows * BERT_FF);
-  for (int l = 0; l < BERT_L; ++l) {
-    const double *wqkv = next_tensor(m), *bqkv = next_tensor(m), *wo = next_tensor(m), *bo = next_tensor(m);
-    const double *w1 = next_tensor(m), *b1 = next_tensor(m), *w2 = next_tensor(m), *b2 = next_tensor(m);
-    bert_linear(x, rows, BERT_H, wqkv, bqkv, 3 * BERT_H, NULL, 0, parity, qkv);
-    oracle_attention(qkv, n, T, BERT_HEADS, BERT_DH, att);
-    round_all(att, rows * BERT_H, parity);
-    bert_linear(att, rows, BERT_H, wo, bo, BERT_H, x, 0, parity, a);
-    bert_ln(a, rows, parity);
-    bert_linear(a, rows, BERT_H, w1, b1, BERT_FF, NULL, 3, parity, f);
-    bert_linear(f, rows, BERT_FF, w2, b2, BERT_H, a, 0, parity, x);
-    bert_ln(x, rows, parity);
-  }
+  for (int l = 1; l <= layers; ++l) bert_layer(m, l, n, T, parity, x);
+}
+
+static int bert_check(model_t* m, int n, const int32_t* ids) {
+  if (!m || (m->arch != ARCH_BERT && m->arch != ARCH_BERT_LONG)) return -1;
+  const long rows = (long)n * (m->arch == ARCH_BERT ? 20 : 40);
+  for (long i = 0; i < rows; ++i)
+    if (ids[i] < 0 || ids[i] >= BERT_VOCAB) return -1;
+  return 0;
+}
+
+/* The hidden state [n][T][768] after encoder layer `layers` (0: the
+ * embeddings; 12: the encoder's output), a test hook beside the classifier
+ * output of oracle_bert_forward.  Returns 0, or -1 as it (or a layer
+ * outside 0..12). */
+int oracle_bert_hidden(void* h, int n, const int32_t* ids, int parity, int layers, double* out) {
+  model_t* m = h;
+  if (bert_check(m, n, ids) || layers < 0 || layers > BERT_L) return -1;
+  bert_encode(m, n, m->arch == ARCH_BERT ? 20 : 40, ids, parity, layers, out);
+  return 0;
+}
+
+/* Encoder layer l (1..12) alone on a given input x_in [n][T][768] (its
+ * values used as they are), into x_out: per-layer parity with the GPU's own
+ * bf16 layer input.  Returns 0 or -1. */
+int oracle_bert_layer(void* h, int n, int l, const double* x_in, int parity, double* x_out) {
+  model_t* m = h;
+  if (!m || (m->arch != ARCH_BERT && m->arch != ARCH_BERT_LONG) || l < 1 || l > BERT_L) return -1;
+  const int T = m->arch == ARCH_BERT ? 20 : 40;
+  memcpy(x_out, x_in, sizeof(double) * (size_t)n * T * BERT_H);
+  bert_layer(m, l, n, T, parity, x_out);
+  return 0;
+}
+
+int oracle_bert_forward(void* h, int n, const int32_t* ids, int parity, double* out) {
+  model_t* m = h;
+  if (bert_check(m, n, ids)) return -1;
+  const int T = m->arch == ARCH_BERT ? 20 : 40;
+  double* x = malloc(sizeof(double) * (size_t)n * T * BERT_H);
+  bert_encode(m, n, T, ids, parity, BERT_L, x);
+  m->cursor = 3 + 8 * BERT_L;
   const double *wp = next_tensor(m), *bp = next_tensor(m), *wc = next_tensor(m), *bc = next_tensor(m);
   double* cls = malloc(sizeof(double) * (size_t)n * BERT_H);
   double* pooled = malloc(sizeof(double) * (size_t)n * BERT_H);
@@ -837,10 +884,6 @@ int oracle_bert_forward(void* h, int n, const int32_t* ids, int parity, double* 
   bert_linear(cls, n, BERT_H, wp, bp, BERT_H, NULL, 4, parity, pooled);
   oracle_fc(pooled, n, BERT_H, wc, bc, BERT_CLASSES, out);
   free(x);
-  free(qkv);
-  free(att);
-  free(a);
-  free(f);
   free(cls);
   free(pooled);
   return 0;

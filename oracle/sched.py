@@ -86,7 +86,12 @@ def knee_search(latency, b: int, candidates, start: int):
     keep the index interval [lo, hi] = [0, n - 1], probe candidates mid and
     mid + 1 (mid = the last candidate <= start first, then the midpoint,
     clamped into [lo, hi - 1]); if eta rises from mid to mid + 1 the knee is
-    above mid, else at or below it.  latency(s) is called once per slot
+    above mid, else at or below it.  On a fine GPU% grid the latency falls
+    in steps (whole rounds of workgroups), so eta can have a local maximum
+    where the bisection stops; the result is then confirmed against its grid
+    neighbours k-2, k-1, k+1, k+2 (in that order): while one of them has a
+    higher eta (or an equal eta with fewer slots) the search moves to the
+    best of them and confirms again.  latency(s) is called once per slot
     count.  Returns (knee slots, probes)."""
     c = list(candidates)
     seen = {}
@@ -108,7 +113,19 @@ def knee_search(latency, b: int, candidates, start: int):
         else:
             hi = mid
         mid = (lo + hi) // 2
-    return c[lo], probes
+    k = lo
+
+    def better(j, i):  # higher eta, or equal eta on fewer slots
+        return eta_gt(b, L(j), c[j], b, L(i), c[i]) or (not eta_gt(b, L(i), c[i], b, L(j), c[j]) and c[j] < c[i])
+
+    while True:
+        best = k
+        for j in (k - 2, k - 1, k + 1, k + 2):
+            if 0 <= j < len(c) and better(j, best):
+                best = j
+        if best == k:
+            return c[k], probes
+        k = best
 
 
 def deployed_slots(knee_s: int, overprov=OVERPROVISION_SLOTS, total=TOTAL_SLOTS) -> int:

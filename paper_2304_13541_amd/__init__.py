@@ -170,6 +170,7 @@ _SIGS = {
     "dstack_model_destroy": ([_vp], None),
     "dstack_generate_params": ([ctypes.c_char_p, _u64, _i, _vp, _sz, ctypes.POINTER(ctypes.c_int64)], _i),
     "dstack_infer": ([_vp, _i, _vp, _vp, _vp], _i),
+    "dstack_infer_hidden": ([_vp, _i, _vp, _i, _vp, _vp], _i),
     "dstack_profile_layers": ([_vp, _i, _vp, _vp, _vp, ctypes.POINTER(LayerTime), _i, ctypes.POINTER(_i)], _i),
     "dstack_kernel_shapes": ([_vp, _i, _vp, _vp, _vp, ctypes.POINTER(KernelShape), _i, ctypes.POINTER(_i)], _i),
     "dstack_knee_model_eval": ([ctypes.POINTER(KneeModel), ctypes.POINTER(_i), _i, ctypes.POINTER(_d),
@@ -337,6 +338,11 @@ class Model:
     def infer(self, batch, x, y, partition):
         """x: bf16 device tensor, y: fp32 device tensor; async on the partition's stream."""
         _check(lib().dstack_infer(self.h, batch, _ptr(x), _ptr(y), partition.h))
+
+    def infer_hidden(self, batch, x, hidden, partition, layer=-1):
+        """Transformer: the hidden state after encoder layer `layer` (0: embeddings; -1: the last)
+        into `hidden` (bf16 [batch, T, 768])."""
+        _check(lib().dstack_infer_hidden(self.h, batch, _ptr(x), int(layer), _ptr(hidden), partition.h))
 
     def profile_layers(self, batch, x, y, partition, max_layers=512):
         arr = (LayerTime * max_layers)()

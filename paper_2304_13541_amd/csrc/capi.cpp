@@ -426,6 +426,40 @@ dstack_status dstack_infer(dstack_model h, int batch, const void* d_in, void* d_
   });
 }
 
+dstack_status dstack_infer_hidden(dstack_model h, int batch, const void* d_in, int layer, void* d_hidden,
+                                  dstack_partition p) {
+  return guarded([&] {
+    DS_CHECK(h && d_in && d_hidden && p, DSTACK_E_INVALID, "infer_hidden: null pointer");
+    Model& m = h->m;
+    DS_CHECK(m.input_tokens, DSTACK_E_UNSUPPORTED, "infer_hidden: only the transformer models have hidden states");
+    dstack_status s = check_batch(m, batch);
+    if (s != DSTACK_OK) return s;
+    // the op that ends each stage: the embedding (+ layer norm), then every
+    // second layer norm (the one closing an encoder layer)
+    std::vector<int> ends;
+    int n_ln = 0;
+    for (size_t i = 0; i < m.ops.size(); ++i) {
+      if (m.ops[i].kind == OP_EMBED_LN) ends.push_back((int)i);
+      if (m.ops[i].kind == OP_LAYERNORM && ++n_ln % 2 == 0) ends.push_back((int)i);
+    }
+    const int n_layers = (int)ends.size() - 1;
+    if (layer < 0) layer = n_layers;
+    DS_CHECK(layer <= n_layers, DSTACK_E_INVALID, "infer_hidden: layer must be in 0.." + std::to_string(n_layers));
+    Workspace* ws;
+    s = get_workspace(m, p->id, p->n_cu, p->stream, &ws);
+    if (s != DSTACK_OK) return s;
+    BusyGuard g(ws->busy);
+    DS_CHECK(g.ok, DSTACK_E_STATE, "infer_hidden: another call on this (model, partition) is in progress");
+    void* hid = nullptr;
+    s = forward(m, batch, d_in, nullptr, *ws, p->n_cu, p->stream, nullptr, ends[layer] + 1, &hid);
+    if (s != DSTACK_OK) return s;
+    const Op& op = m.ops[ends[layer]];
+    const size_t bytes = (size_t)batch * (op.kind == OP_EMBED_LN ? (size_t)op.T * op.C : (size_t)op.H * op.W * op.C) * 2;
+    DS_HIP(hipMemcpyAsync(d_hidden, hid, bytes, hipMemcpyDeviceToDevice, p->stream));
+    return DSTACK_OK;
+  });
+}
+
 dstack_status dstack_profile_layers(dstack_model h, int batch, const void* d_in, void* d_out, dstack_partition p,
                                     dstack_layer_time* out, int max_layers, int* n_layers) {
   return guarded([&] {

@@ -775,7 +775,7 @@ dstack_status lstm_layer_run(const bf16* x, int T, int B, int I, int H, const bf
 }
 
 dstack_status forward(Model& m, int batch, const void* d_in, void* d_out, Workspace& ws, int n_cu, hipStream_t st,
-                      KernelTimer* timer) {
+                      KernelTimer* timer, int n_ops, void** last_out) {
   auto bufp = [&](int id, const void* in, void* out) -> void* {
     if (id == BUF_IN) return const_cast<void*>(in);
     if (id == BUF_OUT) return out;
@@ -783,10 +783,13 @@ dstack_status forward(Model& m, int batch, const void* d_in, void* d_out, Worksp
     return ws.bufs[id];
   };
   const float* f32 = m.d_f32;
-  for (const Op& op : m.ops) {
+  const size_t n_run = n_ops < 0 ? m.ops.size() : std::min(m.ops.size(), (size_t)n_ops);
+  for (size_t oi = 0; oi < n_run; ++oi) {
+    const Op& op = m.ops[oi];
     dstack_status s = DSTACK_OK;
     const bf16* src = (const bf16*)bufp(op.in, d_in, d_out);
     void* dst = bufp(op.out, d_in, d_out);
+    if (last_out) *last_out = dst;
     if (op.kind == OP_LSTM) {
       // layer 1 (reads the model input) -> lstm_h[0]; layer 2 -> lstm_h[1] and d_out
       const bf16* x = op.in == BUF_IN ? (const bf16*)d_in : ws.lstm_h[0];

@@ -134,9 +134,11 @@ dstack_status get_workspace(Model& m, int partition_id, int n_cu, hipStream_t st
 // any and not in use; called when the partition is destroyed.
 void release_workspace(Model& m, int partition_id);
 
-// Enqueue one forward pass on `st`.  `timer` may be null.
+// Enqueue one forward pass on `st`.  `timer` may be null.  n_ops >= 0 runs
+// only the first n_ops ops; last_out (may be null) receives the output
+// buffer of the last op run.
 dstack_status forward(Model& m, int batch, const void* d_in, void* d_out, Workspace& ws, int n_cu, hipStream_t st,
-                      KernelTimer* timer);
+                      KernelTimer* timer, int n_ops = -1, void** last_out = nullptr);
 
 // Algorithmic cost of the ops at a batch size.
 void model_cost(const Model& m, int batch, double* flops, double* mfma_flops, double* weight_bytes, int* n_kernels);

@@ -67,7 +67,21 @@ int knee_search(int b, const std::vector<int>& cand, int start, const std::funct
       hi = mid;
     mid = lo + (hi - lo) / 2;
   }
-  return lo;
+  // confirmation against the grid neighbours k-2, k-1, k+1, k+2: latency
+  // falls in steps, so the bisection can stop on a local maximum of eta
+  auto better = [&](int j, int i) {
+    const int64_t lj = L(j), li = L(i);
+    return eta_greater(b, lj, cand[j], b, li, cand[i]) ||
+           (!eta_greater(b, li, cand[i], b, lj, cand[j]) && cand[j] < cand[i]);
+  };
+  int k = lo;
+  for (;;) {
+    int best = k;
+    for (int j : {k - 2, k - 1, k + 1, k + 2})
+      if (j >= 0 && j < n && better(j, best)) best = j;
+    if (best == k) return k;
+    k = best;
+  }
 }
 
 namespace {

@@ -74,5 +74,11 @@ def test_bert_forward_vs_torch_modules(arch, T):
         ref = F.linear(pooled, t(wc, 2, H), t(bc, 2)).numpy()
     got = m.forward(ids, parity=False)
     assert np.max(np.abs(got - ref)) < 1e-9 * max(1.0, np.max(np.abs(ref)))
+    # the encoder's final hidden states too, and layer by layer the same chain
+    assert oracle.rel_err(oracle.bert_hidden(m, ids, parity=False), x.numpy()) < 1e-9
+    h = oracle.bert_hidden(m, ids, parity=True, layers=0)
+    for l in range(1, L + 1):
+        h = oracle.bert_layer(m, l, h, parity=True)
+    assert np.array_equal(h, oracle.bert_hidden(m, ids, parity=True))
     # parity mode stays within bf16 storage error of the pure result
     assert oracle.rel_err(m.forward(ids, parity=True), ref) < 5e-2
