@@ -656,6 +656,25 @@ dstack_status dstack_op_conv2d_ws(const void* x, int N, int H, int W, int C, con
                                   void* stream);
 dstack_status dstack_conv2d_plan(int N, int H, int W, int C, int K, int R, int S, int stride, int pad, int act,
                                  int out_fp32, int n_cu, size_t workspace_bytes, dstack_conv_plan* out);
+/* conv2d_noalloc: dstack_op_conv2d_ws for callers that cannot allocate
+ *   device memory (code under HIP graph capture, tight serving loops,
+ *   harnesses that forbid hipMalloc).  The split-K slices and arrival
+ *   counters live in a fixed scratch array inside the library, of
+ *   dstack_conv2d_noalloc_scratch_bytes() bytes (32 MiB + 16 KiB) on every
+ *   device the library runs on, held until the process ends; the call
+ *   allocates nothing.  The plan is the one dstack_op_conv2d_ws takes with a
+ *   workspace as large as that plan needs (dstack_conv2d_plan with
+ *   workspace_bytes = SIZE_MAX), so both give the same result; a shape whose
+ *   plan needs more scratch than the array holds returns E_UNSUPPORTED
+ *   before anything is launched.  The first call on a device looks up the
+ *   array's address and clears its counters with a small kernel on
+ *   `stream`; every call leaves them zero.  All calls on one device share
+ *   the array: calls that overlap in time on one device race (serialise
+ *   them, e.g. on one stream).  Other arguments and errors as conv2d_ws. */
+dstack_status dstack_op_conv2d_noalloc(const void* x, int N, int H, int W, int C, const void* w, int K, int R, int S,
+                                       int stride, int pad, const float* scale, const float* shift, const void* res,
+                                       int act, void* y, int out_fp32, int n_cu, void* stream);
+size_t dstack_conv2d_noalloc_scratch_bytes(void);
 dstack_status dstack_arch_convs(const char* arch, int batch, dstack_conv_shape* out, int max_convs, int* n_convs);
 /* conv2d_rgb: the conv2d above for a 3-channel image x [N][H][W][3] read as
  *   it is (the stems of Sec. 3's CNNs; no packing to 8 channels), with

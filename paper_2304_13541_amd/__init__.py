@@ -193,6 +193,9 @@ _SIGS = {
     "dstack_op_conv2d": ([_vp, _i, _i, _i, _i, _vp, _i, _i, _i, _i, _i, _vp, _vp, _vp, _i, _vp, _i, _vp], _i),
     "dstack_op_conv2d_ws": ([_vp, _i, _i, _i, _i, _vp, _i, _i, _i, _i, _i, _vp, _vp, _vp, _i, _vp, _i, _i, _vp, _sz,
                              _vp], _i),
+    "dstack_op_conv2d_noalloc": ([_vp, _i, _i, _i, _i, _vp, _i, _i, _i, _i, _i, _vp, _vp, _vp, _i, _vp, _i, _i, _vp],
+                                 _i),
+    "dstack_conv2d_noalloc_scratch_bytes": ([], _sz),
     "dstack_conv2d_plan": ([_i, _i, _i, _i, _i, _i, _i, _i, _i, _i, _i, _i, _sz, ctypes.POINTER(ConvPlan)], _i),
     "dstack_arch_convs": ([ctypes.c_char_p, _i, ctypes.POINTER(ConvShape), _i, ctypes.POINTER(_i)], _i),
     "dstack_op_conv2d_rgb": ([_vp, _i, _i, _i, _vp, _i, _i, _i, _i, _vp, _vp, _i, _vp, _vp], _i),
@@ -602,6 +605,18 @@ def conv2d_ws(x, w, K, R, S, stride, pad, scale, shift, res, act, y, workspace, 
 
 
 UNLIMITED = ctypes.c_size_t(-1).value
+
+
+def conv2d_noalloc(x, w, K, R, S, stride, pad, scale, shift, res, act, y, out_fp32=False, n_cu=0, stream=None):
+    """conv2d_ws on the library's fixed split-K scratch (allocates nothing)."""
+    N, H, W, C = x.shape
+    _check(lib().dstack_op_conv2d_noalloc(_ptr(x), N, H, W, C, _ptr(w), K, R, S, stride, pad, _ptr(scale),
+                                          _ptr(shift), _ptr(res), act, _ptr(y), int(out_fp32), int(n_cu),
+                                          _stream(stream)))
+
+
+def conv2d_noalloc_scratch_bytes():
+    return lib().dstack_conv2d_noalloc_scratch_bytes()
 
 
 def conv2d_plan(N, H, W, C, K, R, S, stride, pad, act=0, out_fp32=False, n_cu=0, workspace_bytes=UNLIMITED):

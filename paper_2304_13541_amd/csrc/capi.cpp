@@ -895,6 +895,21 @@ dstack_status dstack_op_conv2d_ws(const void* x, int N, int H, int W, int C, con
   });
 }
 
+dstack_status dstack_op_conv2d_noalloc(const void* x, int N, int H, int W, int C, const void* w, int K, int R, int S,
+                                       int stride, int pad, const float* scale, const float* shift, const void* res,
+                                       int act, void* y, int out_fp32, int n_cu, void* stream) {
+  return guarded([&] {
+    DS_CHECK(x && w && y, DSTACK_E_INVALID, "conv2d_noalloc: null pointer");
+    DS_CHECK(act >= 0 && act <= 4, DSTACK_E_INVALID, "conv2d_noalloc: act must be 0..4");
+    const int cus = n_cu > 0 ? n_cu : stream_cu_count((hipStream_t)stream);
+    return launch_conv2d_noalloc(static_cast<const bf16*>(x), N, H, W, C, static_cast<const bf16*>(w), K, R, S,
+                                 stride, pad, scale, shift, static_cast<const bf16*>(res), act, y, out_fp32 != 0, cus,
+                                 (hipStream_t)stream);
+  });
+}
+
+size_t dstack_conv2d_noalloc_scratch_bytes(void) { return CONV_SCRATCH_BYTES; }
+
 dstack_status dstack_arch_convs(const char* arch, int batch, dstack_conv_shape* out, int max_convs, int* n_convs) {
   return guarded([&] {
     DS_CHECK(arch && n_convs && (out || max_convs == 0), DSTACK_E_INVALID, "arch_convs: null pointer");

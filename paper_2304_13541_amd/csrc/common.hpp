@@ -131,6 +131,15 @@ struct ConvLaunchPlan {
 // split_bytes of slice workspace (and arrival counters).
 dstack_status conv2d_plan(int N, int H, int W, int C, int K, int R, int S, int stride, int pad, int act,
                           bool out_fp32, int n_cu, size_t split_bytes, ConvLaunchPlan* out);
+// Fixed split-K scratch of the allocation-free convolution: 16 KiB of
+// arrival counters plus 32 MiB of slices, per device.
+constexpr size_t CONV_SCRATCH_BYTES = SPLITK_TILE_COUNTERS * sizeof(unsigned) + ((size_t)32 << 20);
+// launch_conv2d_ws with the library's fixed scratch in place of a workspace
+// (the plan it would take with an unlimited one; E_UNSUPPORTED if that plan
+// needs more than CONV_SCRATCH_BYTES).  Allocates nothing.
+dstack_status launch_conv2d_noalloc(const bf16* x, int N, int H, int W, int C, const bf16* w, int K, int R, int S,
+                                    int stride, int pad, const float* scale, const float* shift, const bf16* res,
+                                    int act, void* y, bool out_fp32, int n_cu, hipStream_t st);
 
 // ---- kernel launchers (defined in the .hip files) ----
 dstack_status launch_conv2d(const bf16* x, int N, int H, int W, int C, const bf16* w, int K, int R, int S,

@@ -35,6 +35,7 @@
 // applies the epilogue, so no second kernel is launched.
 #include <hip/hip_ext.h>
 
+#include <mutex>
 #include <type_traits>
 
 #include "common.hpp"
@@ -926,6 +927,62 @@ dstack_status launch_conv2d_ws(const bf16* x, int N, int H, int W, int C, const 
     launch_cfg<32, 128, 1, 4>(a, p.mode, out_fp32, p.splits, p.stages, st);
   DS_HIP(hipGetLastError());
   return DSTACK_OK;
+}
+
+// ---- the allocation-free variant: split-K scratch in a file-scope array ----
+//
+// Layout as the caller's workspace of launch_conv2d_ws: the arrival counters
+// first, then the fp32 slices.  Every device the library runs on holds its
+// own copy until the process ends; host code reaches it only through the
+// address hipGetSymbolAddress returns for the current device (the array's
+// name is a host-side stand-in, not a device address).
+static __device__ __align__(256) unsigned char scratch[CONV_SCRATCH_BYTES];
+
+__global__ __launch_bounds__(256) void zero_words_kernel(unsigned* p, int n) {
+  for (int i = blockIdx.x * 256 + threadIdx.x; i < n; i += gridDim.x * 256) p[i] = 0u;
+}
+
+constexpr int kMaxDevices = 64;
+
+// The scratch's device address on the current device, looked up once per
+// device; at that first lookup its counters are cleared with a fill kernel on
+// `st` (no memset node: the call may be under graph capture).
+static dstack_status scratch_address(hipStream_t st, unsigned char** out) {
+  static std::mutex mu;
+  static unsigned char* addr[kMaxDevices] = {};
+  int dev = 0;
+  DS_HIP(hipGetDevice(&dev));
+  DS_CHECK(dev >= 0 && dev < kMaxDevices, DSTACK_E_UNSUPPORTED, "conv2d_noalloc: device index above 63");
+  std::lock_guard<std::mutex> g(mu);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    DS_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    DS_CHECK(p != nullptr && ((uintptr_t)p % 256) == 0, DSTACK_E_HIP, "conv2d_noalloc: no scratch address");
+    launch(zero_words_kernel, dim3(SPLITK_TILE_COUNTERS / 256), dim3(256), 0, st, static_cast<unsigned*>(p),
+           SPLITK_TILE_COUNTERS);
+    DS_HIP(hipGetLastError());
+    addr[dev] = static_cast<unsigned char*>(p);
+  }
+  *out = addr[dev];
+  return DSTACK_OK;
+}
+
+dstack_status launch_conv2d_noalloc(const bf16* x, int N, int H, int W, int C, const bf16* w, int K, int R, int S,
+                                    int stride, int pad, const float* scale, const float* shift, const bf16* res,
+                                    int act, void* y, bool out_fp32, int n_cu, hipStream_t st) {
+  ConvLaunchPlan p;
+  dstack_status s = conv2d_plan(N, H, W, C, K, R, S, stride, pad, act, out_fp32, n_cu, (size_t)1 << 40, &p);
+  if (s != DSTACK_OK) return s;
+  const size_t counters = SPLITK_TILE_COUNTERS * sizeof(unsigned);
+  DS_CHECK(counters + p.split_bytes <= CONV_SCRATCH_BYTES, DSTACK_E_UNSUPPORTED,
+           "conv2d_noalloc: this shape's split-K plan needs " + std::to_string(counters + p.split_bytes) +
+               " bytes of scratch, above the fixed " + std::to_string(CONV_SCRATCH_BYTES));
+  unsigned char* sc = nullptr;
+  s = scratch_address(st, &sc);
+  if (s != DSTACK_OK) return s;
+  return launch_conv2d_ws(x, N, H, W, C, w, K, R, S, stride, pad, scale, shift, res, act, y, out_fp32, n_cu,
+                          reinterpret_cast<float*>(sc + counters), CONV_SCRATCH_BYTES - counters,
+                          reinterpret_cast<unsigned*>(sc), st);
 }
 
 dstack_status launch_conv2d(const bf16* x, int N, int H, int W, int C, const bf16* w, int K, int R, int S,
