@@ -455,7 +455,19 @@ dstack_status dstack_schedule(const dstack_sched_model* models, int n_models, co
  * with queued requests, that model starts a job (kind 0) on all the slots
  * with the largest grid batch (<= max_batch, <= queued) whose table latency
  * at total_slots ends by its slice's end; none fits: it waits.  No plan, no
- * FOD (fod is ignored).  Other values -> E_INVALID. */
+ * FOD (fod is ignored).  Other values -> E_INVALID.
+ *
+ * resize_violations > 0 (policy 0 with placement 1 only, else E_INVALID): a
+ * GPU% change triggered by SLO violations (Sec. 3.5's dynamic GPU resource
+ * reconfiguration; the trigger count is a parameter).  When the requests of
+ * model i that completed late since its last change reach the count, at
+ * the completion that reaches it the model moves to the next larger slot
+ * count of its table's columns that has a latency at its plan batch (none:
+ * it stays, the count restarts), keeping its home offset if the larger range
+ * fits, else ending at the last slot.  From then on its planned jobs and
+ * FOD jobs use that range and the table latency there; a planned start runs
+ * only if its slots are free.  The live launcher moves the model to a new
+ * CU-masked stream at that moment (between its batches). */
 typedef struct {
   int64_t duration_us;
   int fod;
@@ -463,14 +475,16 @@ typedef struct {
   const int64_t* arrivals_us[DSTACK_MAX_MODELS];
   int n_arrivals[DSTACK_MAX_MODELS];
   int policy;                                   /* 0 D-STACK, 1 max-throughput, 2 max-min fair, 3 temporal */
-  int pad;
+  int resize_violations;                        /* 0: off; else late requests that trigger a GPU% change */
   int64_t slice_cycle_us;                       /* policy 3: slice cycle (0: the smallest SLO); >= 0 */
 } dstack_sim_params;
 
 typedef struct {
   int64_t served, violations, unserved, planned_runs, fod_runs, busy_us, p50_us, p99_us;
   int64_t plan_skips;   /* planned starts that did not run (empty queue, model still running,
-                           or -- live launcher only -- its slots still held by an overrunning job) */
+                           or its slots still held: an overrunning job, a GPU% change) */
+  int64_t resizes;      /* GPU% changes on SLO violations */
+  int64_t final_slots;  /* the model's slots at the end (temporal: all) */
 } dstack_model_stats;
 
 typedef struct {

@@ -393,7 +393,8 @@ def _nearest_rank(sorted_vals, pct):
 
 
 def simulate(models, period, duration, arrivals, total=TOTAL_SLOTS, overprov=OVERPROVISION_SLOTS, fod=True,
-             sessions_window=10, placement="lowest", policy="dstack", slice_cycle=0, replay_events=None):
+             sessions_window=10, placement="lowest", policy="dstack", slice_cycle=0, replay_events=None,
+             resize_violations=0):
     """models: as for schedule(); arrivals: per model sorted list of integer us in [0, duration).
     Returns dict with per-model counters, utilisation_ppm and a hash of the job log.
 
@@ -419,6 +420,16 @@ def simulate(models, period, duration, arrivals, total=TOTAL_SLOTS, overprov=OVE
     table latency at all the slots ends by its slice's end (the adaptive
     batch of the slice); none fits: it waits.  No plan, no FOD.
 
+    resize_violations > 0 (D-STACK with home placement): a GPU% change on
+    SLO violations (Sec. 3.5's dynamic reconfiguration, the trigger count a
+    parameter).  Once the late requests of a model's completed jobs since its
+    last change reach the count, at that completion the model moves to the
+    next larger column of its table (over all batches) that has a latency at
+    its plan batch -- none: it stays, the count restarts -- keeping its home
+    offset if the range fits, else ending at the last slot; from then on its
+    planned and FOD jobs use that range and the table latency there.  A
+    planned start runs only if its slots are free.
+
     replay_events: instead of the virtual clock, the triggers a live launcher
     handled, in its order, as dicts (kind, t_us, model, value_us, slot_mask):
     kind 0 a completion seen (the model's job ends), 1 a planned start due
@@ -436,6 +447,12 @@ def simulate(models, period, duration, arrivals, total=TOTAL_SLOTS, overprov=OVE
     planned = [j for j in jobs if not j.missed] if policy == "dstack" else []
     if policy != "dstack":
         fod = True
+    assert resize_violations == 0 or (policy == "dstack" and homes is not None)
+    cur_dep = list(dep)
+    cur_home = list(homes) if homes is not None else [0] * n
+    viol = [0] * n
+    resizes = [0] * n
+    columns = [sorted(set().union(*[set(r) for r in m["table"].values()])) for m in models]
     if policy == "temporal":
         cycle = slice_cycle if slice_cycle > 0 else min(m["slo_us"] for m in models)
         slo_sum = sum(m["slo_us"] for m in models)
@@ -490,7 +507,7 @@ def simulate(models, period, duration, arrivals, total=TOTAL_SLOTS, overprov=OVE
     def start_job(t, i, mask, dur, b, kind):
         nonlocal used, seq, slot_us, h, last_end
         reqs = [queue[i].popleft() for _ in range(b)]
-        running[i] = (t + dur, mask)
+        running[i] = (t + dur, mask, reqs)
         used |= mask
         heapq.heappush(ev, (t + dur, 0, i, seq, reqs))
         seq += 1
@@ -505,6 +522,27 @@ def simulate(models, period, duration, arrivals, total=TOTAL_SLOTS, overprov=OVE
             planned_runs[i] += 1
         else:
             fod_runs[i] += 1
+
+    def current(i, mask, dur):
+        """A planned job of model i as it runs now (its size may have changed)."""
+        if not resizes[i]:
+            return mask, dur
+        return range_mask(cur_home[i], cur_dep[i]), lat(i, choices[i].batch, cur_dep[i])
+
+    def note_late(i, late_n):
+        if policy != "dstack" or resize_violations <= 0:
+            return
+        viol[i] += late_n
+        if viol[i] < resize_violations:
+            return
+        viol[i] = 0
+        nxt = [c for c in columns[i] if cur_dep[i] < c <= total and lat(i, choices[i].batch, c)]
+        if not nxt:
+            return
+        cur_dep[i] = nxt[0]
+        if cur_home[i] + nxt[0] > total:
+            cur_home[i] = total - nxt[0]
+        resizes[i] += 1
 
     def temporal_pass(t):
         if t >= duration or running:
@@ -540,9 +578,9 @@ def simulate(models, period, duration, arrivals, total=TOTAL_SLOTS, overprov=OVE
         else:
             cands.sort(key=lambda i: (sum(runs[i][s] for s in range(cur - sessions_window + 1, cur + 1)), busy[i], i))
         for i in cands:
-            s = dep[i]
+            s = cur_dep[i]
             if homes is not None:  # its own range, all of it free
-                mask = range_mask(homes[i], s)
+                mask = range_mask(cur_home[i], s)
                 if used & mask:
                     continue
             else:  # the lowest-numbered free slots
@@ -554,6 +592,7 @@ def simulate(models, period, duration, arrivals, total=TOTAL_SLOTS, overprov=OVE
                     mask |= 1 << sid
             gap = None
             for (ps, pm, pmask) in planned_starts:
+                pmask = current(pm, pmask, 0)[0]
                 if ps >= t and ((pmask & mask) or pm == i):
                     gap = ps - t
                     break
@@ -571,18 +610,21 @@ def simulate(models, period, duration, arrivals, total=TOTAL_SLOTS, overprov=OVE
             return
 
     if replay_events is not None:
-        plan_dur = {(p * period + j.start, j.model, j.slot_mask): j.duration for p in range(n_periods) for j in planned}
+        plan_dur = {(p * period + j.start, j.model): (j.slot_mask, j.duration) for p in range(n_periods)
+                    for j in planned}
         for e in replay_events:
             t, i = e["t_us"], e["model"]
             if e["kind"] == 0:
-                _, mask = running.pop(i)
+                _, mask, reqs = running.pop(i)
                 used &= ~mask
+                note_late(i, sum(1 for a in reqs if t - a > models[i]["slo_us"]))
                 if fod:
                     fod_pass(t)
             elif e["kind"] == 1 and policy == "temporal":
                 temporal_pass(t)
             elif e["kind"] == 1:
-                mask, dur = e["slot_mask"], plan_dur[(e["value_us"], i, e["slot_mask"])]
+                key = (e["value_us"], i)
+                mask, dur = current(i, *plan_dur[key])
                 if queue[i] and i not in running and not used & mask:
                     start_job(t, i, mask, dur, min(choices[i].batch, len(queue[i])), 0)
                 else:
@@ -591,7 +633,7 @@ def simulate(models, period, duration, arrivals, total=TOTAL_SLOTS, overprov=OVE
                 queue[i].append(e["value_us"])
                 if fod:
                     fod_pass(t)
-        return dict(log=log, plan_skips=plan_skips, job_hash=h)
+        return dict(log=log, plan_skips=plan_skips, job_hash=h, resizes=resizes, final_slots=cur_dep)
 
     events = []  # the triggers in the order handled, in the form replay_events takes
     while ev:
@@ -600,20 +642,23 @@ def simulate(models, period, duration, arrivals, total=TOTAL_SLOTS, overprov=OVE
                            slot_mask=payload[0] if kind == 1 and payload else
                            (range_mask(0, total) if kind == 1 else 0)))
         if kind == 0:
-            end, mask = running.pop(i)
+            end, mask, _ = running.pop(i)
             used &= ~mask
+            job_late = 0
             for a in payload:
                 served[i] += 1
                 lats[i].append(t - a)
                 if t - a > models[i]["slo_us"]:
-                    late[i] += 1
+                    job_late += 1
+            late[i] += job_late
+            note_late(i, job_late)
             if fod:
                 fod_pass(t)
         elif kind == 1 and policy == "temporal":
             temporal_pass(t)
         elif kind == 1:
-            mask, dur = payload
-            if queue[i] and i not in running:
+            mask, dur = current(i, *payload)
+            if queue[i] and i not in running and not used & mask:
                 start_job(t, i, mask, dur, min(choices[i].batch, len(queue[i])), 0)
             else:
                 plan_skips[i] += 1
@@ -626,7 +671,8 @@ def simulate(models, period, duration, arrivals, total=TOTAL_SLOTS, overprov=OVE
         L = sorted(lats[i])
         out.append(dict(served=served[i], violations=late[i] + len(queue[i]), unserved=len(queue[i]),
                         planned_runs=planned_runs[i], fod_runs=fod_runs[i], busy_us=busy[i],
-                        p50_us=_nearest_rank(L, 50), p99_us=_nearest_rank(L, 99), plan_skips=plan_skips[i]))
+                        p50_us=_nearest_rank(L, 50), p99_us=_nearest_rank(L, 99), plan_skips=plan_skips[i],
+                        resizes=resizes[i], final_slots=total if policy == "temporal" else cur_dep[i]))
     return dict(models=out, utilisation_ppm=slot_us * 1000000 // (total * max(duration, 1)), job_hash=h,
                 last_end_us=last_end, log=log, events=events)
 

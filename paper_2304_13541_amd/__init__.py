@@ -104,7 +104,7 @@ class ScheduleOut(ctypes.Structure):
 class SimParams(ctypes.Structure):
     _fields_ = [("duration_us", ctypes.c_int64), ("fod", ctypes.c_int), ("sessions_window", ctypes.c_int),
                 ("arrivals_us", ctypes.POINTER(ctypes.c_int64) * MAX_MODELS), ("n_arrivals", ctypes.c_int * MAX_MODELS),
-                ("policy", ctypes.c_int), ("pad", ctypes.c_int), ("slice_cycle_us", ctypes.c_int64)]
+                ("policy", ctypes.c_int), ("resize_violations", ctypes.c_int), ("slice_cycle_us", ctypes.c_int64)]
 
 
 class ServeEvent(ctypes.Structure):
@@ -125,7 +125,8 @@ class IdealOut(ctypes.Structure):
 
 class ModelStats(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int64) for n in ("served", "violations", "unserved", "planned_runs", "fod_runs",
-                                               "busy_us", "p50_us", "p99_us", "plan_skips")]
+                                               "busy_us", "p50_us", "p99_us", "plan_skips", "resizes",
+                                               "final_slots")]
 
 
 class JobRecord(ctypes.Structure):
@@ -468,7 +469,7 @@ PLACEMENTS = {"lowest": 0, "home": 1}
 POLICIES = {"dstack": 0, "maxthroughput": 1, "maxmin": 2, "temporal": 3}
 
 
-def _sim_params(duration_us, arrivals, fod, sessions_window, policy="dstack", slice_cycle_us=0):
+def _sim_params(duration_us, arrivals, fod, sessions_window, policy="dstack", slice_cycle_us=0, resize_violations=0):
     """SimParams plus the arrival buffers it points into (keep them alive)."""
     sp = SimParams()
     sp.duration_us = duration_us
@@ -476,6 +477,7 @@ def _sim_params(duration_us, arrivals, fod, sessions_window, policy="dstack", sl
     sp.sessions_window = sessions_window
     sp.policy = POLICIES[policy]
     sp.slice_cycle_us = slice_cycle_us
+    sp.resize_violations = resize_violations
     keep = []
     for i, a in enumerate(arrivals):
         buf = (ctypes.c_int64 * max(1, len(a)))(*a)
@@ -486,12 +488,12 @@ def _sim_params(duration_us, arrivals, fod, sessions_window, policy="dstack", sl
 
 
 def simulate(models, period_us, duration_us, arrivals, total_slots=TOTAL_SLOTS, overprov_slots=2, fod=True,
-             sessions_window=10, placement="lowest", policy="dstack", slice_cycle_us=0):
+             sessions_window=10, placement="lowest", policy="dstack", slice_cycle_us=0, resize_violations=0):
     """Launcher simulation on the timing table (see dstack_simulate); policy
     "dstack", "maxthroughput", "maxmin" or "temporal".  arrivals: per model
     sorted integer-us arrival times.  Returns a dict."""
     arr = _sched_models(models)
-    sp, keep = _sim_params(duration_us, arrivals, fod, sessions_window, policy, slice_cycle_us)
+    sp, keep = _sim_params(duration_us, arrivals, fod, sessions_window, policy, slice_cycle_us, resize_violations)
     out = RunOut()
     prm = SchedParams(period_us, total_slots, overprov_slots, PLACEMENTS[placement])
     _check(lib().dstack_simulate(arr, len(models), ctypes.byref(prm), ctypes.byref(sp), ctypes.byref(out)))
@@ -519,7 +521,7 @@ def simulate_ideal(models, horizon_us, slot_us, total_slots=TOTAL_SLOTS):
 
 def serve(handles, tables, inputs, outputs, period_us, duration_us, arrivals, total_slots=TOTAL_SLOTS,
           overprov_slots=2, fod=True, sessions_window=10, log_capacity=1 << 16, policy="dstack", slice_cycle_us=0,
-          event_capacity=0):
+          event_capacity=0, resize_violations=0):
     """Live launcher (see dstack_serve): handles are Model objects, tables the
     timing tables in the form simulate() takes, inputs/outputs device tensors
     sized for each model's max batch; policy "dstack" or "temporal".  Blocks
@@ -527,7 +529,7 @@ def serve(handles, tables, inputs, outputs, period_us, duration_us, arrivals, to
     launcher's triggers ("events") for a replay."""
     n = len(handles)
     arr = _sched_models(tables)
-    sp, keep = _sim_params(duration_us, arrivals, fod, sessions_window, policy, slice_cycle_us)
+    sp, keep = _sim_params(duration_us, arrivals, fod, sessions_window, policy, slice_cycle_us, resize_violations)
     hv = (_vp * n)(*[m.h.value for m in handles])
     iv = (_vp * n)(*[t.data_ptr() for t in inputs])
     ov = (_vp * n)(*[t.data_ptr() for t in outputs])

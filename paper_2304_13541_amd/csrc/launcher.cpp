@@ -72,7 +72,7 @@ int64_t nearest_rank(std::vector<int64_t>& v, int pct) {
 
 bool check_trace(int n, const dstack_sim_params* sim) {
   if (sim->duration_us <= 0 || sim->sessions_window < 1 || sim->policy < 0 || sim->policy > 3 ||
-      sim->slice_cycle_us < 0)
+      sim->slice_cycle_us < 0 || sim->resize_violations < 0)
     return false;
   for (int i = 0; i < n; ++i) {
     if (sim->n_arrivals[i] < 0 || (sim->n_arrivals[i] > 0 && !sim->arrivals_us[i])) return false;
@@ -87,7 +87,12 @@ bool check_trace(int n, const dstack_sim_params* sim) {
 LaunchState::LaunchState(const dstack_sched_model* models, int n, const dstack_sched_params* prm,
                          const dstack_sim_params* sim, const dstack_schedule_out* plan)
     : models_(models), n_(n), prm_(prm), sim_(sim), plan_(plan), T_(prm->period_us), D_(sim->duration_us),
-      queue_(n), running_(n, 0), run_mask_(n, 0), runs_(n), busy_(n, 0) {
+      queue_(n), running_(n, 0), run_mask_(n, 0), runs_(n), busy_(n, 0), dep_(n), home_(n), viol_(n, 0),
+      resizes_(n, 0) {
+  for (int i = 0; i < n; ++i) {
+    dep_[i] = plan->deployed_slots[i];
+    home_[i] = prm->placement == 1 ? plan->home_offset[i] : 0;
+  }
   const int64_t n_periods = sim->policy == 0 ? (D_ + T_ - 1) / T_ : 0;  // the comparators run no plan
   for (int64_t p = 0; p < n_periods; ++p)
     for (int j = 0; j < plan->n_jobs; ++j) {
@@ -119,6 +124,30 @@ LaunchState::LaunchState(const dstack_sched_model* models, int n, const dstack_s
         if (slice_len_[i] > 0 && t < D_) slices_.push_back(PlannedStart{t, i, all, 0});
       }
   }
+}
+
+bool LaunchState::note_late(int64_t t, int i, int64_t late) {
+  (void)t;
+  if (sim_->policy != 0 || sim_->resize_violations <= 0) return false;
+  viol_[i] += late;
+  if (viol_[i] < sim_->resize_violations) return false;
+  viol_[i] = 0;
+  const dstack_sched_model& m = models_[i];
+  int next = -1;
+  for (int q = 0; q < m.n_slots && next < 0; ++q)
+    if (m.slots[q] > dep_[i] && m.slots[q] <= prm_->total_slots && table_latency(i, plan_->batch[i], m.slots[q]) > 0)
+      next = m.slots[q];
+  if (next < 0) return false;  // already at its largest swept share
+  dep_[i] = next;
+  if (home_[i] + next > prm_->total_slots) home_[i] = prm_->total_slots - next;
+  resizes_[i] += 1;
+  return true;
+}
+
+PlannedStart LaunchState::current(const PlannedStart& ps) const {
+  if (resizes_[ps.model] == 0) return ps;
+  return PlannedStart{ps.t, ps.model, range_mask(home_[ps.model], dep_[ps.model]),
+                      table_latency(ps.model, plan_->batch[ps.model], dep_[ps.model])};
 }
 
 bool LaunchState::temporal_pick(int64_t t, Pick* out) const {
@@ -187,10 +216,10 @@ bool LaunchState::fod_pick(int64_t t, Pick* out) const {
   });
   const int total = prm_->total_slots;
   for (int i : cands) {
-    const int s = plan_->deployed_slots[i];
+    const int s = dep_[i];
     uint64_t mask = 0;
     if (prm_->placement == 1) {
-      mask = range_mask(plan_->home_offset[i], s);
+      mask = range_mask(home_[i], s);
       if (used_ & mask) continue;
     } else {
       int got = 0;
@@ -205,11 +234,13 @@ bool LaunchState::fod_pick(int64_t t, Pick* out) const {
     // instant counts (same-instant planned starts are processed after
     // completions)
     int64_t gap = -1;
-    for (const PlannedStart& ps : pstarts_)
+    for (const PlannedStart& p0 : pstarts_) {
+      const PlannedStart ps = current(p0);
       if (ps.t >= t && ((ps.mask & mask) || ps.model == i)) {
         gap = ps.t - t;
         break;
       }
+    }
     int bb = -1;
     int64_t bL = 0;
     for (int b : kGrid) {
@@ -250,7 +281,9 @@ dstack_status simulate(const dstack_sched_model* models, int n, const dstack_sch
   DS_CHECK(sim && out && prm, DSTACK_E_INVALID, "simulate: null pointer");
   DS_CHECK(n >= 1 && n <= DSTACK_MAX_MODELS, DSTACK_E_INVALID, "simulate: bad model count");
   DS_CHECK(check_trace(n, sim), DSTACK_E_INVALID,
-           "simulate: bad trace (duration > 0, window >= 1, policy 0..2, arrivals sorted inside [0, duration))");
+           "simulate: bad trace (duration > 0, window >= 1, policy 0..3, arrivals sorted inside [0, duration))");
+  DS_CHECK(sim->resize_violations == 0 || (sim->policy == 0 && prm->placement == 1), DSTACK_E_INVALID,
+           "simulate: GPU% changes on SLO violations need the D-STACK policy with home placement");
   std::vector<dstack_schedule_out> plan_box(1);
   dstack_schedule_out* plan = &plan_box[0];
   dstack_status st = schedule(models, n, prm, plan);
@@ -295,17 +328,22 @@ dstack_status simulate(const dstack_sched_model* models, int n, const dstack_sch
     const int i = e.model;
     if (e.kind == 0) {
       ls.finish(i);
+      int64_t job_late = 0;
       for (int64_t a : e.reqs) {
         served[i] += 1;
         lats[i].push_back(e.t - a);
-        if (e.t - a > models[i].slo_us) late[i] += 1;
+        if (e.t - a > models[i].slo_us) job_late += 1;
       }
+      late[i] += job_late;
+      ls.note_late(e.t, i, job_late);
       fod_pass(e.t);
     } else if (e.kind == 1 && ls.temporal()) {
       fod_pass(e.t);
     } else if (e.kind == 1) {
-      if (ls.queued(i) && !ls.running(i))
-        launch(e.t, i, e.mask, e.dur, std::min<int>(ls.plan_batch(i), (int)ls.queued(i)), 0);
+      // a planned start (its model may have changed size since the plan)
+      const PlannedStart ps = ls.current(PlannedStart{e.t, i, e.mask, e.dur});
+      if (ls.queued(i) && !ls.running(i) && ls.free(ps.mask))
+        launch(e.t, i, ps.mask, ps.dur, std::min<int>(ls.plan_batch(i), (int)ls.queued(i)), 0);
       else
         skips[i] += 1;
     } else {
@@ -327,6 +365,8 @@ dstack_status simulate(const dstack_sched_model* models, int n, const dstack_sch
     s.p50_us = nearest_rank(lats[i], 50);
     s.p99_us = nearest_rank(lats[i], 99);
     s.plan_skips = skips[i];
+    s.resizes = ls.resizes(i);
+    s.final_slots = ls.temporal() ? total : ls.deployed(i);
   }
   out->utilisation_ppm = (int64_t)((unsigned __int128)slot_us * 1000000 / ((unsigned __int128)total * (uint64_t)D));
   out->job_hash = h;

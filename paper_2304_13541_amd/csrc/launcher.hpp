@@ -43,6 +43,16 @@ class LaunchState {
   };
   // the FOD choice at time t (false: nothing fits)
   bool fod_pick(int64_t t, Pick* out) const;
+  // GPU% change on SLO violations (resize_violations > 0, D-STACK with home
+  // placement): a job of model i ended at t with `late` requests past their
+  // SLO; once its late count since its last change reaches the threshold the
+  // model moves to the next larger swept slot count (true returned).  Its
+  // current size, home offset and the planned job as it now runs:
+  bool note_late(int64_t t, int i, int64_t late);
+  int deployed(int i) const { return dep_[i]; }
+  int home(int i) const { return home_[i]; }
+  int64_t resizes(int i) const { return resizes_[i]; }
+  PlannedStart current(const PlannedStart& ps) const;
   // temporal policy: the slice starts in time order, and the job its slice
   // owner starts at time t on the whole GPU (false: none)
   const std::vector<PlannedStart>& slice_starts() const { return slices_; }
@@ -74,6 +84,8 @@ class LaunchState {
   uint64_t used_ = 0;
   std::vector<std::map<int64_t, int64_t>> runs_;  // session -> runs started
   std::vector<int64_t> busy_;
+  std::vector<int> dep_, home_;                 // current deployed slots and home offset
+  std::vector<int64_t> viol_, resizes_;         // late requests since the last change, changes
 };
 
 // nearest-rank percentile (sorts v)

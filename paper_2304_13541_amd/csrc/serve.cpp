@@ -72,6 +72,8 @@ dstack_status serve(const dstack_model* models, int n, const void* const* d_in, 
            "serve: runs the D-STACK policy (0) or temporal sharing (3)");
   const bool temporal = sim->policy == 3;
   DS_CHECK(temporal || prm->placement == 1, DSTACK_E_INVALID, "serve: D-STACK needs placement 1 (home ranges)");
+  DS_CHECK(!temporal || sim->resize_violations == 0, DSTACK_E_INVALID,
+           "serve: GPU% changes on SLO violations are a D-STACK feature (policy 0)");
   DS_CHECK(prm->total_slots >= 1 && prm->total_slots <= DSTACK_TOTAL_SLOTS, DSTACK_E_INVALID,
            "serve: total_slots must be in 1..32 (one GPU)");
   for (int i = 0; i < n; ++i) {
@@ -205,11 +207,13 @@ dstack_status serve(const dstack_model* models, int n, const void* const* d_in, 
       Running& r = run[i];
       r.on = false;
       ls.finish(i);
+      int64_t job_late = 0;
       for (int64_t a : r.reqs) {
         served[i] += 1;
         lats[i].push_back(te - a);
-        if (te - a > tables[i].slo_us) late[i] += 1;
+        if (te - a > tables[i].slo_us) job_late += 1;
       }
+      late[i] += job_late;
       busy[i] += gpu_us;
       slot_us += (int64_t)__builtin_popcountll(r.mask) * std::max<int64_t>(0, std::min(r.start + gpu_us, D) - r.start);
       last_end = std::max(last_end, te);
@@ -217,12 +221,28 @@ dstack_status serve(const dstack_model* models, int n, const void* const* d_in, 
         log[jobs] = dstack_job_record{r.start, te, gpu_us, r.table_us, i, r.batch, r.kind, r.mask};
       ++jobs;
       note(te, 0, i, 0, 0);
+      if (ls.note_late(te, i, job_late)) {
+        // GPU% change between batches: the model's next jobs run on a new
+        // CU-masked stream over its larger range (the old one is destroyed
+        // first; weights are shared, its workspace and graphs are rebuilt
+        // at its first job there)
+        dstack_partition np = nullptr;
+        dstack_partition_destroy(res.part[i]);
+        res.part[i] = nullptr;
+        st = dstack_partition_create_at(ls.home(i), ls.deployed(i), &np);
+        if (st != DSTACK_OK) return st;
+        void* sp = nullptr;
+        st = dstack_partition_query(np, nullptr, nullptr, &sp);
+        if (st != DSTACK_OK) return st;
+        res.part[i] = part[i] = np;
+        stream[i] = (hipStream_t)sp;
+      }
       st = fod_pass(te);
       if (st != DSTACK_OK) return st;
     }
     // planned starts (temporal: slice starts) that are due
     while (next_plan < P.size() && P[next_plan].t <= t) {
-      const PlannedStart& ps = P[next_plan++];
+      const PlannedStart ps = ls.current(P[next_plan++]);
       const int i = ps.model;
       const int64_t tn = clock();
       note(tn, 1, i, ps.t, ps.mask);
@@ -278,6 +298,8 @@ dstack_status serve(const dstack_model* models, int n, const void* const* d_in, 
     s.p50_us = nearest_rank(lats[i], 50);
     s.p99_us = nearest_rank(lats[i], 99);
     s.plan_skips = skips[i];
+    s.resizes = ls.resizes(i);
+    s.final_slots = temporal ? total : ls.deployed(i);
   }
   out->utilisation_ppm = (int64_t)((unsigned __int128)slot_us * 1000000 / ((unsigned __int128)total * (uint64_t)D));
   out->job_hash = h;

@@ -138,3 +138,37 @@ def test_serve_rejects_bad_arguments(env):
         ds.serve([m], [dict(tab, max_batch=10_000)], [x], [y], 10_000, 50_000, [[]])
     assert e.value.status == ds.E_INVALID
     m.destroy()
+
+
+def test_serve_resizes_on_violations_and_replays(env):
+    """GPU% change on SLO violations in the live launcher: a tight SLO for
+    MobileNetV2 under load makes its requests late; every 3 late ones it
+    moves to a larger home range on a new CU-masked stream.  The trigger log
+    replayed through the oracle (which applies the same rule to the logged
+    completion times) starts exactly the same jobs, and the model's job
+    ranges only grow."""
+    ds, sched, poisson_arrivals, torch = env
+    models = [ds.Model("tinycnn", 27), ds.Model("mobilenetv2", 28)]
+    tables = [dict(slo_us=4000, max_batch=4, rate_per_s=0, table=measured_table(ds, models[0], [1, 2, 4])),
+              dict(slo_us=1500, max_batch=8, rate_per_s=0, table=measured_table(ds, models[1], [1, 2, 4, 8]))]
+    duration = 300_000
+    arrivals = [poisson_arrivals(31, 1500, duration), poisson_arrivals(32, 30000, duration)]
+    xs = [torch.zeros(m.input_shape(t["max_batch"]), device="cuda", dtype=torch.bfloat16) for m, t in zip(models, tables)]
+    ys = [torch.zeros(m.output_shape(t["max_batch"]), device="cuda", dtype=torch.float32) for m, t in zip(models, tables)]
+    r = ds.serve(models, tables, xs, ys, period_us=10_000, duration_us=duration, arrivals=arrivals, overprov_slots=0,
+                 event_capacity=1 << 16, resize_violations=3)
+    torch.cuda.synchronize()
+    rep = sched.simulate(tables, 10_000, duration, arrivals, overprov=0, placement="home",
+                         replay_events=r["events"], resize_violations=3)
+    live = sorted((j["start_us"], j["model"], j["batch"], j["slot_mask"], j["kind"]) for j in r["log"])
+    replayed = sorted((j[0], j[2], j[5], j[3], j[4]) for j in rep["log"])
+    print("resizes", [s["resizes"] for s in r["models"]], "final slots", [s["final_slots"] for s in r["models"]],
+          "jobs", len(live), flush=True)
+    assert live == replayed
+    assert [s["resizes"] for s in r["models"]] == rep["resizes"]
+    assert [s["final_slots"] for s in r["models"]] == rep["final_slots"]
+    assert r["models"][1]["resizes"] > 0
+    sizes = [bin(j[3]).count("1") for j in live if j[1] == 1]
+    assert sizes == sorted(sizes) and sizes[-1] > sizes[0]
+    for m in models:
+        m.destroy()

@@ -222,3 +222,27 @@ def test_replay_of_own_triggers_reproduces_the_run(policy, placement):
                          policy=policy, replay_events=run["events"])
     assert len(run["log"]) > 50
     assert rep["log"] == run["log"] and rep["job_hash"] == run["job_hash"]
+
+
+@pytest.mark.parametrize("scale,trigger", [(8, 5), (16, 5), (16, 1)])
+def test_resize_on_violations_parity(scale, trigger):
+    """GPU% changes on SLO violations: library and oracle bit-exact on the
+    four-model mix under heavy load (every counter, the final sizes and the
+    job hash)."""
+    models, arrivals = four_model_mix(scale)
+    kw = dict(overprov_slots=0, placement="home")
+    arr = [[t for t in a if t < 3_000_000] for a in arrivals]
+    got = ds.simulate(models, 100000, 3_000_000, arr, resize_violations=trigger, **kw)
+    ref = sched.simulate(models, 100000, 3_000_000, arr, overprov=0, placement="home", resize_violations=trigger)
+    for k in ("models", "utilisation_ppm", "last_end_us", "job_hash"):
+        assert got[k] == ref[k], k
+    assert sum(m["resizes"] for m in got["models"]) > 0
+
+
+def test_resize_needs_dstack_with_home_ranges():
+    models, arrivals = four_model_mix()
+    with pytest.raises(ds.DStackError):
+        ds.simulate(models, 100000, 100000, [[] for _ in arrivals], placement="lowest", resize_violations=3)
+    with pytest.raises(ds.DStackError):
+        ds.simulate(models, 100000, 100000, [[] for _ in arrivals], placement="home", policy="temporal",
+                    resize_violations=3)

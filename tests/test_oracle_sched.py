@@ -429,3 +429,57 @@ def test_temporal_invariants_random():
             assert nxt is None or nxt[0] >= e0
             k = s0 // C
             assert k * C + offs[i] <= s0 and e0 <= k * C + offs[i] + lens[i]
+
+
+# ---- GPU% change on SLO violations (Sec. 3.5's dynamic reconfiguration) ----
+
+def test_resize_on_violations_hand_worked():
+    """One model at batch 1 whose optimum share (2 slots, 2 ms a request) is
+    slower than its arrivals (one every 1.5 ms): requests turn late, and every
+    3 late completions it moves up its table's columns, 2 -> 4 -> 8 slots,
+    where 1 ms a request keeps up.  Before the first change every job runs on
+    slots 0-1, between the changes on 0-3, after them on 0-7."""
+    table = {1: {2: 2000, 4: 1800, 8: 1000}}
+    m = [dict(slo_us=5000, max_batch=1, rate_per_s=0, table=table)]
+    _, plan = sched.schedule(m, 100000, overprov=0, placement="home")[:2]
+    assert sched.schedule(m, 100000, overprov=0, placement="home")[0][0].slots == 2
+    arr = list(range(0, 300000, 1500))
+    r = sched.simulate(m, 100000, 300000, [arr], overprov=0, placement="home", resize_violations=3)
+    st = r["models"][0]
+    assert st["resizes"] == 2 and st["final_slots"] == 8
+    sizes = [bin(j[3]).count("1") for j in r["log"]]
+    assert sizes == sorted(sizes) and sizes[0] == 2 and sizes[-1] == 8 and 4 in sizes
+    assert all(j[3] == (1 << bin(j[3]).count("1")) - 1 for j in r["log"])  # home offset 0 kept
+    # without the trigger it stays on 2 slots and falls behind
+    r0 = sched.simulate(m, 100000, 300000, [arr], overprov=0, placement="home")
+    assert r0["models"][0]["resizes"] == 0 and r0["models"][0]["violations"] > st["violations"]
+
+
+def test_resize_keeps_ranges_inside_the_gpu_and_disjoint():
+    """Random four-model tables under load: a model's size only grows, along
+    its table's columns; its range stays inside the slots (a range that
+    would pass the last slot ends there); running jobs never share a slot."""
+    rng = random.Random(23)
+    for trial in range(20):
+        n = 4
+        models = []
+        for _ in range(n):
+            cols = sorted(rng.sample(GRID, 6))
+            models.append(dict(slo_us=rng.choice([10000, 20000, 40000]), max_batch=8, rate_per_s=0,
+                               table={b: {s: int((300 + 2000 * rng.random()) * b ** 0.6 * (32 / s) ** 0.6)
+                                          for s in cols} for b in (1, 2, 4, 8)}))
+        arr = [sorted(rng.randrange(400000) for _ in range(rng.randint(100, 900))) for _ in range(n)]
+        r = sched.simulate(models, 100000, 400000, arr, overprov=0, placement="home", resize_violations=2)
+        log = sorted(r["log"])
+        for i in range(n):
+            sizes = [bin(j[3]).count("1") for j in log if j[2] == i]
+            assert sizes == sorted(sizes)
+            cols = set().union(*[set(row) for row in models[i]["table"].values()])
+            assert all(s in cols for s in set(sizes[1:]) - {sizes[0]})
+            assert r["models"][i]["final_slots"] == (sizes[-1] if sizes else r["models"][i]["final_slots"])
+        for a in range(len(log)):
+            for b in range(a + 1, len(log)):
+                if log[b][0] >= log[a][1]:
+                    break
+                assert log[a][3] & log[b][3] == 0
+        assert all(m < (1 << 32) for *_, m, _, _ in [(j[0], j[1], j[2], j[3], j[4], j[5]) for j in log])
