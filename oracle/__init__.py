@@ -20,12 +20,26 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "oracle_numerics.c")
-_LIB = os.path.join(_HERE, "liboracle.so")
+# ORACLE_LIBRARY may name the CPU sanitizer build (liboracle_san.so, see build()).
+_LIB = os.environ.get("ORACLE_LIBRARY") or os.path.join(_HERE, "liboracle.so")
+_SAN_LIB = os.path.join(_HERE, "liboracle_san.so")
 _lib = None
 
 
-def build(force=False):
-    """Compile the fp64 numerics with gcc (no GPU involved)."""
+def build(force=False, sanitize=False):
+    """Compile the fp64 numerics with gcc (no GPU involved).  sanitize=True
+    builds liboracle_san.so with clang's AddressSanitizer and
+    UndefinedBehaviorSanitizer instead (the runtime the library's sanitizer
+    build uses, so both load into one process)."""
+    if sanitize:
+        tmp = _SAN_LIB + ".tmp%d" % os.getpid()
+        subprocess.check_call(["/opt/rocm/llvm/bin/clang", "-O1", "-g", "-fopenmp", "-ffp-contract=off", "-shared",
+                               "-fPIC", "-fsanitize=address,undefined", "-fno-sanitize-recover=undefined",
+                               "-fno-omit-frame-pointer", "-shared-libasan", "-o", tmp, _SRC, "-lm"])
+        os.replace(tmp, _SAN_LIB)
+        return _SAN_LIB
+    if os.environ.get("ORACLE_LIBRARY"):  # a prebuilt variant was named: use it as it is
+        return _LIB
     if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
         tmp = _LIB + ".tmp%d" % os.getpid()
         subprocess.check_call(["gcc", "-O2", "-fopenmp", "-ffp-contract=off", "-shared", "-fPIC",

@@ -11,7 +11,9 @@ import os
 import numpy as np
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libdstack.so")
+# DSTACK_LIBRARY may name another build of the same sources (the CPU
+# sanitizer build libdstack_san.so); the default is the in-tree library.
+LIB_PATH = os.environ.get("DSTACK_LIBRARY") or os.path.join(HERE, "libdstack.so")
 
 OK, E_INVALID, E_UNSUPPORTED, E_HIP, E_OOM, E_INFEASIBLE, E_STATE = 0, -1, -2, -3, -4, -5, -6
 TOTAL_SLOTS = 32
