@@ -76,6 +76,10 @@ DSTACK_OVERPROV = [0, 2]          # D-STACK: over-provision (slots) tried (the b
 # config 3: ResNet-50 (SLO 25 ms) + MobileNetV2 (SLO 15 ms); indices into MIX4
 PAIR = [(0, 25000, 16), (1, 15000, 32)]
 
+# probe-kernel markers (grid of n x 64 threads) that let a kernel trace or a
+# counter run attribute the dispatches of the roofline forwards to their model
+MIX_MARKER, CAL_MARKER, END_MARKER = 1100, 1199, 999
+
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "conv_igemm_mix_traffic.md")
 CONV_SRC = os.path.join(ROOT, "paper_2304_13541_amd", "csrc", "conv_igemm.hip")
 
@@ -95,7 +99,15 @@ def parse():
     p.add_argument("--steps3", type=int, default=20, help="steps of the config-3 closed-loop pair")
     p.add_argument("--steps4", type=int, default=40, help="steps of the VGG-19 + LSTM pair")
     p.add_argument("--headline-only", action="store_true", help="skip everything but the four-model mix")
+    p.add_argument("--at-k", type=float, default=None,
+                   help="serve at this rate scale instead of searching the capacity (with --at-overprov)")
+    p.add_argument("--at-overprov", type=int, default=0)
     return p.parse_args()
+
+
+def note(msg):
+    """A progress line on stderr (the JSON result is the only stdout line)."""
+    print("bench: " + msg, file=sys.stderr, flush=True)
 
 
 def sweep_tables(models, specs, args):
@@ -107,23 +119,25 @@ def sweep_tables(models, specs, args):
             r = m.knee_sweep(b, FRACTIONS, warmup=args.sweep_warmup, reps=args.sweep_reps)
             tab[b] = dict(zip(r["slots"], r["latency_us"]))
         tables.append(tab)
+        note("timing table of %s done" % spec[0])
     return tables
 
 
 def measured_traffic():
-    """HBM bytes per conv launch from the committed FETCH_SIZE/WRITE_SIZE
-    summary, or None when the kernel source changed since it was taken."""
+    """(HBM bytes per conv launch, operating point they were counted at) from
+    the committed FETCH_SIZE/WRITE_SIZE summary; (None, None) when the kernel
+    source changed since it was taken."""
     if not os.path.exists(TRAFFIC_FILE):
-        return None
+        return None, None
     vals = {}
     for line in open(TRAFFIC_FILE):
-        if ":" in line and line.split(":")[0].strip() in ("source_sha256", "traffic_bytes_per_launch"):
+        if ":" in line and line.split(":")[0].strip() in ("source_sha256", "traffic_bytes_per_launch", "plan"):
             k, v = line.split(":", 1)
             vals[k.strip()] = v.strip().strip("`")
     sha = hashlib.sha256(open(CONV_SRC, "rb").read()).hexdigest()
     if vals.get("source_sha256") != sha or "traffic_bytes_per_launch" not in vals:
-        return None
-    return float(vals["traffic_bytes_per_launch"])
+        return None, None
+    return float(vals["traffic_bytes_per_launch"]), json.loads(vals["plan"]) if "plan" in vals else None
 
 
 def cpu_baseline(budget_s, sched_in):
@@ -609,7 +623,9 @@ def mix_rooflines(ds, torch, mix, k, overprov):
         for _ in range(2):
             m.infer(b, mix.xs[i], mix.ys[i], p)
         p.synchronize()
+        p.probe_cu_ids(MIX_MARKER + i)
         recs, by_kind = layer_stats(ds, m, b, mix.xs[i], mix.ys[i], p)
+        p.probe_cu_ids(END_MARKER)
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         sp = p.torch_stream()
         e0.record(sp)
@@ -805,15 +821,22 @@ def main():
 
     # ---- capacity at <= 1% violations: D-STACK and temporal sharing, same traces ----
     t_cap = time.perf_counter()
-    dstack = []
-    for ov in DSTACK_OVERPROV:
-        k_d, probes_d = mix.capacity("dstack", ov, args.probe_seconds)
-        dstack.append(dict(overprov_slots=ov, k=k_d, capacity_req_s=k_d * mix.rate, probes=probes_d))
+    dstack, temporal = [], []
+    if args.at_k is not None:  # a given operating point (profiling runs): no search
+        dstack.append(dict(overprov_slots=args.at_overprov, k=args.at_k, capacity_req_s=args.at_k * mix.rate,
+                           probes=[], given=True))
+        temporal.append(dict(cycle_us=TEMPORAL_CYCLES[0], k=args.at_k, capacity_req_s=args.at_k * mix.rate,
+                             probes=[], given=True))
+    else:
+        for ov in DSTACK_OVERPROV:
+            k_d, probes_d = mix.capacity("dstack", ov, args.probe_seconds)
+            dstack.append(dict(overprov_slots=ov, k=k_d, capacity_req_s=k_d * mix.rate, probes=probes_d))
+            note("D-STACK capacity at over-provision %d: k = %.4g" % (ov, k_d))
+        for cyc in TEMPORAL_CYCLES:
+            k_t, probes_t = mix.capacity("temporal", cyc, args.probe_seconds)
+            temporal.append(dict(cycle_us=cyc, k=k_t, capacity_req_s=k_t * mix.rate, probes=probes_t))
+            note("temporal capacity at cycle %d us: k = %.4g" % (cyc, k_t))
     best_d = max(dstack, key=lambda d: d["k"])
-    temporal = []
-    for cyc in TEMPORAL_CYCLES:
-        k_t, probes_t = mix.capacity("temporal", cyc, args.probe_seconds)
-        temporal.append(dict(cycle_us=cyc, k=k_t, capacity_req_s=k_t * mix.rate, probes=probes_t))
     best_t = max(temporal, key=lambda d: d["k"])
     capacity_s = time.perf_counter() - t_cap
     k_ds, ov = best_d["k"], best_d["overprov_slots"]
@@ -825,18 +848,21 @@ def main():
                       args.warmup)
     run_t_same = mix.run(k_run, args.steps * PERIOD_US, "temporal", best_t["cycle_us"])
     value = run_ds["on_time_per_s"]
+    note("timed runs done: %.1f on-time req/s" % value)
 
     # ---- the dominant kernel (implicit-GEMM convolution) and per-model rooflines at the deployment ----
     plan, per_model, conv = mix_rooflines(ds, torch, mix, k_run, ov)
     avg_ms = conv["ms"] / max(conv["n"], 1)
     achieved = (conv["fl"] / max(conv["n"], 1)) / (avg_ms * 1e-3) / 1e12 if avg_ms > 0 else 0.0
     knee_cu = conv["cu_ms"] / max(conv["ms"], 1e-12)
+    note("roofline forwards done: %.1f TFLOP/s per conv launch" % achieved)
 
     # ---- the other workloads ----
     c1 = c2 = c3 = c4 = c6 = cmp = ideal = None
     reconf = []
     if not args.headline_only:
         c3 = config3(ds, torch, models, tables, args)
+        note("config 3 done")
         pair = [models[i] for i, _, _ in PAIR]
         for (i, slo, bmax), m in zip(PAIR, pair):
             dep = min(ds.TOTAL_SLOTS, knee_at(tables[i][bmax], bmax) + OVERPROV)
@@ -845,10 +871,13 @@ def main():
             reconf.append(dict(arch=MIX4[i][0], batch=bmax, search_knee_slots=ks["knee_slots"],
                                sweep_knee_slots=knee_at(tables[i][bmax], bmax), search_probes=ks["probes"],
                                search_seconds=ks["seconds"], switch_from_slots=10, switch_to_slots=dep, **sw))
+        note("reconfiguration probes done")
         c1 = config1(ds)
         c2 = config2(ds, torch, args)
+        note("configs 1 and 2 done")
         c6 = config6(ds, args)
         c4 = config4(ds, torch, args)
+        note("configs 6 and 4 done")
         cmp = comparators(ds, tables)
         pb = [bmax for _, _, bmax in PAIR]
         ideal = ideal_vs_dstack(ds, pair, [slo for _, slo, _ in PAIR], pb,
@@ -858,12 +887,18 @@ def main():
     # calibration copy for the HBM byte counters (a plain 256 MiB device copy)
     a = torch.empty(64 * 1024 * 1024, dtype=torch.float32, device="cuda:0")
     b = torch.empty_like(a)
+    pm = ds.Partition(1.0)
+    pm.probe_cu_ids(CAL_MARKER)
     b.copy_(a)
     torch.cuda.synchronize()
+    pm.probe_cu_ids(END_MARKER)
+    pm.destroy()
     del a, b
 
+    traffic, traffic_plan = measured_traffic()
     sched_in = mix.tabs(k_run)
     cpu = None if args.no_cpu_baseline else cpu_baseline(args.cpu_seconds, sched_in)
+    note("done")
     run_keys = ("k", "offered_req_s", "requests", "served", "on_time", "violation_frac", "on_time_per_s", "run_us",
                 "call_wall_s", "utilisation_ppm", "per_model", "param")
     out = {
@@ -908,7 +943,9 @@ def main():
             "launches": conv["n"], "avg_launch_us": 1000.0 * avg_ms,
             "flops_per_launch": conv["fl"] / max(conv["n"], 1),
             "algorithmic_bytes_per_launch": conv["by"] / max(conv["n"], 1),
-            "traffic": measured_traffic(),
+            "traffic": traffic,
+            "traffic_plan": traffic_plan,
+            "traffic_plan_matches": traffic_plan == {k: plan[k] for k in ("batch", "deployed_slots", "home_offset")},
         },
         "cpu_baseline": cpu,
         "per_model": per_model,

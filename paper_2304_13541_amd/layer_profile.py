@@ -10,7 +10,9 @@ same GEMM shape on the same masked stream, as a vendor-library reference.
 Inputs are synthetic N(0,1) values.
 
     python -m paper_2304_13541_amd.layer_profile --sweep
-    python -m paper_2304_13541_amd.layer_profile --summarize PASS_DIR [PASS_DIR ...]
+    python -m paper_2304_13541_amd.layer_profile --summarize PASS_DIR [PASS_DIR ...] [--trace TRACE_DIR]
+    python -m paper_2304_13541_amd.layer_profile --bench-kernels TRACE_DIR BENCH_LOG [UNPROFILED_BENCH_LOG]
+    python -m paper_2304_13541_amd.layer_profile --bench-traffic FETCH_DIR WRITE_DIR BENCH_LOG
 
 --sweep runs the measured workloads (ResNet-50 b16, MobileNetV2 b32, VGG-19
 b8, the LSTM b32) on partitions of 25%, 50% and 100% of the CUs, one eager
@@ -23,11 +25,20 @@ GRBM_GUI_ACTIVE, FETCH_SIZE, WRITE_SIZE in any passes), splits them at the
 markers and prints per (partition, model, kernel class): dispatches, time,
 MFMA rate from the MFMA op counter against the partition's peak, MFMA busy
 cycles per CU-cycle, and calibrated HBM bytes and GB/s.
+
+--bench-kernels and --bench-traffic read rocprofv3 runs of bench.py (kernel
+trace; FETCH_SIZE and WRITE_SIZE passes), whose roofline forwards are marked
+the same way, and summarise its dominant kernel, the implicit-GEMM
+convolution: mean dispatch duration against the bench's HIP-event figure,
+and calibrated HBM bytes per launch (the figure bench.py reports as its
+roofline traffic while the kernel source and the operating point match).
 """
 import argparse
 import collections
 import csv
 import glob
+import hashlib
+import json
 import os
 
 import torch
@@ -172,6 +183,122 @@ def summarize(dirs):
                 fmt(gbs, "%.0f")))
 
 
+# bench.py's markers: the roofline forwards of model i follow 1000 + 100 + i,
+# its calibration copy follows 1000 + 199
+BENCH_MODEL_SEG, BENCH_CAL_SEG = 100, 199
+BENCH_MODELS = ["resnet50", "mobilenetv2", "vgg19", "lstm2"]
+CONV_SRC = os.path.join(os.path.dirname(os.path.abspath(__file__)), "csrc", "conv_igemm.hip")
+
+
+def _segmented(rows, grid_of):
+    """(segment or None, row) in dispatch order; a marker opens a segment,
+    the end marker closes it."""
+    seg = None
+    for r in sorted(rows, key=lambda r: int(r["Dispatch_Id"])):
+        if kernel_class(r["Kernel_Name"]) == "marker":
+            g = grid_of(r) // 64
+            seg = g - MARKER_BASE if g >= MARKER_BASE else None
+            continue
+        yield seg, r
+
+
+def _bench_json(path):
+    for line in open(path):
+        line = line.strip()
+        if line.startswith("{") and '"metric"' in line:
+            return json.loads(line)
+    raise SystemExit("no bench JSON line in %s" % path)
+
+
+def bench_kernels(trace_dir, bench_log, ref_log=None):
+    """Markdown summary of a kernel-trace run of bench.py: the implicit-GEMM
+    convolution dispatches of the roofline forwards (the launches the
+    bench's own figure averages) against the bench's HIP-event figure, and
+    the top kernels of the whole command."""
+    path = glob.glob(os.path.join(trace_dir, "**", "*kernel_trace.csv"), recursive=True)[0]
+    grid = lambda r: int(r["Grid_Size_X"]) * int(r["Grid_Size_Y"]) * int(r["Grid_Size_Z"])
+    per = collections.OrderedDict((i, []) for i in range(len(BENCH_MODELS)))
+    for seg, r in _segmented(csv.DictReader(open(path)), grid):
+        if seg is not None and BENCH_MODEL_SEG <= seg < BENCH_MODEL_SEG + len(BENCH_MODELS):
+            if kernel_class(r["Kernel_Name"]) in ("conv", "conv_1x1_stream"):
+                per[seg - BENCH_MODEL_SEG].append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-3)
+    allv = [v for vs in per.values() for v in vs]
+    bj = _bench_json(bench_log)
+    rf = bj["roofline"]
+    print("| quantity | value |")
+    print("|---|---|")
+    print("| operating point | k = %g, over-provision %d slots, batches %s, deployed slots %s, home offsets %s |" % (
+        bj["config"]["capacity_k"], bj["config"]["overprov_slots"], bj["config"]["batch"],
+        bj["config"]["deployed_slots"], bj["config"]["home_offset"]))
+    for i, vs in per.items():
+        if vs:
+            print("| %s conv dispatches / mean us (rocprofv3) | %d / %.2f |" % (BENCH_MODELS[i], len(vs),
+                                                                            sum(vs) / len(vs)))
+    print("| all conv dispatches of the roofline forwards / mean us (rocprofv3) | %d / %.2f |" % (
+        len(allv), sum(allv) / max(len(allv), 1)))
+    print("| same launches, HIP events inside bench.py under the profiler: launches per pass / mean us | %d / %.2f |"
+          % (rf["launches"], rf["avg_launch_us"]))
+    if ref_log:
+        r0 = _bench_json(ref_log)["roofline"]
+        print("| same, unprofiled bench run: launches per pass / mean us | %d / %.2f |" % (r0["launches"],
+                                                                                        r0["avg_launch_us"]))
+    print("| algorithmic FLOP per launch (bench) | %.4g |" % rf["flops_per_launch"])
+    print("| achieved TFLOP/s = FLOP per launch / rocprofv3 mean | %.1f |" % (
+        rf["flops_per_launch"] / (sum(allv) / max(len(allv), 1) * 1e-6) / 1e12))
+    stats = glob.glob(os.path.join(trace_dir, "**", "*kernel_stats.csv"), recursive=True)
+    if stats:
+        print("\nTop kernels of the whole command (rocprofv3 --stats):\n")
+        print("| kernel | calls | total ms | avg us | min us | max us |")
+        print("|---|---|---|---|---|---|")
+        for r in list(csv.DictReader(open(stats[0])))[:12]:
+            name = r["Name"] if len(r["Name"]) < 110 else r["Name"][:107] + "..."
+            print("| `%s` | %s | %.2f | %.1f | %.1f | %.1f |" % (name, r["Calls"], int(r["TotalDurationNs"]) * 1e-6,
+                                                              float(r["AverageNs"]) * 1e-3, int(r["MinNs"]) * 1e-3,
+                                                              int(r["MaxNs"]) * 1e-3))
+
+
+def bench_traffic(fetch_dir, write_dir, bench_log):
+    """Markdown summary of two counter runs of bench.py (FETCH_SIZE, then
+    WRITE_SIZE): calibrated HBM bytes per implicit-GEMM conv launch of the
+    roofline forwards, with the conv source hash and the operating point the
+    bench checks before using the figure."""
+    tot, cal, n = {}, {}, {}
+    for cname, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
+        path = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)[0]
+        rows = [r for r in csv.DictReader(open(path)) if r["Counter_Name"] == cname]
+        by = collections.OrderedDict()
+        for r in rows:  # one row per dispatch and counter instance: sum them
+            e = by.setdefault(int(r["Dispatch_Id"]), dict(r, v=0.0))
+            e["v"] += float(r["Counter_Value"])
+        tot[cname] = cal[cname] = 0.0
+        n[cname] = 0
+        for seg, e in _segmented(by.values(), lambda r: int(r["Grid_Size"])):
+            if seg == BENCH_CAL_SEG:
+                cal[cname] += e["v"]
+            elif seg is not None and BENCH_MODEL_SEG <= seg < BENCH_MODEL_SEG + len(BENCH_MODELS) and \
+                    kernel_class(e["Kernel_Name"]) in ("conv", "conv_1x1_stream"):
+                tot[cname] += e["v"]
+                n[cname] += 1
+    cal_kib = CALIBRATION_BYTES / 1024.0
+    f = {c: cal_kib / cal[c] if cal[c] else None for c in cal}
+    bj = _bench_json(bench_log)
+    rf = bj["roofline"]
+    print("| quantity | FETCH | WRITE |")
+    print("|---|---|---|")
+    print("| conv dispatches counted | %d | %d |" % (n["FETCH_SIZE"], n["WRITE_SIZE"]))
+    print("| calibration copy reading (KiB) vs %d KiB moved | %.0f | %.0f |" % (cal_kib, cal["FETCH_SIZE"],
+                                                                              cal["WRITE_SIZE"]))
+    print("| calibration factor | %.4f | %.4f |" % (f["FETCH_SIZE"], f["WRITE_SIZE"]))
+    per = {c: tot[c] * 1024 * f[c] / max(n[c], 1) for c in tot}
+    print("| bytes per conv launch (calibrated) | %.4g | %.4g |" % (per["FETCH_SIZE"], per["WRITE_SIZE"]))
+    print("\nAlgorithmic bytes per launch (each input, weight, residual and output once): %.4g\n" %
+          rf["algorithmic_bytes_per_launch"])
+    plan = {k: bj["config"][k] for k in ("batch", "deployed_slots", "home_offset")}
+    print("traffic_bytes_per_launch: %.6g" % (per["FETCH_SIZE"] + per["WRITE_SIZE"]))
+    print("plan: %s" % json.dumps(plan))
+    print("source_sha256: %s" % hashlib.sha256(open(CONV_SRC, "rb").read()).hexdigest())
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--arch", default="resnet50", choices=ds.ARCHS)
@@ -183,7 +310,14 @@ def main():
     ap.add_argument("--sweep", action="store_true")
     ap.add_argument("--summarize", nargs="+", default=None)
     ap.add_argument("--trace", default=None, help="with --summarize: a kernel-trace run of the same sweep")
+    ap.add_argument("--bench-kernels", nargs="+", default=None, metavar=("TRACE_DIR", "BENCH_LOG"),
+                    help="kernel-trace run of bench.py, its output, [an unprofiled bench output]")
+    ap.add_argument("--bench-traffic", nargs=3, default=None, metavar=("FETCH_DIR", "WRITE_DIR", "BENCH_LOG"))
     a = ap.parse_args()
+    if a.bench_kernels:
+        return bench_kernels(*a.bench_kernels)
+    if a.bench_traffic:
+        return bench_traffic(*a.bench_traffic)
     if a.sweep:
         return sweep()
     if a.summarize:

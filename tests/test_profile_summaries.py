@@ -1,0 +1,124 @@
+"""Host logic of the rocprofv3 summaries: dispatches are attributed to the
+segment their marker opened, the calibration copy scales the byte counters,
+and bench.py takes the traffic figure back only for the same conv source.
+
+Synthetic CSVs in rocprofv3's column layout stand in for real runs."""
+import contextlib
+import csv
+import io
+import json
+import os
+
+import pytest
+
+CONV = "void dstack::conv_igemm_kernel<64, 64, 2, 2, 4, 3, false, false>(dstack::ConvArgs)"
+CONV1 = "void dstack::conv_igemm_1x1s_kernel<1>(dstack::ConvArgs)"
+PROBE = "dstack::probe_kernel(unsigned int*)"
+COPY = "void at::native::elementwise_kernel<copy>"
+OTHER = "dstack::maxpool_kernel(...)"
+
+
+def dispatches():
+    """(name, grid threads, duration ns, fetch KiB, write KiB) in dispatch order."""
+    return [
+        (CONV, 4096, 9000, 99.0, 99.0),       # before any marker: ignored
+        (PROBE, 1100 * 64, 1000, 0, 0),       # model 0
+        (CONV, 4096, 10000, 100.0, 40.0),
+        (OTHER, 4096, 3000, 7.0, 7.0),        # not a conv: ignored
+        (CONV1, 4096, 6000, 50.0, 20.0),
+        (PROBE, 999 * 64, 1000, 0, 0),
+        (CONV, 4096, 50000, 999.0, 999.0),    # between segments: ignored
+        (PROBE, 1103 * 64, 1000, 0, 0),       # model 3
+        (CONV, 4096, 20000, 200.0, 80.0),
+        (PROBE, 999 * 64, 1000, 0, 0),
+        (PROBE, 1199 * 64, 1000, 0, 0),       # calibration: 256 MiB copy read at half, written at full count
+        (COPY, 1 << 20, 40000, 131072.0, 262144.0),
+        (PROBE, 999 * 64, 1000, 0, 0),
+    ]
+
+
+def write_trace(d):
+    os.makedirs(d)
+    with open(os.path.join(d, "x_kernel_trace.csv"), "w", newline="") as f:
+        w = csv.writer(f, quoting=csv.QUOTE_NONNUMERIC)
+        w.writerow(["Dispatch_Id", "Kernel_Name", "Start_Timestamp", "End_Timestamp", "Grid_Size_X", "Grid_Size_Y",
+                    "Grid_Size_Z"])
+        t = 1000
+        for i, (name, grid, dur, _, _) in enumerate(dispatches()):
+            w.writerow([i + 1, name, t, t + dur, grid, 1, 1])
+            t += dur + 100
+    with open(os.path.join(d, "x_kernel_stats.csv"), "w", newline="") as f:
+        w = csv.writer(f, quoting=csv.QUOTE_NONNUMERIC)
+        w.writerow(["Name", "Calls", "TotalDurationNs", "AverageNs", "Percentage", "MinNs", "MaxNs", "StdDev"])
+        w.writerow([CONV, 4, 89000, 22250.0, 50.0, 9000, 50000, 1.0])
+
+
+def write_counters(d, counter, col):
+    os.makedirs(d)
+    with open(os.path.join(d, "x_counter_collection.csv"), "w", newline="") as f:
+        w = csv.writer(f, quoting=csv.QUOTE_NONNUMERIC)
+        w.writerow(["Dispatch_Id", "Grid_Size", "Kernel_Name", "Counter_Name", "Counter_Value", "Start_Timestamp",
+                    "End_Timestamp"])
+        for i, row in enumerate(dispatches()):
+            w.writerow([i + 1, row[1], row[0], counter, row[col], 0, 1])
+
+
+def bench_log(path):
+    line = dict(metric="m", config=dict(capacity_k=1.5, overprov_slots=0, batch=[8, 16, 4, 16],
+                                        deployed_slots=[10, 6, 12, 4], home_offset=[0, 10, 16, 28]),
+                roofline=dict(launches=3, avg_launch_us=11.0, flops_per_launch=1e9, algorithmic_bytes_per_launch=1e5))
+    with open(path, "w") as f:
+        f.write("progress text\n" + json.dumps(line) + "\n")
+
+
+@pytest.fixture()
+def runs(tmp_path):
+    write_trace(str(tmp_path / "kt"))
+    write_counters(str(tmp_path / "fetch"), "FETCH_SIZE", 3)
+    write_counters(str(tmp_path / "write"), "WRITE_SIZE", 4)
+    bench_log(str(tmp_path / "bench.log"))
+    return tmp_path
+
+
+def captured(fn, *a):
+    buf = io.StringIO()
+    with contextlib.redirect_stdout(buf):
+        fn(*a)
+    return buf.getvalue()
+
+
+def test_bench_kernels_attributes_marked_conv_dispatches(runs):
+    from paper_2304_13541_amd import layer_profile as lp
+    out = captured(lp.bench_kernels, str(runs / "kt"), str(runs / "bench.log"))
+    assert "| resnet50 conv dispatches / mean us (rocprofv3) | 2 / 8.00 |" in out
+    assert "| lstm2 conv dispatches / mean us (rocprofv3) | 1 / 20.00 |" in out
+    assert "| all conv dispatches of the roofline forwards / mean us (rocprofv3) | 3 / 12.00 |" in out
+    assert "mobilenetv2 conv" not in out and "vgg19 conv" not in out
+    # 1e9 FLOP / 12 us = 83.3 TFLOP/s
+    assert "| 83.3 |" in out
+
+
+def test_bench_traffic_calibrates_and_records_source(runs, monkeypatch):
+    from paper_2304_13541_amd import layer_profile as lp
+    out = captured(lp.bench_traffic, str(runs / "fetch"), str(runs / "write"), str(runs / "bench.log"))
+    assert "| conv dispatches counted | 3 | 3 |" in out
+    assert "| calibration factor | 2.0000 | 1.0000 |" in out
+    # fetch (100 + 50 + 200) KiB x 2, write (40 + 20 + 80) KiB x 1, over 3 launches
+    expect = ((100 + 50 + 200) * 2 + (40 + 20 + 80)) * 1024 / 3
+    vals = dict(l.split(":", 1) for l in out.splitlines() if l.split(":")[0] in ("traffic_bytes_per_launch", "plan",
+                                                                                  "source_sha256"))
+    assert float(vals["traffic_bytes_per_launch"]) == pytest.approx(expect, rel=1e-5)
+    assert json.loads(vals["plan"]) == dict(batch=[8, 16, 4, 16], deployed_slots=[10, 6, 12, 4],
+                                            home_offset=[0, 10, 16, 28])
+
+    # bench.py reads it back while the conv source is the one hashed, not after it changed
+    import bench
+    f = runs / "traffic.md"
+    f.write_text("# summary\n" + out)
+    monkeypatch.setattr(bench, "TRAFFIC_FILE", str(f))
+    t, plan = bench.measured_traffic()
+    assert t == pytest.approx(expect, rel=1e-5) and plan["batch"] == [8, 16, 4, 16]
+    src = runs / "conv.hip"
+    src.write_text("changed")
+    monkeypatch.setattr(bench, "CONV_SRC", str(src))
+    assert bench.measured_traffic() == (None, None)
