@@ -166,7 +166,13 @@ def cpu_baseline(budget_s, sched_in):
         if el >= budget_s and i % len(MIX4) == 0:
             break
     threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
-    return dict(value=done / el, unit="inferences/s", cores=threads, kind="oracle",
+    cpu_model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            cpu_model = next((l.split(":", 1)[1].strip() for l in f if l.startswith("model name")), None)
+    except OSError:
+        pass
+    return dict(value=done / el, unit="inferences/s", cores=threads, kind="oracle", cpu_model=cpu_model,
                 sample="%d single items round-robin over ResNet-50 / MobileNetV2 / VGG-19 images (224x224) and "
                        "LSTM sequences (50 x 512): %s each (fp64 oracle, parity mode), %.1f s" %
                        (done, "/".join(map(str, counts)), el),
