@@ -466,8 +466,13 @@ dstack_status dstack_schedule(const dstack_sched_model* models, int n_models, co
  * it stays, the count restarts), keeping its home offset if the larger range
  * fits, else ending at the last slot.  From then on its planned jobs and
  * FOD jobs use that range and the table latency there; a planned start runs
- * only if its slots are free.  The live launcher moves the model to a new
- * CU-masked stream at that moment (between its batches). */
+ * only if its slots are free.  Only requests that arrived at or after the
+ * model's last change count towards the next one (earlier ones waited
+ * through the previous size).  The live launcher moves the model to a new
+ * CU-masked stream at that moment (between its batches): it destroys the
+ * old stream, creates the new one on a helper thread while the other models
+ * keep running, and the model starts no job until that stream is ready;
+ * its count then restarts from that time. */
 typedef struct {
   int64_t duration_us;
   int fod;
@@ -539,8 +544,10 @@ dstack_status dstack_simulate_ideal(const dstack_ideal_model* models, int n_mode
 /* Runs the same plan and the same FOD decisions as dstack_simulate, on the
  * host's monotonic clock (us since the call's start, after a warm-up) with
  * real batches: model i owns one partition on its home range (placement
- * must be 1) and every job of model i is dstack_infer(models[i], b, d_in[i],
- * d_out[i], that partition).  Requests arrive when the clock passes their
+ * must be 1) and every job of model i runs as dstack_infer(models[i], b,
+ * d_in[i], d_out[i], that partition) would, with a workspace (activations,
+ * split-K buffers, captured graphs) the model keeps for the launcher across
+ * partitions and calls.  Requests arrive when the clock passes their
  * trace time; a job's requests complete when its end event is seen by the
  * polling host thread (latency = that time - arrival).  Decisions use the
  * timing table only (busy time is charged with the table latency); a planned
@@ -567,7 +574,8 @@ dstack_status dstack_simulate_ideal(const dstack_ideal_model* models, int n_mode
  *    completion seen (model), kind 1 a planned start due (model, value_us =
  *    its planned time, slot_mask = its slots; temporal: a slice start, mask
  *    all slots), kind 2 an arrival admitted (model, value_us = its trace
- *    time); t_us is the clock value the decision taken at that trigger used
+ *    time), kind 3 a GPU% change took effect (model, slot_mask = its new
+ *    range); t_us is the clock value the decision taken at that trigger used
  *    (a job started there has start_us == t_us), so that the decisions can be
  *    replayed from the table and this list alone.
  * Errors: E_INVALID (bad arguments, D-STACK without placement 1, a policy
@@ -587,7 +595,7 @@ typedef struct {
   int64_t t_us;        /* clock value of the decision at this trigger */
   int64_t value_us;    /* arrival: trace time; planned / slice start: its planned time; else 0 */
   uint64_t slot_mask;  /* planned / slice start: its slots; else 0 */
-  int kind;            /* 0 completion seen, 1 planned or slice start due, 2 arrival admitted */
+  int kind;            /* 0 completion seen, 1 planned or slice start due, 2 arrival admitted, 3 GPU% change ready */
   int model;
 } dstack_serve_event;
 

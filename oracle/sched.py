@@ -423,7 +423,9 @@ def simulate(models, period, duration, arrivals, total=TOTAL_SLOTS, overprov=OVE
     resize_violations > 0 (D-STACK with home placement): a GPU% change on
     SLO violations (Sec. 3.5's dynamic reconfiguration, the trigger count a
     parameter).  Once the late requests of a model's completed jobs since its
-    last change reach the count, at that completion the model moves to the
+    last change -- counting only requests that arrived at or after that
+    change, since earlier ones waited through the previous size -- reach the
+    count, at that completion the model moves to the
     next larger column of its table (over all batches) that has a latency at
     its plan batch -- none: it stays, the count restarts -- keeping its home
     offset if the range fits, else ending at the last slot; from then on its
@@ -434,10 +436,14 @@ def simulate(models, period, duration, arrivals, total=TOTAL_SLOTS, overprov=OVE
     handled, in its order, as dicts (kind, t_us, model, value_us, slot_mask):
     kind 0 a completion seen (the model's job ends), 1 a planned start due
     (value_us its planned time, slot_mask its slots; temporal: a slice
-    start), 2 an arrival admitted (value_us its trace time); each decision is
-    taken at t_us with the same rules (a planned start also needs its slots
-    free, since a measured job may overrun its table time).  The jobs started
-    are then in "log" as (start, table end, model, mask, kind, batch)."""
+    start), 2 an arrival admitted (value_us its trace time), 3 a GPU% change
+    took effect (the live launcher builds the model's new stream meanwhile:
+    from the completion that triggers the change until this event the model
+    starts no job, and its late-request count restarts here); each decision
+    is taken at t_us with the same rules (a planned start also needs its
+    slots free, since a measured job may overrun its table time).  The jobs
+    started are then in "log" as (start, table end, model, mask, kind,
+    batch)."""
     import collections
     import heapq
     choices, jobs, _, _ = schedule(models, period, total, overprov, placement)
@@ -452,6 +458,8 @@ def simulate(models, period, duration, arrivals, total=TOTAL_SLOTS, overprov=OVE
     cur_home = list(homes) if homes is not None else [0] * n
     viol = [0] * n
     resizes = [0] * n
+    changed_at = [0] * n  # time of each model's last GPU% change
+    unavailable = set()   # replay of a live run: models whose new stream is not ready yet
     columns = [sorted(set().union(*[set(r) for r in m["table"].values()])) for m in models]
     if policy == "temporal":
         cycle = slice_cycle if slice_cycle > 0 else min(m["slo_us"] for m in models)
@@ -529,10 +537,10 @@ def simulate(models, period, duration, arrivals, total=TOTAL_SLOTS, overprov=OVE
             return mask, dur
         return range_mask(cur_home[i], cur_dep[i]), lat(i, choices[i].batch, cur_dep[i])
 
-    def note_late(i, late_n):
+    def note_late(i, t, reqs):
         if policy != "dstack" or resize_violations <= 0:
             return
-        viol[i] += late_n
+        viol[i] += sum(1 for a in reqs if t - a > models[i]["slo_us"] and a >= changed_at[i])
         if viol[i] < resize_violations:
             return
         viol[i] = 0
@@ -543,6 +551,9 @@ def simulate(models, period, duration, arrivals, total=TOTAL_SLOTS, overprov=OVE
         if cur_home[i] + nxt[0] > total:
             cur_home[i] = total - nxt[0]
         resizes[i] += 1
+        changed_at[i] = t
+        if replay_events is not None:  # live: the model waits for its new stream (an event of kind 3)
+            unavailable.add(i)
 
     def temporal_pass(t):
         if t >= duration or running:
@@ -569,7 +580,7 @@ def simulate(models, period, duration, arrivals, total=TOTAL_SLOTS, overprov=OVE
             return
         if t >= duration:  # nothing starts once the trace has ended
             return
-        cands = [i for i in range(n) if i not in running and queue[i]]
+        cands = [i for i in range(n) if i not in running and queue[i] and i not in unavailable]
         cur = t // period
         if policy == "maxthroughput":
             cands.sort(key=lambda i: (choices[i].latency, i))
@@ -617,7 +628,7 @@ def simulate(models, period, duration, arrivals, total=TOTAL_SLOTS, overprov=OVE
             if e["kind"] == 0:
                 _, mask, reqs = running.pop(i)
                 used &= ~mask
-                note_late(i, sum(1 for a in reqs if t - a > models[i]["slo_us"]))
+                note_late(i, t, reqs)
                 if fod:
                     fod_pass(t)
             elif e["kind"] == 1 and policy == "temporal":
@@ -625,10 +636,15 @@ def simulate(models, period, duration, arrivals, total=TOTAL_SLOTS, overprov=OVE
             elif e["kind"] == 1:
                 key = (e["value_us"], i)
                 mask, dur = current(i, *plan_dur[key])
-                if queue[i] and i not in running and not used & mask:
+                if queue[i] and i not in running and i not in unavailable and not used & mask:
                     start_job(t, i, mask, dur, min(choices[i].batch, len(queue[i])), 0)
                 else:
                     plan_skips[i] += 1
+            elif e["kind"] == 3:  # a GPU% change took effect: the model runs again, its count restarts now
+                unavailable.discard(i)
+                changed_at[i] = t
+                if fod:
+                    fod_pass(t)
             else:
                 queue[i].append(e["value_us"])
                 if fod:
@@ -651,7 +667,7 @@ def simulate(models, period, duration, arrivals, total=TOTAL_SLOTS, overprov=OVE
                 if t - a > models[i]["slo_us"]:
                     job_late += 1
             late[i] += job_late
-            note_late(i, job_late)
+            note_late(i, t, payload)
             if fod:
                 fod_pass(t)
         elif kind == 1 and policy == "temporal":

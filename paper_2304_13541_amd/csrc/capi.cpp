@@ -46,7 +46,8 @@ struct dstack_model_s {
 namespace {
 
 // Partition ids start at 16: workspace ids below that are the library's own
-// (knee sweeps, GPU% change probes), never a partition's.
+// (knee sweeps 0, GPU% change probes 1 and 2, the live launcher's models 4..7),
+// never a partition's.
 std::atomic<int> g_next_partition_id{16};
 
 // Live partitions.  Each owns one CU-masked HIP stream, and a CU-masked
@@ -365,7 +366,7 @@ dstack_status check_batch(const Model& m, int batch) {
 // Workspace id 0 is reserved for knee sweeps, which run one partition at a
 // time and reuse a single workspace across fractions.
 constexpr int SWEEP_WS_ID = 0;
-constexpr size_t kMaxGraphsPerWorkspace = 32;
+constexpr size_t kMaxGraphsPerWorkspace = 64;
 
 // Forward passes are replayed as HIP graphs unless DSTACK_GRAPH=0.
 bool graphs_enabled() {
@@ -376,8 +377,11 @@ bool graphs_enabled() {
   return on;
 }
 
+// capture_n_cu > 0: only record and instantiate the graph of a forward
+// planned for that many CUs (on p's stream, which runs nothing), so that a
+// later call on a partition of that size finds it.
 dstack_status infer_impl(Model& m, int batch, const void* d_in, void* d_out, dstack_partition p, KernelTimer* timer,
-                         int ws_id = -1) {
+                         int ws_id = -1, int capture_n_cu = 0) {
   DS_CHECK(d_in && d_out && p, DSTACK_E_INVALID, "infer: null pointer");
   dstack_status s = check_batch(m, batch);
   if (s != DSTACK_OK) return s;
@@ -386,13 +390,15 @@ dstack_status infer_impl(Model& m, int batch, const void* d_in, void* d_out, dst
   if (s != DSTACK_OK) return s;
   BusyGuard g(ws->busy);
   DS_CHECK(g.ok, DSTACK_E_STATE, "infer: another call on this (model, partition) is in progress");
-  if (timer || !graphs_enabled()) return forward(m, batch, d_in, d_out, *ws, p->n_cu, p->stream, timer);
+  if (timer || !graphs_enabled())
+    return capture_n_cu > 0 ? DSTACK_OK : forward(m, batch, d_in, d_out, *ws, p->n_cu, p->stream, timer);
   // one forward = one graph launch: captured on first use of this key
-  const Workspace::GraphKey key{batch, d_in, d_out, p->n_cu};
+  const int n_cu = capture_n_cu > 0 ? capture_n_cu : p->n_cu;
+  const Workspace::GraphKey key{batch, d_in, d_out, n_cu};
   auto it = ws->graphs.find(key);
   if (it == ws->graphs.end()) {
     DS_HIP(hipStreamBeginCapture(p->stream, hipStreamCaptureModeThreadLocal));
-    s = forward(m, batch, d_in, d_out, *ws, p->n_cu, p->stream, nullptr);
+    s = forward(m, batch, d_in, d_out, *ws, n_cu, p->stream, nullptr);
     hipGraph_t graph = nullptr;
     hipError_t e = hipStreamEndCapture(p->stream, &graph);
     if (s != DSTACK_OK) {
@@ -413,11 +419,14 @@ dstack_status infer_impl(Model& m, int batch, const void* d_in, void* d_out, dst
     it = ws->graphs.emplace(key, exec).first;
     ws->graph_order.push_back(key);
   }
+  if (capture_n_cu > 0) return DSTACK_OK;
   DS_HIP(hipGraphLaunch(it->second, p->stream));
   return DSTACK_OK;
 }
 
 }  // namespace
+
+
 
 dstack_status dstack_infer(dstack_model h, int batch, const void* d_in, void* d_out, dstack_partition p) {
   return guarded([&] {
@@ -1042,3 +1051,26 @@ dstack_status dstack_op_attention(const void* qkv, int B, int T, int heads, int 
 }
 
 }  // extern "C"
+
+// Launcher-internal entry points (C++ linkage; see launcher.hpp).
+namespace dstack {
+
+dstack_status launcher_infer(dstack_model h, int batch, const void* d_in, void* d_out, dstack_partition p,
+                             int ws_id) {
+  return guarded([&] {
+    DS_CHECK(h && ws_id >= kLauncherWsBase && ws_id < kLauncherWsBase + kLauncherWsCount, DSTACK_E_INVALID,
+             "launcher: bad model or workspace id");
+    return infer_impl(h->m, batch, d_in, d_out, p, nullptr, ws_id);
+  });
+}
+
+dstack_status launcher_prepare(dstack_model h, int batch, const void* d_in, void* d_out, dstack_partition p, int n_cu,
+                               int ws_id) {
+  return guarded([&] {
+    DS_CHECK(h && ws_id >= kLauncherWsBase && ws_id < kLauncherWsBase + kLauncherWsCount && n_cu >= 1,
+             DSTACK_E_INVALID, "launcher: bad model, workspace id or CU count");
+    return infer_impl(h->m, batch, d_in, d_out, p, nullptr, ws_id, n_cu);
+  });
+}
+
+}  // namespace dstack

@@ -88,7 +88,7 @@ LaunchState::LaunchState(const dstack_sched_model* models, int n, const dstack_s
                          const dstack_sim_params* sim, const dstack_schedule_out* plan)
     : models_(models), n_(n), prm_(prm), sim_(sim), plan_(plan), T_(prm->period_us), D_(sim->duration_us),
       queue_(n), running_(n, 0), run_mask_(n, 0), runs_(n), busy_(n, 0), dep_(n), home_(n), viol_(n, 0),
-      resizes_(n, 0) {
+      resizes_(n, 0), changed_at_(n, 0), avail_(n, 1) {
   for (int i = 0; i < n; ++i) {
     dep_[i] = plan->deployed_slots[i];
     home_[i] = prm->placement == 1 ? plan->home_offset[i] : 0;
@@ -127,7 +127,6 @@ LaunchState::LaunchState(const dstack_sched_model* models, int n, const dstack_s
 }
 
 bool LaunchState::note_late(int64_t t, int i, int64_t late) {
-  (void)t;
   if (sim_->policy != 0 || sim_->resize_violations <= 0) return false;
   viol_[i] += late;
   if (viol_[i] < sim_->resize_violations) return false;
@@ -141,6 +140,7 @@ bool LaunchState::note_late(int64_t t, int i, int64_t late) {
   dep_[i] = next;
   if (home_[i] + next > prm_->total_slots) home_[i] = prm_->total_slots - next;
   resizes_[i] += 1;
+  changed_at_[i] = t;
   return true;
 }
 
@@ -189,7 +189,7 @@ bool LaunchState::fod_pick(int64_t t, Pick* out) const {
   if (t >= D_) return false;  // nothing starts once the trace has ended
   std::vector<int> cands;
   for (int i = 0; i < n_; ++i)
-    if (!running_[i] && !queue_[i].empty()) cands.push_back(i);
+    if (!running_[i] && !queue_[i].empty() && avail_[i]) cands.push_back(i);
   const int64_t cur = t / T_;
   auto recent = [&](int i) {
     int64_t r = 0;
@@ -328,14 +328,17 @@ dstack_status simulate(const dstack_sched_model* models, int n, const dstack_sch
     const int i = e.model;
     if (e.kind == 0) {
       ls.finish(i);
-      int64_t job_late = 0;
+      int64_t job_late = 0, late_since = 0;
       for (int64_t a : e.reqs) {
         served[i] += 1;
         lats[i].push_back(e.t - a);
-        if (e.t - a > models[i].slo_us) job_late += 1;
+        if (e.t - a > models[i].slo_us) {
+          job_late += 1;
+          if (a >= ls.changed_at(i)) late_since += 1;
+        }
       }
       late[i] += job_late;
-      ls.note_late(e.t, i, job_late);
+      ls.note_late(e.t, i, late_since);
       fod_pass(e.t);
     } else if (e.kind == 1 && ls.temporal()) {
       fod_pass(e.t);

@@ -45,10 +45,23 @@ class LaunchState {
   bool fod_pick(int64_t t, Pick* out) const;
   // GPU% change on SLO violations (resize_violations > 0, D-STACK with home
   // placement): a job of model i ended at t with `late` requests past their
-  // SLO; once its late count since its last change reaches the threshold the
-  // model moves to the next larger swept slot count (true returned).  Its
-  // current size, home offset and the planned job as it now runs:
+  // SLO among those that arrived at or after changed_at(i) (earlier ones
+  // waited through the previous size and say nothing about the current one);
+  // once that count since its last change reaches the threshold the model
+  // moves to the next larger swept slot count (true returned) and
+  // changed_at(i) becomes t.  Its current size, home offset and the planned
+  // job as it now runs:
   bool note_late(int64_t t, int i, int64_t late);
+  int64_t changed_at(int i) const { return changed_at_[i]; }
+  // the live launcher: model i's new stream is being created (it neither
+  // starts planned jobs nor is picked by FOD) until ready(i, t), which also
+  // moves changed_at(i) to t
+  void unavailable(int i) { avail_[i] = 0; }
+  void ready(int i, int64_t t) {
+    avail_[i] = 1;
+    changed_at_[i] = t;
+  }
+  bool available(int i) const { return avail_[i] != 0; }
   int deployed(int i) const { return dep_[i]; }
   int home(int i) const { return home_[i]; }
   int64_t resizes(int i) const { return resizes_[i]; }
@@ -86,6 +99,8 @@ class LaunchState {
   std::vector<int64_t> busy_;
   std::vector<int> dep_, home_;                 // current deployed slots and home offset
   std::vector<int64_t> viol_, resizes_;         // late requests since the last change, changes
+  std::vector<int64_t> changed_at_;             // time of the last change (0: none)
+  std::vector<char> avail_;                     // 0 while the live launcher builds its new stream
 };
 
 // nearest-rank percentile (sorts v)
@@ -95,6 +110,19 @@ bool check_trace(int n, const dstack_sim_params* sim);
 
 dstack_status simulate_ideal(const dstack_ideal_model* models, int n, int64_t horizon, int64_t slot, int total,
                              dstack_ideal_out* out);
+
+// The live launcher's model workspaces: model i of a run uses workspace id
+// kLauncherWsBase + i, whose activations, split-K buffers and captured graphs
+// belong to the model rather than to a partition, so a GPU% change (a new
+// partition) reuses them and allocates, frees and synchronises nothing.
+constexpr int kLauncherWsBase = 4, kLauncherWsCount = 4;
+// dstack_infer with the launcher workspace ws_id
+dstack_status launcher_infer(dstack_model h, int batch, const void* d_in, void* d_out, dstack_partition p, int ws_id);
+// records and instantiates the graph of a forward planned for n_cu CUs
+// (captured on p's stream, nothing runs), for a later launcher_infer on a
+// partition of that size
+dstack_status launcher_prepare(dstack_model h, int batch, const void* d_in, void* d_out, dstack_partition p, int n_cu,
+                               int ws_id);
 
 dstack_status serve(const dstack_model* models, int n, const void* const* d_in, void* const* d_out,
                     const dstack_sched_model* tables, const dstack_sched_params* prm, const dstack_sim_params* sim,

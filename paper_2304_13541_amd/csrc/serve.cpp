@@ -15,7 +15,9 @@
 #include <chrono>
 #include <cmath>
 #include <cstring>
+#include <future>
 #include <string>
+#include <utility>
 #include <vector>
 
 #include "launcher.hpp"
@@ -30,6 +32,8 @@ int64_t host_us() {
 }
 
 constexpr int kMaxServeModels = 4;
+static_assert(kMaxServeModels <= kLauncherWsCount, "one launcher workspace per model");
+constexpr int kResizeAhead = 3;  // GPU% changes per model whose graphs the warm-up captures
 constexpr int64_t kDrainLimitUs = 60LL * 1000 * 1000;  // a job still running this long after the trace: error
 const int kGrid[] = {1, 2, 4, 8, 16, 32};
 
@@ -41,11 +45,21 @@ struct Running {
   std::vector<int64_t> reqs;
 };
 
+// A GPU% change's new partition, created on a helper thread so that the
+// launcher keeps serving the other models meanwhile.
+using NewPartition = std::pair<dstack_status, dstack_partition>;
+
 struct Resources {
   std::vector<dstack_partition> part;
+  std::vector<std::future<NewPartition>> pending;  // per model; valid() while its stream is being created
   std::vector<hipEvent_t> ev0, ev1;
   bool drained = true;  // false: a job may still run, keep the partitions
   ~Resources() {
+    for (auto& f : pending)
+      if (f.valid()) {  // an early return: wait for the creation, keep the partition with the others
+        NewPartition np = f.get();
+        if (np.first == DSTACK_OK) part.push_back(np.second);
+      }
     for (hipEvent_t e : ev0)
       if (e) (void)hipEventDestroy(e);
     for (hipEvent_t e : ev1)
@@ -94,6 +108,7 @@ dstack_status serve(const dstack_model* models, int n, const void* const* d_in, 
   Resources res;
   const int n_parts = temporal ? 1 : n;
   res.part.assign(n_parts, nullptr);
+  res.pending.resize(n);
   res.ev0.assign(n, nullptr);
   res.ev1.assign(n, nullptr);
   std::vector<hipStream_t> pstream(n_parts);
@@ -116,16 +131,36 @@ dstack_status serve(const dstack_model* models, int n, const void* const* d_in, 
   }
   LaunchState ls(tables, n, prm, sim, plan);
 
-  // warm-up: every batch a job of this run can take (captures its graph)
+  // warm-up: every batch a job of this run can take (captures its graph);
+  // with GPU% changes on, also the graphs of the next kResizeAhead larger
+  // GPU% each model can move to (captured only), so that a change needs a
+  // new stream and nothing else
   for (int i = 0; i < n; ++i) {
     const int slots = temporal ? prm->total_slots : plan->deployed_slots[i];
     for (int b : kGrid) {
       if (b > tables[i].max_batch) continue;
       if ((temporal || b != plan->batch[i]) && ls.table_latency(i, b, slots) <= 0) continue;
       for (int r = 0; r < 2; ++r) {
-        st = dstack_infer(models[i], b, d_in[i], d_out[i], part[i]);
+        st = launcher_infer(models[i], b, d_in[i], d_out[i], part[i], kLauncherWsBase + i);
         if (st != DSTACK_OK) return st;
       }
+    }
+    if (temporal || sim->resize_violations <= 0) continue;
+    int cur = slots;
+    for (int step = 0; step < kResizeAhead; ++step) {
+      int next = -1;  // the rule of LaunchState::note_late
+      for (int q = 0; q < tables[i].n_slots && next < 0; ++q)
+        if (tables[i].slots[q] > cur && tables[i].slots[q] <= prm->total_slots &&
+            ls.table_latency(i, plan->batch[i], tables[i].slots[q]) > 0)
+          next = tables[i].slots[q];
+      if (next < 0) break;
+      for (int b : kGrid) {
+        if (b > tables[i].max_batch || (b != plan->batch[i] && ls.table_latency(i, b, next) <= 0)) continue;
+        st = launcher_prepare(models[i], b, d_in[i], d_out[i], part[i], next * DSTACK_CUS_PER_SLOT,
+                              kLauncherWsBase + i);
+        if (st != DSTACK_OK) return st;
+      }
+      cur = next;
     }
   }
   for (int q = 0; q < n_parts; ++q) {
@@ -162,7 +197,7 @@ dstack_status serve(const dstack_model* models, int n, const void* const* d_in, 
     r.batch = b;
     r.kind = kind;
     DS_HIP(hipEventRecord(res.ev0[i], stream[i]));
-    dstack_status s = dstack_infer(models[i], b, d_in[i], d_out[i], part[i]);
+    dstack_status s = launcher_infer(models[i], b, d_in[i], d_out[i], part[i], kLauncherWsBase + i);
     if (s != DSTACK_OK) return s;
     DS_HIP(hipEventRecord(res.ev1[i], stream[i]));
     for (int64_t v : {t, (int64_t)i, (int64_t)b, (int64_t)mask, table_us, (int64_t)kind})
@@ -207,11 +242,14 @@ dstack_status serve(const dstack_model* models, int n, const void* const* d_in, 
       Running& r = run[i];
       r.on = false;
       ls.finish(i);
-      int64_t job_late = 0;
+      int64_t job_late = 0, late_since = 0;
       for (int64_t a : r.reqs) {
         served[i] += 1;
         lats[i].push_back(te - a);
-        if (te - a > tables[i].slo_us) job_late += 1;
+        if (te - a > tables[i].slo_us) {
+          job_late += 1;
+          if (a >= ls.changed_at(i)) late_since += 1;
+        }
       }
       late[i] += job_late;
       busy[i] += gpu_us;
@@ -221,23 +259,42 @@ dstack_status serve(const dstack_model* models, int n, const void* const* d_in, 
         log[jobs] = dstack_job_record{r.start, te, gpu_us, r.table_us, i, r.batch, r.kind, r.mask};
       ++jobs;
       note(te, 0, i, 0, 0);
-      if (ls.note_late(te, i, job_late)) {
+      if (ls.note_late(te, i, late_since)) {
         // GPU% change between batches: the model's next jobs run on a new
-        // CU-masked stream over its larger range (the old one is destroyed
-        // first; weights are shared, its workspace and graphs are rebuilt
-        // at its first job there)
-        dstack_partition np = nullptr;
+        // CU-masked stream over its larger range.  The old one is destroyed
+        // first (so no more than four exist), the new one is created on a
+        // helper thread while the other models keep running; weights,
+        // workspace and the graphs captured for that size at warm-up belong
+        // to the model and carry over.
         dstack_partition_destroy(res.part[i]);
-        res.part[i] = nullptr;
-        st = dstack_partition_create_at(ls.home(i), ls.deployed(i), &np);
-        if (st != DSTACK_OK) return st;
-        void* sp = nullptr;
-        st = dstack_partition_query(np, nullptr, nullptr, &sp);
-        if (st != DSTACK_OK) return st;
-        res.part[i] = part[i] = np;
-        stream[i] = (hipStream_t)sp;
+        res.part[i] = part[i] = nullptr;
+        ls.unavailable(i);
+        const int home = ls.home(i), dep = ls.deployed(i);
+        res.pending[i] = std::async(std::launch::async, [home, dep] {
+          dstack_partition np = nullptr;
+          const dstack_status s = dstack_partition_create_at(home, dep, &np);
+          return NewPartition{s, np};
+        });
       }
       st = fod_pass(te);
+      if (st != DSTACK_OK) return st;
+    }
+    // GPU% changes whose new stream is ready
+    for (int i = 0; i < n; ++i) {
+      if (!res.pending[i].valid() ||
+          res.pending[i].wait_for(std::chrono::seconds(0)) != std::future_status::ready)
+        continue;
+      const NewPartition np = res.pending[i].get();
+      if (np.first != DSTACK_OK) return np.first;
+      res.part[i] = part[i] = np.second;
+      void* sp = nullptr;
+      st = dstack_partition_query(np.second, nullptr, nullptr, &sp);
+      if (st != DSTACK_OK) return st;
+      stream[i] = (hipStream_t)sp;
+      const int64_t tn = clock();
+      ls.ready(i, tn);
+      note(tn, 3, i, 0, range_mask(ls.home(i), ls.deployed(i)));
+      st = fod_pass(tn);
       if (st != DSTACK_OK) return st;
     }
     // planned starts (temporal: slice starts) that are due
@@ -249,7 +306,7 @@ dstack_status serve(const dstack_model* models, int n, const void* const* d_in, 
       if (temporal) {
         st = fod_pass(tn);
         if (st != DSTACK_OK) return st;
-      } else if (ls.queued(i) && !ls.running(i) && ls.free(ps.mask)) {
+      } else if (ls.queued(i) && !ls.running(i) && ls.available(i) && ls.free(ps.mask)) {
         st = launch(tn, i, ps.mask, ps.dur, std::min<int>(ls.plan_batch(i), (int)ls.queued(i)), 0);
         if (st != DSTACK_OK) return st;
         busy_now = true;
@@ -273,7 +330,7 @@ dstack_status serve(const dstack_model* models, int n, const void* const* d_in, 
       st = fod_pass(tn);
       if (st != DSTACK_OK) return st;
     }
-    for (int i = 0; i < n; ++i) busy_now = busy_now || run[i].on;
+    for (int i = 0; i < n; ++i) busy_now = busy_now || run[i].on || res.pending[i].valid();
     if (t >= D && !busy_now) break;
     if (t > D + kDrainLimitUs) {
       res.drained = false;
