@@ -260,6 +260,37 @@ def test_lstm_layer(env, case):
     assert oracle.rel_err(gu.host(hb), h_ref) <= TOL
 
 
+@pytest.mark.parametrize("slots", [1, 3, 16])
+def test_lstm_layer_on_partitions(env, slots):
+    """The layer on CU-masked streams of 8, 24 and 128 CUs (256 blocks per
+    step, from 32 down to 2 per CU); same bar as above."""
+    ds, gu, inputs, oracle, torch = env
+    T, B, I, H = 50, 32, 512, 1024
+    print("lstm layer on %d slots" % slots, flush=True)
+    xb = inputs.normal_bf16(22, (T, B, I))
+    a = 1.0 / np.sqrt(H)
+    wih = inputs.uniform_bf16(23, (4 * H, I), -a, a)
+    whh = inputs.uniform_bf16(24, (4 * H, H), -a, a)
+    bias = np.random.default_rng(25).uniform(-2 * a, 2 * a, 4 * H).astype(np.float32)
+    hb = gu.empty_bf16((T, B, H))
+    hf = gu.empty_f32((T, B, H))
+    ws = torch.empty(ds.lstm_workspace_bytes(T, B, H), dtype=torch.uint8, device="cuda:0")
+    part = ds.Partition(slot_offset=0, n_slots=slots)
+    try:
+        ds.lstm_layer(gu.dev_bf16(xb), gu.dev_bf16(wih), gu.dev_bf16(whh), gu.dev_f32(bias), hb, hf, ws,
+                      stream=part.stream_ptr)
+        part.synchronize()
+        h_ref, _ = oracle.lstm_layer(oracle.bf16_bits_to_f64(xb), oracle.bf16_bits_to_f64(wih),
+                                     oracle.bf16_bits_to_f64(whh), bias.astype(np.float64), np.zeros(4 * H),
+                                     round_h=True)
+        err = oracle.rel_err(gu.host(hf), h_ref)
+        print("  rel_err %.3e" % err, flush=True)
+        assert err <= TOL
+        assert oracle.rel_err(gu.host(hb), h_ref) <= TOL
+    finally:
+        part.destroy()
+
+
 def test_kernel_argument_errors(env):
     ds, gu, inputs, oracle, torch = env
     x = gu.empty_bf16((1, 4, 4, 12))
