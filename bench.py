@@ -624,6 +624,25 @@ class Mix4:
         return self.run(k, steps * PERIOD_US, policy, param)
 
 
+def confirm_capacity(mix, policy, param, entry, steps, warmup):
+    """The timed run at a policy's capacity must itself meet the bar (a probe
+    near saturation can pass over its shorter trace): if it does not, it is
+    repeated at the next lower k that passed its probe.  Returns (k, run);
+    entry["timed_k"] lists the k tried."""
+    k = entry["k"] if entry["k"] > 0 else 1.0
+    run = mix.timed(k, policy, param, steps, warmup)
+    tried = [k]
+    while run["violation_frac"] > VIOLATION_BAR:
+        lower = [p["k"] for p in entry["probes"] if p["violation_frac"] <= VIOLATION_BAR and p["k"] < k]
+        if not lower:
+            break
+        k = max(lower)
+        run = mix.timed(k, policy, param, steps, warmup)
+        tried.append(k)
+    entry["timed_k"] = tried
+    return k, run
+
+
 def mix_rooflines(ds, torch, mix, k, overprov):
     """Each model of the four-model mix on its deployed home partition at the
     plan's batch (dstack_schedule with the rates at k): per-layer kernel
@@ -857,25 +876,8 @@ def main():
     k_ds, ov, rv = best_d["k"], best_d["overprov_slots"], best_d["resize_violations"]
 
     # ---- timed: K sessions of live serving at each policy's capacity ----
-    # The timed run must meet the bar itself (a probe near saturation can pass
-    # over its shorter trace): if it does not, it is repeated at the next lower
-    # k that passed its probe.
-    def confirmed(policy, param, entry):
-        k = entry["k"] if entry["k"] > 0 else 1.0
-        run = mix.timed(k, policy, param, args.steps, args.warmup)
-        tried = [k]
-        while run["violation_frac"] > VIOLATION_BAR:
-            lower = [p["k"] for p in entry["probes"] if p["violation_frac"] <= VIOLATION_BAR and p["k"] < k]
-            if not lower:
-                break
-            k = max(lower)
-            run = mix.timed(k, policy, param, args.steps, args.warmup)
-            tried.append(k)
-        entry["timed_k"] = tried
-        return k, run
-
-    k_run, run_ds = confirmed("dstack", (ov, rv), best_d)
-    k_t, run_t = confirmed("temporal", best_t["cycle_us"], best_t)
+    k_run, run_ds = confirm_capacity(mix, "dstack", (ov, rv), best_d, args.steps, args.warmup)
+    k_t, run_t = confirm_capacity(mix, "temporal", best_t["cycle_us"], best_t, args.steps, args.warmup)
     run_t_same = mix.run(k_run, args.steps * PERIOD_US, "temporal", best_t["cycle_us"])
     value = run_ds["on_time_per_s"]
     note("timed runs done: %.1f on-time req/s" % value)

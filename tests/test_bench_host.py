@@ -1,6 +1,7 @@
 """Host-side helpers of bench.py that decide the timed workload: the knee of
-a timing-table row, fitting the deployed slot counts into the GPU, and
-packing them into disjoint partitions (no GPU needed)."""
+a timing-table row, fitting the deployed slot counts into the GPU, packing
+them into disjoint partitions, and the capacity search with its confirming
+timed run (on a stand-in for the live mix; no GPU needed)."""
 import random
 
 import bench
@@ -44,3 +45,50 @@ def test_pack_lanes_disjoint_and_bounded():
         assert not (span & used) and off + n <= 32
         used |= span
     assert {mi for mi, _, _ in lanes} == {0, 1}  # round-robin over the models
+
+
+class FakeMix:
+    """Stands in for the live four-model mix: a run at rate scale k violates
+    when k exceeds a threshold (the probes) or a lower one for the longer
+    timed runs (saturation grows with the trace length)."""
+
+    def __init__(self, probe_limit, timed_limit):
+        self.probe_limit, self.timed_limit, self.calls = probe_limit, timed_limit, []
+
+    def run(self, k, dur_us, policy, param=0):
+        self.calls.append(("run", k))
+        bad = k > (self.timed_limit if dur_us > 1600000 else self.probe_limit)
+        return dict(k=k, offered_req_s=k * 1650, on_time_per_s=k * 1650 * (0.5 if bad else 1.0),
+                    violation_frac=0.5 if bad else 0.0, utilisation_ppm=0)
+
+    def timed(self, k, policy, param, steps, warmup):
+        self.calls.append(("timed", k))
+        return self.run(k, steps * bench.PERIOD_US, policy, param)
+
+
+def test_capacity_search_doubles_then_bisects():
+    m = FakeMix(probe_limit=19.0, timed_limit=19.0)
+    k, probes = bench.Mix4.capacity(m, "dstack", (0, 0), 1.5)
+    ks = [p["k"] for p in probes]
+    assert ks[:6] == [1.0, 2.0, 4.0, 8.0, 16.0, 32.0]  # doubling until a probe fails
+    assert len(ks) == 9  # then three bisections on the geometric mean
+    assert 16.0 <= k <= 19.0 and all(p["violation_frac"] == 0.0 for p in probes if p["k"] <= k)
+    assert k == max(p["k"] for p in probes if p["violation_frac"] <= bench.VIOLATION_BAR)
+    # below 1: halving
+    k2, probes2 = bench.Mix4.capacity(FakeMix(0.3, 0.3), "temporal", 15000, 1.5)
+    assert [p["k"] for p in probes2][:3] == [1.0, 0.5, 0.25] and 0.25 <= k2 <= 0.3
+
+
+def test_timed_run_falls_back_to_the_next_passing_probe():
+    m = FakeMix(probe_limit=19.0, timed_limit=17.0)
+    k, probes = bench.Mix4.capacity(m, "dstack", (0, 0), 1.5)
+    entry = dict(k=k, probes=probes)
+    k_run, run = bench.confirm_capacity(m, "dstack", (0, 0), entry, 20, 3)
+    assert run["violation_frac"] <= bench.VIOLATION_BAR and k_run <= 17.0
+    assert entry["timed_k"][0] == k and entry["timed_k"][-1] == k_run
+    assert k_run == max(p["k"] for p in probes if p["k"] <= 17.0)
+    # a capacity that holds over the timed run is kept as it is
+    m2 = FakeMix(probe_limit=19.0, timed_limit=19.0)
+    k2, probes2 = bench.Mix4.capacity(m2, "dstack", (0, 0), 1.5)
+    e2 = dict(k=k2, probes=probes2)
+    assert bench.confirm_capacity(m2, "dstack", (0, 0), e2, 20, 3)[0] == k2 and e2["timed_k"] == [k2]
