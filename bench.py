@@ -815,7 +815,9 @@ def ideal_vs_dstack(ds, models, slos, batch, xs, ys, seconds=0.2, slot_us=1):
     dense = [list(range(0, hor, 20)) for _ in models]
     sim = ds.simulate(tabs, PERIOD_US, hor, dense)
     d_items = [mm["served"] for mm in sim["models"]]
-    return dict(slot_us=slot_us, seconds=seconds, kernel_sum_tables=[t["table"][b] for t, b in zip(tabs, batch)],
+    return dict(note="simulate mode on event-timed per-kernel durations; 1 us slots (these kernels last 5-50 us), "
+                     "so not like-for-like with the paper's 100 us slots over millisecond kernels",
+                slot_us=slot_us, seconds=seconds, kernel_sum_tables=[t["table"][b] for t, b in zip(tabs, batch)],
                 kernels=[len(im["dur"]) for im in ideal_models],
                 kernel_knee_slots_median=[sorted(im["slots"])[len(im["slots"]) // 2] for im in ideal_models],
                 forward_us_at_kernel_knees=[sum(im["dur"]) for im in ideal_models],
