@@ -627,18 +627,28 @@ class Mix4:
 def confirm_capacity(mix, policy, param, entry, steps, warmup):
     """The timed run at a policy's capacity must itself meet the bar (a probe
     near saturation can pass over its shorter trace): if it does not, it is
-    repeated at the next lower k that passed its probe.  Returns (k, run);
-    entry["timed_k"] lists the k tried."""
+    repeated at the next lower k that passed its probe, then once at the
+    geometric mean of that k and the failed one (kept if it meets the bar).
+    Returns (k, run); entry["timed_k"] lists the k tried."""
     k = entry["k"] if entry["k"] > 0 else 1.0
     run = mix.timed(k, policy, param, steps, warmup)
     tried = [k]
+    k_fail = None
     while run["violation_frac"] > VIOLATION_BAR:
+        k_fail = k
         lower = [p["k"] for p in entry["probes"] if p["violation_frac"] <= VIOLATION_BAR and p["k"] < k]
         if not lower:
             break
         k = max(lower)
         run = mix.timed(k, policy, param, steps, warmup)
         tried.append(k)
+    if k_fail is not None and run["violation_frac"] <= VIOLATION_BAR:
+        # one timed bisection step between the confirmed k and the failed one
+        mid = math.sqrt(k * k_fail)
+        run_mid = mix.timed(mid, policy, param, steps, warmup)
+        tried.append(mid)
+        if run_mid["violation_frac"] <= VIOLATION_BAR:
+            k, run = mid, run_mid
     entry["timed_k"] = tried
     return k, run
 

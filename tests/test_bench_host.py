@@ -85,8 +85,11 @@ def test_timed_run_falls_back_to_the_next_passing_probe():
     entry = dict(k=k, probes=probes)
     k_run, run = bench.confirm_capacity(m, "dstack", (0, 0), entry, 20, 3)
     assert run["violation_frac"] <= bench.VIOLATION_BAR and k_run <= 17.0
-    assert entry["timed_k"][0] == k and entry["timed_k"][-1] == k_run
-    assert k_run == max(p["k"] for p in probes if p["k"] <= 17.0)
+    assert entry["timed_k"][0] == k
+    lower = max(p["k"] for p in probes if p["k"] <= 17.0)
+    # the fallback probe, then one step between it and the failed k
+    assert entry["timed_k"][1] == lower and abs(entry["timed_k"][2] - (lower * k) ** 0.5) < 1e-9
+    assert k_run == (entry["timed_k"][2] if entry["timed_k"][2] <= 17.0 else lower)
     # a capacity that holds over the timed run is kept as it is
     m2 = FakeMix(probe_limit=19.0, timed_limit=19.0)
     k2, probes2 = bench.Mix4.capacity(m2, "dstack", (0, 0), 1.5)
