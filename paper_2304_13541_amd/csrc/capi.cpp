@@ -1020,8 +1020,8 @@ dstack_status dstack_op_lstm_layer(const void* x, int T, int B, int I, int H, co
     float* gx = static_cast<float*>(workspace);
     float* c = reinterpret_cast<float*>(static_cast<char*>(workspace) + ((size_t)T * B * 4 * H * 4 + 255) / 256 * 256);
     return lstm_layer_run(static_cast<const bf16*>(x), T, B, I, H, static_cast<const bf16*>(w_ih),
-                          static_cast<const bf16*>(w_hh), bias, static_cast<bf16*>(h_bf16), h_f32, gx, c, 256,
-                          (hipStream_t)stream, nullptr);
+                          static_cast<const bf16*>(w_hh), bias, static_cast<bf16*>(h_bf16), h_f32, gx, c,
+                          stream_cu_count((hipStream_t)stream), (hipStream_t)stream, nullptr);
   });
 }
 

@@ -160,21 +160,28 @@ dstack_status launch_fc(const bf16* x, int B, int I, const bf16* w, const float*
 // ----------------------------------------------------------- LSTM step ----
 // gates[b][g*H + j] = gx_t[b][g*H + j] + sum_k W_hh[g*H + j][k] * h_prev[b][k],
 // then c = f*c + i*g~, h = o*tanh(c) (gate order i, f, g, o; h_prev = 0 at t = 0).
-// Block: 4 hidden units, i.e. the 16 rows (gate, unit) = (row / 4, row % 4)
-// of one v_mfma_f32_16x16x32_bf16 A operand; wave w takes depth steps
-// [w*KSW, (w+1)*KSW) of 32 and loads all of its W_hh fragments before the
-// first MFMA.  B operand: h_prev rows (batch) read from L2.  Lane l ends with
-// gate l/16 of units 0..3 for batch column l%16; the four waves' partial sums
-// meet in LDS, where the 128 (unit, batch) cells are then updated by the
-// first 128 threads.
-template <int KSW>
+// Block: U groups of 4 hidden units; group u holds the 16 rows (gate, unit)
+// = (row / 4, row % 4) of one v_mfma_f32_16x16x32_bf16 A operand for units
+// j0 + 4u .. + 3.  Wave w takes depth steps [w*KSW, (w+1)*KSW) of 32 for all
+// U groups and loads all of its W_hh and h_prev fragments before the first
+// MFMA.  B operand: h_prev rows (batch) read from L2.  Lane l ends with gate
+// l/16 of a group's units 0..3 for batch column l%16; the four waves'
+// partial sums meet in LDS, where the 4U x B (unit, batch) cells are then
+// updated, 256 threads striding over them.
+// Every block reads all of h_prev (B x H) besides its 16U rows of W_hh, so U
+// sets the step's L2 -> CU bytes: larger U reads h_prev fewer times but
+// leaves fewer blocks for the CUs.  The per-row sums (waves added in order
+// 0..3, then the input projection) do not depend on U.
+template <int U, int KSW>
 __global__ __launch_bounds__(256) void lstm_step_kernel(const float* __restrict__ gx, const bf16* __restrict__ whh,
                                                         const bf16* __restrict__ hprev, float* __restrict__ c,
                                                         bf16* __restrict__ hnext, float* __restrict__ hf32, int B,
                                                         int H, int first) {
-  __shared__ float gs[4][2][16][16];  // [wave][batch tile][row = gate*4 + unit][batch column]
+  // [wave][batch tile][group][row = gate*4 + unit][batch column]
+  __shared__ float gs[4][2][U][16][16];
+  constexpr int CPT = (128 * U + 255) / 256;  // cells per thread (a cell = (unit, batch), batch < 32)
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int j0 = blockIdx.x * 4;
+  const int j0 = blockIdx.x * 4 * U;
   const int nmt = (B + 15) >> 4;
   const int nks = H >> 5;
   const int k0 = wave * KSW, k1 = min(nks, k0 + KSW);
@@ -182,24 +189,34 @@ __global__ __launch_bounds__(256) void lstm_step_kernel(const float* __restrict_
   const int koff = (lane >> 4) * 8;
   // the cell threads fetch their input-projection gates and cell state now,
   // so that these loads overlap the recurrent product
-  const int cu = tid >> 5, cb = tid & 31, cj = j0 + cu;  // unit, batch of a cell thread
-  const bool cell = tid < 128 && cb < B;
-  float gxv[4] = {0.f, 0.f, 0.f, 0.f}, cprev = 0.f;
-  if (cell) {
+  float gxv[CPT][4], cprev[CPT];
 #pragma unroll
-    for (int g = 0; g < 4; ++g) gxv[g] = gx[(long)cb * 4 * H + g * H + cj];
-    if (!first) cprev = c[(long)cb * H + cj];
+  for (int q = 0; q < CPT; ++q) {
+    const int cell = tid + 256 * q, ul = cell >> 5, cb = cell & 31, cj = j0 + ul;
+#pragma unroll
+    for (int g = 0; g < 4; ++g) gxv[q][g] = 0.f;
+    cprev[q] = 0.f;
+    if (ul < 4 * U && cb < B) {
+#pragma unroll
+      for (int g = 0; g < 4; ++g) gxv[q][g] = gx[(long)cb * 4 * H + g * H + cj];
+      if (!first) cprev[q] = c[(long)cb * H + cj];
+    }
   }
 
-  f32x4 acc[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+  f32x4 acc[U][2];
+#pragma unroll
+  for (int u = 0; u < U; ++u) acc[u][0] = acc[u][1] = f32x4{0.f, 0.f, 0.f, 0.f};
   if (!first && k0 < k1) {
-    const bf16* wrow = whh + (long)((row >> 2) * H + j0 + (row & 3)) * H;
-    bf16x8 a[KSW], bv[2][KSW];
+    bf16x8 a[U][KSW], bv[2][KSW];
 #pragma unroll
     for (int s = 0; s < KSW; ++s) {
       const int k = (k0 + s) * 32 + koff;
       const bool in = k0 + s < k1;
-      a[s] = in ? ld8(wrow + k) : bf16x8{};
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const bf16* wrow = whh + (long)((row >> 2) * H + j0 + 4 * u + (row & 3)) * H;
+        a[u][s] = in ? ld8(wrow + k) : bf16x8{};
+      }
 #pragma unroll
       for (int mt = 0; mt < 2; ++mt) {
         const int b = mt * 16 + (lane & 15);
@@ -209,28 +226,35 @@ __global__ __launch_bounds__(256) void lstm_step_kernel(const float* __restrict_
 #pragma unroll
     for (int s = 0; s < KSW; ++s)
 #pragma unroll
-      for (int mt = 0; mt < 2; ++mt)
-        if (mt < nmt) acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[s], bv[mt][s], acc[mt], 0, 0, 0);
+      for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int mt = 0; mt < 2; ++mt)
+          if (mt < nmt) acc[u][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[u][s], bv[mt][s], acc[u][mt], 0, 0, 0);
   }
   // C layout: lane holds rows 4*(lane/16) + i, column lane%16
 #pragma unroll
-  for (int mt = 0; mt < 2; ++mt)
+  for (int u = 0; u < U; ++u)
 #pragma unroll
-    for (int i = 0; i < 4; ++i) gs[wave][mt][4 * (lane >> 4) + i][lane & 15] = acc[mt][i];
+    for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) gs[wave][mt][u][4 * (lane >> 4) + i][lane & 15] = acc[u][mt][i];
   __syncthreads();
-  if (cell) {
-    const int mt = cb >> 4, bc = cb & 15;
+#pragma unroll
+  for (int q = 0; q < CPT; ++q) {
+    const int cell = tid + 256 * q, ul = cell >> 5, cb = cell & 31, cj = j0 + ul;
+    if (ul >= 4 * U || cb >= B) continue;
+    const int mt = cb >> 4, bc = cb & 15, u = ul >> 2, cu = ul & 3;
     float g4[4];
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
       const int r = g * 4 + cu;
-      g4[g] = gs[0][mt][r][bc] + gs[1][mt][r][bc] + gs[2][mt][r][bc] + gs[3][mt][r][bc] + gxv[g];
+      g4[g] = gs[0][mt][u][r][bc] + gs[1][mt][u][r][bc] + gs[2][mt][u][r][bc] + gs[3][mt][u][r][bc] + gxv[q][g];
     }
     const float ig = 1.f / (1.f + __expf(-g4[0]));
     const float fg = 1.f / (1.f + __expf(-g4[1]));
     const float gt = tanhf(g4[2]);
     const float og = 1.f / (1.f + __expf(-g4[3]));
-    const float cn = fg * cprev + ig * gt;
+    const float cn = fg * cprev[q] + ig * gt;
     const float hn = og * tanhf(cn);
     c[(long)cb * H + cj] = cn;
     hnext[(long)cb * H + cj] = (bf16)hn;
@@ -238,22 +262,54 @@ __global__ __launch_bounds__(256) void lstm_step_kernel(const float* __restrict_
   }
 }
 
+// Groups of 4 units per block for a step on n_cu CUs: the U in {1, 2, 4}
+// that gives the busiest CU the fewest bytes to load (its blocks' W_hh rows
+// plus one h_prev each); ties go to the smaller U (more blocks).
+int lstm_units_per_block(int B, int H, int n_cu) {
+  const long cus = n_cu > 0 ? n_cu : 256;
+  int best = 1;
+  long best_bytes = -1;
+  for (int u = 1; u <= 4; u *= 2) {
+    const long blocks = H / (4 * u);
+    const long per_cu = (blocks + cus - 1) / cus;
+    const long bytes = per_cu * (16L * u * H * 2 + (long)B * H * 2);
+    if (best_bytes < 0 || bytes < best_bytes) {
+      best = u;
+      best_bytes = bytes;
+    }
+  }
+  return best;
+}
+
+template <int U>
+static void launch_lstm_u(int ksw, dim3 grid, hipStream_t st, const float* gx_t, const bf16* w_hh,
+                          const bf16* h_prev, float* c, bf16* h_next, float* h_f32, int B, int H, int f) {
+  const dim3 blk(256);
+  if (ksw <= 2)
+    launch(lstm_step_kernel<U, 2>, grid, blk, 0, st, gx_t, w_hh, h_prev, c, h_next, h_f32, B, H, f);
+  else if (ksw <= 4)
+    launch(lstm_step_kernel<U, 4>, grid, blk, 0, st, gx_t, w_hh, h_prev, c, h_next, h_f32, B, H, f);
+  else if (ksw <= 8)
+    launch(lstm_step_kernel<U, 8>, grid, blk, 0, st, gx_t, w_hh, h_prev, c, h_next, h_f32, B, H, f);
+  else
+    launch(lstm_step_kernel<U, 16>, grid, blk, 0, st, gx_t, w_hh, h_prev, c, h_next, h_f32, B, H, f);
+}
+
 dstack_status launch_lstm_step(const float* gx_t, const bf16* w_hh, const bf16* h_prev, float* c, bf16* h_next,
-                               float* h_f32, int B, int H, bool first, hipStream_t st) {
+                               float* h_f32, int B, int H, bool first, int n_cu, hipStream_t st) {
   DS_CHECK(B >= 1 && B <= 32, DSTACK_E_UNSUPPORTED, "lstm: batch must be 1..32");
-  // depth is consumed in steps of 32; a block owns 4 hidden units
+  // depth is consumed in steps of 32; a block owns 4U hidden units (4U divides 32)
   DS_CHECK(H % 32 == 0 && H >= 32 && H <= 2048, DSTACK_E_UNSUPPORTED, "lstm: H must be a multiple of 32, <= 2048");
   const int nks = H / 32, ksw = (nks + 3) / 4;
-  dim3 grid(H / 4), blk(256);
+  const int u = lstm_units_per_block(B, H, n_cu);
+  const dim3 grid(H / (4 * u));
   const int f = first ? 1 : 0;
-  if (ksw <= 2)
-    launch(lstm_step_kernel<2>, grid, blk, 0, st, gx_t, w_hh, h_prev, c, h_next, h_f32, B, H, f);
-  else if (ksw <= 4)
-    launch(lstm_step_kernel<4>, grid, blk, 0, st, gx_t, w_hh, h_prev, c, h_next, h_f32, B, H, f);
-  else if (ksw <= 8)
-    launch(lstm_step_kernel<8>, grid, blk, 0, st, gx_t, w_hh, h_prev, c, h_next, h_f32, B, H, f);
+  if (u == 1)
+    launch_lstm_u<1>(ksw, grid, st, gx_t, w_hh, h_prev, c, h_next, h_f32, B, H, f);
+  else if (u == 2)
+    launch_lstm_u<2>(ksw, grid, st, gx_t, w_hh, h_prev, c, h_next, h_f32, B, H, f);
   else
-    launch(lstm_step_kernel<16>, grid, blk, 0, st, gx_t, w_hh, h_prev, c, h_next, h_f32, B, H, f);
+    launch_lstm_u<4>(ksw, grid, st, gx_t, w_hh, h_prev, c, h_next, h_f32, B, H, f);
   DS_HIP(hipGetLastError());
   return DSTACK_OK;
 }

@@ -763,7 +763,7 @@ dstack_status lstm_layer_run(const bf16* x, int T, int B, int I, int H, const bf
   for (int t = 0; t < T; ++t) {
     if (timer) timer->before();
     s = launch_lstm_step(gx + (size_t)t * B * 4 * H, w_hh, t ? h_bf16 + (size_t)(t - 1) * B * H : nullptr, c,
-                         h_bf16 + (size_t)t * B * H, h_f32 ? h_f32 + (size_t)t * B * H : nullptr, B, H, t == 0, st);
+                         h_bf16 + (size_t)t * B * H, h_f32 ? h_f32 + (size_t)t * B * H : nullptr, B, H, t == 0, n_cu, st);
     if (s != DSTACK_OK) return s;
     if (timer)
       timer->after(KC_LSTM, 2.0 * B * H * 4.0 * H,

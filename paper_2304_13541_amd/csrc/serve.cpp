@@ -46,8 +46,13 @@ struct Running {
 };
 
 // A GPU% change's new partition, created on a helper thread so that the
-// launcher keeps serving the other models meanwhile.
-using NewPartition = std::pair<dstack_status, dstack_partition>;
+// launcher keeps serving the other models meanwhile.  The error text is
+// carried back because dstack_last_error() is per thread.
+struct NewPartition {
+  dstack_status first = DSTACK_OK;
+  dstack_partition second = nullptr;
+  std::string err;
+};
 
 struct Resources {
   std::vector<dstack_partition> part;
@@ -270,10 +275,19 @@ dstack_status serve(const dstack_model* models, int n, const void* const* d_in, 
         res.part[i] = part[i] = nullptr;
         ls.unavailable(i);
         const int home = ls.home(i), dep = ls.deployed(i);
-        res.pending[i] = std::async(std::launch::async, [home, dep] {
-          dstack_partition np = nullptr;
-          const dstack_status s = dstack_partition_create_at(home, dep, &np);
-          return NewPartition{s, np};
+        int dev = 0;
+        DS_HIP(hipGetDevice(&dev));
+        res.pending[i] = std::async(std::launch::async, [home, dep, dev] {
+          NewPartition np;
+          const hipError_t e = hipSetDevice(dev);  // the helper starts on device 0
+          if (e != hipSuccess) {
+            np.first = DSTACK_E_HIP;
+            np.err = std::string("serve: hipSetDevice: ") + hipGetErrorString(e);
+            return np;
+          }
+          np.first = dstack_partition_create_at(home, dep, &np.second);
+          if (np.first != DSTACK_OK) np.err = dstack_last_error();
+          return np;
         });
       }
       st = fod_pass(te);
@@ -285,7 +299,7 @@ dstack_status serve(const dstack_model* models, int n, const void* const* d_in, 
           res.pending[i].wait_for(std::chrono::seconds(0)) != std::future_status::ready)
         continue;
       const NewPartition np = res.pending[i].get();
-      if (np.first != DSTACK_OK) return np.first;
+      if (np.first != DSTACK_OK) return fail(np.first, np.err);
       res.part[i] = part[i] = np.second;
       void* sp = nullptr;
       st = dstack_partition_query(np.second, nullptr, nullptr, &sp);

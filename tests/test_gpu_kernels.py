@@ -260,13 +260,16 @@ def test_lstm_layer(env, case):
     assert oracle.rel_err(gu.host(hb), h_ref) <= TOL
 
 
-@pytest.mark.parametrize("slots", [1, 3, 16])
-def test_lstm_layer_on_partitions(env, slots):
-    """The layer on CU-masked streams of 8, 24 and 128 CUs (256 blocks per
-    step, from 32 down to 2 per CU); same bar as above."""
+@pytest.mark.parametrize("slots,shape", [(1, (50, 32, 512, 1024)), (3, (50, 32, 512, 1024)), (16, (50, 32, 512, 1024)),
+                                         (1, (7, 17, 40, 96)), (3, (5, 3, 64, 64)), (16, (6, 17, 72, 1024))])
+def test_lstm_layer_on_partitions(env, slots, shape):
+    """The layer on CU-masked streams of 8, 24 and 128 CUs: the step launch
+    is chosen for the stream's CUs (H = 1024, B = 32: 16 hidden units per
+    block on 8 and 24 CUs, 8 on 128, 4 on the whole GPU; the small shapes
+    take ragged batches through the wider blocks); same bar as above."""
     ds, gu, inputs, oracle, torch = env
-    T, B, I, H = 50, 32, 512, 1024
-    print("lstm layer on %d slots" % slots, flush=True)
+    T, B, I, H = shape
+    print("lstm layer %s on %d slots" % (shape, slots), flush=True)
     xb = inputs.normal_bf16(22, (T, B, I))
     a = 1.0 / np.sqrt(H)
     wih = inputs.uniform_bf16(23, (4 * H, I), -a, a)
