@@ -634,7 +634,10 @@ dstack_status dstack_serve(const dstack_model* models, int n_models, const void*
  *   = 0); x [T][B][I] bf16; w_ih [4H][I], w_hh [4H][H] bf16; bias [4H]
  *   fp32 (= b_ih + b_hh); h_bf16 [T][B][H] receives h rounded to bf16;
  *   h_f32 [T][B][H] (may be NULL) receives h in fp32; B in 1..32,
- *   H % 32 == 0 and H <= 2048, I % 8 == 0; workspace needs lstm_workspace_bytes.
+ *   H % 32 == 0 and H <= 2048, I % 8 == 0; workspace (device, 256-byte
+ *   aligned, caller owned) needs lstm_workspace_bytes(T, B, H) bytes: the
+ *   input projections, the cell state, and copies of W_hh and of h(t-1) in
+ *   the recurrent product's fragment order (W_hh is repacked on each call).
  *   The recurrent step's launch (hidden units per workgroup) is chosen for
  *   the CUs of the stream's CU mask; the result does not depend on it. */
 dstack_status dstack_op_conv2d(const void* x, int N, int H, int W, int C, const void* w, int K, int R, int S,

@@ -1005,9 +1005,13 @@ dstack_status dstack_op_avgpool(const void* x, int N, int H, int W, int C, void*
   });
 }
 
+// gx [T][B][4H] fp32 | c [B][H] fp32 | W_hh in fragment order [4H][H] bf16 |
+// h(t-1), h(t) in fragment order [2][B][H] bf16, each part 256-byte aligned
+static size_t align256z(size_t n) { return (n + 255) / 256 * 256; }
 size_t dstack_lstm_workspace_bytes(int T, int B, int H) {
   if (T <= 0 || B <= 0 || H <= 0) return 0;
-  return ((size_t)T * B * 4 * H * 4 + 255) / 256 * 256 + (size_t)B * H * 4;
+  return align256z((size_t)T * B * 4 * H * 4) + align256z((size_t)B * H * 4) + align256z((size_t)4 * H * H * 2) +
+         (size_t)2 * B * H * 2;
 }
 
 dstack_status dstack_op_lstm_layer(const void* x, int T, int B, int I, int H, const void* w_ih, const void* w_hh,
@@ -1017,10 +1021,16 @@ dstack_status dstack_op_lstm_layer(const void* x, int T, int B, int I, int H, co
     DS_CHECK(T >= 1 && I % 8 == 0 && I > 0, DSTACK_E_UNSUPPORTED, "lstm_layer: T >= 1, I % 8 == 0");
     DS_CHECK(B >= 1 && B <= 32, DSTACK_E_UNSUPPORTED, "lstm_layer: batch must be 1..32");
     DS_CHECK(H >= 32 && H % 32 == 0 && H <= 2048, DSTACK_E_UNSUPPORTED, "lstm_layer: H must be a multiple of 32, <= 2048");
-    float* gx = static_cast<float*>(workspace);
-    float* c = reinterpret_cast<float*>(static_cast<char*>(workspace) + ((size_t)T * B * 4 * H * 4 + 255) / 256 * 256);
+    char* p = static_cast<char*>(workspace);
+    float* gx = reinterpret_cast<float*>(p);
+    p += align256z((size_t)T * B * 4 * H * 4);
+    float* c = reinterpret_cast<float*>(p);
+    p += align256z((size_t)B * H * 4);
+    bf16* wp = reinterpret_cast<bf16*>(p);
+    p += align256z((size_t)4 * H * H * 2);
+    bf16* hp = reinterpret_cast<bf16*>(p);
     return lstm_layer_run(static_cast<const bf16*>(x), T, B, I, H, static_cast<const bf16*>(w_ih),
-                          static_cast<const bf16*>(w_hh), bias, static_cast<bf16*>(h_bf16), h_f32, gx, c,
+                          static_cast<const bf16*>(w_hh), bias, static_cast<bf16*>(h_bf16), h_f32, gx, c, wp, hp,
                           stream_cu_count((hipStream_t)stream), (hipStream_t)stream, nullptr);
   });
 }

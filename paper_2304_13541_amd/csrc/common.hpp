@@ -166,8 +166,9 @@ dstack_status launch_layernorm(const bf16* x, int rows, int H, const float* gamm
 dstack_status launch_attention(const bf16* qkv, int B, int T, int heads, int dh, bf16* out, hipStream_t st);
 dstack_status launch_conv2d_rgb(const bf16* x, int N, int H, int W, const bf16* w4, int K, int R, int stride, int pad,
                                 const float* scale, const float* shift, int act, bf16* y, hipStream_t st);
-dstack_status launch_lstm_step(const float* gx_t, const bf16* w_hh, const bf16* h_prev, float* c, bf16* h_next,
-                               float* h_f32, int B, int H, bool first, int n_cu, hipStream_t st);
+dstack_status launch_lstm_pack_whh(const bf16* w_hh, bf16* wp, int H, hipStream_t st);
+dstack_status launch_lstm_step(const float* gx_t, const bf16* wp, const bf16* hp_prev, float* c, bf16* h_next,
+                               bf16* hp_next, float* h_f32, int B, int H, bool first, int n_cu, hipStream_t st);
 int lstm_units_per_block(int B, int H, int n_cu);
 dstack_status launch_probe(uint32_t* d_out, int n_blocks, hipStream_t st);
 

@@ -160,28 +160,48 @@ dstack_status launch_fc(const bf16* x, int B, int I, const bf16* w, const float*
 // ----------------------------------------------------------- LSTM step ----
 // gates[b][g*H + j] = gx_t[b][g*H + j] + sum_k W_hh[g*H + j][k] * h_prev[b][k],
 // then c = f*c + i*g~, h = o*tanh(c) (gate order i, f, g, o; h_prev = 0 at t = 0).
-// Block: U groups of 4 hidden units; group u holds the 16 rows (gate, unit)
-// = (row / 4, row % 4) of one v_mfma_f32_16x16x32_bf16 A operand for units
-// j0 + 4u .. + 3.  Wave w takes depth steps [w*KSW, (w+1)*KSW) of 32 for all
-// U groups and loads all of its W_hh and h_prev fragments before the first
-// MFMA.  B operand: h_prev rows (batch) read from L2.  Lane l ends with gate
-// l/16 of a group's units 0..3 for batch column l%16; the four waves'
-// partial sums meet in LDS, where the 4U x B (unit, batch) cells are then
-// updated, 256 threads striding over them.
-// Every block reads all of h_prev (B x H) besides its 16U rows of W_hh, so U
-// sets the step's L2 -> CU bytes: larger U reads h_prev fewer times but
-// leaves fewer blocks for the CUs.  The per-row sums (waves added in order
-// 0..3, then the input projection) do not depend on U.
+// Operands in MFMA fragment order, so that every wave load reads 1 KB of
+// consecutive bytes (whole cache lines) rather than 16 half lines of 16
+// different rows:
+//  - W_hh packed once per layer run: row tile rt (the 16 rows (gate, unit) =
+//    (r / 4, 4 rt + r % 4) of units 4rt .. 4rt+3) and depth step s (32 deep)
+//    form a 16 x 32 block at ((rt * H/32 + s) * 16 + r) * 32;
+//  - h(t-1) as written by the previous step: depth step s of batch row b at
+//    (s * B + b) * 32.
+// Block: U row tiles, i.e. 4U hidden units j0 .. j0 + 4U - 1.  Wave w takes
+// depth steps [w*KSW, (w+1)*KSW) for all U row tiles and loads all of its
+// W_hh and h fragments before the first MFMA.  Lane l ends with gate l/16 of
+// a row tile's units for batch column l%16; the four waves' partial sums
+// meet in LDS, where the 4U x B (unit, batch) cells are then updated, 256
+// threads striding over them; each cell writes h in bf16 both row-major (the
+// layer's output) and packed (the next step's operand), c in fp32.
+// Every block reads all of h(t-1) (B x H) besides its 16U rows of W_hh, so U
+// sets the step's L2 -> CU bytes: larger U reads h fewer times but leaves
+// fewer blocks for the CUs.  The per-row sums (waves added in order 0..3,
+// then the input projection) do not depend on U.
+__global__ __launch_bounds__(256) void lstm_pack_whh_kernel(const bf16* __restrict__ w, bf16* __restrict__ wp,
+                                                            int H) {
+  const long v = (long)blockIdx.x * 256 + threadIdx.x;  // 16-byte vector of wp
+  if (v >= (long)H * H / 2) return;                     // 4H x H elements, 8 per vector
+  const int nks = H >> 5;
+  const int q = (int)(v & 3);  // which 8 of the 32 depth values
+  const int r = (int)((v >> 2) & 15);
+  const long ts = v >> 6;  // rt * nks + s
+  const int rt = (int)(ts / nks), st = (int)(ts - (long)rt * nks);
+  const long src = (long)((r >> 2) * H + 4 * rt + (r & 3)) * H + st * 32 + q * 8;
+  *reinterpret_cast<uint4*>(wp + v * 8) = *reinterpret_cast<const uint4*>(w + src);
+}
+
 template <int U, int KSW>
-__global__ __launch_bounds__(256) void lstm_step_kernel(const float* __restrict__ gx, const bf16* __restrict__ whh,
-                                                        const bf16* __restrict__ hprev, float* __restrict__ c,
-                                                        bf16* __restrict__ hnext, float* __restrict__ hf32, int B,
-                                                        int H, int first) {
-  // [wave][batch tile][group][row = gate*4 + unit][batch column]
+__global__ __launch_bounds__(256) void lstm_step_kernel(const float* __restrict__ gx, const bf16* __restrict__ wp,
+                                                        const bf16* __restrict__ hp_prev, float* __restrict__ c,
+                                                        bf16* __restrict__ hnext, bf16* __restrict__ hp_next,
+                                                        float* __restrict__ hf32, int B, int H, int first) {
+  // [wave][batch tile][row tile][row = gate*4 + unit][batch column]
   __shared__ float gs[4][2][U][16][16];
   constexpr int CPT = (128 * U + 255) / 256;  // cells per thread (a cell = (unit, batch), batch < 32)
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int j0 = blockIdx.x * 4 * U;
+  const int rt0 = blockIdx.x * U, j0 = 4 * rt0;
   const int nmt = (B + 15) >> 4;
   const int nks = H >> 5;
   const int k0 = wave * KSW, k1 = min(nks, k0 + KSW);
@@ -210,17 +230,14 @@ __global__ __launch_bounds__(256) void lstm_step_kernel(const float* __restrict_
     bf16x8 a[U][KSW], bv[2][KSW];
 #pragma unroll
     for (int s = 0; s < KSW; ++s) {
-      const int k = (k0 + s) * 32 + koff;
       const bool in = k0 + s < k1;
 #pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const bf16* wrow = whh + (long)((row >> 2) * H + j0 + 4 * u + (row & 3)) * H;
-        a[u][s] = in ? ld8(wrow + k) : bf16x8{};
-      }
+      for (int u = 0; u < U; ++u)
+        a[u][s] = in ? ld8(wp + ((long)((rt0 + u) * nks + k0 + s) * 16 + row) * 32 + koff) : bf16x8{};
 #pragma unroll
       for (int mt = 0; mt < 2; ++mt) {
         const int b = mt * 16 + (lane & 15);
-        bv[mt][s] = (in && mt < nmt && b < B) ? ld8(hprev + (long)b * H + k) : bf16x8{};
+        bv[mt][s] = (in && mt < nmt && b < B) ? ld8(hp_prev + ((long)(k0 + s) * B + b) * 32 + koff) : bf16x8{};
       }
     }
 #pragma unroll
@@ -257,7 +274,9 @@ __global__ __launch_bounds__(256) void lstm_step_kernel(const float* __restrict_
     const float cn = fg * cprev[q] + ig * gt;
     const float hn = og * tanhf(cn);
     c[(long)cb * H + cj] = cn;
-    hnext[(long)cb * H + cj] = (bf16)hn;
+    const bf16 hb = (bf16)hn;
+    hnext[(long)cb * H + cj] = hb;
+    hp_next[((long)(cj >> 5) * B + cb) * 32 + (cj & 31)] = hb;
     if (hf32) hf32[(long)cb * H + cj] = hn;
   }
 }
@@ -282,34 +301,49 @@ int lstm_units_per_block(int B, int H, int n_cu) {
 }
 
 template <int U>
-static void launch_lstm_u(int ksw, dim3 grid, hipStream_t st, const float* gx_t, const bf16* w_hh,
-                          const bf16* h_prev, float* c, bf16* h_next, float* h_f32, int B, int H, int f) {
+static void launch_lstm_u(int ksw, dim3 grid, hipStream_t st, const float* gx_t, const bf16* wp, const bf16* hp_prev,
+                          float* c, bf16* h_next, bf16* hp_next, float* h_f32, int B, int H, int f) {
   const dim3 blk(256);
   if (ksw <= 2)
-    launch(lstm_step_kernel<U, 2>, grid, blk, 0, st, gx_t, w_hh, h_prev, c, h_next, h_f32, B, H, f);
+    launch(lstm_step_kernel<U, 2>, grid, blk, 0, st, gx_t, wp, hp_prev, c, h_next, hp_next, h_f32, B, H, f);
   else if (ksw <= 4)
-    launch(lstm_step_kernel<U, 4>, grid, blk, 0, st, gx_t, w_hh, h_prev, c, h_next, h_f32, B, H, f);
+    launch(lstm_step_kernel<U, 4>, grid, blk, 0, st, gx_t, wp, hp_prev, c, h_next, hp_next, h_f32, B, H, f);
   else if (ksw <= 8)
-    launch(lstm_step_kernel<U, 8>, grid, blk, 0, st, gx_t, w_hh, h_prev, c, h_next, h_f32, B, H, f);
+    launch(lstm_step_kernel<U, 8>, grid, blk, 0, st, gx_t, wp, hp_prev, c, h_next, hp_next, h_f32, B, H, f);
   else
-    launch(lstm_step_kernel<U, 16>, grid, blk, 0, st, gx_t, w_hh, h_prev, c, h_next, h_f32, B, H, f);
+    launch(lstm_step_kernel<U, 16>, grid, blk, 0, st, gx_t, wp, hp_prev, c, h_next, hp_next, h_f32, B, H, f);
 }
 
-dstack_status launch_lstm_step(const float* gx_t, const bf16* w_hh, const bf16* h_prev, float* c, bf16* h_next,
-                               float* h_f32, int B, int H, bool first, int n_cu, hipStream_t st) {
+static dstack_status lstm_check(int B, int H) {
   DS_CHECK(B >= 1 && B <= 32, DSTACK_E_UNSUPPORTED, "lstm: batch must be 1..32");
   // depth is consumed in steps of 32; a block owns 4U hidden units (4U divides 32)
   DS_CHECK(H % 32 == 0 && H >= 32 && H <= 2048, DSTACK_E_UNSUPPORTED, "lstm: H must be a multiple of 32, <= 2048");
+  return DSTACK_OK;
+}
+
+dstack_status launch_lstm_pack_whh(const bf16* w_hh, bf16* wp, int H, hipStream_t st) {
+  dstack_status s = lstm_check(1, H);
+  if (s != DSTACK_OK) return s;
+  const long vecs = (long)H * H / 2;
+  launch(lstm_pack_whh_kernel, dim3((unsigned)((vecs + 255) / 256)), dim3(256), 0, st, w_hh, wp, H);
+  DS_HIP(hipGetLastError());
+  return DSTACK_OK;
+}
+
+dstack_status launch_lstm_step(const float* gx_t, const bf16* wp, const bf16* hp_prev, float* c, bf16* h_next,
+                               bf16* hp_next, float* h_f32, int B, int H, bool first, int n_cu, hipStream_t st) {
+  dstack_status s = lstm_check(B, H);
+  if (s != DSTACK_OK) return s;
   const int nks = H / 32, ksw = (nks + 3) / 4;
   const int u = lstm_units_per_block(B, H, n_cu);
   const dim3 grid(H / (4 * u));
   const int f = first ? 1 : 0;
   if (u == 1)
-    launch_lstm_u<1>(ksw, grid, st, gx_t, w_hh, h_prev, c, h_next, h_f32, B, H, f);
+    launch_lstm_u<1>(ksw, grid, st, gx_t, wp, hp_prev, c, h_next, hp_next, h_f32, B, H, f);
   else if (u == 2)
-    launch_lstm_u<2>(ksw, grid, st, gx_t, w_hh, h_prev, c, h_next, h_f32, B, H, f);
+    launch_lstm_u<2>(ksw, grid, st, gx_t, wp, hp_prev, c, h_next, hp_next, h_f32, B, H, f);
   else
-    launch_lstm_u<4>(ksw, grid, st, gx_t, w_hh, h_prev, c, h_next, h_f32, B, H, f);
+    launch_lstm_u<4>(ksw, grid, st, gx_t, wp, hp_prev, c, h_next, hp_next, h_f32, B, H, f);
   DS_HIP(hipGetLastError());
   return DSTACK_OK;
 }

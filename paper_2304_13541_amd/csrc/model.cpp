@@ -638,7 +638,7 @@ dstack_status get_workspace(Model& m, int pid, int n_cu, hipStream_t st, Workspa
   total += align256(sk);
   const size_t cnt_off = total;
   if (sk) total += align256(SPLITK_TILE_COUNTERS * sizeof(unsigned));
-  size_t gx_off = 0, c_off = 0, h0_off = 0, h1_off = 0;
+  size_t gx_off = 0, c_off = 0, h0_off = 0, h1_off = 0, wp_off = 0, hp_off = 0;
   if (m.is_lstm) {
     gx_off = total;
     total += align256((size_t)m.lstm_T * m.max_batch * 4 * m.lstm_H * 4);
@@ -648,6 +648,10 @@ dstack_status get_workspace(Model& m, int pid, int n_cu, hipStream_t st, Workspa
     total += align256((size_t)m.lstm_T * m.max_batch * m.lstm_H * 2);
     h1_off = total;
     total += align256((size_t)m.lstm_T * m.max_batch * m.lstm_H * 2);
+    wp_off = total;
+    total += align256((size_t)4 * m.lstm_H * m.lstm_H * 2);
+    hp_off = total;
+    total += align256((size_t)2 * m.max_batch * m.lstm_H * 2);
   }
   DS_HIP(hipMalloc(&w->base, total));
   w->bytes = total;
@@ -672,6 +676,8 @@ dstack_status get_workspace(Model& m, int pid, int n_cu, hipStream_t st, Workspa
     w->lstm_c = (float*)(base + c_off);
     w->lstm_h[0] = (bf16*)(base + h0_off);
     w->lstm_h[1] = (bf16*)(base + h1_off);
+    w->lstm_wp = (bf16*)(base + wp_off);
+    w->lstm_hp = (bf16*)(base + hp_off);
   }
   *out = w.get();
   m.ws[pid] = std::move(w);
@@ -750,8 +756,8 @@ static double conv_bytes(const Op& op, int b) {
 }
 
 dstack_status lstm_layer_run(const bf16* x, int T, int B, int I, int H, const bf16* w_ih, const bf16* w_hh,
-                             const float* bias, bf16* h_bf16, float* h_f32, float* gx, float* c, int n_cu,
-                             hipStream_t st, KernelTimer* timer) {
+                             const float* bias, bf16* h_bf16, float* h_f32, float* gx, float* c, bf16* wp,
+                             bf16* hp, int n_cu, hipStream_t st, KernelTimer* timer) {
   // input projection of all steps at once: gx[t*B + b][:] = W_ih x + b_ih + b_hh (fp32)
   if (timer) timer->before();
   dstack_status s = launch_conv2d_ws(x, T * B, 1, 1, I, w_ih, 4 * H, 1, 1, 1, 0, nullptr, bias, nullptr, ACT_NONE,
@@ -760,14 +766,21 @@ dstack_status lstm_layer_run(const bf16* x, int T, int B, int I, int H, const bf
   if (timer)
     timer->after(KC_MFMA, 2.0 * T * B * I * 4.0 * H,
                  (double)T * B * I * 2 + 4.0 * H * I * 2 + (double)T * B * 4 * H * 4, T * B, 4 * H, I);
+  // W_hh in the fragment order of the recurrent product
+  if (timer) timer->before();
+  s = launch_lstm_pack_whh(w_hh, wp, H, st);
+  if (s != DSTACK_OK) return s;
+  if (timer) timer->after(KC_GLUE, 0.0, 2.0 * 4.0 * H * H * 2, 0, 0, 0);
   for (int t = 0; t < T; ++t) {
     if (timer) timer->before();
-    s = launch_lstm_step(gx + (size_t)t * B * 4 * H, w_hh, t ? h_bf16 + (size_t)(t - 1) * B * H : nullptr, c,
-                         h_bf16 + (size_t)t * B * H, h_f32 ? h_f32 + (size_t)t * B * H : nullptr, B, H, t == 0, n_cu, st);
+    bf16* hp_t = hp + (size_t)(t & 1) * B * H;
+    const bf16* hp_prev = hp + (size_t)((t + 1) & 1) * B * H;
+    s = launch_lstm_step(gx + (size_t)t * B * 4 * H, wp, t ? hp_prev : nullptr, c, h_bf16 + (size_t)t * B * H, hp_t,
+                         h_f32 ? h_f32 + (size_t)t * B * H : nullptr, B, H, t == 0, n_cu, st);
     if (s != DSTACK_OK) return s;
     if (timer)
       timer->after(KC_LSTM, 2.0 * B * H * 4.0 * H,
-                   4.0 * H * H * 2 + (double)B * H * 2 + (double)B * 4 * H * 4 + 2.0 * B * H * 4 + (double)B * H * 2 +
+                   4.0 * H * H * 2 + (double)B * H * 2 + (double)B * 4 * H * 4 + 2.0 * B * H * 4 + 2.0 * B * H * 2 +
                        (h_f32 ? (double)B * H * 4 : 0.0),
                    B, 4 * H, H);
   }
@@ -796,7 +809,7 @@ dstack_status forward(Model& m, int batch, const void* d_in, void* d_out, Worksp
       bf16* hb = op.in == BUF_IN ? ws.lstm_h[0] : ws.lstm_h[1];
       float* hf = op.out == BUF_OUT ? (float*)d_out : nullptr;
       s = lstm_layer_run(x, op.T, batch, op.I, op.Hd, m.d_w + op.wih_off, m.d_w + op.whh_off, f32 + op.bias_off, hb, hf,
-                         ws.lstm_gx, ws.lstm_c, n_cu, st, timer);
+                         ws.lstm_gx, ws.lstm_c, ws.lstm_wp, ws.lstm_hp, n_cu, st, timer);
       if (s != DSTACK_OK) return s;
       continue;
     }

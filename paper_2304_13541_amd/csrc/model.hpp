@@ -78,6 +78,8 @@ struct Workspace {
   float* lstm_gx = nullptr;
   float* lstm_c = nullptr;
   bf16* lstm_h[2] = {nullptr, nullptr};
+  bf16* lstm_wp = nullptr;  // W_hh of the running layer in fragment order (4H x H)
+  bf16* lstm_hp = nullptr;  // h(t-1), h(t) in fragment order (2 x max batch x H)
   std::atomic<bool> busy{false};
   // captured forward passes, keyed by (batch, input, output, CUs of the
   // partition); replayed with one hipGraphLaunch
@@ -176,7 +178,7 @@ dstack_status launch_conv2d_ws(const bf16* x, int N, int H, int W, int C, const 
                                int act, void* y, bool out_fp32, int n_cu, float* splitk_ws, size_t splitk_bytes,
                                unsigned* tile_counters, hipStream_t st);
 dstack_status lstm_layer_run(const bf16* x, int T, int B, int I, int H, const bf16* w_ih, const bf16* w_hh,
-                             const float* bias, bf16* h_bf16, float* h_f32, float* gx, float* c, int n_cu,
-                             hipStream_t st, KernelTimer* timer);
+                             const float* bias, bf16* h_bf16, float* h_f32, float* gx, float* c, bf16* wp,
+                             bf16* hp, int n_cu, hipStream_t st, KernelTimer* timer);
 
 }  // namespace dstack
