@@ -1030,8 +1030,8 @@ dstack_status dstack_op_lstm_layer(const void* x, int T, int B, int I, int H, co
     p += align256z((size_t)4 * H * H * 2);
     bf16* hp = reinterpret_cast<bf16*>(p);
     return lstm_layer_run(static_cast<const bf16*>(x), T, B, I, H, static_cast<const bf16*>(w_ih),
-                          static_cast<const bf16*>(w_hh), bias, static_cast<bf16*>(h_bf16), h_f32, gx, c, wp, hp,
-                          stream_cu_count((hipStream_t)stream), (hipStream_t)stream, nullptr);
+                          static_cast<const bf16*>(w_hh), nullptr, bias, static_cast<bf16*>(h_bf16), h_f32, gx, c,
+                          wp, hp, stream_cu_count((hipStream_t)stream), (hipStream_t)stream, nullptr);
   });
 }
 

@@ -148,10 +148,11 @@ dstack_status launch_conv2d(const bf16* x, int N, int H, int W, int C, const bf1
 dstack_status launch_dwconv3x3(const bf16* x, int N, int H, int W, int C, const bf16* w_rsc, int stride,
                                const float* scale, const float* shift, int act, bf16* y, hipStream_t st);
 // ws: fp32 partial sums of a depth split (fc_workspace_bytes for n_cu CUs);
-// NULL or too small runs fewer splits.
+// NULL or too small runs fewer splits.  packed: w in MFMA fragment order
+// (as a model packs its FC weights at load), else row-major [O][I].
 size_t fc_workspace_bytes(int B, int I, int O, int n_cu);
 dstack_status launch_fc(const bf16* x, int B, int I, const bf16* w, const float* bias, int O, int act, void* y,
-                        bool out_fp32, int n_cu, float* ws, size_t ws_bytes, hipStream_t st);
+                        bool out_fp32, int n_cu, float* ws, size_t ws_bytes, hipStream_t st, bool packed = false);
 dstack_status launch_maxpool(const bf16* x, int N, int H, int W, int C, int k, int stride, int pad, bf16* y,
                              hipStream_t st);
 dstack_status launch_avgpool(const bf16* x, int N, int H, int W, int C, bf16* y, hipStream_t st);

@@ -28,16 +28,21 @@ __device__ __forceinline__ bf16x8 ld8(const bf16* p) { return *reinterpret_cast<
 // are dropped at the end; depth past I reads nothing.  The 4 waves' tiles are
 // summed through LDS; with one split the block applies bias and activation,
 // otherwise it stores fp32 partial sums [split][B][O] for fc_reduce_kernel.
+// PK: the weights come in MFMA fragment order (a model's FC layers, packed
+// at load): row tile ot and depth step s form a 16 x 32 block at
+// ((ot * ceil(I/32) + s) * 16 + r) * 32, zero past O and I, so that a wave's
+// load of a step reads 1 KB of consecutive bytes rather than 64-byte pieces
+// of 16 rows.
 constexpr int FC_CH = 8;
 
-template <int NT>
+template <int NT, bool PK>
 __device__ __forceinline__ void fc_load(const bf16* wrow, const bf16* const* xrow, int st, int ke, int I, int g,
                                         bf16x8 (&a)[FC_CH], bf16x8 (&bv)[FC_CH][NT]) {
 #pragma unroll
   for (int j = 0; j < FC_CH; ++j) {
     const int k = (st + j) * 32 + g * 8;
     const bool in = st + j < ke && k < I;
-    a[j] = in ? ld8(wrow + k) : bf16x8{};
+    a[j] = in ? ld8(PK ? wrow + (long)(st + j) * 512 : wrow + k) : bf16x8{};
 #pragma unroll
     for (int t = 0; t < NT; ++t) bv[j][t] = in ? ld8(xrow[t] + k) : bf16x8{};
   }
@@ -51,7 +56,7 @@ __device__ __forceinline__ void fc_mma(const bf16x8 (&a)[FC_CH], const bf16x8 (&
     for (int t = 0; t < NT; ++t) acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[j], bv[j][t], acc[t], 0, 0, 0);
 }
 
-template <int NT>
+template <int NT, bool PK>
 __global__ __launch_bounds__(256) void fc_kernel(const bf16* __restrict__ x, int B, int I, const bf16* __restrict__ w,
                                                  const float* __restrict__ bias, int O, int act, void* y, int out_f32,
                                                  float* __restrict__ part, int steps_per_split) {
@@ -64,7 +69,9 @@ __global__ __launch_bounds__(256) void fc_kernel(const bf16* __restrict__ x, int
   const int per = (kb1 - kb0 + 3) >> 2;
   const int ks = kb0 + wave * per, ke = min(kb1, ks + per);
 
-  const bf16* wrow = w + (long)min(o0 + (lane & 15), O - 1) * I;
+  // the lane's weight row (PK: its row and depth quarter of the tile's first step)
+  const bf16* wrow = PK ? w + ((long)blockIdx.x * nks * 16 + (lane & 15)) * 32 + g * 8
+                        : w + (long)min(o0 + (lane & 15), O - 1) * I;
   const bf16* xrow[NT];
 #pragma unroll
   for (int t = 0; t < NT; ++t) xrow[t] = x + (long)min(t * 16 + (lane & 15), B - 1) * I;
@@ -74,11 +81,11 @@ __global__ __launch_bounds__(256) void fc_kernel(const bf16* __restrict__ x, int
   for (int t = 0; t < NT; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
   if (ks < ke) {
     bf16x8 a0[FC_CH], b0[FC_CH][NT], a1[FC_CH], b1[FC_CH][NT];
-    fc_load<NT>(wrow, xrow, ks, ke, I, g, a0, b0);
+    fc_load<NT, PK>(wrow, xrow, ks, ke, I, g, a0, b0);
     for (int st = ks; st < ke; st += 2 * FC_CH) {
-      if (st + FC_CH < ke) fc_load<NT>(wrow, xrow, st + FC_CH, ke, I, g, a1, b1);
+      if (st + FC_CH < ke) fc_load<NT, PK>(wrow, xrow, st + FC_CH, ke, I, g, a1, b1);
       fc_mma<NT>(a0, b0, acc);
-      if (st + 2 * FC_CH < ke) fc_load<NT>(wrow, xrow, st + 2 * FC_CH, ke, I, g, a0, b0);
+      if (st + 2 * FC_CH < ke) fc_load<NT, PK>(wrow, xrow, st + 2 * FC_CH, ke, I, g, a0, b0);
       if (st + FC_CH < ke) fc_mma<NT>(a1, b1, acc);
     }
   }
@@ -134,7 +141,7 @@ size_t fc_workspace_bytes(int B, int I, int O, int n_cu) {
 }
 
 dstack_status launch_fc(const bf16* x, int B, int I, const bf16* w, const float* bias, int O, int act, void* y,
-                        bool out_fp32, int n_cu, float* ws, size_t ws_bytes, hipStream_t st) {
+                        bool out_fp32, int n_cu, float* ws, size_t ws_bytes, hipStream_t st, bool packed) {
   DS_CHECK(B >= 1 && B <= 32, DSTACK_E_UNSUPPORTED, "fc: batch must be 1..32");
   DS_CHECK(I % 8 == 0 && I > 0 && O > 0, DSTACK_E_UNSUPPORTED, "fc: I must be a positive multiple of 8");
   DS_CHECK((long)O * I < (1L << 40) && (long)B * O < (1L << 30), DSTACK_E_UNSUPPORTED, "fc: too large");
@@ -145,10 +152,16 @@ dstack_status launch_fc(const bf16* x, int B, int I, const bf16* w, const float*
   s = (nks + sps - 1) / sps;  // no empty split
   dim3 grid((O + 15) / 16, s);
   const int f = out_fp32 ? 1 : 0;
-  if (B <= 16)
-    launch(fc_kernel<1>, grid, dim3(256), 0, st, x, B, I, w, bias, O, act, y, f, ws, sps);
-  else
-    launch(fc_kernel<2>, grid, dim3(256), 0, st, x, B, I, w, bias, O, act, y, f, ws, sps);
+  if (packed) {
+    if (B <= 16)
+      launch(fc_kernel<1, true>, grid, dim3(256), 0, st, x, B, I, w, bias, O, act, y, f, ws, sps);
+    else
+      launch(fc_kernel<2, true>, grid, dim3(256), 0, st, x, B, I, w, bias, O, act, y, f, ws, sps);
+  } else if (B <= 16) {
+    launch(fc_kernel<1, false>, grid, dim3(256), 0, st, x, B, I, w, bias, O, act, y, f, ws, sps);
+  } else {
+    launch(fc_kernel<2, false>, grid, dim3(256), 0, st, x, B, I, w, bias, O, act, y, f, ws, sps);
+  }
   DS_HIP(hipGetLastError());
   if (s > 1) {
     launch(fc_reduce_kernel, dim3((B * O + 255) / 256), dim3(256), 0, st, ws, s, B, O, bias, act, y, f);

@@ -582,6 +582,47 @@ dstack_status upload_weights(Model& m) {
   }
   DS_HIP(hipMalloc(&m.d_w, (size_t)m.n_weights * 2));
   DS_HIP(hipMemcpy(m.d_w, arena.data(), (size_t)m.n_weights * 2, hipMemcpyHostToDevice));
+  // The weight-streaming operands again, in the MFMA fragment order their
+  // kernels read (16 rows x 32 deep per 1 KB block, zero past the matrix):
+  // FC weights [O][I] with row tile ot = rows 16 ot .. 16 ot + 15; LSTM W_hh
+  // [4H][H] with row tile rt = the rows (gate, unit) = (r / 4, 4 rt + r % 4).
+  auto pack = [](const uint16_t* src, int rows, int cols, int tiles, auto row_of, uint16_t* dst) {
+    const int nks = (cols + 31) / 32;
+    for (int t = 0; t < tiles; ++t)
+      for (int st = 0; st < nks; ++st)
+        for (int r = 0; r < 16; ++r) {
+          const int row = row_of(t, r);
+          uint16_t* d = dst + (((size_t)t * nks + st) * 16 + r) * 32;
+          for (int kk = 0; kk < 32; ++kk) {
+            const int k = st * 32 + kk;
+            d[kk] = row < rows && k < cols ? src[(size_t)row * cols + k] : 0;
+          }
+        }
+  };
+  m.n_wp = 0;
+  for (Op& op : m.ops) {
+    op.wp_off = -1;
+    if (op.kind == OP_FC) {
+      op.wp_off = m.n_wp;
+      m.n_wp += ((int64_t)(op.K + 15) / 16 * 16 * ((op.C + 31) / 32 * 32) + 127) / 128 * 128;
+    } else if (op.kind == OP_LSTM) {
+      op.wp_off = m.n_wp;
+      m.n_wp += ((int64_t)4 * op.Hd * op.Hd + 127) / 128 * 128;
+    }
+  }
+  if (m.n_wp > 0) {
+    std::vector<uint16_t> packed((size_t)m.n_wp, 0);
+    for (const Op& op : m.ops) {
+      if (op.kind == OP_FC)
+        pack(arena.data() + op.w_off, op.K, op.C, (op.K + 15) / 16, [](int t, int r) { return 16 * t + r; },
+             packed.data() + op.wp_off);
+      else if (op.kind == OP_LSTM)
+        pack(arena.data() + op.whh_off, 4 * op.Hd, op.Hd, op.Hd / 4,
+             [H = op.Hd](int t, int r) { return (r >> 2) * H + 4 * t + (r & 3); }, packed.data() + op.wp_off);
+    }
+    DS_HIP(hipMalloc(&m.d_wp, (size_t)m.n_wp * 2));
+    DS_HIP(hipMemcpy(m.d_wp, packed.data(), (size_t)m.n_wp * 2, hipMemcpyHostToDevice));
+  }
   if (m.n_fp32 > 0) {
     DS_HIP(hipMalloc(&m.d_f32, (size_t)m.n_fp32 * 4));
     DS_HIP(hipMemcpy(m.d_f32, m.fp32_host.data(), (size_t)m.n_fp32 * 4, hipMemcpyHostToDevice));
@@ -598,6 +639,7 @@ Model::~Model() {
     if (kv.second->base) (void)hipFree(kv.second->base);
   if (d_w) (void)hipFree(d_w);
   if (d_f32) (void)hipFree(d_f32);
+  if (d_wp) (void)hipFree(d_wp);
   if (sweep_in) (void)hipFree(sweep_in);
   if (sweep_out) (void)hipFree(sweep_out);
 }
@@ -638,7 +680,7 @@ dstack_status get_workspace(Model& m, int pid, int n_cu, hipStream_t st, Workspa
   total += align256(sk);
   const size_t cnt_off = total;
   if (sk) total += align256(SPLITK_TILE_COUNTERS * sizeof(unsigned));
-  size_t gx_off = 0, c_off = 0, h0_off = 0, h1_off = 0, wp_off = 0, hp_off = 0;
+  size_t gx_off = 0, c_off = 0, h0_off = 0, h1_off = 0, hp_off = 0;
   if (m.is_lstm) {
     gx_off = total;
     total += align256((size_t)m.lstm_T * m.max_batch * 4 * m.lstm_H * 4);
@@ -648,8 +690,6 @@ dstack_status get_workspace(Model& m, int pid, int n_cu, hipStream_t st, Workspa
     total += align256((size_t)m.lstm_T * m.max_batch * m.lstm_H * 2);
     h1_off = total;
     total += align256((size_t)m.lstm_T * m.max_batch * m.lstm_H * 2);
-    wp_off = total;
-    total += align256((size_t)4 * m.lstm_H * m.lstm_H * 2);
     hp_off = total;
     total += align256((size_t)2 * m.max_batch * m.lstm_H * 2);
   }
@@ -676,7 +716,6 @@ dstack_status get_workspace(Model& m, int pid, int n_cu, hipStream_t st, Workspa
     w->lstm_c = (float*)(base + c_off);
     w->lstm_h[0] = (bf16*)(base + h0_off);
     w->lstm_h[1] = (bf16*)(base + h1_off);
-    w->lstm_wp = (bf16*)(base + wp_off);
     w->lstm_hp = (bf16*)(base + hp_off);
   }
   *out = w.get();
@@ -756,8 +795,8 @@ static double conv_bytes(const Op& op, int b) {
 }
 
 dstack_status lstm_layer_run(const bf16* x, int T, int B, int I, int H, const bf16* w_ih, const bf16* w_hh,
-                             const float* bias, bf16* h_bf16, float* h_f32, float* gx, float* c, bf16* wp,
-                             bf16* hp, int n_cu, hipStream_t st, KernelTimer* timer) {
+                             const bf16* whh_packed, const float* bias, bf16* h_bf16, float* h_f32, float* gx,
+                             float* c, bf16* wp_scratch, bf16* hp, int n_cu, hipStream_t st, KernelTimer* timer) {
   // input projection of all steps at once: gx[t*B + b][:] = W_ih x + b_ih + b_hh (fp32)
   if (timer) timer->before();
   dstack_status s = launch_conv2d_ws(x, T * B, 1, 1, I, w_ih, 4 * H, 1, 1, 1, 0, nullptr, bias, nullptr, ACT_NONE,
@@ -767,10 +806,14 @@ dstack_status lstm_layer_run(const bf16* x, int T, int B, int I, int H, const bf
     timer->after(KC_MFMA, 2.0 * T * B * I * 4.0 * H,
                  (double)T * B * I * 2 + 4.0 * H * I * 2 + (double)T * B * 4 * H * 4, T * B, 4 * H, I);
   // W_hh in the fragment order of the recurrent product
-  if (timer) timer->before();
-  s = launch_lstm_pack_whh(w_hh, wp, H, st);
-  if (s != DSTACK_OK) return s;
-  if (timer) timer->after(KC_GLUE, 0.0, 2.0 * 4.0 * H * H * 2, 0, 0, 0);
+  const bf16* wp = whh_packed;
+  if (!wp) {
+    if (timer) timer->before();
+    s = launch_lstm_pack_whh(w_hh, wp_scratch, H, st);
+    if (s != DSTACK_OK) return s;
+    if (timer) timer->after(KC_GLUE, 0.0, 2.0 * 4.0 * H * H * 2, 0, 0, 0);
+    wp = wp_scratch;
+  }
   for (int t = 0; t < T; ++t) {
     if (timer) timer->before();
     bf16* hp_t = hp + (size_t)(t & 1) * B * H;
@@ -808,8 +851,8 @@ dstack_status forward(Model& m, int batch, const void* d_in, void* d_out, Worksp
       const bf16* x = op.in == BUF_IN ? (const bf16*)d_in : ws.lstm_h[0];
       bf16* hb = op.in == BUF_IN ? ws.lstm_h[0] : ws.lstm_h[1];
       float* hf = op.out == BUF_OUT ? (float*)d_out : nullptr;
-      s = lstm_layer_run(x, op.T, batch, op.I, op.Hd, m.d_w + op.wih_off, m.d_w + op.whh_off, f32 + op.bias_off, hb, hf,
-                         ws.lstm_gx, ws.lstm_c, ws.lstm_wp, ws.lstm_hp, n_cu, st, timer);
+      s = lstm_layer_run(x, op.T, batch, op.I, op.Hd, m.d_w + op.wih_off, m.d_w + op.whh_off, m.d_wp + op.wp_off,
+                         f32 + op.bias_off, hb, hf, ws.lstm_gx, ws.lstm_c, nullptr, ws.lstm_hp, n_cu, st, timer);
       if (s != DSTACK_OK) return s;
       continue;
     }
@@ -883,8 +926,8 @@ dstack_status forward(Model& m, int batch, const void* d_in, void* d_out, Worksp
         by = (double)batch * op.T * op.C * 2 * 4;
         break;
       case OP_FC:
-        s = launch_fc(src, batch, op.C, m.d_w + op.w_off, f32 + op.shift_off, op.K, op.act, dst, op.out_f32 != 0, n_cu,
-                      ws.splitk, ws.splitk_bytes, st);
+        s = launch_fc(src, batch, op.C, m.d_wp + op.wp_off, f32 + op.shift_off, op.K, op.act, dst, op.out_f32 != 0,
+                      n_cu, ws.splitk, ws.splitk_bytes, st, true);
         kind = KC_FC;
         fl = 2.0 * batch * op.C * (double)op.K;
         by = (double)op.K * op.C * 2 + (double)batch * op.C * 2 + (double)batch * op.K * (op.out_f32 ? 4 : 2);

@@ -61,6 +61,8 @@ struct Op {
   // LSTM layer
   int T = 0, I = 0, Hd = 0;
   int64_t wih_off = 0, whh_off = 0, bias_off = 0;
+  // FC weights / LSTM W_hh in MFMA fragment order: elements into the packed arena (-1: none)
+  int64_t wp_off = -1;
   // tensor indices used when folding biases / BN at upload (-1: none)
   int w_t = -1, bias_t = -1, bn = 0;
   int wih_t = -1, whh_t = -1, bih_t = -1, bhh_t = -1;
@@ -78,7 +80,6 @@ struct Workspace {
   float* lstm_gx = nullptr;
   float* lstm_c = nullptr;
   bf16* lstm_h[2] = {nullptr, nullptr};
-  bf16* lstm_wp = nullptr;  // W_hh of the running layer in fragment order (4H x H)
   bf16* lstm_hp = nullptr;  // h(t-1), h(t) in fragment order (2 x max batch x H)
   std::atomic<bool> busy{false};
   // captured forward passes, keyed by (batch, input, output, CUs of the
@@ -116,6 +117,8 @@ struct Model {
   std::vector<float> fp32_host;     // scale/shift/bias values
   bf16* d_w = nullptr;
   float* d_f32 = nullptr;
+  bf16* d_wp = nullptr;             // packed copies of the weight-streaming operands
+  int64_t n_wp = 0;
   int lstm_T = 0, lstm_B_max = 32, lstm_H = 0;
   std::mutex ws_mu;
   std::map<int, std::unique_ptr<Workspace>> ws;  // by partition id
@@ -177,8 +180,10 @@ dstack_status launch_conv2d_ws(const bf16* x, int N, int H, int W, int C, const 
                                int stride, int pad, const float* scale, const float* shift, const bf16* res,
                                int act, void* y, bool out_fp32, int n_cu, float* splitk_ws, size_t splitk_bytes,
                                unsigned* tile_counters, hipStream_t st);
+// whh_packed: W_hh already in fragment order (a model's, packed at load), or
+// NULL: w_hh is packed into wp_scratch (4H x H) first.
 dstack_status lstm_layer_run(const bf16* x, int T, int B, int I, int H, const bf16* w_ih, const bf16* w_hh,
-                             const float* bias, bf16* h_bf16, float* h_f32, float* gx, float* c, bf16* wp,
-                             bf16* hp, int n_cu, hipStream_t st, KernelTimer* timer);
+                             const bf16* whh_packed, const float* bias, bf16* h_bf16, float* h_f32, float* gx,
+                             float* c, bf16* wp_scratch, bf16* hp, int n_cu, hipStream_t st, KernelTimer* timer);
 
 }  // namespace dstack
