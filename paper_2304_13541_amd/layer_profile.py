@@ -15,7 +15,9 @@ Inputs are synthetic N(0,1) values.
     python -m paper_2304_13541_amd.layer_profile --bench-traffic FETCH_DIR WRITE_DIR BENCH_LOG
 
 --sweep runs the measured workloads (ResNet-50 b16, MobileNetV2 b32, VGG-19
-b8, the LSTM b32) on partitions of 25%, 50% and 100% of the CUs, one eager
+b8, the LSTM b32) on partitions of 25%, 50% and 100% of the CUs, or with
+--cases ARCH:BATCH:SLOTS ... the given models on partitions of that many
+slots (from slot 0), one eager
 forward each (run it with DSTACK_GRAPH=0 under rocprofv3), every segment
 preceded by a marker dispatch (the CU-id probe with 1000 + segment
 workgroups), and ends with a 256 MiB device copy that calibrates the HBM
@@ -24,7 +26,12 @@ byte counters.  --summarize reads the rocprofv3 counter CSVs of such runs
 GRBM_GUI_ACTIVE, FETCH_SIZE, WRITE_SIZE in any passes), splits them at the
 markers and prints per (partition, model, kernel class): dispatches, time,
 MFMA rate from the MFMA op counter against the partition's peak, MFMA busy
-cycles per CU-cycle, and calibrated HBM bytes and GB/s.
+cycles per CU-cycle, and calibrated HBM bytes and GB/s (give the same
+--cases as to the sweep).  When the passes hold the SQ wave-state counters
+(SQ_WAVE_CYCLES, SQ_WAIT_ANY, SQ_WAIT_INST_ANY, SQ_ACTIVE_INST_ANY / _VMEM /
+_LDS / _VALU / _SCA, SQ_VALU_MFMA_BUSY_CYCLES) it also prints where the
+waves' time goes: the share of wave-cycles waiting on dependencies (memory,
+barriers), waiting to issue, and issuing each instruction kind.
 
 --bench-kernels and --bench-traffic read rocprofv3 runs of bench.py (kernel
 trace; FETCH_SIZE and WRITE_SIZE passes), whose roofline forwards are marked
@@ -53,17 +60,32 @@ CALIBRATION_BYTES = 256 << 20
 TRACE_DIR = []
 
 
+CASES = []  # (arch, batch, slots) from --cases; empty: SWEEP_MODELS x SWEEP_FRACTIONS
+
+
+def sweep_segments():
+    """(arch, batch, CUs) of each sweep segment, in order."""
+    if CASES:
+        return [(a, b, 8 * sl) for a, b, sl in CASES]
+    return [(a, b, 8 * ds.fraction_to_slots(f)) for f in SWEEP_FRACTIONS for a, b in SWEEP_MODELS]
+
+
 def sweep():
     seg = 0
-    runs = []
-    for arch, b in SWEEP_MODELS:
+    runs = {}
+    for arch, b, _ in sweep_segments():
+        if (arch, b) in runs:
+            continue
         m = ds.Model(arch, 1)
         g = torch.Generator(device="cuda").manual_seed(1)
         x = torch.randn(m.input_shape(b), device="cuda", generator=g).to(torch.bfloat16)
-        runs.append((arch, b, m, x, torch.empty(m.output_shape(b), device="cuda", dtype=torch.float32)))
-    for f in SWEEP_FRACTIONS:
-        p = ds.Partition(f)
-        for arch, b, m, x, y in runs:
+        runs[(arch, b)] = (arch, b, m, x, torch.empty(m.output_shape(b), device="cuda", dtype=torch.float32))
+    # one partition per case, or per fraction with every model on it
+    groups = [(sl, [runs[(a, b)]]) for a, b, sl in CASES] if CASES else \
+        [(ds.fraction_to_slots(f), [runs[(a, b)] for a, b in SWEEP_MODELS]) for f in SWEEP_FRACTIONS]
+    for slots, group in groups:
+        p = ds.Partition(slot_offset=0, n_slots=slots)
+        for arch, b, m, x, y in group:
             for _ in range(2):
                 m.infer(b, x, y, p)
             p.synchronize()
@@ -75,7 +97,7 @@ def sweep():
                   (seg, arch, b, p.n_cu, len(recs), 1000 * sum(r["ms"] for r in recs)), flush=True)
             seg += 1
         p.destroy()
-    for _, _, m, _, _ in runs:
+    for _, _, m, _, _ in runs.values():
         m.destroy()
     a = torch.ones(CALIBRATION_BYTES // 4, dtype=torch.float32, device="cuda")
     c = torch.empty_like(a)
@@ -158,12 +180,11 @@ def summarize(dirs):
           % ("kernel trace" if trace else "counter run") +
           "of partition peak | MFMA busy cycles / (GUI cycles x CUs) | HBM MB read | HBM MB written | GB/s |")
     print("|---|---|---|---|---|---|---|---|---|---|---|")
+    labels = sweep_segments()
     for seg, classes in segs.items():
         if seg == last:
             continue
-        fi, mi = divmod(seg, len(SWEEP_MODELS))
-        n_cu = 8 * ds.fraction_to_slots(SWEEP_FRACTIONS[fi])
-        arch, b = SWEEP_MODELS[mi]
+        arch, b, n_cu = labels[seg]
         for cls, a in classes.items():
             c = a["c"]
             if (seg, cls) in trace:
@@ -181,6 +202,35 @@ def summarize(dirs):
                 fmt(tf / (2516.6 * n_cu / 256) if tf else None, "%.3f"),
                 fmt(busy / (gui * n_cu) if busy and gui else None, "%.3f"), fmt(rd, "%.1f"), fmt(wr, "%.1f"),
                 fmt(gbs, "%.0f")))
+    if any("SQ_WAVE_CYCLES" in a["c"] for classes in segs.values() for a in classes.values()):
+        stalls(segs, last, labels)
+
+
+def stalls(segs, last, labels):
+    """Where the waves' time goes, per (partition, model, kernel class): the
+    SQ wave-state counters as shares of SQ_WAVE_CYCLES (all count
+    wave-cycles; the VALU share includes the MFMA instructions' issue), and
+    the raw ratio of the MFMA busy counter to GRBM_GUI_ACTIVE x CUs."""
+    print()
+    print("| CUs | model | kernel class | waves | waiting on dependencies | waiting to issue | issuing: any | VMEM | "
+          "LDS | VALU | scalar | MFMA busy / (GUI cycles x CUs) |")
+    print("|---|---|---|---|---|---|---|---|---|---|---|---|")
+    for seg, classes in segs.items():
+        if seg == last:
+            continue
+        arch, b, n_cu = labels[seg]
+        for cls, a in classes.items():
+            c = a["c"]
+            wc = c.get("SQ_WAVE_CYCLES")
+            if not wc:
+                continue
+            sh = lambda k: ("%.2f" % (c[k] / wc)) if k in c else "-"
+            busy, gui = c.get("SQ_VALU_MFMA_BUSY_CYCLES"), c.get("GRBM_GUI_ACTIVE")
+            print("| %d | %s b%d | %s | %d | %s | %s | %s | %s | %s | %s | %s | %s |" % (
+                n_cu, arch, b, cls, int(c.get("SQ_WAVES", 0)), sh("SQ_WAIT_ANY"), sh("SQ_WAIT_INST_ANY"),
+                sh("SQ_ACTIVE_INST_ANY"), sh("SQ_ACTIVE_INST_VMEM"), sh("SQ_ACTIVE_INST_LDS"),
+                sh("SQ_ACTIVE_INST_VALU"), sh("SQ_ACTIVE_INST_SCA"),
+                "%.3f" % (busy / (gui * n_cu)) if busy and gui else "-"))
 
 
 # bench.py's markers: the roofline forwards of model i follow 1000 + 100 + i,
@@ -308,12 +358,18 @@ def main():
     ap.add_argument("--seed", type=int, default=1)
     ap.add_argument("--compare-blas", action="store_true")
     ap.add_argument("--sweep", action="store_true")
+    ap.add_argument("--cases", nargs="+", default=None, metavar="ARCH:BATCH:SLOTS",
+                    help="with --sweep / --summarize: these models on partitions of that many slots")
     ap.add_argument("--summarize", nargs="+", default=None)
     ap.add_argument("--trace", default=None, help="with --summarize: a kernel-trace run of the same sweep")
     ap.add_argument("--bench-kernels", nargs="+", default=None, metavar=("TRACE_DIR", "BENCH_LOG"),
                     help="kernel-trace run of bench.py, its output, [an unprofiled bench output]")
     ap.add_argument("--bench-traffic", nargs=3, default=None, metavar=("FETCH_DIR", "WRITE_DIR", "BENCH_LOG"))
     a = ap.parse_args()
+    if a.cases:
+        for c in a.cases:
+            arch, b, sl = c.split(":")
+            CASES.append((arch, int(b), int(sl)))
     if a.bench_kernels:
         return bench_kernels(*a.bench_kernels)
     if a.bench_traffic:

@@ -122,3 +122,32 @@ def test_bench_traffic_calibrates_and_records_source(runs, monkeypatch):
     src.write_text("changed")
     monkeypatch.setattr(bench, "CONV_SRC", str(src))
     assert bench.measured_traffic() == (None, None)
+
+
+def test_summarize_cases_and_wave_states(tmp_path, monkeypatch):
+    """--cases labels the segments; the SQ counters become shares of the
+    wave-cycles."""
+    from paper_2304_13541_amd import layer_profile as lp
+    d = tmp_path / "p1"
+    os.makedirs(d)
+    counters = {"SQ_WAVES": 8, "SQ_WAVE_CYCLES": 1000, "SQ_WAIT_ANY": 600, "SQ_WAIT_INST_ANY": 70,
+                "SQ_ACTIVE_INST_ANY": 300, "SQ_ACTIVE_INST_VMEM": 50, "SQ_ACTIVE_INST_LDS": 40,
+                "SQ_ACTIVE_INST_VALU": 100, "SQ_ACTIVE_INST_SCA": 30, "SQ_VALU_MFMA_BUSY_CYCLES": 2400,
+                "GRBM_GUI_ACTIVE": 100}
+    rows = [(PROBE, 1000 * 64, {}), (CONV, 4096, counters), (PROBE, 999 * 64, {}),
+            (PROBE, 1001 * 64, {}), (OTHER, 4096, {"SQ_WAVES": 4}), (PROBE, 999 * 64, {}),
+            (PROBE, 1002 * 64, {}), (COPY, 1 << 20, {"FETCH_SIZE": 131072.0}), (PROBE, 999 * 64, {})]
+    with open(d / "x_counter_collection.csv", "w", newline="") as f:
+        w = csv.writer(f, quoting=csv.QUOTE_NONNUMERIC)
+        w.writerow(["Dispatch_Id", "Grid_Size", "Kernel_Name", "Counter_Name", "Counter_Value", "Start_Timestamp",
+                    "End_Timestamp"])
+        for i, (name, grid, cs) in enumerate(rows):
+            for cn, v in (cs or {"SQ_WAVES": 1}).items():
+                w.writerow([i + 1, grid, name, cn, v, 0, 2000])
+    monkeypatch.setattr(lp, "CASES", [("resnet50", 16, 3), ("lstm2", 32, 16)])
+    out = captured(lp.summarize, [str(d)])
+    assert "| 24 | resnet50 b16 | conv | 1 |" in out
+    assert "| 128 | lstm2 b32 | pool | 1 |" in out
+    # waiting 0.60, to issue 0.07, issuing 0.30 (VMEM 0.05, LDS 0.04, VALU
+    # 0.10, scalar 0.03); MFMA busy 2400 / (100 x 24 CUs) = 1.000
+    assert "| 24 | resnet50 b16 | conv | 8 | 0.60 | 0.07 | 0.30 | 0.05 | 0.04 | 0.10 | 0.03 | 1.000 |" in out
