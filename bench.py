@@ -73,6 +73,7 @@ MIX4 = [
     ("vgg19", 1052, 50000, 150, 8, [1, 2, 4, 8]),
     ("lstm2", 1053, 30000, 300, 32, [1, 2, 4, 8, 16, 32]),
 ]
+CAPACITY_BISECTIONS = 4           # after the doubling: geometric bisections of the capacity bracket
 TEMPORAL_CYCLES = [15000, 7500]   # temporal sharing: slice cycles tried (the best is the baseline)
 # D-STACK settings tried (the best is the headline): (over-provision slots,
 # late requests that move a model to its next larger swept GPU% -- Sec. 3.5's
@@ -582,7 +583,8 @@ class Mix4:
     def capacity(self, policy, param, seconds):
         """Largest k (offered rate k x the stated rates) with at most 1% of the
         requests late or unserved: double from 1 until a probe fails (halve
-        if 1 fails), then bisect three times on the geometric mean."""
+        if 1 fails), then bisect four times on the geometric mean (the last
+        step is 2^(1/16), about 4.4%)."""
         dur = int(seconds * 1e6)
         probes = []
 
@@ -608,7 +610,7 @@ class Mix4:
                     break
                 k_bad, k = k, k / 2
         if k_ok is not None and k_bad is not None:
-            for _ in range(3):
+            for _ in range(CAPACITY_BISECTIONS):
                 mid = math.sqrt(k_ok * k_bad)
                 if ok(mid):
                     k_ok = mid

@@ -71,7 +71,7 @@ def test_capacity_search_doubles_then_bisects():
     k, probes = bench.Mix4.capacity(m, "dstack", (0, 0), 1.5)
     ks = [p["k"] for p in probes]
     assert ks[:6] == [1.0, 2.0, 4.0, 8.0, 16.0, 32.0]  # doubling until a probe fails
-    assert len(ks) == 9  # then three bisections on the geometric mean
+    assert len(ks) == 6 + bench.CAPACITY_BISECTIONS  # then bisections on the geometric mean
     assert 16.0 <= k <= 19.0 and all(p["violation_frac"] == 0.0 for p in probes if p["k"] <= k)
     assert k == max(p["k"] for p in probes if p["violation_frac"] <= bench.VIOLATION_BAR)
     # below 1: halving
@@ -85,11 +85,17 @@ def test_timed_run_falls_back_to_the_next_passing_probe():
     entry = dict(k=k, probes=probes)
     k_run, run = bench.confirm_capacity(m, "dstack", (0, 0), entry, 20, 3)
     assert run["violation_frac"] <= bench.VIOLATION_BAR and k_run <= 17.0
-    assert entry["timed_k"][0] == k
+    tried = entry["timed_k"]
+    assert tried[0] == k
     lower = max(p["k"] for p in probes if p["k"] <= 17.0)
-    # the fallback probe, then one step between it and the failed k
-    assert entry["timed_k"][1] == lower and abs(entry["timed_k"][2] - (lower * k) ** 0.5) < 1e-9
-    assert k_run == (entry["timed_k"][2] if entry["timed_k"][2] <= 17.0 else lower)
+    # the passing probes below k in descending order until one holds, then
+    # one step between it and the last failed k
+    i = tried.index(lower)
+    passing = sorted((p["k"] for p in probes if p["violation_frac"] <= bench.VIOLATION_BAR and lower <= p["k"] < k),
+                     reverse=True)
+    assert tried[1:i + 1] == passing and len(tried) == i + 2
+    assert abs(tried[-1] - (lower * tried[i - 1]) ** 0.5) < 1e-9
+    assert k_run == (tried[-1] if tried[-1] <= 17.0 else lower)
     # a capacity that holds over the timed run is kept as it is
     m2 = FakeMix(probe_limit=19.0, timed_limit=19.0)
     k2, probes2 = bench.Mix4.capacity(m2, "dstack", (0, 0), 1.5)
