@@ -204,6 +204,8 @@ def summarize(dirs):
                 fmt(gbs, "%.0f")))
     if any("SQ_WAVE_CYCLES" in a["c"] for classes in segs.values() for a in classes.values()):
         stalls(segs, last, labels)
+    if any("SQ_INSTS_LDS_LOAD_BANDWIDTH" in a["c"] for classes in segs.values() for a in classes.values()):
+        lds_port(segs, last, labels)
 
 
 def stalls(segs, last, labels):
@@ -231,6 +233,48 @@ def stalls(segs, last, labels):
                 sh("SQ_ACTIVE_INST_ANY"), sh("SQ_ACTIVE_INST_VMEM"), sh("SQ_ACTIVE_INST_LDS"),
                 sh("SQ_ACTIVE_INST_VALU"), sh("SQ_ACTIVE_INST_SCA"),
                 "%.3f" % (busy / (gui * n_cu)) if busy and gui else "-"))
+
+
+LDS_PORT_BYTES_PER_CLK = 128  # one CU's LDS bandwidth (bytes per clock)
+SHADER_MHZ = 2400             # the MI355X's peak engine clock
+
+
+def lds_port(segs, last, labels):
+    """LDS traffic per (partition, model, kernel class), per CU and clock
+    cycle of the class's kernel-trace time at the 2.4 GHz peak clock (a lower
+    clock would raise every per-cycle figure): LDS reads =
+    SQ_INSTS_LDS_LOAD_BANDWIDTH x 64 bytes (ds_read data); LDS fills by the
+    buffer-to-LDS loads = TA_BUFFER_READ_LDS_WAVEFRONTS x 1 KB (every such
+    load of this library moves 16 bytes per lane); the MFMA busy counter per
+    SIMD-cycle; the LDS bytes the class moves per MFMA-busy cycle, and the
+    MFMA share a 128-byte-per-clock LDS port would allow at that ratio; the
+    bank-conflict and full-data-FIFO counters per CU-cycle as read."""
+    print()
+    print("| CUs | model | kernel class | us | LDS read B/clk/CU | LDS fill B/clk/CU | LDS total B/clk/CU | "
+          "MFMA busy / SIMD-cycle | LDS B per MFMA-busy cycle | MFMA share the LDS port allows | "
+          "bank conflict / CU-cycle | data FIFO full / CU-cycle |")
+    print("|---|---|---|---|---|---|---|---|---|---|---|---|")
+    for seg, classes in segs.items():
+        if seg == last:
+            continue
+        arch, b, n_cu = labels[seg]
+        for cls, a in classes.items():
+            c = a["c"]
+            if "SQ_INSTS_LDS_LOAD_BANDWIDTH" not in c or not a["us"]:
+                continue
+            cu_cyc = a["us"] * SHADER_MHZ * n_cu
+            rd = c["SQ_INSTS_LDS_LOAD_BANDWIDTH"] * 64 / cu_cyc
+            fill_w = c.get("TA_BUFFER_READ_LDS_WAVEFRONTS_sum", c.get("TA_BUFFER_READ_LDS_WAVEFRONTS"))
+            tot = rd + (fill_w * 1024 / cu_cyc if fill_w is not None else 0.0)
+            busy = c.get("SQ_VALU_MFMA_BUSY_CYCLES")
+            share = busy / (4 * cu_cyc) if busy else None
+            per_busy = tot / share if share else None
+            per = lambda k: ("%.3f" % (c[k] / cu_cyc)) if k in c else "-"
+            print("| %d | %s b%d | %s | %.1f | %.1f | %s | %.1f | %s | %s | %s | %s | %s |" % (
+                n_cu, arch, b, cls, a["us"], rd, "%.1f" % (tot - rd) if fill_w is not None else "-", tot,
+                "%.3f" % share if share is not None else "-", "%.0f" % per_busy if per_busy else "-",
+                "%.2f" % min(1.0, LDS_PORT_BYTES_PER_CLK / per_busy) if per_busy else "-",
+                per("SQ_LDS_BANK_CONFLICT"), per("SQ_LDS_DATA_FIFO_FULL")))
 
 
 # bench.py's markers: the roofline forwards of model i follow 1000 + 100 + i,

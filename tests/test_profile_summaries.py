@@ -151,3 +151,31 @@ def test_summarize_cases_and_wave_states(tmp_path, monkeypatch):
     # waiting 0.60, to issue 0.07, issuing 0.30 (VMEM 0.05, LDS 0.04, VALU
     # 0.10, scalar 0.03); MFMA busy 2400 / (100 x 24 CUs) = 1.000
     assert "| 24 | resnet50 b16 | conv | 8 | 0.60 | 0.07 | 0.30 | 0.05 | 0.04 | 0.10 | 0.03 | 1.000 |" in out
+
+
+def test_summarize_lds_port(tmp_path, monkeypatch):
+    """LDS reads and buffer-to-LDS fills per CU-cycle of the kernel time at
+    the 2.4 GHz clock, per MFMA-busy cycle, and the MFMA share a 128-byte
+    port allows at that ratio."""
+    from paper_2304_13541_amd import layer_profile as lp
+    d = tmp_path / "p1"
+    os.makedirs(d)
+    # 2 us on 24 CUs = 2 x 2400 x 24 = 115200 CU-cycles
+    counters = {"SQ_INSTS_LDS_LOAD_BANDWIDTH": 115200, "TA_BUFFER_READ_LDS_WAVEFRONTS_sum": 3600,
+                "SQ_VALU_MFMA_BUSY_CYCLES": 115200, "SQ_LDS_BANK_CONFLICT": 0, "SQ_LDS_DATA_FIFO_FULL": 1152,
+                "GRBM_GUI_ACTIVE": 1}
+    rows = [(PROBE, 1000 * 64, {}), (CONV, 4096, counters), (PROBE, 999 * 64, {}),
+            (PROBE, 1001 * 64, {}), (COPY, 1 << 20, {"FETCH_SIZE": 131072.0}), (PROBE, 999 * 64, {})]
+    with open(d / "x_counter_collection.csv", "w", newline="") as f:
+        w = csv.writer(f, quoting=csv.QUOTE_NONNUMERIC)
+        w.writerow(["Dispatch_Id", "Grid_Size", "Kernel_Name", "Counter_Name", "Counter_Value", "Start_Timestamp",
+                    "End_Timestamp"])
+        for i, (name, grid, cs) in enumerate(rows):
+            for cn, v in (cs or {"SQ_WAVES": 1}).items():
+                w.writerow([i + 1, grid, name, cn, v, 0, 2000])
+    monkeypatch.setattr(lp, "CASES", [("resnet50", 16, 3)])
+    out = captured(lp.summarize, [str(d)])
+    # reads 64 B/clk/CU, fills 3600 KB / 115200 = 32, total 96; MFMA busy
+    # 115200 / (4 x 115200) = 0.25, so 384 LDS bytes per busy cycle and a
+    # 128-byte port allows 0.33 of the MFMA rate
+    assert "| 24 | resnet50 b16 | conv | 2.0 | 64.0 | 32.0 | 96.0 | 0.250 | 384 | 0.33 | 0.000 | 0.010 |" in out
