@@ -79,7 +79,7 @@ TEMPORAL_CYCLES = [15000, 7500]   # temporal sharing: slice cycles tried (the be
 # late requests that move a model to its next larger swept GPU% -- Sec. 3.5's
 # reconfiguration, 0: off)
 RESIZE_VIOLATIONS = 5
-DSTACK_VARIANTS = [(0, 0), (2, 0), (0, RESIZE_VIOLATIONS)]
+DSTACK_VARIANTS = [(0, 0), (2, 0), (0, RESIZE_VIOLATIONS), (0, 2)]
 # config 3: ResNet-50 (SLO 25 ms) + MobileNetV2 (SLO 15 ms); indices into MIX4
 PAIR = [(0, 25000, 16), (1, 15000, 32)]
 
@@ -590,8 +590,10 @@ class Mix4:
 
         def ok(k):
             r = self.run(k, dur, policy, param)
-            probes.append({kk: r[kk] for kk in ("k", "offered_req_s", "on_time_per_s", "violation_frac",
-                                                "utilisation_ppm")})
+            probes.append(dict({kk: r[kk] for kk in ("k", "offered_req_s", "on_time_per_s", "violation_frac",
+                                                     "utilisation_ppm")},
+                               resizes=[m["resizes"] for m in r.get("per_model", [])],
+                               final_slots=[m["final_slots"] for m in r.get("per_model", [])]))
             return r["violation_frac"] <= VIOLATION_BAR
 
         k_ok = k_bad = None

@@ -543,8 +543,9 @@ dstack_status dstack_simulate_ideal(const dstack_ideal_model* models, int n_mode
 /* ------------------------------------------------------------------ */
 /* Runs the same plan and the same FOD decisions as dstack_simulate, on the
  * host's monotonic clock (us since the call's start, after a warm-up) with
- * real batches: model i owns one partition on its home range (placement
- * must be 1) and every job of model i runs as dstack_infer(models[i], b,
+ * real batches: model i runs on a partition over its home range (placement
+ * must be 1; models with identical ranges share one, as their jobs never
+ * overlap) and every job of model i runs as dstack_infer(models[i], b,
  * d_in[i], d_out[i], that partition) would, with a workspace (activations,
  * split-K buffers, captured graphs) the model keeps for the launcher across
  * partitions and calls.  Requests arrive when the clock passes their
@@ -555,7 +556,13 @@ dstack_status dstack_simulate_ideal(const dstack_ideal_model* models, int n_mode
  * still running, and is skipped (plan_skips).  busy_us, the percentiles and
  * utilisation_ppm use measured GPU time (device events around each job).
  * Not reproducible run to run: job_hash covers the decisions taken.
- *  - n_models in 1..4 (one CU-masked stream per model);
+ *  - n_models in 1..4 (at most one CU-masked stream per model);
+ *  - GPU% changes (sim->resize_violations > 0): a model's next range runs
+ *    on the stream of that range if one is live, else on a new one created
+ *    on a helper thread; while the partition limit leaves room, a model with
+ *    late requests since its last change gets that stream ahead of the
+ *    change (a standby), so that the change takes effect when it is decided
+ *    (kind 3 below at that time);
  *  - d_in[i], d_out[i]: caller-owned device buffers holding the model's
  *    input and output at tables[i].max_batch (shapes of dstack_model_query);
  *    a job of batch b reads its input from the start of d_in[i] and writes

@@ -131,16 +131,24 @@ bool LaunchState::note_late(int64_t t, int i, int64_t late) {
   viol_[i] += late;
   if (viol_[i] < sim_->resize_violations) return false;
   viol_[i] = 0;
+  int home = 0, next = 0;
+  if (!next_range(i, &home, &next)) return false;  // already at its largest swept share
+  dep_[i] = next;
+  home_[i] = home;
+  resizes_[i] += 1;
+  changed_at_[i] = t;
+  return true;
+}
+
+bool LaunchState::next_range(int i, int* home, int* dep) const {
   const dstack_sched_model& m = models_[i];
   int next = -1;
   for (int q = 0; q < m.n_slots && next < 0; ++q)
     if (m.slots[q] > dep_[i] && m.slots[q] <= prm_->total_slots && table_latency(i, plan_->batch[i], m.slots[q]) > 0)
       next = m.slots[q];
-  if (next < 0) return false;  // already at its largest swept share
-  dep_[i] = next;
-  if (home_[i] + next > prm_->total_slots) home_[i] = prm_->total_slots - next;
-  resizes_[i] += 1;
-  changed_at_[i] = t;
+  if (next < 0) return false;
+  *dep = next;
+  *home = home_[i] + next > prm_->total_slots ? prm_->total_slots - next : home_[i];
   return true;
 }
 

@@ -53,6 +53,11 @@ class LaunchState {
   // job as it now runs:
   bool note_late(int64_t t, int i, int64_t late);
   int64_t changed_at(int i) const { return changed_at_[i]; }
+  // the home offset and size model i moves to at its next GPU% change
+  // (false: it is at its largest swept share), and the late requests
+  // counted towards that change so far
+  bool next_range(int i, int* home, int* dep) const;
+  int64_t late_count(int i) const { return viol_[i]; }
   // the live launcher: model i's new stream is being created (it neither
   // starts planned jobs nor is picked by FOD) until ready(i, t), which also
   // moves changed_at(i) to t

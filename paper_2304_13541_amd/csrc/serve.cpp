@@ -1,7 +1,12 @@
 // Live launcher: the session plan and the FOD fill of Sec. 6.1.2 driving
-// real batches on CU-masked streams.  Model i owns one partition on its home
-// range (the plan's home placement), so at most four masked streams exist at
-// once; the host thread follows the request trace on its monotonic clock,
+// real batches on CU-masked streams.  Model i runs on a partition over its
+// home range (the plan's home placement); models whose ranges are identical
+// share one (a job needs its whole range free, so their jobs never overlap),
+// and at most four masked streams exist at once.  A slot the sharing leaves
+// free holds a standby: the stream of the next larger range of a model that
+// has started to miss its SLO, created ahead on a helper thread, so that its
+// GPU% change (Sec. 3.5's active-standby pair) takes effect at once.  The
+// host thread follows the request trace on its monotonic clock,
 // launches planned and FOD jobs through dstack_infer, and polls each job's
 // end event.  The decisions are those of the virtual-clock simulation (the
 // same LaunchState, fed with table latencies); only the completion times and
@@ -54,24 +59,35 @@ struct NewPartition {
   std::string err;
 };
 
+// A live partition and the models whose current range it covers.
+struct PoolEntry {
+  int off = 0, n = 0, users = 0;
+  dstack_partition p = nullptr;
+  hipStream_t s = nullptr;
+};
+
 struct Resources {
-  std::vector<dstack_partition> part;
-  std::vector<std::future<NewPartition>> pending;  // per model; valid() while its stream is being created
+  std::vector<PoolEntry> pool;                      // p == nullptr: a free entry
+  std::vector<std::future<NewPartition>> pending;  // per model; valid() while a stream of its next range is created
+  std::vector<dstack_partition> made;              // per model: that stream, created and not used yet
+  std::vector<int> made_off, made_n;               // the range pending[i] / made[i] covers
   std::vector<hipEvent_t> ev0, ev1;
-  bool drained = true;  // false: a job may still run, keep the partitions
+  bool drained = true;  // false: a job may still run, keep the partitions that ran jobs
   ~Resources() {
-    for (auto& f : pending)
-      if (f.valid()) {  // an early return: wait for the creation, keep the partition with the others
-        NewPartition np = f.get();
-        if (np.first == DSTACK_OK) part.push_back(np.second);
+    for (size_t i = 0; i < pending.size(); ++i)
+      if (pending[i].valid()) {  // an early return: wait for the creation
+        NewPartition np = pending[i].get();
+        if (np.first == DSTACK_OK) made[i] = np.second;
       }
     for (hipEvent_t e : ev0)
       if (e) (void)hipEventDestroy(e);
     for (hipEvent_t e : ev1)
       if (e) (void)hipEventDestroy(e);
+    for (dstack_partition p : made)  // never ran a job
+      if (p) dstack_partition_destroy(p);
     if (drained)
-      for (dstack_partition p : part)
-        if (p) dstack_partition_destroy(p);
+      for (const PoolEntry& e : pool)
+        if (e.p) dstack_partition_destroy(e.p);
   }
 };
 
@@ -108,29 +124,68 @@ dstack_status serve(const dstack_model* models, int n, const void* const* d_in, 
   dstack_status st = schedule(tables, n, prm, plan);
   if (st != DSTACK_OK && st != DSTACK_E_INFEASIBLE) return st;
 
-  // D-STACK: model i owns a partition on its home range.  Temporal sharing:
-  // one partition of all the slots, which every model's jobs use in turn.
+  // D-STACK: model i runs on a partition over its home range, shared with
+  // the models of the same range.  Temporal sharing: one partition of all
+  // the slots, which every model's jobs use in turn.
   Resources res;
-  const int n_parts = temporal ? 1 : n;
-  res.part.assign(n_parts, nullptr);
   res.pending.resize(n);
+  res.made.assign(n, nullptr);
+  res.made_off.assign(n, -1);
+  res.made_n.assign(n, 0);
   res.ev0.assign(n, nullptr);
   res.ev1.assign(n, nullptr);
-  std::vector<hipStream_t> pstream(n_parts);
-  for (int q = 0; q < n_parts; ++q) {
-    st = temporal ? dstack_partition_create_at(0, prm->total_slots, &res.part[q])
-                  : dstack_partition_create_at(plan->home_offset[q], plan->deployed_slots[q], &res.part[q]);
-    if (st != DSTACK_OK) return st;
-    void* sp = nullptr;
-    st = dstack_partition_query(res.part[q], nullptr, nullptr, &sp);
-    if (st != DSTACK_OK) return st;
-    pstream[q] = (hipStream_t)sp;
-  }
+  std::vector<int> cur(n, -1);  // model i's pool entry (-1 while it waits for a new one)
   std::vector<dstack_partition> part(n);
   std::vector<hipStream_t> stream(n);
+  auto find_entry = [&](int off, int cnt) {
+    for (size_t k = 0; k < res.pool.size(); ++k)
+      if (res.pool[k].p && res.pool[k].off == off && res.pool[k].n == cnt) return (int)k;
+    return -1;
+  };
+  auto add_entry = [&](dstack_partition p, int off, int cnt, int* k) -> dstack_status {
+    void* sp = nullptr;
+    dstack_status s = dstack_partition_query(p, nullptr, nullptr, &sp);
+    if (s != DSTACK_OK) {
+      dstack_partition_destroy(p);
+      return s;
+    }
+    *k = -1;
+    for (size_t q = 0; q < res.pool.size() && *k < 0; ++q)
+      if (!res.pool[q].p) *k = (int)q;
+    if (*k < 0) {
+      *k = (int)res.pool.size();
+      res.pool.emplace_back();
+    }
+    res.pool[*k] = PoolEntry{off, cnt, 0, p, (hipStream_t)sp};
+    return DSTACK_OK;
+  };
+  auto attach = [&](int i, int k) {
+    cur[i] = k;
+    res.pool[k].users += 1;
+    part[i] = res.pool[k].p;
+    stream[i] = res.pool[k].s;
+  };
+  auto detach = [&](int i) {  // model i's last job on its entry has completed
+    PoolEntry& e = res.pool[cur[i]];
+    if (--e.users == 0) {
+      dstack_partition_destroy(e.p);
+      e = PoolEntry{};
+    }
+    cur[i] = -1;
+    part[i] = nullptr;
+    stream[i] = nullptr;
+  };
   for (int i = 0; i < n; ++i) {
-    part[i] = res.part[temporal ? 0 : i];
-    stream[i] = pstream[temporal ? 0 : i];
+    const int off = temporal ? 0 : plan->home_offset[i], cnt = temporal ? prm->total_slots : plan->deployed_slots[i];
+    int k = find_entry(off, cnt);
+    if (k < 0) {
+      dstack_partition p = nullptr;
+      st = dstack_partition_create_at(off, cnt, &p);
+      if (st != DSTACK_OK) return st;
+      st = add_entry(p, off, cnt, &k);
+      if (st != DSTACK_OK) return st;
+    }
+    attach(i, k);
     DS_HIP(hipEventCreate(&res.ev0[i]));
     DS_HIP(hipEventCreate(&res.ev1[i]));
   }
@@ -168,10 +223,58 @@ dstack_status serve(const dstack_model* models, int n, const void* const* d_in, 
       cur = next;
     }
   }
-  for (int q = 0; q < n_parts; ++q) {
-    st = dstack_synchronize(res.part[q]);
+  for (const PoolEntry& e : res.pool) {
+    if (!e.p) continue;
+    st = dstack_synchronize(e.p);
     if (st != DSTACK_OK) return st;
   }
+
+  // streams of a model's next range, created on a helper thread; partitions
+  // live in the process (this launcher's and any other) plus those being
+  // created stay within the library's limit
+  auto room = [&]() {
+    int live = 0, max_live = 0;
+    dstack_partition_count(&live, &max_live);
+    for (int i = 0; i < n; ++i) live += res.pending[i].valid() ? 1 : 0;
+    return max_live - live;
+  };
+  auto start_create = [&](int i, int off, int cnt) -> dstack_status {
+    int dev = 0;
+    DS_HIP(hipGetDevice(&dev));
+    res.made_off[i] = off;
+    res.made_n[i] = cnt;
+    res.pending[i] = std::async(std::launch::async, [off, cnt, dev] {
+      NewPartition np;
+      const hipError_t e = hipSetDevice(dev);  // the helper starts on device 0
+      if (e != hipSuccess) {
+        np.first = DSTACK_E_HIP;
+        np.err = std::string("serve: hipSetDevice: ") + hipGetErrorString(e);
+        return np;
+      }
+      np.first = dstack_partition_create_at(off, cnt, &np.second);
+      if (np.first != DSTACK_OK) np.err = dstack_last_error();
+      return np;
+    });
+    return DSTACK_OK;
+  };
+  auto collect = [&](int i, bool wait) -> dstack_status {  // a finished creation into made[i]
+    if (!res.pending[i].valid()) return DSTACK_OK;
+    if (!wait && res.pending[i].wait_for(std::chrono::seconds(0)) != std::future_status::ready) return DSTACK_OK;
+    const NewPartition np = res.pending[i].get();
+    if (np.first != DSTACK_OK) return fail(np.first, np.err);
+    res.made[i] = np.second;
+    return DSTACK_OK;
+  };
+  auto drop_standby = [&](int i) -> dstack_status {  // an unused stream of model i's
+    dstack_status s = collect(i, true);
+    if (s != DSTACK_OK) return s;
+    if (res.made[i]) dstack_partition_destroy(res.made[i]);
+    res.made[i] = nullptr;
+    res.made_off[i] = -1;
+    res.made_n[i] = 0;
+    return DSTACK_OK;
+  };
+  std::vector<char> switching(n, 0);  // model i waits for its new range's stream
 
   const int64_t D = sim->duration_us;
   const int total = prm->total_slots;
@@ -265,49 +368,66 @@ dstack_status serve(const dstack_model* models, int n, const void* const* d_in, 
       ++jobs;
       note(te, 0, i, 0, 0);
       if (ls.note_late(te, i, late_since)) {
-        // GPU% change between batches: the model's next jobs run on a new
-        // CU-masked stream over its larger range.  The old one is destroyed
-        // first (so no more than four exist), the new one is created on a
-        // helper thread while the other models keep running; weights,
-        // workspace and the graphs captured for that size at warm-up belong
-        // to the model and carry over.
-        dstack_partition_destroy(res.part[i]);
-        res.part[i] = part[i] = nullptr;
+        // GPU% change between batches: the model's next jobs run over its
+        // larger range, on the stream of that range if one exists (another
+        // model's, or its standby), else on a new one created on a helper
+        // thread while the other models keep running (the old stream goes
+        // first if nothing else uses it, and an unused standby of another
+        // model if the limit needs the room).  Weights, workspace and the
+        // graphs captured for that size at warm-up belong to the model and
+        // carry over.
         ls.unavailable(i);
+        switching[i] = 1;
         const int home = ls.home(i), dep = ls.deployed(i);
-        int dev = 0;
-        DS_HIP(hipGetDevice(&dev));
-        res.pending[i] = std::async(std::launch::async, [home, dep, dev] {
-          NewPartition np;
-          const hipError_t e = hipSetDevice(dev);  // the helper starts on device 0
-          if (e != hipSuccess) {
-            np.first = DSTACK_E_HIP;
-            np.err = std::string("serve: hipSetDevice: ") + hipGetErrorString(e);
-            return np;
-          }
-          np.first = dstack_partition_create_at(home, dep, &np.second);
-          if (np.first != DSTACK_OK) np.err = dstack_last_error();
-          return np;
-        });
+        const bool have = find_entry(home, dep) >= 0 ||
+                          (res.made_off[i] == home && res.made_n[i] == dep && (res.pending[i].valid() || res.made[i]));
+        if (!have) {
+          st = drop_standby(i);
+          if (st != DSTACK_OK) return st;
+          detach(i);
+          for (int j = 0; j < n && room() < 1; ++j)
+            if (j != i && !switching[j]) {
+              st = drop_standby(j);
+              if (st != DSTACK_OK) return st;
+            }
+          st = start_create(i, home, dep);
+          if (st != DSTACK_OK) return st;
+        }
+      } else if (!temporal && sim->resize_violations > 0 && ls.late_count(i) > 0 && !switching[i] &&
+                 !res.pending[i].valid() && !res.made[i] && room() >= 1) {
+        // the model has begun to miss its SLO: its next range's stream as a standby
+        int home = 0, dep = 0;
+        if (ls.next_range(i, &home, &dep) && find_entry(home, dep) < 0) {
+          st = start_create(i, home, dep);
+          if (st != DSTACK_OK) return st;
+        }
       }
       st = fod_pass(te);
       if (st != DSTACK_OK) return st;
     }
-    // GPU% changes whose new stream is ready
+    // GPU% changes whose stream is ready
     for (int i = 0; i < n; ++i) {
-      if (!res.pending[i].valid() ||
-          res.pending[i].wait_for(std::chrono::seconds(0)) != std::future_status::ready)
-        continue;
-      const NewPartition np = res.pending[i].get();
-      if (np.first != DSTACK_OK) return fail(np.first, np.err);
-      res.part[i] = part[i] = np.second;
-      void* sp = nullptr;
-      st = dstack_partition_query(np.second, nullptr, nullptr, &sp);
+      st = collect(i, false);
       if (st != DSTACK_OK) return st;
-      stream[i] = (hipStream_t)sp;
+      if (!switching[i]) continue;
+      const int home = ls.home(i), dep = ls.deployed(i);
+      int k = find_entry(home, dep);
+      if (k < 0) {
+        if (!res.made[i]) continue;  // still being created
+        st = add_entry(res.made[i], home, dep, &k);
+        res.made[i] = nullptr;
+        res.made_off[i] = -1;
+        if (st != DSTACK_OK) return st;
+      } else {
+        st = drop_standby(i);  // (a stream of that range came about meanwhile)
+        if (st != DSTACK_OK) return st;
+      }
+      if (cur[i] >= 0) detach(i);
+      attach(i, k);
+      switching[i] = 0;
       const int64_t tn = clock();
       ls.ready(i, tn);
-      note(tn, 3, i, 0, range_mask(ls.home(i), ls.deployed(i)));
+      note(tn, 3, i, 0, range_mask(home, dep));
       st = fod_pass(tn);
       if (st != DSTACK_OK) return st;
     }
@@ -344,15 +464,16 @@ dstack_status serve(const dstack_model* models, int n, const void* const* d_in, 
       st = fod_pass(tn);
       if (st != DSTACK_OK) return st;
     }
-    for (int i = 0; i < n; ++i) busy_now = busy_now || run[i].on || res.pending[i].valid();
+    for (int i = 0; i < n; ++i) busy_now = busy_now || run[i].on || switching[i];
     if (t >= D && !busy_now) break;
     if (t > D + kDrainLimitUs) {
       res.drained = false;
       return fail(DSTACK_E_HIP, "serve: a job did not complete within 60 s after the trace");
     }
   }
-  for (int q = 0; q < n_parts; ++q) {
-    st = dstack_synchronize(res.part[q]);
+  for (const PoolEntry& e : res.pool) {
+    if (!e.p) continue;
+    st = dstack_synchronize(e.p);
     if (st != DSTACK_OK) return st;
   }
 

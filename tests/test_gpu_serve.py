@@ -172,3 +172,65 @@ def test_serve_resizes_on_violations_and_replays(env):
     assert sizes == sorted(sizes) and sizes[-1] > sizes[0]
     for m in models:
         m.destroy()
+
+
+def test_serve_shares_ranges_and_changes_without_waiting(env):
+    """Models whose home ranges are identical share one CU-masked stream, so
+    a four-model run fits beside a partition the caller holds (three
+    streams for four models); a GPU% change into a range another model
+    already runs on takes effect as soon as it is decided, and so does one
+    whose standby stream was made ahead when the limit leaves room; the
+    trigger log replays through the oracle to the same jobs, and no
+    partition outlives the call.  Synthetic tables put three models on
+    16-slot ranges [0, 16), [16, 32), [0, 16) and MobileNetV2 on 8 slots at
+    16; its changes go to [16, 32), [8, 32) and [0, 32)."""
+    ds, sched, poisson_arrivals, torch = env
+    live0, limit = ds.partition_count()
+    if live0 + 4 > limit:
+        pytest.skip("partitions of other tests are live")
+    tiny = {b: {8: 300 + 10 * b, 16: 150 + 5 * b, 24: 140 + 5 * b, 32: 135 + 5 * b} for b in (1, 2, 4)}
+    mb = {b: {8: 400 + 50 * b, 16: 350 + 40 * b, 24: 340 + 38 * b, 32: 335 + 37 * b} for b in (1, 2, 4, 8)}
+    models = [ds.Model("tinycnn", 41 + i) for i in range(3)] + [ds.Model("mobilenetv2", 44)]
+    tables = [dict(slo_us=20000, max_batch=4, rate_per_s=0, table=tiny) for _ in range(3)] + \
+        [dict(slo_us=1500, max_batch=8, rate_per_s=0, table=mb)]
+    st, plan = ds.schedule(tables, 10_000, overprov_slots=0, placement="home")
+    assert plan["home_offset"] == [0, 16, 0, 16] and plan["deployed_slots"] == [16, 16, 16, 8]
+    duration = 300_000
+    arrivals = [poisson_arrivals(51 + i, 500, duration) for i in range(3)] + [poisson_arrivals(54, 30000, duration)]
+    xs = [torch.zeros(m.input_shape(t["max_batch"]), device="cuda", dtype=torch.bfloat16) for m, t in zip(models, tables)]
+    ys = [torch.zeros(m.output_shape(t["max_batch"]), device="cuda", dtype=torch.float32) for m, t in zip(models, tables)]
+
+    def run(held):
+        r = ds.serve(models, tables, xs, ys, period_us=10_000, duration_us=duration, arrivals=arrivals,
+                     overprov_slots=0, event_capacity=1 << 16, resize_violations=3)
+        torch.cuda.synchronize()
+        assert ds.partition_count()[0] == live0 + held
+        rep = sched.simulate(tables, 10_000, duration, arrivals, overprov=0, placement="home",
+                             replay_events=r["events"], resize_violations=3)
+        live = sorted((j["start_us"], j["model"], j["batch"], j["slot_mask"], j["kind"]) for j in r["log"])
+        replayed = sorted((j[0], j[2], j[5], j[3], j[4]) for j in rep["log"])
+        assert live == replayed
+        assert [s["resizes"] for s in r["models"]] == rep["resizes"]
+        assert r["models"][3]["resizes"] > 0
+        # delay of each change of MobileNetV2 after the completion that decided it
+        delays, last_done = [], None
+        for e in r["events"]:
+            if e["model"] != 3:
+                continue
+            if e["kind"] == 0:
+                last_done = e["t_us"]
+            elif e["kind"] == 3:
+                delays.append((bin(e["slot_mask"]).count("1"), e["t_us"] - last_done))
+        print("held %d: resizes %s, changes (slots, us after the deciding completion) %s" %
+              (held, [s["resizes"] for s in r["models"]], delays), flush=True)
+        return delays
+
+    held = ds.Partition(slot_offset=0, n_slots=4)  # three streams for the four models fit beside it
+    try:
+        delays = run(1)
+    finally:
+        held.destroy()
+    assert delays[0][0] == 16 and delays[0][1] < 2000  # into [16, 32), the range model 1 runs on
+    run(0)
+    for m in models:
+        m.destroy()
