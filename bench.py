@@ -73,7 +73,7 @@ MIX4 = [
     ("vgg19", 1052, 50000, 150, 8, [1, 2, 4, 8]),
     ("lstm2", 1053, 30000, 300, 32, [1, 2, 4, 8, 16, 32]),
 ]
-CAPACITY_BISECTIONS = 4           # after the doubling: geometric bisections of the capacity bracket
+CAPACITY_BISECTIONS = 6           # after the doubling: geometric bisections of the capacity bracket
 TEMPORAL_CYCLES = [15000, 7500]   # temporal sharing: slice cycles tried (the best is the baseline)
 # D-STACK settings tried (the best is the headline): (over-provision slots,
 # late requests that move a model to its next larger swept GPU% -- Sec. 3.5's
@@ -583,8 +583,8 @@ class Mix4:
     def capacity(self, policy, param, seconds):
         """Largest k (offered rate k x the stated rates) with at most 1% of the
         requests late or unserved: double from 1 until a probe fails (halve
-        if 1 fails), then bisect four times on the geometric mean (the last
-        step is 2^(1/16), about 4.4%)."""
+        if 1 fails), then bisect six times on the geometric mean (the last
+        step is 2^(1/64), about 1.1%)."""
         dur = int(seconds * 1e6)
         probes = []
 
@@ -593,7 +593,8 @@ class Mix4:
             probes.append(dict({kk: r[kk] for kk in ("k", "offered_req_s", "on_time_per_s", "violation_frac",
                                                      "utilisation_ppm")},
                                resizes=[m["resizes"] for m in r.get("per_model", [])],
-                               final_slots=[m["final_slots"] for m in r.get("per_model", [])]))
+                               final_slots=[m["final_slots"] for m in r.get("per_model", [])],
+                               violations=[m["violations"] for m in r.get("per_model", [])]))
             return r["violation_frac"] <= VIOLATION_BAR
 
         k_ok = k_bad = None
