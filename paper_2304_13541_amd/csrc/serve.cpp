@@ -19,9 +19,16 @@
 
 #include <chrono>
 #include <cmath>
+#include <atomic>
+#include <condition_variable>
 #include <cstring>
+#include <deque>
+#include <functional>
+#include <memory>
 #include <future>
+#include <mutex>
 #include <string>
+#include <thread>
 #include <utility>
 #include <vector>
 
@@ -59,6 +66,82 @@ struct NewPartition {
   std::string err;
 };
 
+// Partition creations and destructions run on one helper thread in the
+// order they are submitted, so that the launcher thread never waits for a
+// stream to be made or torn down (a stream's destruction can take
+// milliseconds), and a creation submitted after a destruction runs after it
+// (the live count then never passes the library's limit).  Queued work is
+// finished before the thread ends.
+class PartitionWorker {
+ public:
+  explicit PartitionWorker(int dev) : dev_(dev), th_([this] { loop(); }) {}
+  ~PartitionWorker() {
+    {
+      std::lock_guard<std::mutex> g(mu_);
+      stop_ = true;
+    }
+    cv_.notify_all();
+    th_.join();
+  }
+  std::future<NewPartition> create(int off, int cnt) {
+    auto task = std::make_shared<std::packaged_task<NewPartition()>>([this, off, cnt] {
+      NewPartition np;
+      if (dev_err_ != hipSuccess) {
+        np.first = DSTACK_E_HIP;
+        np.err = std::string("serve: hipSetDevice: ") + hipGetErrorString(dev_err_);
+      } else {
+        np.first = dstack_partition_create_at(off, cnt, &np.second);
+        if (np.first != DSTACK_OK) np.err = dstack_last_error();
+      }
+      return np;
+    });
+    std::future<NewPartition> f = task->get_future();
+    submit([task] { (*task)(); }, &creates_);
+    return f;
+  }
+  void destroy(dstack_partition p) {
+    submit([p] { dstack_partition_destroy(p); }, &destroys_);
+  }
+  // submitted and not finished yet
+  int creates() const { return creates_.load(); }
+  int destroys() const { return destroys_.load(); }
+
+ private:
+  void submit(std::function<void()> f, std::atomic<int>* counter) {
+    counter->fetch_add(1);
+    {
+      std::lock_guard<std::mutex> g(mu_);
+      q_.emplace_back([f, counter] {
+        f();
+        counter->fetch_sub(1);
+      });
+    }
+    cv_.notify_one();
+  }
+  void loop() {
+    dev_err_ = hipSetDevice(dev_);  // a new thread starts on device 0
+    for (;;) {
+      std::function<void()> f;
+      {
+        std::unique_lock<std::mutex> g(mu_);
+        cv_.wait(g, [this] { return stop_ || !q_.empty(); });
+        if (q_.empty()) return;  // stop_ and nothing left
+        f = std::move(q_.front());
+        q_.pop_front();
+      }
+      f();
+    }
+  }
+  int dev_;
+  hipError_t dev_err_ = hipSuccess;
+  std::mutex mu_;
+  std::condition_variable cv_;
+  std::deque<std::function<void()>> q_;
+  bool stop_ = false;
+  std::atomic<int> creates_{0}, destroys_{0};
+  std::thread th_;  // last: starts after the members it uses
+};
+
 // A live partition and the models whose current range it covers.
 struct PoolEntry {
   int off = 0, n = 0, users = 0;
@@ -67,6 +150,7 @@ struct PoolEntry {
 };
 
 struct Resources {
+  std::unique_ptr<PartitionWorker> worker;           // made after the first partitions
   std::vector<PoolEntry> pool;                      // p == nullptr: a free entry
   std::vector<std::future<NewPartition>> pending;  // per model; valid() while a stream of its next range is created
   std::vector<dstack_partition> made;              // per model: that stream, created and not used yet
@@ -74,8 +158,9 @@ struct Resources {
   std::vector<hipEvent_t> ev0, ev1;
   bool drained = true;  // false: a job may still run, keep the partitions that ran jobs
   ~Resources() {
+    worker.reset();  // finishes the queued creations and destructions
     for (size_t i = 0; i < pending.size(); ++i)
-      if (pending[i].valid()) {  // an early return: wait for the creation
+      if (pending[i].valid()) {  // an early return: the creation is done
         NewPartition np = pending[i].get();
         if (np.first == DSTACK_OK) made[i] = np.second;
       }
@@ -168,7 +253,10 @@ dstack_status serve(const dstack_model* models, int n, const void* const* d_in, 
   auto detach = [&](int i) {  // model i's last job on its entry has completed
     PoolEntry& e = res.pool[cur[i]];
     if (--e.users == 0) {
-      dstack_partition_destroy(e.p);
+      if (res.worker)
+        res.worker->destroy(e.p);
+      else
+        dstack_partition_destroy(e.p);
       e = PoolEntry{};
     }
     cur[i] = -1;
@@ -229,32 +317,24 @@ dstack_status serve(const dstack_model* models, int n, const void* const* d_in, 
     if (st != DSTACK_OK) return st;
   }
 
-  // streams of a model's next range, created on a helper thread; partitions
-  // live in the process (this launcher's and any other) plus those being
-  // created stay within the library's limit
+  // streams of a model's next range, created (and unused ones destroyed) by
+  // the helper thread; the partitions live in the process (this launcher's
+  // and any other), less those queued for destruction (which run first),
+  // plus those queued for creation, stay within the library's limit
+  {
+    int dev = 0;
+    DS_HIP(hipGetDevice(&dev));
+    res.worker.reset(new PartitionWorker(dev));
+  }
   auto room = [&]() {
     int live = 0, max_live = 0;
     dstack_partition_count(&live, &max_live);
-    for (int i = 0; i < n; ++i) live += res.pending[i].valid() ? 1 : 0;
-    return max_live - live;
+    return max_live - live - res.worker->creates() + res.worker->destroys();
   };
   auto start_create = [&](int i, int off, int cnt) -> dstack_status {
-    int dev = 0;
-    DS_HIP(hipGetDevice(&dev));
     res.made_off[i] = off;
     res.made_n[i] = cnt;
-    res.pending[i] = std::async(std::launch::async, [off, cnt, dev] {
-      NewPartition np;
-      const hipError_t e = hipSetDevice(dev);  // the helper starts on device 0
-      if (e != hipSuccess) {
-        np.first = DSTACK_E_HIP;
-        np.err = std::string("serve: hipSetDevice: ") + hipGetErrorString(e);
-        return np;
-      }
-      np.first = dstack_partition_create_at(off, cnt, &np.second);
-      if (np.first != DSTACK_OK) np.err = dstack_last_error();
-      return np;
-    });
+    res.pending[i] = res.worker->create(off, cnt);
     return DSTACK_OK;
   };
   auto collect = [&](int i, bool wait) -> dstack_status {  // a finished creation into made[i]
@@ -268,13 +348,24 @@ dstack_status serve(const dstack_model* models, int n, const void* const* d_in, 
   auto drop_standby = [&](int i) -> dstack_status {  // an unused stream of model i's
     dstack_status s = collect(i, true);
     if (s != DSTACK_OK) return s;
-    if (res.made[i]) dstack_partition_destroy(res.made[i]);
+    if (res.made[i]) res.worker->destroy(res.made[i]);
     res.made[i] = nullptr;
     res.made_off[i] = -1;
     res.made_n[i] = 0;
     return DSTACK_OK;
   };
   std::vector<char> switching(n, 0);  // model i waits for its new range's stream
+  // model i is at risk of its next GPU% change (a request late since its last
+  // change, or one that waited more than half its SLO before its job
+  // started): the stream of its next range as a standby, if there is room
+  auto standby = [&](int i) -> dstack_status {
+    if (temporal || sim->resize_violations <= 0 || switching[i] || res.pending[i].valid() || res.made[i] ||
+        room() < 1)
+      return DSTACK_OK;
+    int home = 0, dep = 0;
+    if (!ls.next_range(i, &home, &dep) || find_entry(home, dep) >= 0) return DSTACK_OK;
+    return start_create(i, home, dep);
+  };
 
   const int64_t D = sim->duration_us;
   const int total = prm->total_slots;
@@ -298,6 +389,10 @@ dstack_status serve(const dstack_model* models, int n, const void* const* d_in, 
   auto launch = [&](int64_t t, int i, uint64_t mask, int64_t table_us, int b, int kind) -> dstack_status {
     Running& r = run[i];
     r.reqs = ls.start(t, i, mask, table_us, b);
+    if (!r.reqs.empty() && t - r.reqs.front() > tables[i].slo_us / 2) {  // (requests leave in arrival order)
+      dstack_status s = standby(i);
+      if (s != DSTACK_OK) return s;
+    }
     r.on = true;
     r.start = t;
     r.table_us = table_us;
@@ -393,14 +488,9 @@ dstack_status serve(const dstack_model* models, int n, const void* const* d_in, 
           st = start_create(i, home, dep);
           if (st != DSTACK_OK) return st;
         }
-      } else if (!temporal && sim->resize_violations > 0 && ls.late_count(i) > 0 && !switching[i] &&
-                 !res.pending[i].valid() && !res.made[i] && room() >= 1) {
-        // the model has begun to miss its SLO: its next range's stream as a standby
-        int home = 0, dep = 0;
-        if (ls.next_range(i, &home, &dep) && find_entry(home, dep) < 0) {
-          st = start_create(i, home, dep);
-          if (st != DSTACK_OK) return st;
-        }
+      } else if (ls.late_count(i) > 0) {
+        st = standby(i);
+        if (st != DSTACK_OK) return st;
       }
       st = fod_pass(te);
       if (st != DSTACK_OK) return st;
