@@ -629,11 +629,15 @@ class Mix4:
         return self.run(k, steps * PERIOD_US, policy, param)
 
 
+CONFIRM_BISECTIONS = 3  # timed runs between the confirmed k and the failed one
+
+
 def confirm_capacity(mix, policy, param, entry, steps, warmup):
     """The timed run at a policy's capacity must itself meet the bar (a probe
     near saturation can pass over its shorter trace): if it does not, it is
-    repeated at the next lower k that passed its probe, then once at the
-    geometric mean of that k and the failed one (kept if it meets the bar).
+    repeated at the next lower k that passed its probe, then bisected on the
+    geometric mean between that k and the failed one with timed runs
+    (CONFIRM_BISECTIONS of them; the highest k that meets the bar is kept).
     Returns (k, run); entry["timed_k"] lists the k tried."""
     k = entry["k"] if entry["k"] > 0 else 1.0
     run = mix.timed(k, policy, param, steps, warmup)
@@ -648,12 +652,15 @@ def confirm_capacity(mix, policy, param, entry, steps, warmup):
         run = mix.timed(k, policy, param, steps, warmup)
         tried.append(k)
     if k_fail is not None and run["violation_frac"] <= VIOLATION_BAR:
-        # one timed bisection step between the confirmed k and the failed one
-        mid = math.sqrt(k * k_fail)
-        run_mid = mix.timed(mid, policy, param, steps, warmup)
-        tried.append(mid)
-        if run_mid["violation_frac"] <= VIOLATION_BAR:
-            k, run = mid, run_mid
+        # timed bisection steps between the confirmed k and the failed one
+        for _ in range(CONFIRM_BISECTIONS):
+            mid = math.sqrt(k * k_fail)
+            run_mid = mix.timed(mid, policy, param, steps, warmup)
+            tried.append(mid)
+            if run_mid["violation_frac"] <= VIOLATION_BAR:
+                k, run = mid, run_mid
+            else:
+                k_fail = mid
     entry["timed_k"] = tried
     return k, run
 

@@ -459,6 +459,7 @@ def simulate(models, period, duration, arrivals, total=TOTAL_SLOTS, overprov=OVE
     viol = [0] * n
     resizes = [0] * n
     changed_at = [0] * n  # time of each model's last GPU% change
+    job_start = [0] * n   # start of each model's current (or last) job
     unavailable = set()   # replay of a live run: models whose new stream is not ready yet
     columns = [sorted(set().union(*[set(r) for r in m["table"].values()])) for m in models]
     if policy == "temporal":
@@ -515,6 +516,11 @@ def simulate(models, period, duration, arrivals, total=TOTAL_SLOTS, overprov=OVE
     def start_job(t, i, mask, dur, b, kind):
         nonlocal used, seq, slot_us, h, last_end
         reqs = [queue[i].popleft() for _ in range(b)]
+        job_start[i] = t
+        if policy == "dstack" and resize_violations > 0:
+            # requests (since the last change) that have waited more than half
+            # their SLO when their job starts count towards the next change now
+            viol[i] += sum(1 for a in reqs if a >= changed_at[i] and 2 * (t - a) > models[i]["slo_us"])
         running[i] = (t + dur, mask, reqs)
         used |= mask
         heapq.heappush(ev, (t + dur, 0, i, seq, reqs))
@@ -538,18 +544,28 @@ def simulate(models, period, duration, arrivals, total=TOTAL_SLOTS, overprov=OVE
         return range_mask(cur_home[i], cur_dep[i]), lat(i, choices[i].batch, cur_dep[i])
 
     def note_late(i, t, reqs):
+        """GPU% change on SLO violations (Sec. 3.5): the job of model i that
+        ended at t adds its requests (since the last change) that completed
+        past their SLO and were not counted at its start; the change is
+        decided once the count reaches the threshold."""
         if policy != "dstack" or resize_violations <= 0:
             return
-        viol[i] += sum(1 for a in reqs if t - a > models[i]["slo_us"] and a >= changed_at[i])
+        slo = models[i]["slo_us"]
+        viol[i] += sum(1 for a in reqs if t - a > slo and a >= changed_at[i] and 2 * (job_start[i] - a) <= slo)
         if viol[i] < resize_violations:
             return
         viol[i] = 0
         nxt = [c for c in columns[i] if cur_dep[i] < c <= total and lat(i, choices[i].batch, c)]
         if not nxt:
             return
+        home = total - nxt[0] if cur_home[i] + nxt[0] > total else cur_home[i]
+        now, grown = range_mask(cur_home[i], cur_dep[i]), range_mask(home, nxt[0])
+        # no change that would make the model contend with one whose range its current range does not meet
+        if any(grown & range_mask(cur_home[j], cur_dep[j]) and not now & range_mask(cur_home[j], cur_dep[j])
+               for j in range(n) if j != i):
+            return
         cur_dep[i] = nxt[0]
-        if cur_home[i] + nxt[0] > total:
-            cur_home[i] = total - nxt[0]
+        cur_home[i] = home
         resizes[i] += 1
         changed_at[i] = t
         if replay_events is not None:  # live: the model waits for its new stream (an event of kind 3)

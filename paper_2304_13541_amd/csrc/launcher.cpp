@@ -140,6 +140,13 @@ bool LaunchState::note_late(int64_t t, int i, int64_t late) {
   return true;
 }
 
+int64_t LaunchState::late_at_end(int i, int64_t start, int64_t end, const std::vector<int64_t>& reqs) const {
+  int64_t c = 0;
+  for (int64_t a : reqs)
+    if (a >= changed_at_[i] && end - a > models_[i].slo_us && 2 * (start - a) <= models_[i].slo_us) c += 1;
+  return c;
+}
+
 bool LaunchState::next_range(int i, int* home, int* dep) const {
   const dstack_sched_model& m = models_[i];
   int next = -1;
@@ -147,8 +154,17 @@ bool LaunchState::next_range(int i, int* home, int* dep) const {
     if (m.slots[q] > dep_[i] && m.slots[q] <= prm_->total_slots && table_latency(i, plan_->batch[i], m.slots[q]) > 0)
       next = m.slots[q];
   if (next < 0) return false;
+  const int h = home_[i] + next > prm_->total_slots ? prm_->total_slots - next : home_[i];
+  // no change that would make the model contend with one whose range its
+  // current range does not meet
+  const uint64_t now = range_mask(home_[i], dep_[i]), grown = range_mask(h, next);
+  for (int j = 0; j < n_; ++j) {
+    if (j == i) continue;
+    const uint64_t other = range_mask(home_[j], dep_[j]);
+    if ((grown & other) && !(now & other)) return false;
+  }
   *dep = next;
-  *home = home_[i] + next > prm_->total_slots ? prm_->total_slots - next : home_[i];
+  *home = h;
   return true;
 }
 
@@ -271,6 +287,9 @@ std::vector<int64_t> LaunchState::start(int64_t t, int i, uint64_t mask, int64_t
     reqs.push_back(queue_[i].front());
     queue_[i].pop_front();
   }
+  if (sim_->policy == 0 && sim_->resize_violations > 0)
+    for (int64_t a : reqs)
+      if (a >= changed_at_[i] && 2 * (t - a) > models_[i].slo_us) viol_[i] += 1;
   running_[i] = 1;
   run_mask_[i] = mask;
   used_ |= mask;
@@ -336,17 +355,14 @@ dstack_status simulate(const dstack_sched_model* models, int n, const dstack_sch
     const int i = e.model;
     if (e.kind == 0) {
       ls.finish(i);
-      int64_t job_late = 0, late_since = 0;
+      int64_t job_late = 0;
       for (int64_t a : e.reqs) {
         served[i] += 1;
         lats[i].push_back(e.t - a);
-        if (e.t - a > models[i].slo_us) {
-          job_late += 1;
-          if (a >= ls.changed_at(i)) late_since += 1;
-        }
+        if (e.t - a > models[i].slo_us) job_late += 1;
       }
       late[i] += job_late;
-      ls.note_late(e.t, i, late_since);
+      ls.note_late(e.t, i, ls.late_at_end(i, e.t - e.dur, e.t, e.reqs));
       fod_pass(e.t);
     } else if (e.kind == 1 && ls.temporal()) {
       fod_pass(e.t);

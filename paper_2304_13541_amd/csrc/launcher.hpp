@@ -44,14 +44,19 @@ class LaunchState {
   // the FOD choice at time t (false: nothing fits)
   bool fod_pick(int64_t t, Pick* out) const;
   // GPU% change on SLO violations (resize_violations > 0, D-STACK with home
-  // placement): a job of model i ended at t with `late` requests past their
-  // SLO among those that arrived at or after changed_at(i) (earlier ones
-  // waited through the previous size and say nothing about the current one);
-  // once that count since its last change reaches the threshold the model
-  // moves to the next larger swept slot count (true returned) and
-  // changed_at(i) becomes t.  Its current size, home offset and the planned
-  // job as it now runs:
+  // placement).  Among the requests of model i that arrived at or after
+  // changed_at(i) (earlier ones waited through the previous size and say
+  // nothing about the current one), a request counts towards the next change
+  // once: when its job starts, if it has waited more than half its SLO by
+  // then (the share Eq. meet_half_slo leaves to waiting is used up; start()
+  // counts these), else when it completes past its SLO (late_at_end counts
+  // these for a job that started at `start` and ended at `end`).  A job of
+  // model i ended at t adding `late` such requests: once the count since its
+  // last change reaches the threshold the model moves to the next larger
+  // swept slot count (true returned) and changed_at(i) becomes t.  Its
+  // current size, home offset and the planned job as it now runs:
   bool note_late(int64_t t, int i, int64_t late);
+  int64_t late_at_end(int i, int64_t start, int64_t end, const std::vector<int64_t>& reqs) const;
   int64_t changed_at(int i) const { return changed_at_[i]; }
   // the home offset and size model i moves to at its next GPU% change
   // (false: it is at its largest swept share), and the late requests

@@ -445,15 +445,13 @@ dstack_status serve(const dstack_model* models, int n, const void* const* d_in, 
       Running& r = run[i];
       r.on = false;
       ls.finish(i);
-      int64_t job_late = 0, late_since = 0;
+      int64_t job_late = 0;
       for (int64_t a : r.reqs) {
         served[i] += 1;
         lats[i].push_back(te - a);
-        if (te - a > tables[i].slo_us) {
-          job_late += 1;
-          if (a >= ls.changed_at(i)) late_since += 1;
-        }
+        if (te - a > tables[i].slo_us) job_late += 1;
       }
+      const int64_t late_since = ls.late_at_end(i, r.start, te, r.reqs);
       late[i] += job_late;
       busy[i] += gpu_us;
       slot_us += (int64_t)__builtin_popcountll(r.mask) * std::max<int64_t>(0, std::min(r.start + gpu_us, D) - r.start);

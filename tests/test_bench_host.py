@@ -89,13 +89,16 @@ def test_timed_run_falls_back_to_the_next_passing_probe():
     assert tried[0] == k
     lower = max(p["k"] for p in probes if p["k"] <= 17.0)
     # the passing probes below k in descending order until one holds, then
-    # one step between it and the last failed k
+    # timed bisection steps between the last k that held and the last that failed
     i = tried.index(lower)
     passing = sorted((p["k"] for p in probes if p["violation_frac"] <= bench.VIOLATION_BAR and lower <= p["k"] < k),
                      reverse=True)
-    assert tried[1:i + 1] == passing and len(tried) == i + 2
-    assert abs(tried[-1] - (lower * tried[i - 1]) ** 0.5) < 1e-9
-    assert k_run == (tried[-1] if tried[-1] <= 17.0 else lower)
+    assert tried[1:i + 1] == passing and len(tried) == i + 1 + bench.CONFIRM_BISECTIONS
+    lo, hi = lower, tried[i - 1]
+    for mid in tried[i + 1:]:
+        assert abs(mid - (lo * hi) ** 0.5) < 1e-9
+        lo, hi = (mid, hi) if mid <= 17.0 else (lo, mid)
+    assert k_run == lo and lo <= 17.0
     # a capacity that holds over the timed run is kept as it is
     m2 = FakeMix(probe_limit=19.0, timed_limit=19.0)
     k2, probes2 = bench.Mix4.capacity(m2, "dstack", (0, 0), 1.5)

@@ -436,7 +436,8 @@ def test_temporal_invariants_random():
 def test_resize_on_violations_hand_worked():
     """One model at batch 1 whose optimum share (2 slots, 2 ms a request) is
     slower than its arrivals (one every 1.5 ms): requests turn late, and every
-    3 late completions it moves up its table's columns, 2 -> 4 -> 8 slots,
+    3 late requests (late completions, or starts more than half the SLO after
+    arrival) it moves up its table's columns, 2 -> 4 -> 8 slots,
     where 1 ms a request keeps up.  Before the first change every job runs on
     slots 0-1, between the changes on 0-3, after them on 0-7."""
     table = {1: {2: 2000, 4: 1800, 8: 1000}}
@@ -453,6 +454,61 @@ def test_resize_on_violations_hand_worked():
     # without the trigger it stays on 2 slots and falls behind
     r0 = sched.simulate(m, 100000, 300000, [arr], overprov=0, placement="home")
     assert r0["models"][0]["resizes"] == 0 and r0["models"][0]["violations"] > st["violations"]
+
+
+def test_resize_counts_half_slo_waits_at_job_start():
+    """A request counts towards the next GPU% change when its job starts
+    more than half its SLO after its arrival (the share Eq. meet_half_slo
+    leaves to waiting is used up), else when it completes late; never twice.
+    One model at batch 1: 1000 us a job on its 2-slot knee (800 us on 4),
+    SLO 3000 us, requests at 0, 1, 2, 3 us.  The planned start at 0 finds the
+    queue empty and still bounds a fill at 0, so the jobs start at 1, 1001,
+    2001 and 3001 us: the third request has waited 1999 us > 1500 at its
+    start (and ends 2999 us after arriving: on time), the fourth 2998 us (it
+    ends 3998 us after arriving: late, counted once).  Threshold 2: the count
+    reaches 2 at the fourth start and the change to 4 slots comes at its end;
+    threshold 1: at the end of the third job, so the fourth runs on 4 slots
+    (800 us).  Counting late completions alone would give 1 request, so no
+    change at threshold 2.  The library's simulation takes the same jobs."""
+    table = {1: {2: 1000, 4: 800}}
+    m = [dict(slo_us=3000, max_batch=1, rate_per_s=0, table=table)]
+    arr = [[0, 1, 2, 3]]
+    two = sched.simulate(m, 100000, 20000, arr, overprov=0, placement="home", resize_violations=2)
+    assert [(j[0], j[1], bin(j[3]).count("1")) for j in two["log"]] == \
+        [(1, 1001, 2), (1001, 2001, 2), (2001, 3001, 2), (3001, 4001, 2)]
+    assert two["models"][0]["resizes"] == 1 and two["models"][0]["final_slots"] == 4
+    assert two["models"][0]["violations"] == 1
+    one = sched.simulate(m, 100000, 20000, arr, overprov=0, placement="home", resize_violations=1)
+    assert [(j[0], j[1], bin(j[3]).count("1")) for j in one["log"]] == \
+        [(1, 1001, 2), (1001, 2001, 2), (2001, 3001, 2), (3001, 3801, 4)]
+    import paper_2304_13541_amd as ds
+    for rv, ref in ((2, two), (1, one)):
+        lib = ds.simulate(m, 100000, 20000, arr, overprov_slots=0, placement="home", resize_violations=rv)
+        assert lib["job_hash"] == ref["job_hash"]
+        assert [(s["resizes"], s["final_slots"], s["violations"]) for s in lib["models"]] == \
+            [(s["resizes"], s["final_slots"], s["violations"]) for s in ref["models"]]
+
+
+def test_resize_never_adds_contention():
+    """A GPU% change is not made when the larger range would meet the range
+    of a model that the current one does not meet.  Model 0 falls behind on
+    its 16-slot knee at [0, 16) (1000 us a request, one every 700 us); its
+    next columns, 24 and 32 slots, would reach model 1's [16, 32): with model
+    1 there it keeps its range, alone it grows to 24 and then 32.  The
+    library's simulation takes the same jobs."""
+    import paper_2304_13541_amd as ds
+    t0 = {1: {16: 1000, 24: 950, 32: 900}}
+    t1 = {1: {16: 300, 24: 290, 32: 280}}
+    m = [dict(slo_us=5000, max_batch=1, rate_per_s=0, table=t0), dict(slo_us=20000, max_batch=1, rate_per_s=0, table=t1)]
+    st, plan = ds.schedule(m, 100000, overprov_slots=0, placement="home")
+    assert plan["deployed_slots"] == [16, 16] and plan["home_offset"] == [0, 16]
+    arr = [list(range(0, 300000, 700)), list(range(0, 300000, 10000))]
+    both = sched.simulate(m, 100000, 300000, arr, overprov=0, placement="home", resize_violations=3)
+    assert [s["resizes"] for s in both["models"]] == [0, 0] and both["models"][0]["violations"] > 0
+    lib = ds.simulate(m, 100000, 300000, arr, overprov_slots=0, placement="home", resize_violations=3)
+    assert lib["job_hash"] == both["job_hash"]
+    alone = sched.simulate(m[:1], 100000, 300000, arr[:1], overprov=0, placement="home", resize_violations=3)
+    assert alone["models"][0]["resizes"] == 2 and alone["models"][0]["final_slots"] == 32
 
 
 def test_resize_keeps_ranges_inside_the_gpu_and_disjoint():
