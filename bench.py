@@ -665,6 +665,22 @@ def confirm_capacity(mix, policy, param, entry, steps, warmup):
     return k, run
 
 
+def work_rate(mix, run_ds, run_t):
+    """FLOP-weighted rate of the requests served within their SLO (each
+    model's on-time requests per second x its FLOP per inference), for
+    D-STACK and temporal sharing at their capacities: a guard against a
+    ratio won by serving more of the cheap model."""
+    def tflops(run):
+        tot = 0.0
+        for m, st in zip(mix.models, run["per_model"]):
+            on_time = st["served"] - (st["violations"] - st["unserved"])
+            tot += on_time / (run["run_us"] * 1e-6) * m.info.flops_per_item
+        return tot / 1e12
+    d, t = tflops(run_ds), tflops(run_t)
+    return dict(dstack_tflops=d, timesliced_tflops=t, ratio=d / t if t > 0 else None,
+                dstack_frac_of_chip_peak=d / PEAK_BF16_TFLOPS)
+
+
 def mix_rooflines(ds, torch, mix, k, overprov):
     """Each model of the four-model mix on its deployed home partition at the
     plan's batch (dstack_schedule with the rates at k): per-layer kernel
@@ -997,6 +1013,7 @@ def main():
         },
         "timesliced_inferences_per_s": run_t["on_time_per_s"],
         "speedup_vs_timesliced": value / run_t["on_time_per_s"] if run_t["on_time_per_s"] > 0 else None,
+        "work_rate": work_rate(mix, run_ds, run_t),
         "capacity_ratio_vs_timesliced": k_run / k_t if k_t > 0 else None,
         "dstack_run": {k: run_ds[k] for k in run_keys},
         "timesliced_run": {k: run_t[k] for k in run_keys},

@@ -104,3 +104,28 @@ def test_timed_run_falls_back_to_the_next_passing_probe():
     k2, probes2 = bench.Mix4.capacity(m2, "dstack", (0, 0), 1.5)
     e2 = dict(k=k2, probes=probes2)
     assert bench.confirm_capacity(m2, "dstack", (0, 0), e2, 20, 3)[0] == k2 and e2["timed_k"] == [k2]
+
+
+def test_work_rate_weights_on_time_requests_by_flops():
+    """The FLOP-weighted guard: each model's on-time requests per second
+    (served less late ones; unserved ones were never served) x its FLOP per
+    inference, for both policies, and their ratio."""
+    class Info:
+        def __init__(self, f):
+            self.flops_per_item = f
+
+    class M:
+        def __init__(self, f):
+            self.info = Info(f)
+
+    class Mix:
+        models = [M(8e9), M(6e8)]
+    run_d = dict(run_us=2_000_000, per_model=[dict(served=1000, violations=10, unserved=4),
+                                              dict(served=2000, violations=0, unserved=0)])
+    run_t = dict(run_us=2_000_000, per_model=[dict(served=500, violations=0, unserved=0),
+                                              dict(served=1000, violations=0, unserved=0)])
+    w = bench.work_rate(Mix(), run_d, run_t)
+    # D-STACK: (1000 - 6) x 8e9 / 2 s + 2000 x 6e8 / 2 s = 4.576 TFLOP/s; temporal 2.3
+    assert abs(w["dstack_tflops"] - 4.576) < 1e-9 and abs(w["timesliced_tflops"] - 2.3) < 1e-9
+    assert abs(w["ratio"] - 4.576 / 2.3) < 1e-12
+    assert abs(w["dstack_frac_of_chip_peak"] - 4.576 / bench.PEAK_BF16_TFLOPS) < 1e-12
