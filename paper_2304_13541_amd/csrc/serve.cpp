@@ -45,7 +45,7 @@ int64_t host_us() {
 
 constexpr int kMaxServeModels = 4;
 static_assert(kMaxServeModels <= kLauncherWsCount, "one launcher workspace per model");
-constexpr int kResizeAhead = 3;  // GPU% changes per model whose graphs the warm-up captures
+constexpr int kResizeAhead = 5;  // GPU% changes per model whose graphs the warm-up captures
 constexpr int64_t kDrainLimitUs = 60LL * 1000 * 1000;  // a job still running this long after the trace: error
 const int kGrid[] = {1, 2, 4, 8, 16, 32};
 
