@@ -184,7 +184,7 @@ dstack_status serve(const dstack_model* models, int n, const void* const* d_in, 
                     dstack_serve_event* events, int event_capacity, int* n_events) {
   DS_CHECK(models && d_in && d_out && tables && prm && sim && out, DSTACK_E_INVALID, "serve: null pointer");
   DS_CHECK(n >= 1 && n <= DSTACK_MAX_MODELS, DSTACK_E_INVALID, "serve: bad model count");
-  DS_CHECK(n <= kMaxServeModels, DSTACK_E_UNSUPPORTED, "serve: at most 4 models (one CU-masked stream each)");
+  DS_CHECK(n <= kMaxServeModels, DSTACK_E_UNSUPPORTED, "serve: at most 4 models (at most one CU-masked stream each)");
   DS_CHECK(log_capacity >= 0 && (log || log_capacity == 0), DSTACK_E_INVALID, "serve: bad log buffer");
   DS_CHECK(event_capacity >= 0 && (events || event_capacity == 0), DSTACK_E_INVALID, "serve: bad event buffer");
   DS_CHECK(check_trace(n, sim), DSTACK_E_INVALID, "serve: bad trace (see dstack_simulate)");
