@@ -246,6 +246,44 @@ def test_two_model_mix_launch_configuration(env):
         check_against_oracle(env, arch, seed, xb, gu.host(y), items)
 
 
+def test_four_model_mix_launch_configuration(env):
+    """The four-model mix as the live launcher deploys it at the bench's
+    plan: ResNet-50 b16 and the LSTM b32 share the stream of slots 0..15,
+    VGG-19 b2 runs on slots 16..31, MobileNetV2 b4 on its 3 home slots
+    16..18 and, after its GPU% changes, on VGG-19's stream.  All three
+    streams replay captured graphs concurrently (the 3-slot range inside the
+    16-slot one included); sampled items of each model's last output against
+    the oracle."""
+    import gc
+    ds, gu, inputs, oracle, torch = env
+    gc.collect()  # earlier tests' partitions count against the four live streams
+    parts = {"a": ds.Partition(slot_offset=0, n_slots=16), "b": ds.Partition(slot_offset=16, n_slots=16),
+             "c": ds.Partition(slot_offset=16, n_slots=3)}
+    assert [parts[k].n_cu for k in "abc"] == [128, 128, 24]
+    # (arch, seed, batch, partitions it runs on); seeds as the bench's mix
+    cfg = [("resnet50", 1050, 16, "a"), ("mobilenetv2", 1051, 4, "cb"), ("vgg19", 1052, 2, "b"), ("lstm2", 1053, 32, "a")]
+    runs = []
+    for arch, seed, b, on in cfg:
+        m = ds.Model(arch, seed)
+        xb = inputs.sequence_batch(seed + 1, b) if arch == "lstm2" else inputs.image_batch(seed + 1, b, hw=m.info.in_h)
+        ys = [gu.empty_f32(m.output_shape(b)) for _ in on]
+        runs.append((arch, seed, b, on, m, xb, gu.dev_bf16(xb), ys))
+    for _ in range(3):
+        for arch, seed, b, on, m, xb, x, ys in runs:
+            for k, y in zip(on, ys):
+                m.infer(b, x, y, parts[k])
+    for p in parts.values():
+        p.synchronize()
+    try:
+        for arch, seed, b, on, m, xb, x, ys in runs:
+            for k, y in zip(on, ys):  # each partition's plans (tiles, splits) are its own
+                print("%s on partition %s" % (arch, k), flush=True)
+                check_against_oracle(env, arch, seed, xb, gu.host(y), sample_items(b, seed))
+    finally:
+        for p in parts.values():
+            p.destroy()
+
+
 @pytest.mark.parametrize("arch,batch,fraction", [("mobilenetv2", 4, 0.25), ("resnet50", 2, 0.5), ("lstm2", 3, 0.3)])
 def test_graph_replays_equal_eager(env, arch, batch, fraction):
     """dstack_infer replays a captured graph; dstack_profile_layers runs the
