@@ -96,25 +96,29 @@ class PartitionWorker {
       return np;
     });
     std::future<NewPartition> f = task->get_future();
-    submit([task] { (*task)(); }, &creates_);
+    creates_.fetch_add(1);
+    submit([this, task] {
+      (*task)();
+      creates_.fetch_sub(1);  // after the new partition counts as live
+    });
     return f;
   }
   void destroy(dstack_partition p) {
-    submit([p] { dstack_partition_destroy(p); }, &destroys_);
+    destroys_.fetch_add(1);
+    submit([this, p] {
+      destroys_.fetch_sub(1);  // before it stops counting as live
+      dstack_partition_destroy(p);
+    });
   }
   // submitted and not finished yet
   int creates() const { return creates_.load(); }
   int destroys() const { return destroys_.load(); }
 
  private:
-  void submit(std::function<void()> f, std::atomic<int>* counter) {
-    counter->fetch_add(1);
+  void submit(std::function<void()> f) {
     {
       std::lock_guard<std::mutex> g(mu_);
-      q_.emplace_back([f, counter] {
-        f();
-        counter->fetch_sub(1);
-      });
+      q_.emplace_back(std::move(f));
     }
     cv_.notify_one();
   }
@@ -326,10 +330,15 @@ dstack_status serve(const dstack_model* models, int n, const void* const* d_in, 
     DS_HIP(hipGetDevice(&dev));
     res.worker.reset(new PartitionWorker(dev));
   }
+  // Read in this order, a task that finishes between the reads can only make
+  // the result smaller: a creation counts as live before it leaves creates(),
+  // a destruction leaves destroys() before it stops counting as live.
   auto room = [&]() {
+    const int c = res.worker->creates();
     int live = 0, max_live = 0;
     dstack_partition_count(&live, &max_live);
-    return max_live - live - res.worker->creates() + res.worker->destroys();
+    const int d = res.worker->destroys();
+    return max_live - live - c + d;
   };
   auto start_create = [&](int i, int off, int cnt) -> dstack_status {
     res.made_off[i] = off;
