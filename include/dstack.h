@@ -459,20 +459,22 @@ dstack_status dstack_schedule(const dstack_sched_model* models, int n_models, co
  *
  * resize_violations > 0 (policy 0 with placement 1 only, else E_INVALID): a
  * GPU% change triggered by SLO violations (Sec. 3.5's dynamic GPU resource
- * reconfiguration; the trigger count is a parameter).  When the requests of
- * model i that completed late since its last change reach the count, at
- * the completion that reaches it the model moves to the next larger slot
- * count of its table's columns that has a latency at its plan batch (none:
- * it stays, the count restarts), keeping its home offset if the larger range
- * fits, else ending at the last slot.  From then on its planned jobs and
- * FOD jobs use that range and the table latency there; a planned start runs
- * only if its slots are free.  Only requests that arrived at or after the
- * model's last change count towards the next one (earlier ones waited
- * through the previous size).  The live launcher moves the model to a new
- * CU-masked stream at that moment (between its batches): it destroys the
- * old stream, creates the new one on a helper thread while the other models
- * keep running, and the model starts no job until that stream is ready;
- * its count then restarts from that time. */
+ * reconfiguration; the trigger count is a parameter).  A request of model i
+ * that arrived at or after the model's last change (earlier ones waited
+ * through the previous size) counts once: when its job starts, if it has
+ * waited more than half its SLO by then (the share Eq. meet_half_slo leaves
+ * to waiting), else when its job completes past its SLO.  At the completion
+ * that brings the count to the trigger, the model moves to the next larger
+ * slot count of its table's columns that has a latency at its plan batch,
+ * keeping its home offset if the larger range fits, else ending at the last
+ * slot; it stays (and the count restarts) when there is none, or when the
+ * larger range would meet the range of another model that its current range
+ * does not meet (a change never adds contention).  From then on its planned
+ * jobs and FOD jobs use that range and the table latency there; a planned
+ * start runs only if its slots are free.  The live launcher moves the model
+ * at that moment (between its batches) to the stream of its new range (see
+ * dstack_serve); if that stream is not ready yet the model starts no job
+ * until it is, and its count restarts from that time. */
 typedef struct {
   int64_t duration_us;
   int fod;
@@ -557,12 +559,15 @@ dstack_status dstack_simulate_ideal(const dstack_ideal_model* models, int n_mode
  * utilisation_ppm use measured GPU time (device events around each job).
  * Not reproducible run to run: job_hash covers the decisions taken.
  *  - n_models in 1..4 (at most one CU-masked stream per model);
- *  - GPU% changes (sim->resize_violations > 0): a model's next range runs
- *    on the stream of that range if one is live, else on a new one created
- *    on a helper thread; while the partition limit leaves room, a model with
- *    late requests since its last change gets that stream ahead of the
- *    change (a standby), so that the change takes effect when it is decided
- *    (kind 3 below at that time);
+ *  - GPU% changes (sim->resize_violations > 0, the rule of dstack_simulate):
+ *    a model's next range runs on the stream of that range if one is live,
+ *    else on a new one created on a helper thread while the other models
+ *    keep running (the model starts no job until it is ready); while the
+ *    partition limit leaves room, a model at risk of its next change (a
+ *    request late since its last change, or one that waited more than half
+ *    its SLO before its job started) gets that stream ahead of the change (a
+ *    standby), so that the change takes effect when it is decided (kind 3
+ *    below at that time);
  *  - d_in[i], d_out[i]: caller-owned device buffers holding the model's
  *    input and output at tables[i].max_batch (shapes of dstack_model_query);
  *    a job of batch b reads its input from the start of d_in[i] and writes
