@@ -422,13 +422,16 @@ def simulate(models, period, duration, arrivals, total=TOTAL_SLOTS, overprov=OVE
 
     resize_violations > 0 (D-STACK with home placement): a GPU% change on
     SLO violations (Sec. 3.5's dynamic reconfiguration, the trigger count a
-    parameter).  Once the late requests of a model's completed jobs since its
-    last change -- counting only requests that arrived at or after that
-    change, since earlier ones waited through the previous size -- reach the
-    count, at that completion the model moves to the
-    next larger column of its table (over all batches) that has a latency at
-    its plan batch -- none: it stays, the count restarts -- keeping its home
-    offset if the range fits, else ending at the last slot; from then on its
+    parameter).  A request that arrived at or after its model's last change
+    (earlier ones waited through the previous size) counts once: when its
+    job starts, if it has waited more than half its SLO by then (the share
+    Eq. meet_half_slo leaves to waiting), else when its job completes past
+    its SLO.  At the completion that brings the count to the trigger the
+    model moves to the next larger column of its table (over all batches)
+    that has a latency at its plan batch, keeping its home offset if the
+    range fits, else ending at the last slot -- it stays, and the count
+    restarts, when there is none or when the larger range would meet another
+    model's range that the current one does not meet; from then on its
     planned and FOD jobs use that range and the table latency there.  A
     planned start runs only if its slots are free.
 
