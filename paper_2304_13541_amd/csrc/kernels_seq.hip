@@ -126,12 +126,18 @@ __global__ __launch_bounds__(256) void fc_reduce_kernel(const float* __restrict_
     reinterpret_cast<bf16*>(y)[e] = (bf16)v;
 }
 
-// Depth split: double while the grid is below 2 blocks per CU and every block
-// keeps at least 16 depth steps (4 per wave), up to 16 splits.
+// Depth split: double while the grid has fewer blocks than the CUs and every
+// block keeps at least 96 depth steps, up to 16 splits.  The split costs a
+// second launch (the reduction), which only a long depth on a grid that
+// leaves CUs idle repays.  Measured on MI355X (128 CUs, B = 8): 25088 -> 40
+// (3 row tiles) 36.5 us unsplit, 10.0 us in 8; 25088 -> 1000 (63 tiles)
+// 37.6 us unsplit, 23.2 us in 2; but VGG-19's 4096 -> 1000 (128 steps), and
+// ResNet-50's and MobileNetV2's classifiers (64 and 40 steps), ran fastest
+// unsplit, as did VGG-19's 25088 -> 4096 (256 tiles).
 static int fc_splits(int I, int O, int n_cu) {
   const int tiles = (O + 15) / 16, nks = (I + 31) / 32;
   int s = 1;
-  while (s < 16 && tiles * s < 2 * n_cu && nks / (2 * s) >= 16) s *= 2;
+  while (s < 16 && tiles * s < n_cu && nks / (2 * s) >= 96) s *= 2;
   return s;
 }
 

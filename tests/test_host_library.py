@@ -148,13 +148,17 @@ def test_schedule_rejects_bad_arguments():
 
 def test_fc_workspace_bytes():
     """Depth-split plan of the FC kernel on 256 CUs: splits double while the
-    grid (16-row tiles x splits) stays below 512 blocks and each split keeps
-    16 or more 32-deep steps; the workspace holds splits x B x O fp32 sums."""
+    grid (16-row tiles x splits) has fewer than 256 blocks and each split
+    keeps 96 or more 32-deep steps; the workspace holds splits x B x O fp32
+    sums."""
     import paper_2304_13541_amd as ds
-    assert ds.fc_workspace_bytes(8, 4096, 1000) == 8 * 8 * 1000 * 4      # 63 tiles, 128 steps -> 8 splits
-    assert ds.fc_workspace_bytes(8, 25088, 4096) == 2 * 8 * 4096 * 4     # 256 tiles -> 2 splits
-    assert ds.fc_workspace_bytes(16, 1280, 1000) == 2 * 16 * 1000 * 4    # 40 steps -> 2 splits
-    assert ds.fc_workspace_bytes(1, 64, 10) == 0                         # 2 steps: unsplit
+    assert ds.fc_workspace_bytes(8, 25088, 40) == 8 * 8 * 40 * 4         # 3 tiles, 784 steps -> 8 splits (98 each)
+    assert ds.fc_workspace_bytes(8, 25088, 1000) == 8 * 8 * 1000 * 4     # 63 tiles, 784 steps -> 8 splits (98 each)
+    assert ds.fc_workspace_bytes(17, 9216, 33) == 2 * 17 * 33 * 4        # 288 steps -> 2 splits (144; 72 is too few)
+    assert ds.fc_workspace_bytes(8, 25088, 4096) == 0                    # 256 tiles: a block per CU already
+    assert ds.fc_workspace_bytes(8, 4096, 1000) == 0                     # 128 steps: 64 per split is too few
+    assert ds.fc_workspace_bytes(16, 1280, 1000) == 0                    # 40 steps
+    assert ds.fc_workspace_bytes(1, 64, 10) == 0                         # 2 steps
     assert ds.fc_workspace_bytes(0, 64, 10) == 0
 
 
